@@ -1,0 +1,438 @@
+"""Pins of the fp64 oracle against facts other than itself (CPU only).
+
+Each test names what fixes the expected result: a textbook/library routine the
+method reduces to, an exact identity or invariant of Eq. (7)-(13), brute force,
+a closed form, finite differences, or a number the paper prints.
+"""
+from __future__ import annotations
+
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle.network as onet
+import synth
+from tests.formulations import brute_force, lstm_lines, torch_layer
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rand_layer(seed, N, D, H, W, C, O, K=3, scale=0.3):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((N, D, H, W, C))
+    wx = rng.uniform(-scale, scale, (6, 4 * O, C, K, K))
+    wh = rng.uniform(-scale, scale, (6, 4 * O, O, K, K))
+    b = rng.uniform(-scale, scale, (6, 4 * O))
+    return x, wx, wh, b
+
+
+def only_direction(d, wx, wh, b):
+    """Zero the parameters of every direction except d."""
+    keep = np.zeros(6, dtype=bool)
+    keep[d] = True
+    return (np.where(keep[:, None, None, None, None], wx, 0.0),
+            np.where(keep[:, None, None, None, None], wh, 0.0),
+            np.where(keep[:, None], b, 0.0))
+
+
+# ---------------------------------------------------------------- P3 identity
+def test_zero_parameters_give_exact_zero():
+    """All-zero parameters: i = f = o = 1/2, g = tanh(0) = 0, so c = 0 and
+    h = 0 exactly (Eq. (7)-(12) at A = 0)."""
+    x, wx, wh, b = rand_layer(1, 2, 3, 4, 5, 2, 3)
+    out = oracle.forward(x, 0 * wx, 0 * wh, 0 * b, want_hd=True)
+    assert np.all(out["h"] == 0.0) and np.all(out["hd"] == 0.0)
+
+
+@pytest.mark.parametrize("d", range(6))
+def test_zeroed_directions_isolate_one(d):
+    """With the other five directions' parameters at zero their h^d vanish
+    exactly, so the summed output of Eq. (13) equals h^d bitwise."""
+    x, wx, wh, b = rand_layer(2, 1, 4, 5, 6, 2, 3)
+    full = oracle.forward(x, wx, wh, b, want_hd=True)
+    iso = oracle.forward(x, *only_direction(d, wx, wh, b))
+    assert np.array_equal(iso["h"], full["hd"][d])
+    # and the summed output is the sum of the six directions
+    np.testing.assert_allclose(full["h"], full["hd"].sum(0), rtol=0, atol=1e-14)
+
+
+# ----------------------------------------------------- P1 textbook 1D LSTM
+@pytest.mark.parametrize("d", range(6))
+def test_centre_taps_reduce_to_textbook_lstm(d):
+    """Off-centre taps zero: each direction is an independent 1D LSTM of
+    Eq. (1)-(6) along every line of its axis.  torch.nn.LSTM (fp64, gate order
+    i, f, g, o; weight_ih = centre taps of wx, weight_hh = centre taps of wh,
+    bias_ih = b, bias_hh = 0) computes the same thing."""
+    N, D, H, W, C, O = 2, 5, 4, 6, 3, 4
+    x, wx, wh, b = rand_layer(10 + d, N, D, H, W, C, O, scale=0.5)
+    mask = np.zeros((3, 3))
+    mask[1, 1] = 1.0
+    wx, wh = wx * mask, wh * mask
+    out = oracle.forward(x, wx, wh, b, want_hd=True)
+    ref = lstm_lines(x, wx[d, :, :, 1, 1], b[d], wh[d, :, :, 1, 1], axis=d // 2,
+                     sign=1 if d % 2 == 0 else -1)
+    np.testing.assert_allclose(out["hd"][d], ref, rtol=0, atol=1e-13)
+
+
+# ------------------------------------------------- P2 library convolution
+def _conv_planes(x, wx, b, d):
+    """A = conv2d(plane, wx[d]) + b[d] for every plane of direction d
+    (library cross-correlation, padding 1); returns [N][D][H][W][4O]."""
+    xt = torch.from_numpy(x)
+    out = []
+    a = d // 2
+    perm = {0: (1, 0, 4, 2, 3), 1: (2, 0, 4, 1, 3), 2: (3, 0, 4, 1, 2)}[a]
+    xp = xt.permute(*perm)
+    for s in range(xp.shape[0]):
+        out.append(torch.nn.functional.conv2d(xp[s], torch.from_numpy(wx[d]),
+                                              torch.from_numpy(b[d]), padding=1))
+    A = torch.stack(out)                                  # [T][N][4O][P][Q]
+    inv = [0] * 5
+    for i, p in enumerate(perm):
+        inv[p] = i
+    return A.permute(*inv).numpy()
+
+
+@pytest.mark.parametrize("d", range(6))
+def test_no_recurrence_no_forget_is_per_plane_conv(d):
+    """W_h = 0, W_xf = 0 and forget bias -200 (sigma = 1e-87): every plane is
+    independent and h^d = sigma(A_o) tanh(sigma(A_i) tanh(A_g)) with A the
+    library 2D convolution of the plane.  Pins padding, cross-correlation and
+    the tap orientation of each direction."""
+    N, D, H, W, C, O = 1, 4, 5, 7, 2, 3
+    x, wx, wh, b = rand_layer(20 + d, N, D, H, W, C, O, scale=0.5)
+    wh = 0 * wh
+    wx[:, O:2 * O] = 0.0
+    b[:, O:2 * O] = -200.0
+    out = oracle.forward(x, wx, wh, b, want_hd=True)
+    A = _conv_planes(x, wx, b, d)
+    sig = lambda v: 1.0 / (1.0 + np.exp(-v))
+    ref = sig(A[..., 3 * O:]) * np.tanh(sig(A[..., :O]) * np.tanh(A[..., 2 * O:3 * O]))
+    np.testing.assert_allclose(out["hd"][d], ref, rtol=0, atol=1e-14)
+
+
+@pytest.mark.parametrize("d", range(6))
+def test_no_recurrence_is_linear_cell_scan(d):
+    """W_h = 0 alone: pre-activations are per-plane library convolutions and
+    the cell is the linear scan c_t = i_t g_t + f_t c_{t-1} along each line
+    (Eq. (10)), h_t = o_t tanh c_t (Eq. (12))."""
+    N, D, H, W, C, O = 2, 5, 3, 4, 2, 3
+    x, wx, wh, b = rand_layer(30 + d, N, D, H, W, C, O, scale=0.5)
+    wh = 0 * wh
+    out = oracle.forward(x, wx, wh, b, want_hd=True)
+    A = _conv_planes(x, wx, b, d)
+    sig = lambda v: 1.0 / (1.0 + np.exp(-v))
+    i, f = sig(A[..., :O]), sig(A[..., O:2 * O])
+    g, o = np.tanh(A[..., 2 * O:3 * O]), sig(A[..., 3 * O:])
+    ax = d // 2 + 1
+    i, f, g, o = (np.moveaxis(v, ax, 0) for v in (i, f, g, o))
+    if d % 2:
+        i, f, g, o = (v[::-1] for v in (i, f, g, o))
+    c = np.zeros_like(i[0])
+    hs = []
+    for t in range(i.shape[0]):
+        c = i[t] * g[t] + f[t] * c
+        hs.append(o[t] * np.tanh(c))
+    h = np.stack(hs)
+    if d % 2:
+        h = h[::-1]
+    np.testing.assert_allclose(out["hd"][d], np.moveaxis(h, 0, ax), rtol=0, atol=1e-14)
+
+
+# ------------------------------------------- library-convolution formulation
+@pytest.mark.parametrize("shape", [(1, 4, 5, 6, 2, 3), (2, 3, 3, 4, 1, 2), (1, 2, 6, 3, 3, 4)])
+def test_matches_library_conv_formulation(shape):
+    """Eq. (7)-(13) written with torch conv2d on whole planes (fp64) agrees
+    with the nested loops; pins both convolutions' layouts for all six
+    directions with generic (off-centre) weights."""
+    N, D, H, W, C, O = shape
+    x, wx, wh, b = rand_layer(40, N, D, H, W, C, O, scale=0.4)
+    out = oracle.forward(x, wx, wh, b, want_hd=True)
+    t = [torch.from_numpy(v) for v in (x, wx, wh, b)]
+    ref = torch_layer(*t, per_direction=True)
+    for d in range(6):
+        np.testing.assert_allclose(out["hd"][d], ref[d].numpy(), rtol=0, atol=1e-13)
+
+
+# ------------------------------------------------------ P7 brute force
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1, 1, 1), (1, 2, 3, 4, 2, 2), (2, 3, 2, 2, 1, 3),
+                                   (1, 4, 3, 2, 3, 1), (1, 3, 3, 3, 2, 2)])
+def test_brute_force_recursion(shape):
+    """A pull-style memoised recursion from Eq. (7)-(12) at every voxel of
+    small non-cubic volumes (axis swaps would show) agrees with the sweep."""
+    N, D, H, W, C, O = shape
+    x, wx, wh, b = rand_layer(50, N, D, H, W, C, O, scale=0.5)
+    out = oracle.forward(x, wx, wh, b, want_hd=True)
+    ref = brute_force(x, wx, wh, b)
+    np.testing.assert_allclose(out["hd"], ref, rtol=0, atol=1e-13)
+
+
+# ---------------------------------------------------- P9 closed form 1x1x1
+def test_single_voxel_closed_form():
+    """A 1x1x1 volume: every direction takes one step with its centre taps,
+    no predecessor, so h = sum_d o_d tanh(i_d g_d) with
+    A_d = b_d + wx_d[:, :, 1, 1] x (Eq. (7)-(13))."""
+    x, wx, wh, b = rand_layer(60, 1, 1, 1, 1, 3, 2, scale=0.8)
+    out = oracle.forward(x, wx, wh, b)
+    O = 2
+    xv = x.reshape(3)
+    sig = lambda v: 1.0 / (1.0 + math.exp(-v))
+    h = np.zeros(O)
+    for d in range(6):
+        A = b[d] + wx[d, :, :, 1, 1] @ xv
+        for o in range(O):
+            h[o] += sig(A[3 * O + o]) * math.tanh(sig(A[o]) * math.tanh(A[2 * O + o]))
+    np.testing.assert_allclose(out["h"].reshape(O), h, rtol=0, atol=1e-15)
+
+
+# ------------------------------------------------------- P4 symmetries
+@pytest.mark.parametrize("axis", [0, 1, 2])
+def test_mirror_isolated_swaps_plus_minus(axis):
+    """Mirroring the volume along a sweep axis turns the + sweep into the -
+    sweep: with the same parameters in both directions of that axis,
+    h^{a-}(x) = M h^{a+}(M x), bitwise (identical per-voxel operations)."""
+    x, wx, wh, b = rand_layer(70 + axis, 2, 4, 5, 6, 2, 3)
+    dp, dm = 2 * axis, 2 * axis + 1
+    wx[dm], wh[dm], b[dm] = wx[dp], wh[dp], b[dp]
+    ref = oracle.forward(x, wx, wh, b, want_hd=True)["hd"]
+    xm = np.flip(x, axis=axis + 1).copy()
+    mir = oracle.forward(xm, wx, wh, b, want_hd=True)["hd"]
+    assert np.array_equal(ref[dm], np.flip(mir[dp], axis=axis + 1))
+    assert np.array_equal(ref[dp], np.flip(mir[dm], axis=axis + 1))
+
+
+@pytest.mark.parametrize("axis", [0, 1, 2])
+def test_mirror_full_layer(axis):
+    """h(M x; theta') = M h(x; theta), where theta' swaps the + and - parameter
+    sets of the mirrored axis and flips the other four directions' kernels
+    along the tap that runs over that axis."""
+    x, wx, wh, b = rand_layer(80 + axis, 1, 4, 5, 6, 2, 3)
+    wx2, wh2, b2 = wx.copy(), wh.copy(), b.copy()
+    for d in range(6):
+        a = d // 2
+        if a == axis:
+            other = d ^ 1
+            wx2[d], wh2[d], b2[d] = wx[other], wh[other], b[other]
+        else:
+            inplane = [ax for ax in range(3) if ax != a]
+            tap = 2 + inplane.index(axis)        # ka is dim 2, kb dim 3 of wx[d]
+            wx2[d] = np.flip(wx[d], axis=tap)
+            wh2[d] = np.flip(wh[d], axis=tap)
+    ref = oracle.forward(x, wx, wh, b)["h"]
+    mir = oracle.forward(np.flip(x, axis=axis + 1).copy(), wx2, wh2, b2)["h"]
+    np.testing.assert_allclose(np.flip(mir, axis=axis + 1), ref, rtol=0, atol=1e-13)
+
+
+def test_transpose_h_w_swaps_y_and_x():
+    """Swapping the H and W axes of the volume maps the y sweeps onto the x
+    sweeps (same taps: ka over D, kb over the other in-plane axis) and the z
+    sweeps onto themselves with transposed 3x3 kernels."""
+    x, wx, wh, b = rand_layer(90, 1, 3, 4, 6, 2, 3)
+    perm = [0, 1, 3, 2, 4]
+    wx2, wh2, b2 = wx.copy(), wh.copy(), b.copy()
+    for d in (0, 1):
+        wx2[d] = np.swapaxes(wx[d], 2, 3)
+        wh2[d] = np.swapaxes(wh[d], 2, 3)
+    for d, e in ((2, 4), (3, 5), (4, 2), (5, 3)):
+        wx2[d], wh2[d], b2[d] = wx[e], wh[e], b[e]
+    ref = oracle.forward(x, wx, wh, b)["h"]
+    tr = oracle.forward(np.transpose(x, perm).copy(), wx2, wh2, b2)["h"]
+    np.testing.assert_allclose(np.transpose(tr, perm), ref, rtol=0, atol=1e-13)
+
+
+# ----------------------------------------------------- P5 dependency cone
+@pytest.mark.parametrize("d", range(6))
+def test_dependency_cone(d):
+    """Perturb one input voxel.  With only direction d active, an output voxel
+    changes iff it lies in the perturbation's pyramid: at or after the
+    perturbed plane in sweep order, within Chebyshev distance 1 + (t - t') in
+    the plane (one pixel per 3 x 3 convolution).  Outside: bitwise unchanged."""
+    N, D, H, W, C, O = 1, 6, 7, 8, 1, 2
+    x, wx, wh, b = rand_layer(100 + d, N, D, H, W, C, O, scale=0.5)
+    wx, wh, b = only_direction(d, wx, wh, b)
+    src = (2, 3, 4)
+    ref = oracle.forward(x, wx, wh, b)["h"][0]
+    x2 = x.copy()
+    x2[0][src] += 1.0
+    per = oracle.forward(x2, wx, wh, b)["h"][0]
+    changed = np.any(per != ref, axis=-1)
+    a, sign = d // 2, (1 if d % 2 == 0 else -1)
+    inplane = [ax for ax in range(3) if ax != a]
+    idx = np.indices((D, H, W))
+    dt = sign * (idx[a] - src[a])
+    cheb = np.maximum(abs(idx[inplane[0]] - src[inplane[0]]),
+                      abs(idx[inplane[1]] - src[inplane[1]]))
+    cone = (dt >= 0) & (cheb <= 1 + dt)
+    assert np.array_equal(changed, cone)
+
+
+def test_summed_output_sees_whole_volume():
+    """With all six directions, every output voxel depends on every input
+    voxel (the six pyramids tile the volume; full context, Section 2.2)."""
+    x, wx, wh, b = rand_layer(110, 1, 5, 6, 7, 1, 2, scale=0.5)
+    ref = oracle.forward(x, wx, wh, b)["h"][0]
+    for src in [(0, 0, 0), (2, 3, 4), (4, 5, 6)]:
+        x2 = x.copy()
+        x2[0][src] += 1.0
+        per = oracle.forward(x2, wx, wh, b)["h"][0]
+        assert np.all(np.any(per != ref, axis=-1))
+
+
+# ------------------------------------------------ P6 gradients
+def _loss(x, wx, wh, b, dh):
+    return float(np.sum(oracle.forward(x, wx, wh, b)["h"] * dh))
+
+
+def test_backward_finite_differences():
+    """Central differences (eps = 1e-6) of L = sum(h * dh) against the oracle's
+    analytic gradient, for every parameter tensor and the input."""
+    N, D, H, W, C, O = 1, 2, 3, 4, 2, 3
+    x, wx, wh, b = rand_layer(120, N, D, H, W, C, O, scale=0.5)
+    dh = np.random.default_rng(121).standard_normal((N, D, H, W, O))
+    g = oracle.backward(x, wx, wh, b, dh)
+    eps = 1e-6
+    rng = np.random.default_rng(122)
+    args = {"x": x, "wx": wx, "wh": wh, "b": b}
+    for name, key in (("x", "dx"), ("wx", "dwx"), ("wh", "dwh"), ("b", "db")):
+        arr = args[name]
+        flat = arr.reshape(-1)
+        picks = rng.choice(flat.size, size=min(flat.size, 40), replace=False)
+        for k in picks:
+            saved = flat[k]
+            flat[k] = saved + eps
+            lp = _loss(**args, dh=dh)
+            flat[k] = saved - eps
+            lm = _loss(**args, dh=dh)
+            flat[k] = saved
+            fd = (lp - lm) / (2 * eps)
+            an = g[key].reshape(-1)[k]
+            assert abs(fd - an) <= 1e-7 + 1e-6 * abs(an), (name, k, fd, an)
+
+
+@pytest.mark.parametrize("shape", [(2, 3, 4, 5, 2, 3), (1, 5, 2, 3, 3, 2)])
+def test_backward_matches_autograd(shape):
+    """torch.autograd through the library-convolution formulation (fp64)
+    gives the same gradients as the oracle's hand-derived back-propagation."""
+    N, D, H, W, C, O = shape
+    x, wx, wh, b = rand_layer(130, N, D, H, W, C, O, scale=0.4)
+    dh = np.random.default_rng(131).standard_normal((N, D, H, W, O))
+    g = oracle.backward(x, wx, wh, b, dh)
+    t = [torch.from_numpy(v.copy()).requires_grad_(True) for v in (x, wx, wh, b)]
+    h = torch_layer(*t)
+    (h * torch.from_numpy(dh)).sum().backward()
+    for tv, key in zip(t, ("dx", "dwx", "dwh", "db")):
+        np.testing.assert_allclose(g[key], tv.grad.numpy(), rtol=0,
+                                   atol=1e-12 * max(1.0, np.abs(g[key]).max()))
+
+
+# ---------------------------------------------- fully connected + softmax
+def test_fc_tanh_and_softmax_ce_match_torch():
+    """Per-voxel FC + tanh and the final linear + softmax + mean cross-entropy
+    (Section 2.3, Fig. 3) against torch fp64 functions and autograd."""
+    rng = np.random.default_rng(140)
+    M, Cin, Cout, Kc = 37, 5, 7, 4
+    x = rng.standard_normal((M, Cin))
+    w1, b1 = rng.uniform(-0.5, 0.5, (Cout, Cin)), rng.uniform(-0.5, 0.5, Cout)
+    w2, b2 = rng.uniform(-0.5, 0.5, (Kc, Cout)), rng.uniform(-0.5, 0.5, Kc)
+    lab = rng.integers(0, Kc, M)
+    y = oracle.fc_tanh_forward(x, w1, b1)
+    sm = oracle.softmax_ce(y, w2, b2, lab, grad=True)
+    dy = sm["dx"]
+    fb = oracle.fc_tanh_backward(x, w1, y, dy)
+
+    tx, tw1, tb1, tw2, tb2 = [torch.from_numpy(v.copy()).requires_grad_(True)
+                              for v in (x, w1, b1, w2, b2)]
+    ty = torch.tanh(torch.nn.functional.linear(tx, tw1, tb1))
+    logits = torch.nn.functional.linear(ty, tw2, tb2)
+    loss = torch.nn.functional.cross_entropy(logits, torch.from_numpy(lab))
+    loss.backward()
+    np.testing.assert_allclose(y, ty.detach().numpy(), rtol=0, atol=1e-14)
+    np.testing.assert_allclose(sm["p"], torch.softmax(logits, -1).detach().numpy(), rtol=0, atol=1e-14)
+    assert abs(sm["loss"] - loss.item()) < 1e-13
+    for got, ref in ((sm["dw"], tw2), (sm["db"], tb2), (fb["dw"], tw1), (fb["db"], tb1),
+                     (fb["dx"], tx)):
+        np.testing.assert_allclose(got, ref.grad.numpy(), rtol=0, atol=1e-14)
+
+
+def test_network_backward_finite_differences():
+    """The stacked network (PyraMiD -> FC tanh -> PyraMiD -> FC tanh ->
+    linear -> softmax -> mean CE): chain-rule gradients of every parameter
+    tensor against central differences."""
+    rng = np.random.default_rng(150)
+    N, D, H, W, C = 1, 2, 3, 3, 2
+    x = rng.standard_normal((N, D, H, W, C))
+    layers = [synth.layer_params(rng, C, 2), synth.layer_params(rng, 4, 3)]
+    layers = [(l.wx.astype(np.float64) * 3, l.wh.astype(np.float64) * 3, l.b.astype(np.float64))
+              for l in layers]
+    fcs = [(rng.uniform(-0.5, 0.5, (4, 2)), rng.uniform(-0.5, 0.5, 4)),
+           (rng.uniform(-0.5, 0.5, (6, 3)), rng.uniform(-0.5, 0.5, 6))]
+    head = (rng.uniform(-0.5, 0.5, (4, 6)), rng.uniform(-0.5, 0.5, 4))
+    lab = rng.integers(0, 4, N * D * H * W)
+    g = onet.backward(x, layers, fcs, head, lab)
+    eps = 1e-6
+
+    def L():
+        return onet.forward(x, layers, fcs, head, lab)["loss"]
+
+    checks = [(head[0], g["head"][0]), (head[1], g["head"][1])]
+    for li in range(2):
+        checks += [(fcs[li][0], g["fcs"][li][0]), (fcs[li][1], g["fcs"][li][1])]
+        checks += [(layers[li][0], g["layers"][li][0]), (layers[li][1], g["layers"][li][1]),
+                   (layers[li][2], g["layers"][li][2])]
+    for arr, grad in checks:
+        flat = arr.reshape(-1)
+        for k in rng.choice(flat.size, size=min(flat.size, 6), replace=False):
+            s = flat[k]
+            flat[k] = s + eps
+            lp = L()
+            flat[k] = s - eps
+            lm = L()
+            flat[k] = s
+            fd = (lp - lm) / (2 * eps)
+            an = grad.reshape(-1)[k]
+            assert abs(fd - an) <= 1e-8 + 1e-5 * abs(an), (fd, an)
+
+
+# ------------------------------------------------- P8 parameter structure
+def test_parameter_count_matches_paper():
+    """Section 3 ("Experimental Setup") prints 10,751,549 weights for three
+    PyraMiD-LSTM layers (16, 32, 64 hidden) with FC layers (25, 45, classes),
+    7x7 filters.  Six independent parameter sets per layer, four gates, a KxK
+    filter on the input and on the hidden state, no peepholes, and a bias per
+    convolution per gate (the two are sum-equivalent, so the layer folds them
+    into one b) reproduce it to within 2 with 5 input channels and 5 outputs;
+    one bias per gate is 2,690 short."""
+    with open(os.path.join(GOLDEN, "param_count.txt")) as f:
+        fields = dict(line.split("=", 1) for line in f.read().splitlines()
+                      if "=" in line and not line.startswith("#"))
+    printed = int(fields["printed_weights"])
+    K, C, classes = int(fields["K"]), int(fields["C_in"]), int(fields["classes"])
+    layers = [(16, 25), (32, 45), (64, classes)]
+    # Parameter shapes as the oracle consumes them, per layer:
+    def count(bias_per_gate):
+        tot, cin = 0, C
+        for O, fc in layers:
+            tot += int(np.prod((6, 4 * O, cin, K, K)))      # wx
+            tot += int(np.prod((6, 4 * O, O, K, K)))        # wh
+            tot += bias_per_gate * int(np.prod((6, 4 * O)))  # b
+            tot += O * fc + fc                               # per-voxel FC
+            cin = fc
+        return tot
+    assert abs(count(2) - printed) <= 2
+    assert abs(count(1) - printed) > 1000
+
+
+# --------------------------------------------- generator determinism
+def test_generators_are_deterministic():
+    a, b2 = synth.config(1), synth.config(1)
+    assert np.array_equal(a.x, b2.x)
+    for la, lb in zip(a.layers, b2.layers):
+        assert np.array_equal(la.wx, lb.wx) and np.array_equal(la.wh, lb.wh)
+    assert a.x.dtype == np.float32
+    bf = synth.round_bf16(np.array([1.0, 1.00390625, 1.005859375, -3.14159], np.float32))
+    assert bf[0] == 1.0 and bf[1] == 1.0 and bf[2] == 1.0078125   # ties to even
+    assert np.all(synth.bf16_bits(bf).astype(np.uint32) << 16 == bf.view(np.uint32))

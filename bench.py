@@ -1,0 +1,197 @@
+#!/usr/bin/env python3
+"""Benchmark of the PyraMiD-LSTM hot path on one MI355X; prints one JSON line.
+
+Workload: the MR-like volume 48 x 240 x 240 x 3 (seeded, synthetic; stands in
+for the MRBrainS13 stacks), one PyraMiD-LSTM layer with 16 hidden units and
+3x3 filters (six directions summed), fp32.
+
+A timed step is one pass of the whole hot path: layer forward (six sweeps,
+saving activations), per-voxel FC tanh (16 -> 32), linear + softmax +
+cross-entropy head against seeded labels, and back-propagation through all of
+it (head, FC, the six reverse sweeps, parameter and input gradients).  The
+layer forward alone (inference, the single-layer forward workload) is timed as
+well and reported under "fwd".  Inputs are resident in HBM before timing.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "voxel-direction LSTM updates/sec (fwd, fwd+bwd) + % peak MFMA, 1 MI355X"
+UNIT = "voxel-direction updates/s"
+PEAK_FP32_TFLOPS = 157.3     # MI355X dense fp32 MFMA
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+
+
+def phase_work(name, V, C, O):
+    """(bound, algorithmic amount per pass, unit) of a library phase for one
+    layer over V voxels.  Contraction flops count the dense 3x3 stencils."""
+    G = 4 * O
+    if name.startswith("sweep_fwd"):
+        return "mfma", 6 * V * 2 * 9 * G * (C + O), "TFLOP/s"
+    if name.startswith("sweep_bwd"):
+        # recurrent transposed convolution (dh) plus the gate gradients
+        return "mfma", 6 * V * 2 * 9 * G * O, "TFLOP/s"
+    if name.startswith("wgrad"):
+        return "mfma", 6 * V * 2 * G * (9 * (C + O) + 1), "TFLOP/s"
+    if name.startswith("dx"):
+        return "mfma", 6 * V * 2 * 9 * G * C, "TFLOP/s"
+    if name.startswith("sum_dirs"):
+        return "hbm", (6 + 1) * V * O * 4, "GB/s"
+    return None, None, None
+
+
+def roofline(phases, name, passes, V, C, O):
+    ms, launches = phases[name]
+    bound, amount, unit = phase_work(name, V, C, O)
+    if bound is None:
+        return None
+    per_launch = amount * passes / launches
+    avg_s = ms / 1e3 / launches
+    if bound == "hbm":
+        achieved, peak = per_launch / avg_s / 1e9, PEAK_HBM_GBS
+    else:
+        achieved, peak = per_launch / avg_s / 1e12, PEAK_FP32_TFLOPS
+    return {"kernel": name, "bound": bound, "achieved": round(achieved, 3), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+            "launches_per_pass": launches // passes,
+            "avg_launch_ms": round(ms / launches, 4)}
+
+
+def cpu_baseline(inst_cfg, crop):
+    """The fp64 oracle (as is) on a bounded crop of the same workload."""
+    import numpy as np
+    import oracle
+    import oracle.network as onet
+    D, H, W = crop
+    x = inst_cfg.x[:, :D, :H, :W, :]
+    lab = inst_cfg.labels.reshape(inst_cfg.x.shape[:4])[:, :D, :H, :W].reshape(-1)
+    layers = [(L.wx, L.wh, L.b) for L in inst_cfg.layers]
+    t0 = time.perf_counter()
+    onet.backward(x, layers, inst_cfg.fcs, inst_cfg.head, lab)
+    dt = time.perf_counter() - t0
+    vdu = 6 * int(np.prod(x.shape[:4]))
+    return {"value": vdu / dt, "unit": UNIT, "cores": oracle.threads(), "kind": "oracle",
+            "sample": "oracle fp64 training step (layer fwd+bwd, FC tanh, softmax-CE) on a "
+                      "%dx%dx%dx%d crop of the same volume, %.1f s" % (D, H, W, x.shape[-1], dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-crop", default="48x120x120")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the six sweeps of a layer run concurrently "
+              "on a single MI355X and this build has no multi-GPU path (--gpus 1).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_1506_07452_amd as P
+    from paper_1506_07452_amd.network import (layer_forward, network_train_step,
+                                              workspace_for)
+    from paper_1506_07452_amd.network import LayerW
+
+    def dev(a):
+        return torch.from_numpy(a).to("cuda:0").contiguous()
+
+    def layer_dev(L):
+        return LayerW(dev(L.wx), dev(L.wh), dev(L.b))
+
+    wl = synth.Workload("MR-like 48x240x240x3 O=16 step", 1, 48, 240, 240, 3, [16], fc=True,
+                        classes=4, labels=True, kind="mr", cfg=2)
+    inst = synth.make(wl)
+    N, D, H, W, C = inst.x.shape
+    O = wl.hidden[0]
+    V = N * D * H * W
+    torch.cuda.init()
+    x = dev(inst.x)
+    layers = [layer_dev(L) for L in inst.layers]
+    fcs = [(dev(w), dev(b)) for w, b in inst.fcs]
+    head = (dev(inst.head[0]), dev(inst.head[1]))
+    labels = torch.from_numpy(inst.labels).to("cuda:0")
+    ws = workspace_for(x.shape, wl.hidden, True, torch.float32, True, "cuda:0")
+    torch.cuda.synchronize()
+
+    def step():
+        return network_train_step(x, layers, fcs, head, labels, ws=ws)
+
+    def fwd():
+        return layer_forward(x, layers[0], False, ws=ws)
+
+    # --- fwd+bwd (headline) ---
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    P.pyramid_lstm_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t_step = (time.perf_counter() - t0) / args.steps
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+
+    # --- forward only ---
+    for _ in range(args.warmup):
+        fwd()
+    torch.cuda.synchronize()
+    P.pyramid_lstm_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        fwd()
+    torch.cuda.synchronize()
+    t_fwd = (time.perf_counter() - t0) / args.steps
+    phases_fwd = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+
+    vdu = 6 * V
+    fwd_flops = 6 * V * 2 * 9 * 4 * O * (C + O)
+    dom = max(phases, key=lambda k: phases[k][0])
+    sweep_fwd_name = [k for k in phases_fwd if k.startswith("sweep_fwd")][0]
+    out = {
+        "metric": METRIC,
+        "value": vdu / t_step,
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "MR-like 48x240x240x3 volume, one PyraMiD-LSTM layer (O=16, "
+                               "3x3, 6 directions) + FC tanh 32 + softmax-CE head, fwd+bwd",
+                   "N": N, "D": D, "H": H, "W": W, "C": C, "O": O, "classes": 4},
+        "fwd": {"value": vdu / t_fwd, "ms_per_pass": t_fwd * 1e3,
+                "tflops": fwd_flops / t_fwd / 1e12,
+                "frac_fp32_mfma_peak": fwd_flops / t_fwd / 1e12 / PEAK_FP32_TFLOPS,
+                "roofline": roofline(phases_fwd, sweep_fwd_name, args.steps, V, C, O)},
+        "roofline": roofline(phases, dom, args.steps, V, C, O),
+        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
+    }
+    if not args.no_cpu_baseline:
+        crop = tuple(int(v) for v in args.cpu_crop.split("x"))
+        out["cpu_baseline"] = cpu_baseline(inst, crop)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,159 @@
+/*
+ * pyramid_lstm.h -- C ABI of the MI355X (gfx950) PyraMiD-LSTM library.
+ *
+ * The layer (Stollenga et al., arXiv 1506.07452, Section 2.3):
+ *   six C-LSTMs, one per direction d in {z+, z-, y+, y-, x+, x-} (paper axes
+ *   x, y, z = volume W, H, D; direction set of Section 2.3), each sweeping the
+ *   volume plane by plane.  At every plane each voxel computes the gate
+ *   pre-activations of Eq. (7)-(9), (11) as a 3x3 2D convolution of the input
+ *   plane plus a 3x3 2D convolution of the previous plane's hidden state plus a
+ *   per-gate bias shared by all positions, then the cell and hidden update of
+ *   Eq. (10), (12); the layer output is the sum of the six directions, Eq. (13).
+ *
+ * Conventions shared by every entry point:
+ *   - All tensor pointers are DEVICE pointers (hipMalloc'd or equivalent),
+ *     owned by the caller, aligned to 16 bytes.  The library never allocates,
+ *     frees, or synchronises: work is enqueued on `stream` (a hipStream_t; NULL
+ *     is the legacy default stream) and completes asynchronously.
+ *   - Arguments are validated before anything is enqueued; an error is a
+ *     negative return code (never an abort or exception) and nothing has been
+ *     launched.  PLSTM_EHIP means a HIP launch failed after validation.
+ *   - Calls on distinct streams with distinct buffers are independent.
+ *   - Storage type (plstm_shape.dtype): PLSTM_F32 = IEEE fp32; PLSTM_BF16 =
+ *     bfloat16 (uint16 bit patterns) for x, wx, wh, b and h.  Accumulation is
+ *     always fp32; the cell state is always fp32.
+ *   - Layouts are row-major, channels last:
+ *       x   [N][D][H][W][C]        volume, C input channels
+ *       h   [N][D][H][W][O]        layer output (sum of the six directions)
+ *       wx  [6][4*O][C][3][3]      input filters, per direction
+ *       wh  [6][4*O][O][3][3]      recurrent filters, per direction
+ *       b   [6][4*O]               biases, per direction
+ *     Direction order 0..5 = z+, z-, y+, y-, x+, x- (Section 2.3).  Row g*O+o
+ *     of wx/wh/b is unit o of gate g, gates in the order (i, f, g=c~, o) of
+ *     Eq. (7), (8), (9), (11).  The 3x3 taps (ka, kb) run over the plane's two
+ *     in-plane axes in (D, H, W) order: z+- -> (H, W), y+- -> (D, W),
+ *     x+- -> (D, H); the same for the + and - direction of an axis.  The
+ *     convolution is a cross-correlation with zero "same" padding:
+ *       A[p][q][g*O+o] += in[p+ka-1][q+kb-1][c] * w[g*O+o][c][ka][kb].
+ *     Plane t of a + sweep is index t along its axis, of a - sweep index T-1-t;
+ *     the first plane has no predecessor (h_{-1} = c_{-1} = 0, Section 2.3).
+ *   - Supported: N, D, H, W >= 1; 1 <= C <= 1024; O in {4, 8, 16, 32, 64}.
+ */
+#ifndef PYRAMID_LSTM_H
+#define PYRAMID_LSTM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum plstm_status {
+    PLSTM_OK = 0,
+    PLSTM_EINVAL = -1,          /* null pointer, bad dimension or alignment */
+    PLSTM_EUNSUPPORTED = -2,    /* valid but not supported (O, dtype, size) */
+    PLSTM_EWORKSPACE = -3,      /* ws_bytes smaller than the required size */
+    PLSTM_EHIP = -4,            /* a HIP runtime call or launch failed */
+    PLSTM_ENOTCORESIDENT = -5   /* the GPU cannot hold the persistent grid */
+};
+
+enum plstm_dtype { PLSTM_F32 = 0, PLSTM_BF16 = 1 };
+
+typedef struct plstm_shape {
+    int32_t N, D, H, W;   /* batch and volume extents */
+    int32_t C;            /* input channels */
+    int32_t O;            /* hidden units per direction */
+    int32_t dtype;        /* enum plstm_dtype */
+} plstm_shape;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *pyramid_lstm_status_string(int status);
+
+/* Bytes of device workspace `ws` needed by pyramid_lstm_forward (training = 0
+ * or 1) and pyramid_lstm_backward (training = 1 covers both).  Returns 0 for an
+ * invalid or unsupported shape. */
+size_t pyramid_lstm_workspace_size(const plstm_shape *s, int training);
+
+/* Bytes of the `saved` buffer that a training forward fills and the backward
+ * reads (gate activations and cell states of every voxel and direction, in a
+ * library-private layout).  Returns 0 for an invalid or unsupported shape. */
+size_t pyramid_lstm_saved_size(const plstm_shape *s);
+
+/* Forward pass of one layer, Eq. (7)-(13).
+ *   x, wx, wh, b : inputs (layouts above), read only.
+ *   h            : output [N][D][H][W][O], overwritten.
+ *   saved        : NULL for inference; else pyramid_lstm_saved_size() bytes,
+ *                  overwritten with what pyramid_lstm_backward needs.
+ *   ws, ws_bytes : scratch of at least pyramid_lstm_workspace_size(s, saved != NULL)
+ *                  bytes; contents undefined on return.
+ * Returns PLSTM_OK or a negative status. */
+int pyramid_lstm_forward(const plstm_shape *s, const void *x, const void *wx,
+                         const void *wh, const void *b, void *h, void *saved,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* Backward pass of one layer: back-propagation through the six sweeps (the
+ * chain rule through Eq. (7)-(13); the paper trains the layer by gradient
+ * descent, Section 3 "Training").  fp32 only.
+ *   x, wx, wh, b : the forward's inputs; saved: the forward's saved buffer.
+ *   dh           : dL/dh [N][D][H][W][O].
+ *   dx           : NULL, or dL/dx [N][D][H][W][C], overwritten.
+ *   dwx, dwh, db : dL/dwx, dL/dwh, dL/db in the layouts of wx, wh, b, summed
+ *                  over the batch, overwritten.
+ *   ws, ws_bytes : at least pyramid_lstm_workspace_size(s, 1) bytes.
+ * Returns PLSTM_OK or a negative status. */
+int pyramid_lstm_backward(const plstm_shape *s, const void *x, const void *wx,
+                          const void *wh, const void *b, const void *saved,
+                          const void *dh, void *dx, void *dwx, void *dwh, void *db,
+                          void *ws, size_t ws_bytes, void *stream);
+
+/* Per-voxel fully connected layer squashed by tanh (Section 2.3,
+ * "Fully-Connected Layer"):  y[m][o] = tanh(sum_i w[o][i] x[m][i] + b[o]).
+ *   x [M][Cin], w [Cout][Cin], b [Cout], y [M][Cout]; storage `dtype` for all
+ *   four (fp32 accumulation).  1 <= Cin, Cout <= 1024. */
+int pyramid_fc_tanh_forward(int64_t M, int32_t Cin, int32_t Cout, int32_t dtype,
+                            const void *x, const void *w, const void *b, void *y,
+                            void *stream);
+
+/* Bytes of workspace for pyramid_fc_tanh_backward / pyramid_softmax_ce. */
+size_t pyramid_fc_workspace_size(int64_t M, int32_t Cin, int32_t Cout);
+
+/* Gradient of pyramid_fc_tanh_forward (fp32): given x, w, the forward's output
+ * y and dL/dy, writes dL/dx (nullable) [M][Cin], dL/dw [Cout][Cin] and dL/db
+ * [Cout] (overwritten; deterministic reduction order). */
+int pyramid_fc_tanh_backward(int64_t M, int32_t Cin, int32_t Cout, const void *x,
+                             const void *w, const void *y, const void *dy, void *dx,
+                             void *dw, void *db, void *ws, size_t ws_bytes, void *stream);
+
+/* Last fully connected layer + per-voxel softmax (Fig. 3; Section 2.3):
+ *   p[m][k] = softmax_k(sum_i w[k][i] x[m][i] + b[k]),  1 <= K <= 16.
+ *   x [M][Cin], w [K][Cin], b [K] in storage `dtype`; p [M][K] fp32 output.
+ * If labels (int32 [M], values in [0, K)) is non-NULL, also writes the mean
+ * cross-entropy over the M voxels to *loss (one fp32 on the device) and, when
+ * dx/dw/db are non-NULL (fp32 only), its gradient: dL/dx [M][Cin],
+ * dL/dw [K][Cin], dL/db [K] (overwritten).  ws: pyramid_fc_workspace_size(M,
+ * Cin, K) bytes when labels is non-NULL, else may be NULL. */
+int pyramid_softmax_ce(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const void *x,
+                       const void *w, const void *b, const int32_t *labels, void *p,
+                       void *loss, void *dx, void *dw, void *db, void *ws,
+                       size_t ws_bytes, void *stream);
+
+
+/* Optional kernel timing for measurement tools (off by default).
+ * pyramid_lstm_timing_enable(1) clears earlier records and makes every later
+ * call of this library in the process record a pair of HIP events on its
+ * stream around each kernel phase ("sweep_fwd", "sum_dirs", "sweep_bwd",
+ * "wgrad", "dx", ...); pyramid_lstm_timing_enable(0) clears and stops.
+ * pyramid_lstm_timing_read waits for the recorded events and writes, per
+ * distinct phase (at most max_phases): its name into names[32*k .. 32*k+31]
+ * (NUL-terminated), the summed milliseconds into ms[k] and the number of
+ * kernel launches into launches[k]; *count receives the number of phases. */
+int pyramid_lstm_timing_enable(int on);
+int pyramid_lstm_timing_read(int max_phases, char *names, double *ms, int *launches,
+                             int *count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PYRAMID_LSTM_H */

@@ -56,8 +56,15 @@ def _load():
         lib.oracle_fc_tanh_backward.restype = None
         lib.oracle_softmax_ce.argtypes = [ctypes.c_long, i, i, dp, dp, dp, ip, dp, dp, dp, dp]
         lib.oracle_softmax_ce.restype = ctypes.c_double
+        lib.oracle_threads.argtypes = []
+        lib.oracle_threads.restype = i
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """OpenMP threads used by the oracle's parallel loops."""
+    return int(_load().oracle_threads())
 
 
 def _f64(a):

@@ -51,6 +51,7 @@
  * differences and autograd of the gradients).
  */
 #include <math.h>
+#include <omp.h>
 #include <stddef.h>
 #include <stdlib.h>
 #include <string.h>
@@ -85,6 +86,9 @@ static size_t vidx(int D, int H, int W, int n, int z, int y, int x)
 {
     return (((size_t)n * D + z) * H + y) * W + x;
 }
+
+/* Number of OpenMP threads the oracle's parallel loops use. */
+int oracle_threads(void) { return omp_get_max_threads(); }
 
 static double sigmoid(double a) { return 1.0 / (1.0 + exp(-a)); }
 

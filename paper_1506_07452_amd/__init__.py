@@ -1,0 +1,216 @@
+"""Python binding of libpyramid_lstm.so (the MI355X PyraMiD-LSTM library).
+
+Argument marshalling only: every function here has the name of a C entry point
+declared in include/pyramid_lstm.h, converts torch tensors to device pointers
+and the current HIP stream, calls the entry point and raises on a negative
+status.  All computation runs in the library's HIP kernels; torch provides
+device memory and streams.  There is no fallback: if the library is not built
+the binding raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "PyramidLSTMError", "plstm_shape", "shape_for", "PLSTM_F32", "PLSTM_BF16",
+    "pyramid_lstm_status_string", "pyramid_lstm_workspace_size", "pyramid_lstm_saved_size",
+    "pyramid_lstm_forward", "pyramid_lstm_backward", "pyramid_fc_tanh_forward",
+    "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
+    "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "library_path", "load",
+]
+
+PLSTM_F32 = 0
+PLSTM_BF16 = 1
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libpyramid_lstm.so")
+_lib = None
+
+
+class PyramidLSTMError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (fn, pyramid_lstm_status_string(status), status))
+
+
+class plstm_shape(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int32), ("D", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("W", ctypes.c_int32), ("C", ctypes.c_int32), ("O", ctypes.c_int32),
+                ("dtype", ctypes.c_int32)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError("libpyramid_lstm.so is not built; run "
+                           "`python -m paper_1506_07452_amd.build` first")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, sz, i32, i64 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int64
+    sp = ctypes.POINTER(plstm_shape)
+    lib.pyramid_lstm_status_string.argtypes = [ctypes.c_int]
+    lib.pyramid_lstm_status_string.restype = ctypes.c_char_p
+    lib.pyramid_lstm_workspace_size.argtypes = [sp, ctypes.c_int]
+    lib.pyramid_lstm_workspace_size.restype = sz
+    lib.pyramid_lstm_saved_size.argtypes = [sp]
+    lib.pyramid_lstm_saved_size.restype = sz
+    lib.pyramid_lstm_forward.argtypes = [sp] + [vp] * 7 + [sz, vp]
+    lib.pyramid_lstm_forward.restype = ctypes.c_int
+    lib.pyramid_lstm_backward.argtypes = [sp] + [vp] * 11 + [sz, vp]
+    lib.pyramid_lstm_backward.restype = ctypes.c_int
+    lib.pyramid_fc_tanh_forward.argtypes = [i64, i32, i32, i32] + [vp] * 4 + [vp]
+    lib.pyramid_fc_tanh_forward.restype = ctypes.c_int
+    lib.pyramid_fc_workspace_size.argtypes = [i64, i32, i32]
+    lib.pyramid_fc_workspace_size.restype = sz
+    lib.pyramid_fc_tanh_backward.argtypes = [i64, i32, i32] + [vp] * 8 + [sz, vp]
+    lib.pyramid_fc_tanh_backward.restype = ctypes.c_int
+    lib.pyramid_softmax_ce.argtypes = [i64, i32, i32, i32] + [vp] * 10 + [sz, vp]
+    lib.pyramid_softmax_ce.restype = ctypes.c_int
+    lib.pyramid_lstm_timing_enable.argtypes = [ctypes.c_int]
+    lib.pyramid_lstm_timing_enable.restype = ctypes.c_int
+    lib.pyramid_lstm_timing_read.argtypes = [ctypes.c_int, ctypes.c_char_p,
+                                             ctypes.POINTER(ctypes.c_double),
+                                             ctypes.POINTER(ctypes.c_int),
+                                             ctypes.POINTER(ctypes.c_int)]
+    lib.pyramid_lstm_timing_read.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+# ----------------------------------------------------------------- marshalling
+_DT = {torch.float32: PLSTM_F32, torch.bfloat16: PLSTM_BF16}
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch.Tensor, got %r" % type(t))
+    if not t.is_cuda:
+        raise ValueError("tensor must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(fn, rc):
+    if rc != 0:
+        raise PyramidLSTMError(fn, rc)
+
+
+def shape_for(x: torch.Tensor, O: int) -> plstm_shape:
+    """plstm_shape of a [N][D][H][W][C] volume and hidden size O."""
+    if x.dim() != 5:
+        raise ValueError("x must be [N][D][H][W][C]")
+    if x.dtype not in _DT:
+        raise ValueError("x must be float32 or bfloat16")
+    N, D, H, W, C = x.shape
+    return plstm_shape(N, D, H, W, C, O, _DT[x.dtype])
+
+
+def _workspace(nbytes, device):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+# --------------------------------------------------------------- entry points
+def pyramid_lstm_status_string(status: int) -> str:
+    return load().pyramid_lstm_status_string(int(status)).decode()
+
+
+def pyramid_lstm_workspace_size(shape: plstm_shape, training: int) -> int:
+    return int(load().pyramid_lstm_workspace_size(ctypes.byref(shape), int(training)))
+
+
+def pyramid_lstm_saved_size(shape: plstm_shape) -> int:
+    return int(load().pyramid_lstm_saved_size(ctypes.byref(shape)))
+
+
+def pyramid_lstm_forward(shape, x, wx, wh, b, h, saved=None, ws=None, stream=None):
+    """Layer forward.  ws=None allocates the workspace with torch."""
+    lib = load()
+    if ws is None:
+        ws = _workspace(pyramid_lstm_workspace_size(shape, saved is not None), x.device)
+    _check("pyramid_lstm_forward", lib.pyramid_lstm_forward(
+        ctypes.byref(shape), _ptr(x), _ptr(wx), _ptr(wh), _ptr(b), _ptr(h), _ptr(saved),
+        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_lstm_backward(shape, x, wx, wh, b, saved, dh, dx, dwx, dwh, db, ws=None,
+                          stream=None):
+    lib = load()
+    if ws is None:
+        ws = _workspace(pyramid_lstm_workspace_size(shape, 1), x.device)
+    _check("pyramid_lstm_backward", lib.pyramid_lstm_backward(
+        ctypes.byref(shape), _ptr(x), _ptr(wx), _ptr(wh), _ptr(b), _ptr(saved), _ptr(dh),
+        _ptr(dx), _ptr(dwx), _ptr(dwh), _ptr(db), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def pyramid_fc_tanh_forward(x, w, b, y, stream=None):
+    """x [M][Cin], w [Cout][Cin], b [Cout], y [M][Cout] (same dtype)."""
+    M, Cin = x.shape
+    Cout = w.shape[0]
+    _check("pyramid_fc_tanh_forward", load().pyramid_fc_tanh_forward(
+        M, Cin, Cout, _DT[x.dtype], _ptr(x), _ptr(w), _ptr(b), _ptr(y), _stream(stream)))
+
+
+def pyramid_fc_workspace_size(M: int, Cin: int, Cout: int) -> int:
+    return int(load().pyramid_fc_workspace_size(M, Cin, Cout))
+
+
+def pyramid_fc_tanh_backward(x, w, y, dy, dx, dw, db, ws=None, stream=None):
+    M, Cin = x.shape
+    Cout = w.shape[0]
+    if ws is None:
+        ws = _workspace(pyramid_fc_workspace_size(M, Cin, Cout), x.device)
+    _check("pyramid_fc_tanh_backward", load().pyramid_fc_tanh_backward(
+        M, Cin, Cout, _ptr(x), _ptr(w), _ptr(y), _ptr(dy), _ptr(dx), _ptr(dw), _ptr(db),
+        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_softmax_ce(x, w, b, p, labels=None, loss=None, dx=None, dw=None, db=None, ws=None,
+                       stream=None):
+    """Final linear + softmax (+ mean cross-entropy and its gradient)."""
+    M, Cin = x.shape
+    K = w.shape[0]
+    if labels is not None and ws is None:
+        ws = _workspace(pyramid_fc_workspace_size(M, Cin, K), x.device)
+    _check("pyramid_softmax_ce", load().pyramid_softmax_ce(
+        M, Cin, K, _DT[x.dtype], _ptr(x), _ptr(w), _ptr(b), _ptr(labels), _ptr(p), _ptr(loss),
+        _ptr(dx), _ptr(dw), _ptr(db), _ptr(ws),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_lstm_timing_enable(on: bool) -> None:
+    """Start (clearing earlier records) or stop per-phase HIP-event timing."""
+    _check("pyramid_lstm_timing_enable", load().pyramid_lstm_timing_enable(int(bool(on))))
+
+
+def pyramid_lstm_timing_read(max_phases: int = 32):
+    """{phase: (total_ms, launches)} accumulated since timing was enabled."""
+    names = ctypes.create_string_buffer(32 * max_phases)
+    ms = (ctypes.c_double * max_phases)()
+    launches = (ctypes.c_int * max_phases)()
+    count = ctypes.c_int(0)
+    _check("pyramid_lstm_timing_read", load().pyramid_lstm_timing_read(
+        max_phases, names, ms, launches, ctypes.byref(count)))
+    out = {}
+    for k in range(count.value):
+        nm = names.raw[32 * k:32 * k + 32].split(b"\0", 1)[0].decode()
+        out[nm] = (ms[k], launches[k])
+    return out

@@ -1,0 +1,177 @@
+// C ABI of the PyraMiD-LSTM library: argument validation, workspace sizing and
+// carving, and dispatch to the HIP kernels.  Every check happens before the
+// first HIP call; errors are status codes (no abort, no exception).
+#include <limits.h>
+
+#include "common.h"
+#include "sweep.h"
+
+using namespace plstm;
+
+namespace {
+
+bool aligned(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_shape(const plstm_shape *s)
+{
+    if (!s) return PLSTM_EINVAL;
+    if (s->N < 1 || s->D < 1 || s->H < 1 || s->W < 1 || s->C < 1 || s->O < 1)
+        return PLSTM_EINVAL;
+    if (s->dtype != PLSTM_F32 && s->dtype != PLSTM_BF16) return PLSTM_EINVAL;
+    if (s->C > 1024) return PLSTM_EUNSUPPORTED;
+    if (s->O != 4 && s->O != 8 && s->O != 16 && s->O != 32 && s->O != 64)
+        return PLSTM_EUNSUPPORTED;
+    // grid limits of the generic path: 6N blocks in z, one plane per launch
+    if ((long long)s->N * kDirs > 65535) return PLSTM_EUNSUPPORTED;
+    const long long V = (long long)s->D * s->H * s->W;
+    if (V > (1LL << 31) / 64 || (long long)s->N * V * 4 * s->O * kDirs > (1LL << 40))
+        return PLSTM_EUNSUPPORTED;
+    return PLSTM_OK;
+}
+
+size_t saved_bytes(const Geom &g)
+{
+    Carve cv(nullptr);
+    cv.take<float>(saved_gates_count(g));
+    cv.take<float>(saved_cell_count(g));
+    return cv.off;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *pyramid_lstm_status_string(int status)
+{
+    switch (status) {
+    case PLSTM_OK: return "ok";
+    case PLSTM_EINVAL: return "invalid argument";
+    case PLSTM_EUNSUPPORTED: return "unsupported shape or type";
+    case PLSTM_EWORKSPACE: return "workspace too small";
+    case PLSTM_EHIP: return "HIP runtime error";
+    case PLSTM_ENOTCORESIDENT: return "persistent grid does not fit on the device";
+    default: return "unknown status";
+    }
+}
+
+size_t pyramid_lstm_saved_size(const plstm_shape *s)
+{
+    if (check_shape(s) != PLSTM_OK) return 0;
+    return saved_bytes(make_geom(*s));
+}
+
+size_t pyramid_lstm_workspace_size(const plstm_shape *s, int training)
+{
+    if (check_shape(s) != PLSTM_OK) return 0;
+    const Geom g = make_geom(*s);
+    size_t need = forward_ws(g, s->dtype, training != 0);
+    if (training) {
+        const size_t b = generic_backward_ws(g);
+        if (b > need) need = b;
+    }
+    return need < 256 ? 256 : need;
+}
+
+int pyramid_lstm_forward(const plstm_shape *s, const void *x, const void *wx, const void *wh,
+                         const void *b, void *h, void *saved, void *ws, size_t ws_bytes,
+                         void *stream)
+{
+    int rc = check_shape(s);
+    if (rc != PLSTM_OK) return rc;
+    if (!x || !wx || !wh || !b || !h || !ws) return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(wx) || !aligned(wh) || !aligned(b) || !aligned(h) ||
+        !aligned(ws) || (saved && !aligned(saved)))
+        return PLSTM_EINVAL;
+    if (saved && s->dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
+    if (ws_bytes < pyramid_lstm_workspace_size(s, saved != nullptr)) return PLSTM_EWORKSPACE;
+    const Geom g = make_geom(*s);
+    float *gates = nullptr, *cell = nullptr;
+    if (saved) {
+        Carve cv(saved);
+        gates = cv.take<float>(saved_gates_count(g));
+        cell = cv.take<float>(saved_cell_count(g));
+    }
+    return forward_dispatch(g, s->dtype, x, wx, wh, b, h, gates, cell, ws, (hipStream_t)stream);
+}
+
+int pyramid_lstm_backward(const plstm_shape *s, const void *x, const void *wx, const void *wh,
+                          const void *b, const void *saved, const void *dh, void *dx, void *dwx,
+                          void *dwh, void *db, void *ws, size_t ws_bytes, void *stream)
+{
+    int rc = check_shape(s);
+    if (rc != PLSTM_OK) return rc;
+    if (!x || !wx || !wh || !b || !saved || !dh || !dwx || !dwh || !db || !ws)
+        return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(wx) || !aligned(wh) || !aligned(b) || !aligned(saved) ||
+        !aligned(dh) || (dx && !aligned(dx)) || !aligned(dwx) || !aligned(dwh) ||
+        !aligned(db) || !aligned(ws))
+        return PLSTM_EINVAL;
+    if (s->dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
+    if (ws_bytes < pyramid_lstm_workspace_size(s, 1)) return PLSTM_EWORKSPACE;
+    const Geom g = make_geom(*s);
+    Carve cv(const_cast<void *>(saved));
+    const float *gates = cv.take<float>(saved_gates_count(g));
+    const float *cell = cv.take<float>(saved_cell_count(g));
+    return generic_backward(g, (const float *)x, (const float *)wx, (const float *)wh, gates,
+                            cell, (const float *)dh, (float *)dx, (float *)dwx, (float *)dwh,
+                            (float *)db, ws, (hipStream_t)stream);
+}
+
+size_t pyramid_fc_workspace_size(int64_t M, int32_t Cin, int32_t Cout)
+{
+    if (M < 1 || Cin < 1 || Cout < 1 || Cin > 1024 || Cout > 1024) return 0;
+    const size_t need = fc_ws(M, Cin, Cout);
+    return need < 256 ? 256 : need;
+}
+
+int pyramid_fc_tanh_forward(int64_t M, int32_t Cin, int32_t Cout, int32_t dtype, const void *x,
+                            const void *w, const void *b, void *y, void *stream)
+{
+    if (M < 1 || Cin < 1 || Cout < 1) return PLSTM_EINVAL;
+    if (Cin > 1024 || Cout > 1024 || M > (1LL << 40) / Cout) return PLSTM_EUNSUPPORTED;
+    if (dtype != PLSTM_F32 && dtype != PLSTM_BF16) return PLSTM_EINVAL;
+    if (!x || !w || !b || !y) return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(w) || !aligned(b) || !aligned(y)) return PLSTM_EINVAL;
+    return fc_tanh_forward(M, Cin, Cout, dtype, x, w, b, y, (hipStream_t)stream);
+}
+
+int pyramid_fc_tanh_backward(int64_t M, int32_t Cin, int32_t Cout, const void *x, const void *w,
+                             const void *y, const void *dy, void *dx, void *dw, void *db,
+                             void *ws, size_t ws_bytes, void *stream)
+{
+    if (M < 1 || Cin < 1 || Cout < 1) return PLSTM_EINVAL;
+    if (Cin > 1024 || Cout > 1024 || M > (1LL << 40) / Cout) return PLSTM_EUNSUPPORTED;
+    if (!x || !w || !y || !dy || !dw || !db || !ws) return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(w) || !aligned(y) || !aligned(dy) || (dx && !aligned(dx)) ||
+        !aligned(dw) || !aligned(db) || !aligned(ws))
+        return PLSTM_EINVAL;
+    if (ws_bytes < pyramid_fc_workspace_size(M, Cin, Cout)) return PLSTM_EWORKSPACE;
+    return fc_tanh_backward(M, Cin, Cout, (const float *)x, (const float *)w, (const float *)y,
+                            (const float *)dy, (float *)dx, (float *)dw, (float *)db, ws,
+                            (hipStream_t)stream);
+}
+
+int pyramid_softmax_ce(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const void *x,
+                       const void *w, const void *b, const int32_t *labels, void *p, void *loss,
+                       void *dx, void *dw, void *db, void *ws, size_t ws_bytes, void *stream)
+{
+    if (M < 1 || Cin < 1 || K < 1) return PLSTM_EINVAL;
+    if (Cin > 1024 || K > 16 || M > (1LL << 40) / 16) return PLSTM_EUNSUPPORTED;
+    if (dtype != PLSTM_F32 && dtype != PLSTM_BF16) return PLSTM_EINVAL;
+    if (!x || !w || !b || !p) return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(w) || !aligned(b) || !aligned(p)) return PLSTM_EINVAL;
+    const bool grad = dw || db || dx;
+    if (labels) {
+        if (!loss || !ws || !aligned(labels)) return PLSTM_EINVAL;
+        if (ws_bytes < pyramid_fc_workspace_size(M, Cin, K)) return PLSTM_EWORKSPACE;
+    }
+    if (grad) {
+        if (!labels || !dw || !db) return PLSTM_EINVAL;
+        if (dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
+        if ((dx && !aligned(dx)) || !aligned(dw) || !aligned(db)) return PLSTM_EINVAL;
+    }
+    return softmax_ce(M, Cin, K, dtype, x, w, b, labels, (float *)p, (float *)loss,
+                      (float *)dx, (float *)dw, (float *)db, ws, (hipStream_t)stream);
+}
+
+}  // extern "C"

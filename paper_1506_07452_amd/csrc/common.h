@@ -1,0 +1,121 @@
+// Internal helpers shared by the library's translation units (host + device).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "pyramid_lstm.h"
+
+namespace plstm {
+
+constexpr int kDirs = 6;
+
+// Geometry of one sweep direction (Section 2.3, direction set).  A voxel of
+// batch element n at sweep position s and in-plane pixel (p, q) has linear
+// index n * V + s * ss + p * sp + q * sq in the [N][D][H][W] volume.
+struct DirGeom {
+    int T, P, Q;          // sweep length, in-plane extents (first, second axis)
+    int sign;             // +1: plane t is s = t; -1: plane t is s = T - 1 - t
+    long long ss, sp, sq; // voxel strides of s, p, q
+};
+
+struct Geom {
+    int N, D, H, W, C, O;
+    long long V;          // D * H * W
+    DirGeom dir[kDirs];
+};
+
+inline Geom make_geom(const plstm_shape &s) {
+    Geom g;
+    g.N = s.N; g.D = s.D; g.H = s.H; g.W = s.W; g.C = s.C; g.O = s.O;
+    const long long HW = (long long)s.H * s.W;
+    g.V = (long long)s.D * HW;
+    for (int d = 0; d < kDirs; ++d) {
+        DirGeom &r = g.dir[d];
+        r.sign = (d % 2 == 0) ? 1 : -1;
+        switch (d / 2) {
+        case 0: r.T = s.D; r.P = s.H; r.Q = s.W; r.ss = HW; r.sp = s.W; r.sq = 1; break;
+        case 1: r.T = s.H; r.P = s.D; r.Q = s.W; r.ss = s.W; r.sp = HW; r.sq = 1; break;
+        default: r.T = s.W; r.P = s.D; r.Q = s.H; r.ss = 1; r.sp = HW; r.sq = s.W; break;
+        }
+    }
+    return g;
+}
+
+// bf16 <-> fp32 (round to nearest even; NaN kept quiet).
+__host__ __device__ inline float bf16_to_f32(uint16_t v) {
+    union { uint32_t u; float f; } c;
+    c.u = (uint32_t)v << 16;
+    return c.f;
+}
+__host__ __device__ inline uint16_t f32_to_bf16(float f) {
+    union { uint32_t u; float f; } c;
+    c.f = f;
+    if ((c.u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((c.u >> 16) | 0x40);
+    const uint32_t lsb = (c.u >> 16) & 1u;
+    return (uint16_t)((c.u + 0x7fffu + lsb) >> 16);
+}
+
+template <typename T> struct Store;
+template <> struct Store<float> {
+    __device__ static float load(const float *p, long long i) { return p[i]; }
+    __device__ static void store(float *p, long long i, float v) { p[i] = v; }
+};
+template <> struct Store<uint16_t> {
+    __device__ static float load(const uint16_t *p, long long i) { return bf16_to_f32(p[i]); }
+    __device__ static void store(uint16_t *p, long long i, float v) { p[i] = f32_to_bf16(v); }
+};
+
+__device__ inline float sigmoidf_(float a) { return 1.0f / (1.0f + __expf(-a)); }
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Bump allocator over a caller-provided workspace.
+struct Carve {
+    char *base;
+    size_t off = 0;
+    explicit Carve(void *p) : base((char *)p) {}
+    template <typename T> T *take(size_t count) {
+        off = align_up(off, 256);
+        T *p = base ? (T *)(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+};
+
+#define PLSTM_LAUNCH_CHECK()                                   \
+    do {                                                       \
+        if (hipGetLastError() != hipSuccess) return PLSTM_EHIP; \
+    } while (0)
+
+// ---- launchers implemented in the .hip translation units -------------------
+
+// Generic path (any supported shape): one launch per plane step.
+int generic_forward(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
+                    const void *b, void *h, float *gates, float *cell, void *ws,
+                    hipStream_t st);
+size_t generic_forward_ws(const Geom &g, bool training);
+int generic_backward(const Geom &g, const float *x, const float *wx, const float *wh,
+                     const float *gates, const float *cell, const float *dh, float *dx,
+                     float *dwx, float *dwh, float *db, void *ws, hipStream_t st);
+size_t generic_backward_ws(const Geom &g);
+
+// Saved-activation layout shared by every forward/backward pair:
+//   gates [6][N][V][4O] fp32 (i, f, g, o after the nonlinearity), then
+//   cell  [6][N][V][O]  fp32.
+inline size_t saved_gates_count(const Geom &g) { return (size_t)kDirs * g.N * g.V * 4 * g.O; }
+inline size_t saved_cell_count(const Geom &g) { return (size_t)kDirs * g.N * g.V * g.O; }
+
+// Fully connected glue.
+int fc_tanh_forward(long long M, int Cin, int Cout, int dtype, const void *x, const void *w,
+                    const void *b, void *y, hipStream_t st);
+int fc_tanh_backward(long long M, int Cin, int Cout, const float *x, const float *w,
+                     const float *y, const float *dy, float *dx, float *dw, float *db,
+                     void *ws, hipStream_t st);
+size_t fc_ws(long long M, int Cin, int Cout);
+int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void *w,
+               const void *b, const int32_t *labels, float *p, float *loss, float *dx,
+               float *dw, float *db, void *ws, hipStream_t st);
+
+}  // namespace plstm

@@ -1,0 +1,418 @@
+// Generic PyraMiD-LSTM path: any supported shape, one launch per plane step.
+//
+// Forward (Section 2.3, Eq. (7)-(13)): for step t, every direction d with
+// t < T_d updates all pixels of its plane t at once.  One thread owns one
+// (direction, batch element, pixel, hidden unit) and produces the four gate
+// pre-activations of that unit by direct 3x3 loops over the input plane and
+// the previous plane's h^d; the cell state lives in a per-direction volume.
+// The six per-direction outputs are summed in the fixed order d = 0..5.
+//
+// Backward (the chain rule through Eq. (7)-(13), reverse plane order): for
+// step t every thread owns one (d, n, pixel, unit j): it collects dL/dh^d from
+// the upstream gradient and from the next plane's gate gradients (a transposed
+// 3x3 convolution with wh), forms dL/dc and the four gate gradients of unit j.
+// Parameter gradients are then block-tiled reductions over all voxels
+// (deterministic two-stage sums), and dL/dx a transposed 3x3 convolution with
+// wx summed over the six directions.
+#include "common.h"
+#include "timing.h"
+
+namespace plstm {
+namespace {
+
+constexpr int kThreads = 256;
+
+template <typename TS>
+__global__ void __launch_bounds__(kThreads)
+k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
+           const TS *__restrict__ wh, const TS *__restrict__ b, float *__restrict__ hd,
+           float *__restrict__ cellbuf, float *__restrict__ gates)
+{
+    const int d = blockIdx.z / g.N, n = blockIdx.z % g.N, o = blockIdx.y;
+    const DirGeom dg = g.dir[d];
+    if (t >= dg.T) return;
+    const int px = blockIdx.x * kThreads + threadIdx.x;
+    if (px >= dg.P * dg.Q) return;
+    const int p = px / dg.Q, q = px % dg.Q;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int sprev = s - dg.sign;
+    const int C = g.C, O = g.O, G = 4 * O;
+    const long long nbase = (long long)n * g.V;
+    const long long dbase = (long long)d * g.N * g.V;
+
+    float acc[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc[k] = Store<TS>::load(b, (long long)d * G + k * O + o);
+
+    for (int ka = 0; ka < 3; ++ka) {
+        const int pp = p + ka - 1;
+        if (pp < 0 || pp >= dg.P) continue;
+        for (int kb = 0; kb < 3; ++kb) {
+            const int qq = q + kb - 1;
+            if (qq < 0 || qq >= dg.Q) continue;
+            const long long vin = nbase + s * dg.ss + pp * dg.sp + qq * dg.sq;
+            for (int c = 0; c < C; ++c) {
+                const float xv = Store<TS>::load(x, vin * C + c);
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    acc[k] += xv * Store<TS>::load(
+                        wx, (((long long)d * G + k * O + o) * C + c) * 9 + ka * 3 + kb);
+            }
+            if (t > 0) {
+                const long long vh = dbase + nbase + sprev * dg.ss + pp * dg.sp + qq * dg.sq;
+                for (int j = 0; j < O; ++j) {
+                    const float hv = hd[vh * O + j];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        acc[k] += hv * Store<TS>::load(
+                            wh, (((long long)d * G + k * O + o) * O + j) * 9 + ka * 3 + kb);
+                }
+            }
+        }
+    }
+    const float gi = sigmoidf_(acc[0]);
+    const float gf = sigmoidf_(acc[1]);
+    const float gg = tanhf(acc[2]);
+    const float go = sigmoidf_(acc[3]);
+    const long long v = dbase + nbase + s * dg.ss + p * dg.sp + q * dg.sq;
+    float c = gg * gi;
+    if (t > 0) c += cellbuf[(dbase + nbase + sprev * dg.ss + p * dg.sp + q * dg.sq) * O + o] * gf;
+    cellbuf[v * O + o] = c;
+    hd[v * O + o] = go * tanhf(c);
+    if (gates) {
+        gates[v * G + 0 * O + o] = gi;
+        gates[v * G + 1 * O + o] = gf;
+        gates[v * G + 2 * O + o] = gg;
+        gates[v * G + 3 * O + o] = go;
+    }
+}
+
+// h = sum_d h^d in the fixed order d = 0..5 (Eq. (13)).
+template <typename TS>
+__global__ void __launch_bounds__(kThreads)
+k_sum_dirs(long long count, const float *__restrict__ hd, TS *__restrict__ h)
+{
+    const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= count) return;
+    float acc = hd[i];
+#pragma unroll
+    for (int d = 1; d < kDirs; ++d) acc += hd[(long long)d * count + i];
+    Store<TS>::store(h, i, acc);
+}
+
+__global__ void __launch_bounds__(kThreads)
+k_bwd_step(Geom g, int t, const float *__restrict__ wh, const float *__restrict__ gates,
+           const float *__restrict__ cell, const float *__restrict__ dh,
+           float *__restrict__ dA, float *__restrict__ gc)
+{
+    const int d = blockIdx.z / g.N, n = blockIdx.z % g.N, j = blockIdx.y;
+    const DirGeom dg = g.dir[d];
+    if (t >= dg.T) return;
+    const int px = blockIdx.x * kThreads + threadIdx.x;
+    if (px >= dg.P * dg.Q) return;
+    const int p = px / dg.Q, q = px % dg.Q;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int snext = s + dg.sign, sprev = s - dg.sign;
+    const int O = g.O, G = 4 * O;
+    const long long nbase = (long long)n * g.V;
+    const long long dbase = (long long)d * g.N * g.V;
+    const long long vloc = nbase + s * dg.ss + p * dg.sp + q * dg.sq;
+    const long long v = dbase + vloc;
+    const bool has_next = t + 1 < dg.T;
+
+    float gh = dh[vloc * O + j];
+    if (has_next) {
+        // h_t[p][q][j] entered A_{t+1}[p - (ka-1)][q - (kb-1)] through tap (ka, kb).
+        for (int ka = 0; ka < 3; ++ka) {
+            const int pp = p - (ka - 1);
+            if (pp < 0 || pp >= dg.P) continue;
+            for (int kb = 0; kb < 3; ++kb) {
+                const int qq = q - (kb - 1);
+                if (qq < 0 || qq >= dg.Q) continue;
+                const long long vn = dbase + nbase + snext * dg.ss + pp * dg.sp + qq * dg.sq;
+                for (int gn = 0; gn < G; ++gn)
+                    gh += dA[vn * G + gn] * wh[(((long long)d * G + gn) * O + j) * 9 + ka * 3 + kb];
+            }
+        }
+    }
+    const float gi = gates[v * G + 0 * O + j];
+    const float gf = gates[v * G + 1 * O + j];
+    const float gg = gates[v * G + 2 * O + j];
+    const float go = gates[v * G + 3 * O + j];
+    const float c = cell[v * O + j];
+    const float tc = tanhf(c);
+    float gcv = gh * go * (1.0f - tc * tc);
+    if (has_next) {
+        const long long vn = dbase + nbase + snext * dg.ss + p * dg.sp + q * dg.sq;
+        gcv += gc[vn * O + j] * gates[vn * G + 1 * O + j];
+    }
+    gc[v * O + j] = gcv;
+    const float cprev =
+        t > 0 ? cell[(dbase + nbase + sprev * dg.ss + p * dg.sp + q * dg.sq) * O + j] : 0.0f;
+    dA[v * G + 0 * O + j] = gcv * gg * gi * (1.0f - gi);
+    dA[v * G + 1 * O + j] = gcv * cprev * gf * (1.0f - gf);
+    dA[v * G + 2 * O + j] = gcv * gi * (1.0f - gg * gg);
+    dA[v * G + 3 * O + j] = gh * tc * go * (1.0f - go);
+}
+
+// Parameter-gradient partial sums.  For direction d the reduction runs over
+// every voxel (n, t, p, q); column k of the "im2col" row is
+//   k < 9C        : x at tap (ka, kb) = divmod(k / C, 3), channel k % C
+//   9C <= k < 9(C+O): h^d_{t-1} at tap, unit, recomputed as o * tanh(c) of the
+//                   previous plane (0 for t = 0 or outside the plane)
+//   k = 9(C+O)    : 1 (bias)
+// Each block owns a 16 x 16 (gate-unit x column) tile and one chunk of voxels;
+// partial[d][chunk][gn][k].
+constexpr int kTile = 16;
+constexpr int kVB = 64;   // voxels staged per LDS batch
+
+__global__ void __launch_bounds__(kThreads)
+k_wgrad_partial(Geom g, long long chunk_len, int nchunk, const float *__restrict__ x,
+                const float *__restrict__ gates, const float *__restrict__ cell,
+                const float *__restrict__ dA, float *__restrict__ partial)
+{
+    const int C = g.C, O = g.O, G = 4 * O;
+    const int KT = 9 * (C + O) + 1;
+    const int d = blockIdx.z / nchunk, chunk = blockIdx.z % nchunk;
+    const int k0 = blockIdx.x * kTile, g0 = blockIdx.y * kTile;
+    const DirGeom dg = g.dir[d];
+    const long long PQ = (long long)dg.P * dg.Q;
+    const long long total = (long long)g.N * g.V;   // voxels in sweep order (n, t, p, q)
+    const long long v0 = (long long)chunk * chunk_len;
+    const long long v1 = v0 + chunk_len < total ? v0 + chunk_len : total;
+    const long long dbase = (long long)d * g.N * g.V;
+
+    __shared__ float sA[kVB][kTile + 1];
+    __shared__ float sIn[kVB][kTile + 1];
+    const int tg = threadIdx.x / kTile, tk = threadIdx.x % kTile;
+    float acc = 0.0f;
+    for (long long vb = v0; vb < v1; vb += kVB) {
+        for (int e = threadIdx.x; e < kVB * kTile; e += kThreads) {
+            const int vi = e / kTile, col = e % kTile;
+            const long long lin = vb + vi;
+            float a = 0.0f, in = 0.0f;
+            if (lin < v1) {
+                const int n = (int)(lin / g.V);
+                const long long rem = lin % g.V;
+                const int t = (int)(rem / PQ);
+                const int pix = (int)(rem % PQ);
+                const int p = pix / dg.Q, q = pix % dg.Q;
+                const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+                const long long nbase = (long long)n * g.V;
+                const long long v = nbase + s * dg.ss + p * dg.sp + q * dg.sq;
+                if (g0 + col < G) a = dA[(dbase + v) * G + g0 + col];
+                const int k = k0 + col;
+                if (k < 9 * C) {
+                    const int tap = k / C, c = k % C;
+                    const int pp = p + tap / 3 - 1, qq = q + tap % 3 - 1;
+                    if (pp >= 0 && pp < dg.P && qq >= 0 && qq < dg.Q)
+                        in = x[(nbase + s * dg.ss + pp * dg.sp + qq * dg.sq) * C + c];
+                } else if (k < 9 * (C + O)) {
+                    const int kk = k - 9 * C;
+                    const int tap = kk / O, j = kk % O;
+                    const int pp = p + tap / 3 - 1, qq = q + tap % 3 - 1;
+                    if (t > 0 && pp >= 0 && pp < dg.P && qq >= 0 && qq < dg.Q) {
+                        const long long vp =
+                            dbase + nbase + (s - dg.sign) * dg.ss + pp * dg.sp + qq * dg.sq;
+                        in = gates[vp * G + 3 * O + j] * tanhf(cell[vp * O + j]);
+                    }
+                } else if (k == KT - 1) {
+                    in = 1.0f;
+                }
+            }
+            sA[vi][col] = a;
+            sIn[vi][col] = in;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int vi = 0; vi < kVB; ++vi) acc += sA[vi][tg] * sIn[vi][tk];
+        __syncthreads();
+    }
+    const int gn = g0 + tg, k = k0 + tk;
+    if (gn < G && k < KT)
+        partial[(((long long)d * nchunk + chunk) * G + gn) * KT + k] = acc;
+}
+
+__global__ void __launch_bounds__(kThreads)
+k_wgrad_reduce(Geom g, int nchunk, const float *__restrict__ partial, float *__restrict__ dwx,
+               float *__restrict__ dwh, float *__restrict__ db)
+{
+    const int C = g.C, O = g.O, G = 4 * O;
+    const int KT = 9 * (C + O) + 1;
+    const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= (long long)kDirs * G * KT) return;
+    const int k = (int)(i % KT);
+    const int gn = (int)((i / KT) % G);
+    const int d = (int)(i / ((long long)KT * G));
+    float acc = 0.0f;
+    for (int ch = 0; ch < nchunk; ++ch)
+        acc += partial[(((long long)d * nchunk + ch) * G + gn) * KT + k];
+    if (k < 9 * C) {
+        const int tap = k / C, c = k % C;
+        dwx[(((long long)d * G + gn) * C + c) * 9 + tap] = acc;
+    } else if (k < 9 * (C + O)) {
+        const int kk = k - 9 * C;
+        const int tap = kk / O, j = kk % O;
+        dwh[(((long long)d * G + gn) * O + j) * 9 + tap] = acc;
+    } else {
+        db[(long long)d * G + gn] = acc;
+    }
+}
+
+// dL/dx[v][c] = sum_d sum_taps sum_gn dA^d[pixel - (tap - 1)][gn] * wx[d][gn][c][tap].
+__global__ void __launch_bounds__(kThreads)
+k_dx(Geom g, const float *__restrict__ wx, const float *__restrict__ dA, float *__restrict__ dx)
+{
+    const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
+    const int C = g.C, O = g.O, G = 4 * O;
+    if (i >= (long long)g.N * g.V * C) return;
+    const int c = (int)(i % C);
+    const long long vloc = i / C;
+    const int n = (int)(vloc / g.V);
+    const long long r = vloc % g.V;
+    const int z = (int)(r / ((long long)g.H * g.W));
+    const int y = (int)((r / g.W) % g.H);
+    const int xw = (int)(r % g.W);
+    const long long nbase = (long long)n * g.V;
+    float acc = 0.0f;
+    for (int d = 0; d < kDirs; ++d) {
+        const DirGeom dg = g.dir[d];
+        int s, p, q;
+        switch (d / 2) {
+        case 0: s = z; p = y; q = xw; break;
+        case 1: s = y; p = z; q = xw; break;
+        default: s = xw; p = z; q = y; break;
+        }
+        const long long dbase = (long long)d * g.N * g.V;
+        for (int ka = 0; ka < 3; ++ka) {
+            const int pp = p - (ka - 1);
+            if (pp < 0 || pp >= dg.P) continue;
+            for (int kb = 0; kb < 3; ++kb) {
+                const int qq = q - (kb - 1);
+                if (qq < 0 || qq >= dg.Q) continue;
+                const long long v = dbase + nbase + s * dg.ss + pp * dg.sp + qq * dg.sq;
+                const float *a = dA + v * G;
+                const float *w = wx + ((long long)d * G * C + c) * 9 + ka * 3 + kb;
+                for (int gn = 0; gn < G; ++gn) acc += a[gn] * w[(long long)gn * C * 9];
+            }
+        }
+    }
+    dx[i] = acc;
+}
+
+inline int max_plane(const Geom &g) {
+    int m = 0;
+    for (int d = 0; d < kDirs; ++d) m = g.dir[d].P * g.dir[d].Q > m ? g.dir[d].P * g.dir[d].Q : m;
+    return m;
+}
+inline int max_T(const Geom &g) {
+    int m = 0;
+    for (int d = 0; d < kDirs; ++d) m = g.dir[d].T > m ? g.dir[d].T : m;
+    return m;
+}
+
+// Voxels per reduction chunk: at least 8192, and at most 4096 chunks so that
+// the grid's z extent (6 x chunks) stays within HIP's limit.
+inline long long wgrad_chunk_len(const Geom &g) {
+    const long long nv = (long long)g.N * g.V;
+    long long len = 8192;
+    if ((nv + len - 1) / len > 4096) len = (nv + 4095) / 4096;
+    return len;
+}
+inline int wgrad_chunks(const Geom &g) {
+    const long long len = wgrad_chunk_len(g);
+    return (int)(((long long)g.N * g.V + len - 1) / len);
+}
+
+}  // namespace
+
+size_t generic_forward_ws(const Geom &g, bool training)
+{
+    Carve cv(nullptr);
+    cv.take<float>((size_t)kDirs * g.N * g.V * g.O);                  // h^d
+    if (!training) cv.take<float>((size_t)kDirs * g.N * g.V * g.O);   // c^d
+    return cv.off;
+}
+
+int generic_forward(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
+                    const void *b, void *h, float *gates, float *cell, void *ws,
+                    hipStream_t st)
+{
+    Carve cv(ws);
+    float *hd = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
+    float *cellbuf = cell ? cell : cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
+    const dim3 grid((max_plane(g) + kThreads - 1) / kThreads, g.O, kDirs * g.N);
+    const int T = max_T(g);
+    timing_begin("sweep_fwd_generic", st);
+    for (int t = 0; t < T; ++t) {
+        if (dtype == PLSTM_BF16)
+            k_fwd_step<uint16_t><<<grid, kThreads, 0, st>>>(
+                g, t, (const uint16_t *)x, (const uint16_t *)wx, (const uint16_t *)wh,
+                (const uint16_t *)b, hd, cellbuf, gates);
+        else
+            k_fwd_step<float><<<grid, kThreads, 0, st>>>(
+                g, t, (const float *)x, (const float *)wx, (const float *)wh,
+                (const float *)b, hd, cellbuf, gates);
+        PLSTM_LAUNCH_CHECK();
+    }
+    timing_end(T, st);
+    const long long count = (long long)g.N * g.V * g.O;
+    const unsigned blocks = (unsigned)((count + kThreads - 1) / kThreads);
+    timing_begin("sum_dirs", st);
+    if (dtype == PLSTM_BF16)
+        k_sum_dirs<uint16_t><<<blocks, kThreads, 0, st>>>(count, hd, (uint16_t *)h);
+    else
+        k_sum_dirs<float><<<blocks, kThreads, 0, st>>>(count, hd, (float *)h);
+    PLSTM_LAUNCH_CHECK();
+    timing_end(1, st);
+    return PLSTM_OK;
+}
+
+size_t generic_backward_ws(const Geom &g)
+{
+    Carve cv(nullptr);
+    const int G = 4 * g.O, KT = 9 * (g.C + g.O) + 1;
+    cv.take<float>((size_t)kDirs * g.N * g.V * G);                      // dA
+    cv.take<float>((size_t)kDirs * g.N * g.V * g.O);                    // dL/dc
+    cv.take<float>((size_t)kDirs * wgrad_chunks(g) * G * KT);           // partials
+    return cv.off;
+}
+
+int generic_backward(const Geom &g, const float *x, const float *wx, const float *wh,
+                     const float *gates, const float *cell, const float *dh, float *dx,
+                     float *dwx, float *dwh, float *db, void *ws, hipStream_t st)
+{
+    const int G = 4 * g.O, KT = 9 * (g.C + g.O) + 1;
+    Carve cv(ws);
+    float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * G);
+    float *gc = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
+    const int nchunk = wgrad_chunks(g);
+    float *partial = cv.take<float>((size_t)kDirs * nchunk * G * KT);
+
+    const dim3 grid((max_plane(g) + kThreads - 1) / kThreads, g.O, kDirs * g.N);
+    timing_begin("sweep_bwd_generic", st);
+    for (int t = max_T(g) - 1; t >= 0; --t) {
+        k_bwd_step<<<grid, kThreads, 0, st>>>(g, t, wh, gates, cell, dh, dA, gc);
+        PLSTM_LAUNCH_CHECK();
+    }
+    timing_end(max_T(g), st);
+    timing_begin("wgrad_generic", st);
+    const dim3 wg_grid((KT + kTile - 1) / kTile, (G + kTile - 1) / kTile, kDirs * nchunk);
+    k_wgrad_partial<<<wg_grid, kThreads, 0, st>>>(g, wgrad_chunk_len(g), nchunk, x, gates, cell, dA, partial);
+    PLSTM_LAUNCH_CHECK();
+    const long long nout = (long long)kDirs * G * KT;
+    k_wgrad_reduce<<<(unsigned)((nout + kThreads - 1) / kThreads), kThreads, 0, st>>>(
+        g, nchunk, partial, dwx, dwh, db);
+    PLSTM_LAUNCH_CHECK();
+    timing_end(2, st);
+    if (dx) {
+        const long long cnt = (long long)g.N * g.V * g.C;
+        timing_begin("dx_generic", st);
+        k_dx<<<(unsigned)((cnt + kThreads - 1) / kThreads), kThreads, 0, st>>>(g, wx, dA, dx);
+        PLSTM_LAUNCH_CHECK();
+        timing_end(1, st);
+    }
+    return PLSTM_OK;
+}
+
+}  // namespace plstm

@@ -1,0 +1,123 @@
+"""Stacked PyraMiD-LSTM networks on the GPU, composed from the C entry points.
+
+Fig. 3 / Section 2.3: PyraMiD-LSTM layer -> per-voxel FC + tanh, repeated;
+the last FC layer feeds a per-voxel softmax.  This module only allocates
+tensors with torch and calls the library (every arithmetic step runs in the
+HIP kernels); gradients flow through the same entry points in reverse.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import List, Optional, Tuple
+
+import torch
+
+from . import (plstm_shape, pyramid_fc_tanh_backward, pyramid_fc_tanh_forward,
+               pyramid_lstm_backward, pyramid_lstm_forward, pyramid_lstm_saved_size,
+               pyramid_lstm_workspace_size, pyramid_softmax_ce, shape_for)
+
+
+@dataclass
+class LayerW:
+    wx: torch.Tensor      # [6][4O][C][3][3]
+    wh: torch.Tensor      # [6][4O][O][3][3]
+    b: torch.Tensor       # [6][4O]
+
+    @property
+    def O(self):
+        return self.wh.shape[2]
+
+
+def layer_forward(x: torch.Tensor, L: LayerW, training: bool = False, ws=None, stream=None):
+    """One layer; returns (h, saved or None)."""
+    s = shape_for(x, L.O)
+    h = torch.empty(x.shape[:-1] + (L.O,), dtype=x.dtype, device=x.device)
+    saved = None
+    if training:
+        saved = torch.empty(pyramid_lstm_saved_size(s), dtype=torch.uint8, device=x.device)
+    pyramid_lstm_forward(s, x, L.wx, L.wh, L.b, h, saved, ws, stream)
+    return h, saved
+
+
+def layer_backward(x, L: LayerW, saved, dh, want_dx=True, ws=None, stream=None):
+    s = shape_for(x, L.O)
+    dx = torch.empty_like(x) if want_dx else None
+    dwx, dwh, db = (torch.empty_like(t, dtype=torch.float32) for t in (L.wx, L.wh, L.b))
+    pyramid_lstm_backward(s, x, L.wx, L.wh, L.b, saved, dh, dx, dwx, dwh, db, ws, stream)
+    return dx, dwx, dwh, db
+
+
+def workspace_for(x_shape, hidden: List[int], fc: bool, dtype, training: bool, device):
+    """One workspace big enough for every layer of a network."""
+    need = 256
+    C = x_shape[-1]
+    for O in hidden:
+        s = plstm_shape(*x_shape[:-1], C, O, 0 if dtype == torch.float32 else 1)
+        need = max(need, pyramid_lstm_workspace_size(s, int(training)))
+        C = 2 * O if fc else O
+    return torch.empty(need, dtype=torch.uint8, device=device)
+
+
+def network_forward(x, layers: List[LayerW], fcs: List[Tuple[torch.Tensor, torch.Tensor]],
+                    head: Tuple[torch.Tensor, torch.Tensor], labels: Optional[torch.Tensor] = None,
+                    training: bool = False, ws=None, stream=None):
+    """Returns dict: 'p' [M][K] fp32, 'loss' (device scalar, with labels),
+    'acts' (per-layer inputs/outputs and saved activations for training)."""
+    N, D, H, W, _ = x.shape
+    M = N * D * H * W
+    a = x
+    acts = []
+    for L, (wf, bf) in zip(layers, fcs):
+        h, saved = layer_forward(a, L, training, ws, stream)
+        y = torch.empty((N, D, H, W, wf.shape[0]), dtype=a.dtype, device=a.device)
+        pyramid_fc_tanh_forward(h.view(M, -1), wf, bf, y.view(M, -1), stream)
+        acts.append({"in": a, "h": h, "y": y, "saved": saved})
+        a = y
+    K = head[0].shape[0]
+    p = torch.empty((M, K), dtype=torch.float32, device=x.device)
+    out = {"p": p, "acts": acts}
+    if labels is None:
+        pyramid_softmax_ce(a.view(M, -1), head[0], head[1], p, stream=stream)
+        return out
+    loss = torch.empty(1, dtype=torch.float32, device=x.device)
+    out["loss"] = loss
+    if training:
+        dlast = torch.empty((M, a.shape[-1]), dtype=torch.float32, device=x.device)
+        dw = torch.empty_like(head[0])
+        db = torch.empty_like(head[1])
+        pyramid_softmax_ce(a.view(M, -1), head[0], head[1], p, labels, loss, dlast, dw, db,
+                           stream=stream)
+        out.update({"dlast": dlast, "head_grad": (dw, db)})
+    else:
+        pyramid_softmax_ce(a.view(M, -1), head[0], head[1], p, labels, loss, stream=stream)
+    return out
+
+
+def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None):
+    """Forward + back-propagation through the whole network (fp32).
+    Returns dict with 'loss', 'p', 'head' (dw, db), 'fcs' [(dw, db)],
+    'layers' [(dwx, dwh, db)]."""
+    out = network_forward(x, layers, fcs, head, labels, training=True, ws=ws, stream=stream)
+    acts = out["acts"]
+    g = out["dlast"]
+    N, D, H, W, _ = x.shape
+    M = N * D * H * W
+    fc_grads = [None] * len(fcs)
+    layer_grads = [None] * len(layers)
+    for li in range(len(layers) - 1, -1, -1):
+        wf, _ = fcs[li]
+        act = acts[li]
+        O = act["h"].shape[-1]
+        dh = torch.empty((M, O), dtype=torch.float32, device=x.device)
+        dwf, dbf = torch.empty_like(wf), torch.empty(wf.shape[0], device=x.device)
+        pyramid_fc_tanh_backward(act["h"].view(M, O), wf, act["y"].view(M, -1), g.view(M, -1),
+                                 dh, dwf, dbf, stream=stream)
+        fc_grads[li] = (dwf, dbf)
+        dx, dwx, dwh, db = layer_backward(act["in"], layers[li], act["saved"],
+                                          dh.view(act["h"].shape), want_dx=li > 0, ws=ws,
+                                          stream=stream)
+        layer_grads[li] = (dwx, dwh, db)
+        if li > 0:
+            g = dx
+    return {"loss": out["loss"], "p": out["p"], "head": out["head_grad"], "fcs": fc_grads,
+            "layers": layer_grads}

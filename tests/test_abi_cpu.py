@@ -1,0 +1,136 @@
+"""C-ABI checks that need no GPU: symbols, sizes, argument validation.
+
+Every call here is rejected by validation before the library touches HIP, so
+the fake (aligned, never dereferenced) pointers are never used.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1506_07452_amd as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pyramid_lstm.h")
+FAKE = ctypes.c_void_p(0x10000)      # aligned, never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pyramid_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return P.load()
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("pyramid_lstm_forward", "pyramid_lstm_backward", "pyramid_lstm_workspace_size",
+              "pyramid_lstm_saved_size", "pyramid_lstm_status_string", "pyramid_fc_tanh_forward",
+              "pyramid_fc_tanh_backward", "pyramid_softmax_ce", "pyramid_fc_workspace_size"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert hasattr(P, name), "binding lacks " + name
+
+
+def shape(**kw):
+    d = dict(N=1, D=8, H=8, W=8, C=1, O=4, dtype=P.PLSTM_F32)
+    d.update(kw)
+    return P.plstm_shape(**d)
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert P.pyramid_lstm_status_string(code) not in ("", "unknown status")
+    assert P.pyramid_lstm_status_string(-99) == "unknown status"
+
+
+def test_sizes(lib):
+    s = shape()
+    V = 8 * 8 * 8
+    assert P.pyramid_lstm_saved_size(s) >= 6 * V * 5 * 4 * 4
+    assert P.pyramid_lstm_workspace_size(s, 0) > 0
+    assert P.pyramid_lstm_workspace_size(s, 1) >= P.pyramid_lstm_workspace_size(s, 0)
+    for bad in (dict(O=5), dict(O=0), dict(C=0), dict(D=0), dict(dtype=7), dict(C=5000),
+                dict(N=20000)):
+        assert P.pyramid_lstm_workspace_size(shape(**bad), 0) == 0, bad
+        assert P.pyramid_lstm_saved_size(shape(**bad)) == 0, bad
+    assert lib.pyramid_lstm_workspace_size(None, 0) == 0
+
+
+def fwd(lib, s, x=FAKE, wx=FAKE, wh=FAKE, b=FAKE, h=FAKE, saved=None, ws=FAKE, nbytes=None):
+    if nbytes is None:
+        nbytes = 0
+    return lib.pyramid_lstm_forward(ctypes.byref(s) if s is not None else None, x, wx, wh, b, h,
+                                    saved, ws, nbytes, None)
+
+
+def test_forward_validation(lib):
+    s = shape()
+    assert fwd(lib, None) == -1
+    assert fwd(lib, s, x=None) == -1
+    assert fwd(lib, s, h=None) == -1
+    assert fwd(lib, s, ws=None) == -1
+    assert fwd(lib, s, wx=ctypes.c_void_p(0x10004)) == -1            # misaligned
+    assert fwd(lib, shape(O=5)) == -2
+    assert fwd(lib, shape(D=-1)) == -1
+    assert fwd(lib, s, nbytes=0) == -3                                # workspace too small
+    need = P.pyramid_lstm_workspace_size(s, 1)
+    assert fwd(lib, s, saved=FAKE, nbytes=need - 1) == -3
+    assert fwd(lib, shape(dtype=P.PLSTM_BF16), saved=FAKE, nbytes=1 << 40) == -2
+
+
+def test_backward_validation(lib):
+    s = shape()
+    args = [FAKE] * 11
+    def call(sh=s, nbytes=0, **over):
+        a = list(args)
+        names = ["x", "wx", "wh", "b", "saved", "dh", "dx", "dwx", "dwh", "db", "ws"]
+        for k, v in over.items():
+            a[names.index(k)] = v
+        return lib.pyramid_lstm_backward(ctypes.byref(sh), *a, nbytes, None)
+    assert call(saved=None) == -1
+    assert call(dh=None) == -1
+    assert call(dwh=None) == -1
+    assert call(ws=None) == -1
+    assert call(dh=ctypes.c_void_p(0x10002)) == -1
+    assert call(shape(dtype=P.PLSTM_BF16), nbytes=1 << 40) == -2
+    assert call(nbytes=16) == -3
+
+
+def test_fc_validation(lib):
+    assert lib.pyramid_fc_tanh_forward(0, 4, 4, 0, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert lib.pyramid_fc_tanh_forward(10, 4, 4, 3, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert lib.pyramid_fc_tanh_forward(10, 4, 4, 0, FAKE, None, FAKE, FAKE, None) == -1
+    assert lib.pyramid_fc_tanh_forward(10, 4, 4000, 0, FAKE, FAKE, FAKE, FAKE, None) == -2
+    assert lib.pyramid_fc_tanh_backward(10, 4, 4, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                                        FAKE, 0, None) == -3
+    assert lib.pyramid_fc_workspace_size(0, 4, 4) == 0
+    assert lib.pyramid_fc_workspace_size(100, 4, 4) > 0
+    # softmax: K too large, missing loss with labels, gradient without labels
+    assert lib.pyramid_softmax_ce(10, 4, 17, 0, FAKE, FAKE, FAKE, None, FAKE, None, None, None,
+                                  None, None, 0, None) == -2
+    assert lib.pyramid_softmax_ce(10, 4, 4, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None,
+                                  None, FAKE, 1 << 30, None) == -1
+    assert lib.pyramid_softmax_ce(10, 4, 4, 0, FAKE, FAKE, FAKE, None, FAKE, None, None, FAKE,
+                                  FAKE, None, 0, None) == -1
+    assert lib.pyramid_softmax_ce(10, 4, 4, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None,
+                                  None, FAKE, 8, None) == -3
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    x = torch.zeros(1, 2, 2, 2, 1)
+    with pytest.raises((ValueError, RuntimeError)):
+        P.pyramid_fc_tanh_forward(x.view(-1, 1), torch.zeros(1, 1), torch.zeros(1),
+                                  torch.zeros(8, 1))

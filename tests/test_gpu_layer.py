@@ -1,0 +1,192 @@
+"""GPU parity of one PyraMiD-LSTM layer (forward and backward) against the
+fp64 oracle, plus invariants that hold at any size, through the C ABI."""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from paper_1506_07452_amd.network import LayerW, layer_backward, layer_forward
+from tests.gpu_util import DEV, TOL, dev, host, layer_dev, normwise, say
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+# (N, D, H, W, C, O): tiny, ragged (planes not multiples of any tile), several
+# tiles per plane, degenerate extents, every supported O.
+SHAPES = [
+    (1, 8, 8, 8, 1, 4),
+    (1, 5, 37, 29, 3, 16),
+    (2, 7, 9, 11, 2, 8),
+    (1, 3, 3, 3, 1, 32),
+    (1, 4, 6, 70, 3, 64),
+    (1, 1, 1, 1, 1, 4),
+    (1, 1, 13, 1, 2, 16),
+    (1, 12, 64, 50, 3, 16),
+    (2, 9, 17, 40, 32, 32),
+]
+
+
+def instance(shape, seed, dtype="f32"):
+    N, D, H, W, C, O = shape
+    wl = synth.Workload("t", N, D, H, W, C, [O], dtype=dtype, seed=seed)
+    return synth.make(wl)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_forward_matches_oracle(shape):
+    inst = instance(shape, 1000 + sum(shape))
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    say("forward", shape)
+    h, _ = layer_forward(dev(inst.x), layer_dev(L))
+    torch.cuda.synchronize()
+    err = normwise(host(h), ref)
+    assert err <= TOL["f32"], err
+
+
+@pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[1], SHAPES[2], SHAPES[4], SHAPES[8]],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_forward_bf16_matches_oracle(shape):
+    inst = instance(shape, 2000 + sum(shape), "bf16")
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    say("forward bf16", shape)
+    h, _ = layer_forward(dev(inst.x, "bf16"), layer_dev(L, "bf16"))
+    torch.cuda.synchronize()
+    assert h.dtype == torch.bfloat16
+    err = normwise(host(h), ref)
+    assert err <= TOL["bf16"], err
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_training_forward_and_backward_match_oracle(shape):
+    inst = instance(shape, 3000 + sum(shape))
+    L = inst.layers[0]
+    dh = synth.upstream_grad(inst.x.shape[:-1] + (shape[-1],), 7 + sum(shape))
+    ref_h = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    ref = oracle.backward(inst.x, L.wx, L.wh, L.b, dh)
+    say("backward", shape)
+    x, Ld = dev(inst.x), layer_dev(L)
+    h, saved = layer_forward(x, Ld, training=True)
+    dx, dwx, dwh, db = layer_backward(x, Ld, saved, dev(dh))
+    torch.cuda.synchronize()
+    assert normwise(host(h), ref_h) <= TOL["f32"]
+    for name, got in (("dx", dx), ("dwx", dwx), ("dwh", dwh), ("db", db)):
+        err = normwise(host(got), ref[name])
+        assert err <= TOL["f32"], (name, err)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_config_forward(cfg):
+    """Configs 1-3 at full size.  Config 1 against the oracle directly; 2 and 3
+    against the oracle's stored results (sampled entries, per-slice sums)."""
+    inst = synth.config(cfg)
+    L = inst.layers[0]
+    say("config", cfg)
+    h, _ = layer_forward(dev(inst.x), layer_dev(L))
+    torch.cuda.synchronize()
+    if cfg == 1:
+        ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+        assert normwise(host(h), ref) <= TOL["f32"]
+        return
+    gold = np.load(os.path.join(GOLDEN, "cfg%d.npz" % cfg))
+    hv = h.reshape(-1)[torch.from_numpy(gold["idx"]).to(DEV)]
+    err = float(np.abs(host(hv) - gold["val"]).max() / gold["absmax"])
+    assert err <= TOL["f32"], err
+    hh = host(h)
+    N, D = hh.shape[:2]
+    sums = hh.reshape(N * D, -1).sum(1)
+    # a slice sum of V/D entries: allow the per-entry tolerance times sqrt(count)
+    n_per = hh[0, 0].size
+    bound = TOL["f32"] * gold["absmax"] * np.sqrt(n_per) + 1e-6 * np.abs(gold["slice_sum"])
+    assert np.all(np.abs(sums - gold["slice_sum"]) <= bound)
+    sq = (hh.reshape(N * D, -1) ** 2).sum(1)
+    assert np.allclose(sq, gold["slice_sumsq"], rtol=2 * TOL["f32"])
+
+
+def test_zero_parameters_exact_zero():
+    """All-zero parameters give h = 0 exactly (sigma(0) = 1/2, tanh(0) = 0)."""
+    inst = instance((1, 6, 10, 12, 3, 16), 11)
+    L = inst.layers[0]
+    Lz = LayerW(*(torch.zeros_like(t) for t in layer_dev(L).__dict__.values()))
+    say("zero parameters")
+    h, _ = layer_forward(dev(inst.x), Lz)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(h).item() == 0
+
+
+@pytest.mark.parametrize("d", range(6))
+def test_dependency_cone_on_gpu(d):
+    """Only direction d active: perturbing one input voxel leaves every output
+    outside its pyramid bitwise unchanged.  Inside, the change decays along the
+    sweep (at the cone's edge it passes only through corner taps and can drop
+    below fp32 resolution), so every voxel within one plane of the source must
+    change."""
+    N, D, H, W, C, O = 1, 7, 9, 11, 1, 16
+    inst = instance((N, D, H, W, C, O), 40 + d)
+    L = inst.layers[0]
+    keep = np.zeros(6)
+    keep[d] = 1
+    Ld = LayerW(dev(L.wx * keep[:, None, None, None, None]),
+                dev(L.wh * keep[:, None, None, None, None]), dev(L.b * keep[:, None]))
+    src = (3, 4, 5)
+    x2 = inst.x.copy()
+    x2[0][src] += 1.0
+    say("cone", d)
+    h1, _ = layer_forward(dev(inst.x), Ld)
+    h2, _ = layer_forward(dev(x2), Ld)
+    torch.cuda.synchronize()
+    changed = np.any(host(h1)[0] != host(h2)[0], axis=-1)
+    a, sign = d // 2, (1 if d % 2 == 0 else -1)
+    inplane = [ax for ax in range(3) if ax != a]
+    idx = np.indices((D, H, W))
+    dt = sign * (idx[a] - src[a])
+    cheb = np.maximum(abs(idx[inplane[0]] - src[inplane[0]]),
+                      abs(idx[inplane[1]] - src[inplane[1]]))
+    cone = (dt >= 0) & (cheb <= 1 + dt)
+    assert not np.any(changed & ~cone)
+    assert np.all(changed[cone & (dt <= 1)])
+
+
+@pytest.mark.parametrize("axis", [0, 1, 2])
+def test_mirror_swaps_plus_minus_on_gpu(axis):
+    """Same parameters for both directions of an axis: mirroring the input
+    along that axis mirrors the layer output, bitwise."""
+    inst = instance((1, 6, 9, 13, 2, 16), 50 + axis)
+    L = inst.layers[0]
+    wx, wh, b = L.wx.copy(), L.wh.copy(), L.b.copy()
+    dp, dm = 2 * axis, 2 * axis + 1
+    wx[dm], wh[dm], b[dm] = wx[dp], wh[dp], b[dp]
+    for d in range(6):               # other axes off
+        if d // 2 != axis:
+            wx[d], wh[d], b[d] = 0, 0, 0
+    Ld = LayerW(dev(wx), dev(wh), dev(b))
+    say("mirror", axis)
+    h1, _ = layer_forward(dev(inst.x), Ld)
+    h2, _ = layer_forward(dev(np.flip(inst.x, axis=axis + 1).copy()), Ld)
+    torch.cuda.synchronize()
+    a, m = host(h1), np.flip(host(h2), axis=axis + 1)
+    # h = h^{a+} + h^{a-}; mirroring swaps the two terms, and fp32 addition
+    # commutes exactly
+    assert np.array_equal(a, m)
+
+
+def test_repeat_runs_bitwise_identical():
+    inst = instance((1, 10, 48, 40, 3, 16), 60)
+    L = inst.layers[0]
+    x, Ld = dev(inst.x), layer_dev(L)
+    say("determinism")
+    outs = [layer_forward(x, Ld)[0].clone() for _ in range(3)]
+    dh = dev(synth.upstream_grad(tuple(outs[0].shape), 61))
+    grads = []
+    for _ in range(2):
+        h, saved = layer_forward(x, Ld, training=True)
+        grads.append([t.clone() for t in layer_backward(x, Ld, saved, dh)])
+    torch.cuda.synchronize()
+    assert all(torch.equal(outs[0], o) for o in outs[1:])
+    assert all(torch.equal(a, b) for a, b in zip(grads[0], grads[1]))

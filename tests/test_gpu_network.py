@@ -1,0 +1,137 @@
+"""GPU parity of the stacked networks (configs 4 and 5, and small versions of
+them checked against the oracle directly), through the C ABI."""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle.network as onet
+import synth
+from paper_1506_07452_amd.network import network_forward, network_train_step
+from tests.gpu_util import DEV, TOL, dev, host, layer_dev, normwise, say
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def to_device(inst, dtype):
+    layers = [layer_dev(L, dtype) for L in inst.layers]
+    fcs = [(dev(w, dtype), dev(b, dtype)) for w, b in inst.fcs]
+    head = (dev(inst.head[0], dtype), dev(inst.head[1], dtype))
+    labels = None
+    if inst.labels is not None:
+        labels = torch.from_numpy(inst.labels).to(DEV)
+    return dev(inst.x, dtype), layers, fcs, head, labels
+
+
+def oracle_args(inst):
+    return ([(L.wx, L.wh, L.b) for L in inst.layers], inst.fcs, inst.head)
+
+
+def small(wl_kw, seed):
+    wl = synth.Workload("small", seed=seed, **wl_kw)
+    return synth.make(wl)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_small_network_forward(dtype):
+    inst = small(dict(N=2, D=6, H=10, W=9, C=3, hidden=[16, 32], dtype=dtype, fc=True,
+                      classes=4), 70)
+    ref = onet.forward(inst.x, *oracle_args(inst))["p"]
+    say("small network forward", dtype)
+    x, layers, fcs, head, _ = to_device(inst, dtype)
+    out = network_forward(x, layers, fcs, head)
+    torch.cuda.synchronize()
+    assert normwise(host(out["p"]), ref) <= TOL[dtype]
+
+
+def test_small_network_training_step():
+    inst = small(dict(N=1, D=5, H=12, W=7, C=3, hidden=[16, 32], fc=True, classes=4,
+                      labels=True), 80)
+    ref = onet.backward(inst.x, *oracle_args(inst), inst.labels)
+    say("small network training step")
+    x, layers, fcs, head, labels = to_device(inst, "f32")
+    g = network_train_step(x, layers, fcs, head, labels)
+    torch.cuda.synchronize()
+    assert abs(g["loss"].item() - ref["loss"]) <= TOL["f32"] * abs(ref["loss"])
+    pairs = [(g["head"][0], ref["head"][0]), (g["head"][1], ref["head"][1])]
+    for li in range(2):
+        pairs += list(zip(g["fcs"][li], ref["fcs"][li]))
+        pairs += list(zip(g["layers"][li], ref["layers"][li]))
+    for got, want in pairs:
+        assert normwise(host(got), want) <= TOL["f32"]
+
+
+def test_fc_and_softmax_match_oracle():
+    rng = np.random.default_rng(90)
+    M, Cin, Cout, K = 1000, 16, 32, 4
+    xa = rng.standard_normal((M, Cin)).astype(np.float32)
+    w1 = rng.uniform(-0.3, 0.3, (Cout, Cin)).astype(np.float32)
+    b1 = rng.uniform(-0.3, 0.3, Cout).astype(np.float32)
+    w2 = rng.uniform(-0.3, 0.3, (K, Cout)).astype(np.float32)
+    b2 = rng.uniform(-0.3, 0.3, K).astype(np.float32)
+    lab = rng.integers(0, K, M).astype(np.int32)
+    dy = rng.standard_normal((M, Cout)).astype(np.float32)
+    import paper_1506_07452_amd as P
+    y = torch.empty(M, Cout, device=DEV)
+    P.pyramid_fc_tanh_forward(dev(xa), dev(w1), dev(b1), y)
+    dx, dw, db = (torch.empty(M, Cin, device=DEV), torch.empty(Cout, Cin, device=DEV),
+                  torch.empty(Cout, device=DEV))
+    P.pyramid_fc_tanh_backward(dev(xa), dev(w1), y, dev(dy), dx, dw, db)
+    p = torch.empty(M, K, device=DEV)
+    loss = torch.empty(1, device=DEV)
+    ldx, ldw, ldb = (torch.empty(M, Cout, device=DEV), torch.empty(K, Cout, device=DEV),
+                     torch.empty(K, device=DEV))
+    P.pyramid_softmax_ce(y, dev(w2), dev(b2), p, torch.from_numpy(lab).to(DEV), loss, ldx, ldw, ldb)
+    torch.cuda.synchronize()
+    ry = oracle.fc_tanh_forward(xa, w1, b1)
+    assert normwise(host(y), ry) <= TOL["f32"]
+    rb = oracle.fc_tanh_backward(xa, w1, ry, dy)
+    for got, want in ((dx, rb["dx"]), (dw, rb["dw"]), (db, rb["db"])):
+        assert normwise(host(got), want) <= TOL["f32"]
+    rs = oracle.softmax_ce(host(y), w2, b2, lab, grad=True)
+    assert normwise(host(p), rs["p"]) <= TOL["f32"]
+    assert abs(loss.item() - rs["loss"]) <= TOL["f32"] * rs["loss"]
+    for got, want in ((ldx, rs["dx"]), (ldw, rs["dw"]), (ldb, rs["db"])):
+        assert normwise(host(got), want) <= TOL["f32"]
+
+
+def test_config4_network_forward_bf16():
+    """8 x 64^3 x 3, three layers (16, 32, 64) + FC tanh + softmax, bf16
+    storage: sampled softmax outputs and per-class sums vs the oracle."""
+    inst = synth.config(4)
+    gold = np.load(os.path.join(GOLDEN, "cfg4.npz"))
+    say("config 4")
+    x, layers, fcs, head, _ = to_device(inst, "bf16")
+    out = network_forward(x, layers, fcs, head)
+    torch.cuda.synchronize()
+    p = out["p"]
+    got = host(p[torch.from_numpy(gold["vox"]).to(DEV)])
+    assert normwise(got, gold["p"]) <= TOL["bf16"]
+    cs = host(p.sum(0))
+    assert np.allclose(cs, gold["class_sum"], rtol=TOL["bf16"])
+
+
+def test_config5_training_step():
+    """48 x 240 x 240 x 3, two layers (16, 32) + FC + softmax + CE, fp32:
+    loss, sampled probabilities and every parameter gradient vs the oracle."""
+    inst = synth.config(5)
+    gold = np.load(os.path.join(GOLDEN, "cfg5.npz"))
+    say("config 5")
+    x, layers, fcs, head, labels = to_device(inst, "f32")
+    g = network_train_step(x, layers, fcs, head, labels)
+    torch.cuda.synchronize()
+    assert abs(g["loss"].item() - float(gold["loss"])) <= TOL["f32"] * float(gold["loss"])
+    got_p = host(g["p"][torch.from_numpy(gold["vox"]).to(DEV)])
+    assert normwise(got_p, gold["p"]) <= TOL["f32"]
+    named = {"head_dw": g["head"][0], "head_db": g["head"][1]}
+    for li in range(2):
+        named["l%d_dwx" % li], named["l%d_dwh" % li], named["l%d_db" % li] = g["layers"][li]
+        named["fc%d_dw" % li], named["fc%d_db" % li] = g["fcs"][li]
+    for k, t in named.items():
+        err = normwise(host(t), gold[k])
+        assert err <= TOL["f32"], (k, err)

@@ -152,6 +152,13 @@ int pyramid_lstm_timing_enable(int on);
 int pyramid_lstm_timing_read(int max_phases, char *names, double *ms, int *launches,
                              int *count);
 
+
+/* Forward implementation selection, for testing and tuning (process-wide):
+ * 0 = automatic (default): the persistent MFMA sweep where it supports the
+ * shape (fp32, O = 16, C <= 4, grid co-resident), else the generic path;
+ * 1 = generic path only; 2 = same as 0.  Returns PLSTM_EINVAL for other values. */
+int pyramid_lstm_set_forward_path(int path);
+
 #ifdef __cplusplus
 }
 #endif

@@ -19,7 +19,8 @@ __all__ = [
     "pyramid_lstm_status_string", "pyramid_lstm_workspace_size", "pyramid_lstm_saved_size",
     "pyramid_lstm_forward", "pyramid_lstm_backward", "pyramid_fc_tanh_forward",
     "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
-    "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "library_path", "load",
+    "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
+    "library_path", "load",
 ]
 
 PLSTM_F32 = 0
@@ -82,6 +83,8 @@ def load():
                                              ctypes.POINTER(ctypes.c_int),
                                              ctypes.POINTER(ctypes.c_int)]
     lib.pyramid_lstm_timing_read.restype = ctypes.c_int
+    lib.pyramid_lstm_set_forward_path.argtypes = [ctypes.c_int]
+    lib.pyramid_lstm_set_forward_path.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -214,3 +217,8 @@ def pyramid_lstm_timing_read(max_phases: int = 32):
         nm = names.raw[32 * k:32 * k + 32].split(b"\0", 1)[0].decode()
         out[nm] = (ms[k], launches[k])
     return out
+
+
+def pyramid_lstm_set_forward_path(path: int) -> None:
+    """0 = automatic, 1 = generic path only, 2 = MFMA sweep where supported."""
+    _check("pyramid_lstm_set_forward_path", load().pyramid_lstm_set_forward_path(int(path)))

@@ -15,6 +15,7 @@
 // (deterministic two-stage sums), and dL/dx a transposed 3x3 convolution with
 // wx summed over the six directions.
 #include "common.h"
+#include "sweep.h"
 #include "timing.h"
 
 namespace plstm {
@@ -356,6 +357,11 @@ int generic_forward(const Geom &g, int dtype, const void *x, const void *wx, con
         PLSTM_LAUNCH_CHECK();
     }
     timing_end(T, st);
+    return sum_dirs(g, dtype, hd, h, st);
+}
+
+int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st)
+{
     const long long count = (long long)g.N * g.V * g.O;
     const unsigned blocks = (unsigned)((count + kThreads - 1) / kThreads);
     timing_begin("sum_dirs", st);

@@ -5,12 +5,24 @@
 
 namespace plstm {
 
-// Workspace bytes of the forward actually dispatched for this shape.
+// Persistent MFMA sweep (sweep_fwd.hip): O = 16, C <= 4, fp32.
+bool sweep_fwd_supported(const Geom &g, int dtype);
+size_t sweep_fwd_ws(const Geom &g, bool training);
+int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, const float *b,
+              float *hd, float *cell, float *gates, int *flags, hipStream_t st);
+
+// h = sum of the six per-direction outputs (generic.hip).
+int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st);
+
+// Workspace bytes of the forward for this shape (covers every path it may take).
 size_t forward_ws(const Geom &g, int dtype, bool training);
 
 // Runs the layer forward on the fastest path that supports the shape.
 int forward_dispatch(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
                      const void *b, void *h, float *gates, float *cell, void *ws,
                      hipStream_t st);
+
+// 0 = automatic, 1 = generic path only, 2 = persistent MFMA sweep where supported.
+extern int g_forward_path;
 
 }  // namespace plstm

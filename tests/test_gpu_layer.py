@@ -9,6 +9,7 @@ import pytest
 import torch
 
 import oracle
+import paper_1506_07452_amd as P
 import synth
 from paper_1506_07452_amd.network import LayerW, layer_backward, layer_forward
 from tests.gpu_util import DEV, TOL, dev, host, layer_dev, normwise, say
@@ -37,7 +38,16 @@ def instance(shape, seed, dtype="f32"):
     return synth.make(wl)
 
 
-@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.fixture
+def generic_path():
+    """Run the forward on the generic per-plane path only."""
+    P.pyramid_lstm_set_forward_path(1)
+    yield
+    P.pyramid_lstm_set_forward_path(0)
+
+
+@pytest.mark.parametrize("shape", SHAPES + [(3, 6, 20, 18, 2, 16), (1, 9, 2, 300, 4, 16)],
+                         ids=lambda s: "x".join(map(str, s)))
 def test_forward_matches_oracle(shape):
     inst = instance(shape, 1000 + sum(shape))
     L = inst.layers[0]
@@ -47,6 +57,35 @@ def test_forward_matches_oracle(shape):
     torch.cuda.synchronize()
     err = normwise(host(h), ref)
     assert err <= TOL["f32"], err
+
+
+@pytest.mark.parametrize("shape", [(1, 5, 37, 29, 3, 16), (2, 4, 9, 7, 1, 16)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_generic_path_forward_matches_oracle(shape, generic_path):
+    inst = instance(shape, 1100 + sum(shape))
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    say("forward generic", shape)
+    P.pyramid_lstm_timing_enable(True)
+    h, _ = layer_forward(dev(inst.x), layer_dev(L))
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    assert "sweep_fwd_generic" in phases and "sweep_fwd_mfma" not in phases
+    assert normwise(host(h), ref) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_mfma_sweep_runs_for_the_o16_workloads(cfg):
+    """The persistent MFMA sweep (one launch) is the path taken for the
+    16-hidden-unit fp32 workloads, not the generic fallback."""
+    inst = synth.config(cfg)
+    say("mfma path", cfg)
+    P.pyramid_lstm_timing_enable(True)
+    layer_forward(dev(inst.x), layer_dev(inst.layers[0]))
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    assert phases.get("sweep_fwd_mfma", (0, 0))[1] == 1, phases
+    assert "sweep_fwd_generic" not in phases
 
 
 @pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[1], SHAPES[2], SHAPES[4], SHAPES[8]],

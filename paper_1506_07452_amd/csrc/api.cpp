@@ -24,7 +24,7 @@ int check_shape(const plstm_shape *s)
     // grid limits of the generic path: 6N blocks in z, one plane per launch
     if ((long long)s->N * kDirs > 65535) return PLSTM_EUNSUPPORTED;
     const long long V = (long long)s->D * s->H * s->W;
-    if (V > (1LL << 31) / 64 || (long long)s->N * V * 4 * s->O * kDirs > (1LL << 40))
+    if (V >= (1LL << 31) / 64 || (long long)s->N * V * 4 * s->O * kDirs > (1LL << 40))
         return PLSTM_EUNSUPPORTED;
     return PLSTM_OK;
 }

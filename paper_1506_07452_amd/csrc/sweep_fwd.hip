@@ -4,7 +4,8 @@
 //
 // One cooperative launch runs all six directions (and all batch elements) at
 // once.  The plane of each direction is cut into strips of whole rows x a few
-// columns; one workgroup (4 waves) owns one strip for the whole sweep:
+// columns; one workgroup (8 waves, two per SIMD) owns one strip for the whole
+// sweep:
 //
 //   for t in 0..T-1:
 //     wait until the two neighbouring strips have published h_{t-1}
@@ -16,7 +17,8 @@
 //         write h_t, c_t (and the gates when training) to global memory
 //     publish: release fence, flag = t + 1
 //
-// The weights live in VGPRs as MFMA B fragments for the whole kernel; h of
+// The recurrent weights live in VGPRs as MFMA B fragments for the whole
+// kernel (the input-convolution fragments in LDS); h of
 // every plane stays in the per-direction volume in global memory, so a step
 // only reads plane t-1 and writes plane t (no write-after-read hazard), and
 // LDS is just a staging copy.  MFMA layout (16x16x4 f32, one block): lane l
@@ -37,10 +39,12 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kO = 16;
 constexpr int kG = 4 * kO;
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;          // two waves per SIMD: one computes gates while the other runs MFMAs
 constexpr int kThreads = 64 * kWaves;
 constexpr int kHS = 20;          // LDS floats per staged h pixel (16 + 4 pad)
 constexpr int kMaxSpin = 1 << 21;
+constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unconstrained
+constexpr int kBatch = 4;        // staging loads in flight per thread
 
 struct SweepArgs {
     Geom g;
@@ -56,10 +60,19 @@ struct SweepArgs {
     int max_w;          // widest strip (LDS layout)
 };
 
-__device__ inline float fsig(float a) { return 1.0f / (1.0f + __expf(-a)); }
-__device__ inline float ftanh(float a) {
-    // tanh(a) = 1 - 2 / (exp(2a) + 1); saturates correctly at +-inf.
-    return 1.0f - 2.0f / (__expf(2.0f * a) + 1.0f);
+// Gate nonlinearities from exp and the hardware reciprocal (1 ulp each):
+// sigma(a) = 1 / (1 + e^-a);  tanh(a) = 1 - 2 / (e^{2a} + 1), which saturates
+// to +-1 at +-inf.
+__device__ inline float frcp(float v) { return __builtin_amdgcn_rcpf(v); }
+__device__ inline float fsig(float a) { return frcp(1.0f + __expf(-a)); }
+__device__ inline float ftanh(float a) { return 1.0f - 2.0f * frcp(__expf(2.0f * a) + 1.0f); }
+
+// floor(i / w) for 0 <= i < 2^20, w >= 1, from a float reciprocal: the
+// fraction of (i + 0.5) / w is at least 0.5 / w away from an integer, while the
+// product's rounding error is below (i / w) 2^-23 <= 0.125 / w, so the
+// truncation is exact.
+__device__ inline int fdiv_floor(int i, float inv_w) {
+    return (int)(((float)i + 0.5f) * inv_w);
 }
 
 template <int C>
@@ -83,8 +96,10 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q4 = lane >> 4, col = lane & 15;
-    float *hs = smem;
-    float *xs = smem + (a.chunk_rows + 2) * (a.max_w + 2) * kHS;
+    constexpr int KXS = (9 * C + 3) / 4;    // MFMA k-steps of the input convolution
+    float *wxs = smem;                       // [KXS][64 lanes][4 N-tiles] B fragments
+    float *hs = smem + KXS * 256;
+    float *xs = hs + (a.chunk_rows + 2) * (a.max_w + 2) * kHS;
 
     // ---- weights as MFMA B fragments (resident for the whole sweep) -----
     const long long V = a.g.V;
@@ -98,27 +113,39 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
                 const int j = 4 * q4 + s, gn = nt * kO + col;
                 bh[tap][s][nt] = a.wh[(((long long)d * kG + gn) * kO + j) * 9 + tap];
             }
-    constexpr int KXS = (9 * C + 3) / 4;
-    float bx[KXS][4];
+    // Input-convolution B fragments go to LDS (they feed few MFMAs; keeping
+    // them out of VGPRs lets two waves share a SIMD).
     int xoff[KXS];
 #pragma unroll
     for (int ks = 0; ks < KXS; ++ks) {
         const int k = 4 * ks + q4;
         const int tap = k < 9 * C ? k / C : 0, c = k % C;   // padding lanes read tap 0
         xoff[ks] = k < 9 * C ? ((tap / 3 - 1) * W2 + (tap % 3 - 1)) * C + c : 0;
+        if (wave == 0) {
+            f4 w4;
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-            const int gn = nt * kO + col;
-            const float w = a.wx[(((long long)d * kG + gn) * C + c) * 9 + tap];
-            bx[ks][nt] = k < 9 * C ? w : 0.0f;
+            for (int nt = 0; nt < 4; ++nt) {
+                const int gn = nt * kO + col;
+                const float w = a.wx[(((long long)d * kG + gn) * C + c) * 9 + tap];
+                w4[nt] = k < 9 * C ? w : 0.0f;
+            }
+            *(f4 *)&wxs[(ks * 64 + lane) * 4] = w4;
         }
     }
+    __syncthreads();
     float bias[4];
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) bias[nt] = a.b[d * kG + nt * kO + col];
 
-    const long long dn = ((long long)d * a.g.N + n) * V;   // h^d / c^d base (voxels)
-    const long long xn = (long long)n * V;                  // x base (voxels)
+    // Base pointers of this (direction, batch element); element offsets inside
+    // a slice fit in 32 bits (V * 64 < 2^31 is checked at the boundary).
+    const long long dn = ((long long)d * a.g.N + n) * V;
+    float *const hd_dn = a.hd + dn * kO;
+    float *const cell_dn = a.cell + dn * kO;
+    float *const gates_dn = a.gates ? a.gates + dn * kG : nullptr;
+    const float *const x_n = a.x + (long long)n * V * C;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const float inv_tq = 1.0f / (float)TQ, inv_w2 = 1.0f / (float)W2;
 
     for (int t = 0; t < dg.T; ++t) {
         const int s = dg.sign > 0 ? t : dg.T - 1 - t;
@@ -143,26 +170,47 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
             }
             __syncthreads();
         }
+        const int splane = s * ss, sprev_plane = sprev * ss;
+        const int cplane = t > 0 ? sprev_plane : splane;
         for (int r0 = 0; r0 < dg.P; r0 += a.chunk_rows) {
             const int CH = min(a.chunk_rows, dg.P - r0);
             const int npl = (CH + 2) * W2;            // staged pixels incl. halo
             // ---- stage h_{t-1} and x_t (zero outside the plane) ----------
-            for (int e = threadIdx.x; e < npl * 4; e += kThreads) {
-                const int pix = e >> 2, qd = e & 3;
-                const int pr = pix / W2 + r0 - 1, pc = pix % W2 + q0 - 1;
-                f4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-                if (t > 0 && pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q)
-                    v = *(const f4 *)&a.hd[(dn + sprev * dg.ss + pr * dg.sp + pc * dg.sq) * kO +
-                                          qd * 4];
-                *(f4 *)&hs[pix * kHS + qd * 4] = v;
-            }
-            for (int e = threadIdx.x; e < npl * C; e += kThreads) {
-                const int pix = e / C, c = e % C;
-                const int pr = pix / W2 + r0 - 1, pc = pix % W2 + q0 - 1;
-                float v = 0.0f;
-                if (pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q)
-                    v = a.x[(xn + s * dg.ss + pr * dg.sp + pc * dg.sq) * C + c];
-                xs[pix * C + c] = v;
+            // Branch-free loads from clamped addresses, kBatch per thread in
+            // flight before the LDS stores: one memory round trip per batch.
+            const int nh = npl * 4, nx = npl * C;
+            for (int e0 = threadIdx.x; e0 < max(nh, nx); e0 += kThreads * kBatch) {
+                f4 hv[kBatch];
+                float xv[kBatch];
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    const int e = e0 + u * kThreads;
+                    {
+                        const int pix = e >> 2, qd = e & 3;
+                        const int rr = fdiv_floor(pix, inv_w2);
+                        const int pr = rr + r0 - 1, pc = pix - rr * W2 + q0 - 1;
+                        const bool ok = e < nh && t > 0 && pr >= 0 && pr < dg.P && pc >= 0 &&
+                                        pc < dg.Q;
+                        const int off = ok ? (sprev_plane + pr * sp + pc * sq) * kO + qd * 4 : 0;
+                        const f4 v = *(const f4 *)&hd_dn[off];
+                        hv[u] = ok ? v : f4{0.0f, 0.0f, 0.0f, 0.0f};
+                    }
+                    {
+                        const int pix = e / C, c = e - (e / C) * C;
+                        const int rr = fdiv_floor(pix, inv_w2);
+                        const int pr = rr + r0 - 1, pc = pix - rr * W2 + q0 - 1;
+                        const bool ok = e < nx && pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q;
+                        const int off = ok ? (splane + pr * sp + pc * sq) * C + c : 0;
+                        const float v = x_n[off];
+                        xv[u] = ok ? v : 0.0f;
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    const int e = e0 + u * kThreads;
+                    if (e < nh) *(f4 *)&hs[(e >> 2) * kHS + (e & 3) * 4] = hv[u];
+                    if (e < nx) xs[e] = xv[u];
+                }
             }
             __syncthreads();
             // ---- 16-pixel tiles -----------------------------------------
@@ -170,7 +218,25 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
             const int nmt = (npx + 15) >> 4;
             for (int mt = wave; mt < nmt; mt += kWaves) {
                 const int pa = min(mt * 16 + col, npx - 1);     // this lane's A row
-                const int base = (pa / TQ + 1) * W2 + (pa % TQ + 1);
+                const int ra = fdiv_floor(pa, inv_tq);
+                const int base = (ra + 1) * W2 + (pa - ra * TQ) + 1;
+                // Output rows 4 q4 + i of this lane; c_{t-1} is loaded now so
+                // the load overlaps the contraction below.
+                float cprev[4];
+                int vout[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int px = min(mt * 16 + 4 * q4 + i, npx - 1);
+                    const int rr = fdiv_floor(px, inv_tq);
+                    vout[i] = splane + (rr + r0) * sp + (px - rr * TQ + q0) * sq;
+                    // at t = 0 there is no previous plane: read (and discard)
+                    // this plane's entry so the address stays inside the slice
+                    const float cv = cell_dn[(vout[i] - splane + cplane) * kO + col];
+                    cprev[i] = t > 0 ? cv : 0.0f;
+                }
+                // keep the loads above the contraction (the scheduler would
+                // otherwise sink them to their use and expose their latency)
+                __builtin_amdgcn_sched_barrier(0);
                 f4 acc[4];
 #pragma unroll
                 for (int nt = 0; nt < 4; ++nt) acc[nt] = f4{bias[nt], bias[nt], bias[nt], bias[nt]};
@@ -188,28 +254,26 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
 #pragma unroll
                 for (int ks = 0; ks < KXS; ++ks) {
                     const float av = (4 * ks + q4 < 9 * C) ? xs[base * C + xoff[ks]] : 0.0f;
+                    const f4 bxv = *(const f4 *)&wxs[(ks * 64 + lane) * 4];
 #pragma unroll
                     for (int nt = 0; nt < 4; ++nt)
-                        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bx[ks][nt], acc[nt],
+                        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bxv[nt], acc[nt],
                                                                      0, 0, 0);
                 }
                 // ---- gates and cell update: rows 4 q4 + i, unit col ------
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int px = mt * 16 + 4 * q4 + i;
-                    if (px >= npx) continue;
-                    const int pr = px / TQ + r0, pc = px % TQ + q0;
-                    const long long v = dn + s * dg.ss + pr * dg.sp + pc * dg.sq;
+                    if (mt * 16 + 4 * q4 + i >= npx) continue;
+                    const int v = vout[i];
                     const float gi = fsig(acc[0][i]);
                     const float gf = fsig(acc[1][i]);
                     const float gg = ftanh(acc[2][i]);
                     const float go = fsig(acc[3][i]);
-                    float c = gg * gi;
-                    if (t > 0) c += a.cell[(v + (long long)(sprev - s) * dg.ss) * kO + col] * gf;
-                    a.cell[v * kO + col] = c;
-                    a.hd[v * kO + col] = go * ftanh(c);
-                    if (a.gates) {
-                        float *gp = a.gates + v * kG + col;
+                    const float c = gg * gi + cprev[i] * gf;
+                    cell_dn[v * kO + col] = c;
+                    hd_dn[v * kO + col] = go * ftanh(c);
+                    if (gates_dn) {
+                        float *gp = gates_dn + v * kG + col;
                         gp[0] = gi;
                         gp[kO] = gf;
                         gp[2 * kO] = gg;
@@ -220,11 +284,17 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
             __syncthreads();
         }
         // ---- publish h_t -------------------------------------------------
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        // Every wave waits until its own stores have reached L2, then one
+        // thread writes L2 back (release at agent scope) and raises the flag:
+        // one cache writeback per workgroup and step instead of one per wave.
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
-        if (threadIdx.x == 0)
+        if (threadIdx.x == 0) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");   // L2 writeback
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);             // ... completed
             __hip_atomic_store(&a.flags[blockIdx.x], t + 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
 }
 
@@ -304,10 +374,11 @@ Plan make_plan(const Geom &g, int budget, int C, size_t lds_limit)
     int maxP = 1;
     for (int d = 0; d < kDirs; ++d) maxP = g.dir[d].P > maxP ? g.dir[d].P : maxP;
     const size_t per_row = (size_t)(max_w + 2) * (kHS + C) * sizeof(float);
-    long long rows = (long long)(lds_limit / per_row) - 2;
+    const size_t fixed = (size_t)((9 * C + 3) / 4) * 256 * sizeof(float);   // wx fragments
+    long long rows = (long long)((lds_limit - fixed) / per_row) - 2;
     if (rows > maxP) rows = maxP;
     pl.chunk_rows = rows < 1 ? 0 : (int)rows;
-    pl.lds = (size_t)(pl.chunk_rows + 2) * per_row;
+    pl.lds = fixed + (size_t)(pl.chunk_rows + 2) * per_row;
     return pl;
 }
 

@@ -77,7 +77,8 @@ size_t pyramid_lstm_workspace_size(const plstm_shape *s, int training);
 
 /* Bytes of the `saved` buffer that a training forward fills and the backward
  * reads (gate activations and cell states of every voxel and direction, in a
- * library-private layout).  Returns 0 for an invalid or unsupported shape. */
+ * library-private layout: gates, c^d and h^d, fp32).  Returns 0 for an invalid
+ * or unsupported shape. */
 size_t pyramid_lstm_saved_size(const plstm_shape *s);
 
 /* Forward pass of one layer, Eq. (7)-(13).
@@ -158,6 +159,10 @@ int pyramid_lstm_timing_read(int max_phases, char *names, double *ms, int *launc
  * shape (fp32, O = 16, C <= 4, grid co-resident), else the generic path;
  * 1 = generic path only; 2 = same as 0.  Returns PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_forward_path(int path);
+
+/* Backward implementation selection, for testing and tuning (process-wide):
+ * 0 = automatic (default), 1 = generic per-plane path only, 2 = same as 0. */
+int pyramid_lstm_set_backward_path(int path);
 
 #ifdef __cplusplus
 }

@@ -20,6 +20,7 @@ __all__ = [
     "pyramid_lstm_forward", "pyramid_lstm_backward", "pyramid_fc_tanh_forward",
     "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
+    "pyramid_lstm_set_backward_path",
     "library_path", "load",
 ]
 
@@ -85,6 +86,8 @@ def load():
     lib.pyramid_lstm_timing_read.restype = ctypes.c_int
     lib.pyramid_lstm_set_forward_path.argtypes = [ctypes.c_int]
     lib.pyramid_lstm_set_forward_path.restype = ctypes.c_int
+    lib.pyramid_lstm_set_backward_path.argtypes = [ctypes.c_int]
+    lib.pyramid_lstm_set_backward_path.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -222,3 +225,8 @@ def pyramid_lstm_timing_read(max_phases: int = 32):
 def pyramid_lstm_set_forward_path(path: int) -> None:
     """0 = automatic, 1 = generic path only, 2 = MFMA sweep where supported."""
     _check("pyramid_lstm_set_forward_path", load().pyramid_lstm_set_forward_path(int(path)))
+
+
+def pyramid_lstm_set_backward_path(path: int) -> None:
+    """0 = automatic, 1 = generic path only, 2 = MFMA sweep where supported."""
+    _check("pyramid_lstm_set_backward_path", load().pyramid_lstm_set_backward_path(int(path)))

@@ -29,14 +29,6 @@ int check_shape(const plstm_shape *s)
     return PLSTM_OK;
 }
 
-size_t saved_bytes(const Geom &g)
-{
-    Carve cv(nullptr);
-    cv.take<float>(saved_gates_count(g));
-    cv.take<float>(saved_cell_count(g));
-    return cv.off;
-}
-
 }  // namespace
 
 extern "C" {
@@ -66,7 +58,7 @@ size_t pyramid_lstm_workspace_size(const plstm_shape *s, int training)
     const Geom g = make_geom(*s);
     size_t need = forward_ws(g, s->dtype, training != 0);
     if (training) {
-        const size_t b = generic_backward_ws(g);
+        const size_t b = backward_ws(g);
         if (b > need) need = b;
     }
     return need < 256 ? 256 : need;
@@ -85,13 +77,10 @@ int pyramid_lstm_forward(const plstm_shape *s, const void *x, const void *wx, co
     if (saved && s->dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
     if (ws_bytes < pyramid_lstm_workspace_size(s, saved != nullptr)) return PLSTM_EWORKSPACE;
     const Geom g = make_geom(*s);
-    float *gates = nullptr, *cell = nullptr;
-    if (saved) {
-        Carve cv(saved);
-        gates = cv.take<float>(saved_gates_count(g));
-        cell = cv.take<float>(saved_cell_count(g));
-    }
-    return forward_dispatch(g, s->dtype, x, wx, wh, b, h, gates, cell, ws, (hipStream_t)stream);
+    Saved sv{};
+    if (saved) sv = carve_saved(saved, g);
+    return forward_dispatch(g, s->dtype, x, wx, wh, b, h, saved ? &sv : nullptr, ws,
+                            (hipStream_t)stream);
 }
 
 int pyramid_lstm_backward(const plstm_shape *s, const void *x, const void *wx, const void *wh,
@@ -109,12 +98,10 @@ int pyramid_lstm_backward(const plstm_shape *s, const void *x, const void *wx, c
     if (s->dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
     if (ws_bytes < pyramid_lstm_workspace_size(s, 1)) return PLSTM_EWORKSPACE;
     const Geom g = make_geom(*s);
-    Carve cv(const_cast<void *>(saved));
-    const float *gates = cv.take<float>(saved_gates_count(g));
-    const float *cell = cv.take<float>(saved_cell_count(g));
-    return generic_backward(g, (const float *)x, (const float *)wx, (const float *)wh, gates,
-                            cell, (const float *)dh, (float *)dx, (float *)dwx, (float *)dwh,
-                            (float *)db, ws, (hipStream_t)stream);
+    const Saved sv = carve_saved(const_cast<void *>(saved), g);
+    return backward_dispatch(g, (const float *)x, (const float *)wx, (const float *)wh, sv,
+                             (const float *)dh, (float *)dx, (float *)dwx, (float *)dwh,
+                             (float *)db, ws, (hipStream_t)stream);
 }
 
 size_t pyramid_fc_workspace_size(int64_t M, int32_t Cin, int32_t Cout)

@@ -89,23 +89,46 @@ struct Carve {
         if (hipGetLastError() != hipSuccess) return PLSTM_EHIP; \
     } while (0)
 
+// Saved-activation layout shared by every forward/backward pair (fp32,
+// per-direction volumes in [N][D][H][W] voxel order):
+//   gates [6][N][V][4O]  i, f, g, o after the nonlinearity
+//   cell  [6][N][V][O]   c^d
+//   hd    [6][N][V][O]   h^d
+struct Saved {
+    float *gates, *cell, *hd;
+};
+inline size_t saved_gates_count(const Geom &g) { return (size_t)kDirs * g.N * g.V * 4 * g.O; }
+inline size_t saved_state_count(const Geom &g) { return (size_t)kDirs * g.N * g.V * g.O; }
+inline Saved carve_saved(void *p, const Geom &g) {
+    Carve cv(p);
+    Saved s;
+    s.gates = cv.take<float>(saved_gates_count(g));
+    s.cell = cv.take<float>(saved_state_count(g));
+    s.hd = cv.take<float>(saved_state_count(g));
+    return s;
+}
+inline size_t saved_bytes(const Geom &g) {
+    Carve cv(nullptr);
+    cv.take<float>(saved_gates_count(g));
+    cv.take<float>(saved_state_count(g));
+    cv.take<float>(saved_state_count(g));
+    return cv.off;
+}
+
 // ---- launchers implemented in the .hip translation units -------------------
 
 // Generic path (any supported shape): one launch per plane step.
+// Forward: with `sv` (training) h^d, c^d and the gates go to the saved buffer,
+// otherwise h^d and c^d live in the workspace.
 int generic_forward(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
-                    const void *b, void *h, float *gates, float *cell, void *ws,
-                    hipStream_t st);
+                    const void *b, void *h, const Saved *sv, void *ws, hipStream_t st);
 size_t generic_forward_ws(const Geom &g, bool training);
 int generic_backward(const Geom &g, const float *x, const float *wx, const float *wh,
-                     const float *gates, const float *cell, const float *dh, float *dx,
-                     float *dwx, float *dwh, float *db, void *ws, hipStream_t st);
+                     const Saved &sv, const float *dh, float *dx, float *dwx, float *dwh,
+                     float *db, void *ws, hipStream_t st);
 size_t generic_backward_ws(const Geom &g);
-
-// Saved-activation layout shared by every forward/backward pair:
-//   gates [6][N][V][4O] fp32 (i, f, g, o after the nonlinearity), then
-//   cell  [6][N][V][O]  fp32.
-inline size_t saved_gates_count(const Geom &g) { return (size_t)kDirs * g.N * g.V * 4 * g.O; }
-inline size_t saved_cell_count(const Geom &g) { return (size_t)kDirs * g.N * g.V * g.O; }
+// dL/dx from the gate gradients dA [6][N][V][4O] of every direction.
+int generic_dx(const Geom &g, const float *wx, const float *dA, float *dx, hipStream_t st);
 
 // Fully connected glue.
 int fc_tanh_forward(long long M, int Cin, int Cout, int dtype, const void *x, const void *w,

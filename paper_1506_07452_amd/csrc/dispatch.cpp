@@ -4,6 +4,7 @@
 namespace plstm {
 
 int g_forward_path = 0;
+int g_backward_path = 0;
 
 size_t forward_ws(const Geom &g, int dtype, bool training)
 {
@@ -16,22 +17,43 @@ size_t forward_ws(const Geom &g, int dtype, bool training)
 }
 
 int forward_dispatch(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
-                     const void *b, void *h, float *gates, float *cell, void *ws,
-                     hipStream_t st)
+                     const void *b, void *h, const Saved *sv, void *ws, hipStream_t st)
 {
     if (g_forward_path != 1 && sweep_fwd_supported(g, dtype)) {
         Carve cv(ws);
-        float *hd = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
-        float *cellbuf = cell ? cell : cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
+        float *hd = sv ? sv->hd : cv.take<float>(saved_state_count(g));
+        float *cellbuf = sv ? sv->cell : cv.take<float>(saved_state_count(g));
         int *flags = cv.take<int>(1024 + 1);
         const int rc = sweep_fwd(g, (const float *)x, (const float *)wx, (const float *)wh,
-                                 (const float *)b, hd, cellbuf, gates, flags, st);
+                                 (const float *)b, hd, cellbuf, sv ? sv->gates : nullptr, flags,
+                                 st);
         if (rc == PLSTM_OK) return sum_dirs(g, dtype, hd, h, st);
         // A grid that cannot be co-resident or a plane too wide for LDS runs
         // on the generic path instead.
         if (rc != PLSTM_ENOTCORESIDENT && rc != PLSTM_EUNSUPPORTED) return rc;
     }
-    return generic_forward(g, dtype, x, wx, wh, b, h, gates, cell, ws, st);
+    return generic_forward(g, dtype, x, wx, wh, b, h, sv, ws, st);
+}
+
+size_t backward_ws(const Geom &g)
+{
+    size_t need = generic_backward_ws(g);
+    if (sweep_bwd_supported(g)) {
+        const size_t s = sweep_bwd_ws(g);
+        if (s > need) need = s;
+    }
+    return need;
+}
+
+int backward_dispatch(const Geom &g, const float *x, const float *wx, const float *wh,
+                      const Saved &sv, const float *dh, float *dx, float *dwx, float *dwh,
+                      float *db, void *ws, hipStream_t st)
+{
+    if (g_backward_path != 1 && sweep_bwd_supported(g)) {
+        const int rc = sweep_bwd(g, x, wx, wh, sv, dh, dx, dwx, dwh, db, ws, st);
+        if (rc != PLSTM_ENOTCORESIDENT && rc != PLSTM_EUNSUPPORTED) return rc;
+    }
+    return generic_backward(g, x, wx, wh, sv, dh, dx, dwx, dwh, db, ws, st);
 }
 
 }  // namespace plstm
@@ -40,5 +62,12 @@ extern "C" int pyramid_lstm_set_forward_path(int path)
 {
     if (path < 0 || path > 2) return PLSTM_EINVAL;
     plstm::g_forward_path = path;
+    return PLSTM_OK;
+}
+
+extern "C" int pyramid_lstm_set_backward_path(int path)
+{
+    if (path < 0 || path > 2) return PLSTM_EINVAL;
+    plstm::g_backward_path = path;
     return PLSTM_OK;
 }

@@ -330,18 +330,20 @@ inline int wgrad_chunks(const Geom &g) {
 size_t generic_forward_ws(const Geom &g, bool training)
 {
     Carve cv(nullptr);
-    cv.take<float>((size_t)kDirs * g.N * g.V * g.O);                  // h^d
-    if (!training) cv.take<float>((size_t)kDirs * g.N * g.V * g.O);   // c^d
+    if (!training) {
+        cv.take<float>(saved_state_count(g));   // h^d
+        cv.take<float>(saved_state_count(g));   // c^d
+    }
     return cv.off;
 }
 
 int generic_forward(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
-                    const void *b, void *h, float *gates, float *cell, void *ws,
-                    hipStream_t st)
+                    const void *b, void *h, const Saved *sv, void *ws, hipStream_t st)
 {
     Carve cv(ws);
-    float *hd = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
-    float *cellbuf = cell ? cell : cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
+    float *hd = sv ? sv->hd : cv.take<float>(saved_state_count(g));
+    float *cellbuf = sv ? sv->cell : cv.take<float>(saved_state_count(g));
+    float *gates = sv ? sv->gates : nullptr;
     const dim3 grid((max_plane(g) + kThreads - 1) / kThreads, g.O, kDirs * g.N);
     const int T = max_T(g);
     timing_begin("sweep_fwd_generic", st);
@@ -385,9 +387,10 @@ size_t generic_backward_ws(const Geom &g)
 }
 
 int generic_backward(const Geom &g, const float *x, const float *wx, const float *wh,
-                     const float *gates, const float *cell, const float *dh, float *dx,
-                     float *dwx, float *dwh, float *db, void *ws, hipStream_t st)
+                     const Saved &sv, const float *dh, float *dx, float *dwx, float *dwh,
+                     float *db, void *ws, hipStream_t st)
 {
+    const float *gates = sv.gates, *cell = sv.cell;
     const int G = 4 * g.O, KT = 9 * (g.C + g.O) + 1;
     Carve cv(ws);
     float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * G);
@@ -411,13 +414,17 @@ int generic_backward(const Geom &g, const float *x, const float *wx, const float
         g, nchunk, partial, dwx, dwh, db);
     PLSTM_LAUNCH_CHECK();
     timing_end(2, st);
-    if (dx) {
-        const long long cnt = (long long)g.N * g.V * g.C;
-        timing_begin("dx_generic", st);
-        k_dx<<<(unsigned)((cnt + kThreads - 1) / kThreads), kThreads, 0, st>>>(g, wx, dA, dx);
-        PLSTM_LAUNCH_CHECK();
-        timing_end(1, st);
-    }
+    if (dx) return generic_dx(g, wx, dA, dx, st);
+    return PLSTM_OK;
+}
+
+int generic_dx(const Geom &g, const float *wx, const float *dA, float *dx, hipStream_t st)
+{
+    const long long cnt = (long long)g.N * g.V * g.C;
+    timing_begin("dx_generic", st);
+    k_dx<<<(unsigned)((cnt + kThreads - 1) / kThreads), kThreads, 0, st>>>(g, wx, dA, dx);
+    PLSTM_LAUNCH_CHECK();
+    timing_end(1, st);
     return PLSTM_OK;
 }
 

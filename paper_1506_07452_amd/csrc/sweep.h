@@ -11,6 +11,14 @@ size_t sweep_fwd_ws(const Geom &g, bool training);
 int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, const float *b,
               float *hd, float *cell, float *gates, int *flags, hipStream_t st);
 
+// Persistent MFMA backward sweep + MFMA parameter gradients (sweep_bwd.hip):
+// O = 16, C <= 4, fp32.
+bool sweep_bwd_supported(const Geom &g);
+size_t sweep_bwd_ws(const Geom &g);
+int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, const Saved &sv,
+              const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
+              hipStream_t st);
+
 // h = sum of the six per-direction outputs (generic.hip).
 int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st);
 
@@ -19,10 +27,16 @@ size_t forward_ws(const Geom &g, int dtype, bool training);
 
 // Runs the layer forward on the fastest path that supports the shape.
 int forward_dispatch(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
-                     const void *b, void *h, float *gates, float *cell, void *ws,
-                     hipStream_t st);
+                     const void *b, void *h, const Saved *sv, void *ws, hipStream_t st);
+
+// Backward (fp32): workspace bytes and dispatch.
+size_t backward_ws(const Geom &g);
+int backward_dispatch(const Geom &g, const float *x, const float *wx, const float *wh,
+                      const Saved &sv, const float *dh, float *dx, float *dwx, float *dwh,
+                      float *db, void *ws, hipStream_t st);
 
 // 0 = automatic, 1 = generic path only, 2 = persistent MFMA sweep where supported.
 extern int g_forward_path;
+extern int g_backward_path;
 
 }  // namespace plstm

@@ -1,0 +1,487 @@
+// Backward of the layer for O = 16 hidden units, fp32: back-propagation
+// through the six sweeps (the chain rule through Section 2.3, Eq. (7)-(13),
+// in reverse plane order) and the parameter gradients.
+//
+// (1) k_sweep_bwd, persistent, one cooperative launch for all directions, on
+//     the forward's strip decomposition.  For plane t (last to first):
+//       gh   = dL/dh[plane t] + sum_taps dA_{t+1}[p - tap] W_h^T      (MFMA)
+//       gc   = gh o (1 - tanh^2 c_t) + gc_{t+1} f_{t+1}
+//       dA_o = gh tanh(c_t) o (1 - o)     dA_i = gc g i (1 - i)
+//       dA_g = gc i (1 - g^2)             dA_f = gc c_{t-1} f (1 - f)
+//     The transposed 3x3 convolution is an MFMA contraction of K = 9 x 64
+//     (tap, gate-unit) with units on M and pixels on N: lane l takes pixel
+//     l%16 and gate l/16 (16 units = 4 LDS reads of 16 bytes per tap) for the
+//     B operand, the transposed recurrent weights are the A operand, resident
+//     in VGPRs, and each lane ends with four consecutive units of one pixel,
+//     so every epilogue load and store is a 16-byte vector.  dA of every voxel
+//     is kept for (2) and for dL/dx.
+// (2) k_wgrad: dW = sum over voxels of dA (x) im2col(h_{t-1}, x_t, 1), an
+//     implicit GEMM per row segment of up to 64 voxels: M = 64 gate-units,
+//     N = 9 x 16 + 9 C + 1 columns, K = voxels; the previous plane's h^d and
+//     the input rows are staged in LDS and read with the tap offsets.  Each
+//     workgroup reduces a fixed set of segments of one direction; (3)
+//     k_wgrad_reduce sums the per-workgroup partials in a fixed order.
+#include "common.h"
+#include "strip_plan.h"
+#include "sweep.h"
+#include "timing.h"
+
+namespace plstm {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kO = 16;
+constexpr int kG = 4 * kO;
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kAS = 68;                // LDS floats per staged dA pixel (64 + 4 pad)
+constexpr int kMaxSpin = 1 << 21;
+constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unconstrained
+constexpr int kBatch = 4;              // staging loads in flight per thread
+
+__device__ inline float frcp(float v) { return __builtin_amdgcn_rcpf(v); }
+__device__ inline float ftanh(float a) { return 1.0f - 2.0f * frcp(__expf(2.0f * a) + 1.0f); }
+// floor(i / w) for 0 <= i < 2^20 (see the forward sweep for the error bound)
+__device__ inline int fdiv_floor(int i, float inv_w) { return (int)(((float)i + 0.5f) * inv_w); }
+
+struct BwdArgs {
+    Geom g;
+    const float *wh;
+    const float *gates, *cell;   // saved forward activations [6][N][V][64], [6][N][V][16]
+    const float *dh;             // dL/dh [N][V][16]
+    float *dA;                   // [6][N][V][64] gate pre-activation gradients
+    float *gc;                   // [6][N][V][16] dL/dc
+    int *flags, *err;
+    int nstrip[kDirs], first[kDirs], chunk_rows[kDirs], max_w[kDirs];
+};
+
+__global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
+{
+    extern __shared__ float smem[];
+    int d = 0;
+#pragma unroll
+    for (int k = 1; k < kDirs; ++k)
+        if ((int)blockIdx.x >= a.first[k]) d = k;
+    const int local = blockIdx.x - a.first[d];
+    const int ns = a.nstrip[d];
+    const int n = local / ns, strip = local % ns;
+    const DirGeom dg = a.g.dir[d];
+    const int q0 = (int)((long long)strip * dg.Q / ns);
+    const int q1 = (int)((long long)(strip + 1) * dg.Q / ns);
+    const int TQ = q1 - q0, W2 = TQ + 2;
+    const int nb_lo = strip > 0 ? (int)blockIdx.x - 1 : -1;
+    const int nb_hi = strip + 1 < ns ? (int)blockIdx.x + 1 : -1;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int q4 = lane >> 4, col = lane & 15;
+    const int chunk_rows = a.chunk_rows[d];
+    float *as = smem;
+
+    // A fragments: W_h^T with the tap's K index k = (s, q4) -> gate-unit 16 q4 + s.
+    float wa[9][16];
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+        for (int s = 0; s < 16; ++s)
+            wa[tap][s] = a.wh[(((long long)d * kG + 16 * q4 + s) * kO + col) * 9 + tap];
+
+    const long long V = a.g.V;
+    const long long dn = ((long long)d * a.g.N + n) * V;
+    const float *const gates_dn = a.gates + dn * kG;
+    const float *const cell_dn = a.cell + dn * kO;
+    float *const dA_dn = a.dA + dn * kG;
+    float *const gc_dn = a.gc + dn * kO;
+    const float *const dh_n = a.dh + (long long)n * V * kO;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const float inv_tq = 1.0f / (float)TQ, inv_w2 = 1.0f / (float)W2;
+
+    for (int r = 0; r < dg.T; ++r) {
+        const int t = dg.T - 1 - r;                   // plane processed at this step
+        const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+        const bool has_next = t + 1 < dg.T, has_prev = t > 0;
+        // ---- wait for the neighbours' dA_{t+1} --------------------------
+        if (r > 0) {
+            const int nb = threadIdx.x == 0 ? nb_lo : (threadIdx.x == 1 ? nb_hi : -1);
+            if (nb >= 0) {
+                int spins = 0;
+                while (__hip_atomic_load(&a.flags[nb], __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT) < r) {
+                    __builtin_amdgcn_s_sleep(1);
+                    if (++spins > kMaxSpin) {
+                        __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        break;
+                    }
+                    if ((spins & 1023) == 0 &&
+                        __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+                        break;
+                }
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            }
+            __syncthreads();
+        }
+        const int splane = s * ss;
+        const int nplane = has_next ? (s + dg.sign) * ss : splane;   // in-slice when read
+        const int pplane = has_prev ? (s - dg.sign) * ss : splane;
+        for (int r0 = 0; r0 < dg.P; r0 += chunk_rows) {
+            const int CH = min(chunk_rows, dg.P - r0);
+            const int npl = (CH + 2) * W2;
+            // ---- stage dA_{t+1} (chunk + halo), zero outside / at the end
+            const int nA = npl * 16;
+            for (int e0 = threadIdx.x; e0 < nA; e0 += kThreads * kBatch) {
+                f4 v[kBatch];
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    const int e = e0 + u * kThreads;
+                    const int pix = e >> 4, qd = e & 15;
+                    const int rr = fdiv_floor(pix, inv_w2);
+                    const int pr = rr + r0 - 1, pc = pix - rr * W2 + q0 - 1;
+                    const bool ok = e < nA && has_next && pr >= 0 && pr < dg.P && pc >= 0 &&
+                                    pc < dg.Q;
+                    const int off = ok ? (nplane + pr * sp + pc * sq) * kG + qd * 4 : 0;
+                    const f4 val = *(const f4 *)&dA_dn[off];
+                    v[u] = ok ? val : f4{0.0f, 0.0f, 0.0f, 0.0f};
+                }
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    const int e = e0 + u * kThreads;
+                    if (e < nA) *(f4 *)&as[(e >> 4) * kAS + (e & 15) * 4] = v[u];
+                }
+            }
+            __syncthreads();
+            // ---- 16-pixel tiles ------------------------------------------
+            const int npx = CH * TQ;
+            const int nmt = (npx + 15) >> 4;
+            for (int mt = wave; mt < nmt; mt += kWaves) {
+                const int pb = min(mt * 16 + col, npx - 1);      // this lane's pixel
+                const int rb = fdiv_floor(pb, inv_tq);
+                const int cb = pb - rb * TQ;
+                const int base = (rb + 1) * W2 + cb + 1;
+                const int vo = splane + (rb + r0) * sp + (cb + q0) * sq;
+                const int von = vo - splane + nplane, vop = vo - splane + pplane;
+                // epilogue operands, loaded ahead of the contraction
+                const f4 dh4 = *(const f4 *)&dh_n[vo * kO + 4 * q4];
+                const f4 gi = *(const f4 *)&gates_dn[vo * kG + 0 * kO + 4 * q4];
+                const f4 gf = *(const f4 *)&gates_dn[vo * kG + 1 * kO + 4 * q4];
+                const f4 gg = *(const f4 *)&gates_dn[vo * kG + 2 * kO + 4 * q4];
+                const f4 go = *(const f4 *)&gates_dn[vo * kG + 3 * kO + 4 * q4];
+                const f4 c4 = *(const f4 *)&cell_dn[vo * kO + 4 * q4];
+                const f4 gcn = *(const f4 *)&gc_dn[von * kO + 4 * q4];
+                const f4 fn = *(const f4 *)&gates_dn[von * kG + 1 * kO + 4 * q4];
+                const f4 cp = *(const f4 *)&cell_dn[vop * kO + 4 * q4];
+                __builtin_amdgcn_sched_barrier(0);
+                f4 acc[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) acc[k] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int tap = 0; tap < 9; ++tap) {
+                    // h_t at pixel p fed A_{t+1} at p - (tap offset)
+                    const int o = (tap / 3 - 1) * W2 + (tap % 3 - 1);
+                    const float *src = &as[(base - o) * kAS + 16 * q4];
+                    f4 bv[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) bv[k] = *(const f4 *)&src[4 * k];
+#pragma unroll
+                    for (int s2 = 0; s2 < 16; ++s2)
+                        acc[s2 & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            wa[tap][s2], bv[s2 >> 2][s2 & 3], acc[s2 & 3], 0, 0, 0);
+                }
+                if (mt * 16 + col >= npx) continue;
+                f4 dAi, dAf, dAg, dAo, gcv;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float gh = acc[0][i] + acc[1][i] + acc[2][i] + acc[3][i] + dh4[i];
+                    const float tc = ftanh(c4[i]);
+                    float gcs = gh * go[i] * (1.0f - tc * tc);
+                    if (has_next) gcs += gcn[i] * fn[i];
+                    const float cprev = has_prev ? cp[i] : 0.0f;
+                    gcv[i] = gcs;
+                    dAi[i] = gcs * gg[i] * gi[i] * (1.0f - gi[i]);
+                    dAf[i] = gcs * cprev * gf[i] * (1.0f - gf[i]);
+                    dAg[i] = gcs * gi[i] * (1.0f - gg[i] * gg[i]);
+                    dAo[i] = gh * tc * go[i] * (1.0f - go[i]);
+                }
+                *(f4 *)&dA_dn[vo * kG + 0 * kO + 4 * q4] = dAi;
+                *(f4 *)&dA_dn[vo * kG + 1 * kO + 4 * q4] = dAf;
+                *(f4 *)&dA_dn[vo * kG + 2 * kO + 4 * q4] = dAg;
+                *(f4 *)&dA_dn[vo * kG + 3 * kO + 4 * q4] = dAo;
+                *(f4 *)&gc_dn[vo * kO + 4 * q4] = gcv;
+            }
+            __syncthreads();
+        }
+        // ---- publish dA_t (see the forward sweep) -------------------------
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+            __hip_atomic_store(&a.flags[blockIdx.x], r + 1, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+// ---- parameter gradients ----------------------------------------------------
+constexpr int kSeg = 64;        // voxels per work unit (one row segment)
+constexpr int kHW = kSeg + 2;   // staged columns per row
+constexpr int kHP = 17;         // LDS floats per staged h pixel (16 + 1 pad)
+constexpr int kDP = 65;         // LDS floats per staged dA voxel (64 + 1 pad)
+
+struct WgradArgs {
+    Geom g;
+    const float *x, *hd, *dA;
+    float *partial;     // [6][bpd][64][KCp]
+    int bpd;            // workgroups per direction
+    int KCp;            // columns padded to 16: 144 + 9C + 1 -> multiple of 16
+};
+
+template <int C>
+__global__ void __launch_bounds__(kThreads, 1) k_wgrad(WgradArgs a)
+{
+    __shared__ float hs[3 * kHW * kHP];
+    __shared__ float xs[3 * kHW * C];
+    __shared__ float das[kSeg * kDP];
+    const int d = blockIdx.x / a.bpd, bi = blockIdx.x % a.bpd;
+    const DirGeom dg = a.g.dir[d];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int q4 = lane >> 4, col = lane & 15;
+    const int NT = a.KCp / 16;
+    const int m = wave & 3;                   // gate of this wave's output tiles
+    constexpr int kMaxT = 6;                  // N-tiles per wave: wave/4, +2, +4, ...
+    f4 acc[kMaxT];
+#pragma unroll
+    for (int i = 0; i < kMaxT; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    const int nseg = (dg.Q + kSeg - 1) / kSeg;
+    const int segw = (dg.Q + nseg - 1) / nseg;
+    const long long units = (long long)a.g.N * dg.T * dg.P * nseg;
+    const long long V = a.g.V;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+
+    for (long long u = bi; u < units; u += a.bpd) {
+        const int seg = (int)(u % nseg);
+        const long long rest = u / nseg;
+        const int p = (int)(rest % dg.P);
+        const int t = (int)((rest / dg.P) % dg.T);
+        const int n = (int)(rest / ((long long)dg.P * dg.T));
+        const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+        const int qs = seg * segw;
+        const int nq = min(segw, dg.Q - qs);
+        const long long dn = ((long long)d * a.g.N + n) * V;
+        const float *hd_dn = a.hd + dn * kO;
+        const float *dA_dn = a.dA + dn * kG;
+        const float *x_n = a.x + (long long)n * V * C;
+        const int splane = s * ss;
+        const int pplane = (t > 0 ? s - dg.sign : s) * ss;
+        // ---- stage h_{t-1} and x_t rows p-1..p+1, cols qs-1..qs+kSeg; dA row p
+        for (int e = threadIdx.x; e < 3 * kHW * 4; e += kThreads) {
+            const int pix = e >> 2, qd = e & 3;
+            const int rr = pix / kHW, cc = pix % kHW;
+            const int pr = p + rr - 1, pc = qs + cc - 1;
+            const bool ok = t > 0 && pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q && cc <= nq + 1;
+            const int off = ok ? (pplane + pr * sp + pc * sq) * kO + qd * 4 : 0;
+            const f4 v = *(const f4 *)&hd_dn[off];
+            const f4 w = ok ? v : f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) hs[pix * kHP + qd * 4 + k] = w[k];
+        }
+        for (int e = threadIdx.x; e < 3 * kHW * C; e += kThreads) {
+            const int pix = e / C, c = e % C;
+            const int rr = pix / kHW, cc = pix % kHW;
+            const int pr = p + rr - 1, pc = qs + cc - 1;
+            const bool ok = pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q && cc <= nq + 1;
+            const int off = ok ? (splane + pr * sp + pc * sq) * C + c : 0;
+            const float v = x_n[off];
+            xs[e] = ok ? v : 0.0f;
+        }
+        for (int e = threadIdx.x; e < kSeg * 16; e += kThreads) {
+            const int vx = e >> 4, qd = e & 15;
+            const bool ok = vx < nq;
+            const int off = ok ? (splane + p * sp + (qs + vx) * sq) * kG + qd * 4 : 0;
+            const f4 v = *(const f4 *)&dA_dn[off];
+            const f4 w = ok ? v : f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) das[vx * kDP + qd * 4 + k] = w[k];
+        }
+        __syncthreads();
+        // ---- D[gate-unit][column] += dA^T . im2col over the segment -------
+        const int ksteps = (nq + 3) >> 2;
+        for (int ks = 0; ks < ksteps; ++ks) {
+            const int vv = 4 * ks + q4;               // this lane's voxel (K index)
+            const float av = das[vv * kDP + m * 16 + col];
+#pragma unroll
+            for (int i = 0; i < kMaxT; ++i) {
+                const int nt = (wave >> 2) + 2 * i;
+                if (nt >= NT) break;
+                const int k = nt * 16 + col;          // this lane's column
+                float bv;
+                if (k < 144) {
+                    const int tap = nt;               // 16 columns per tap: unit = col
+                    bv = hs[((tap / 3) * kHW + vv + (tap % 3)) * kHP + col];
+                } else {
+                    const int kk = k - 144;
+                    if (kk < 9 * C) {
+                        const int tap = kk / C, c = kk - (kk / C) * C;
+                        bv = xs[((tap / 3) * kHW + vv + (tap % 3)) * C + c];
+                    } else {
+                        bv = kk == 9 * C ? 1.0f : 0.0f;   // bias column, then padding
+                    }
+                }
+                acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+    // ---- this workgroup's partial sums --------------------------------------
+    float *out = a.partial + ((long long)d * a.bpd + bi) * kG * a.KCp;
+#pragma unroll
+    for (int i = 0; i < kMaxT; ++i) {
+        const int nt = (wave >> 2) + 2 * i;
+        if (nt >= NT) break;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            out[(m * 16 + 4 * q4 + r) * a.KCp + nt * 16 + col] = acc[i][r];
+    }
+}
+
+// dW = sum of the per-workgroup partials in workgroup order.
+__global__ void __launch_bounds__(256)
+k_wgrad_reduce(int C, int bpd, int KCp, const float *__restrict__ partial,
+               float *__restrict__ dwx, float *__restrict__ dwh, float *__restrict__ db)
+{
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int KC = 144 + 9 * C + 1;
+    if (i >= kDirs * kG * KC) return;
+    const int k = i % KC;
+    const int gn = (i / KC) % kG;
+    const int d = i / (KC * kG);
+    float acc = 0.0f;
+    for (int b = 0; b < bpd; ++b) acc += partial[(((long long)d * bpd + b) * kG + gn) * KCp + k];
+    if (k < 144) {
+        const int tap = k / 16, j = k % 16;
+        dwh[(((long long)d * kG + gn) * kO + j) * 9 + tap] = acc;
+    } else if (k < 144 + 9 * C) {
+        const int kk = k - 144, tap = kk / C, c = kk % C;
+        dwx[(((long long)d * kG + gn) * C + c) * 9 + tap] = acc;
+    } else {
+        db[d * kG + gn] = acc;
+    }
+}
+
+__global__ void k_fill_zero(int *p, int n)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
+}
+
+StripCostModel bwd_model()
+{
+    StripCostModel m;
+    m.fixed_bytes = 0;
+    m.px_bytes = kAS * sizeof(float);
+    m.c_sync = 3.0;
+    m.c_tile = 2.9;
+    m.c_stage0 = 1.0;
+    m.c_stage_px = 0.008;
+    return m;
+}
+
+inline int wgrad_kcp(int C) { return (144 + 9 * C + 1 + 15) / 16 * 16; }
+constexpr int kWgradBlocksPerDir = 42;
+
+template <int C>
+int launch_wgrad(const Geom &g, const float *x, const float *hd, const float *dA, float *partial,
+                 hipStream_t st)
+{
+    WgradArgs wa;
+    wa.g = g;
+    wa.x = x; wa.hd = hd; wa.dA = dA;
+    wa.partial = partial;
+    wa.bpd = kWgradBlocksPerDir;
+    wa.KCp = wgrad_kcp(C);
+    k_wgrad<C><<<kDirs * kWgradBlocksPerDir, kThreads, 0, st>>>(wa);
+    PLSTM_LAUNCH_CHECK();
+    return PLSTM_OK;
+}
+
+}  // namespace
+
+bool sweep_bwd_supported(const Geom &g) { return g.O == kO && g.C >= 1 && g.C <= 4; }
+
+size_t sweep_bwd_ws(const Geom &g)
+{
+    Carve cv(nullptr);
+    cv.take<float>((size_t)kDirs * g.N * g.V * kG);                     // dA
+    cv.take<float>((size_t)kDirs * g.N * g.V * kO);                     // dL/dc
+    cv.take<int>(1024 + 1);                                              // flags + err
+    cv.take<float>((size_t)kDirs * kWgradBlocksPerDir * kG * wgrad_kcp(g.C));   // partials
+    return cv.off;
+}
+
+int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, const Saved &sv,
+              const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
+              hipStream_t st)
+{
+    const DevInfo di = device_info();
+    if (di.cus <= 0) return PLSTM_EHIP;
+    const size_t lds_limit = (size_t)(di.max_lds > 0 ? di.max_lds : 65536) - 1024;
+    const int budget = di.cus < 1024 ? di.cus : 1024;
+    const Plan pl = make_plan(g, budget, bwd_model(), lds_limit);
+    if (pl.blocks > budget) return PLSTM_EUNSUPPORTED;
+    for (int d = 0; d < kDirs; ++d)
+        if (pl.chunk_rows[d] < 1) return PLSTM_EUNSUPPORTED;
+
+    Carve cv(ws);
+    float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * kG);
+    float *gc = cv.take<float>((size_t)kDirs * g.N * g.V * kO);
+    int *flags = cv.take<int>(1024 + 1);
+    float *partial = cv.take<float>((size_t)kDirs * kWgradBlocksPerDir * kG * wgrad_kcp(g.C));
+
+    BwdArgs args;
+    args.g = g;
+    args.wh = wh;
+    args.gates = sv.gates; args.cell = sv.cell;
+    args.dh = dh;
+    args.dA = dA; args.gc = gc;
+    args.flags = flags; args.err = flags + 1024;
+    for (int d = 0; d < kDirs; ++d) {
+        args.nstrip[d] = pl.nstrip[d];
+        args.first[d] = pl.first[d];
+        args.chunk_rows[d] = pl.chunk_rows[d];
+        args.max_w[d] = pl.max_w[d];
+    }
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_bwd, kThreads, pl.lds) !=
+        hipSuccess)
+        return PLSTM_EHIP;
+    if ((long long)per_cu * di.cus < pl.blocks) return PLSTM_ENOTCORESIDENT;
+    (void)hipFuncSetAttribute((const void *)k_sweep_bwd,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
+
+    k_fill_zero<<<(1025 + 255) / 256, 256, 0, st>>>(flags, 1025);
+    PLSTM_LAUNCH_CHECK();
+    timing_begin("sweep_bwd_mfma", st);
+    void *kargs[] = {&args};
+    if (hipLaunchCooperativeKernel((const void *)k_sweep_bwd, dim3(pl.blocks), dim3(kThreads),
+                                   kargs, pl.lds, st) != hipSuccess)
+        return PLSTM_EHIP;
+    timing_end(1, st);
+
+    timing_begin("wgrad_mfma", st);
+    int rc;
+    switch (g.C) {
+    case 1: rc = launch_wgrad<1>(g, x, sv.hd, dA, partial, st); break;
+    case 2: rc = launch_wgrad<2>(g, x, sv.hd, dA, partial, st); break;
+    case 3: rc = launch_wgrad<3>(g, x, sv.hd, dA, partial, st); break;
+    default: rc = launch_wgrad<4>(g, x, sv.hd, dA, partial, st); break;
+    }
+    if (rc != PLSTM_OK) return rc;
+    const int nout = kDirs * kG * (144 + 9 * g.C + 1);
+    k_wgrad_reduce<<<(nout + 255) / 256, 256, 0, st>>>(g.C, kWgradBlocksPerDir, wgrad_kcp(g.C),
+                                                       partial, dwx, dwh, db);
+    PLSTM_LAUNCH_CHECK();
+    timing_end(2, st);
+    if (dx) return generic_dx(g, wx, dA, dx, st);
+    return PLSTM_OK;
+}
+
+}  // namespace plstm

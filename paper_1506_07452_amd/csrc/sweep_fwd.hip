@@ -30,6 +30,7 @@
 // pixels and the cell update needs no data exchange.
 #include "common.h"
 #include "sweep.h"
+#include "strip_plan.h"
 #include "timing.h"
 
 namespace plstm {
@@ -56,8 +57,8 @@ struct SweepArgs {
     int *err;           // set when a wait gives up
     int nstrip[kDirs];  // strips per (direction, batch element)
     int first[kDirs];   // first block of direction d
-    int chunk_rows;     // rows staged per LDS chunk
-    int max_w;          // widest strip (LDS layout)
+    int chunk_rows[kDirs];  // rows staged per LDS chunk, per direction
+    int max_w[kDirs];       // widest strip of each direction (LDS layout)
 };
 
 // Gate nonlinearities from exp and the hardware reciprocal (1 ulp each):
@@ -98,8 +99,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
     const int q4 = lane >> 4, col = lane & 15;
     constexpr int KXS = (9 * C + 3) / 4;    // MFMA k-steps of the input convolution
     float *wxs = smem;                       // [KXS][64 lanes][4 N-tiles] B fragments
+    const int chunk_rows = a.chunk_rows[d];
     float *hs = smem + KXS * 256;
-    float *xs = hs + (a.chunk_rows + 2) * (a.max_w + 2) * kHS;
+    float *xs = hs + (chunk_rows + 2) * (a.max_w[d] + 2) * kHS;
 
     // ---- weights as MFMA B fragments (resident for the whole sweep) -----
     const long long V = a.g.V;
@@ -172,8 +174,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
         }
         const int splane = s * ss, sprev_plane = sprev * ss;
         const int cplane = t > 0 ? sprev_plane : splane;
-        for (int r0 = 0; r0 < dg.P; r0 += a.chunk_rows) {
-            const int CH = min(a.chunk_rows, dg.P - r0);
+        for (int r0 = 0; r0 < dg.P; r0 += chunk_rows) {
+            const int CH = min(chunk_rows, dg.P - r0);
             const int npl = (CH + 2) * W2;            // staged pixels incl. halo
             // ---- stage h_{t-1} and x_t (zero outside the plane) ----------
             // Branch-free loads from clamped addresses, kBatch per thread in
@@ -305,81 +307,16 @@ __global__ void k_fill_zero(int *p, int n)
 }
 
 // ---- launch planning ------------------------------------------------------
-struct Plan {
-    int nstrip[kDirs];
-    int first[kDirs];
-    int blocks;
-    int chunk_rows;
-    int max_w;
-    size_t lds;
-};
-
-struct DevInfo {
-    int cus = 0;
-    int max_lds = 0;
-};
-
-DevInfo device_info()
+StripCostModel fwd_model(int C)
 {
-    static DevInfo cache[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DevInfo{};
-    DevInfo &di = cache[dev];
-    if (di.cus == 0) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
-            di.cus = v;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess)
-            di.max_lds = v;
-    }
-    return di;
-}
-
-// Strip counts that balance T_d x (pixels per strip x per-pixel cost +
-// per-step synchronisation cost) over the directions, within `budget` blocks.
-Plan make_plan(const Geom &g, int budget, int C, size_t lds_limit)
-{
-    Plan pl{};
-    const double px_cost = 1.0, sync_cost = 80.0;   // relative: ~one 16-px tile per sync
-    int ns[kDirs];
-    for (int d = 0; d < kDirs; ++d) ns[d] = 1;
-    auto cost = [&](int d, int k) {
-        const DirGeom &r = g.dir[d];
-        const double px = (double)r.P * ((r.Q + k - 1) / k);
-        return (double)r.T * (px * px_cost + sync_cost);
-    };
-    int used = kDirs * g.N;
-    while (true) {
-        int worst = -1;
-        double wc = -1.0;
-        for (int d = 0; d < kDirs; ++d) {
-            const double c = cost(d, ns[d]);
-            if (c > wc) { wc = c; worst = d; }
-        }
-        if (worst < 0 || ns[worst] >= g.dir[worst].Q || used + g.N > budget) break;
-        ++ns[worst];
-        used += g.N;
-    }
-    int first = 0, max_w = 1;
-    for (int d = 0; d < kDirs; ++d) {
-        pl.nstrip[d] = ns[d];
-        pl.first[d] = first;
-        first += ns[d] * g.N;
-        const int w = (g.dir[d].Q + ns[d] - 1) / ns[d];
-        max_w = w > max_w ? w : max_w;
-    }
-    pl.blocks = first;
-    pl.max_w = max_w;
-    // rows per chunk: fill the LDS budget
-    int maxP = 1;
-    for (int d = 0; d < kDirs; ++d) maxP = g.dir[d].P > maxP ? g.dir[d].P : maxP;
-    const size_t per_row = (size_t)(max_w + 2) * (kHS + C) * sizeof(float);
-    const size_t fixed = (size_t)((9 * C + 3) / 4) * 256 * sizeof(float);   // wx fragments
-    long long rows = (long long)((lds_limit - fixed) / per_row) - 2;
-    if (rows > maxP) rows = maxP;
-    pl.chunk_rows = rows < 1 ? 0 : (int)rows;
-    pl.lds = fixed + (size_t)(pl.chunk_rows + 2) * per_row;
-    return pl;
+    StripCostModel m;
+    m.fixed_bytes = (size_t)((9 * C + 3) / 4) * 256 * sizeof(float);   // wx fragments
+    m.px_bytes = (size_t)(kHS + C) * sizeof(float);                     // h + x per pixel
+    m.c_sync = 3.0;
+    m.c_tile = 3.2;
+    m.c_stage0 = 1.0;
+    m.c_stage_px = 0.0031;
+    return m;
 }
 
 template <int C>
@@ -409,9 +346,11 @@ bool sweep_fwd_supported(const Geom &g, int dtype)
 size_t sweep_fwd_ws(const Geom &g, bool training)
 {
     Carve cv(nullptr);
-    cv.take<float>((size_t)kDirs * g.N * g.V * kO);                 // h^d
-    if (!training) cv.take<float>((size_t)kDirs * g.N * g.V * kO);  // c^d
-    cv.take<int>(1024 + 1);                                          // flags + err
+    if (!training) {
+        cv.take<float>(saved_state_count(g));   // h^d
+        cv.take<float>(saved_state_count(g));   // c^d
+    }
+    cv.take<int>(1024 + 1);                     // flags + err
     return cv.off;
 }
 
@@ -422,8 +361,10 @@ int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     if (di.cus <= 0) return PLSTM_EHIP;
     const size_t lds_limit = (size_t)(di.max_lds > 0 ? di.max_lds : 65536) - 1024;
     const int budget = di.cus < 1024 ? di.cus : 1024;
-    const Plan pl = make_plan(g, budget, g.C, lds_limit);
-    if (pl.blocks > budget || pl.chunk_rows < 1) return PLSTM_EUNSUPPORTED;
+    const Plan pl = make_plan(g, budget, fwd_model(g.C), lds_limit);
+    if (pl.blocks > budget) return PLSTM_EUNSUPPORTED;
+    for (int d = 0; d < kDirs; ++d)
+        if (pl.chunk_rows[d] < 1) return PLSTM_EUNSUPPORTED;
 
     SweepArgs args;
     args.g = g;
@@ -435,8 +376,10 @@ int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, c
         args.nstrip[d] = pl.nstrip[d];
         args.first[d] = pl.first[d];
     }
-    args.chunk_rows = pl.chunk_rows;
-    args.max_w = pl.max_w;
+    for (int d = 0; d < kDirs; ++d) {
+        args.chunk_rows[d] = pl.chunk_rows[d];
+        args.max_w[d] = pl.max_w[d];
+    }
 
     k_fill_zero<<<(1025 + 255) / 256, 256, 0, st>>>(flags, 1025);
     PLSTM_LAUNCH_CHECK();

@@ -134,3 +134,14 @@ def test_binding_refuses_host_tensors():
     with pytest.raises((ValueError, RuntimeError)):
         P.pyramid_fc_tanh_forward(x.view(-1, 1), torch.zeros(1, 1), torch.zeros(1),
                                   torch.zeros(8, 1))
+
+
+def test_path_knobs_and_timing_without_gpu():
+    for fn in (P.pyramid_lstm_set_forward_path, P.pyramid_lstm_set_backward_path):
+        for v in (1, 2, 0):
+            fn(v)
+        with pytest.raises(P.PyramidLSTMError):
+            fn(3)
+    P.pyramid_lstm_timing_enable(True)
+    assert P.pyramid_lstm_timing_read() == {}
+    P.pyramid_lstm_timing_enable(False)

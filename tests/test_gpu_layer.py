@@ -74,6 +74,49 @@ def test_generic_path_forward_matches_oracle(shape, generic_path):
     assert normwise(host(h), ref) <= TOL["f32"]
 
 
+@pytest.fixture
+def generic_backward():
+    """Run the backward on the generic per-plane path only."""
+    P.pyramid_lstm_set_backward_path(1)
+    yield
+    P.pyramid_lstm_set_backward_path(0)
+
+
+@pytest.mark.parametrize("shape", [(1, 5, 37, 29, 3, 16), (2, 4, 9, 7, 1, 16)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_generic_path_backward_matches_oracle(shape, generic_backward):
+    inst = instance(shape, 3100 + sum(shape))
+    L = inst.layers[0]
+    dh = synth.upstream_grad(inst.x.shape[:-1] + (shape[-1],), 17 + sum(shape))
+    ref = oracle.backward(inst.x, L.wx, L.wh, L.b, dh)
+    say("backward generic", shape)
+    x, Ld = dev(inst.x), layer_dev(L)
+    h, saved = layer_forward(x, Ld, training=True)
+    P.pyramid_lstm_timing_enable(True)
+    grads = layer_backward(x, Ld, saved, dev(dh))
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    assert "sweep_bwd_generic" in phases and "sweep_bwd_mfma" not in phases
+    for name, got in zip(("dx", "dwx", "dwh", "db"), grads):
+        assert normwise(host(got), ref[name]) <= TOL["f32"], name
+
+
+def test_mfma_backward_runs_for_o16():
+    """The persistent MFMA reverse sweep and MFMA parameter gradients are the
+    path taken for 16 hidden units."""
+    inst = instance((1, 12, 40, 36, 3, 16), 77)
+    L = inst.layers[0]
+    x, Ld = dev(inst.x), layer_dev(L)
+    say("mfma backward path")
+    h, saved = layer_forward(x, Ld, training=True)
+    P.pyramid_lstm_timing_enable(True)
+    layer_backward(x, Ld, saved, torch.ones_like(h))
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    assert phases.get("sweep_bwd_mfma", (0, 0))[1] == 1, phases
+    assert "wgrad_mfma" in phases and "sweep_bwd_generic" not in phases
+
+
 @pytest.mark.parametrize("cfg", [2, 3])
 def test_mfma_sweep_runs_for_the_o16_workloads(cfg):
     """The persistent MFMA sweep (one launch) is the path taken for the
@@ -102,7 +145,8 @@ def test_forward_bf16_matches_oracle(shape):
     assert err <= TOL["bf16"], err
 
 
-@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("shape", SHAPES + [(3, 6, 20, 18, 2, 16), (1, 7, 130, 90, 1, 16)],
+                         ids=lambda s: "x".join(map(str, s)))
 def test_training_forward_and_backward_match_oracle(shape):
     inst = instance(shape, 3000 + sum(shape))
     L = inst.layers[0]

@@ -174,6 +174,142 @@ k_loss_reduce(long long M, int nblk, const float *__restrict__ lossp, float *__r
     if (threadIdx.x == 0) *loss = red[0] / (float)M;
 }
 
+// ---- one thread per row, weights (a chunk of up to kOC outputs) in LDS ----
+// Used when the weight chunk fits LDS (Cin * kOC floats); every thread reads
+// its input row once per chunk and keeps kOC accumulators in registers.
+constexpr int kOC = 32;
+constexpr int kRowWMax = 16384;   // floats of W staged per block (64 KB)
+
+inline bool rows_ok(int Cin, int width) { return (long long)Cin * width <= kRowWMax; }
+
+template <typename TS>
+__global__ void __launch_bounds__(kThreads)
+k_fc_tanh_rows(long long M, int Cin, int Cout, const TS *__restrict__ x, const TS *__restrict__ w,
+               const TS *__restrict__ b, TS *__restrict__ y)
+{
+    extern __shared__ float sw[];                 // [oc][Cin] then bias [oc]
+    const int o0 = blockIdx.y * kOC;
+    const int oc = min(kOC, Cout - o0);
+    for (int e = threadIdx.x; e < oc * Cin; e += kThreads)
+        sw[e] = Store<TS>::load(w, (long long)o0 * Cin + e);
+    float *sb = sw + oc * Cin;
+    for (int e = threadIdx.x; e < oc; e += kThreads) sb[e] = Store<TS>::load(b, o0 + e);
+    __syncthreads();
+    const long long m = (long long)blockIdx.x * kThreads + threadIdx.x;
+    if (m >= M) return;
+    float acc[kOC];
+#pragma unroll
+    for (int j = 0; j < kOC; ++j) acc[j] = j < oc ? sb[j] : 0.0f;
+    const TS *xr = x + m * Cin;
+    for (int c = 0; c < Cin; ++c) {
+        const float xv = Store<TS>::load(xr, c);
+#pragma unroll
+        for (int j = 0; j < kOC; ++j)
+            if (j < oc) acc[j] += xv * sw[j * Cin + c];
+    }
+    TS *yr = y + m * Cout + o0;
+#pragma unroll
+    for (int j = 0; j < kOC; ++j)
+        if (j < oc) Store<TS>::store(yr, j, tanhf(acc[j]));
+}
+
+// dx[m][i0 + i] = sum_o grad[m][o] w[o][i0 + i] for a chunk of kOC inputs.
+__global__ void __launch_bounds__(kThreads)
+k_fc_dx_rows(long long M, int Cin, int Cout, RowGrad rg, const float *__restrict__ w,
+             float *__restrict__ dx)
+{
+    extern __shared__ float sw[];                 // [Cout][ic]
+    const int i0 = blockIdx.y * kOC;
+    const int ic = min(kOC, Cin - i0);
+    for (int e = threadIdx.x; e < Cout * ic; e += kThreads) {
+        const int o = e / ic, i = e % ic;
+        sw[e] = w[(long long)o * Cin + i0 + i];
+    }
+    __syncthreads();
+    const long long m = (long long)blockIdx.x * kThreads + threadIdx.x;
+    if (m >= M) return;
+    float acc[kOC];
+#pragma unroll
+    for (int j = 0; j < kOC; ++j) acc[j] = 0.0f;
+    for (int o = 0; o < Cout; ++o) {
+        const float gv = rg.at(m * Cout + o);
+#pragma unroll
+        for (int j = 0; j < kOC; ++j)
+            if (j < ic) acc[j] += gv * sw[o * ic + j];
+    }
+#pragma unroll
+    for (int j = 0; j < kOC; ++j)
+        if (j < ic) dx[m * Cin + i0 + j] = acc[j];
+}
+
+// Softmax head, one thread per row: logits in registers (K <= 16), the
+// label's probability picked by comparison (no dynamically indexed arrays).
+template <typename TS>
+__global__ void __launch_bounds__(kThreads)
+k_softmax_rows(long long M, int Cin, int K, const TS *__restrict__ x, const TS *__restrict__ w,
+               const TS *__restrict__ b, const int32_t *__restrict__ labels,
+               float *__restrict__ p, float *__restrict__ dlogits, float *__restrict__ lossp)
+{
+    extern __shared__ float sw[];                 // [K][Cin] then bias [K]
+    for (int e = threadIdx.x; e < K * Cin; e += kThreads) sw[e] = Store<TS>::load(w, e);
+    float *sb = sw + K * Cin;
+    for (int e = threadIdx.x; e < K; e += kThreads) sb[e] = Store<TS>::load(b, e);
+    __syncthreads();
+    const long long m = (long long)blockIdx.x * kThreads + threadIdx.x;
+    float l = 0.0f;
+    if (m < M) {
+        float z[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) z[k] = k < K ? sb[k] : 0.0f;
+        const TS *xr = x + m * Cin;
+        for (int c = 0; c < Cin; ++c) {
+            const float xv = Store<TS>::load(xr, c);
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                if (k < K) z[k] += xv * sw[k * Cin + c];
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (k < K) mx = fmaxf(mx, z[k]);
+        float sum = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            z[k] = k < K ? __expf(z[k] - mx) : 0.0f;
+            sum += z[k];
+        }
+        const float inv = 1.0f / sum;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (k < K) p[m * K + k] = z[k] * inv;
+        if (labels) {
+            // An out-of-range label poisons the loss with NaN.
+            const int lab = labels[m];
+            const bool ok = lab >= 0 && lab < K;
+            float pl = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                if (k == lab) pl = z[k] * inv;
+            l = ok ? -logf(pl) : NAN;
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                if (k < K)
+                    dlogits[m * K + k] =
+                        ok ? (z[k] * inv - (k == lab ? 1.0f : 0.0f)) / (float)M : NAN;
+        }
+    }
+    if (labels) {
+        __shared__ float red[kThreads];
+        red[threadIdx.x] = l;
+        __syncthreads();
+        for (int off = kThreads / 2; off > 0; off >>= 1) {
+            if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) lossp[blockIdx.x] = red[0];
+    }
+}
+
 inline long long fc_chunk_len(long long M) {
     long long len = 8192;
     if ((M + len - 1) / len > 4096) len = (M + 4095) / 4096;
@@ -185,6 +321,19 @@ inline int fc_chunks(long long M) {
 }
 
 inline unsigned blocks_for(long long n) { return (unsigned)((n + kThreads - 1) / kThreads); }
+
+int fc_dx(long long M, int Cin, int Cout, RowGrad rg, const float *w, float *dx, hipStream_t st)
+{
+    if (rows_ok(Cout, kOC)) {
+        const dim3 grid(blocks_for(M), (Cin + kOC - 1) / kOC);
+        k_fc_dx_rows<<<grid, kThreads, (size_t)Cout * kOC * sizeof(float), st>>>(M, Cin, Cout, rg,
+                                                                               w, dx);
+    } else {
+        k_fc_dx<<<blocks_for(M * Cin), kThreads, 0, st>>>(M, Cin, Cout, rg, w, dx);
+    }
+    PLSTM_LAUNCH_CHECK();
+    return PLSTM_OK;
+}
 
 int fc_wgrad(long long M, int Cin, int Cout, RowGrad rg, const float *x, float *dw, float *db,
              float *partial, hipStream_t st)
@@ -213,6 +362,19 @@ size_t fc_ws(long long M, int Cin, int Cout)
 int fc_tanh_forward(long long M, int Cin, int Cout, int dtype, const void *x, const void *w,
                     const void *b, void *y, hipStream_t st)
 {
+    if (rows_ok(Cin + 1, kOC)) {
+        const dim3 grid(blocks_for(M), (Cout + kOC - 1) / kOC);
+        const size_t lds = (size_t)kOC * (Cin + 1) * sizeof(float);
+        if (dtype == PLSTM_BF16)
+            k_fc_tanh_rows<uint16_t><<<grid, kThreads, lds, st>>>(
+                M, Cin, Cout, (const uint16_t *)x, (const uint16_t *)w, (const uint16_t *)b,
+                (uint16_t *)y);
+        else
+            k_fc_tanh_rows<float><<<grid, kThreads, lds, st>>>(
+                M, Cin, Cout, (const float *)x, (const float *)w, (const float *)b, (float *)y);
+        PLSTM_LAUNCH_CHECK();
+        return PLSTM_OK;
+    }
     const unsigned nb = blocks_for(M * Cout);
     if (dtype == PLSTM_BF16)
         k_fc_tanh<uint16_t><<<nb, kThreads, 0, st>>>(M, Cin, Cout, (const uint16_t *)x,
@@ -234,8 +396,8 @@ int fc_tanh_backward(long long M, int Cin, int Cout, const float *x, const float
     float *partial = cv.take<float>((size_t)fc_chunks(M) * Cout * (Cin + 1));
     const RowGrad rg{y, dy};
     if (dx) {
-        k_fc_dx<<<blocks_for(M * Cin), kThreads, 0, st>>>(M, Cin, Cout, rg, w, dx);
-        PLSTM_LAUNCH_CHECK();
+        const int rc = fc_dx(M, Cin, Cout, rg, w, dx, st);
+        if (rc != PLSTM_OK) return rc;
     }
     return fc_wgrad(M, Cin, Cout, rg, x, dw, db, partial, st);
 }
@@ -249,13 +411,24 @@ int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void
     float *dlogits = cv.take<float>((size_t)M * K);
     float *lossp = cv.take<float>((size_t)blocks_for(M));
     const unsigned nb = blocks_for(M);
-    if (dtype == PLSTM_BF16)
+    if (rows_ok(Cin + 1, K)) {
+        const size_t lds = (size_t)K * (Cin + 1) * sizeof(float);
+        if (dtype == PLSTM_BF16)
+            k_softmax_rows<uint16_t><<<nb, kThreads, lds, st>>>(
+                M, Cin, K, (const uint16_t *)x, (const uint16_t *)w, (const uint16_t *)b, labels,
+                p, dlogits, lossp);
+        else
+            k_softmax_rows<float><<<nb, kThreads, lds, st>>>(
+                M, Cin, K, (const float *)x, (const float *)w, (const float *)b, labels, p,
+                dlogits, lossp);
+    } else if (dtype == PLSTM_BF16) {
         k_softmax<uint16_t><<<nb, kThreads, 0, st>>>(M, Cin, K, (const uint16_t *)x,
                                                       (const uint16_t *)w, (const uint16_t *)b,
                                                       labels, p, dlogits, lossp);
-    else
+    } else {
         k_softmax<float><<<nb, kThreads, 0, st>>>(M, Cin, K, (const float *)x, (const float *)w,
                                                    (const float *)b, labels, p, dlogits, lossp);
+    }
     PLSTM_LAUNCH_CHECK();
     if (!labels) return PLSTM_OK;
     k_loss_reduce<<<1, kThreads, 0, st>>>(M, (int)nb, lossp, loss);
@@ -263,8 +436,8 @@ int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void
     if (!dw) return PLSTM_OK;
     const RowGrad rg{nullptr, dlogits};
     if (dx) {
-        k_fc_dx<<<blocks_for(M * Cin), kThreads, 0, st>>>(M, Cin, K, rg, (const float *)w, dx);
-        PLSTM_LAUNCH_CHECK();
+        const int rc = fc_dx(M, Cin, K, rg, (const float *)w, dx, st);
+        if (rc != PLSTM_OK) return rc;
     }
     return fc_wgrad(M, Cin, K, rg, (const float *)x, dw, db, partial, st);
 }

@@ -234,6 +234,155 @@ struct WgradArgs {
     int KCp;            // columns padded to 16: 144 + 9C + 1 -> multiple of 16
 };
 
+// One work unit: row p of plane t (batch element n), columns qs .. qs+nq-1.
+struct WgUnit {
+    int n, t, p, qs, nq;
+};
+
+__device__ inline WgUnit wg_unit(const DirGeom &dg, int nseg, int segw, long long u)
+{
+    WgUnit w;
+    const int seg = (int)(u % nseg);
+    const long long rest = u / nseg;
+    w.p = (int)(rest % dg.P);
+    w.t = (int)((rest / dg.P) % dg.T);
+    w.n = (int)(rest / ((long long)dg.P * dg.T));
+    w.qs = seg * segw;
+    w.nq = min(segw, dg.Q - w.qs);
+    return w;
+}
+
+// Staged arrays of a unit, each with a fixed number of elements per thread
+// (loads from clamped addresses, no divergent branches): the three h_{t-1}
+// rows as float4s, the dA row as float4s and the three x rows as scalars.
+constexpr int kNH = 3 * kHW * 4;                           // float4s of the h rows
+constexpr int kNA = kSeg * 16;                             // float4s of the dA row
+constexpr int kRH = (kNH + kThreads - 1) / kThreads;
+constexpr int kRA = (kNA + kThreads - 1) / kThreads;
+template <int C> struct WgStage {
+    static constexpr int kNX = 3 * kHW * C;
+    static constexpr int kRX = (kNX + kThreads - 1) / kThreads;
+    f4 h[kRH];
+    f4 a[kRA];
+    float x[kRX];
+};
+
+template <int C>
+__device__ inline void wg_issue(const WgradArgs &a, const DirGeom &dg, int d, const WgUnit &w,
+                                WgStage<C> &st)
+{
+    const long long V = a.g.V;
+    const long long dn = ((long long)d * a.g.N + w.n) * V;
+    const float *hd_dn = a.hd + dn * kO;
+    const float *dA_dn = a.dA + dn * kG;
+    const float *x_n = a.x + (long long)w.n * V * C;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int s = dg.sign > 0 ? w.t : dg.T - 1 - w.t;
+    const int splane = s * ss;
+    const int pplane = (w.t > 0 ? s - dg.sign : s) * ss;
+#pragma unroll
+    for (int k = 0; k < kRH; ++k) {
+        const int e = min((int)threadIdx.x + k * kThreads, kNH - 1);
+        const int pix = e >> 2, qd = e & 3;
+        const int rr = pix / kHW, cc = pix - (pix / kHW) * kHW;
+        const int pr = w.p + rr - 1, pc = w.qs + cc - 1;
+        const bool ok = w.t > 0 && pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q;
+        const int off = ok ? (pplane + pr * sp + pc * sq) * kO + qd * 4 : 0;
+        const f4 val = *(const f4 *)&hd_dn[off];
+        st.h[k] = ok ? val : f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+#pragma unroll
+    for (int k = 0; k < kRA; ++k) {
+        const int e = (int)threadIdx.x + k * kThreads;     // kNA is a multiple of kThreads
+        const int vx = e >> 4, qd = e & 15;
+        const bool ok = vx < w.nq;
+        const int off = ok ? (splane + w.p * sp + (w.qs + vx) * sq) * kG + qd * 4 : 0;
+        const f4 val = *(const f4 *)&dA_dn[off];
+        st.a[k] = ok ? val : f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+#pragma unroll
+    for (int k = 0; k < WgStage<C>::kRX; ++k) {
+        const int e = min((int)threadIdx.x + k * kThreads, WgStage<C>::kNX - 1);
+        const int pix = e / C, c = e - (e / C) * C;
+        const int rr = pix / kHW, cc = pix - (pix / kHW) * kHW;
+        const int pr = w.p + rr - 1, pc = w.qs + cc - 1;
+        const bool ok = pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q;
+        const int off = ok ? (splane + pr * sp + pc * sq) * C + c : 0;
+        const float val = x_n[off];
+        st.x[k] = ok ? val : 0.0f;
+    }
+}
+
+template <int C>
+__device__ inline void wg_commit(const WgStage<C> &st, float *hs, float *das, float *xs)
+{
+#pragma unroll
+    for (int k = 0; k < kRH; ++k) {
+        const int e = (int)threadIdx.x + k * kThreads;
+        if (e < kNH) {
+            const int pix = e >> 2, qd = e & 3;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) hs[pix * kHP + qd * 4 + j] = st.h[k][j];
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kRA; ++k) {
+        const int e = (int)threadIdx.x + k * kThreads;
+        const int vx = e >> 4, qd = e & 15;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) das[vx * kDP + qd * 4 + j] = st.a[k][j];
+    }
+#pragma unroll
+    for (int k = 0; k < WgStage<C>::kRX; ++k) {
+        const int e = (int)threadIdx.x + k * kThreads;
+        if (e < WgStage<C>::kNX) xs[e] = st.x[k];
+    }
+}
+
+// Column nt*16 + col of the im2col row of voxel vv: h_{t-1} (taps 0..8 hold
+// 16 units each), then the input taps x channels, the bias column, padding.
+template <int C>
+__device__ inline float wg_col(const float *hs, const float *xs, int nt, int vv, int col)
+{
+    if (nt < 9) return hs[((nt / 3) * kHW + vv + (nt % 3)) * kHP + col];
+    const int kk = (nt - 9) * 16 + col;
+    if (kk < 9 * C) {
+        const int tap = kk / C, c = kk - (kk / C) * C;
+        return xs[((tap / 3) * kHW + vv + (tap % 3)) * C + c];
+    }
+    return kk == 9 * C ? 1.0f : 0.0f;
+}
+
+// Output tiles of a wave: gate m = wave % 4 and N-tiles NT0, NT0 + 2, ...;
+// the compile-time start lets every tile index, and so every branch on it,
+// resolve at compile time.
+template <int C, int NT0>
+__device__ inline void wg_tiles(const float *hs, const float *xs, const float *das, int nq,
+                                int m, int q4, int col, f4 (&acc)[6])
+{
+    constexpr int NT = (144 + 9 * C + 1 + 15) / 16;
+    constexpr int NTW = (NT - NT0 + 1) / 2;          // tiles of this wave
+    // Four k-steps (16 voxels) per iteration: all their LDS reads are issued
+    // before their MFMAs.  Voxels past the segment have dA = 0 in LDS (and
+    // staged neighbours), so rounding up to 16 voxels adds only zeros.
+    const int kgroups = (nq + 15) >> 4;
+    for (int kg = 0; kg < kgroups; ++kg) {
+        float av[4], bv[4][NTW];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int vv = 16 * kg + 4 * u + q4;
+            av[u] = das[vv * kDP + m * 16 + col];
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) bv[u][i] = wg_col<C>(hs, xs, NT0 + 2 * i, vv, col);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int i = 0; i < NTW; ++i)
+                acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u][i], acc[i], 0, 0, 0);
+    }
+}
+
 template <int C>
 __global__ void __launch_bounds__(kThreads, 1) k_wgrad(WgradArgs a)
 {
@@ -242,100 +391,41 @@ __global__ void __launch_bounds__(kThreads, 1) k_wgrad(WgradArgs a)
     __shared__ float das[kSeg * kDP];
     const int d = blockIdx.x / a.bpd, bi = blockIdx.x % a.bpd;
     const DirGeom dg = a.g.dir[d];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int q4 = lane >> 4, col = lane & 15;
-    const int NT = a.KCp / 16;
+    constexpr int NT = (144 + 9 * C + 1 + 15) / 16;
     const int m = wave & 3;                   // gate of this wave's output tiles
-    constexpr int kMaxT = 6;                  // N-tiles per wave: wave/4, +2, +4, ...
-    f4 acc[kMaxT];
+    const int nt0 = wave >> 2;                // first N-tile; then every second one
+    f4 acc[6];
 #pragma unroll
-    for (int i = 0; i < kMaxT; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int i = 0; i < 6; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
     const int nseg = (dg.Q + kSeg - 1) / kSeg;
     const int segw = (dg.Q + nseg - 1) / nseg;
     const long long units = (long long)a.g.N * dg.T * dg.P * nseg;
-    const long long V = a.g.V;
-    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
 
-    for (long long u = bi; u < units; u += a.bpd) {
-        const int seg = (int)(u % nseg);
-        const long long rest = u / nseg;
-        const int p = (int)(rest % dg.P);
-        const int t = (int)((rest / dg.P) % dg.T);
-        const int n = (int)(rest / ((long long)dg.P * dg.T));
-        const int s = dg.sign > 0 ? t : dg.T - 1 - t;
-        const int qs = seg * segw;
-        const int nq = min(segw, dg.Q - qs);
-        const long long dn = ((long long)d * a.g.N + n) * V;
-        const float *hd_dn = a.hd + dn * kO;
-        const float *dA_dn = a.dA + dn * kG;
-        const float *x_n = a.x + (long long)n * V * C;
-        const int splane = s * ss;
-        const int pplane = (t > 0 ? s - dg.sign : s) * ss;
-        // ---- stage h_{t-1} and x_t rows p-1..p+1, cols qs-1..qs+kSeg; dA row p
-        for (int e = threadIdx.x; e < 3 * kHW * 4; e += kThreads) {
-            const int pix = e >> 2, qd = e & 3;
-            const int rr = pix / kHW, cc = pix % kHW;
-            const int pr = p + rr - 1, pc = qs + cc - 1;
-            const bool ok = t > 0 && pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q && cc <= nq + 1;
-            const int off = ok ? (pplane + pr * sp + pc * sq) * kO + qd * 4 : 0;
-            const f4 v = *(const f4 *)&hd_dn[off];
-            const f4 w = ok ? v : f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int k = 0; k < 4; ++k) hs[pix * kHP + qd * 4 + k] = w[k];
-        }
-        for (int e = threadIdx.x; e < 3 * kHW * C; e += kThreads) {
-            const int pix = e / C, c = e % C;
-            const int rr = pix / kHW, cc = pix % kHW;
-            const int pr = p + rr - 1, pc = qs + cc - 1;
-            const bool ok = pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q && cc <= nq + 1;
-            const int off = ok ? (splane + pr * sp + pc * sq) * C + c : 0;
-            const float v = x_n[off];
-            xs[e] = ok ? v : 0.0f;
-        }
-        for (int e = threadIdx.x; e < kSeg * 16; e += kThreads) {
-            const int vx = e >> 4, qd = e & 15;
-            const bool ok = vx < nq;
-            const int off = ok ? (splane + p * sp + (qs + vx) * sq) * kG + qd * 4 : 0;
-            const f4 v = *(const f4 *)&dA_dn[off];
-            const f4 w = ok ? v : f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int k = 0; k < 4; ++k) das[vx * kDP + qd * 4 + k] = w[k];
-        }
+    // Software pipeline: the next unit's loads are in flight while the
+    // current unit's MFMAs run.
+    WgStage<C> stage;
+    long long u = bi;
+    if (u < units) wg_issue<C>(a, dg, d, wg_unit(dg, nseg, segw, u), stage);
+    for (; u < units; u += a.bpd) {
+        const WgUnit w = wg_unit(dg, nseg, segw, u);
+        wg_commit<C>(stage, hs, das, xs);
         __syncthreads();
-        // ---- D[gate-unit][column] += dA^T . im2col over the segment -------
-        const int ksteps = (nq + 3) >> 2;
-        for (int ks = 0; ks < ksteps; ++ks) {
-            const int vv = 4 * ks + q4;               // this lane's voxel (K index)
-            const float av = das[vv * kDP + m * 16 + col];
-#pragma unroll
-            for (int i = 0; i < kMaxT; ++i) {
-                const int nt = (wave >> 2) + 2 * i;
-                if (nt >= NT) break;
-                const int k = nt * 16 + col;          // this lane's column
-                float bv;
-                if (k < 144) {
-                    const int tap = nt;               // 16 columns per tap: unit = col
-                    bv = hs[((tap / 3) * kHW + vv + (tap % 3)) * kHP + col];
-                } else {
-                    const int kk = k - 144;
-                    if (kk < 9 * C) {
-                        const int tap = kk / C, c = kk - (kk / C) * C;
-                        bv = xs[((tap / 3) * kHW + vv + (tap % 3)) * C + c];
-                    } else {
-                        bv = kk == 9 * C ? 1.0f : 0.0f;   // bias column, then padding
-                    }
-                }
-                acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i], 0, 0, 0);
-            }
-        }
+        if (u + a.bpd < units) wg_issue<C>(a, dg, d, wg_unit(dg, nseg, segw, u + a.bpd), stage);
+        if (nt0 == 0)
+            wg_tiles<C, 0>(hs, xs, das, w.nq, m, q4, col, acc);
+        else
+            wg_tiles<C, 1>(hs, xs, das, w.nq, m, q4, col, acc);
         __syncthreads();
     }
     // ---- this workgroup's partial sums --------------------------------------
     float *out = a.partial + ((long long)d * a.bpd + bi) * kG * a.KCp;
 #pragma unroll
-    for (int i = 0; i < kMaxT; ++i) {
-        const int nt = (wave >> 2) + 2 * i;
+    for (int i = 0; i < 6; ++i) {
+        const int nt = nt0 + 2 * i;
         if (nt >= NT) break;
 #pragma unroll
         for (int r = 0; r < 4; ++r)

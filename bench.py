@@ -91,6 +91,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-crop", default="48x120x120")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first copy 1 GiB device-to-device three times (a plain copy kernel "
+                         "of known size, to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the six sweeps of a layer run concurrently "
@@ -118,6 +121,13 @@ def main():
     O = wl.hidden[0]
     V = N * D * H * W
     torch.cuda.init()
+    if args.copy_calibration:
+        src = torch.zeros(1 << 28, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     x = dev(inst.x)
     layers = [layer_dev(L) for L in inst.layers]
     fcs = [(dev(w), dev(b)) for w, b in inst.fcs]

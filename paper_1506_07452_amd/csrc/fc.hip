@@ -174,96 +174,153 @@ k_loss_reduce(long long M, int nblk, const float *__restrict__ lossp, float *__r
     if (threadIdx.x == 0) *loss = red[0] / (float)M;
 }
 
-// ---- one thread per row, weights (a chunk of up to kOC outputs) in LDS ----
-// Used when the weight chunk fits LDS (Cin * kOC floats); every thread reads
-// its input row once per chunk and keeps kOC accumulators in registers.
-constexpr int kOC = 32;
-constexpr int kRowWMax = 16384;   // floats of W staged per block (64 KB)
+// ---- one thread per row, rows staged through LDS ------------------------------
+// A block handles kRB consecutive rows: their inputs (contiguous in memory) are
+// copied into LDS with coalesced loads, each thread computes its row from LDS
+// against the weights (a chunk of up to kOC outputs, also in LDS), and the
+// block's outputs leave through LDS with coalesced stores.
+constexpr int kRB = 128;          // rows (= threads) per block
+constexpr int kOC = 32;           // outputs per thread
+constexpr int kRowsMaxIn = 128;   // widest row staged this way
 
-inline bool rows_ok(int Cin, int width) { return (long long)Cin * width <= kRowWMax; }
+inline bool rows_ok(int in_width) { return in_width <= kRowsMaxIn; }
+inline size_t rows_lds(int in_w, int out_w, int wcount) {
+    return ((size_t)kRB * (in_w + 1) + (size_t)kRB * (out_w + 1) + wcount) * sizeof(float);
+}
+
+// Coalesced copy of rows [m0, m0 + nr) x cols [c0, c0 + nc) of a row-major
+// [M][ld] matrix into an LDS tile with row pitch nc + 1 (bank-conflict free).
+template <typename TS>
+__device__ inline void rows_to_lds(const TS *src, long long m0, int nr, int ld, int c0, int nc,
+                                   float *tile)
+{
+    const int n = nr * nc;
+    for (int e = threadIdx.x; e < n; e += kRB) {
+        const int r = e / nc, c = e - (e / nc) * nc;
+        tile[r * (nc + 1) + c] = Store<TS>::load(src, (m0 + r) * ld + c0 + c);
+    }
+}
 
 template <typename TS>
-__global__ void __launch_bounds__(kThreads)
+__device__ inline void lds_to_rows(const float *tile, long long m0, int nr, int ld, int c0, int nc,
+                                   TS *dst)
+{
+    const int n = nr * nc;
+    for (int e = threadIdx.x; e < n; e += kRB) {
+        const int r = e / nc, c = e - (e / nc) * nc;
+        Store<TS>::store(dst, (m0 + r) * ld + c0 + c, tile[r * (nc + 1) + c]);
+    }
+}
+
+template <typename TS>
+__global__ void __launch_bounds__(kRB)
 k_fc_tanh_rows(long long M, int Cin, int Cout, const TS *__restrict__ x, const TS *__restrict__ w,
                const TS *__restrict__ b, TS *__restrict__ y)
 {
-    extern __shared__ float sw[];                 // [oc][Cin] then bias [oc]
+    extern __shared__ float lds[];
     const int o0 = blockIdx.y * kOC;
     const int oc = min(kOC, Cout - o0);
-    for (int e = threadIdx.x; e < oc * Cin; e += kThreads)
-        sw[e] = Store<TS>::load(w, (long long)o0 * Cin + e);
+    const long long m0 = (long long)blockIdx.x * kRB;
+    const int nr = (int)min((long long)kRB, M - m0);
+    float *xs = lds;                               // [kRB][Cin + 1]
+    float *ys = xs + kRB * (Cin + 1);              // [kRB][oc + 1]
+    float *sw = ys + kRB * (kOC + 1);              // [oc][Cin], then bias [oc]
     float *sb = sw + oc * Cin;
-    for (int e = threadIdx.x; e < oc; e += kThreads) sb[e] = Store<TS>::load(b, o0 + e);
+    for (int e = threadIdx.x; e < oc * Cin; e += kRB)
+        sw[e] = Store<TS>::load(w, (long long)o0 * Cin + e);
+    for (int e = threadIdx.x; e < oc; e += kRB) sb[e] = Store<TS>::load(b, o0 + e);
+    rows_to_lds<TS>(x, m0, nr, Cin, 0, Cin, xs);
     __syncthreads();
-    const long long m = (long long)blockIdx.x * kThreads + threadIdx.x;
-    if (m >= M) return;
-    float acc[kOC];
+    const int r = threadIdx.x;
+    if (r < nr) {
+        float acc[kOC];
 #pragma unroll
-    for (int j = 0; j < kOC; ++j) acc[j] = j < oc ? sb[j] : 0.0f;
-    const TS *xr = x + m * Cin;
-    for (int c = 0; c < Cin; ++c) {
-        const float xv = Store<TS>::load(xr, c);
+        for (int j = 0; j < kOC; ++j) acc[j] = j < oc ? sb[j] : 0.0f;
+        const float *xr = xs + r * (Cin + 1);
+        for (int c = 0; c < Cin; ++c) {
+            const float xv = xr[c];
+#pragma unroll
+            for (int j = 0; j < kOC; ++j)
+                if (j < oc) acc[j] += xv * sw[j * Cin + c];
+        }
 #pragma unroll
         for (int j = 0; j < kOC; ++j)
-            if (j < oc) acc[j] += xv * sw[j * Cin + c];
+            if (j < oc) ys[r * (oc + 1) + j] = tanhf(acc[j]);
     }
-    TS *yr = y + m * Cout + o0;
-#pragma unroll
-    for (int j = 0; j < kOC; ++j)
-        if (j < oc) Store<TS>::store(yr, j, tanhf(acc[j]));
+    __syncthreads();
+    lds_to_rows<TS>(ys, m0, nr, Cout, o0, oc, y);
 }
 
 // dx[m][i0 + i] = sum_o grad[m][o] w[o][i0 + i] for a chunk of kOC inputs.
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kRB)
 k_fc_dx_rows(long long M, int Cin, int Cout, RowGrad rg, const float *__restrict__ w,
              float *__restrict__ dx)
 {
-    extern __shared__ float sw[];                 // [Cout][ic]
+    extern __shared__ float lds[];
     const int i0 = blockIdx.y * kOC;
     const int ic = min(kOC, Cin - i0);
-    for (int e = threadIdx.x; e < Cout * ic; e += kThreads) {
+    const long long m0 = (long long)blockIdx.x * kRB;
+    const int nr = (int)min((long long)kRB, M - m0);
+    float *gs = lds;                               // [kRB][Cout + 1] row gradients
+    float *os = gs + kRB * (Cout + 1);             // [kRB][ic + 1]
+    float *sw = os + kRB * (kOC + 1);              // [Cout][ic]
+    for (int e = threadIdx.x; e < Cout * ic; e += kRB) {
         const int o = e / ic, i = e % ic;
         sw[e] = w[(long long)o * Cin + i0 + i];
     }
+    for (int e = threadIdx.x; e < nr * Cout; e += kRB) {
+        const int r = e / Cout, o = e - (e / Cout) * Cout;
+        gs[r * (Cout + 1) + o] = rg.at((m0 + r) * Cout + o);
+    }
     __syncthreads();
-    const long long m = (long long)blockIdx.x * kThreads + threadIdx.x;
-    if (m >= M) return;
-    float acc[kOC];
+    const int r = threadIdx.x;
+    if (r < nr) {
+        float acc[kOC];
 #pragma unroll
-    for (int j = 0; j < kOC; ++j) acc[j] = 0.0f;
-    for (int o = 0; o < Cout; ++o) {
-        const float gv = rg.at(m * Cout + o);
+        for (int j = 0; j < kOC; ++j) acc[j] = 0.0f;
+        const float *gr = gs + r * (Cout + 1);
+        for (int o = 0; o < Cout; ++o) {
+            const float gv = gr[o];
+#pragma unroll
+            for (int j = 0; j < kOC; ++j)
+                if (j < ic) acc[j] += gv * sw[o * ic + j];
+        }
 #pragma unroll
         for (int j = 0; j < kOC; ++j)
-            if (j < ic) acc[j] += gv * sw[o * ic + j];
+            if (j < ic) os[r * (ic + 1) + j] = acc[j];
     }
-#pragma unroll
-    for (int j = 0; j < kOC; ++j)
-        if (j < ic) dx[m * Cin + i0 + j] = acc[j];
+    __syncthreads();
+    lds_to_rows<float>(os, m0, nr, Cin, i0, ic, dx);
 }
 
 // Softmax head, one thread per row: logits in registers (K <= 16), the
 // label's probability picked by comparison (no dynamically indexed arrays).
 template <typename TS>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kRB)
 k_softmax_rows(long long M, int Cin, int K, const TS *__restrict__ x, const TS *__restrict__ w,
                const TS *__restrict__ b, const int32_t *__restrict__ labels,
                float *__restrict__ p, float *__restrict__ dlogits, float *__restrict__ lossp)
 {
-    extern __shared__ float sw[];                 // [K][Cin] then bias [K]
-    for (int e = threadIdx.x; e < K * Cin; e += kThreads) sw[e] = Store<TS>::load(w, e);
+    extern __shared__ float lds[];
+    const long long m0 = (long long)blockIdx.x * kRB;
+    const int nr = (int)min((long long)kRB, M - m0);
+    float *xs = lds;                               // [kRB][Cin + 1]
+    float *ps = xs + kRB * (Cin + 1);              // [kRB][K + 1] probabilities
+    float *sw = ps + kRB * (16 + 1);               // [K][Cin], then bias [K]
     float *sb = sw + K * Cin;
-    for (int e = threadIdx.x; e < K; e += kThreads) sb[e] = Store<TS>::load(b, e);
+    for (int e = threadIdx.x; e < K * Cin; e += kRB) sw[e] = Store<TS>::load(w, e);
+    for (int e = threadIdx.x; e < K; e += kRB) sb[e] = Store<TS>::load(b, e);
+    rows_to_lds<TS>(x, m0, nr, Cin, 0, Cin, xs);
     __syncthreads();
-    const long long m = (long long)blockIdx.x * kThreads + threadIdx.x;
+    const int r = threadIdx.x;
     float l = 0.0f;
-    if (m < M) {
+    if (r < nr) {
         float z[16];
 #pragma unroll
         for (int k = 0; k < 16; ++k) z[k] = k < K ? sb[k] : 0.0f;
-        const TS *xr = x + m * Cin;
+        const float *xr = xs + r * (Cin + 1);
         for (int c = 0; c < Cin; ++c) {
-            const float xv = Store<TS>::load(xr, c);
+            const float xv = xr[c];
 #pragma unroll
             for (int k = 0; k < 16; ++k)
                 if (k < K) z[k] += xv * sw[k * Cin + c];
@@ -281,28 +338,34 @@ k_softmax_rows(long long M, int Cin, int K, const TS *__restrict__ x, const TS *
         const float inv = 1.0f / sum;
 #pragma unroll
         for (int k = 0; k < 16; ++k)
-            if (k < K) p[m * K + k] = z[k] * inv;
+            if (k < K) ps[r * (K + 1) + k] = z[k] * inv;
         if (labels) {
             // An out-of-range label poisons the loss with NaN.
-            const int lab = labels[m];
+            const int lab = labels[m0 + r];
             const bool ok = lab >= 0 && lab < K;
             float pl = 0.0f;
 #pragma unroll
             for (int k = 0; k < 16; ++k)
                 if (k == lab) pl = z[k] * inv;
             l = ok ? -logf(pl) : NAN;
-#pragma unroll
-            for (int k = 0; k < 16; ++k)
-                if (k < K)
-                    dlogits[m * K + k] =
-                        ok ? (z[k] * inv - (k == lab ? 1.0f : 0.0f)) / (float)M : NAN;
         }
     }
+    __syncthreads();
+    lds_to_rows<float>(ps, m0, nr, K, 0, K, p);
     if (labels) {
-        __shared__ float red[kThreads];
+        // dlogits = (p - onehot(label)) / M, written coalesced from the tile
+        const int n = nr * K;
+        for (int e = threadIdx.x; e < n; e += kRB) {
+            const int rr = e / K, k = e - (e / K) * K;
+            const int lab = labels[m0 + rr];
+            const bool ok = lab >= 0 && lab < K;
+            dlogits[(m0 + rr) * K + k] =
+                ok ? (ps[rr * (K + 1) + k] - (k == lab ? 1.0f : 0.0f)) / (float)M : NAN;
+        }
+        __shared__ float red[kRB];
         red[threadIdx.x] = l;
         __syncthreads();
-        for (int off = kThreads / 2; off > 0; off >>= 1) {
+        for (int off = kRB / 2; off > 0; off >>= 1) {
             if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
             __syncthreads();
         }
@@ -324,10 +387,10 @@ inline unsigned blocks_for(long long n) { return (unsigned)((n + kThreads - 1) /
 
 int fc_dx(long long M, int Cin, int Cout, RowGrad rg, const float *w, float *dx, hipStream_t st)
 {
-    if (rows_ok(Cout, kOC)) {
-        const dim3 grid(blocks_for(M), (Cin + kOC - 1) / kOC);
-        k_fc_dx_rows<<<grid, kThreads, (size_t)Cout * kOC * sizeof(float), st>>>(M, Cin, Cout, rg,
-                                                                               w, dx);
+    if (rows_ok(Cout)) {
+        const dim3 grid((unsigned)((M + kRB - 1) / kRB), (Cin + kOC - 1) / kOC);
+        k_fc_dx_rows<<<grid, kRB, rows_lds(Cout, kOC, Cout * kOC), st>>>(M, Cin, Cout, rg, w,
+                                                                           dx);
     } else {
         k_fc_dx<<<blocks_for(M * Cin), kThreads, 0, st>>>(M, Cin, Cout, rg, w, dx);
     }
@@ -355,22 +418,22 @@ size_t fc_ws(long long M, int Cin, int Cout)
     Carve cv(nullptr);
     cv.take<float>((size_t)fc_chunks(M) * Cout * (Cin + 1));   // weight-gradient partials
     cv.take<float>((size_t)M * (Cout < kMaxK ? Cout : kMaxK)); // dlogits (softmax head)
-    cv.take<float>((size_t)blocks_for(M));                     // per-block losses
+    cv.take<float>((size_t)(M + kRB - 1) / kRB);               // per-block losses
     return cv.off;
 }
 
 int fc_tanh_forward(long long M, int Cin, int Cout, int dtype, const void *x, const void *w,
                     const void *b, void *y, hipStream_t st)
 {
-    if (rows_ok(Cin + 1, kOC)) {
-        const dim3 grid(blocks_for(M), (Cout + kOC - 1) / kOC);
-        const size_t lds = (size_t)kOC * (Cin + 1) * sizeof(float);
+    if (rows_ok(Cin)) {
+        const dim3 grid((unsigned)((M + kRB - 1) / kRB), (Cout + kOC - 1) / kOC);
+        const size_t lds = rows_lds(Cin, kOC, kOC * (Cin + 1));
         if (dtype == PLSTM_BF16)
-            k_fc_tanh_rows<uint16_t><<<grid, kThreads, lds, st>>>(
+            k_fc_tanh_rows<uint16_t><<<grid, kRB, lds, st>>>(
                 M, Cin, Cout, (const uint16_t *)x, (const uint16_t *)w, (const uint16_t *)b,
                 (uint16_t *)y);
         else
-            k_fc_tanh_rows<float><<<grid, kThreads, lds, st>>>(
+            k_fc_tanh_rows<float><<<grid, kRB, lds, st>>>(
                 M, Cin, Cout, (const float *)x, (const float *)w, (const float *)b, (float *)y);
         PLSTM_LAUNCH_CHECK();
         return PLSTM_OK;
@@ -409,16 +472,17 @@ int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void
     Carve cv(ws);
     float *partial = cv.take<float>((size_t)fc_chunks(M) * K * (Cin + 1));
     float *dlogits = cv.take<float>((size_t)M * K);
-    float *lossp = cv.take<float>((size_t)blocks_for(M));
-    const unsigned nb = blocks_for(M);
-    if (rows_ok(Cin + 1, K)) {
-        const size_t lds = (size_t)K * (Cin + 1) * sizeof(float);
+    float *lossp = cv.take<float>((size_t)(M + kRB - 1) / kRB);
+    unsigned nb = blocks_for(M);
+    if (rows_ok(Cin)) {
+        nb = (unsigned)((M + kRB - 1) / kRB);
+        const size_t lds = rows_lds(Cin, 16, K * (Cin + 1));
         if (dtype == PLSTM_BF16)
-            k_softmax_rows<uint16_t><<<nb, kThreads, lds, st>>>(
+            k_softmax_rows<uint16_t><<<nb, kRB, lds, st>>>(
                 M, Cin, K, (const uint16_t *)x, (const uint16_t *)w, (const uint16_t *)b, labels,
                 p, dlogits, lossp);
         else
-            k_softmax_rows<float><<<nb, kThreads, lds, st>>>(
+            k_softmax_rows<float><<<nb, kRB, lds, st>>>(
                 M, Cin, K, (const float *)x, (const float *)w, (const float *)b, labels, p,
                 dlogits, lossp);
     } else if (dtype == PLSTM_BF16) {

@@ -49,7 +49,41 @@ def phase_work(name, V, C, O):
     return None, None, None
 
 
-def roofline(phases, name, passes, V, C, O):
+# HBM bytes per launch measured with rocprofv3 counters (FETCH_SIZE, WRITE_SIZE,
+# calibrated against a copy of known size); valid while the kernel sources are
+# the ones measured.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_mr48x240x240.md")
+KERNEL_SOURCES = {
+    "sweep_fwd_mfma": ["sweep_fwd.hip", "strip_plan.h", "common.h"],
+    "sweep_bwd_mfma": ["sweep_bwd.hip", "strip_plan.h", "common.h"],
+    "wgrad_mfma": ["sweep_bwd.hip", "strip_plan.h", "common.h"],
+}
+
+
+def source_hash(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_1506_07452_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, mode):
+    """Bytes per launch from the committed counter profile, or None when the
+    kernel is not in it or its sources changed since."""
+    if kernel not in KERNEL_SOURCES or not os.path.exists(TRAFFIC_FILE):
+        return None
+    for line in open(TRAFFIC_FILE):
+        if not line.startswith("traffic "):
+            continue
+        f = dict(kv.split("=", 1) for kv in line.split()[1:])
+        if f["kernel"] == kernel and f["mode"] == mode:
+            return int(f["bytes"]) if f["src"] == source_hash(kernel) else None
+    return None
+
+
+def roofline(phases, name, passes, V, C, O, mode="training"):
     ms, launches = phases[name]
     bound, amount, unit = phase_work(name, V, C, O)
     if bound is None:
@@ -61,7 +95,8 @@ def roofline(phases, name, passes, V, C, O):
     else:
         achieved, peak = per_launch / avg_s / 1e12, PEAK_FP32_TFLOPS
     return {"kernel": name, "bound": bound, "achieved": round(achieved, 3), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+            "unit": unit, "frac": round(achieved / peak, 4),
+            "traffic": measured_traffic(name, mode),
             "launches_per_pass": launches // passes,
             "avg_launch_ms": round(ms / launches, 4)}
 
@@ -193,7 +228,8 @@ def main():
         "fwd": {"value": vdu / t_fwd, "ms_per_pass": t_fwd * 1e3,
                 "tflops": fwd_flops / t_fwd / 1e12,
                 "frac_fp32_mfma_peak": fwd_flops / t_fwd / 1e12 / PEAK_FP32_TFLOPS,
-                "roofline": roofline(phases_fwd, sweep_fwd_name, args.steps, V, C, O)},
+                "roofline": roofline(phases_fwd, sweep_fwd_name, args.steps, V, C, O,
+                                     mode="inference")},
         "roofline": roofline(phases, dom, args.steps, V, C, O),
         "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
     }

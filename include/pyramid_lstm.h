@@ -76,9 +76,12 @@ const char *pyramid_lstm_status_string(int status);
 size_t pyramid_lstm_workspace_size(const plstm_shape *s, int training);
 
 /* Bytes of the `saved` buffer that a training forward fills and the backward
- * reads (gate activations and cell states of every voxel and direction, in a
- * library-private layout: gates, c^d and h^d, fp32).  Returns 0 for an invalid
- * or unsupported shape. */
+ * reads: three fp32 arrays, each starting at the next 256-byte boundary,
+ *   gates [6][N][D][H][W][4O]  i, f, g, o of Eq. (7)-(10) after the nonlinearity
+ *   c^d   [6][N][D][H][W][O]   cell states, Eq. (11)
+ *   h^d   [6][N][D][H][W][O]   per-direction outputs, Eq. (12)
+ * with directions in the order z+, z-, y+, y-, x+, x-.  Returns 0 for an
+ * invalid or unsupported shape. */
 size_t pyramid_lstm_saved_size(const plstm_shape *s);
 
 /* Forward pass of one layer, Eq. (7)-(13).
@@ -157,7 +160,9 @@ int pyramid_lstm_timing_read(int max_phases, char *names, double *ms, int *launc
 /* Forward implementation selection, for testing and tuning (process-wide):
  * 0 = automatic (default): the persistent MFMA sweep where it supports the
  * shape (fp32, O = 16, C <= 4, grid co-resident), else the generic path;
- * 1 = generic path only; 2 = same as 0.  Returns PLSTM_EINVAL for other values. */
+ * 1 = generic path only; 2 = same as 0; 3 = as 0, but the MFMA sweep stages
+ * every strip chunk by chunk (no strip kept whole in LDS).  Returns
+ * PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_forward_path(int path);
 
 /* Backward implementation selection, for testing and tuning (process-wide):

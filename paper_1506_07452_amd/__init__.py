@@ -223,7 +223,8 @@ def pyramid_lstm_timing_read(max_phases: int = 32):
 
 
 def pyramid_lstm_set_forward_path(path: int) -> None:
-    """0 = automatic, 1 = generic path only, 2 = MFMA sweep where supported."""
+    """0 = automatic, 1 = generic path only, 2 = MFMA sweep where supported,
+    3 = MFMA sweep with every strip staged chunk by chunk."""
     _check("pyramid_lstm_set_forward_path", load().pyramid_lstm_set_forward_path(int(path)))
 
 

@@ -26,7 +26,7 @@ int forward_dispatch(const Geom &g, int dtype, const void *x, const void *wx, co
         int *flags = cv.take<int>(1024 + 1);
         const int rc = sweep_fwd(g, (const float *)x, (const float *)wx, (const float *)wh,
                                  (const float *)b, hd, cellbuf, sv ? sv->gates : nullptr, flags,
-                                 st);
+                                 st, g_forward_path != 3);
         if (rc == PLSTM_OK) return sum_dirs(g, dtype, hd, h, st);
         // A grid that cannot be co-resident or a plane too wide for LDS runs
         // on the generic path instead.
@@ -60,7 +60,7 @@ int backward_dispatch(const Geom &g, const float *x, const float *wx, const floa
 
 extern "C" int pyramid_lstm_set_forward_path(int path)
 {
-    if (path < 0 || path > 2) return PLSTM_EINVAL;
+    if (path < 0 || path > 3) return PLSTM_EINVAL;
     plstm::g_forward_path = path;
     return PLSTM_OK;
 }

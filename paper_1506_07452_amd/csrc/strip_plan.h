@@ -40,6 +40,13 @@ struct StripCostModel {
     size_t fixed_bytes;   // LDS independent of the strip size
     size_t px_bytes;      // LDS per staged pixel
     double c_sync, c_tile, c_stage0, c_stage_px;
+    // Resident mode (optional): the whole strip stays in LDS for the sweep,
+    // res_px_bytes per staged pixel (incl. halo) plus res_own_bytes per strip
+    // pixel plus res_fixed_bytes; one step then costs c_res_step + the tiles.
+    bool allow_resident = false;
+    size_t res_px_bytes = 0, res_own_bytes = 0, res_fixed_bytes = 0;
+    int res_max_staged = 0;   // most staged elements the kernel supports
+    double c_res_step = 0.0;
 };
 
 struct Plan {
@@ -47,12 +54,14 @@ struct Plan {
     int first[kDirs];
     int chunk_rows[kDirs];
     int max_w[kDirs];
+    int resident[kDirs];
     int blocks;
     size_t lds;
 };
 
 struct StripShape {
     int w, rows, chunks;
+    bool resident;
     size_t lds;
 };
 
@@ -60,6 +69,18 @@ inline StripShape strip_shape(const DirGeom &r, int k, const StripCostModel &m, 
 {
     StripShape sh{};
     sh.w = (r.Q + k - 1) / k;
+    if (m.allow_resident) {
+        const long long staged = (long long)(r.P + 2) * (sh.w + 2);
+        const size_t lds = m.fixed_bytes + m.res_fixed_bytes + (size_t)staged * m.res_px_bytes +
+                           (size_t)r.P * sh.w * m.res_own_bytes;
+        if (lds <= lds_limit && staged <= m.res_max_staged) {
+            sh.rows = r.P;
+            sh.chunks = 1;
+            sh.resident = true;
+            sh.lds = lds;
+            return sh;
+        }
+    }
     const size_t per_row = (size_t)(sh.w + 2) * m.px_bytes;
     const long long max_rows =
         lds_limit > m.fixed_bytes ? (long long)((lds_limit - m.fixed_bytes) / per_row) - 2 : 0;
@@ -75,6 +96,7 @@ inline double strip_cost(const DirGeom &r, int k, const StripCostModel &m, size_
     const StripShape sh = strip_shape(r, k, m, lds_limit);
     if (sh.rows < 1) return 1e30;
     const int tiles = (sh.rows * sh.w + 15) / 16;
+    if (sh.resident) return (double)r.T * (m.c_res_step + ((tiles + 3) / 4) * m.c_tile);
     const double stage = m.c_stage0 + m.c_stage_px * (sh.rows + 2) * (sh.w + 2);
     return (double)r.T * (m.c_sync + sh.chunks * (stage + ((tiles + 3) / 4) * m.c_tile));
 }
@@ -126,6 +148,7 @@ inline Plan make_plan(const Geom &g, int budget, const StripCostModel &m, size_t
         pl.first[d] = first;
         pl.chunk_rows[d] = sh.rows;
         pl.max_w[d] = sh.w;
+        pl.resident[d] = sh.resident ? 1 : 0;
         first += k * g.N;
         if (sh.lds > lds) lds = sh.lds;
     }

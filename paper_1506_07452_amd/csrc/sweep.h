@@ -9,7 +9,8 @@ namespace plstm {
 bool sweep_fwd_supported(const Geom &g, int dtype);
 size_t sweep_fwd_ws(const Geom &g, bool training);
 int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, const float *b,
-              float *hd, float *cell, float *gates, int *flags, hipStream_t st);
+              float *hd, float *cell, float *gates, int *flags, hipStream_t st,
+              bool allow_resident);
 
 // Persistent MFMA backward sweep + MFMA parameter gradients (sweep_bwd.hip):
 // O = 16, C <= 4, fp32.

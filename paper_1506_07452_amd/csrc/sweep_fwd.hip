@@ -23,11 +23,13 @@
 // only reads plane t-1 and writes plane t (no write-after-read hazard), and
 // LDS is just a staging copy.  MFMA layout (16x16x4 f32, one block): lane l
 // supplies A[m = l%16][k = l/16] and B[k = l/16][n = l%16] and receives
-// D[4(l/16) + i][l%16], i = 0..3.  The K index of a tap is permuted so that
-// lane group q = l/16 takes hidden channels 4q..4q+3 with one 16-byte LDS
-// read; B uses the same permutation.  N-tile g holds gate g (i, f, g, o) of
-// the 16 units, so every lane ends with all four gates of unit l%16 for four
-// pixels and the cell update needs no data exchange.
+// D[4(l/16) + i][l%16], i = 0..3.  Gate-units are on M (M-tile g = gate g of
+// the 16 units, the weights are the A operand) and pixels on N (B = im2col).
+// The K index of a tap is permuted so that lane group q = l/16 takes hidden
+// channels 4q..4q+3 of its pixel with one 16-byte LDS read; A uses the same
+// permutation.  Every lane ends with all four gates of units 4q..4q+3 of
+// pixel l%16, so the cell update needs no data exchange and its loads and
+// stores are 16-byte vectors.
 #include "common.h"
 #include "sweep.h"
 #include "strip_plan.h"
@@ -46,6 +48,8 @@ constexpr int kHS = 20;          // LDS floats per staged h pixel (16 + 4 pad)
 constexpr int kMaxSpin = 1 << 21;
 constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unconstrained
 constexpr int kBatch = 4;        // staging loads in flight per thread
+constexpr int kCS = 20;          // LDS floats per cell state of a resident strip (16 + 4 pad)
+constexpr int kResX = 8;         // x_t staging registers per thread (resident strips)
 
 struct SweepArgs {
     Geom g;
@@ -59,6 +63,7 @@ struct SweepArgs {
     int first[kDirs];   // first block of direction d
     int chunk_rows[kDirs];  // rows staged per LDS chunk, per direction
     int max_w[kDirs];       // widest strip of each direction (LDS layout)
+    int resident[kDirs];    // 1: strips of this direction stay in LDS
 };
 
 // Gate nonlinearities from exp and the hardware reciprocal (1 ulp each):
@@ -74,6 +79,87 @@ __device__ inline float ftanh(float a) { return 1.0f - 2.0f * frcp(__expf(2.0f *
 // truncation is exact.
 __device__ inline int fdiv_floor(int i, float inv_w) {
     return (int)(((float)i + 0.5f) * inv_w);
+}
+
+// Waits until the strip's neighbours have published `step` steps (bounded:
+// a wait that never ends raises the error flag and gives up).
+__device__ inline void wait_neighbours(const SweepArgs &a, int nb_lo, int nb_hi, int step)
+{
+    const int nb = threadIdx.x == 0 ? nb_lo : (threadIdx.x == 1 ? nb_hi : -1);
+    if (nb >= 0) {
+        int spins = 0;
+        while (__hip_atomic_load(&a.flags[nb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
+               step) {
+            __builtin_amdgcn_s_sleep(1);
+            if (++spins > kMaxSpin) {
+                __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+            if ((spins & 1023) == 0 &&
+                __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+                break;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+}
+
+// Publishes `step` completed steps of this strip: the calling wave writes L2
+// back (agent-scope release), waits for it, then stores the flag.  Callers
+// make sure every store to publish has reached L2 first.
+__device__ inline void publish(const SweepArgs &a, int step)
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __hip_atomic_store(&a.flags[blockIdx.x], step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Gate pre-activations of one 16-pixel tile: bias + W_x im2col(x_t) +
+// W_h im2col(h_{t-1}); `base` is the LDS pixel index of this lane's pixel in
+// the staged (halo-padded) tile whose rows are `rs` and columns `cs` pixels
+// apart.
+template <int C>
+__device__ __forceinline__ void tile_preact(const float (&bh)[9][4][4], const float *hsrc,
+                                            const float *xs, const float *wxs, const float *bs,
+                                            int base, int rs, int cs, const int *xoff, int q4,
+                                            int lane, f4 (&acc)[4])
+{
+    constexpr int KXS = (9 * C + 3) / 4;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[g] = *(const f4 *)&bs[g * kO + 4 * q4];
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) {
+        const int o = (tap / 3 - 1) * rs + (tap % 3 - 1) * cs;
+        const f4 hv = *(const f4 *)&hsrc[(base + o) * kHS + 4 * q4];
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(bh[tap][s2][g], hv[s2], acc[g], 0,
+                                                            0, 0);
+    }
+#pragma unroll
+    for (int ks = 0; ks < KXS; ++ks) {
+        const float xv = (4 * ks + q4 < 9 * C) ? xs[base * C + xoff[ks]] : 0.0f;
+        const f4 wxv = *(const f4 *)&wxs[(ks * 64 + lane) * 4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(wxv[g], xv, acc[g], 0, 0, 0);
+    }
+}
+
+// Gates, cell and hidden update of four units of one pixel (Eq. (7)-(12)).
+__device__ __forceinline__ void lstm_cell(const f4 (&acc)[4], f4 cprev, bool has_prev, f4 &gi,
+                                          f4 &gf, f4 &gg, f4 &go, f4 &cn, f4 &hn)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        gi[i] = fsig(acc[0][i]);
+        gf[i] = fsig(acc[1][i]);
+        gg[i] = ftanh(acc[2][i]);
+        go[i] = fsig(acc[3][i]);
+        cn[i] = gg[i] * gi[i] + (has_prev ? cprev[i] : 0.0f) * gf[i];
+        hn[i] = go[i] * ftanh(cn[i]);
+    }
 }
 
 template <int C>
@@ -98,12 +184,16 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q4 = lane >> 4, col = lane & 15;
     constexpr int KXS = (9 * C + 3) / 4;    // MFMA k-steps of the input convolution
-    float *wxs = smem;                       // [KXS][64 lanes][4 N-tiles] B fragments
-    const int chunk_rows = a.chunk_rows[d];
-    float *hs = smem + KXS * 256;
-    float *xs = hs + (chunk_rows + 2) * (a.max_w[d] + 2) * kHS;
+    float *wxs = smem;                       // [KXS][64 lanes][4 M-tiles] A fragments
+    float *bs = wxs + KXS * 256;             // [64] bias
+    const bool resident = a.resident[d] != 0;
+    const int P = dg.P;
+    // LDS pixel strides of a staged tile: chunked strips are row-major,
+    // resident strips column-major (a tile then covers one or two columns,
+    // so the columns next to a neighbour strip form their own tiles).
+    const int rs = resident ? 1 : W2, cs = resident ? P + 2 : 1;
 
-    // ---- weights as MFMA B fragments (resident for the whole sweep) -----
+    // ---- recurrent weights as MFMA A fragments (resident for the sweep) ---
     const long long V = a.g.V;
     float bh[9][4][4];
 #pragma unroll
@@ -111,33 +201,30 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
 #pragma unroll
         for (int s = 0; s < 4; ++s)
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                const int j = 4 * q4 + s, gn = nt * kO + col;
-                bh[tap][s][nt] = a.wh[(((long long)d * kG + gn) * kO + j) * 9 + tap];
+            for (int g = 0; g < 4; ++g) {
+                const int j = 4 * q4 + s, gn = g * kO + col;
+                bh[tap][s][g] = a.wh[(((long long)d * kG + gn) * kO + j) * 9 + tap];
             }
-    // Input-convolution B fragments go to LDS (they feed few MFMAs; keeping
+    // Input-convolution A fragments go to LDS (they feed few MFMAs; keeping
     // them out of VGPRs lets two waves share a SIMD).
     int xoff[KXS];
 #pragma unroll
     for (int ks = 0; ks < KXS; ++ks) {
         const int k = 4 * ks + q4;
         const int tap = k < 9 * C ? k / C : 0, c = k % C;   // padding lanes read tap 0
-        xoff[ks] = k < 9 * C ? ((tap / 3 - 1) * W2 + (tap % 3 - 1)) * C + c : 0;
+        xoff[ks] = k < 9 * C ? ((tap / 3 - 1) * rs + (tap % 3 - 1) * cs) * C + c : 0;
         if (wave == 0) {
             f4 w4;
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                const int gn = nt * kO + col;
+            for (int g = 0; g < 4; ++g) {
+                const int gn = g * kO + col;
                 const float w = a.wx[(((long long)d * kG + gn) * C + c) * 9 + tap];
-                w4[nt] = k < 9 * C ? w : 0.0f;
+                w4[g] = k < 9 * C ? w : 0.0f;
             }
             *(f4 *)&wxs[(ks * 64 + lane) * 4] = w4;
         }
     }
-    __syncthreads();
-    float bias[4];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) bias[nt] = a.b[d * kG + nt * kO + col];
+    if (threadIdx.x < kG) bs[threadIdx.x] = a.b[d * kG + threadIdx.x];
 
     // Base pointers of this (direction, batch element); element offsets inside
     // a slice fit in 32 bits (V * 64 < 2^31 is checked at the boundary).
@@ -147,29 +234,155 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
     float *const gates_dn = a.gates ? a.gates + dn * kG : nullptr;
     const float *const x_n = a.x + (long long)n * V * C;
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
-    const float inv_tq = 1.0f / (float)TQ, inv_w2 = 1.0f / (float)W2;
+    const float inv_w2 = 1.0f / (float)W2;
 
+    if (resident) {
+        // ================= resident strip: the whole strip in LDS ===========
+        // h is double-buffered (h_{t-1} read, h_t written by the epilogue),
+        // c stays in LDS, only the two halo columns come from global memory
+        // each step and x_{t+1} is loaded while step t computes.  Pixels are
+        // numbered column by column; the tiles touching a column next to a
+        // neighbour strip run first and the step is published as soon as
+        // they are stored, so neighbours seldom wait.
+        const int P2 = P + 2;
+        const int npl = P2 * W2;
+        const int npx = P * TQ;
+        const int nmt = (npx + 15) >> 4;
+        float *hb0 = bs + kG;
+        float *hb1 = hb0 + npl * kHS;
+        float *xs = hb1 + npl * kHS;
+        float *cb = xs + ((npl * C + 3) & ~3);     // [npx][kCS] cell states (16-byte aligned)
+        int *order = (int *)(cb + npx * kCS);      // tile order, edge tiles first
+        int *cnt = order + nmt;                    // edge tiles stored this step
+        const float inv_p = 1.0f / (float)P;
+        for (int e = threadIdx.x; e < 2 * npl * kHS; e += kThreads) hb0[e] = 0.0f;
+        if (threadIdx.x == 0) {
+            int k = 0;
+            for (int pass = 0; pass < 2; ++pass)
+                for (int mt = 0; mt < nmt; ++mt) {
+                    const int c0 = (mt * 16) / P, c1 = min(mt * 16 + 15, npx - 1) / P;
+                    const bool edge = (c0 == 0 && nb_lo >= 0) || (c1 == TQ - 1 && nb_hi >= 0);
+                    if (edge == (pass == 0)) order[k++] = mt;
+                }
+            int ne = 0;
+            for (int mt = 0; mt < nmt; ++mt) {
+                const int c0 = (mt * 16) / P, c1 = min(mt * 16 + 15, npx - 1) / P;
+                ne += ((c0 == 0 && nb_lo >= 0) || (c1 == TQ - 1 && nb_hi >= 0)) ? 1 : 0;
+            }
+            cnt[0] = 0;
+            cnt[1] = ne;
+        }
+        // x_t staging registers (loaded one step ahead).  Threads walk the
+        // staged plane row by row (coalesced in global memory) and store
+        // into the column-major LDS copy.
+        float xr[kResX];
+        auto issue_x = [&](int splane) {
+#pragma unroll
+            for (int u = 0; u < kResX; ++u) {
+                const int e = threadIdx.x + u * kThreads;
+                const int pix = e / C, c = e - (e / C) * C;
+                const int rr = fdiv_floor(pix, inv_w2);
+                const int pr = rr - 1, pc = pix - rr * W2 + q0 - 1;
+                const bool ok = e < npl * C && pr >= 0 && pr < P && pc >= 0 && pc < dg.Q;
+                const int off = ok ? (splane + pr * sp + pc * sq) * C + c : 0;
+                const float v = x_n[off];
+                xr[u] = ok ? v : 0.0f;
+            }
+        };
+        auto commit_x = [&]() {
+#pragma unroll
+            for (int u = 0; u < kResX; ++u) {
+                const int e = threadIdx.x + u * kThreads;
+                const int pix = e / C, c = e - (e / C) * C;
+                const int rr = fdiv_floor(pix, inv_w2);
+                if (e < npl * C) xs[((pix - rr * W2) * P2 + rr) * C + c] = xr[u];
+            }
+        };
+        issue_x((dg.sign > 0 ? 0 : dg.T - 1) * ss);
+        __syncthreads();
+        const int n_edge = cnt[1];
+        for (int t = 0; t < dg.T; ++t) {
+            const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+            const int splane = s * ss;
+            float *hprev = (t & 1) ? hb0 : hb1;      // h_{t-1}
+            float *hcur = (t & 1) ? hb1 : hb0;       // h_t
+            if (t > 0) {
+                // halo columns of h_{t-1} from the neighbours
+                wait_neighbours(a, nb_lo, nb_hi, t);
+                __syncthreads();
+                const int pplane = (s - dg.sign) * ss;
+                for (int e = threadIdx.x; e < 2 * P * 4; e += kThreads) {
+                    const int side = e / (P * 4), rem = e - side * P * 4;
+                    const int r = rem >> 2, qd = rem & 3;
+                    const int pc = side ? q1 : q0 - 1;
+                    if (pc >= 0 && pc < dg.Q) {
+                        const f4 v =
+                            *(const f4 *)&hd_dn[(pplane + r * sp + pc * sq) * kO + qd * 4];
+                        *(f4 *)&hprev[((side ? TQ + 1 : 0) * P2 + r + 1) * kHS + qd * 4] = v;
+                    }
+                }
+            }
+            commit_x();
+            __syncthreads();
+            // One tile: contraction, cell update, stores (h_t to LDS for the
+            // next step and to the volume for the neighbours and the sum).
+            auto tile = [&](int mt) {
+                const int pa = min(mt * 16 + col, npx - 1);     // this lane's pixel
+                const int ca = fdiv_floor(pa, inv_p), ra = pa - ca * P;
+                const int base = (ca + 1) * P2 + ra + 1;
+                const int v = splane + ra * sp + (q0 + ca) * sq;
+                const f4 cv = *(const f4 *)&cb[pa * kCS + 4 * q4];
+                f4 acc[4];
+                tile_preact<C>(bh, hprev, xs, wxs, bs, base, 1, P2, xoff, q4, lane, acc);
+                f4 gi, gf, gg, go, cn, hn;
+                lstm_cell(acc, cv, t > 0, gi, gf, gg, go, cn, hn);
+                if (mt * 16 + col < npx) {
+                    *(f4 *)&cb[pa * kCS + 4 * q4] = cn;
+                    *(f4 *)&hcur[base * kHS + 4 * q4] = hn;
+                    *(f4 *)&hd_dn[v * kO + 4 * q4] = hn;
+                    if (gates_dn) {
+                        *(f4 *)&cell_dn[v * kO + 4 * q4] = cn;
+                        float *gp = gates_dn + v * kG + 4 * q4;
+                        *(f4 *)&gp[0] = gi;
+                        *(f4 *)&gp[kO] = gf;
+                        *(f4 *)&gp[2 * kO] = gg;
+                        *(f4 *)&gp[3 * kO] = go;
+                    }
+                }
+            };
+            // Edge tiles first; once a wave's edge tile has reached L2 it
+            // counts it, and the wave that stores the last one publishes.
+            // The x_{t+1} prefetch goes out only after a wave's edge tiles,
+            // so the store waits do not wait for it.
+            int k = wave;
+            for (; k < n_edge; k += kWaves) {
+                tile(order[k]);
+                __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+                if (lane == 0 && atomicAdd(cnt, 1) == n_edge - 1) publish(a, t + 1);
+            }
+            if (t + 1 < dg.T) issue_x((dg.sign > 0 ? t + 1 : dg.T - 2 - t) * ss);
+            for (; k < nmt; k += kWaves) tile(order[k]);
+            if (n_edge == 0) __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                if (n_edge == 0) publish(a, t + 1);
+                cnt[0] = 0;
+            }
+        }
+        return;
+    }
+
+    // ================= chunked strip: rows staged per step =================
+    const int chunk_rows = a.chunk_rows[d];
+    float *hs = bs + kG;
+    float *xs = hs + (chunk_rows + 2) * (a.max_w[d] + 2) * kHS;
+    const float inv_tq = 1.0f / (float)TQ;
+    __syncthreads();
     for (int t = 0; t < dg.T; ++t) {
         const int s = dg.sign > 0 ? t : dg.T - 1 - t;
         const int sprev = s - dg.sign;
-        // ---- wait for the neighbours' h_{t-1} ---------------------------
         if (t > 0) {
-            const int nb = threadIdx.x == 0 ? nb_lo : (threadIdx.x == 1 ? nb_hi : -1);
-            if (nb >= 0) {
-                int spins = 0;
-                while (__hip_atomic_load(&a.flags[nb], __ATOMIC_RELAXED,
-                                         __HIP_MEMORY_SCOPE_AGENT) < t) {
-                    __builtin_amdgcn_s_sleep(1);
-                    if (++spins > kMaxSpin) {
-                        __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        break;
-                    }
-                    if ((spins & 1023) == 0 &&
-                        __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-                        break;
-                }
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-            }
+            wait_neighbours(a, nb_lo, nb_hi, t);
             __syncthreads();
         }
         const int splane = s * ss, sprev_plane = sprev * ss;
@@ -198,7 +411,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
                         hv[u] = ok ? v : f4{0.0f, 0.0f, 0.0f, 0.0f};
                     }
                     {
-                        const int pix = e / C, c = e - (e / C) * C;
+                        const int pix = e / C, c = e % C;
                         const int rr = fdiv_floor(pix, inv_w2);
                         const int pr = rr + r0 - 1, pc = pix - rr * W2 + q0 - 1;
                         const bool ok = e < nx && pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q;
@@ -219,68 +432,31 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
             const int npx = CH * TQ;
             const int nmt = (npx + 15) >> 4;
             for (int mt = wave; mt < nmt; mt += kWaves) {
-                const int pa = min(mt * 16 + col, npx - 1);     // this lane's A row
+                const int pa = min(mt * 16 + col, npx - 1);     // this lane's pixel
                 const int ra = fdiv_floor(pa, inv_tq);
                 const int base = (ra + 1) * W2 + (pa - ra * TQ) + 1;
-                // Output rows 4 q4 + i of this lane; c_{t-1} is loaded now so
-                // the load overlaps the contraction below.
-                float cprev[4];
-                int vout[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int px = min(mt * 16 + 4 * q4 + i, npx - 1);
-                    const int rr = fdiv_floor(px, inv_tq);
-                    vout[i] = splane + (rr + r0) * sp + (px - rr * TQ + q0) * sq;
-                    // at t = 0 there is no previous plane: read (and discard)
-                    // this plane's entry so the address stays inside the slice
-                    const float cv = cell_dn[(vout[i] - splane + cplane) * kO + col];
-                    cprev[i] = t > 0 ? cv : 0.0f;
-                }
-                // keep the loads above the contraction (the scheduler would
-                // otherwise sink them to their use and expose their latency)
+                const int v = splane + (ra + r0) * sp + (pa - ra * TQ + q0) * sq;
+                // c_{t-1} of this lane's units, loaded now so the load overlaps
+                // the contraction below; at t = 0 there is no previous plane:
+                // read (and discard) this plane's entry so the address stays
+                // inside the slice.
+                const f4 cv = *(const f4 *)&cell_dn[(v - splane + cplane) * kO + 4 * q4];
+                // keep the load above the contraction (the scheduler would
+                // otherwise sink it to its use and expose its latency)
                 __builtin_amdgcn_sched_barrier(0);
                 f4 acc[4];
-#pragma unroll
-                for (int nt = 0; nt < 4; ++nt) acc[nt] = f4{bias[nt], bias[nt], bias[nt], bias[nt]};
-#pragma unroll
-                for (int tap = 0; tap < 9; ++tap) {
-                    const int o = (tap / 3 - 1) * W2 + (tap % 3 - 1);
-                    const f4 hv = *(const f4 *)&hs[(base + o) * kHS + 4 * q4];
-#pragma unroll
-                    for (int s2 = 0; s2 < 4; ++s2)
-#pragma unroll
-                        for (int nt = 0; nt < 4; ++nt)
-                            acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(hv[s2], bh[tap][s2][nt],
-                                                                         acc[nt], 0, 0, 0);
-                }
-#pragma unroll
-                for (int ks = 0; ks < KXS; ++ks) {
-                    const float av = (4 * ks + q4 < 9 * C) ? xs[base * C + xoff[ks]] : 0.0f;
-                    const f4 bxv = *(const f4 *)&wxs[(ks * 64 + lane) * 4];
-#pragma unroll
-                    for (int nt = 0; nt < 4; ++nt)
-                        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bxv[nt], acc[nt],
-                                                                     0, 0, 0);
-                }
-                // ---- gates and cell update: rows 4 q4 + i, unit col ------
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    if (mt * 16 + 4 * q4 + i >= npx) continue;
-                    const int v = vout[i];
-                    const float gi = fsig(acc[0][i]);
-                    const float gf = fsig(acc[1][i]);
-                    const float gg = ftanh(acc[2][i]);
-                    const float go = fsig(acc[3][i]);
-                    const float c = gg * gi + cprev[i] * gf;
-                    cell_dn[v * kO + col] = c;
-                    hd_dn[v * kO + col] = go * ftanh(c);
-                    if (gates_dn) {
-                        float *gp = gates_dn + v * kG + col;
-                        gp[0] = gi;
-                        gp[kO] = gf;
-                        gp[2 * kO] = gg;
-                        gp[3 * kO] = go;
-                    }
+                tile_preact<C>(bh, hs, xs, wxs, bs, base, W2, 1, xoff, q4, lane, acc);
+                if (mt * 16 + col >= npx) continue;
+                f4 gi, gf, gg, go, cn, hn;
+                lstm_cell(acc, cv, t > 0, gi, gf, gg, go, cn, hn);
+                *(f4 *)&cell_dn[v * kO + 4 * q4] = cn;
+                *(f4 *)&hd_dn[v * kO + 4 * q4] = hn;
+                if (gates_dn) {
+                    float *gp = gates_dn + v * kG + 4 * q4;
+                    *(f4 *)&gp[0] = gi;
+                    *(f4 *)&gp[kO] = gf;
+                    *(f4 *)&gp[2 * kO] = gg;
+                    *(f4 *)&gp[3 * kO] = go;
                 }
             }
             __syncthreads();
@@ -291,12 +467,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
         // one cache writeback per workgroup and step instead of one per wave.
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
-        if (threadIdx.x == 0) {
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");   // L2 writeback
-            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);             // ... completed
-            __hip_atomic_store(&a.flags[blockIdx.x], t + 1, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        }
+        if (threadIdx.x == 0) publish(a, t + 1);
     }
 }
 
@@ -310,12 +481,18 @@ __global__ void k_fill_zero(int *p, int n)
 StripCostModel fwd_model(int C)
 {
     StripCostModel m;
-    m.fixed_bytes = (size_t)((9 * C + 3) / 4) * 256 * sizeof(float);   // wx fragments
+    m.fixed_bytes = (size_t)(((9 * C + 3) / 4) * 256 + kG) * sizeof(float);   // wx fragments, bias
     m.px_bytes = (size_t)(kHS + C) * sizeof(float);                     // h + x per pixel
     m.c_sync = 3.0;
     m.c_tile = 3.2;
     m.c_stage0 = 1.0;
     m.c_stage_px = 0.0031;
+    m.allow_resident = true;
+    m.res_px_bytes = (size_t)(2 * kHS + C) * sizeof(float);   // two h buffers + x
+    m.res_own_bytes = (size_t)kCS * sizeof(float) + 1 * sizeof(int);   // c + tile order
+    m.res_fixed_bytes = 16 * sizeof(int);                      // counters + alignment of c
+    m.res_max_staged = kResX * kThreads / C;                   // x_t fits the registers
+    m.c_res_step = 1.6;
     return m;
 }
 
@@ -355,16 +532,24 @@ size_t sweep_fwd_ws(const Geom &g, bool training)
 }
 
 int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, const float *b,
-              float *hd, float *cell, float *gates, int *flags, hipStream_t st)
+              float *hd, float *cell, float *gates, int *flags, hipStream_t st,
+              bool allow_resident)
 {
     const DevInfo di = device_info();
     if (di.cus <= 0) return PLSTM_EHIP;
     const size_t lds_limit = (size_t)(di.max_lds > 0 ? di.max_lds : 65536) - 1024;
     const int budget = di.cus < 1024 ? di.cus : 1024;
-    const Plan pl = make_plan(g, budget, fwd_model(g.C), lds_limit);
+    StripCostModel model = fwd_model(g.C);
+    model.allow_resident = allow_resident;
+    const Plan pl = make_plan(g, budget, model, lds_limit);
     if (pl.blocks > budget) return PLSTM_EUNSUPPORTED;
-    for (int d = 0; d < kDirs; ++d)
+    for (int d = 0; d < kDirs; ++d) {
         if (pl.chunk_rows[d] < 1) return PLSTM_EUNSUPPORTED;
+        // a resident strip's x_t plane must fit the staging registers
+        if (pl.resident[d] &&
+            (long long)(g.dir[d].P + 2) * (pl.max_w[d] + 2) * g.C > (long long)kResX * kThreads)
+            return PLSTM_EUNSUPPORTED;
+    }
 
     SweepArgs args;
     args.g = g;
@@ -379,6 +564,7 @@ int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     for (int d = 0; d < kDirs; ++d) {
         args.chunk_rows[d] = pl.chunk_rows[d];
         args.max_w[d] = pl.max_w[d];
+        args.resident[d] = pl.resident[d];
     }
 
     k_fill_zero<<<(1025 + 255) / 256, 256, 0, st>>>(flags, 1025);

@@ -43,3 +43,21 @@ def say(*a):
     """Name the case before a GPU step (survives a crash of the process)."""
     print("[gpu-case]", *a, flush=True)
     sys.stdout.flush()
+
+
+def saved_view(saved, name, shape):
+    """One array of a training forward's `saved` buffer as float64 numpy, in
+    the layout the C header documents: gates, c^d, h^d, each starting at the
+    next 256-byte boundary, shape [6][N][D][H][W][4O or O]."""
+    N, D, H, W, C, O = shape
+    counts = {"gates": 6 * N * D * H * W * 4 * O, "cell": 6 * N * D * H * W * O,
+              "hd": 6 * N * D * H * W * O}
+    off = 0
+    for key in ("gates", "cell", "hd"):
+        off = (off + 255) // 256 * 256
+        if key == name:
+            break
+        off += counts[key] * 4
+    flat = saved[off:off + counts[name] * 4].view(torch.float32)
+    last = 4 * O if name == "gates" else O
+    return host(flat).reshape(6, N, D, H, W, last)

@@ -137,11 +137,11 @@ def test_binding_refuses_host_tensors():
 
 
 def test_path_knobs_and_timing_without_gpu():
-    for fn in (P.pyramid_lstm_set_forward_path, P.pyramid_lstm_set_backward_path):
-        for v in (1, 2, 0):
+    for fn, top in ((P.pyramid_lstm_set_forward_path, 3), (P.pyramid_lstm_set_backward_path, 2)):
+        for v in list(range(1, top + 1)) + [0]:
             fn(v)
         with pytest.raises(P.PyramidLSTMError):
-            fn(3)
+            fn(top + 1)
     P.pyramid_lstm_timing_enable(True)
     assert P.pyramid_lstm_timing_read() == {}
     P.pyramid_lstm_timing_enable(False)

@@ -12,7 +12,7 @@ import oracle
 import paper_1506_07452_amd as P
 import synth
 from paper_1506_07452_amd.network import LayerW, layer_backward, layer_forward
-from tests.gpu_util import DEV, TOL, dev, host, layer_dev, normwise, say
+from tests.gpu_util import DEV, TOL, dev, host, layer_dev, normwise, saved_view, say
 
 pytestmark = pytest.mark.gpu
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -57,6 +57,51 @@ def test_forward_matches_oracle(shape):
     torch.cuda.synchronize()
     err = normwise(host(h), ref)
     assert err <= TOL["f32"], err
+
+
+@pytest.fixture
+def chunked_sweep():
+    """Run the MFMA forward sweep with every strip staged chunk by chunk (no
+    strip kept whole in LDS), so both strip kinds are covered on small shapes."""
+    P.pyramid_lstm_set_forward_path(3)
+    yield
+    P.pyramid_lstm_set_forward_path(0)
+
+
+# O = 16 shapes of both strip kinds: several strips per direction, ragged
+# strips and tiles, single-row / single-column planes, C = 1..4.
+O16_SHAPES = [(1, 5, 37, 29, 3, 16), (3, 6, 20, 18, 2, 16), (1, 9, 2, 300, 4, 16),
+              (1, 12, 64, 50, 1, 16), (2, 17, 3, 1, 3, 16), (1, 30, 70, 9, 4, 16)]
+
+
+@pytest.mark.parametrize("shape", O16_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_chunked_sweep_matches_oracle(shape, chunked_sweep):
+    inst = instance(shape, 1200 + sum(shape))
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)
+    say("forward chunked", shape)
+    x, Ld = dev(inst.x), layer_dev(L)
+    h, _ = layer_forward(x, Ld)
+    assert normwise(host(h), ref["h"]) <= TOL["f32"]
+    h2, saved = layer_forward(x, Ld, training=True)
+    torch.cuda.synchronize()
+    assert torch.equal(h, h2)
+
+
+@pytest.mark.parametrize("shape", O16_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_sweep_saved_state_matches_oracle(shape):
+    """Training forward of the default sweep: the saved per-direction h^d,
+    c^d and gates match the oracle's, not only their sum."""
+    inst = instance(shape, 1300 + sum(shape))
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b, want_hd=True, want_saved=True)
+    say("forward saved", shape)
+    h, saved = layer_forward(dev(inst.x), layer_dev(L), training=True)
+    torch.cuda.synchronize()
+    assert normwise(host(h), ref["h"]) <= TOL["f32"]
+    for name in ("hd", "cell", "gates"):
+        got = saved_view(saved, name, shape)
+        assert normwise(got, ref[name]) <= TOL["f32"], name
 
 
 @pytest.mark.parametrize("shape", [(1, 5, 37, 29, 3, 16), (2, 4, 9, 7, 1, 16)],

@@ -126,6 +126,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-crop", default="48x120x120")
+    ap.add_argument("--separate-head", action="store_true",
+                    help="run the FC / softmax head as separate kernels instead of the fused one")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device three times (a plain copy kernel "
                          "of known size, to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -172,7 +174,8 @@ def main():
     torch.cuda.synchronize()
 
     def step():
-        return network_train_step(x, layers, fcs, head, labels, ws=ws)
+        return network_train_step(x, layers, fcs, head, labels, ws=ws,
+                                  fused_head=not args.separate_head)
 
     def fwd():
         return layer_forward(x, layers[0], False, ws=ws)

@@ -142,6 +142,31 @@ int pyramid_softmax_ce(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const v
                        void *loss, void *dx, void *dw, void *db, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* Bytes of workspace for pyramid_head_train, or 0 when the fused kernel does
+ * not cover (Cin, F, K). */
+size_t pyramid_head_workspace_size(int64_t M, int32_t Cin, int32_t F, int32_t K);
+
+/* The output end of a training step in one pass over the rows (fp32): the
+ * last per-voxel fully connected layer with tanh, the per-voxel linear layer
+ * + softmax and the mean cross-entropy (Section 2.3, "Fully-Connected Layer";
+ * Fig. 3), with the gradients of the loss:
+ *   y = tanh(w1 x + b1),  p = softmax(w2 y + b2),
+ *   loss = (1/M) sum_m -log p[m][labels[m]].
+ *   x [M][Cin] (16-byte aligned rows), w1 [F][Cin], b1 [F], w2 [K][F], b2 [K],
+ *   labels int32 [M] in [0, K) (an out-of-range label makes loss and the
+ *   gradients NaN).  Outputs, all overwritten: p [M][K], *loss (one float),
+ *   dx = dL/dx [M][Cin] (nullable), dw1 [F][Cin], db1 [F], dw2 [K][F], db2 [K].
+ * Gives the same values as pyramid_fc_tanh_forward + pyramid_softmax_ce +
+ * pyramid_fc_tanh_backward (deterministic sums, fixed order).  Covers
+ * (Cin, F) = (16, 32) and (32, 64) with K <= 16; other shapes return
+ * PLSTM_EUNSUPPORTED (the separate entry points cover every shape).
+ * ws: pyramid_head_workspace_size(M, Cin, F, K) bytes. */
+int pyramid_head_train(int64_t M, int32_t Cin, int32_t F, int32_t K, const void *x,
+                       const void *w1, const void *b1, const void *w2, const void *b2,
+                       const int32_t *labels, void *p, void *loss, void *dx, void *dw1,
+                       void *db1, void *dw2, void *db2, void *ws, size_t ws_bytes,
+                       void *stream);
+
 
 /* Optional kernel timing for measurement tools (off by default).
  * pyramid_lstm_timing_enable(1) clears earlier records and makes every later

@@ -19,6 +19,7 @@ __all__ = [
     "pyramid_lstm_status_string", "pyramid_lstm_workspace_size", "pyramid_lstm_saved_size",
     "pyramid_lstm_forward", "pyramid_lstm_backward", "pyramid_fc_tanh_forward",
     "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
+    "pyramid_head_workspace_size", "pyramid_head_train",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
     "pyramid_lstm_set_backward_path",
     "library_path", "load",
@@ -77,6 +78,10 @@ def load():
     lib.pyramid_fc_tanh_backward.restype = ctypes.c_int
     lib.pyramid_softmax_ce.argtypes = [i64, i32, i32, i32] + [vp] * 10 + [sz, vp]
     lib.pyramid_softmax_ce.restype = ctypes.c_int
+    lib.pyramid_head_workspace_size.argtypes = [i64, i32, i32, i32]
+    lib.pyramid_head_workspace_size.restype = sz
+    lib.pyramid_head_train.argtypes = [i64, i32, i32, i32] + [vp] * 14 + [sz, vp]
+    lib.pyramid_head_train.restype = ctypes.c_int
     lib.pyramid_lstm_timing_enable.argtypes = [ctypes.c_int]
     lib.pyramid_lstm_timing_enable.restype = ctypes.c_int
     lib.pyramid_lstm_timing_read.argtypes = [ctypes.c_int, ctypes.c_char_p,
@@ -200,6 +205,23 @@ def pyramid_softmax_ce(x, w, b, p, labels=None, loss=None, dx=None, dw=None, db=
         M, Cin, K, _DT[x.dtype], _ptr(x), _ptr(w), _ptr(b), _ptr(labels), _ptr(p), _ptr(loss),
         _ptr(dx), _ptr(dw), _ptr(db), _ptr(ws),
         0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_head_workspace_size(M: int, Cin: int, F: int, K: int) -> int:
+    return int(load().pyramid_head_workspace_size(M, Cin, F, K))
+
+
+def pyramid_head_train(x, w1, b1, w2, b2, labels, p, loss, dx, dw1, db1, dw2, db2, ws=None,
+                       stream=None):
+    """Fused FC tanh + linear + softmax + mean cross-entropy and their backward."""
+    M, Cin = x.shape
+    F, K = w1.shape[0], w2.shape[0]
+    if ws is None:
+        ws = _workspace(max(pyramid_head_workspace_size(M, Cin, F, K), 256), x.device)
+    _check("pyramid_head_train", load().pyramid_head_train(
+        M, Cin, F, K, _ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(labels), _ptr(p),
+        _ptr(loss), _ptr(dx), _ptr(dw1), _ptr(db1), _ptr(dw2), _ptr(db2), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def pyramid_lstm_timing_enable(on: bool) -> None:

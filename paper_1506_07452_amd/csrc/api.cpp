@@ -161,4 +161,34 @@ int pyramid_softmax_ce(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const v
                       (float *)dx, (float *)dw, (float *)db, ws, (hipStream_t)stream);
 }
 
+size_t pyramid_head_workspace_size(int64_t M, int32_t Cin, int32_t F, int32_t K)
+{
+    if (M < 1 || M > (1LL << 40) / 64 || !head_supported(Cin, F, K)) return 0;
+    const size_t need = head_ws(M, Cin, F, K);
+    return need < 256 ? 256 : need;
+}
+
+int pyramid_head_train(int64_t M, int32_t Cin, int32_t F, int32_t K, const void *x,
+                       const void *w1, const void *b1, const void *w2, const void *b2,
+                       const int32_t *labels, void *p, void *loss, void *dx, void *dw1,
+                       void *db1, void *dw2, void *db2, void *ws, size_t ws_bytes,
+                       void *stream)
+{
+    if (M < 1 || Cin < 1 || F < 1 || K < 1) return PLSTM_EINVAL;
+    if (!x || !w1 || !b1 || !w2 || !b2 || !labels || !p || !loss || !dw1 || !db1 || !dw2 ||
+        !db2 || !ws)
+        return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(w1) || !aligned(b1) || !aligned(w2) || !aligned(b2) ||
+        !aligned(labels) || !aligned(p) || !aligned(loss) || (dx && !aligned(dx)) ||
+        !aligned(dw1) || !aligned(db1) || !aligned(dw2) || !aligned(db2) || !aligned(ws))
+        return PLSTM_EINVAL;
+    const size_t need = pyramid_head_workspace_size(M, Cin, F, K);
+    if (need == 0) return PLSTM_EUNSUPPORTED;
+    if (ws_bytes < need) return PLSTM_EWORKSPACE;
+    return head_train(M, Cin, F, K, (const float *)x, (const float *)w1, (const float *)b1,
+                      (const float *)w2, (const float *)b2, labels, (float *)p, (float *)loss,
+                      (float *)dx, (float *)dw1, (float *)db1, (float *)dw2, (float *)db2, ws,
+                      (hipStream_t)stream);
+}
+
 }  // extern "C"

@@ -140,5 +140,12 @@ size_t fc_ws(long long M, int Cin, int Cout);
 int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void *w,
                const void *b, const int32_t *labels, float *p, float *loss, float *dx,
                float *dw, float *db, void *ws, hipStream_t st);
+// Fused FC + tanh, linear + softmax, cross-entropy and backward (fp32).
+bool head_supported(int Cin, int F, int K);
+size_t head_ws(long long M, int Cin, int F, int K);
+int head_train(long long M, int Cin, int F, int K, const float *x, const float *w1,
+               const float *b1, const float *w2, const float *b2, const int32_t *labels,
+               float *p, float *loss, float *dx, float *dw1, float *db1, float *dw2, float *db2,
+               void *ws, hipStream_t st);
 
 }  // namespace plstm

@@ -4,6 +4,7 @@
 // gradient for training.  Weight-gradient sums over voxels are deterministic
 // two-stage reductions (fixed chunking, fixed order).
 #include "common.h"
+#include "timing.h"
 
 namespace plstm {
 namespace {
@@ -373,6 +374,321 @@ k_softmax_rows(long long M, int Cin, int K, const TS *__restrict__ x, const TS *
     }
 }
 
+// ---- fused head: FC + tanh, linear + softmax, cross-entropy, backward --------
+// Every row is read once and only p and dx are written per row.  A wave
+// takes 16 rows at a time and runs the whole chain as MFMA contractions
+// whose outputs feed the next one in registers (v_mfma_f32_16x16x4f32: lane
+// l gives A[l%16][k], B[k][l%16] and holds D[4(l/16) + i][l%16]; with rows on
+// N, lane (q = l/16, col = l%16) holds units 4q..4q+3 of row col, which is
+// exactly the B operand of the next contraction when its K index for lane
+// group q and k-step i is unit 4q + i):
+//   Z^T = W1 X^T + b1,  y = tanh z,  L^T = W2 Y^T + b2,  p = softmax over the
+//   lane groups,  dl = (p - onehot) / M,  dY^T = W2^T dl^T,  dz = dy (1 - y^2),
+//   dX^T = W1^T dz^T.
+// The weight gradients sum over rows (K = rows), so dz, dl, x and y of the 16
+// rows are transposed through a per-wave LDS tile; dW1 = dz^T x and
+// dW2 = dl^T y accumulate in VGPRs over all rows of the wave, the bias
+// gradients as per-lane sums.  Workgroup partials are summed in a fixed
+// order (deterministic).
+constexpr int kHW = 4;              // waves per workgroup of the fused head
+constexpr int kHT = 64 * kHW;
+
+// tanh(a) = 1 - 2 / (e^{2a} + 1), branch-free (saturates to +-1).
+__device__ inline float tanh_fast(float a)
+{
+    return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * a) + 1.0f);
+}
+
+template <int CIN, int F>
+struct HeadCfg {
+    static constexpr int CT = CIN / 16, FT = F / 16;
+    static constexpr int XP = CIN + 4, YP = F + 4, LP = 20;   // LDS row pitches (floats)
+    static constexpr int per_wave = 16 * (XP + 2 * YP + LP);
+    static constexpr int red = F * (CIN + 1) + 16 * (F + 1) + 1;
+    static constexpr size_t bytes = (size_t)(kHW * per_wave + red) * sizeof(float);
+};
+
+template <int CIN, int F>
+__global__ void __launch_bounds__(kHT)
+k_head_train(long long M, int K, const float *__restrict__ x, const float *__restrict__ w1,
+             const float *__restrict__ b1, const float *__restrict__ w2,
+             const float *__restrict__ b2, const int32_t *__restrict__ labels,
+             float *__restrict__ p, float *__restrict__ dx, float *__restrict__ partial)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    using HC = HeadCfg<CIN, F>;
+    static_assert(CIN % 16 == 0 && F % 16 == 0, "tile multiples");
+    constexpr int CT = HC::CT, FT = HC::FT;
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int q = lane >> 4, col = lane & 15;
+    float *xs = lds + wave * HC::per_wave;   // [16][XP]  x
+    float *ys = xs + 16 * HC::XP;            // [16][YP]  y
+    float *zs = ys + 16 * HC::YP;            // [16][YP]  dz
+    float *ls = zs + 16 * HC::YP;            // [16][LP]  dl (zero beyond K)
+    float *R = lds + kHW * HC::per_wave;     // workgroup reduction
+
+    // ---- weights as MFMA A fragments, for the whole kernel ---------------
+    float a1[FT][CT][4];   // W1[f = 16mt + col][c = 16kt + 4q + i]
+    float a2[FT][4];       // W2[k = col][f = 16mt + 4q + i]
+    float a3[FT][4];       // W2[k = 4q + i][f = 16mt + col]
+    float a4[CT][FT][4];   // W1[f = 16mt + 4q + i][c = 16ct + col]
+    f4 bias1[FT], bias2;
+#pragma unroll
+    for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int kt = 0; kt < CT; ++kt) {
+                a1[mt][kt][i] = w1[(16 * mt + col) * CIN + 16 * kt + 4 * q + i];
+                a4[kt][mt][i] = w1[(16 * mt + 4 * q + i) * CIN + 16 * kt + col];
+            }
+            a2[mt][i] = col < K ? w2[col * F + 16 * mt + 4 * q + i] : 0.0f;
+            a3[mt][i] = 4 * q + i < K ? w2[(4 * q + i) * F + 16 * mt + col] : 0.0f;
+            bias1[mt][i] = b1[16 * mt + 4 * q + i];
+        }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) bias2[i] = 4 * q + i < K ? b2[4 * q + i] : 0.0f;
+
+    f4 g1[FT][CT], g2[FT], gb1[FT], gb2 = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int mt = 0; mt < FT; ++mt) {
+        g2[mt] = gb1[mt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) g1[mt][ct] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    float lacc = 0.0f;
+    const float inv_m = 1.0f / (float)M;
+    const long long nsub = (M + 15) / 16;
+    const long long gw = (long long)blockIdx.x * kHW + wave, nw = (long long)gridDim.x * kHW;
+    // the next 16 rows and labels are loaded while these compute
+    f4 xn[CT];
+    int labn;
+    auto load = [&](long long st) {
+        const long long row = st * 16 + col;
+        const bool v = st < nsub && row < M;
+#pragma unroll
+        for (int kt = 0; kt < CT; ++kt) xn[kt] = *(const f4 *)&x[(v ? row : 0) * CIN + 16 * kt + 4 * q];
+        labn = labels[v ? row : 0];
+    };
+    load(gw);
+    for (long long st = gw; st < nsub; st += nw) {
+        const long long row = st * 16 + col;
+        const bool valid = row < M;
+        f4 xv[CT];
+#pragma unroll
+        for (int kt = 0; kt < CT; ++kt) xv[kt] = valid ? xn[kt] : f4{0.0f, 0.0f, 0.0f, 0.0f};
+        const int lab = labn;
+        load(st + nw);
+        // ---- forward: y = tanh(W1 x + b1), logits = W2 y + b2 ------------
+        f4 yv[FT];
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt) {
+            f4 acc = bias1[mt];
+#pragma unroll
+            for (int kt = 0; kt < CT; ++kt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[mt][kt][i], xv[kt][i], acc, 0,
+                                                               0, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) yv[mt][i] = tanh_fast(acc[i]);
+        }
+        f4 lg = bias2;
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                lg = __builtin_amdgcn_mfma_f32_16x16x4f32(a2[mt][i], yv[mt][i], lg, 0, 0, 0);
+        // ---- softmax over classes 4q + i, spread over the four lane groups
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (4 * q + i < K) mx = fmaxf(mx, lg[i]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        f4 pv;
+        float sum = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            pv[i] = 4 * q + i < K ? __expf(lg[i] - mx) : 0.0f;
+            sum += pv[i];
+        }
+        sum += __shfl_xor(sum, 16);
+        sum += __shfl_xor(sum, 32);
+        const float inv = 1.0f / sum;
+        pv *= inv;
+        const bool ok = lab >= 0 && lab < K;     // an out-of-range label poisons with NaN
+        f4 dl;
+        float pl = 1.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int k = 4 * q + i;
+            if (k == lab) pl = pv[i];
+            const float g = ok ? (pv[i] - (k == lab ? 1.0f : 0.0f)) * inv_m : NAN;
+            dl[i] = (valid && k < K) ? g : 0.0f;
+        }
+        if (valid) {
+            if ((K & 3) == 0) {
+                if (4 * q < K) *(f4 *)&p[row * K + 4 * q] = pv;
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (4 * q + i < K) p[row * K + 4 * q + i] = pv[i];
+            }
+            // the lane holding the label's class adds -log p; a bad label adds NaN once
+            if (ok ? (lab >> 2) == q : q == 0) lacc += ok ? -logf(pl) : NAN;
+        }
+        // ---- backward: dz = (W2^T dl) (1 - y^2), dx = W1^T dz -------------
+        f4 dz[FT];
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt) {
+            f4 acc = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a3[mt][i], dl[i], acc, 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dz[mt][i] = acc[i] * (1.0f - yv[mt][i] * yv[mt][i]);
+            gb1[mt] += dz[mt];
+        }
+        gb2 += dl;
+        if (dx) {
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                f4 acc = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[ct][mt][i], dz[mt][i], acc,
+                                                                   0, 0, 0);
+                if (valid) *(f4 *)&dx[row * CIN + 16 * ct + 4 * q] = acc;
+            }
+        }
+        // ---- weight gradients over these 16 rows (K = rows) ----------------
+#pragma unroll
+        for (int kt = 0; kt < CT; ++kt) *(f4 *)&xs[col * HC::XP + 16 * kt + 4 * q] = xv[kt];
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt) {
+            *(f4 *)&ys[col * HC::YP + 16 * mt + 4 * q] = yv[mt];
+            *(f4 *)&zs[col * HC::YP + 16 * mt + 4 * q] = dz[mt];
+        }
+        *(f4 *)&ls[col * HC::LP + 4 * q] = dl;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int r = 4 * ks + q;
+            const float al = ls[r * HC::LP + col];
+#pragma unroll
+            for (int mt = 0; mt < FT; ++mt) {
+                const float az = zs[r * HC::YP + 16 * mt + col];
+                const float by = ys[r * HC::YP + 16 * mt + col];
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+                    g1[mt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        az, xs[r * HC::XP + 16 * ct + col], g1[mt][ct], 0, 0, 0);
+                g2[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(al, by, g2[mt], 0, 0, 0);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    // ---- bias sums over the 16 row lanes of each lane group, loss over the wave
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) gb1[mt][i] += __shfl_xor(gb1[mt][i], off);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gb2[i] += __shfl_xor(gb2[i], off);
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) lacc += __shfl_xor(lacc, off);
+    // ---- workgroup sum in wave order: [F][CIN + 1], [K][F + 1], loss --------
+    constexpr int P1 = F * (CIN + 1);
+    const int P2 = K * (F + 1), PT = P1 + P2 + 1;
+    for (int w = 0; w < kHW; ++w) {
+        if (wave == w) {
+            auto put = [&](int idx, float v) { R[idx] = w == 0 ? v : R[idx] + v; };
+#pragma unroll
+            for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int f = 16 * mt + 4 * q + i;
+#pragma unroll
+                    for (int ct = 0; ct < CT; ++ct) put(f * (CIN + 1) + 16 * ct + col, g1[mt][ct][i]);
+                    if (col == 0) put(f * (CIN + 1) + CIN, gb1[mt][i]);
+                    const int k = 4 * q + i;
+                    if (k < K) put(P1 + k * (F + 1) + 16 * mt + col, g2[mt][i]);
+                }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (col == 0 && 4 * q + i < K) put(P1 + (4 * q + i) * (F + 1) + F, gb2[i]);
+            if (lane == 0) put(P1 + P2, lacc);
+        }
+        __syncthreads();
+    }
+    float *part = partial + (long long)blockIdx.x * PT;
+    for (int e = threadIdx.x; e < PT; e += kHT) part[e] = R[e];
+}
+
+// Sums the per-block partials in block order and scatters them to the outputs.
+__global__ void __launch_bounds__(kThreads)
+k_head_reduce(long long M, int Cin, int F, int K, int nblk, const float *__restrict__ partial,
+              float *__restrict__ dw1, float *__restrict__ db1, float *__restrict__ dw2,
+              float *__restrict__ db2, float *__restrict__ loss)
+{
+    const int P1 = F * (Cin + 1), P2 = K * (F + 1), PT = P1 + P2 + 1;
+    const int i = blockIdx.x * kThreads + threadIdx.x;
+    if (i >= PT) return;
+    float acc = 0.0f;
+    for (int b = 0; b < nblk; ++b) acc += partial[(long long)b * PT + i];
+    if (i < P1) {
+        const int f = i / (Cin + 1), c = i % (Cin + 1);
+        if (c < Cin) dw1[f * Cin + c] = acc;
+        else db1[f] = acc;
+    } else if (i < P1 + P2) {
+        const int k = (i - P1) / (F + 1), f = (i - P1) % (F + 1);
+        if (f < F) dw2[k * F + f] = acc;
+        else db2[k] = acc;
+    } else {
+        *loss = acc / (float)M;
+    }
+}
+
+constexpr int kHeadMaxBlocks = 1024;
+
+inline int head_blocks(long long M)
+{
+    const long long t = (M + 16 * kHW - 1) / (16 * kHW);
+    return (int)(t < kHeadMaxBlocks ? t : kHeadMaxBlocks);
+}
+
+template <int CIN, int F>
+int head_launch(long long M, int K, const float *x, const float *w1, const float *b1,
+                const float *w2, const float *b2, const int32_t *labels, float *p, float *loss,
+                float *dx, float *dw1, float *db1, float *dw2, float *db2, float *partial,
+                hipStream_t st)
+{
+    const int nb = head_blocks(M);
+    const size_t lds = HeadCfg<CIN, F>::bytes;
+    timing_begin("head_fused", st);
+    (void)hipFuncSetAttribute((const void *)k_head_train<CIN, F>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    k_head_train<CIN, F><<<nb, kHT, lds, st>>>(M, K, x, w1, b1, w2, b2, labels, p, dx, partial);
+    PLSTM_LAUNCH_CHECK();
+    const int PT = F * (CIN + 1) + K * (F + 1) + 1;
+    k_head_reduce<<<(PT + kThreads - 1) / kThreads, kThreads, 0, st>>>(
+        M, CIN, F, K, nb, partial, dw1, db1, dw2, db2, loss);
+    PLSTM_LAUNCH_CHECK();
+    timing_end(2, st);
+    return PLSTM_OK;
+}
+
 inline long long fc_chunk_len(long long M) {
     long long len = 8192;
     if ((M + len - 1) / len > 4096) len = (M + 4095) / 4096;
@@ -422,8 +738,8 @@ size_t fc_ws(long long M, int Cin, int Cout)
     return cv.off;
 }
 
-int fc_tanh_forward(long long M, int Cin, int Cout, int dtype, const void *x, const void *w,
-                    const void *b, void *y, hipStream_t st)
+static int fc_tanh_forward_impl(long long M, int Cin, int Cout, int dtype, const void *x,
+                                const void *w, const void *b, void *y, hipStream_t st)
 {
     if (rows_ok(Cin)) {
         const dim3 grid((unsigned)((M + kRB - 1) / kRB), (Cout + kOC - 1) / kOC);
@@ -451,9 +767,9 @@ int fc_tanh_forward(long long M, int Cin, int Cout, int dtype, const void *x, co
     return PLSTM_OK;
 }
 
-int fc_tanh_backward(long long M, int Cin, int Cout, const float *x, const float *w,
-                     const float *y, const float *dy, float *dx, float *dw, float *db,
-                     void *ws, hipStream_t st)
+static int fc_tanh_backward_impl(long long M, int Cin, int Cout, const float *x,
+                                 const float *w, const float *y, const float *dy, float *dx,
+                                 float *dw, float *db, void *ws, hipStream_t st)
 {
     Carve cv(ws);
     float *partial = cv.take<float>((size_t)fc_chunks(M) * Cout * (Cin + 1));
@@ -465,9 +781,10 @@ int fc_tanh_backward(long long M, int Cin, int Cout, const float *x, const float
     return fc_wgrad(M, Cin, Cout, rg, x, dw, db, partial, st);
 }
 
-int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void *w,
-               const void *b, const int32_t *labels, float *p, float *loss, float *dx,
-               float *dw, float *db, void *ws, hipStream_t st)
+static int softmax_ce_impl(long long M, int Cin, int K, int dtype, const void *x,
+                           const void *w, const void *b, const int32_t *labels, float *p,
+                           float *loss, float *dx, float *dw, float *db, void *ws,
+                           hipStream_t st)
 {
     Carve cv(ws);
     float *partial = cv.take<float>((size_t)fc_chunks(M) * K * (Cin + 1));
@@ -504,6 +821,60 @@ int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void
         if (rc != PLSTM_OK) return rc;
     }
     return fc_wgrad(M, Cin, K, rg, (const float *)x, dw, db, partial, st);
+}
+
+int fc_tanh_forward(long long M, int Cin, int Cout, int dtype, const void *x, const void *w,
+                    const void *b, void *y, hipStream_t st)
+{
+    timing_begin("fc_tanh_fwd", st);
+    const int rc = fc_tanh_forward_impl(M, Cin, Cout, dtype, x, w, b, y, st);
+    timing_end(1, st);
+    return rc;
+}
+
+int fc_tanh_backward(long long M, int Cin, int Cout, const float *x, const float *w,
+                     const float *y, const float *dy, float *dx, float *dw, float *db,
+                     void *ws, hipStream_t st)
+{
+    timing_begin("fc_tanh_bwd", st);
+    const int rc = fc_tanh_backward_impl(M, Cin, Cout, x, w, y, dy, dx, dw, db, ws, st);
+    timing_end(dx ? 3 : 2, st);
+    return rc;
+}
+
+int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void *w,
+               const void *b, const int32_t *labels, float *p, float *loss, float *dx,
+               float *dw, float *db, void *ws, hipStream_t st)
+{
+    timing_begin("softmax_ce", st);
+    const int rc = softmax_ce_impl(M, Cin, K, dtype, x, w, b, labels, p, loss, dx, dw, db, ws, st);
+    timing_end(1 + (labels ? 1 : 0) + (dw ? 2 : 0) + (dx ? 1 : 0), st);
+    return rc;
+}
+
+bool head_supported(int Cin, int F, int K)
+{
+    return K >= 1 && K <= 16 && ((Cin == 16 && F == 32) || (Cin == 32 && F == 64));
+}
+
+size_t head_ws(long long M, int Cin, int F, int K)
+{
+    return (size_t)head_blocks(M) * (F * (Cin + 1) + K * (F + 1) + 1) * sizeof(float);
+}
+
+int head_train(long long M, int Cin, int F, int K, const float *x, const float *w1,
+               const float *b1, const float *w2, const float *b2, const int32_t *labels,
+               float *p, float *loss, float *dx, float *dw1, float *db1, float *dw2, float *db2,
+               void *ws, hipStream_t st)
+{
+    float *partial = (float *)ws;
+    if (Cin == 16 && F == 32)
+        return head_launch<16, 32>(M, K, x, w1, b1, w2, b2, labels, p, loss, dx, dw1, db1, dw2,
+                                   db2, partial, st);
+    if (Cin == 32 && F == 64)
+        return head_launch<32, 64>(M, K, x, w1, b1, w2, b2, labels, p, loss, dx, dw1, db1, dw2,
+                                   db2, partial, st);
+    return PLSTM_EUNSUPPORTED;
 }
 
 }  // namespace plstm

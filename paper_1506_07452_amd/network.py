@@ -13,8 +13,9 @@ from typing import List, Optional, Tuple
 import torch
 
 from . import (plstm_shape, pyramid_fc_tanh_backward, pyramid_fc_tanh_forward,
-               pyramid_lstm_backward, pyramid_lstm_forward, pyramid_lstm_saved_size,
-               pyramid_lstm_workspace_size, pyramid_softmax_ce, shape_for)
+               pyramid_head_train, pyramid_head_workspace_size, pyramid_lstm_backward,
+               pyramid_lstm_forward, pyramid_lstm_saved_size, pyramid_lstm_workspace_size,
+               pyramid_softmax_ce, shape_for)
 
 
 @dataclass
@@ -93,10 +94,62 @@ def network_forward(x, layers: List[LayerW], fcs: List[Tuple[torch.Tensor, torch
     return out
 
 
-def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None):
+def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None, fused_head=True):
     """Forward + back-propagation through the whole network (fp32).
     Returns dict with 'loss', 'p', 'head' (dw, db), 'fcs' [(dw, db)],
-    'layers' [(dwx, dwh, db)]."""
+    'layers' [(dwx, dwh, db)].  With `fused_head` (default) the last FC + tanh,
+    the softmax head, the loss and their backward run as one pass over the
+    voxels (pyramid_head_train) where it covers the widths."""
+    N, D, H, W, _ = x.shape
+    M = N * D * H * W
+    nl = len(layers)
+    O_last, F_last, K = layers[-1].O, fcs[-1][0].shape[0], head[0].shape[0]
+    if not (fused_head and pyramid_head_workspace_size(M, O_last, F_last, K) > 0):
+        return _train_step_unfused(x, layers, fcs, head, labels, ws, stream)
+    a = x
+    acts = []
+    for li in range(nl):
+        h, saved = layer_forward(a, layers[li], True, ws, stream)
+        act = {"in": a, "h": h, "saved": saved}
+        if li < nl - 1:
+            wf, bf = fcs[li]
+            y = torch.empty((N, D, H, W, wf.shape[0]), dtype=a.dtype, device=a.device)
+            pyramid_fc_tanh_forward(h.view(M, -1), wf, bf, y.view(M, -1), stream)
+            act["y"] = y
+            a = y
+        acts.append(act)
+    p = torch.empty((M, K), dtype=torch.float32, device=x.device)
+    loss = torch.empty(1, dtype=torch.float32, device=x.device)
+    dh = torch.empty((M, O_last), dtype=torch.float32, device=x.device)
+    wf, bf = fcs[-1]
+    dwf, dbf = torch.empty_like(wf), torch.empty_like(bf)
+    dw, db = torch.empty_like(head[0]), torch.empty_like(head[1])
+    pyramid_head_train(acts[-1]["h"].view(M, O_last), wf, bf, head[0], head[1], labels, p, loss,
+                       dh, dwf, dbf, dw, db, stream=stream)
+    fc_grads = [None] * len(fcs)
+    layer_grads = [None] * nl
+    fc_grads[-1] = (dwf, dbf)
+    g = None
+    for li in range(nl - 1, -1, -1):
+        act = acts[li]
+        O = act["h"].shape[-1]
+        if li < nl - 1:
+            wf, _ = fcs[li]
+            dh = torch.empty((M, O), dtype=torch.float32, device=x.device)
+            dwf, dbf = torch.empty_like(wf), torch.empty(wf.shape[0], device=x.device)
+            pyramid_fc_tanh_backward(act["h"].view(M, O), wf, act["y"].view(M, -1),
+                                     g.view(M, -1), dh, dwf, dbf, stream=stream)
+            fc_grads[li] = (dwf, dbf)
+        dx, dwx, dwh, db_l = layer_backward(act["in"], layers[li], act["saved"],
+                                            dh.view(act["h"].shape), want_dx=li > 0, ws=ws,
+                                            stream=stream)
+        layer_grads[li] = (dwx, dwh, db_l)
+        g = dx
+    return {"loss": loss, "p": p, "head": (dw, db), "fcs": fc_grads, "layers": layer_grads}
+
+
+def _train_step_unfused(x, layers, fcs, head, labels, ws=None, stream=None):
+    """network_train_step composed from the separate FC / softmax entry points."""
     out = network_forward(x, layers, fcs, head, labels, training=True, ws=ws, stream=stream)
     acts = out["acts"]
     g = out["dlast"]

@@ -128,6 +128,28 @@ def test_fc_validation(lib):
                                   None, FAKE, 8, None) == -3
 
 
+def test_head_validation(lib):
+    assert lib.pyramid_head_workspace_size(1000, 16, 32, 4) > 0
+    assert lib.pyramid_head_workspace_size(1000, 32, 64, 16) > 0
+    for bad in ((1000, 16, 33, 4), (1000, 8, 32, 4), (1000, 16, 32, 17), (0, 16, 32, 4)):
+        assert lib.pyramid_head_workspace_size(*bad) == 0, bad
+    args = [FAKE] * 13
+    def call(M=1000, Cin=16, F=32, K=4, nbytes=1 << 30, **over):
+        a = list(args)
+        names = ["x", "w1", "b1", "w2", "b2", "labels", "p", "loss", "dx", "dw1", "db1", "dw2",
+                 "db2"]
+        for k, v in over.items():
+            a[names.index(k)] = v
+        return lib.pyramid_head_train(M, Cin, F, K, *a, FAKE, nbytes, None)
+    assert call(Cin=8) == -2
+    assert call(K=17) == -2
+    assert call(M=0) == -1
+    assert call(labels=None) == -1
+    assert call(dw2=None) == -1
+    assert call(x=ctypes.c_void_p(0x10008)) == -1
+    assert call(nbytes=16) == -3
+
+
 def test_binding_refuses_host_tensors():
     import torch
     x = torch.zeros(1, 2, 2, 2, 1)

@@ -49,13 +49,14 @@ def test_small_network_forward(dtype):
     assert normwise(host(out["p"]), ref) <= TOL[dtype]
 
 
-def test_small_network_training_step():
+@pytest.mark.parametrize("fused", [True, False], ids=["fused_head", "separate_head"])
+def test_small_network_training_step(fused):
     inst = small(dict(N=1, D=5, H=12, W=7, C=3, hidden=[16, 32], fc=True, classes=4,
                       labels=True), 80)
     ref = onet.backward(inst.x, *oracle_args(inst), inst.labels)
-    say("small network training step")
+    say("small network training step", fused)
     x, layers, fcs, head, labels = to_device(inst, "f32")
-    g = network_train_step(x, layers, fcs, head, labels)
+    g = network_train_step(x, layers, fcs, head, labels, fused_head=fused)
     torch.cuda.synchronize()
     assert abs(g["loss"].item() - ref["loss"]) <= TOL["f32"] * abs(ref["loss"])
     pairs = [(g["head"][0], ref["head"][0]), (g["head"][1], ref["head"][1])]
@@ -98,6 +99,85 @@ def test_fc_and_softmax_match_oracle():
     assert abs(loss.item() - rs["loss"]) <= TOL["f32"] * rs["loss"]
     for got, want in ((ldx, rs["dx"]), (ldw, rs["dw"]), (ldb, rs["db"])):
         assert normwise(host(got), want) <= TOL["f32"]
+
+
+def oracle_head(xa, w1, b1, w2, b2, lab):
+    """FC tanh -> softmax CE -> backward, chained from the oracle's pieces."""
+    ry = oracle.fc_tanh_forward(xa, w1, b1)
+    rs = oracle.softmax_ce(ry, w2, b2, lab, grad=True)
+    rb = oracle.fc_tanh_backward(xa, w1, ry, rs["dx"])
+    return {"p": rs["p"], "loss": rs["loss"], "dx": rb["dx"], "dw1": rb["dw"], "db1": rb["db"],
+            "dw2": rs["dw"], "db2": rs["db"]}
+
+
+# (M, Cin, F, K): one row, one ragged tile, several tiles, more row tiles
+# than workgroups (each workgroup loops), K at both padded widths.
+HEAD_CASES = [(1, 16, 32, 4), (129, 16, 32, 3), (1000, 16, 32, 4), (777, 32, 64, 5),
+              (300, 16, 32, 16), (140001, 16, 32, 4), (2049, 32, 64, 2)]
+
+
+@pytest.mark.parametrize("case", HEAD_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_fused_head_matches_oracle(case):
+    import paper_1506_07452_amd as P
+    M, Cin, F, K = case
+    rng = np.random.default_rng(91 + sum(case))
+    xa = rng.standard_normal((M, Cin)).astype(np.float32)
+    w1 = rng.uniform(-0.3, 0.3, (F, Cin)).astype(np.float32)
+    b1 = rng.uniform(-0.3, 0.3, F).astype(np.float32)
+    w2 = rng.uniform(-0.3, 0.3, (K, F)).astype(np.float32)
+    b2 = rng.uniform(-0.3, 0.3, K).astype(np.float32)
+    lab = rng.integers(0, K, M).astype(np.int32)
+    say("fused head", case)
+    out = {k: torch.empty(shp, device=DEV) for k, shp in
+           (("p", (M, K)), ("loss", (1,)), ("dx", (M, Cin)), ("dw1", (F, Cin)), ("db1", (F,)),
+            ("dw2", (K, F)), ("db2", (K,)))}
+    P.pyramid_head_train(dev(xa), dev(w1), dev(b1), dev(w2), dev(b2),
+                         torch.from_numpy(lab).to(DEV), out["p"], out["loss"], out["dx"],
+                         out["dw1"], out["db1"], out["dw2"], out["db2"])
+    torch.cuda.synchronize()
+    ref = oracle_head(xa, w1, b1, w2, b2, lab)
+    assert abs(out["loss"].item() - ref["loss"]) <= TOL["f32"] * ref["loss"]
+    for k in ("p", "dx", "dw1", "db1", "dw2", "db2"):
+        assert normwise(host(out[k]), ref[k]) <= TOL["f32"], k
+
+
+def test_fused_head_without_dx_and_bad_label():
+    """dx is optional; an out-of-range label turns the loss into NaN."""
+    import paper_1506_07452_amd as P
+    M, Cin, F, K = 300, 16, 32, 4
+    rng = np.random.default_rng(5)
+    args = [dev(rng.uniform(-0.3, 0.3, s).astype(np.float32))
+            for s in ((M, Cin), (F, Cin), (F,), (K, F), (K,))]
+    lab = torch.from_numpy(rng.integers(0, K, M).astype(np.int32)).to(DEV)
+    outs = [torch.empty(s, device=DEV) for s in ((M, K), (1,), (F, Cin), (F,), (K, F), (K,))]
+    say("fused head no dx")
+    P.pyramid_head_train(*args, lab, outs[0], outs[1], None, *outs[2:])
+    torch.cuda.synchronize()
+    assert torch.isfinite(outs[1]).all()
+    lab[7] = K
+    P.pyramid_head_train(*args, lab, outs[0], outs[1], None, *outs[2:])
+    torch.cuda.synchronize()
+    assert torch.isnan(outs[1]).all()
+
+
+def test_fused_training_step_matches_unfused():
+    """The training step with the fused head equals the one composed from the
+    separate entry points (same math, different summation order)."""
+    inst = small(dict(N=1, D=6, H=20, W=18, C=3, hidden=[16, 32], fc=True, classes=4,
+                      labels=True), 81)
+    x, layers, fcs, head, labels = to_device(inst, "f32")
+    say("fused vs unfused step")
+    a = network_train_step(x, layers, fcs, head, labels, fused_head=True)
+    b = network_train_step(x, layers, fcs, head, labels, fused_head=False)
+    torch.cuda.synchronize()
+    assert abs(a["loss"].item() - b["loss"].item()) <= 1e-5 * abs(b["loss"].item())
+    pairs = [(a["p"], b["p"])] + list(zip(a["head"], b["head"]))
+    for fa, fb in zip(a["fcs"], b["fcs"]):
+        pairs += list(zip(fa, fb))
+    for la, lb in zip(a["layers"], b["layers"]):
+        pairs += list(zip(la, lb))
+    for ta, tb in pairs:
+        assert normwise(host(ta), host(tb)) <= TOL["f32"]
 
 
 def test_config4_network_forward_bf16():

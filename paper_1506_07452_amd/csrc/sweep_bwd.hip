@@ -433,6 +433,200 @@ __global__ void __launch_bounds__(kThreads, 1) k_wgrad(WgradArgs a)
     }
 }
 
+// ---- parameter gradients, register-streamed --------------------------------
+// dW[d] = sum over voxels v of dA[v] (x) [im2col(h_{t-1})(v), im2col(x_t)(v), 1],
+// an implicit GEMM with M = 64 gate-units, N = 144 + 9C + 1 and K = voxels.
+// A team of two waves owns a contiguous range of rows (fixed plane and
+// first in-plane index) of one direction and walks them 16 voxels (four
+// MFMA k-steps) at a time; wave h of the team holds the output tiles of its
+// half of N.  Operands come straight from global memory into registers
+// (lane group q takes voxel 4 ks + q, lane col takes a gate-unit (A) or an
+// im2col column (B), so every load is 64 contiguous bytes per voxel), the
+// next group's loads are in flight while the current group's MFMAs run,
+// and the accumulators stay in VGPRs for the whole launch: no LDS, no
+// barriers.  Zero padding (off-plane taps, h_{-1}) comes from clamped
+// addresses and selects.
+constexpr int kWgWaves = 4;                    // two teams per workgroup
+constexpr int kWgTeamsPerDir = 170;
+
+struct WgRowArgs {
+    Geom g;
+    const float *x, *hd, *dA;
+    float *partial;     // [6][tpd][64][KCp]
+    int tpd;            // teams per direction
+    int KCp;            // columns padded to 16
+};
+
+template <int C> struct WgN {
+    static constexpr int NT = (144 + 9 * C + 1 + 15) / 16;   // N-tiles
+    static constexpr int NT_LO = (NT + 1) / 2;               // tiles of wave 0 of a team
+};
+
+// Cursor of a team: batch element, sweep step, row, group of 16 columns.
+struct WgCursor {
+    int n, t, p, qg;
+};
+
+template <int C, int NT0, int NTC>
+__device__ inline void wg_rows_team(const WgRowArgs &a, int d, long long r0, long long r1, int q,
+                                    int col, float *out)
+{
+    const DirGeom dg = a.g.dir[d];
+    const long long V = a.g.V;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int ngrp = (dg.Q + 15) >> 4;
+    // per-lane constants of the input-tap columns (tiles 9, 10, ...)
+    int xtap_dp[NTC], xtap_dq[NTC], xtap_c[NTC], xkind[NTC];   // kind 0: x, 1: one, 2: zero
+#pragma unroll
+    for (int j = 0; j < NTC; ++j) {
+        const int nt = NT0 + j;
+        const int kk = (nt - 9) * 16 + col;
+        const int tap = kk < 9 * C && kk >= 0 ? kk / C : 4;
+        xtap_dp[j] = tap / 3 - 1;
+        xtap_dq[j] = tap % 3 - 1;
+        xtap_c[j] = kk >= 0 && kk < 9 * C ? kk % C : 0;
+        xkind[j] = kk < 9 * C ? 0 : (kk == 9 * C ? 1 : 2);
+    }
+    f4 acc[4][NTC];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int j = 0; j < NTC; ++j) acc[g][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    struct Ops {
+        float a[4][4];      // [k-step][gate]
+        float b[4][NTC];    // [k-step][tile]
+    };
+    // K order inside a group of 16 voxels: lane group q takes voxels
+    // 4q .. 4q+3 (k-step ks: voxel 4q + ks), so the three column taps of an
+    // h_{t-1} row share six loads per lane.
+    auto load = [&](const WgCursor &cu, bool live, Ops &o) {
+        const int p = cu.p, t = cu.t, n = cu.n;
+        const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+        const long long dn = ((long long)d * a.g.N + n) * V;
+        // row-uniform bases (rows off the plane are clamped and masked)
+        const float *dA_row = a.dA + (dn + (long long)s * ss + (long long)p * sp) * kG;
+        const float *h_pl = a.hd + (dn + (long long)(t > 0 ? s - dg.sign : s) * ss) * kO;
+        const float *x_pl = a.x + ((long long)n * V + (long long)s * ss) * C;
+        const int colbase = cu.qg * 16 + 4 * q;
+        // bounds as non-short-circuit unsigned compares: no branches.  Masks
+        // multiply (not select) the loaded values, so that every load is
+        // unconditional and no branch splits the batch of loads.
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int qq = colbase + ks;
+            const bool vq = live & ((unsigned)qq < (unsigned)dg.Q);
+            const int qc = vq ? qq : 0;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const float v = dA_row[qc * sq * kG + g * 16 + col];
+                o.a[ks][g] = v * (vq ? 1.0f : 0.0f);
+            }
+        }
+        // h_{t-1} taps: rows p-1, p, p+1 (tiles 0-2, 3-5, 6-8)
+#pragma unroll
+        for (int r = 0; r < 3; ++r) {
+            bool any = false;
+#pragma unroll
+            for (int j = 0; j < NTC; ++j) any |= (NT0 + j < 9) && ((NT0 + j) / 3 == r);
+            if (!any) continue;
+            const int pp = p + r - 1;
+            const bool rok = (t > 0) & ((unsigned)pp < (unsigned)dg.P);
+            const float *hrow = h_pl + (long long)(rok ? pp : p) * sp * kO;
+            float hv[6];
+#pragma unroll
+            for (int m = 0; m < 6; ++m) {
+                const int c = colbase - 1 + m;
+                const bool ok = rok & ((unsigned)c < (unsigned)dg.Q);
+                const float v = hrow[(ok ? c : 0) * sq * kO + col];
+                hv[m] = v * (ok ? 1.0f : 0.0f);
+            }
+#pragma unroll
+            for (int j = 0; j < NTC; ++j) {
+                const int nt = NT0 + j;
+                if (nt < 9 && nt / 3 == r)
+#pragma unroll
+                    for (int ks = 0; ks < 4; ++ks) o.b[ks][j] = hv[ks + nt % 3];
+            }
+        }
+        // input taps and the bias column (tiles 9, 10, ...)
+#pragma unroll
+        for (int j = 0; j < NTC; ++j) {
+            if (NT0 + j < 9) continue;
+            const int pp = p + xtap_dp[j];
+            const bool rok = (xkind[j] == 0) & ((unsigned)pp < (unsigned)dg.P);
+            const float *xrow = x_pl + (rok ? pp : p) * sp * C + xtap_c[j];
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const int c = colbase + ks + xtap_dq[j];
+                const bool ok = rok & ((unsigned)c < (unsigned)dg.Q);
+                const float v = xrow[(ok ? c : 0) * sq * C];
+                o.b[ks][j] = v * (ok ? 1.0f : 0.0f) + (xkind[j] == 1 ? 1.0f : 0.0f);
+            }
+        }
+    };
+    Ops cur, nxt;
+    // cursor over (n, t, p, column group), starting at row r0
+    WgCursor cu;
+    cu.p = (int)(r0 % dg.P);
+    cu.t = (int)((r0 / dg.P) % dg.T);
+    cu.n = (int)(r0 / ((long long)dg.P * dg.T));
+    cu.qg = 0;
+    const long long total = (r1 - r0) * ngrp;
+    load(cu, total > 0, cur);
+    for (long long it = 0; it < total; ++it) {
+        // advance the cursor; past the end it stays on a valid row (loads masked)
+        if (++cu.qg == ngrp) {
+            cu.qg = 0;
+            if (++cu.p == dg.P) {
+                cu.p = 0;
+                if (++cu.t == dg.T) {
+                    cu.t = 0;
+                    if (cu.n + 1 < a.g.N) ++cu.n;
+                }
+            }
+        }
+        load(cu, it + 1 < total, nxt);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int j = 0; j < NTC; ++j)
+                    acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.a[ks][g], cur.b[ks][j],
+                                                                     acc[g][j], 0, 0, 0);
+        cur = nxt;
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int j = 0; j < NTC; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                out[(g * 16 + 4 * q + i) * a.KCp + (NT0 + j) * 16 + col] = acc[g][j][i];
+}
+
+template <int C>
+__global__ void __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(2)))
+k_wgrad_rows(WgRowArgs a)
+{
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int q = lane >> 4, col = lane & 15;
+    const int team = blockIdx.x * (kWgWaves / 2) + (wave >> 1);
+    if (team >= kDirs * a.tpd) return;
+    const int d = team / a.tpd, tin = team % a.tpd;
+    const DirGeom dg = a.g.dir[d];
+    const long long rows = (long long)a.g.N * dg.T * dg.P;
+    const long long r0 = rows * tin / a.tpd, r1 = rows * (tin + 1) / a.tpd;
+    float *out = a.partial + (long long)team * kG * a.KCp;
+    constexpr int NT = WgN<C>::NT, LO = WgN<C>::NT_LO;
+    if ((wave & 1) == 0)
+        wg_rows_team<C, 0, LO>(a, d, r0, r1, q, col, out);
+    else
+        wg_rows_team<C, LO, NT - LO>(a, d, r0, r1, q, col, out);
+}
+
 // dW = sum of the per-workgroup partials in workgroup order.
 __global__ void __launch_bounds__(256)
 k_wgrad_reduce(int C, int bpd, int KCp, const float *__restrict__ partial,
@@ -482,13 +676,15 @@ template <int C>
 int launch_wgrad(const Geom &g, const float *x, const float *hd, const float *dA, float *partial,
                  hipStream_t st)
 {
-    WgradArgs wa;
+    WgRowArgs wa;
     wa.g = g;
     wa.x = x; wa.hd = hd; wa.dA = dA;
     wa.partial = partial;
-    wa.bpd = kWgradBlocksPerDir;
+    wa.tpd = kWgTeamsPerDir;
     wa.KCp = wgrad_kcp(C);
-    k_wgrad<C><<<kDirs * kWgradBlocksPerDir, kThreads, 0, st>>>(wa);
+    const int teams = kDirs * kWgTeamsPerDir;
+    const int per_block = kWgWaves / 2;
+    k_wgrad_rows<C><<<(teams + per_block - 1) / per_block, 64 * kWgWaves, 0, st>>>(wa);
     PLSTM_LAUNCH_CHECK();
     return PLSTM_OK;
 }
@@ -503,7 +699,7 @@ size_t sweep_bwd_ws(const Geom &g)
     cv.take<float>((size_t)kDirs * g.N * g.V * kG);                     // dA
     cv.take<float>((size_t)kDirs * g.N * g.V * kO);                     // dL/dc
     cv.take<int>(1024 + 1);                                              // flags + err
-    cv.take<float>((size_t)kDirs * kWgradBlocksPerDir * kG * wgrad_kcp(g.C));   // partials
+    cv.take<float>((size_t)kDirs * kWgTeamsPerDir * kG * wgrad_kcp(g.C));   // partials
     return cv.off;
 }
 
@@ -524,7 +720,7 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * kG);
     float *gc = cv.take<float>((size_t)kDirs * g.N * g.V * kO);
     int *flags = cv.take<int>(1024 + 1);
-    float *partial = cv.take<float>((size_t)kDirs * kWgradBlocksPerDir * kG * wgrad_kcp(g.C));
+    float *partial = cv.take<float>((size_t)kDirs * kWgTeamsPerDir * kG * wgrad_kcp(g.C));
 
     BwdArgs args;
     args.g = g;
@@ -566,7 +762,7 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     }
     if (rc != PLSTM_OK) return rc;
     const int nout = kDirs * kG * (144 + 9 * g.C + 1);
-    k_wgrad_reduce<<<(nout + 255) / 256, 256, 0, st>>>(g.C, kWgradBlocksPerDir, wgrad_kcp(g.C),
+    k_wgrad_reduce<<<(nout + 255) / 256, 256, 0, st>>>(g.C, kWgTeamsPerDir, wgrad_kcp(g.C),
                                                        partial, dwx, dwh, db);
     PLSTM_LAUNCH_CHECK();
     timing_end(2, st);

@@ -436,17 +436,17 @@ __global__ void __launch_bounds__(kThreads, 1) k_wgrad(WgradArgs a)
 // ---- parameter gradients, register-streamed --------------------------------
 // dW[d] = sum over voxels v of dA[v] (x) [im2col(h_{t-1})(v), im2col(x_t)(v), 1],
 // an implicit GEMM with M = 64 gate-units, N = 144 + 9C + 1 and K = voxels.
-// A team of two waves owns a contiguous range of rows (fixed plane and
-// first in-plane index) of one direction and walks them 16 voxels (four
-// MFMA k-steps) at a time; wave h of the team holds the output tiles of its
-// half of N.  Operands come straight from global memory into registers
+// One wave owns a contiguous range of rows (fixed plane and first in-plane
+// index) of one direction and walks them 16 voxels (four MFMA k-steps) at
+// a time, holding all 4 x ceil(N / 16) output tiles (in AGPRs; one wave per
+// SIMD).  Operands come straight from global memory into registers
 // (lane group q takes voxel 4 ks + q, lane col takes a gate-unit (A) or an
 // im2col column (B), so every load is 64 contiguous bytes per voxel), the
 // next group's loads are in flight while the current group's MFMAs run,
 // and the accumulators stay in VGPRs for the whole launch: no LDS, no
 // barriers.  Zero padding (off-plane taps, h_{-1}) comes from clamped
 // addresses and selects.
-constexpr int kWgWaves = 4;                    // two teams per workgroup
+constexpr int kWgWaves = 4;                    // one team (wave) per SIMD
 constexpr int kWgTeamsPerDir = 170;
 
 struct WgRowArgs {
@@ -459,7 +459,6 @@ struct WgRowArgs {
 
 template <int C> struct WgN {
     static constexpr int NT = (144 + 9 * C + 1 + 15) / 16;   // N-tiles
-    static constexpr int NT_LO = (NT + 1) / 2;               // tiles of wave 0 of a team
 };
 
 // Cursor of a team: batch element, sweep step, row, group of 16 columns.
@@ -565,17 +564,14 @@ __device__ inline void wg_rows_team(const WgRowArgs &a, int d, long long r0, lon
             }
         }
     };
-    Ops cur, nxt;
-    // cursor over (n, t, p, column group), starting at row r0
+    // cursor over (n, t, p, column group), starting at row r0; past the end
+    // it stays on a valid row and the loads are masked to zero
     WgCursor cu;
     cu.p = (int)(r0 % dg.P);
     cu.t = (int)((r0 / dg.P) % dg.T);
     cu.n = (int)(r0 / ((long long)dg.P * dg.T));
     cu.qg = 0;
-    const long long total = (r1 - r0) * ngrp;
-    load(cu, total > 0, cur);
-    for (long long it = 0; it < total; ++it) {
-        // advance the cursor; past the end it stays on a valid row (loads masked)
+    auto advance = [&]() {
         if (++cu.qg == ngrp) {
             cu.qg = 0;
             if (++cu.p == dg.P) {
@@ -586,15 +582,24 @@ __device__ inline void wg_rows_team(const WgRowArgs &a, int d, long long r0, lon
                 }
             }
         }
-        load(cu, it + 1 < total, nxt);
+    };
+    auto mfma_group = [&](const Ops &o) {
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
             for (int g = 0; g < 4; ++g)
 #pragma unroll
                 for (int j = 0; j < NTC; ++j)
-                    acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.a[ks][g], cur.b[ks][j],
+                    acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[ks][g], o.b[ks][j],
                                                                      acc[g][j], 0, 0, 0);
+    };
+    const long long total = (r1 - r0) * ngrp;
+    Ops cur, nxt;
+    load(cu, total > 0, cur);
+    for (long long it = 0; it < total; ++it) {
+        advance();
+        load(cu, it + 1 < total, nxt);
+        mfma_group(cur);
         cur = nxt;
     }
 #pragma unroll
@@ -607,24 +612,20 @@ __device__ inline void wg_rows_team(const WgRowArgs &a, int d, long long r0, lon
 }
 
 template <int C>
-__global__ void __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(64 * kWgWaves) __attribute__((amdgpu_waves_per_eu(1)))
 k_wgrad_rows(WgRowArgs a)
 {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int q = lane >> 4, col = lane & 15;
-    const int team = blockIdx.x * (kWgWaves / 2) + (wave >> 1);
+    const int team = blockIdx.x * kWgWaves + wave;
     if (team >= kDirs * a.tpd) return;
     const int d = team / a.tpd, tin = team % a.tpd;
     const DirGeom dg = a.g.dir[d];
     const long long rows = (long long)a.g.N * dg.T * dg.P;
     const long long r0 = rows * tin / a.tpd, r1 = rows * (tin + 1) / a.tpd;
     float *out = a.partial + (long long)team * kG * a.KCp;
-    constexpr int NT = WgN<C>::NT, LO = WgN<C>::NT_LO;
-    if ((wave & 1) == 0)
-        wg_rows_team<C, 0, LO>(a, d, r0, r1, q, col, out);
-    else
-        wg_rows_team<C, LO, NT - LO>(a, d, r0, r1, q, col, out);
+    wg_rows_team<C, 0, WgN<C>::NT>(a, d, r0, r1, q, col, out);
 }
 
 // dW = sum of the per-workgroup partials in workgroup order.
@@ -683,7 +684,7 @@ int launch_wgrad(const Geom &g, const float *x, const float *hd, const float *dA
     wa.tpd = kWgTeamsPerDir;
     wa.KCp = wgrad_kcp(C);
     const int teams = kDirs * kWgTeamsPerDir;
-    const int per_block = kWgWaves / 2;
+    const int per_block = kWgWaves;
     k_wgrad_rows<C><<<(teams + per_block - 1) / per_block, 64 * kWgWaves, 0, st>>>(wa);
     PLSTM_LAUNCH_CHECK();
     return PLSTM_OK;

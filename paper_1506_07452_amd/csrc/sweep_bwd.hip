@@ -12,15 +12,13 @@
 //     (tap, gate-unit) with units on M and pixels on N: lane l takes pixel
 //     l%16 and gate l/16 (16 units = 4 LDS reads of 16 bytes per tap) for the
 //     B operand, the transposed recurrent weights are the A operand, resident
-//     in VGPRs, and each lane ends with four consecutive units of one pixel,
-//     so every epilogue load and store is a 16-byte vector.  dA of every voxel
-//     is kept for (2) and for dL/dx.
-// (2) k_wgrad: dW = sum over voxels of dA (x) im2col(h_{t-1}, x_t, 1), an
-//     implicit GEMM per row segment of up to 64 voxels: M = 64 gate-units,
-//     N = 9 x 16 + 9 C + 1 columns, K = voxels; the previous plane's h^d and
-//     the input rows are staged in LDS and read with the tap offsets.  Each
-//     workgroup reduces a fixed set of segments of one direction; (3)
-//     k_wgrad_reduce sums the per-workgroup partials in a fixed order.
+//     in LDS, and each lane ends with four consecutive units of one
+//     pixel, so every epilogue load and store is a 16-byte vector.  The
+//     product gc_t f_t is what plane t - 1 needs, so that is what is kept.
+//     dA of every voxel is kept for (2) and for dL/dx.
+// (2) k_wgrad_rows: dW = sum over voxels of dA (x) [im2col(h_{t-1}),
+//     im2col(x_t), 1], a register-streamed implicit GEMM (see there), and
+//     (3) k_wgrad_reduce sums the per-wave partials in a fixed order.
 #include "common.h"
 #include "strip_plan.h"
 #include "sweep.h"
@@ -33,7 +31,8 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kO = 16;
 constexpr int kG = 4 * kO;
-constexpr int kWaves = 8;
+constexpr int kWaves = 16;             // four waves per SIMD
+constexpr int kWaFloats = 9 * 4 * 64 * 4;  // W_h^T fragments in LDS
 constexpr int kThreads = 64 * kWaves;
 constexpr int kAS = 68;                // LDS floats per staged dA pixel (64 + 4 pad)
 constexpr int kMaxSpin = 1 << 21;
@@ -51,9 +50,14 @@ struct BwdArgs {
     const float *gates, *cell;   // saved forward activations [6][N][V][64], [6][N][V][16]
     const float *dh;             // dL/dh [N][V][16]
     float *dA;                   // [6][N][V][64] gate pre-activation gradients
-    float *gc;                   // [6][N][V][16] dL/dc
+    float *gcf;                  // [6][N][V][16] dL/dc_t * f_t, carried to plane t - 1
     int *flags, *err;
     int nstrip[kDirs], first[kDirs], chunk_rows[kDirs], max_w[kDirs];
+};
+
+// Epilogue operands of one tile (this lane's pixel, units 4 q4 .. 4 q4 + 3).
+struct BwdEpi {
+    f4 dh, gi, gf, gg, go, c, gcfn, cp;
 };
 
 __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
@@ -72,25 +76,33 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
     const int TQ = q1 - q0, W2 = TQ + 2;
     const int nb_lo = strip > 0 ? (int)blockIdx.x - 1 : -1;
     const int nb_hi = strip + 1 < ns ? (int)blockIdx.x + 1 : -1;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int q4 = lane >> 4, col = lane & 15;
     const int chunk_rows = a.chunk_rows[d];
-    float *as = smem;
-
-    // A fragments: W_h^T with the tap's K index k = (s, q4) -> gate-unit 16 q4 + s.
-    float wa[9][16];
+    // A fragments of W_h^T in LDS (registers stay free for four waves per
+    // SIMD): entry (tap, s4, lane) holds, for lane l, the gate-units
+    // 16 (l/16) + 4 s4 .. + 3 of output unit l%16; the tap's K index
+    // k = (s, q4) -> gate-unit 16 q4 + s.  The first staging barrier orders
+    // these stores before their reads.
+    float *was = smem;
+    float *as = smem + kWaFloats;
+    for (int e = threadIdx.x; e < 9 * 4 * 64; e += kThreads) {
+        const int l = e & 63, s4 = (e >> 6) & 3, tap = e >> 8;
+        const int lq = l >> 4, lc = l & 15;
+        f4 v;
 #pragma unroll
-    for (int tap = 0; tap < 9; ++tap)
-#pragma unroll
-        for (int s = 0; s < 16; ++s)
-            wa[tap][s] = a.wh[(((long long)d * kG + 16 * q4 + s) * kO + col) * 9 + tap];
+        for (int j = 0; j < 4; ++j)
+            v[j] = a.wh[(((long long)d * kG + 16 * lq + 4 * s4 + j) * kO + lc) * 9 + tap];
+        *(f4 *)&was[e * 4] = v;
+    }
 
     const long long V = a.g.V;
     const long long dn = ((long long)d * a.g.N + n) * V;
     const float *const gates_dn = a.gates + dn * kG;
     const float *const cell_dn = a.cell + dn * kO;
     float *const dA_dn = a.dA + dn * kG;
-    float *const gc_dn = a.gc + dn * kO;
+    float *const gcf_dn = a.gcf + dn * kO;
     const float *const dh_n = a.dh + (long long)n * V * kO;
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
     const float inv_tq = 1.0f / (float)TQ, inv_w2 = 1.0f / (float)W2;
@@ -149,27 +161,30 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
             }
             __syncthreads();
             // ---- 16-pixel tiles ------------------------------------------
+            // Each tile's epilogue operands are loaded before its contraction.
+            // Lanes past the chunk redo its last pixel (the same values to
+            // the same addresses).
             const int npx = CH * TQ;
             const int nmt = (npx + 15) >> 4;
-            for (int mt = wave; mt < nmt; mt += kWaves) {
-                const int pb = min(mt * 16 + col, npx - 1);      // this lane's pixel
+            auto pixel = [&](int mt, int &base, int &vo) {
+                const int pb = min(mt * 16 + col, npx - 1);
                 const int rb = fdiv_floor(pb, inv_tq);
                 const int cb = pb - rb * TQ;
-                const int base = (rb + 1) * W2 + cb + 1;
-                const int vo = splane + (rb + r0) * sp + (cb + q0) * sq;
+                base = (rb + 1) * W2 + cb + 1;
+                vo = splane + (rb + r0) * sp + (cb + q0) * sq;
+            };
+            auto load_epi = [&](int vo, BwdEpi &e) {
                 const int von = vo - splane + nplane, vop = vo - splane + pplane;
-                // epilogue operands, loaded ahead of the contraction
-                const f4 dh4 = *(const f4 *)&dh_n[vo * kO + 4 * q4];
-                const f4 gi = *(const f4 *)&gates_dn[vo * kG + 0 * kO + 4 * q4];
-                const f4 gf = *(const f4 *)&gates_dn[vo * kG + 1 * kO + 4 * q4];
-                const f4 gg = *(const f4 *)&gates_dn[vo * kG + 2 * kO + 4 * q4];
-                const f4 go = *(const f4 *)&gates_dn[vo * kG + 3 * kO + 4 * q4];
-                const f4 c4 = *(const f4 *)&cell_dn[vo * kO + 4 * q4];
-                const f4 gcn = *(const f4 *)&gc_dn[von * kO + 4 * q4];
-                const f4 fn = *(const f4 *)&gates_dn[von * kG + 1 * kO + 4 * q4];
-                const f4 cp = *(const f4 *)&cell_dn[vop * kO + 4 * q4];
-                __builtin_amdgcn_sched_barrier(0);
-                f4 acc[4];
+                e.dh = *(const f4 *)&dh_n[vo * kO + 4 * q4];
+                e.gi = *(const f4 *)&gates_dn[vo * kG + 0 * kO + 4 * q4];
+                e.gf = *(const f4 *)&gates_dn[vo * kG + 1 * kO + 4 * q4];
+                e.gg = *(const f4 *)&gates_dn[vo * kG + 2 * kO + 4 * q4];
+                e.go = *(const f4 *)&gates_dn[vo * kG + 3 * kO + 4 * q4];
+                e.c = *(const f4 *)&cell_dn[vo * kO + 4 * q4];
+                e.gcfn = *(const f4 *)&gcf_dn[von * kO + 4 * q4];
+                e.cp = *(const f4 *)&cell_dn[vop * kO + 4 * q4];
+            };
+            auto contract = [&](int base, f4 (&acc)[4]) {
 #pragma unroll
                 for (int k = 0; k < 4; ++k) acc[k] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -177,34 +192,50 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                     // h_t at pixel p fed A_{t+1} at p - (tap offset)
                     const int o = (tap / 3 - 1) * W2 + (tap % 3 - 1);
                     const float *src = &as[(base - o) * kAS + 16 * q4];
-                    f4 bv[4];
+                    f4 bv[4], av[4];
 #pragma unroll
                     for (int k = 0; k < 4; ++k) bv[k] = *(const f4 *)&src[4 * k];
 #pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        av[k] = *(const f4 *)&was[((tap * 4 + k) * 64 + lane) * 4];
+#pragma unroll
                     for (int s2 = 0; s2 < 16; ++s2)
                         acc[s2 & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            wa[tap][s2], bv[s2 >> 2][s2 & 3], acc[s2 & 3], 0, 0, 0);
+                            av[s2 >> 2][s2 & 3], bv[s2 >> 2][s2 & 3], acc[s2 & 3], 0, 0, 0);
                 }
-                if (mt * 16 + col >= npx) continue;
-                f4 dAi, dAf, dAg, dAo, gcv;
+            };
+            auto epilogue = [&](int vo, const f4 (&acc)[4], const BwdEpi &e) {
+                f4 dAi, dAf, dAg, dAo, gcf;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float gh = acc[0][i] + acc[1][i] + acc[2][i] + acc[3][i] + dh4[i];
-                    const float tc = ftanh(c4[i]);
-                    float gcs = gh * go[i] * (1.0f - tc * tc);
-                    if (has_next) gcs += gcn[i] * fn[i];
-                    const float cprev = has_prev ? cp[i] : 0.0f;
-                    gcv[i] = gcs;
-                    dAi[i] = gcs * gg[i] * gi[i] * (1.0f - gi[i]);
-                    dAf[i] = gcs * cprev * gf[i] * (1.0f - gf[i]);
-                    dAg[i] = gcs * gi[i] * (1.0f - gg[i] * gg[i]);
-                    dAo[i] = gh * tc * go[i] * (1.0f - go[i]);
+                    const float gh = acc[0][i] + acc[1][i] + acc[2][i] + acc[3][i] + e.dh[i];
+                    const float tc = ftanh(e.c[i]);
+                    const float gcs = gh * e.go[i] * (1.0f - tc * tc) +
+                                      (has_next ? e.gcfn[i] : 0.0f);
+                    const float cprev = has_prev ? e.cp[i] : 0.0f;
+                    gcf[i] = gcs * e.gf[i];
+                    dAi[i] = gcs * e.gg[i] * e.gi[i] * (1.0f - e.gi[i]);
+                    dAf[i] = gcs * cprev * e.gf[i] * (1.0f - e.gf[i]);
+                    dAg[i] = gcs * e.gi[i] * (1.0f - e.gg[i] * e.gg[i]);
+                    dAo[i] = gh * tc * e.go[i] * (1.0f - e.go[i]);
                 }
                 *(f4 *)&dA_dn[vo * kG + 0 * kO + 4 * q4] = dAi;
                 *(f4 *)&dA_dn[vo * kG + 1 * kO + 4 * q4] = dAf;
                 *(f4 *)&dA_dn[vo * kG + 2 * kO + 4 * q4] = dAg;
                 *(f4 *)&dA_dn[vo * kG + 3 * kO + 4 * q4] = dAo;
-                *(f4 *)&gc_dn[vo * kO + 4 * q4] = gcv;
+                *(f4 *)&gcf_dn[vo * kO + 4 * q4] = gcf;
+            };
+            for (int mt = wave; mt < nmt; mt += kWaves) {
+                int base, vo;
+                pixel(mt, base, vo);
+                BwdEpi e;
+                load_epi(vo, e);
+                // keep the loads above the contraction (the scheduler would
+                // otherwise sink them to their use and expose their latency)
+                __builtin_amdgcn_sched_barrier(0);
+                f4 acc[4];
+                contract(base, acc);
+                epilogue(vo, acc, e);
             }
             __syncthreads();
         }
@@ -217,219 +248,6 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
             __hip_atomic_store(&a.flags[blockIdx.x], r + 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         }
-    }
-}
-
-// ---- parameter gradients ----------------------------------------------------
-constexpr int kSeg = 64;        // voxels per work unit (one row segment)
-constexpr int kHW = kSeg + 2;   // staged columns per row
-constexpr int kHP = 17;         // LDS floats per staged h pixel (16 + 1 pad)
-constexpr int kDP = 65;         // LDS floats per staged dA voxel (64 + 1 pad)
-
-struct WgradArgs {
-    Geom g;
-    const float *x, *hd, *dA;
-    float *partial;     // [6][bpd][64][KCp]
-    int bpd;            // workgroups per direction
-    int KCp;            // columns padded to 16: 144 + 9C + 1 -> multiple of 16
-};
-
-// One work unit: row p of plane t (batch element n), columns qs .. qs+nq-1.
-struct WgUnit {
-    int n, t, p, qs, nq;
-};
-
-__device__ inline WgUnit wg_unit(const DirGeom &dg, int nseg, int segw, long long u)
-{
-    WgUnit w;
-    const int seg = (int)(u % nseg);
-    const long long rest = u / nseg;
-    w.p = (int)(rest % dg.P);
-    w.t = (int)((rest / dg.P) % dg.T);
-    w.n = (int)(rest / ((long long)dg.P * dg.T));
-    w.qs = seg * segw;
-    w.nq = min(segw, dg.Q - w.qs);
-    return w;
-}
-
-// Staged arrays of a unit, each with a fixed number of elements per thread
-// (loads from clamped addresses, no divergent branches): the three h_{t-1}
-// rows as float4s, the dA row as float4s and the three x rows as scalars.
-constexpr int kNH = 3 * kHW * 4;                           // float4s of the h rows
-constexpr int kNA = kSeg * 16;                             // float4s of the dA row
-constexpr int kRH = (kNH + kThreads - 1) / kThreads;
-constexpr int kRA = (kNA + kThreads - 1) / kThreads;
-template <int C> struct WgStage {
-    static constexpr int kNX = 3 * kHW * C;
-    static constexpr int kRX = (kNX + kThreads - 1) / kThreads;
-    f4 h[kRH];
-    f4 a[kRA];
-    float x[kRX];
-};
-
-template <int C>
-__device__ inline void wg_issue(const WgradArgs &a, const DirGeom &dg, int d, const WgUnit &w,
-                                WgStage<C> &st)
-{
-    const long long V = a.g.V;
-    const long long dn = ((long long)d * a.g.N + w.n) * V;
-    const float *hd_dn = a.hd + dn * kO;
-    const float *dA_dn = a.dA + dn * kG;
-    const float *x_n = a.x + (long long)w.n * V * C;
-    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
-    const int s = dg.sign > 0 ? w.t : dg.T - 1 - w.t;
-    const int splane = s * ss;
-    const int pplane = (w.t > 0 ? s - dg.sign : s) * ss;
-#pragma unroll
-    for (int k = 0; k < kRH; ++k) {
-        const int e = min((int)threadIdx.x + k * kThreads, kNH - 1);
-        const int pix = e >> 2, qd = e & 3;
-        const int rr = pix / kHW, cc = pix - (pix / kHW) * kHW;
-        const int pr = w.p + rr - 1, pc = w.qs + cc - 1;
-        const bool ok = w.t > 0 && pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q;
-        const int off = ok ? (pplane + pr * sp + pc * sq) * kO + qd * 4 : 0;
-        const f4 val = *(const f4 *)&hd_dn[off];
-        st.h[k] = ok ? val : f4{0.0f, 0.0f, 0.0f, 0.0f};
-    }
-#pragma unroll
-    for (int k = 0; k < kRA; ++k) {
-        const int e = (int)threadIdx.x + k * kThreads;     // kNA is a multiple of kThreads
-        const int vx = e >> 4, qd = e & 15;
-        const bool ok = vx < w.nq;
-        const int off = ok ? (splane + w.p * sp + (w.qs + vx) * sq) * kG + qd * 4 : 0;
-        const f4 val = *(const f4 *)&dA_dn[off];
-        st.a[k] = ok ? val : f4{0.0f, 0.0f, 0.0f, 0.0f};
-    }
-#pragma unroll
-    for (int k = 0; k < WgStage<C>::kRX; ++k) {
-        const int e = min((int)threadIdx.x + k * kThreads, WgStage<C>::kNX - 1);
-        const int pix = e / C, c = e - (e / C) * C;
-        const int rr = pix / kHW, cc = pix - (pix / kHW) * kHW;
-        const int pr = w.p + rr - 1, pc = w.qs + cc - 1;
-        const bool ok = pr >= 0 && pr < dg.P && pc >= 0 && pc < dg.Q;
-        const int off = ok ? (splane + pr * sp + pc * sq) * C + c : 0;
-        const float val = x_n[off];
-        st.x[k] = ok ? val : 0.0f;
-    }
-}
-
-template <int C>
-__device__ inline void wg_commit(const WgStage<C> &st, float *hs, float *das, float *xs)
-{
-#pragma unroll
-    for (int k = 0; k < kRH; ++k) {
-        const int e = (int)threadIdx.x + k * kThreads;
-        if (e < kNH) {
-            const int pix = e >> 2, qd = e & 3;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) hs[pix * kHP + qd * 4 + j] = st.h[k][j];
-        }
-    }
-#pragma unroll
-    for (int k = 0; k < kRA; ++k) {
-        const int e = (int)threadIdx.x + k * kThreads;
-        const int vx = e >> 4, qd = e & 15;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) das[vx * kDP + qd * 4 + j] = st.a[k][j];
-    }
-#pragma unroll
-    for (int k = 0; k < WgStage<C>::kRX; ++k) {
-        const int e = (int)threadIdx.x + k * kThreads;
-        if (e < WgStage<C>::kNX) xs[e] = st.x[k];
-    }
-}
-
-// Column nt*16 + col of the im2col row of voxel vv: h_{t-1} (taps 0..8 hold
-// 16 units each), then the input taps x channels, the bias column, padding.
-template <int C>
-__device__ inline float wg_col(const float *hs, const float *xs, int nt, int vv, int col)
-{
-    if (nt < 9) return hs[((nt / 3) * kHW + vv + (nt % 3)) * kHP + col];
-    const int kk = (nt - 9) * 16 + col;
-    if (kk < 9 * C) {
-        const int tap = kk / C, c = kk - (kk / C) * C;
-        return xs[((tap / 3) * kHW + vv + (tap % 3)) * C + c];
-    }
-    return kk == 9 * C ? 1.0f : 0.0f;
-}
-
-// Output tiles of a wave: gate m = wave % 4 and N-tiles NT0, NT0 + 2, ...;
-// the compile-time start lets every tile index, and so every branch on it,
-// resolve at compile time.
-template <int C, int NT0>
-__device__ inline void wg_tiles(const float *hs, const float *xs, const float *das, int nq,
-                                int m, int q4, int col, f4 (&acc)[6])
-{
-    constexpr int NT = (144 + 9 * C + 1 + 15) / 16;
-    constexpr int NTW = (NT - NT0 + 1) / 2;          // tiles of this wave
-    // Four k-steps (16 voxels) per iteration: all their LDS reads are issued
-    // before their MFMAs.  Voxels past the segment have dA = 0 in LDS (and
-    // staged neighbours), so rounding up to 16 voxels adds only zeros.
-    const int kgroups = (nq + 15) >> 4;
-    for (int kg = 0; kg < kgroups; ++kg) {
-        float av[4], bv[4][NTW];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int vv = 16 * kg + 4 * u + q4;
-            av[u] = das[vv * kDP + m * 16 + col];
-#pragma unroll
-            for (int i = 0; i < NTW; ++i) bv[u][i] = wg_col<C>(hs, xs, NT0 + 2 * i, vv, col);
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int i = 0; i < NTW; ++i)
-                acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u][i], acc[i], 0, 0, 0);
-    }
-}
-
-template <int C>
-__global__ void __launch_bounds__(kThreads, 1) k_wgrad(WgradArgs a)
-{
-    __shared__ float hs[3 * kHW * kHP];
-    __shared__ float xs[3 * kHW * C];
-    __shared__ float das[kSeg * kDP];
-    const int d = blockIdx.x / a.bpd, bi = blockIdx.x % a.bpd;
-    const DirGeom dg = a.g.dir[d];
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
-    const int q4 = lane >> 4, col = lane & 15;
-    constexpr int NT = (144 + 9 * C + 1 + 15) / 16;
-    const int m = wave & 3;                   // gate of this wave's output tiles
-    const int nt0 = wave >> 2;                // first N-tile; then every second one
-    f4 acc[6];
-#pragma unroll
-    for (int i = 0; i < 6; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-
-    const int nseg = (dg.Q + kSeg - 1) / kSeg;
-    const int segw = (dg.Q + nseg - 1) / nseg;
-    const long long units = (long long)a.g.N * dg.T * dg.P * nseg;
-
-    // Software pipeline: the next unit's loads are in flight while the
-    // current unit's MFMAs run.
-    WgStage<C> stage;
-    long long u = bi;
-    if (u < units) wg_issue<C>(a, dg, d, wg_unit(dg, nseg, segw, u), stage);
-    for (; u < units; u += a.bpd) {
-        const WgUnit w = wg_unit(dg, nseg, segw, u);
-        wg_commit<C>(stage, hs, das, xs);
-        __syncthreads();
-        if (u + a.bpd < units) wg_issue<C>(a, dg, d, wg_unit(dg, nseg, segw, u + a.bpd), stage);
-        if (nt0 == 0)
-            wg_tiles<C, 0>(hs, xs, das, w.nq, m, q4, col, acc);
-        else
-            wg_tiles<C, 1>(hs, xs, das, w.nq, m, q4, col, acc);
-        __syncthreads();
-    }
-    // ---- this workgroup's partial sums --------------------------------------
-    float *out = a.partial + ((long long)d * a.bpd + bi) * kG * a.KCp;
-#pragma unroll
-    for (int i = 0; i < 6; ++i) {
-        const int nt = nt0 + 2 * i;
-        if (nt >= NT) break;
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            out[(m * 16 + 4 * q4 + r) * a.KCp + nt * 16 + col] = acc[i][r];
     }
 }
 
@@ -661,7 +479,7 @@ __global__ void k_fill_zero(int *p, int n)
 StripCostModel bwd_model()
 {
     StripCostModel m;
-    m.fixed_bytes = 0;
+    m.fixed_bytes = kWaFloats * sizeof(float);
     m.px_bytes = kAS * sizeof(float);
     m.c_sync = 3.0;
     m.c_tile = 2.9;
@@ -698,7 +516,7 @@ size_t sweep_bwd_ws(const Geom &g)
 {
     Carve cv(nullptr);
     cv.take<float>((size_t)kDirs * g.N * g.V * kG);                     // dA
-    cv.take<float>((size_t)kDirs * g.N * g.V * kO);                     // dL/dc
+    cv.take<float>((size_t)kDirs * g.N * g.V * kO);                     // dL/dc * f
     cv.take<int>(1024 + 1);                                              // flags + err
     cv.take<float>((size_t)kDirs * kWgTeamsPerDir * kG * wgrad_kcp(g.C));   // partials
     return cv.off;
@@ -719,7 +537,7 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
 
     Carve cv(ws);
     float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * kG);
-    float *gc = cv.take<float>((size_t)kDirs * g.N * g.V * kO);
+    float *gcf = cv.take<float>((size_t)kDirs * g.N * g.V * kO);
     int *flags = cv.take<int>(1024 + 1);
     float *partial = cv.take<float>((size_t)kDirs * kWgTeamsPerDir * kG * wgrad_kcp(g.C));
 
@@ -728,7 +546,7 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     args.wh = wh;
     args.gates = sv.gates; args.cell = sv.cell;
     args.dh = dh;
-    args.dA = dA; args.gc = gc;
+    args.dA = dA; args.gcf = gcf;
     args.flags = flags; args.err = flags + 1024;
     for (int d = 0; d < kDirs; ++d) {
         args.nstrip[d] = pl.nstrip[d];

@@ -106,6 +106,16 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
     const float *const dh_n = a.dh + (long long)n * V * kO;
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
     const float inv_tq = 1.0f / (float)TQ, inv_w2 = 1.0f / (float)W2;
+    // Columns that pass between neighbouring strips (this strip's first and
+    // last, and the halo columns beside them).  Their dA is stored and loaded
+    // at device coherence (write-through / read-through at agent scope, the
+    // accesses relaxed agent-scope atomics use), so a strip's step needs no
+    // L2 writeback before its flag and no L2 invalidate after waiting: once a
+    // strip's coherent stores have completed (vmcnt) its flag goes up.
+    auto is_shared_col = [&](int pc) {
+        return (pc == q0 - 1) | (pc == q1) | ((pc == q0) & (nb_lo >= 0)) |
+               ((pc == q1 - 1) & (nb_hi >= 0));
+    };
 
     for (int r = 0; r < dg.T; ++r) {
         const int t = dg.T - 1 - r;                   // plane processed at this step
@@ -127,7 +137,6 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                         __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
                         break;
                 }
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             }
             __syncthreads();
         }
@@ -150,7 +159,17 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                     const bool ok = e < nA && has_next && pr >= 0 && pr < dg.P && pc >= 0 &&
                                     pc < dg.Q;
                     const int off = ok ? (nplane + pr * sp + pc * sq) * kG + qd * 4 : 0;
-                    const f4 val = *(const f4 *)&dA_dn[off];
+                    f4 val;
+                    if (is_shared_col(pc)) {
+                        // columns exchanged with a neighbour strip: read at
+                        // device coherence (they were written that way)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            val[j] = __hip_atomic_load(&dA_dn[off + j], __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                    } else {
+                        val = *(const f4 *)&dA_dn[off];
+                    }
                     v[u] = ok ? val : f4{0.0f, 0.0f, 0.0f, 0.0f};
                 }
 #pragma unroll
@@ -166,12 +185,13 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
             // the same addresses).
             const int npx = CH * TQ;
             const int nmt = (npx + 15) >> 4;
-            auto pixel = [&](int mt, int &base, int &vo) {
+            auto pixel = [&](int mt, int &base, int &vo, bool &shared) {
                 const int pb = min(mt * 16 + col, npx - 1);
                 const int rb = fdiv_floor(pb, inv_tq);
                 const int cb = pb - rb * TQ;
                 base = (rb + 1) * W2 + cb + 1;
                 vo = splane + (rb + r0) * sp + (cb + q0) * sq;
+                shared = is_shared_col(cb + q0);
             };
             auto load_epi = [&](int vo, BwdEpi &e) {
                 const int von = vo - splane + nplane, vop = vo - splane + pplane;
@@ -204,7 +224,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                             av[s2 >> 2][s2 & 3], bv[s2 >> 2][s2 & 3], acc[s2 & 3], 0, 0, 0);
                 }
             };
-            auto epilogue = [&](int vo, const f4 (&acc)[4], const BwdEpi &e) {
+            auto epilogue = [&](int vo, bool shared, const f4 (&acc)[4], const BwdEpi &e) {
                 f4 dAi, dAf, dAg, dAo, gcf;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -219,15 +239,31 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                     dAg[i] = gcs * e.gi[i] * (1.0f - e.gg[i] * e.gg[i]);
                     dAo[i] = gh * tc * e.go[i] * (1.0f - e.go[i]);
                 }
-                *(f4 *)&dA_dn[vo * kG + 0 * kO + 4 * q4] = dAi;
-                *(f4 *)&dA_dn[vo * kG + 1 * kO + 4 * q4] = dAf;
-                *(f4 *)&dA_dn[vo * kG + 2 * kO + 4 * q4] = dAg;
-                *(f4 *)&dA_dn[vo * kG + 3 * kO + 4 * q4] = dAo;
+                float *dst = &dA_dn[vo * kG + 4 * q4];
+                if (shared) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        __hip_atomic_store(&dst[0 * kO + i], dAi[i], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(&dst[1 * kO + i], dAf[i], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(&dst[2 * kO + i], dAg[i], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(&dst[3 * kO + i], dAo[i], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                } else {
+                    *(f4 *)&dst[0 * kO] = dAi;
+                    *(f4 *)&dst[1 * kO] = dAf;
+                    *(f4 *)&dst[2 * kO] = dAg;
+                    *(f4 *)&dst[3 * kO] = dAo;
+                }
                 *(f4 *)&gcf_dn[vo * kO + 4 * q4] = gcf;
             };
             for (int mt = wave; mt < nmt; mt += kWaves) {
                 int base, vo;
-                pixel(mt, base, vo);
+                bool shared;
+                pixel(mt, base, vo, shared);
                 BwdEpi e;
                 load_epi(vo, e);
                 // keep the loads above the contraction (the scheduler would
@@ -235,19 +271,16 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                 __builtin_amdgcn_sched_barrier(0);
                 f4 acc[4];
                 contract(base, acc);
-                epilogue(vo, acc, e);
+                epilogue(vo, shared, acc, e);
             }
             __syncthreads();
         }
-        // ---- publish dA_t (see the forward sweep) -------------------------
+        // ---- publish dA_t: every wave's coherent stores have completed ---
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
-        if (threadIdx.x == 0) {
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        if (threadIdx.x == 0)
             __hip_atomic_store(&a.flags[blockIdx.x], r + 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-        }
     }
 }
 

@@ -40,6 +40,26 @@ constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unco
 constexpr int kBatch = 4;              // staging loads in flight per thread
 
 __device__ inline float frcp(float v) { return __builtin_amdgcn_rcpf(v); }
+
+// Device-coherent 16-byte accesses (cache policy SC1, the one agent-scope
+// atomics use): stores write through to the device coherence point and
+// loads read from it, so data exchanged between workgroups on different
+// XCDs needs no L2 writeback or invalidate.  `idx` is a float index into the
+// resource.
+constexpr int kBufferRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data
+constexpr int kCachePolicySC1 = 16;
+__device__ inline f4 load_coherent(__amdgpu_buffer_rsrc_t rs, int idx)
+{
+    return __builtin_bit_cast(
+        f4, __builtin_amdgcn_raw_buffer_load_b128(rs, idx * (int)sizeof(float), 0,
+                                                   kCachePolicySC1));
+}
+__device__ inline void store_coherent(__amdgpu_buffer_rsrc_t rs, int idx, f4 v)
+{
+    typedef unsigned u4 __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), rs,
+                                           idx * (int)sizeof(float), 0, kCachePolicySC1);
+}
 __device__ inline float ftanh(float a) { return 1.0f - 2.0f * frcp(__expf(2.0f * a) + 1.0f); }
 // floor(i / w) for 0 <= i < 2^20 (see the forward sweep for the error bound)
 __device__ inline int fdiv_floor(int i, float inv_w) { return (int)(((float)i + 0.5f) * inv_w); }
@@ -102,6 +122,10 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
     const float *const gates_dn = a.gates + dn * kG;
     const float *const cell_dn = a.cell + dn * kO;
     float *const dA_dn = a.dA + dn * kG;
+    // the slice as a buffer resource for the device-coherent accesses
+    // (its byte size fits 32 bits: checked on the host)
+    const __amdgpu_buffer_rsrc_t dA_rs = __builtin_amdgcn_make_buffer_rsrc(
+        dA_dn, (short)0, (int)(V * kG * sizeof(float)), kBufferRsrcWord3);
     float *const gcf_dn = a.gcf + dn * kO;
     const float *const dh_n = a.dh + (long long)n * V * kO;
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
@@ -160,16 +184,10 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                                     pc < dg.Q;
                     const int off = ok ? (nplane + pr * sp + pc * sq) * kG + qd * 4 : 0;
                     f4 val;
-                    if (is_shared_col(pc)) {
-                        // columns exchanged with a neighbour strip: read at
-                        // device coherence (they were written that way)
-#pragma unroll
-                        for (int j = 0; j < 4; ++j)
-                            val[j] = __hip_atomic_load(&dA_dn[off + j], __ATOMIC_RELAXED,
-                                                       __HIP_MEMORY_SCOPE_AGENT);
-                    } else {
+                    if (is_shared_col(pc))   // read at device coherence (written that way)
+                        val = load_coherent(dA_rs, off);
+                    else
                         val = *(const f4 *)&dA_dn[off];
-                    }
                     v[u] = ok ? val : f4{0.0f, 0.0f, 0.0f, 0.0f};
                 }
 #pragma unroll
@@ -239,19 +257,13 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                     dAg[i] = gcs * e.gi[i] * (1.0f - e.gg[i] * e.gg[i]);
                     dAo[i] = gh * tc * e.go[i] * (1.0f - e.go[i]);
                 }
-                float *dst = &dA_dn[vo * kG + 4 * q4];
+                const int o4 = vo * kG + 4 * q4;
+                float *dst = &dA_dn[o4];
                 if (shared) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        __hip_atomic_store(&dst[0 * kO + i], dAi[i], __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-                        __hip_atomic_store(&dst[1 * kO + i], dAf[i], __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-                        __hip_atomic_store(&dst[2 * kO + i], dAg[i], __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-                        __hip_atomic_store(&dst[3 * kO + i], dAo[i], __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-                    }
+                    store_coherent(dA_rs, o4 + 0 * kO, dAi);
+                    store_coherent(dA_rs, o4 + 1 * kO, dAf);
+                    store_coherent(dA_rs, o4 + 2 * kO, dAg);
+                    store_coherent(dA_rs, o4 + 3 * kO, dAo);
                 } else {
                     *(f4 *)&dst[0 * kO] = dAi;
                     *(f4 *)&dst[1 * kO] = dAf;
@@ -543,7 +555,11 @@ int launch_wgrad(const Geom &g, const float *x, const float *hd, const float *dA
 
 }  // namespace
 
-bool sweep_bwd_supported(const Geom &g) { return g.O == kO && g.C >= 1 && g.C <= 4; }
+bool sweep_bwd_supported(const Geom &g)
+{
+    // dA slices are addressed as buffer resources: bytes must fit 32 bits
+    return g.O == kO && g.C >= 1 && g.C <= 4 && g.V * kG * (long long)sizeof(float) < (1LL << 31);
+}
 
 size_t sweep_bwd_ws(const Geom &g)
 {

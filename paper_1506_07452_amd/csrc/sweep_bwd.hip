@@ -20,6 +20,7 @@
 //     im2col(x_t), 1], a register-streamed implicit GEMM (see there), and
 //     (3) k_wgrad_reduce sums the per-wave partials in a fixed order.
 #include "common.h"
+#include "coherent.h"
 #include "strip_plan.h"
 #include "sweep.h"
 #include "timing.h"
@@ -41,25 +42,6 @@ constexpr int kBatch = 4;              // staging loads in flight per thread
 
 __device__ inline float frcp(float v) { return __builtin_amdgcn_rcpf(v); }
 
-// Device-coherent 16-byte accesses (cache policy SC1, the one agent-scope
-// atomics use): stores write through to the device coherence point and
-// loads read from it, so data exchanged between workgroups on different
-// XCDs needs no L2 writeback or invalidate.  `idx` is a float index into the
-// resource.
-constexpr int kBufferRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data
-constexpr int kCachePolicySC1 = 16;
-__device__ inline f4 load_coherent(__amdgpu_buffer_rsrc_t rs, int idx)
-{
-    return __builtin_bit_cast(
-        f4, __builtin_amdgcn_raw_buffer_load_b128(rs, idx * (int)sizeof(float), 0,
-                                                   kCachePolicySC1));
-}
-__device__ inline void store_coherent(__amdgpu_buffer_rsrc_t rs, int idx, f4 v)
-{
-    typedef unsigned u4 __attribute__((ext_vector_type(4)));
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), rs,
-                                           idx * (int)sizeof(float), 0, kCachePolicySC1);
-}
 __device__ inline float ftanh(float a) { return 1.0f - 2.0f * frcp(__expf(2.0f * a) + 1.0f); }
 // floor(i / w) for 0 <= i < 2^20 (see the forward sweep for the error bound)
 __device__ inline int fdiv_floor(int i, float inv_w) { return (int)(((float)i + 0.5f) * inv_w); }
@@ -124,8 +106,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
     float *const dA_dn = a.dA + dn * kG;
     // the slice as a buffer resource for the device-coherent accesses
     // (its byte size fits 32 bits: checked on the host)
-    const __amdgpu_buffer_rsrc_t dA_rs = __builtin_amdgcn_make_buffer_rsrc(
-        dA_dn, (short)0, (int)(V * kG * sizeof(float)), kBufferRsrcWord3);
+    const __amdgpu_buffer_rsrc_t dA_rs = coherent_rsrc(dA_dn, V * kG);
     float *const gcf_dn = a.gcf + dn * kO;
     const float *const dh_n = a.dh + (long long)n * V * kO;
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;

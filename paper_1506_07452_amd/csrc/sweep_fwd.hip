@@ -31,6 +31,7 @@
 // pixel l%16, so the cell update needs no data exchange and its loads and
 // stores are 16-byte vectors.
 #include "common.h"
+#include "coherent.h"
 #include "sweep.h"
 #include "strip_plan.h"
 #include "timing.h"
@@ -82,7 +83,9 @@ __device__ inline int fdiv_floor(int i, float inv_w) {
 }
 
 // Waits until the strip's neighbours have published `step` steps (bounded:
-// a wait that never ends raises the error flag and gives up).
+// a wait that never ends raises the error flag and gives up).  Their shared
+// columns are then read at device coherence, so no cache invalidate is
+// needed.
 __device__ inline void wait_neighbours(const SweepArgs &a, int nb_lo, int nb_hi, int step)
 {
     const int nb = threadIdx.x == 0 ? nb_lo : (threadIdx.x == 1 ? nb_hi : -1);
@@ -99,16 +102,14 @@ __device__ inline void wait_neighbours(const SweepArgs &a, int nb_lo, int nb_hi,
                 __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
                 break;
         }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
 }
 
-// Publishes `step` completed steps of this strip: the calling wave writes L2
-// back (agent-scope release), waits for it, then stores the flag.  Callers
-// make sure every store to publish has reached L2 first.
+// Publishes `step` completed steps of this strip.  The columns neighbours
+// read are written at device coherence; callers make sure those stores have
+// completed (every storing wave waited for vmcnt 0) before the flag goes up.
 __device__ inline void publish(const SweepArgs &a, int step)
 {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __hip_atomic_store(&a.flags[blockIdx.x], step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -230,6 +231,14 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
     // a slice fit in 32 bits (V * 64 < 2^31 is checked at the boundary).
     const long long dn = ((long long)d * a.g.N + n) * V;
     float *const hd_dn = a.hd + dn * kO;
+    // h^d of the slice as a buffer resource for the device-coherent accesses
+    // of the columns shared with neighbour strips (this strip's first and
+    // last columns and the halo columns beside them)
+    const __amdgpu_buffer_rsrc_t hd_rs = coherent_rsrc(hd_dn, V * kO);
+    auto is_shared_col = [&](int pc) {
+        return (pc == q0 - 1) | (pc == q1) | ((pc == q0) & (nb_lo >= 0)) |
+               ((pc == q1 - 1) & (nb_hi >= 0));
+    };
     float *const cell_dn = a.cell + dn * kO;
     float *const gates_dn = a.gates ? a.gates + dn * kG : nullptr;
     const float *const x_n = a.x + (long long)n * V * C;
@@ -317,7 +326,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
                     const int pc = side ? q1 : q0 - 1;
                     if (pc >= 0 && pc < dg.Q) {
                         const f4 v =
-                            *(const f4 *)&hd_dn[(pplane + r * sp + pc * sq) * kO + qd * 4];
+                            load_coherent(hd_rs, (pplane + r * sp + pc * sq) * kO + qd * 4);
                         *(f4 *)&hprev[((side ? TQ + 1 : 0) * P2 + r + 1) * kHS + qd * 4] = v;
                     }
                 }
@@ -339,7 +348,10 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
                 if (mt * 16 + col < npx) {
                     *(f4 *)&cb[pa * kCS + 4 * q4] = cn;
                     *(f4 *)&hcur[base * kHS + 4 * q4] = hn;
-                    *(f4 *)&hd_dn[v * kO + 4 * q4] = hn;
+                    if (is_shared_col(q0 + ca))
+                        store_coherent(hd_rs, v * kO + 4 * q4, hn);
+                    else
+                        *(f4 *)&hd_dn[v * kO + 4 * q4] = hn;
                     if (gates_dn) {
                         *(f4 *)&cell_dn[v * kO + 4 * q4] = cn;
                         float *gp = gates_dn + v * kG + 4 * q4;
@@ -407,7 +419,11 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
                         const bool ok = e < nh && t > 0 && pr >= 0 && pr < dg.P && pc >= 0 &&
                                         pc < dg.Q;
                         const int off = ok ? (sprev_plane + pr * sp + pc * sq) * kO + qd * 4 : 0;
-                        const f4 v = *(const f4 *)&hd_dn[off];
+                        f4 v;
+                        if (is_shared_col(pc))
+                            v = load_coherent(hd_rs, off);
+                        else
+                            v = *(const f4 *)&hd_dn[off];
                         hv[u] = ok ? v : f4{0.0f, 0.0f, 0.0f, 0.0f};
                     }
                     {
@@ -450,7 +466,10 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
                 f4 gi, gf, gg, go, cn, hn;
                 lstm_cell(acc, cv, t > 0, gi, gf, gg, go, cn, hn);
                 *(f4 *)&cell_dn[v * kO + 4 * q4] = cn;
-                *(f4 *)&hd_dn[v * kO + 4 * q4] = hn;
+                if (is_shared_col(pa - ra * TQ + q0))
+                    store_coherent(hd_rs, v * kO + 4 * q4, hn);
+                else
+                    *(f4 *)&hd_dn[v * kO + 4 * q4] = hn;
                 if (gates_dn) {
                     float *gp = gates_dn + v * kG + 4 * q4;
                     *(f4 *)&gp[0] = gi;
@@ -462,9 +481,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
             __syncthreads();
         }
         // ---- publish h_t -------------------------------------------------
-        // Every wave waits until its own stores have reached L2, then one
-        // thread writes L2 back (release at agent scope) and raises the flag:
-        // one cache writeback per workgroup and step instead of one per wave.
+        // Every wave waits until its own stores have completed, then one
+        // thread raises the flag.
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
         if (threadIdx.x == 0) publish(a, t + 1);

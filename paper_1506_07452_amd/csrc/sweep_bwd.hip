@@ -284,12 +284,12 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
 // index) of one direction and walks them 16 voxels (four MFMA k-steps) at
 // a time, holding all 4 x ceil(N / 16) output tiles (in AGPRs; one wave per
 // SIMD).  Operands come straight from global memory into registers
-// (lane group q takes voxel 4 ks + q, lane col takes a gate-unit (A) or an
-// im2col column (B), so every load is 64 contiguous bytes per voxel), the
+// (lane col takes a gate-unit (A) or an im2col column (B), so every load is
+// 64 contiguous bytes per voxel), the
 // next group's loads are in flight while the current group's MFMAs run,
 // and the accumulators stay in VGPRs for the whole launch: no LDS, no
-// barriers.  Zero padding (off-plane taps, h_{-1}) comes from clamped
-// addresses and selects.
+// barriers.  Zero padding (off-plane taps, h_{-1}) comes from the buffer
+// range check.
 constexpr int kWgWaves = 4;                    // one team (wave) per SIMD
 constexpr int kWgTeamsPerDir = 170;
 
@@ -336,77 +336,95 @@ __device__ inline void wg_rows_team(const WgRowArgs &a, int d, long long r0, lon
 #pragma unroll
         for (int j = 0; j < NTC; ++j) acc[g][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
+    // Operands of one group of 16 voxels.  K order inside the group: lane
+    // group q takes voxels 4q .. 4q+3 (k-step ks: voxel 4q + ks), so the
+    // three column taps of an h_{t-1} row read a sliding window of six
+    // loads per lane: tap (r, dq) at k-step ks is hv[r][ks + dq].
+    constexpr int NX = NT0 + NTC > 9 ? NT0 + NTC - (NT0 > 9 ? NT0 : 9) : 0;   // input tiles
+    constexpr int JX = NT0 > 9 ? 0 : 9 - NT0;                                  // first input j
     struct Ops {
-        float a[4][4];      // [k-step][gate]
-        float b[4][NTC];    // [k-step][tile]
+        float a[4][4];                 // [k-step][gate]: dA
+        float hv[3][6];                // [row p-1, p, p+1][column 4q-1 .. 4q+4]: h_{t-1}
+        float bx[4][NX > 0 ? NX : 1];  // [k-step][input tile]: x_t
     };
-    // K order inside a group of 16 voxels: lane group q takes voxels
-    // 4q .. 4q+3 (k-step ks: voxel 4q + ks), so the three column taps of an
-    // h_{t-1} row share six loads per lane.
-    auto load = [&](const WgCursor &cu, bool live, Ops &o) {
-        const int p = cu.p, t = cu.t, n = cu.n;
-        const int s = dg.sign > 0 ? t : dg.T - 1 - t;
-        const long long dn = ((long long)d * a.g.N + n) * V;
-        // row-uniform bases (rows off the plane are clamped and masked)
-        const float *dA_row = a.dA + (dn + (long long)s * ss + (long long)p * sp) * kG;
-        const float *h_pl = a.hd + (dn + (long long)(t > 0 ? s - dg.sign : s) * ss) * kO;
-        const float *x_pl = a.x + ((long long)n * V + (long long)s * ss) * C;
-        const int colbase = cu.qg * 16 + 4 * q;
-        // bounds as non-short-circuit unsigned compares: no branches.  Masks
-        // multiply (not select) the loaded values, so that every load is
-        // unconditional and no branch splits the batch of loads.
+    constexpr bool kRow[3] = {NT0 < 3, NT0 < 6 && NT0 + NTC > 3, NT0 + NTC > 6};
+    // Row-uniform state of the group being loaded: buffer resources of the
+    // slice, planes, row validity.  An invalid lane (off the plane, past the
+    // row, h_{-1}) gets an out-of-range offset and the hardware returns 0,
+    // so no mask touches a loaded value before its MFMA.
+    constexpr int kOOB = 0x7ffffff0;
+    struct Row {
+        __amdgpu_buffer_rsrc_t rs_a, rs_h, rs_x;
+        int s, p, colbase;
+        bool live, hok[3];
+    };
+    auto row_of = [&](const WgCursor &cu, bool live) {
+        Row w;
+        const long long dn = ((long long)d * a.g.N + cu.n) * V;
+        // slice resources (byte sizes fit 31 bits: checked on the host)
+        w.rs_a = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(a.dA + dn * kG), (short)0,
+                                                   (int)(V * kG * 4), kBufferRsrcWord3);
+        w.rs_h = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(a.hd + dn * kO), (short)0,
+                                                   (int)(V * kO * 4), kBufferRsrcWord3);
+        w.rs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(a.x + (long long)cu.n * V * C),
+                                                   (short)0, (int)(V * C * 4), kBufferRsrcWord3);
+        w.s = dg.sign > 0 ? cu.t : dg.T - 1 - cu.t;
+        w.p = cu.p;
+        w.colbase = cu.qg * 16 + 4 * q;
+        w.live = live;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const int qq = colbase + ks;
-            const bool vq = live & ((unsigned)qq < (unsigned)dg.Q);
-            const int qc = vq ? qq : 0;
+        for (int r = 0; r < 3; ++r)
+            w.hok[r] = live & (cu.t > 0) & ((unsigned)(cu.p + r - 1) < (unsigned)dg.P);
+        return w;
+    };
+    // bounds as non-short-circuit unsigned compares: no branches
+    auto load_a = [&](const Row &w, int ks, Ops &o) {
+        const int qq = w.colbase + ks;
+        const bool vq = w.live & ((unsigned)qq < (unsigned)dg.Q);
+        const int off = (w.s * ss + w.p * sp + qq * sq) * kG + col;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const float v = dA_row[qc * sq * kG + g * 16 + col];
-                o.a[ks][g] = v * (vq ? 1.0f : 0.0f);
-            }
-        }
-        // h_{t-1} taps: rows p-1, p, p+1 (tiles 0-2, 3-5, 6-8)
+        for (int g = 0; g < 4; ++g)
+            o.a[ks][g] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                w.rs_a, vq ? (off + g * 16) * 4 : kOOB, 0, 0));
+    };
+    auto load_h = [&](const Row &w, int m, Ops &o) {
+        const int c = w.colbase - 1 + m;
+        const bool okc = (unsigned)c < (unsigned)dg.Q;
+        const int sprev = w.s - dg.sign;
 #pragma unroll
         for (int r = 0; r < 3; ++r) {
-            bool any = false;
+            if (!kRow[r]) continue;
+            const int off = (sprev * ss + (w.p + r - 1) * sp + c * sq) * kO + col;
+            o.hv[r][m] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                w.rs_h, (w.hok[r] & okc) ? off * 4 : kOOB, 0, 0));
+        }
+    };
+    auto load_x = [&](const Row &w, int ks, Ops &o) {
 #pragma unroll
-            for (int j = 0; j < NTC; ++j) any |= (NT0 + j < 9) && ((NT0 + j) / 3 == r);
-            if (!any) continue;
-            const int pp = p + r - 1;
-            const bool rok = (t > 0) & ((unsigned)pp < (unsigned)dg.P);
-            const float *hrow = h_pl + (long long)(rok ? pp : p) * sp * kO;
-            float hv[6];
+        for (int jx = 0; jx < NX; ++jx) {
+            const int j = JX + jx;
+            const int pp = w.p + xtap_dp[j], c = w.colbase + ks + xtap_dq[j];
+            const bool ok = w.live & (xkind[j] == 0) & ((unsigned)pp < (unsigned)dg.P) &
+                            ((unsigned)c < (unsigned)dg.Q);
+            const int off = (w.s * ss + pp * sp + c * sq) * C + xtap_c[j];
+            o.bx[ks][jx] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                w.rs_x, ok ? off * 4 : kOOB, 0, 0));
+        }
+    };
+    // ones of the bias column (1 for a voxel on the plane, else 0: its dA
+    // is 0 then anyway)
+    float bias_one[NTC];
 #pragma unroll
-            for (int m = 0; m < 6; ++m) {
-                const int c = colbase - 1 + m;
-                const bool ok = rok & ((unsigned)c < (unsigned)dg.Q);
-                const float v = hrow[(ok ? c : 0) * sq * kO + col];
-                hv[m] = v * (ok ? 1.0f : 0.0f);
-            }
+    for (int j = 0; j < NTC; ++j) bias_one[j] = (NT0 + j >= 9 && xkind[j] == 1) ? 1.0f : 0.0f;
+    auto mfma_k = [&](const Ops &o, int ks) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
             for (int j = 0; j < NTC; ++j) {
                 const int nt = NT0 + j;
-                if (nt < 9 && nt / 3 == r)
-#pragma unroll
-                    for (int ks = 0; ks < 4; ++ks) o.b[ks][j] = hv[ks + nt % 3];
+                const float b = nt < 9 ? o.hv[nt / 3][ks + nt % 3] : o.bx[ks][j - JX] + bias_one[j];
+                acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[ks][g], b, acc[g][j], 0, 0, 0);
             }
-        }
-        // input taps and the bias column (tiles 9, 10, ...)
-#pragma unroll
-        for (int j = 0; j < NTC; ++j) {
-            if (NT0 + j < 9) continue;
-            const int pp = p + xtap_dp[j];
-            const bool rok = (xkind[j] == 0) & ((unsigned)pp < (unsigned)dg.P);
-            const float *xrow = x_pl + (rok ? pp : p) * sp * C + xtap_c[j];
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const int c = colbase + ks + xtap_dq[j];
-                const bool ok = rok & ((unsigned)c < (unsigned)dg.Q);
-                const float v = xrow[(ok ? c : 0) * sq * C];
-                o.b[ks][j] = v * (ok ? 1.0f : 0.0f) + (xkind[j] == 1 ? 1.0f : 0.0f);
-            }
-        }
     };
     // cursor over (n, t, p, column group), starting at row r0; past the end
     // it stays on a valid row and the loads are masked to zero
@@ -427,24 +445,35 @@ __device__ inline void wg_rows_team(const WgRowArgs &a, int d, long long r0, lon
             }
         }
     };
-    auto mfma_group = [&](const Ops &o) {
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-#pragma unroll
-                for (int j = 0; j < NTC; ++j)
-                    acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[ks][g], o.b[ks][j],
-                                                                     acc[g][j], 0, 0, 0);
-    };
     const long long total = (r1 - r0) * ngrp;
-    Ops cur, nxt;
-    load(cu, total > 0, cur);
+    Ops o;
+    {
+        const Row w = row_of(cu, total > 0);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            load_a(w, ks, o);
+            load_x(w, ks, o);
+        }
+#pragma unroll
+        for (int m = 0; m < 6; ++m) load_h(w, m, o);
+    }
+    // Each operand register is refilled with the next group's value right
+    // after its last use by this group's MFMAs: one group of operands is
+    // live, and every load has a whole group of MFMAs to arrive.
     for (long long it = 0; it < total; ++it) {
         advance();
-        load(cu, it + 1 < total, nxt);
-        mfma_group(cur);
-        cur = nxt;
+        const Row w = row_of(cu, it + 1 < total);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            mfma_k(o, ks);
+            load_a(w, ks, o);
+            load_x(w, ks, o);
+            load_h(w, ks, o);          // hv[.][ks] was last used at k-step ks
+            if (ks == 3) {
+                load_h(w, 4, o);
+                load_h(w, 5, o);
+            }
+        }
     }
 #pragma unroll
     for (int g = 0; g < 4; ++g)

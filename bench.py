@@ -46,6 +46,9 @@ def phase_work(name, V, C, O):
         return "mfma", 6 * V * 2 * 9 * G * C, "TFLOP/s"
     if name.startswith("sum_dirs"):
         return "hbm", (6 + 1) * V * O * 4, "GB/s"
+    if name.startswith("head_fused"):
+        # reads h and the label, writes p (4 classes) and dL/dh per voxel
+        return "hbm", V * (O * 4 + 4 + 4 * 4 + O * 4), "GB/s"
     return None, None, None
 
 
@@ -54,9 +57,10 @@ def phase_work(name, V, C, O):
 # the ones measured.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_mr48x240x240.md")
 KERNEL_SOURCES = {
-    "sweep_fwd_mfma": ["sweep_fwd.hip", "strip_plan.h", "common.h"],
-    "sweep_bwd_mfma": ["sweep_bwd.hip", "strip_plan.h", "common.h"],
-    "wgrad_mfma": ["sweep_bwd.hip", "strip_plan.h", "common.h"],
+    "sweep_fwd_mfma": ["sweep_fwd.hip", "strip_plan.h", "common.h", "coherent.h"],
+    "sweep_bwd_mfma": ["sweep_bwd.hip", "strip_plan.h", "common.h", "coherent.h"],
+    "wgrad_mfma": ["sweep_bwd.hip", "strip_plan.h", "common.h", "coherent.h"],
+    "head_fused": ["fc.hip", "common.h"],
 }
 
 

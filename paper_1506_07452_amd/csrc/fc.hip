@@ -636,17 +636,29 @@ k_head_train(long long M, int K, const float *__restrict__ x, const float *__res
     for (int e = threadIdx.x; e < PT; e += kHT) part[e] = R[e];
 }
 
-// Sums the per-block partials in block order and scatters them to the outputs.
+// Sums the per-block partials and scatters them to the outputs.  A block
+// takes 16 outputs; its 256 threads split the partials into 16 interleaved
+// parts (thread (part, output)), and the 16 part sums of an output are then
+// added in part order: a fixed summation order, 16x shorter dependent chains.
+constexpr int kRedOut = 16, kRedParts = kThreads / kRedOut;
+
 __global__ void __launch_bounds__(kThreads)
 k_head_reduce(long long M, int Cin, int F, int K, int nblk, const float *__restrict__ partial,
               float *__restrict__ dw1, float *__restrict__ db1, float *__restrict__ dw2,
               float *__restrict__ db2, float *__restrict__ loss)
 {
+    __shared__ float part_sum[kRedParts][kRedOut];
     const int P1 = F * (Cin + 1), P2 = K * (F + 1), PT = P1 + P2 + 1;
-    const int i = blockIdx.x * kThreads + threadIdx.x;
-    if (i >= PT) return;
+    const int o = threadIdx.x % kRedOut, part = threadIdx.x / kRedOut;
+    const int i = blockIdx.x * kRedOut + o;
     float acc = 0.0f;
-    for (int b = 0; b < nblk; ++b) acc += partial[(long long)b * PT + i];
+    if (i < PT)
+        for (int b = part; b < nblk; b += kRedParts) acc += partial[(long long)b * PT + i];
+    part_sum[part][o] = acc;
+    __syncthreads();
+    if (part != 0 || i >= PT) return;
+    acc = 0.0f;
+    for (int k = 0; k < kRedParts; ++k) acc += part_sum[k][o];
     if (i < P1) {
         const int f = i / (Cin + 1), c = i % (Cin + 1);
         if (c < Cin) dw1[f * Cin + c] = acc;
@@ -682,7 +694,7 @@ int head_launch(long long M, int K, const float *x, const float *w1, const float
     k_head_train<CIN, F><<<nb, kHT, lds, st>>>(M, K, x, w1, b1, w2, b2, labels, p, dx, partial);
     PLSTM_LAUNCH_CHECK();
     const int PT = F * (CIN + 1) + K * (F + 1) + 1;
-    k_head_reduce<<<(PT + kThreads - 1) / kThreads, kThreads, 0, st>>>(
+    k_head_reduce<<<(PT + kRedOut - 1) / kRedOut, kThreads, 0, st>>>(
         M, CIN, F, K, nb, partial, dw1, db1, dw2, db2, loss);
     PLSTM_LAUNCH_CHECK();
     timing_end(2, st);

@@ -4,8 +4,10 @@
 //
 // One cooperative launch runs all six directions (and all batch elements) at
 // once.  The plane of each direction is cut into strips of whole rows x a few
-// columns; one workgroup (8 waves, two per SIMD) owns one strip for the whole
-// sweep:
+// columns; one workgroup (16 waves, four per SIMD) owns one strip for the
+// whole sweep.  A strip that fits LDS stays there for the whole sweep (h
+// double-buffered, c in LDS, only the halo columns and x_t read per step);
+// otherwise, per step:
 //
 //   for t in 0..T-1:
 //     wait until the two neighbouring strips have published h_{t-1}
@@ -15,13 +17,12 @@
 //         A = bias + im2col(x_t) W_x + im2col(h_{t-1}) W_h   (v_mfma_f32_16x16x4f32)
 //         gates, c_t = g i + c_{t-1} f, h_t = o tanh(c_t)    (in registers)
 //         write h_t, c_t (and the gates when training) to global memory
-//     publish: release fence, flag = t + 1
+//     publish: flag = t + 1 once the stores have completed
 //
-// The recurrent weights live in VGPRs as MFMA B fragments for the whole
-// kernel (the input-convolution fragments in LDS); h of
-// every plane stays in the per-direction volume in global memory, so a step
-// only reads plane t-1 and writes plane t (no write-after-read hazard), and
-// LDS is just a staging copy.  MFMA layout (16x16x4 f32, one block): lane l
+// The weight fragments (recurrent and input) and the bias live in LDS for
+// the whole kernel; h of every plane stays in the per-direction volume in
+// global memory, so a step only reads plane t-1 and writes plane t (no
+// write-after-read hazard).  MFMA layout (16x16x4 f32, one block): lane l
 // supplies A[m = l%16][k = l/16] and B[k = l/16][n = l%16] and receives
 // D[4(l/16) + i][l%16], i = 0..3.  Gate-units are on M (M-tile g = gate g of
 // the 16 units, the weights are the A operand) and pixels on N (B = im2col).
@@ -43,14 +44,15 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kO = 16;
 constexpr int kG = 4 * kO;
-constexpr int kWaves = 8;          // two waves per SIMD: one computes gates while the other runs MFMAs
+constexpr int kWaves = 16;         // four waves per SIMD: gate math of some overlaps the MFMAs of others
+constexpr int kWhFloats = 9 * 4 * 64 * 4;   // recurrent A fragments in LDS
 constexpr int kThreads = 64 * kWaves;
 constexpr int kHS = 20;          // LDS floats per staged h pixel (16 + 4 pad)
 constexpr int kMaxSpin = 1 << 21;
 constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unconstrained
 constexpr int kBatch = 4;        // staging loads in flight per thread
 constexpr int kCS = 20;          // LDS floats per cell state of a resident strip (16 + 4 pad)
-constexpr int kResX = 8;         // x_t staging registers per thread (resident strips)
+constexpr int kResX = 4;         // x_t staging registers per thread (resident strips)
 
 struct SweepArgs {
     Geom g;
@@ -119,7 +121,7 @@ __device__ inline void publish(const SweepArgs &a, int step)
 // the staged (halo-padded) tile whose rows are `rs` and columns `cs` pixels
 // apart.
 template <int C>
-__device__ __forceinline__ void tile_preact(const float (&bh)[9][4][4], const float *hsrc,
+__device__ __forceinline__ void tile_preact(const float *whs, const float *hsrc,
                                             const float *xs, const float *wxs, const float *bs,
                                             int base, int rs, int cs, const int *xoff, int q4,
                                             int lane, f4 (&acc)[4])
@@ -131,11 +133,14 @@ __device__ __forceinline__ void tile_preact(const float (&bh)[9][4][4], const fl
     for (int tap = 0; tap < 9; ++tap) {
         const int o = (tap / 3 - 1) * rs + (tap % 3 - 1) * cs;
         const f4 hv = *(const f4 *)&hsrc[(base + o) * kHS + 4 * q4];
+        f4 w[4];
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) w[s2] = *(const f4 *)&whs[((tap * 4 + s2) * 64 + lane) * 4];
 #pragma unroll
         for (int s2 = 0; s2 < 4; ++s2)
 #pragma unroll
             for (int g = 0; g < 4; ++g)
-                acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(bh[tap][s2][g], hv[s2], acc[g], 0,
+                acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[s2][g], hv[s2], acc[g], 0,
                                                             0, 0);
     }
 #pragma unroll
@@ -196,16 +201,20 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
 
     // ---- recurrent weights as MFMA A fragments (resident for the sweep) ---
     const long long V = a.g.V;
-    float bh[9][4][4];
+    // Recurrent weights as MFMA A fragments in LDS: entry (tap, s, lane)
+    // holds the four gates' weights of gate-unit lane%16 for hidden unit
+    // 4 (lane/16) + s, one 16-byte read per k-step (LDS keeps the waves at
+    // about 110 VGPRs, so four share a SIMD).
+    float *whs = bs + kG;
+    for (int e = threadIdx.x; e < 9 * 4 * 64; e += kThreads) {
+        const int l = e & 63, s = (e >> 6) & 3, tap = e >> 8;
+        const int lq = l >> 4, lc = l & 15;
+        f4 v;
 #pragma unroll
-    for (int tap = 0; tap < 9; ++tap)
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int j = 4 * q4 + s, gn = g * kO + col;
-                bh[tap][s][g] = a.wh[(((long long)d * kG + gn) * kO + j) * 9 + tap];
-            }
+        for (int g = 0; g < 4; ++g)
+            v[g] = a.wh[(((long long)d * kG + g * kO + lc) * kO + 4 * lq + s) * 9 + tap];
+        *(f4 *)&whs[e * 4] = v;
+    }
     // Input-convolution A fragments go to LDS (they feed few MFMAs; keeping
     // them out of VGPRs lets two waves share a SIMD).
     int xoff[KXS];
@@ -257,7 +266,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
         const int npl = P2 * W2;
         const int npx = P * TQ;
         const int nmt = (npx + 15) >> 4;
-        float *hb0 = bs + kG;
+        float *hb0 = whs + kWhFloats;
         float *hb1 = hb0 + npl * kHS;
         float *xs = hb1 + npl * kHS;
         float *cb = xs + ((npl * C + 3) & ~3);     // [npx][kCS] cell states (16-byte aligned)
@@ -342,7 +351,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
                 const int v = splane + ra * sp + (q0 + ca) * sq;
                 const f4 cv = *(const f4 *)&cb[pa * kCS + 4 * q4];
                 f4 acc[4];
-                tile_preact<C>(bh, hprev, xs, wxs, bs, base, 1, P2, xoff, q4, lane, acc);
+                tile_preact<C>(whs, hprev, xs, wxs, bs, base, 1, P2, xoff, q4, lane, acc);
                 f4 gi, gf, gg, go, cn, hn;
                 lstm_cell(acc, cv, t > 0, gi, gf, gg, go, cn, hn);
                 if (mt * 16 + col < npx) {
@@ -386,7 +395,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
 
     // ================= chunked strip: rows staged per step =================
     const int chunk_rows = a.chunk_rows[d];
-    float *hs = bs + kG;
+    float *hs = whs + kWhFloats;
     float *xs = hs + (chunk_rows + 2) * (a.max_w[d] + 2) * kHS;
     const float inv_tq = 1.0f / (float)TQ;
     __syncthreads();
@@ -461,7 +470,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
                 // otherwise sink it to its use and expose its latency)
                 __builtin_amdgcn_sched_barrier(0);
                 f4 acc[4];
-                tile_preact<C>(bh, hs, xs, wxs, bs, base, W2, 1, xoff, q4, lane, acc);
+                tile_preact<C>(whs, hs, xs, wxs, bs, base, W2, 1, xoff, q4, lane, acc);
                 if (mt * 16 + col >= npx) continue;
                 f4 gi, gf, gg, go, cn, hn;
                 lstm_cell(acc, cv, t > 0, gi, gf, gg, go, cn, hn);
@@ -499,7 +508,8 @@ __global__ void k_fill_zero(int *p, int n)
 StripCostModel fwd_model(int C)
 {
     StripCostModel m;
-    m.fixed_bytes = (size_t)(((9 * C + 3) / 4) * 256 + kG) * sizeof(float);   // wx fragments, bias
+    // wx fragments, bias, recurrent fragments
+    m.fixed_bytes = (size_t)(((9 * C + 3) / 4) * 256 + kG + kWhFloats) * sizeof(float);
     m.px_bytes = (size_t)(kHS + C) * sizeof(float);                     // h + x per pixel
     m.c_sync = 3.0;
     m.c_tile = 3.2;

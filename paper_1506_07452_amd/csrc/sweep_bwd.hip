@@ -280,9 +280,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
 // ---- parameter gradients, register-streamed --------------------------------
 // dW[d] = sum over voxels v of dA[v] (x) [im2col(h_{t-1})(v), im2col(x_t)(v), 1],
 // an implicit GEMM with M = 64 gate-units, N = 144 + 9C + 1 and K = voxels.
-// One wave owns a contiguous range of rows (fixed plane and first in-plane
-// index) of one direction and walks them 16 voxels (four MFMA k-steps) at
-// a time, holding all 4 x ceil(N / 16) output tiles (in AGPRs; one wave per
+// One wave owns a contiguous range of units (16 voxels of a row: four MFMA
+// k-steps) of one direction, walking each column group down the rows of a
+// plane, and holds all 4 x ceil(N / 16) output tiles (in AGPRs; one wave per
 // SIMD).  Operands come straight from global memory into registers
 // (lane col takes a gate-unit (A) or an im2col column (B), so every load is
 // 64 contiguous bytes per voxel), the
@@ -426,18 +426,25 @@ __device__ inline void wg_rows_team(const WgRowArgs &a, int d, long long r0, lon
                 acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[ks][g], b, acc[g][j], 0, 0, 0);
             }
     };
-    // cursor over (n, t, p, column group), starting at row r0; past the end
-    // it stays on a valid row and the loads are masked to zero
+    // Cursor over units u = ((n T + t) ngrp + qg) P + p: a column group
+    // walks down the rows, so the h_{t-1} and x rows of one group are
+    // re-read (as p + 1, p, p - 1) by the next two groups from cache.  Past
+    // the end it stays on a valid unit and the loads are masked to zero.
     WgCursor cu;
-    cu.p = (int)(r0 % dg.P);
-    cu.t = (int)((r0 / dg.P) % dg.T);
-    cu.n = (int)(r0 / ((long long)dg.P * dg.T));
-    cu.qg = 0;
+    {
+        long long rest = r0;
+        cu.p = (int)(rest % dg.P);
+        rest /= dg.P;
+        cu.qg = (int)(rest % ngrp);
+        rest /= ngrp;
+        cu.t = (int)(rest % dg.T);
+        cu.n = (int)(rest / dg.T);
+    }
     auto advance = [&]() {
-        if (++cu.qg == ngrp) {
-            cu.qg = 0;
-            if (++cu.p == dg.P) {
-                cu.p = 0;
+        if (++cu.p == dg.P) {
+            cu.p = 0;
+            if (++cu.qg == ngrp) {
+                cu.qg = 0;
                 if (++cu.t == dg.T) {
                     cu.t = 0;
                     if (cu.n + 1 < a.g.N) ++cu.n;
@@ -445,7 +452,7 @@ __device__ inline void wg_rows_team(const WgRowArgs &a, int d, long long r0, lon
             }
         }
     };
-    const long long total = (r1 - r0) * ngrp;
+    const long long total = r1 - r0;
     Ops o;
     {
         const Row w = row_of(cu, total > 0);
@@ -495,8 +502,8 @@ k_wgrad_rows(WgRowArgs a)
     if (team >= kDirs * a.tpd) return;
     const int d = team / a.tpd, tin = team % a.tpd;
     const DirGeom dg = a.g.dir[d];
-    const long long rows = (long long)a.g.N * dg.T * dg.P;
-    const long long r0 = rows * tin / a.tpd, r1 = rows * (tin + 1) / a.tpd;
+    const long long units = (long long)a.g.N * dg.T * ((dg.Q + 15) / 16) * dg.P;
+    const long long r0 = units * tin / a.tpd, r1 = units * (tin + 1) / a.tpd;
     float *out = a.partial + (long long)team * kG * a.KCp;
     wg_rows_team<C, 0, WgN<C>::NT>(a, d, r0, r1, q, col, out);
 }

@@ -35,10 +35,14 @@ constexpr int kG = 4 * kO;
 constexpr int kWaves = 16;             // four waves per SIMD
 constexpr int kWaFloats = 9 * 4 * 64 * 4;  // W_h^T fragments in LDS
 constexpr int kThreads = 64 * kWaves;
-constexpr int kAS = 68;                // LDS floats per staged dA pixel (64 + 4 pad)
+// A staged dA pixel is 64 floats in LDS; its 16-byte chunk c sits at
+// position c ^ (pixel & 15), so the 16 pixels a read instruction touches
+// hit 16 different bank groups.
+__device__ inline int swz(int c, int pix) { return c ^ (pix & 15); }
+constexpr int kOutOfRange = 0x7ffffff0;    // buffer offset past any resource: reads zero
+typedef __attribute__((address_space(3))) void lds_void;
 constexpr int kMaxSpin = 1 << 21;
 constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unconstrained
-constexpr int kBatch = 4;              // staging loads in flight per thread
 
 __device__ inline float frcp(float v) { return __builtin_amdgcn_rcpf(v); }
 
@@ -151,32 +155,33 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
         for (int r0 = 0; r0 < dg.P; r0 += chunk_rows) {
             const int CH = min(chunk_rows, dg.P - r0);
             const int npl = (CH + 2) * W2;
-            // ---- stage dA_{t+1} (chunk + halo), zero outside / at the end
-            const int nA = npl * 16;
-            for (int e0 = threadIdx.x; e0 < nA; e0 += kThreads * kBatch) {
-                f4 v[kBatch];
-#pragma unroll
-                for (int u = 0; u < kBatch; ++u) {
-                    const int e = e0 + u * kThreads;
-                    const int pix = e >> 4, qd = e & 15;
-                    const int rr = fdiv_floor(pix, inv_w2);
-                    const int pr = rr + r0 - 1, pc = pix - rr * W2 + q0 - 1;
-                    const bool ok = e < nA && has_next && pr >= 0 && pr < dg.P && pc >= 0 &&
-                                    pc < dg.Q;
-                    const int off = ok ? (nplane + pr * sp + pc * sq) * kG + qd * 4 : 0;
-                    f4 val;
+            // ---- stage dA_{t+1} (chunk + halo) straight into LDS ------------
+            // Direct-to-LDS buffer loads (no registers, all in flight at
+            // once): one instruction moves 4 pixels, lane l the 16-byte chunk
+            // at position l%16 of pixel 4 i + l/16, which holds its chunk
+            // (l%16) ^ (pixel & 15) (see `swz`).  Off-plane pixels, the halo
+            // past the volume and the plane after the last get an
+            // out-of-range offset and the hardware writes zeros.
+            const int nslots = (npl + 3) >> 2;
+            for (int i = wave; i < nslots; i += kWaves) {
+                const int pix = 4 * i + (lane >> 4);
+                const int chunk = col ^ (pix & 15);
+                const int rr = fdiv_floor(pix, inv_w2);
+                const int pr = rr + r0 - 1, pc = pix - rr * W2 + q0 - 1;
+                const bool ok = has_next & (pr >= 0) & (pr < dg.P) & (pc >= 0) & (pc < dg.Q);
+                const int boff =
+                    ok ? ((nplane + pr * sp + pc * sq) * kG + chunk * 4) * (int)sizeof(float)
+                       : kOutOfRange;
+                lds_void *dst = (lds_void *)&as[i * 4 * kG];
+                if (pix < npl) {
                     if (is_shared_col(pc))   // read at device coherence (written that way)
-                        val = load_coherent(dA_rs, off);
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(dA_rs, dst, 16, boff, 0, 0,
+                                                                 kCachePolicySC1);
                     else
-                        val = *(const f4 *)&dA_dn[off];
-                    v[u] = ok ? val : f4{0.0f, 0.0f, 0.0f, 0.0f};
-                }
-#pragma unroll
-                for (int u = 0; u < kBatch; ++u) {
-                    const int e = e0 + u * kThreads;
-                    if (e < nA) *(f4 *)&as[(e >> 4) * kAS + (e & 15) * 4] = v[u];
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(dA_rs, dst, 16, boff, 0, 0, 0);
                 }
             }
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
             __syncthreads();
             // ---- 16-pixel tiles ------------------------------------------
             // Each tile's epilogue operands are loaded before its contraction.
@@ -210,10 +215,11 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                 for (int tap = 0; tap < 9; ++tap) {
                     // h_t at pixel p fed A_{t+1} at p - (tap offset)
                     const int o = (tap / 3 - 1) * W2 + (tap % 3 - 1);
-                    const float *src = &as[(base - o) * kAS + 16 * q4];
+                    const int pp = base - o;
                     f4 bv[4], av[4];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) bv[k] = *(const f4 *)&src[4 * k];
+                    for (int k = 0; k < 4; ++k)
+                        bv[k] = *(const f4 *)&as[pp * kG + 4 * swz(4 * q4 + k, pp)];
 #pragma unroll
                     for (int k = 0; k < 4; ++k)
                         av[k] = *(const f4 *)&was[((tap * 4 + k) * 64 + lane) * 4];
@@ -542,7 +548,7 @@ StripCostModel bwd_model()
 {
     StripCostModel m;
     m.fixed_bytes = kWaFloats * sizeof(float);
-    m.px_bytes = kAS * sizeof(float);
+    m.px_bytes = kG * sizeof(float);
     m.c_sync = 3.0;
     m.c_tile = 2.9;
     m.c_stage0 = 1.0;

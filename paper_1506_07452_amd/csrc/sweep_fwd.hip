@@ -215,8 +215,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_fwd(SweepArgs a)
             v[g] = a.wh[(((long long)d * kG + g * kO + lc) * kO + 4 * lq + s) * 9 + tap];
         *(f4 *)&whs[e * 4] = v;
     }
-    // Input-convolution A fragments go to LDS (they feed few MFMAs; keeping
-    // them out of VGPRs lets two waves share a SIMD).
+    // Input-convolution A fragments in LDS as well (they feed few MFMAs).
     int xoff[KXS];
 #pragma unroll
     for (int ks = 0; ks < KXS; ++ks) {

@@ -184,14 +184,20 @@ int pyramid_lstm_timing_read(int max_phases, char *names, double *ms, int *launc
 
 /* Forward implementation selection, for testing and tuning (process-wide):
  * 0 = automatic (default): the persistent MFMA sweep where it supports the
- * shape (fp32, O = 16, C <= 4, grid co-resident), else the generic path;
- * 1 = generic path only; 2 = same as 0; 3 = as 0, but the MFMA sweep stages
- * every strip chunk by chunk (no strip kept whole in LDS).  Returns
- * PLSTM_EINVAL for other values. */
+ * shape (fp32, O = 16, C <= 4, grid co-resident), else the plane-step MFMA
+ * path where it does (O = 16, 32 or 64, C <= 64), else the generic path;
+ * 1 = generic path only; 2 = same as 0; 3 = as 0, but the persistent sweep
+ * stages every strip chunk by chunk (no strip kept whole in LDS); 4 = the
+ * plane-step MFMA path where it supports the shape, else the generic path.
+ * Returns PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_forward_path(int path);
 
 /* Backward implementation selection, for testing and tuning (process-wide):
- * 0 = automatic (default), 1 = generic per-plane path only, 2 = same as 0. */
+ * 0 = automatic (default): persistent MFMA reverse sweep, else plane-step
+ * MFMA path, else generic (same shape rules as the forward); 1 = generic
+ * per-plane path only; 2 = same as 0; 3 = the plane-step MFMA path where it
+ * supports the shape, else the generic path.  Returns PLSTM_EINVAL for
+ * other values. */
 int pyramid_lstm_set_backward_path(int path);
 
 #ifdef __cplusplus

@@ -13,24 +13,44 @@ size_t forward_ws(const Geom &g, int dtype, bool training)
         const size_t s = sweep_fwd_ws(g, training);
         if (s > need) need = s;
     }
+    if (step_supported(g)) {
+        Carve cv(nullptr);
+        if (!training) {
+            cv.take<float>(saved_state_count(g));   // h^d
+            cv.take<float>(saved_state_count(g));   // c^d
+        }
+        const size_t s = align_up(cv.off, 256) + step_fwd_ws(g);
+        if (s > need) need = s;
+    }
     return need;
 }
 
 int forward_dispatch(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
                      const void *b, void *h, const Saved *sv, void *ws, hipStream_t st)
 {
-    if (g_forward_path != 1 && sweep_fwd_supported(g, dtype)) {
+    const int path = g_forward_path;
+    if (path != 1 && path != 4 && sweep_fwd_supported(g, dtype)) {
         Carve cv(ws);
         float *hd = sv ? sv->hd : cv.take<float>(saved_state_count(g));
         float *cellbuf = sv ? sv->cell : cv.take<float>(saved_state_count(g));
         int *flags = cv.take<int>(1024 + 1);
         const int rc = sweep_fwd(g, (const float *)x, (const float *)wx, (const float *)wh,
                                  (const float *)b, hd, cellbuf, sv ? sv->gates : nullptr, flags,
-                                 st, g_forward_path != 3);
+                                 st, path != 3);
         if (rc == PLSTM_OK) return sum_dirs(g, dtype, hd, h, st);
         // A grid that cannot be co-resident or a plane too wide for LDS runs
-        // on the generic path instead.
+        // on another path instead.
         if (rc != PLSTM_ENOTCORESIDENT && rc != PLSTM_EUNSUPPORTED) return rc;
+    }
+    if (path != 1 && step_supported(g)) {
+        Carve cv(ws);
+        float *hd = sv ? sv->hd : cv.take<float>(saved_state_count(g));
+        float *cellbuf = sv ? sv->cell : cv.take<float>(saved_state_count(g));
+        char *rest = (char *)ws + align_up(cv.off, 256);
+        const int rc = step_fwd(g, dtype, x, wx, wh, b, hd, cellbuf, sv ? sv->gates : nullptr,
+                                rest, st);
+        if (rc != PLSTM_OK) return rc;
+        return sum_dirs(g, dtype, hd, h, st);
     }
     return generic_forward(g, dtype, x, wx, wh, b, h, sv, ws, st);
 }
@@ -42,6 +62,10 @@ size_t backward_ws(const Geom &g)
         const size_t s = sweep_bwd_ws(g);
         if (s > need) need = s;
     }
+    if (step_supported(g)) {
+        const size_t s = step_bwd_ws(g);
+        if (s > need) need = s;
+    }
     return need;
 }
 
@@ -49,10 +73,13 @@ int backward_dispatch(const Geom &g, const float *x, const float *wx, const floa
                       const Saved &sv, const float *dh, float *dx, float *dwx, float *dwh,
                       float *db, void *ws, hipStream_t st)
 {
-    if (g_backward_path != 1 && sweep_bwd_supported(g)) {
+    const int path = g_backward_path;
+    if (path != 1 && path != 3 && sweep_bwd_supported(g)) {
         const int rc = sweep_bwd(g, x, wx, wh, sv, dh, dx, dwx, dwh, db, ws, st);
         if (rc != PLSTM_ENOTCORESIDENT && rc != PLSTM_EUNSUPPORTED) return rc;
     }
+    if (path != 1 && step_supported(g))
+        return step_bwd(g, x, wh, wx, sv, dh, dx, dwx, dwh, db, ws, st);
     return generic_backward(g, x, wx, wh, sv, dh, dx, dwx, dwh, db, ws, st);
 }
 
@@ -60,14 +87,14 @@ int backward_dispatch(const Geom &g, const float *x, const float *wx, const floa
 
 extern "C" int pyramid_lstm_set_forward_path(int path)
 {
-    if (path < 0 || path > 3) return PLSTM_EINVAL;
+    if (path < 0 || path > 4) return PLSTM_EINVAL;
     plstm::g_forward_path = path;
     return PLSTM_OK;
 }
 
 extern "C" int pyramid_lstm_set_backward_path(int path)
 {
-    if (path < 0 || path > 2) return PLSTM_EINVAL;
+    if (path < 0 || path > 3) return PLSTM_EINVAL;
     plstm::g_backward_path = path;
     return PLSTM_OK;
 }

@@ -20,6 +20,17 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
               const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
               hipStream_t st);
 
+// Plane-step MFMA path (sweep_step.hip): O = 16, 32, 64, C <= 64, fp32
+// arithmetic (bf16 storage converted on entry), one launch per plane step.
+bool step_supported(const Geom &g);
+size_t step_fwd_ws(const Geom &g);
+int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
+             const void *b, float *hd, float *cell, float *gates, void *ws, hipStream_t st);
+size_t step_bwd_ws(const Geom &g);
+int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, const Saved &sv,
+             const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
+             hipStream_t st);
+
 // h = sum of the six per-direction outputs (generic.hip).
 int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st);
 
@@ -36,7 +47,11 @@ int backward_dispatch(const Geom &g, const float *x, const float *wx, const floa
                       const Saved &sv, const float *dh, float *dx, float *dwx, float *dwh,
                       float *db, void *ws, hipStream_t st);
 
-// 0 = automatic, 1 = generic path only, 2 = persistent MFMA sweep where supported.
+// Forward: 0 = automatic, 1 = generic path only, 2 = persistent MFMA sweep where
+// supported, 3 = as 2 without strips kept whole in LDS, 4 = plane-step MFMA
+// path where supported.  Backward: 0 = automatic, 1 = generic path only,
+// 2 = persistent MFMA sweep where supported, 3 = plane-step MFMA path where
+// supported.
 extern int g_forward_path;
 extern int g_backward_path;
 

@@ -1,0 +1,1080 @@
+// Plane-step MFMA path (Section 2.3, Eq. (7)-(13), and the chain rule
+// through them) for O = 16, 32 or 64 hidden units and any number of input
+// channels: the layers of the stacked networks whose recurrent weights do
+// not fit a workgroup's LDS next to its staged planes.
+//
+// The sweeps run one launch per plane step t.  Within a launch every
+// direction with t < T_d updates its whole plane t as independent GEMM
+// tiles on v_mfma_f32_16x16x4f32:
+//   forward   A_t = b + W_x im2col(x_t) + W_h im2col(h_{t-1})
+//             M = the four gates of 16 units, N = pixels, K = 9 (C' + O),
+//             gates and the cell update fused into the epilogue;
+//   backward  dL/dh_t = dL/dh + sum_taps W_h^T dA_{t+1}[p - tap]
+//             M = 16 units, N = pixels, K = 9 * 4O, the gate gradients
+//             fused into the epilogue.
+// The kernel boundary between steps makes plane t visible to step t + 1 on
+// every XCD, so no flags or coherent accesses are needed.  The weights (a
+// few hundred KB per direction) are repacked once per call into MFMA A
+// fragments and read from L2; the four waves of a workgroup work on
+// neighbouring pixel groups of the same unit group, so they share each
+// fragment through the L1.  The input and h_{t-1} planes are read straight
+// from global memory with raw buffer loads: a tap off the plane gets an
+// out-of-range offset and the hardware returns zero.
+//
+// MFMA layout (16x16x4 f32): lane l supplies A[m = l%16][k = l/16] and
+// B[k = l/16][n = l%16] and receives D[4(l/16) + i][l%16], i = 0..3.  In
+// each group of four k-steps lane group q takes channels 4q .. 4q+3 of a
+// 16-channel block (k-step i: channel 4q + i), so every operand load is one
+// 16-byte vector, and every lane ends with four consecutive units of one
+// pixel: the epilogues need no data exchange and move 16-byte vectors.
+//
+// The input volume is converted once per call to fp32 with its channels
+// zero-padded to C' = a multiple of 16 (so bf16 storage and any C share one
+// kernel); the arithmetic and the saved states are fp32.
+//
+// The parameter gradients and dL/dx are implicit GEMMs over all voxels
+// (no recurrence) on the same MFMA: dW = sum_v dA (x) [im2col(h_{t-1}),
+// im2col(x_t), 1] with K = voxels, and dL/dx = sum_d sum_taps W_x^T dA.
+#include "common.h"
+#include "sweep.h"
+#include "timing.h"
+
+namespace plstm {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kSW = 4;                   // waves per workgroup
+constexpr int kNT = 4;                   // 16-pixel tiles per wave
+constexpr int kOOB = 0x7ffffff0;         // byte offset past any buffer: loads return 0
+constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data
+
+__device__ inline float frcp(float v) { return __builtin_amdgcn_rcpf(v); }
+__device__ inline float fsig(float a) { return frcp(1.0f + __expf(-a)); }
+__device__ inline float ftanh(float a) { return 1.0f - 2.0f * frcp(__expf(2.0f * a) + 1.0f); }
+
+// Buffer resource over `nfloats` floats (the host checks that the byte size
+// fits 31 bits).
+__device__ inline __amdgpu_buffer_rsrc_t slice_rsrc(const float *p, long long nfloats)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p), (short)0,
+                                             (int)(nfloats * (long long)sizeof(float)),
+                                             kRsrcWord3);
+}
+__device__ inline f4 bload4(__amdgpu_buffer_rsrc_t rs, unsigned off)
+{
+    return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0));
+}
+__device__ inline float bload1(__amdgpu_buffer_rsrc_t rs, unsigned off)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (int)off, 0, 0));
+}
+__device__ inline f4 mfma(float a, float b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Direction of a wave item: the base offsets are non-decreasing, a direction
+// with no items this step has base[d] == base[d + 1].
+__device__ inline int item_dir(const int *base, int item)
+{
+    int d = 0;
+#pragma unroll
+    for (int k = 1; k < kDirs; ++k) d += item >= base[k] ? 1 : 0;
+    return d;
+}
+
+// ---- conversion and repacking (once per call) -------------------------------
+
+// x [N][V][C] (fp32 or bf16) -> xp [N][V][C'] fp32, channels >= C zero.
+template <typename TS>
+__global__ void __launch_bounds__(256)
+k_pad_x(long long nvox, int C, int Cp, const TS *__restrict__ x, float *__restrict__ xp)
+{
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= nvox * Cp) return;
+    const long long v = i / Cp;
+    const int c = (int)(i - v * Cp);
+    xp[i] = c < C ? Store<TS>::load(x, v * C + c) : 0.0f;
+}
+
+// Forward A fragments frag[d][ug][kg][gate][lane][4]: K-group kg < KX is
+// input tap kg / (C'/16), channel block kg % (C'/16); the rest are h taps
+// (kg - KX) / U, channel block (kg - KX) % U.  Entry i of lane (q, col) is
+// the weight of gate-unit gate*O + 16 ug + col for channel 16 cb + 4q + i.
+template <typename TS>
+__global__ void __launch_bounds__(256)
+k_pack_fwd(int O, int C, int Cp, int KX, int KG, const TS *__restrict__ wx,
+           const TS *__restrict__ wh, const TS *__restrict__ b, float *__restrict__ frag,
+           float *__restrict__ bias)
+{
+    const int U = O / 16, G = 4 * O, CX = Cp / 16;
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i < (long long)kDirs * G) bias[i] = Store<TS>::load(b, i);
+    if (i >= (long long)kDirs * U * KG * 1024) return;
+    const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63), gate = (int)((i >> 8) & 3);
+    long long r = i >> 10;
+    const int kg = (int)(r % KG);
+    r /= KG;
+    const int ug = (int)(r % U), d = (int)(r / U);
+    const int q = lane >> 4, col = lane & 15;
+    const long long gu = (long long)d * G + gate * O + ug * 16 + col;
+    float v = 0.0f;
+    if (kg < KX) {
+        const int tap = kg / CX, c = (kg % CX) * 16 + 4 * q + i4;
+        if (c < C) v = Store<TS>::load(wx, (gu * C + c) * 9 + tap);
+    } else {
+        const int kh = kg - KX, tap = kh / U, j = (kh % U) * 16 + 4 * q + i4;
+        v = Store<TS>::load(wh, (gu * O + j) * 9 + tap);
+    }
+    frag[i] = v;
+}
+
+// Backward A fragments fragB[d][ug][kg][lane][4], kg = tap * 4U + mb: entry
+// i of lane (q, col) is W_h[d][gate-unit 16 mb + 4q + i][unit 16 ug + col][tap].
+__global__ void __launch_bounds__(256)
+k_pack_bwd(int O, const float *__restrict__ wh, float *__restrict__ frag)
+{
+    const int U = O / 16, G = 4 * O, KG = 9 * 4 * U;
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (long long)kDirs * U * KG * 256) return;
+    const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63);
+    long long r = i >> 8;
+    const int kg = (int)(r % KG);
+    r /= KG;
+    const int ug = (int)(r % U), d = (int)(r / U);
+    const int tap = kg / (4 * U), mb = kg % (4 * U);
+    const int q = lane >> 4, col = lane & 15;
+    const long long gu = (long long)d * G + mb * 16 + 4 * q + i4;
+    frag[i] = wh[(gu * O + ug * 16 + col) * 9 + tap];
+}
+
+// dL/dx A fragments fragX[d][tap][mb][ct][lane][4]: entry i of lane (q, col)
+// is W_x[d][gate-unit 16 mb + 4q + i][channel 16 ct + col][tap] (0 past C).
+__global__ void __launch_bounds__(256)
+k_pack_dx(int O, int C, int CT, const float *__restrict__ wx, float *__restrict__ frag)
+{
+    const int G = 4 * O, MB = G / 16;
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (long long)kDirs * 9 * MB * CT * 256) return;
+    const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63);
+    long long r = i >> 8;
+    const int ct = (int)(r % CT);
+    r /= CT;
+    const int mb = (int)(r % MB);
+    r /= MB;
+    const int tap = (int)(r % 9), d = (int)(r / 9);
+    const int q = lane >> 4, col = lane & 15;
+    const int c = ct * 16 + col;
+    const long long gu = (long long)d * G + mb * 16 + 4 * q + i4;
+    frag[i] = c < C ? wx[(gu * C + c) * 9 + tap] : 0.0f;
+}
+
+// ---- forward step -----------------------------------------------------------
+
+struct FwdStepArgs {
+    Geom g;
+    int t;
+    int Cp, KX, KG;           // padded channels, input K-groups (9 C'/16), all K-groups
+    const float *xp;          // [N][V][C']
+    const float *frag;        // [6][U][KG][4][64][4]
+    const float *bias;        // [6][4O]
+    float *hd, *cell;         // [6][N][V][O]
+    float *gates;             // [6][N][V][4O] or null
+    int npg[kDirs];           // pixel groups (kNT tiles) of a plane
+    int base[kDirs + 1];      // first wave item of each direction in this launch
+};
+
+// One wave: the four gates of unit group ug for kNT 16-pixel tiles of one
+// plane.  Items of a (direction, batch element) are ordered unit group
+// major, so the waves of a workgroup share their A fragments.
+template <int U>
+__global__ void __launch_bounds__(64 * kSW)
+k_step_fwd(FwdStepArgs a)
+{
+    constexpr int O = 16 * U, G = 4 * O;
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (item >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, item);
+    const DirGeom dg = a.g.dir[d];
+    const int npg = a.npg[d];
+    int r = item - a.base[d];
+    const int n = r / (U * npg);
+    r -= n * U * npg;
+    const int ug = r / npg, pg = r - ug * npg;
+    const int t = a.t;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const int Cp = a.Cp, CX = Cp >> 4, KX = a.KX;
+    const int hoff = -dg.sign * ss;   // voxel of plane t - 1 = voxel of plane t + hoff
+    const int uo = ug * 16 + 4 * q4;
+
+    // this lane's pixel of each tile; bit tap of nbm: the tap's pixel is on
+    // the plane (bit 4: the pixel itself exists)
+    int vox[kNT];
+    unsigned nbm[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const int pix = (pg * kNT + nt) * 16 + col;
+        const bool live = pix < P * Q;
+        const int p = live ? pix / Q : 0, qq = live ? pix - p * Q : 0;
+        vox[nt] = s * ss + p * sp + qq * sq;
+        unsigned m = 0;
+#pragma unroll
+        for (int ka = 0; ka < 3; ++ka)
+#pragma unroll
+            for (int kb = 0; kb < 3; ++kb)
+                m |= (unsigned)(live & ((unsigned)(p + ka - 1) < (unsigned)P) &
+                                ((unsigned)(qq + kb - 1) < (unsigned)Q))
+                     << (ka * 3 + kb);
+        nbm[nt] = m;
+    }
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    const auto rs_x = slice_rsrc(a.xp + (long long)n * V * Cp, V * Cp);
+    const auto rs_h = slice_rsrc(a.hd + sbase * O, V * O);
+    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+    const float *fr = a.frag + (long long)(d * U + ug) * a.KG * 1024 + lane * 4;
+
+    // c_{t-1} of the epilogue, in flight during the contraction
+    f4 cprev[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt)
+        cprev[nt] = bload4(rs_c, (t > 0 && ((nbm[nt] >> 4) & 1))
+                                     ? (unsigned)((vox[nt] + hoff) * O + uo) * 4u
+                                     : (unsigned)kOOB);
+
+    f4 acc[4][kNT];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const f4 bv = *(const f4 *)(a.bias + d * G + g * O + uo);
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = bv;
+    }
+
+    struct Ops {
+        f4 a[4];
+        f4 b[kNT];
+    };
+    auto ld_a = [&](int kg, Ops &o) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) o.a[g] = *(const f4 *)(fr + kg * 1024 + g * 256);
+    };
+    auto ld_x = [&](int tap, int cb, Ops &o) {
+        const int dv = (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt)
+            o.b[nt] = bload4(rs_x, ((nbm[nt] >> tap) & 1)
+                                       ? (unsigned)((vox[nt] + dv) * Cp + cb * 16 + 4 * q4) * 4u
+                                       : (unsigned)kOOB);
+    };
+    auto ld_h = [&](int tap, int cb, Ops &o) {
+        const int dv = hoff + (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt)
+            o.b[nt] = bload4(rs_h, ((nbm[nt] >> tap) & 1)
+                                       ? (unsigned)((vox[nt] + dv) * O + cb * 16 + 4 * q4) * 4u
+                                       : (unsigned)kOOB);
+    };
+    auto mma = [&](const Ops &o) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = mfma(o.a[g][i], o.b[nt][i], acc[g][nt]);
+    };
+
+    // input part, then (t > 0) the recurrent part; the next K-group's
+    // operands are loaded while the current one's MFMAs run
+    Ops cur, nxt;
+    ld_a(0, cur);
+    ld_x(0, 0, cur);
+    {
+        int tap = 0, cb = 0;
+        for (int kg = 0; kg < KX; ++kg) {
+            int ntap = tap, ncb = cb + 1;
+            if (ncb == CX) {
+                ncb = 0;
+                ++ntap;
+            }
+            if (kg + 1 < KX) {
+                ld_a(kg + 1, nxt);
+                ld_x(ntap, ncb, nxt);
+            } else if (t > 0) {
+                ld_a(KX, nxt);
+                ld_h(0, 0, nxt);
+            }
+            mma(cur);
+            cur = nxt;
+            tap = ntap;
+            cb = ncb;
+        }
+    }
+    if (t > 0) {
+        int tap = 0, cb = 0;
+        for (int kh = 0; kh < 9 * U; ++kh) {
+            int ntap = tap, ncb = cb + 1;
+            if (ncb == U) {
+                ncb = 0;
+                ++ntap;
+            }
+            if (kh + 1 < 9 * U) {
+                ld_a(KX + kh + 1, nxt);
+                ld_h(ntap, ncb, nxt);
+            }
+            mma(cur);
+            cur = nxt;
+            tap = ntap;
+            cb = ncb;
+        }
+    }
+
+    // Eq. (7)-(12): gates, cell and hidden state of units uo .. uo+3
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        if (!((nbm[nt] >> 4) & 1)) continue;
+        const long long vo = sbase + vox[nt];
+        f4 gi, gf, gg, go, c, h;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            gi[i] = fsig(acc[0][nt][i]);
+            gf[i] = fsig(acc[1][nt][i]);
+            gg[i] = ftanh(acc[2][nt][i]);
+            go[i] = fsig(acc[3][nt][i]);
+            c[i] = gg[i] * gi[i] + cprev[nt][i] * gf[i];
+            h[i] = go[i] * ftanh(c[i]);
+        }
+        *(f4 *)(a.cell + vo * O + uo) = c;
+        *(f4 *)(a.hd + vo * O + uo) = h;
+        if (a.gates) {
+            float *gp = a.gates + vo * G + uo;
+            *(f4 *)gp = gi;
+            *(f4 *)(gp + O) = gf;
+            *(f4 *)(gp + 2 * O) = gg;
+            *(f4 *)(gp + 3 * O) = go;
+        }
+    }
+}
+
+// ---- backward step ----------------------------------------------------------
+
+struct BwdStepArgs {
+    Geom g;
+    int t;
+    const float *frag;        // [6][U][9 * 4U][64][4]
+    const float *gates, *cell, *dh;
+    float *dA;                // [6][N][V][4O]
+    float *gcf;               // [6][N][V][O]: dL/dc_t * f_t
+    int npg[kDirs];
+    int base[kDirs + 1];
+};
+
+// One wave: every unit group of kNT 16-pixel tiles of one plane.
+//   gh = dL/dh + sum_taps W_h^T dA_{t+1}[p - tap]            (MFMA)
+//   gc = gh o (1 - tanh^2 c) + (gc f)_{t+1}
+//   dA_i = gc g i (1 - i), dA_f = gc c_{t-1} f (1 - f), dA_g = gc i (1 - g^2),
+//   dA_o = gh tanh(c) o (1 - o)
+template <int U>
+__global__ void __launch_bounds__(64 * kSW)
+k_step_bwd(BwdStepArgs a)
+{
+    constexpr int O = 16 * U, G = 4 * O, MB = 4 * U, KG = 9 * MB;
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (item >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, item);
+    const DirGeom dg = a.g.dir[d];
+    const int npg = a.npg[d];
+    const int r = item - a.base[d];
+    const int n = r / npg, pg = r - n * npg;
+    const int t = a.t;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const bool has_next = t + 1 < dg.T;
+    const int noff = dg.sign * ss;    // voxel of plane t + 1 = voxel of plane t + noff
+
+    // bit tap of nbm: the pixel that received this pixel's h through tap
+    // (p - (ka - 1), q - (kb - 1)) is on the plane
+    int vox[kNT];
+    unsigned nbm[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const int pix = (pg * kNT + nt) * 16 + col;
+        const bool live = pix < P * Q;
+        const int p = live ? pix / Q : 0, qq = live ? pix - p * Q : 0;
+        vox[nt] = s * ss + p * sp + qq * sq;
+        unsigned m = 0;
+#pragma unroll
+        for (int ka = 0; ka < 3; ++ka)
+#pragma unroll
+            for (int kb = 0; kb < 3; ++kb)
+                m |= (unsigned)(live & ((unsigned)(p - ka + 1) < (unsigned)P) &
+                                ((unsigned)(qq - kb + 1) < (unsigned)Q))
+                     << (ka * 3 + kb);
+        nbm[nt] = m;
+    }
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    const auto rs_dA = slice_rsrc(a.dA + sbase * G, V * G);
+    const auto rs_dh = slice_rsrc(a.dh + (long long)n * V * O, V * O);
+    const float *fr = a.frag + (long long)d * U * KG * 256 + lane * 4;
+
+    f4 acc[U][kNT];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt)
+            acc[u][nt] = bload4(rs_dh, ((nbm[nt] >> 4) & 1)
+                                           ? (unsigned)(vox[nt] * O + u * 16 + 4 * q4) * 4u
+                                           : (unsigned)kOOB);
+
+    if (has_next) {
+        struct Ops {
+            f4 a[U];
+            f4 b[kNT];
+        };
+        auto load = [&](int tap, int mb, Ops &o) {
+            const int kg = tap * MB + mb;
+#pragma unroll
+            for (int u = 0; u < U; ++u) o.a[u] = *(const f4 *)(fr + ((long long)u * KG + kg) * 256);
+            const int dv = noff - (tap / 3 - 1) * sp - (tap % 3 - 1) * sq;
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt)
+                o.b[nt] = bload4(rs_dA, ((nbm[nt] >> tap) & 1)
+                                            ? (unsigned)((vox[nt] + dv) * G + mb * 16 + 4 * q4) * 4u
+                                            : (unsigned)kOOB);
+        };
+        Ops cur, nxt;
+        load(0, 0, cur);
+        int tap = 0, mb = 0;
+        for (int kg = 0; kg < KG; ++kg) {
+            int ntap = tap, nmb = mb + 1;
+            if (nmb == MB) {
+                nmb = 0;
+                ++ntap;
+            }
+            if (kg + 1 < KG) load(ntap, nmb, nxt);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int nt = 0; nt < kNT; ++nt)
+                        acc[u][nt] = mfma(cur.a[u][i], cur.b[nt][i], acc[u][nt]);
+            cur = nxt;
+            tap = ntap;
+            mb = nmb;
+        }
+    }
+
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        if (!((nbm[nt] >> 4) & 1)) continue;
+        const long long vo = sbase + vox[nt];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int uo = u * 16 + 4 * q4;
+            const float *gp = a.gates + vo * G + uo;
+            const f4 gi = *(const f4 *)gp, gf = *(const f4 *)(gp + O);
+            const f4 gg = *(const f4 *)(gp + 2 * O), go = *(const f4 *)(gp + 3 * O);
+            const f4 c = *(const f4 *)(a.cell + vo * O + uo);
+            f4 cp = {0.0f, 0.0f, 0.0f, 0.0f}, gn = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (t > 0) cp = *(const f4 *)(a.cell + (vo - noff) * O + uo);
+            if (has_next) gn = *(const f4 *)(a.gcf + (vo + noff) * O + uo);
+            f4 di, df, dgv, dov, gco;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float gh = acc[u][nt][i];
+                const float tc = ftanh(c[i]);
+                const float gc = gh * go[i] * (1.0f - tc * tc) + gn[i];
+                di[i] = gc * gg[i] * gi[i] * (1.0f - gi[i]);
+                df[i] = gc * cp[i] * gf[i] * (1.0f - gf[i]);
+                dgv[i] = gc * gi[i] * (1.0f - gg[i] * gg[i]);
+                dov[i] = gh * tc * go[i] * (1.0f - go[i]);
+                gco[i] = gc * gf[i];
+            }
+            float *dp = a.dA + vo * G + uo;
+            *(f4 *)dp = di;
+            *(f4 *)(dp + O) = df;
+            *(f4 *)(dp + 2 * O) = dgv;
+            *(f4 *)(dp + 3 * O) = dov;
+            *(f4 *)(a.gcf + vo * O + uo) = gco;
+        }
+    }
+}
+
+// ---- parameter gradients ----------------------------------------------------
+// dW[d][m][k] = sum over the voxels of direction d of dA[v][m] col[v][k],
+// col = [im2col(h_{t-1}) (9 O) | im2col(x_t) (9 C') | 1]; K of the MFMA runs
+// over voxels.  A wave owns 4 M-tiles x kWgN N-tiles of one direction and
+// a chunk of its voxels, visited as units of 16 pixels of a row (lane group
+// q takes pixels 4q .. 4q+3, one per k-step), walking each column group
+// down the rows so that the rows read for one unit are re-read from cache
+// by the next two.  The partial sums of the chunks are added in order.
+constexpr int kWgN = 8;
+constexpr int kWgTarget = 170;   // waves per direction (about one per SIMD in all)
+
+struct WgStepArgs {
+    Geom g;
+    int Cp;
+    int NTt;                  // N-tiles: 9U + 9C'/16 + 1
+    int nblk;                 // N-blocks of kWgN tiles
+    int kch;                  // voxel chunks per (direction, M-block, N-block)
+    const float *xp, *hd, *dA;
+    float *partial;           // [6][kch][4O][16 NTt]
+};
+
+template <int U>
+__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(1)))
+k_wgrad_step(WgStepArgs a)
+{
+    constexpr int O = 16 * U, G = 4 * O;
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int per_dir = U * a.nblk * a.kch;
+    if (item >= kDirs * per_dir) return;
+    const int d = item / per_dir;
+    int r = item - d * per_dir;
+    const int kc = r % a.kch;
+    r /= a.kch;
+    const int nb = r % a.nblk, mblk = r / a.nblk;
+    const DirGeom dg = a.g.dir[d];
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const int Cp = a.Cp, CX = Cp >> 4;
+    const int ngrp = (Q + 15) >> 4;
+
+    // the block's N-tiles: kind 0 h_{t-1}, 1 x_t, 2 the ones of the bias,
+    // 3 past the end; tap offsets and channel of this lane
+    int kind[kWgN], dka[kWgN], dkb[kWgN], chn[kWgN];
+#pragma unroll
+    for (int j = 0; j < kWgN; ++j) {
+        const int nt = nb * kWgN + j;
+        int k = 3, tap = 4, cb = 0;
+        if (nt < 9 * U) {
+            k = 0; tap = nt / U; cb = nt % U;
+        } else if (nt < 9 * U + 9 * CX) {
+            k = 1; tap = (nt - 9 * U) / CX; cb = (nt - 9 * U) % CX;
+        } else if (nt == 9 * U + 9 * CX) {
+            k = 2;
+        }
+        kind[j] = __builtin_amdgcn_readfirstlane(k);
+        dka[j] = __builtin_amdgcn_readfirstlane(tap / 3 - 1);
+        dkb[j] = __builtin_amdgcn_readfirstlane(tap % 3 - 1);
+        chn[j] = cb * 16 + col;
+    }
+
+    f4 acc[4][kWgN];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int j = 0; j < kWgN; ++j) acc[m][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    struct Ops {
+        float a[4][4];            // [k-step][M-tile]
+        float b[4][kWgN];         // [k-step][N-tile]
+    };
+    struct Cursor {
+        int n, t, qg, p;
+    };
+    const long long units = (long long)a.g.N * dg.T * ngrp * P;
+    const long long u0 = units * kc / a.kch, u1 = units * (kc + 1) / a.kch;
+    Cursor cu;
+    {
+        long long rest = u0;
+        cu.p = (int)(rest % P);
+        rest /= P;
+        cu.qg = (int)(rest % ngrp);
+        rest /= ngrp;
+        cu.t = (int)(rest % dg.T);
+        cu.n = (int)(rest / dg.T);
+        if (cu.n >= a.g.N) cu.n = a.g.N - 1;
+    }
+    auto advance = [&]() {
+        if (++cu.p == P) {
+            cu.p = 0;
+            if (++cu.qg == ngrp) {
+                cu.qg = 0;
+                if (++cu.t == dg.T) {
+                    cu.t = 0;
+                    if (cu.n + 1 < a.g.N) ++cu.n;
+                }
+            }
+        }
+    };
+    auto load = [&](const Cursor &c, bool live_unit, Ops &o) {
+        const long long sb = ((long long)d * a.g.N + c.n) * V;
+        const auto rs_a = slice_rsrc(a.dA + sb * G, V * G);
+        const auto rs_h = slice_rsrc(a.hd + sb * O, V * O);
+        const auto rs_x = slice_rsrc(a.xp + (long long)c.n * V * Cp, V * Cp);
+        const int s = dg.sign > 0 ? c.t : dg.T - 1 - c.t;
+        const int sprev = s - dg.sign;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int qq = c.qg * 16 + 4 * q4 + ks;
+            const bool live = live_unit & (qq < Q);
+            const int v = s * ss + c.p * sp + qq * sq;
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                o.a[ks][m] = bload1(rs_a, live ? (unsigned)(v * G + mblk * 64 + m * 16 + col) * 4u
+                                               : (unsigned)kOOB);
+#pragma unroll
+            for (int j = 0; j < kWgN; ++j) {
+                const int pp = c.p + dka[j], qn = qq + dkb[j];
+                const bool inpl = live & ((unsigned)pp < (unsigned)P) & ((unsigned)qn < (unsigned)Q);
+                if (kind[j] == 0) {
+                    const bool ok = inpl & (c.t > 0);
+                    o.b[ks][j] = bload1(rs_h, ok ? (unsigned)((sprev * ss + pp * sp + qn * sq) * O +
+                                                              chn[j]) * 4u
+                                                 : (unsigned)kOOB);
+                } else if (kind[j] == 1) {
+                    o.b[ks][j] = bload1(rs_x, inpl ? (unsigned)((s * ss + pp * sp + qn * sq) * Cp +
+                                                                chn[j]) * 4u
+                                                   : (unsigned)kOOB);
+                } else {
+                    o.b[ks][j] = (kind[j] == 2 && live && col == 0) ? 1.0f : 0.0f;
+                }
+            }
+        }
+    };
+    const long long total = u1 - u0;
+    Ops cur, nxt;
+    load(cu, total > 0, cur);
+    for (long long it = 0; it < total; ++it) {
+        advance();
+        load(cu, it + 1 < total, nxt);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+#pragma unroll
+                for (int j = 0; j < kWgN; ++j)
+                    if (kind[j] < 3) acc[m][j] = mfma(cur.a[ks][m], cur.b[ks][j], acc[m][j]);
+        cur = nxt;
+    }
+    const int KCp = a.NTt * 16;
+    float *out = a.partial + ((long long)d * a.kch + kc) * G * KCp;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int j = 0; j < kWgN; ++j) {
+            const int nt = nb * kWgN + j;
+            if (nt >= a.NTt) continue;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                out[(long long)(mblk * 64 + m * 16 + 4 * q4 + i) * KCp + nt * 16 + col] = acc[m][j][i];
+        }
+}
+
+// dW = sum of the chunk partials in chunk order, scattered to the ABI layouts.
+__global__ void __launch_bounds__(256)
+k_wgrad_step_reduce(int O, int C, int Cp, int NTt, int kch, const float *__restrict__ partial,
+                    float *__restrict__ dwx, float *__restrict__ dwh, float *__restrict__ db)
+{
+    const int G = 4 * O, KC = 9 * (O + Cp) + 1, KCp = NTt * 16;
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (long long)kDirs * G * KC) return;
+    const int k = (int)(i % KC);
+    const int gu = (int)((i / KC) % G);
+    const int d = (int)(i / ((long long)KC * G));
+    if (k >= 9 * O && k < 9 * (O + Cp) && (k - 9 * O) % Cp >= C) return;   // padding channel
+    float acc = 0.0f;
+    for (int c = 0; c < kch; ++c) acc += partial[(((long long)d * kch + c) * G + gu) * KCp + k];
+    if (k < 9 * O) {
+        dwh[(((long long)d * G + gu) * O + k % O) * 9 + k / O] = acc;
+    } else if (k < 9 * (O + Cp)) {
+        const int kx = k - 9 * O;
+        dwx[(((long long)d * G + gu) * C + kx % Cp) * 9 + kx / Cp] = acc;
+    } else {
+        db[(long long)d * G + gu] = acc;
+    }
+}
+
+// ---- dL/dx --------------------------------------------------------------------
+// dx[v][c] = sum_d sum_taps sum_m dA^d[v - tap][m] W_x[d][m][c][tap]: M = 16
+// channels per tile (CT tiles), N = kNT 16-voxel tiles of consecutive voxels,
+// K = 6 directions x 9 taps x 4O gate-units.
+struct DxStepArgs {
+    Geom g;
+    int CT;
+    const float *frag;        // [6][9][4U][CT][64][4]
+    const float *dA;          // [6][N][V][4O]
+    float *dx;                // [N][V][C]
+    int nvg;                  // voxel groups (kNT tiles) per batch element
+};
+
+template <int U, int CT>
+__global__ void __launch_bounds__(64 * kSW)
+k_dx_step(DxStepArgs a)
+{
+    constexpr int O = 16 * U, G = 4 * O, MB = 4 * U, KG = 9 * MB;
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (item >= a.g.N * a.nvg) return;
+    const int n = item / a.nvg, vg = item - n * a.nvg;
+    const long long V = a.g.V;
+    const int H = a.g.H, W = a.g.W, C = a.g.C;
+    int vv[kNT], zc[kNT], yc[kNT], xc[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const long long v = (long long)(vg * kNT + nt) * 16 + col;
+        const bool live = v < V;
+        vv[nt] = live ? (int)v : -1;
+        const int vl = live ? (int)v : 0;
+        zc[nt] = vl / (H * W);
+        yc[nt] = (vl / W) % H;
+        xc[nt] = vl % W;
+    }
+    f4 acc[CT][kNT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[ct][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    struct Ops {
+        f4 a[CT];
+        f4 b[kNT];
+    };
+    for (int d = 0; d < kDirs; ++d) {
+        const DirGeom dg = a.g.dir[d];
+        const int sp = (int)dg.sp, sq = (int)dg.sq, P = dg.P, Q = dg.Q;
+        // in-plane coordinates of each voxel for this direction; bit tap:
+        // the pixel (p - (ka - 1), q - (kb - 1)) is on the plane
+        unsigned nbm[kNT];
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) {
+            const int p = d < 2 ? yc[nt] : zc[nt];
+            const int q = d < 4 ? xc[nt] : yc[nt];
+            unsigned m = 0;
+#pragma unroll
+            for (int ka = 0; ka < 3; ++ka)
+#pragma unroll
+                for (int kb = 0; kb < 3; ++kb)
+                    m |= (unsigned)((vv[nt] >= 0) & ((unsigned)(p - ka + 1) < (unsigned)P) &
+                                    ((unsigned)(q - kb + 1) < (unsigned)Q))
+                         << (ka * 3 + kb);
+            nbm[nt] = m;
+        }
+        const auto rs = slice_rsrc(a.dA + ((long long)d * a.g.N + n) * V * G, V * G);
+        const float *fr = a.frag + (long long)d * KG * CT * 256 + lane * 4;
+        auto load = [&](int tap, int mb, Ops &o) {
+            const int kg = tap * MB + mb;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) o.a[ct] = *(const f4 *)(fr + ((long long)kg * CT + ct) * 256);
+            const int dv = -(tap / 3 - 1) * sp - (tap % 3 - 1) * sq;
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt)
+                o.b[nt] = bload4(rs, ((nbm[nt] >> tap) & 1)
+                                         ? (unsigned)((vv[nt] + dv) * G + mb * 16 + 4 * q4) * 4u
+                                         : (unsigned)kOOB);
+        };
+        Ops cur, nxt;
+        load(0, 0, cur);
+        int tap = 0, mb = 0;
+        for (int kg = 0; kg < KG; ++kg) {
+            int ntap = tap, nmb = mb + 1;
+            if (nmb == MB) {
+                nmb = 0;
+                ++ntap;
+            }
+            if (kg + 1 < KG) load(ntap, nmb, nxt);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                    for (int nt = 0; nt < kNT; ++nt)
+                        acc[ct][nt] = mfma(cur.a[ct][i], cur.b[nt][i], acc[ct][nt]);
+            cur = nxt;
+            tap = ntap;
+            mb = nmb;
+        }
+    }
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        if (vv[nt] < 0) continue;
+        float *out = a.dx + ((long long)n * V + vv[nt]) * C;
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+            const int c0 = ct * 16 + 4 * q4;
+            if ((C & 3) == 0 && c0 + 3 < C) {
+                *(f4 *)(out + c0) = acc[ct][nt];
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (c0 + i < C) out[c0 + i] = acc[ct][nt][i];
+            }
+        }
+    }
+}
+
+// ---- host side --------------------------------------------------------------
+
+inline int pad16(int c) { return (c + 15) / 16 * 16; }
+inline unsigned blocks_for(long long n, int per) { return (unsigned)((n + per - 1) / per); }
+
+inline int npg_of(const DirGeom &dg) { return (dg.P * dg.Q + 16 * kNT - 1) / (16 * kNT); }
+inline int max_T(const Geom &g)
+{
+    int m = 0;
+    for (int d = 0; d < kDirs; ++d) m = g.dir[d].T > m ? g.dir[d].T : m;
+    return m;
+}
+
+struct WgShape {
+    int NTt, nblk, kch;
+};
+inline WgShape wg_shape(const Geom &g)
+{
+    const int U = g.O / 16, CX = pad16(g.C) / 16;
+    WgShape w;
+    w.NTt = 9 * U + 9 * CX + 1;
+    w.nblk = (w.NTt + kWgN - 1) / kWgN;
+    const int per = U * w.nblk;
+    w.kch = kWgTarget / per > 1 ? kWgTarget / per : 1;
+    return w;
+}
+
+template <int U>
+int launch_fwd_steps(const Geom &g, FwdStepArgs &a, hipStream_t st)
+{
+    const int T = max_T(g);
+    for (int t = 0; t < T; ++t) {
+        a.t = t;
+        int tot = 0;
+        for (int d = 0; d < kDirs; ++d) {
+            a.base[d] = tot;
+            if (t < g.dir[d].T) tot += g.N * U * a.npg[d];
+        }
+        a.base[kDirs] = tot;
+        k_step_fwd<U><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
+        PLSTM_LAUNCH_CHECK();
+    }
+    return PLSTM_OK;
+}
+
+template <int U>
+int launch_bwd_steps(const Geom &g, BwdStepArgs &a, hipStream_t st)
+{
+    for (int t = max_T(g) - 1; t >= 0; --t) {
+        a.t = t;
+        int tot = 0;
+        for (int d = 0; d < kDirs; ++d) {
+            a.base[d] = tot;
+            if (t < g.dir[d].T) tot += g.N * a.npg[d];
+        }
+        a.base[kDirs] = tot;
+        k_step_bwd<U><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
+        PLSTM_LAUNCH_CHECK();
+    }
+    return PLSTM_OK;
+}
+
+template <int U, int CT>
+int launch_dx(const DxStepArgs &a, hipStream_t st)
+{
+    k_dx_step<U, CT><<<blocks_for((long long)a.g.N * a.nvg, kSW), 64 * kSW, 0, st>>>(a);
+    PLSTM_LAUNCH_CHECK();
+    return PLSTM_OK;
+}
+
+template <int U>
+int launch_dx_ct(const DxStepArgs &a, hipStream_t st)
+{
+    switch (a.CT) {
+    case 1: return launch_dx<U, 1>(a, st);
+    case 2: return launch_dx<U, 2>(a, st);
+    case 3: return launch_dx<U, 3>(a, st);
+    case 4: return launch_dx<U, 4>(a, st);
+    default: return PLSTM_EUNSUPPORTED;
+    }
+}
+
+}  // namespace
+
+bool step_supported(const Geom &g)
+{
+    if (g.O != 16 && g.O != 32 && g.O != 64) return false;
+    const long long Cp = pad16(g.C);
+    if (Cp > 64) return false;
+    // slices addressed through buffer resources: byte sizes fit 31 bits
+    const long long lim = 1LL << 31;
+    if (g.V * 4 * g.O * 4 >= lim || g.V * Cp * 4 >= lim) return false;
+    // wave items of a step fit an int
+    long long items = 0;
+    for (int d = 0; d < kDirs; ++d) items += (long long)g.N * (g.O / 16) * npg_of(g.dir[d]);
+    return items < (1LL << 30);
+}
+
+size_t step_fwd_ws(const Geom &g)
+{
+    const int U = g.O / 16, Cp = pad16(g.C), KG = 9 * (Cp + g.O) / 16;
+    Carve cv(nullptr);
+    cv.take<float>((size_t)g.N * g.V * Cp);          // padded x
+    cv.take<float>((size_t)kDirs * U * KG * 1024);   // A fragments
+    cv.take<float>((size_t)kDirs * 4 * g.O);         // bias
+    return cv.off;
+}
+
+int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
+             const void *b, float *hd, float *cell, float *gates, void *ws, hipStream_t st)
+{
+    if (!step_supported(g)) return PLSTM_EUNSUPPORTED;
+    const int U = g.O / 16, Cp = pad16(g.C);
+    const int KX = 9 * Cp / 16, KG = KX + 9 * U;
+    Carve cv(ws);
+    float *xp = cv.take<float>((size_t)g.N * g.V * Cp);
+    float *frag = cv.take<float>((size_t)kDirs * U * KG * 1024);
+    float *bias = cv.take<float>((size_t)kDirs * 4 * g.O);
+    const long long nvox = (long long)g.N * g.V;
+    const long long nfrag = (long long)kDirs * U * KG * 1024;
+
+    timing_begin("sweep_fwd_step", st);
+    if (dtype == PLSTM_BF16) {
+        k_pad_x<uint16_t><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
+                                                                      (const uint16_t *)x, xp);
+        PLSTM_LAUNCH_CHECK();
+        k_pack_fwd<uint16_t><<<blocks_for(nfrag, 256), 256, 0, st>>>(
+            g.O, g.C, Cp, KX, KG, (const uint16_t *)wx, (const uint16_t *)wh,
+            (const uint16_t *)b, frag, bias);
+    } else {
+        k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
+                                                                   (const float *)x, xp);
+        PLSTM_LAUNCH_CHECK();
+        k_pack_fwd<float><<<blocks_for(nfrag, 256), 256, 0, st>>>(
+            g.O, g.C, Cp, KX, KG, (const float *)wx, (const float *)wh, (const float *)b, frag,
+            bias);
+    }
+    PLSTM_LAUNCH_CHECK();
+
+    FwdStepArgs a;
+    a.g = g;
+    a.Cp = Cp; a.KX = KX; a.KG = KG;
+    a.xp = xp; a.frag = frag; a.bias = bias;
+    a.hd = hd; a.cell = cell; a.gates = gates;
+    for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
+    int rc;
+    switch (U) {
+    case 1: rc = launch_fwd_steps<1>(g, a, st); break;
+    case 2: rc = launch_fwd_steps<2>(g, a, st); break;
+    default: rc = launch_fwd_steps<4>(g, a, st); break;
+    }
+    if (rc != PLSTM_OK) return rc;
+    timing_end(2 + max_T(g), st);
+    return PLSTM_OK;
+}
+
+size_t step_bwd_ws(const Geom &g)
+{
+    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O;
+    const WgShape w = wg_shape(g);
+    Carve cv(nullptr);
+    cv.take<float>((size_t)kDirs * g.N * g.V * G);                 // dA
+    cv.take<float>((size_t)kDirs * g.N * g.V * g.O);               // dL/dc * f
+    cv.take<float>((size_t)kDirs * U * 9 * 4 * U * 256);           // W_h^T fragments
+    cv.take<float>((size_t)g.N * g.V * Cp);                        // padded x
+    cv.take<float>((size_t)kDirs * w.kch * G * w.NTt * 16);        // weight-gradient partials
+    cv.take<float>((size_t)kDirs * 9 * 4 * U * (Cp / 16) * 256);   // W_x^T fragments
+    return cv.off;
+}
+
+// dL/dx from the gate gradients of all six directions (any O in 16, 32, 64;
+// C <= 64).
+int step_dx(const Geom &g, const float *wx, const float *dA, float *fragx, float *dx,
+            hipStream_t st)
+{
+    const int U = g.O / 16, CT = pad16(g.C) / 16;
+    const long long nf = (long long)kDirs * 9 * 4 * U * CT * 256;
+    timing_begin("dx_step", st);
+    k_pack_dx<<<blocks_for(nf, 256), 256, 0, st>>>(g.O, g.C, CT, wx, fragx);
+    PLSTM_LAUNCH_CHECK();
+    DxStepArgs a;
+    a.g = g;
+    a.CT = CT;
+    a.frag = fragx;
+    a.dA = dA;
+    a.dx = dx;
+    a.nvg = (int)((g.V + 16 * kNT - 1) / (16 * kNT));
+    int rc;
+    switch (U) {
+    case 1: rc = launch_dx_ct<1>(a, st); break;
+    case 2: rc = launch_dx_ct<2>(a, st); break;
+    default: rc = launch_dx_ct<4>(a, st); break;
+    }
+    if (rc != PLSTM_OK) return rc;
+    timing_end(2, st);
+    return PLSTM_OK;
+}
+
+size_t step_dx_ws(const Geom &g)
+{
+    Carve cv(nullptr);
+    cv.take<float>((size_t)kDirs * 9 * 4 * (g.O / 16) * (pad16(g.C) / 16) * 256);
+    return cv.off;
+}
+
+int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, const Saved &sv,
+             const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
+             hipStream_t st)
+{
+    if (!step_supported(g)) return PLSTM_EUNSUPPORTED;
+    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O;
+    const WgShape w = wg_shape(g);
+    Carve cv(ws);
+    float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * G);
+    float *gcf = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
+    float *frag = cv.take<float>((size_t)kDirs * U * 9 * 4 * U * 256);
+    float *xp = cv.take<float>((size_t)g.N * g.V * Cp);
+    float *partial = cv.take<float>((size_t)kDirs * w.kch * G * w.NTt * 16);
+    float *fragx = cv.take<float>((size_t)kDirs * 9 * 4 * U * (Cp / 16) * 256);
+    const long long nvox = (long long)g.N * g.V;
+
+    timing_begin("sweep_bwd_step", st);
+    k_pack_bwd<<<blocks_for((long long)kDirs * U * 36 * U * 256, 256), 256, 0, st>>>(g.O, wh, frag);
+    PLSTM_LAUNCH_CHECK();
+    BwdStepArgs a;
+    a.g = g;
+    a.frag = frag;
+    a.gates = sv.gates; a.cell = sv.cell; a.dh = dh;
+    a.dA = dA; a.gcf = gcf;
+    for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
+    int rc;
+    switch (U) {
+    case 1: rc = launch_bwd_steps<1>(g, a, st); break;
+    case 2: rc = launch_bwd_steps<2>(g, a, st); break;
+    default: rc = launch_bwd_steps<4>(g, a, st); break;
+    }
+    if (rc != PLSTM_OK) return rc;
+    timing_end(1 + max_T(g), st);
+
+    timing_begin("wgrad_step", st);
+    k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp, x, xp);
+    PLSTM_LAUNCH_CHECK();
+    WgStepArgs wa;
+    wa.g = g;
+    wa.Cp = Cp;
+    wa.NTt = w.NTt; wa.nblk = w.nblk; wa.kch = w.kch;
+    wa.xp = xp; wa.hd = sv.hd; wa.dA = dA;
+    wa.partial = partial;
+    const long long witems = (long long)kDirs * U * w.nblk * w.kch;
+    switch (U) {
+    case 1: k_wgrad_step<1><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
+    case 2: k_wgrad_step<2><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
+    default: k_wgrad_step<4><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
+    }
+    PLSTM_LAUNCH_CHECK();
+    const long long nout = (long long)kDirs * G * (9 * (g.O + Cp) + 1);
+    k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.O, g.C, Cp, w.NTt, w.kch,
+                                                               partial, dwx, dwh, db);
+    PLSTM_LAUNCH_CHECK();
+    timing_end(3, st);
+    if (dx) return step_dx(g, wx, dA, fragx, dx, st);
+    return PLSTM_OK;
+}
+
+}  // namespace plstm

@@ -146,6 +146,83 @@ def test_generic_path_backward_matches_oracle(shape, generic_backward):
         assert normwise(host(got), ref[name]) <= TOL["f32"], name
 
 
+@pytest.fixture
+def step_path():
+    """Run forward and backward on the plane-step MFMA path wherever it
+    supports the shape (O = 16 included, which otherwise takes the persistent
+    sweeps)."""
+    P.pyramid_lstm_set_forward_path(4)
+    P.pyramid_lstm_set_backward_path(3)
+    yield
+    P.pyramid_lstm_set_forward_path(0)
+    P.pyramid_lstm_set_backward_path(0)
+
+
+# every unit count of the plane-step kernels; channel counts below, at and
+# above one 16-channel block (zero-padded tails); planes smaller than one
+# 64-pixel group, ragged groups, batch > 1
+STEP_SHAPES = [(1, 5, 37, 29, 3, 16), (2, 4, 9, 7, 1, 16), (1, 6, 5, 4, 20, 16),
+               (1, 3, 3, 3, 1, 32), (2, 9, 17, 40, 32, 32), (1, 4, 6, 70, 3, 64),
+               (1, 2, 19, 3, 64, 64)]
+
+
+@pytest.mark.parametrize("shape", STEP_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_step_path_matches_oracle(shape, step_path):
+    inst = instance(shape, 4000 + sum(shape))
+    L = inst.layers[0]
+    dh = synth.upstream_grad(inst.x.shape[:-1] + (shape[-1],), 11 + sum(shape))
+    ref_h = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    ref = oracle.backward(inst.x, L.wx, L.wh, L.b, dh)
+    say("step path", shape)
+    x, Ld = dev(inst.x), layer_dev(L)
+    P.pyramid_lstm_timing_enable(True)
+    h_inf, _ = layer_forward(x, Ld)
+    h, saved = layer_forward(x, Ld, training=True)
+    dx, dwx, dwh, db = layer_backward(x, Ld, saved, dev(dh))
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    torch.cuda.synchronize()
+    assert "sweep_fwd_step" in phases and "sweep_bwd_step" in phases, phases
+    assert "sweep_fwd_mfma" not in phases and "sweep_fwd_generic" not in phases, phases
+    assert normwise(host(h_inf), ref_h) <= TOL["f32"]
+    assert torch.equal(h_inf, h)
+    for name, got in (("dx", dx), ("dwx", dwx), ("dwh", dwh), ("db", db)):
+        err = normwise(host(got), ref[name])
+        assert err <= TOL["f32"], (name, err)
+
+
+@pytest.mark.parametrize("shape", [(1, 5, 37, 29, 3, 16), (1, 4, 6, 70, 3, 64)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_step_path_saved_state_matches_oracle(shape, step_path):
+    """Gates, c^d and h^d that the plane-step forward saves for the backward."""
+    inst = instance(shape, 5000 + sum(shape))
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b, want_hd=True, want_saved=True)
+    say("step path saved", shape)
+    h, saved = layer_forward(dev(inst.x), layer_dev(L), training=True)
+    torch.cuda.synchronize()
+    assert normwise(host(h), ref["h"]) <= TOL["f32"]
+    for name in ("hd", "cell", "gates"):
+        got = saved_view(saved, name, shape)
+        assert normwise(got, ref[name]) <= TOL["f32"], name
+
+
+def test_large_hidden_layers_take_the_step_path():
+    """O = 32 and 64 run on the plane-step MFMA kernels by default."""
+    for shape in [(1, 4, 9, 10, 32, 32), (1, 3, 8, 7, 64, 64)]:
+        inst = instance(shape, 6000 + sum(shape))
+        say("step path default", shape)
+        x, Ld = dev(inst.x), layer_dev(inst.layers[0])
+        P.pyramid_lstm_timing_enable(True)
+        h, saved = layer_forward(x, Ld, training=True)
+        layer_backward(x, Ld, saved, torch.ones_like(h))
+        phases = P.pyramid_lstm_timing_read()
+        P.pyramid_lstm_timing_enable(False)
+        for k in ("sweep_fwd_step", "sweep_bwd_step", "wgrad_step", "dx_step"):
+            assert k in phases, (shape, phases)
+        assert "sweep_fwd_generic" not in phases and "sweep_bwd_generic" not in phases
+
+
 def test_mfma_backward_runs_for_o16():
     """The persistent MFMA reverse sweep and MFMA parameter gradients are the
     path taken for 16 hidden units."""

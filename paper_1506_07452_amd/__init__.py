@@ -246,10 +246,12 @@ def pyramid_lstm_timing_read(max_phases: int = 32):
 
 def pyramid_lstm_set_forward_path(path: int) -> None:
     """0 = automatic, 1 = generic path only, 2 = MFMA sweep where supported,
-    3 = MFMA sweep with every strip staged chunk by chunk."""
+    3 = MFMA sweep with every strip staged chunk by chunk, 4 = plane-step
+    MFMA path where supported."""
     _check("pyramid_lstm_set_forward_path", load().pyramid_lstm_set_forward_path(int(path)))
 
 
 def pyramid_lstm_set_backward_path(path: int) -> None:
-    """0 = automatic, 1 = generic path only, 2 = MFMA sweep where supported."""
+    """0 = automatic, 1 = generic path only, 2 = MFMA sweep where supported,
+    3 = plane-step MFMA path where supported."""
     _check("pyramid_lstm_set_backward_path", load().pyramid_lstm_set_backward_path(int(path)))

@@ -30,6 +30,11 @@ size_t step_bwd_ws(const Geom &g);
 int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, const Saved &sv,
              const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
              hipStream_t st);
+// dL/dx from the gate gradients dA [6][N][V][4O] on the MFMA (step_supported
+// shapes); `fragx` holds step_dx_ws bytes.
+size_t step_dx_ws(const Geom &g);
+int step_dx(const Geom &g, const float *wx, const float *dA, float *fragx, float *dx,
+            hipStream_t st);
 
 // h = sum of the six per-direction outputs (generic.hip).
 int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st);

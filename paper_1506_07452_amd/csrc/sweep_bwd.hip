@@ -591,6 +591,7 @@ size_t sweep_bwd_ws(const Geom &g)
     cv.take<float>((size_t)kDirs * g.N * g.V * kO);                     // dL/dc * f
     cv.take<int>(1024 + 1);                                              // flags + err
     cv.take<float>((size_t)kDirs * kWgTeamsPerDir * kG * wgrad_kcp(g.C));   // partials
+    if (step_supported(g)) cv.take<char>(step_dx_ws(g));                     // dL/dx fragments
     return cv.off;
 }
 
@@ -612,6 +613,7 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     float *gcf = cv.take<float>((size_t)kDirs * g.N * g.V * kO);
     int *flags = cv.take<int>(1024 + 1);
     float *partial = cv.take<float>((size_t)kDirs * kWgTeamsPerDir * kG * wgrad_kcp(g.C));
+    float *fragx = step_supported(g) ? (float *)cv.take<char>(step_dx_ws(g)) : nullptr;
 
     BwdArgs args;
     args.g = g;
@@ -657,7 +659,7 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
                                                        partial, dwx, dwh, db);
     PLSTM_LAUNCH_CHECK();
     timing_end(2, st);
-    if (dx) return generic_dx(g, wx, dA, dx, st);
+    if (dx) return fragx ? step_dx(g, wx, dA, fragx, dx, st) : generic_dx(g, wx, dA, dx, st);
     return PLSTM_OK;
 }
 

@@ -69,6 +69,15 @@ __device__ inline float bload1(__amdgpu_buffer_rsrc_t rs, unsigned off)
 {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (int)off, 0, 0));
 }
+// Byte offset of a masked load: `off` if `ok`, else past the buffer.  The
+// empty asm pins the select in a register, so the compiler cannot turn it
+// into a branch around the load.
+__device__ inline unsigned sel_off(bool ok, unsigned off)
+{
+    unsigned o = ok ? off : (unsigned)kOOB;
+    asm volatile("" : "+v"(o));
+    return o;
+}
 __device__ inline f4 mfma(float a, float b, f4 c)
 {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -242,9 +251,8 @@ k_step_fwd(FwdStepArgs a)
     f4 cprev[kNT];
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt)
-        cprev[nt] = bload4(rs_c, (t > 0 && ((nbm[nt] >> 4) & 1))
-                                     ? (unsigned)((vox[nt] + hoff) * O + uo) * 4u
-                                     : (unsigned)kOOB);
+        cprev[nt] = bload4(rs_c, sel_off(t > 0 && ((nbm[nt] >> 4) & 1),
+                                         (unsigned)((vox[nt] + hoff) * O + uo) * 4u));
 
     f4 acc[4][kNT];
 #pragma unroll
@@ -266,17 +274,15 @@ k_step_fwd(FwdStepArgs a)
         const int dv = (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
-            o.b[nt] = bload4(rs_x, ((nbm[nt] >> tap) & 1)
-                                       ? (unsigned)((vox[nt] + dv) * Cp + cb * 16 + 4 * q4) * 4u
-                                       : (unsigned)kOOB);
+            o.b[nt] = bload4(rs_x, sel_off((nbm[nt] >> tap) & 1,
+                                           (unsigned)((vox[nt] + dv) * Cp + cb * 16 + 4 * q4) * 4u));
     };
     auto ld_h = [&](int tap, int cb, Ops &o) {
         const int dv = hoff + (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
-            o.b[nt] = bload4(rs_h, ((nbm[nt] >> tap) & 1)
-                                       ? (unsigned)((vox[nt] + dv) * O + cb * 16 + 4 * q4) * 4u
-                                       : (unsigned)kOOB);
+            o.b[nt] = bload4(rs_h, sel_off((nbm[nt] >> tap) & 1,
+                                           (unsigned)((vox[nt] + dv) * O + cb * 16 + 4 * q4) * 4u));
     };
     auto mma = [&](const Ops &o) {
 #pragma unroll
@@ -428,9 +434,8 @@ k_step_bwd(BwdStepArgs a)
     for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
-            acc[u][nt] = bload4(rs_dh, ((nbm[nt] >> 4) & 1)
-                                           ? (unsigned)(vox[nt] * O + u * 16 + 4 * q4) * 4u
-                                           : (unsigned)kOOB);
+            acc[u][nt] = bload4(rs_dh, sel_off((nbm[nt] >> 4) & 1,
+                                               (unsigned)(vox[nt] * O + u * 16 + 4 * q4) * 4u));
 
     if (has_next) {
         struct Ops {
@@ -444,9 +449,8 @@ k_step_bwd(BwdStepArgs a)
             const int dv = noff - (tap / 3 - 1) * sp - (tap % 3 - 1) * sq;
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
-                o.b[nt] = bload4(rs_dA, ((nbm[nt] >> tap) & 1)
-                                            ? (unsigned)((vox[nt] + dv) * G + mb * 16 + 4 * q4) * 4u
-                                            : (unsigned)kOOB);
+                o.b[nt] = bload4(rs_dA, sel_off((nbm[nt] >> tap) & 1,
+                                                (unsigned)((vox[nt] + dv) * G + mb * 16 + 4 * q4) * 4u));
         };
         Ops cur, nxt;
         load(0, 0, cur);
@@ -510,19 +514,36 @@ k_step_bwd(BwdStepArgs a)
 // ---- parameter gradients ----------------------------------------------------
 // dW[d][m][k] = sum over the voxels of direction d of dA[v][m] col[v][k],
 // col = [im2col(h_{t-1}) (9 O) | im2col(x_t) (9 C') | 1]; K of the MFMA runs
-// over voxels.  A wave owns 4 M-tiles x kWgN N-tiles of one direction and
-// a chunk of its voxels, visited as units of 16 pixels of a row (lane group
-// q takes pixels 4q .. 4q+3, one per k-step), walking each column group
-// down the rows so that the rows read for one unit are re-read from cache
-// by the next two.  The partial sums of the chunks are added in order.
+// over voxels.  A wave owns 4 M-tiles x up to kWgN N-tiles of one direction,
+// all of the h part or all of the x part (+ the bias column), and a chunk
+// of the direction's voxels, visited as units of 16 pixels of a row (lane
+// group q takes pixels 4q .. 4q+3, one per k-step), walking each column
+// group down the rows so that the rows read for one unit are re-read from
+// cache by the next two.  The partial sums of the chunks are added in order.
 constexpr int kWgN = 8;
 constexpr int kWgTarget = 170;   // waves per direction (about one per SIMD in all)
+
+// N-tiles per block: the h part (9U tiles) and the x part with the bias
+// tile (9 C'/16 + 1 tiles) are each cut into blocks of at most kWgN.
+struct WgBlocks {
+    int nh, nx;       // blocks of each part
+    int th, tx;       // tiles per block of each part (last block may have fewer)
+};
+__host__ __device__ inline WgBlocks wg_blocks(int U, int CX)
+{
+    WgBlocks w;
+    const int h = 9 * U, x = 9 * CX + 1;
+    w.nh = (h + kWgN - 1) / kWgN;
+    w.nx = (x + kWgN - 1) / kWgN;
+    w.th = (h + w.nh - 1) / w.nh;
+    w.tx = (x + w.nx - 1) / w.nx;
+    return w;
+}
 
 struct WgStepArgs {
     Geom g;
     int Cp;
     int NTt;                  // N-tiles: 9U + 9C'/16 + 1
-    int nblk;                 // N-blocks of kWgN tiles
     int kch;                  // voxel chunks per (direction, M-block, N-block)
     const float *xp, *hd, *dA;
     float *partial;           // [6][kch][4O][16 NTt]
@@ -535,38 +556,51 @@ k_wgrad_step(WgStepArgs a)
     constexpr int O = 16 * U, G = 4 * O;
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
     const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int per_dir = U * a.nblk * a.kch;
+    const int Cp = a.Cp, CX = Cp >> 4;
+    const WgBlocks wb = wg_blocks(U, CX);
+    const int nblk = wb.nh + wb.nx;
+    const int per_dir = U * nblk * a.kch;
     if (item >= kDirs * per_dir) return;
     const int d = item / per_dir;
     int r = item - d * per_dir;
     const int kc = r % a.kch;
     r /= a.kch;
-    const int nb = r % a.nblk, mblk = r / a.nblk;
+    const int nb = r % nblk, mblk = r / nblk;
+    const bool is_h = nb < wb.nh;
+    // first N-tile and tile count of this block; tiles of the x part are
+    // numbered from 0 after the h part
+    const int t0 = is_h ? nb * wb.th : (nb - wb.nh) * wb.tx;
+    const int tend = is_h ? 9 * U : 9 * CX + 1;
+    const int ntl = (t0 + (is_h ? wb.th : wb.tx) < tend ? (is_h ? wb.th : wb.tx) : tend - t0);
+    const int first_nt = (is_h ? 0 : 9 * U) + t0;
     const DirGeom dg = a.g.dir[d];
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
     const int P = dg.P, Q = dg.Q;
     const long long V = a.g.V;
-    const int Cp = a.Cp, CX = Cp >> 4;
     const int ngrp = (Q + 15) >> 4;
+    const int cbn = is_h ? U : CX;              // channel blocks per tap
+    const int stride = is_h ? O : Cp;           // floats per voxel of the source
 
-    // the block's N-tiles: kind 0 h_{t-1}, 1 x_t, 2 the ones of the bias,
-    // 3 past the end; tap offsets and channel of this lane
-    int kind[kWgN], dka[kWgN], dkb[kWgN], chn[kWgN];
+    // per tile: tap offsets (uniform) and this lane's channel; the bias
+    // tile (last of the x part) is 1 in its first column and loads nothing
+    int dtap[kWgN], chn[kWgN];
+    float one[kWgN];
 #pragma unroll
     for (int j = 0; j < kWgN; ++j) {
-        const int nt = nb * kWgN + j;
-        int k = 3, tap = 4, cb = 0;
-        if (nt < 9 * U) {
-            k = 0; tap = nt / U; cb = nt % U;
-        } else if (nt < 9 * U + 9 * CX) {
-            k = 1; tap = (nt - 9 * U) / CX; cb = (nt - 9 * U) % CX;
-        } else if (nt == 9 * U + 9 * CX) {
-            k = 2;
-        }
-        kind[j] = __builtin_amdgcn_readfirstlane(k);
-        dka[j] = __builtin_amdgcn_readfirstlane(tap / 3 - 1);
-        dkb[j] = __builtin_amdgcn_readfirstlane(tap % 3 - 1);
-        chn[j] = cb * 16 + col;
+        const int tt = t0 + j;
+        const bool bias = !is_h && tt == 9 * CX;
+        const int tap = bias || j >= ntl ? 4 : tt / cbn;
+        dtap[j] = __builtin_amdgcn_readfirstlane((tap / 3 - 1) * sp + (tap % 3 - 1) * sq);
+        chn[j] = (bias || j >= ntl) ? -1 : (tt % cbn) * 16 + col;
+        one[j] = (bias && col == 0) ? 1.0f : 0.0f;
+        (void)tap;
+    }
+    unsigned tapok[kWgN];   // per tile: row and column offsets + 1, packed
+#pragma unroll
+    for (int j = 0; j < kWgN; ++j) {
+        const int tt = t0 + j;
+        const int tap = (!is_h && tt == 9 * CX) || j >= ntl ? 4 : tt / cbn;
+        tapok[j] = __builtin_amdgcn_readfirstlane((tap / 3) | (tap % 3) << 2);
     }
 
     f4 acc[4][kWgN];
@@ -607,13 +641,16 @@ k_wgrad_step(WgStepArgs a)
             }
         }
     };
+    // Branch-free loads: an operand outside the volume, of h_{-1} or of a
+    // zero tile gets an out-of-range offset.
     auto load = [&](const Cursor &c, bool live_unit, Ops &o) {
         const long long sb = ((long long)d * a.g.N + c.n) * V;
         const auto rs_a = slice_rsrc(a.dA + sb * G, V * G);
-        const auto rs_h = slice_rsrc(a.hd + sb * O, V * O);
-        const auto rs_x = slice_rsrc(a.xp + (long long)c.n * V * Cp, V * Cp);
+        const auto rs_b = is_h ? slice_rsrc(a.hd + sb * O, V * O)
+                               : slice_rsrc(a.xp + (long long)c.n * V * Cp, V * Cp);
         const int s = dg.sign > 0 ? c.t : dg.T - 1 - c.t;
-        const int sprev = s - dg.sign;
+        const int pl = is_h ? s - dg.sign : s;
+        const bool src_ok = live_unit & (!is_h | (c.t > 0));
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
             const int qq = c.qg * 16 + 4 * q4 + ks;
@@ -621,24 +658,16 @@ k_wgrad_step(WgStepArgs a)
             const int v = s * ss + c.p * sp + qq * sq;
 #pragma unroll
             for (int m = 0; m < 4; ++m)
-                o.a[ks][m] = bload1(rs_a, live ? (unsigned)(v * G + mblk * 64 + m * 16 + col) * 4u
-                                               : (unsigned)kOOB);
+                o.a[ks][m] =
+                    bload1(rs_a, sel_off(live, (unsigned)(v * G + mblk * 64 + m * 16 + col) * 4u));
+            const int vb = pl * ss + c.p * sp + qq * sq;
 #pragma unroll
             for (int j = 0; j < kWgN; ++j) {
-                const int pp = c.p + dka[j], qn = qq + dkb[j];
-                const bool inpl = live & ((unsigned)pp < (unsigned)P) & ((unsigned)qn < (unsigned)Q);
-                if (kind[j] == 0) {
-                    const bool ok = inpl & (c.t > 0);
-                    o.b[ks][j] = bload1(rs_h, ok ? (unsigned)((sprev * ss + pp * sp + qn * sq) * O +
-                                                              chn[j]) * 4u
-                                                 : (unsigned)kOOB);
-                } else if (kind[j] == 1) {
-                    o.b[ks][j] = bload1(rs_x, inpl ? (unsigned)((s * ss + pp * sp + qn * sq) * Cp +
-                                                                chn[j]) * 4u
-                                                   : (unsigned)kOOB);
-                } else {
-                    o.b[ks][j] = (kind[j] == 2 && live && col == 0) ? 1.0f : 0.0f;
-                }
+                const int pp = c.p + (int)(tapok[j] & 3) - 1, qn = qq + (int)(tapok[j] >> 2) - 1;
+                const bool ok = src_ok & (chn[j] >= 0) & ((unsigned)pp < (unsigned)P) &
+                                ((unsigned)qn < (unsigned)Q);
+                o.b[ks][j] =
+                    bload1(rs_b, sel_off(ok, (unsigned)((vb + dtap[j]) * stride + chn[j]) * 4u));
             }
         }
     };
@@ -654,7 +683,7 @@ k_wgrad_step(WgStepArgs a)
             for (int m = 0; m < 4; ++m)
 #pragma unroll
                 for (int j = 0; j < kWgN; ++j)
-                    if (kind[j] < 3) acc[m][j] = mfma(cur.a[ks][m], cur.b[ks][j], acc[m][j]);
+                    acc[m][j] = mfma(cur.a[ks][m], cur.b[ks][j] + one[j], acc[m][j]);
         cur = nxt;
     }
     const int KCp = a.NTt * 16;
@@ -663,11 +692,12 @@ k_wgrad_step(WgStepArgs a)
     for (int m = 0; m < 4; ++m)
 #pragma unroll
         for (int j = 0; j < kWgN; ++j) {
-            const int nt = nb * kWgN + j;
-            if (nt >= a.NTt) continue;
+            if (j >= ntl) continue;
+            const int nt = first_nt + j;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                out[(long long)(mblk * 64 + m * 16 + 4 * q4 + i) * KCp + nt * 16 + col] = acc[m][j][i];
+                out[(long long)(mblk * 64 + m * 16 + 4 * q4 + i) * KCp + nt * 16 + col] =
+                    acc[m][j][i];
         }
 }
 
@@ -769,9 +799,8 @@ k_dx_step(DxStepArgs a)
             const int dv = -(tap / 3 - 1) * sp - (tap % 3 - 1) * sq;
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
-                o.b[nt] = bload4(rs, ((nbm[nt] >> tap) & 1)
-                                         ? (unsigned)((vv[nt] + dv) * G + mb * 16 + 4 * q4) * 4u
-                                         : (unsigned)kOOB);
+                o.b[nt] = bload4(rs, sel_off((nbm[nt] >> tap) & 1,
+                                             (unsigned)((vv[nt] + dv) * G + mb * 16 + 4 * q4) * 4u));
         };
         Ops cur, nxt;
         load(0, 0, cur);
@@ -832,9 +861,10 @@ struct WgShape {
 inline WgShape wg_shape(const Geom &g)
 {
     const int U = g.O / 16, CX = pad16(g.C) / 16;
+    const WgBlocks wb = wg_blocks(U, CX);
     WgShape w;
     w.NTt = 9 * U + 9 * CX + 1;
-    w.nblk = (w.NTt + kWgN - 1) / kWgN;
+    w.nblk = wb.nh + wb.nx;
     const int per = U * w.nblk;
     w.kch = kWgTarget / per > 1 ? kWgTarget / per : 1;
     return w;
@@ -1058,7 +1088,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     WgStepArgs wa;
     wa.g = g;
     wa.Cp = Cp;
-    wa.NTt = w.NTt; wa.nblk = w.nblk; wa.kch = w.kch;
+    wa.NTt = w.NTt; wa.kch = w.kch;
     wa.xp = xp; wa.hd = sv.hd; wa.dA = dA;
     wa.partial = partial;
     const long long witems = (long long)kDirs * U * w.nblk * w.kch;

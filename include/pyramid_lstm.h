@@ -200,6 +200,15 @@ int pyramid_lstm_set_forward_path(int path);
  * other values. */
 int pyramid_lstm_set_backward_path(int path);
 
+/* Launch shape of the plane-step MFMA path, for testing and tuning
+ * (process-wide): 0 = automatic (default): a step whose tiles would give
+ * fewer than about two waves per SIMD splits each tile's K dimension over
+ * the four waves of a workgroup, other steps give each wave its own tiles;
+ * 1 = always split; 2 = never split.  Results are identical up to the
+ * summation order of the split partials.  Returns PLSTM_EINVAL for other
+ * values. */
+int pyramid_lstm_set_step_split(int mode);
+
 #ifdef __cplusplus
 }
 #endif

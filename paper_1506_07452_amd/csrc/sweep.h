@@ -59,5 +59,8 @@ int backward_dispatch(const Geom &g, const float *x, const float *wx, const floa
 // supported.
 extern int g_forward_path;
 extern int g_backward_path;
+// Plane-step launches: 0 = automatic, 1 = always split each tile's K over a
+// workgroup's waves, 2 = never.
+extern int g_step_split;
 
 }  // namespace plstm

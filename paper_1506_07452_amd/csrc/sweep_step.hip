@@ -36,6 +36,7 @@
 // (no recurrence) on the same MFMA: dW = sum_v dA (x) [im2col(h_{t-1}),
 // im2col(x_t), 1] with K = voxels, and dL/dx = sum_d sum_taps W_x^T dA.
 #include "common.h"
+#include "strip_plan.h"
 #include "sweep.h"
 #include "timing.h"
 
@@ -185,25 +186,38 @@ struct FwdStepArgs {
     Geom g;
     int t;
     int Cp, KX, KG;           // padded channels, input K-groups (9 C'/16), all K-groups
+    int cx_mul;               // ceil(2^16 / (C'/16)): division by C'/16
     const float *xp;          // [N][V][C']
     const float *frag;        // [6][U][KG][4][64][4]
     const float *bias;        // [6][4O]
     float *hd, *cell;         // [6][N][V][O]
     float *gates;             // [6][N][V][4O] or null
     int npg[kDirs];           // pixel groups (kNT tiles) of a plane
-    int base[kDirs + 1];      // first wave item of each direction in this launch
+    int base[kDirs + 1];      // first workgroup of each direction in this launch
 };
 
-// One wave: the four gates of unit group ug for kNT 16-pixel tiles of one
-// plane.  Items of a (direction, batch element) are ordered unit group
-// major, so the waves of a workgroup share their A fragments.
-template <int U>
+// The four gates of unit group ug for kNT 16-pixel tiles of one plane (an
+// item).  Two launch shapes:
+//   SPLIT   one item per workgroup; its waves split the K-groups (wave w
+//           takes w, w + 4, ...), the partial sums meet in LDS in wave order
+//           and wave w finishes tile w: four times as many waves per step,
+//           for steps with few pixels;
+//   !SPLIT  one item per wave; the four waves of a workgroup take
+//           neighbouring pixel groups of the same unit group, so they share
+//           every A fragment through the L1.
+// Items of a (direction, batch element) are ordered unit group major.
+template <int U, bool SPLIT>
 __global__ void __launch_bounds__(64 * kSW)
 k_step_fwd(FwdStepArgs a)
 {
     constexpr int O = 16 * U, G = 4 * O;
+    constexpr int KS = SPLIT ? kSW : 1;          // waves sharing one item's K
+    constexpr int NE = SPLIT ? 1 : kNT;          // tiles a wave finishes
+    static_assert(kNT == kSW, "wave w finishes tile w");
+    __shared__ f4 red[SPLIT ? kSW : 1][4][kNT][64];
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
-    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int item = SPLIT ? (int)blockIdx.x : (int)blockIdx.x * kSW + wave;
     if (item >= a.base[kDirs]) return;
     const int d = item_dir(a.base, item);
     const DirGeom dg = a.g.dir[d];
@@ -247,110 +261,105 @@ k_step_fwd(FwdStepArgs a)
     const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
     const float *fr = a.frag + (long long)(d * U + ug) * a.KG * 1024 + lane * 4;
 
-    // c_{t-1} of the epilogue, in flight during the contraction
-    f4 cprev[kNT];
+    // the tiles this wave finishes and their c_{t-1}, in flight during the
+    // contraction
+    int evox[NE];
+    unsigned ebits[NE];
+    f4 cprev[NE];
 #pragma unroll
-    for (int nt = 0; nt < kNT; ++nt)
-        cprev[nt] = bload4(rs_c, sel_off(t > 0 && ((nbm[nt] >> 4) & 1),
-                                         (unsigned)((vox[nt] + hoff) * O + uo) * 4u));
+    for (int e = 0; e < NE; ++e) {
+        evox[e] = vox[e];
+        ebits[e] = nbm[e];
+        if (SPLIT) {
+#pragma unroll
+            for (int nt = 1; nt < kNT; ++nt)
+                if (wave == nt) {
+                    evox[e] = vox[nt];
+                    ebits[e] = nbm[nt];
+                }
+        }
+        cprev[e] = bload4(rs_c, sel_off(t > 0 && ((ebits[e] >> 4) & 1),
+                                        (unsigned)((evox[e] + hoff) * O + uo) * 4u));
+    }
 
     f4 acc[4][kNT];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        const f4 bv = *(const f4 *)(a.bias + d * G + g * O + uo);
+    for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = bv;
-    }
+        for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
     struct Ops {
         f4 a[4];
         f4 b[kNT];
     };
-    auto ld_a = [&](int kg, Ops &o) {
+    // K-group kg: input tap / channel block for kg < KX, else h_{t-1}'s
+    auto load = [&](int kg, Ops &o) {
+        const bool is_x = kg < KX;
+        const int kk = is_x ? kg : kg - KX;
+        // kk / CX from a multiplier (exact for kk < 2^12, CX <= 4); U is a
+        // power of two
+        const int tap = is_x ? (kk * a.cx_mul) >> 16 : kk / U;
+        const int cb = kk - tap * (is_x ? CX : U);
+        const int stride = is_x ? Cp : O;
+        const int dv = (is_x ? 0 : hoff) + (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
+        const auto rs = is_x ? rs_x : rs_h;
 #pragma unroll
         for (int g = 0; g < 4; ++g) o.a[g] = *(const f4 *)(fr + kg * 1024 + g * 256);
-    };
-    auto ld_x = [&](int tap, int cb, Ops &o) {
-        const int dv = (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
-            o.b[nt] = bload4(rs_x, sel_off((nbm[nt] >> tap) & 1,
-                                           (unsigned)((vox[nt] + dv) * Cp + cb * 16 + 4 * q4) * 4u));
+            o.b[nt] = bload4(rs, sel_off((nbm[nt] >> tap) & 1,
+                                         (unsigned)((vox[nt] + dv) * stride + cb * 16 + 4 * q4) *
+                                             4u));
     };
-    auto ld_h = [&](int tap, int cb, Ops &o) {
-        const int dv = hoff + (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
-#pragma unroll
-        for (int nt = 0; nt < kNT; ++nt)
-            o.b[nt] = bload4(rs_h, sel_off((nbm[nt] >> tap) & 1,
-                                           (unsigned)((vox[nt] + dv) * O + cb * 16 + 4 * q4) * 4u));
-    };
-    auto mma = [&](const Ops &o) {
+    const int KG = t > 0 ? a.KG : KX;
+    const int k0 = SPLIT ? wave : 0;
+    // the next K-group's operands are loaded while the current one's MFMAs run
+    Ops cur, nxt;
+    if (k0 < KG) load(k0, cur);
+    for (int kg = k0; kg < KG; kg += KS) {
+        if (kg + KS < KG) load(kg + KS, nxt);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int g = 0; g < 4; ++g)
 #pragma unroll
-                for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = mfma(o.a[g][i], o.b[nt][i], acc[g][nt]);
-    };
-
-    // input part, then (t > 0) the recurrent part; the next K-group's
-    // operands are loaded while the current one's MFMAs run
-    Ops cur, nxt;
-    ld_a(0, cur);
-    ld_x(0, 0, cur);
-    {
-        int tap = 0, cb = 0;
-        for (int kg = 0; kg < KX; ++kg) {
-            int ntap = tap, ncb = cb + 1;
-            if (ncb == CX) {
-                ncb = 0;
-                ++ntap;
-            }
-            if (kg + 1 < KX) {
-                ld_a(kg + 1, nxt);
-                ld_x(ntap, ncb, nxt);
-            } else if (t > 0) {
-                ld_a(KX, nxt);
-                ld_h(0, 0, nxt);
-            }
-            mma(cur);
-            cur = nxt;
-            tap = ntap;
-            cb = ncb;
-        }
+                for (int nt = 0; nt < kNT; ++nt)
+                    acc[g][nt] = mfma(cur.a[g][i], cur.b[nt][i], acc[g][nt]);
+        cur = nxt;
     }
-    if (t > 0) {
-        int tap = 0, cb = 0;
-        for (int kh = 0; kh < 9 * U; ++kh) {
-            int ntap = tap, ncb = cb + 1;
-            if (ncb == U) {
-                ncb = 0;
-                ++ntap;
-            }
-            if (kh + 1 < 9 * U) {
-                ld_a(KX + kh + 1, nxt);
-                ld_h(ntap, ncb, nxt);
-            }
-            mma(cur);
-            cur = nxt;
-            tap = ntap;
-            cb = ncb;
-        }
+    if (SPLIT) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) red[SPLIT ? wave : 0][g][nt][lane] = acc[g][nt];
+        __syncthreads();
     }
 
     // Eq. (7)-(12): gates, cell and hidden state of units uo .. uo+3
+    // (split partials added in wave order, then the bias)
 #pragma unroll
-    for (int nt = 0; nt < kNT; ++nt) {
-        if (!((nbm[nt] >> 4) & 1)) continue;
-        const long long vo = sbase + vox[nt];
+    for (int e = 0; e < NE; ++e) {
+        if (!((ebits[e] >> 4) & 1)) continue;
+        f4 pre[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            f4 v = acc[g][e];
+            if (SPLIT) {
+                v = red[0][g][wave][lane];
+#pragma unroll
+                for (int w = 1; w < KS; ++w) v += red[SPLIT ? w : 0][g][wave][lane];
+            }
+            pre[g] = v + *(const f4 *)(a.bias + d * G + g * O + uo);
+        }
+        const long long vo = sbase + evox[e];
         f4 gi, gf, gg, go, c, h;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            gi[i] = fsig(acc[0][nt][i]);
-            gf[i] = fsig(acc[1][nt][i]);
-            gg[i] = ftanh(acc[2][nt][i]);
-            go[i] = fsig(acc[3][nt][i]);
-            c[i] = gg[i] * gi[i] + cprev[nt][i] * gf[i];
+            gi[i] = fsig(pre[0][i]);
+            gf[i] = fsig(pre[1][i]);
+            gg[i] = ftanh(pre[2][i]);
+            go[i] = fsig(pre[3][i]);
+            c[i] = gg[i] * gi[i] + cprev[e][i] * gf[i];
             h[i] = go[i] * ftanh(c[i]);
         }
         *(f4 *)(a.cell + vo * O + uo) = c;
@@ -378,18 +387,25 @@ struct BwdStepArgs {
     int base[kDirs + 1];
 };
 
-// One wave: every unit group of kNT 16-pixel tiles of one plane.
+// Every unit group of kNT 16-pixel tiles of one plane (an item); the two
+// launch shapes of the forward step (SPLIT: one item per workgroup, K split
+// over its waves, wave w finishes tile w; !SPLIT: one item per wave).
 //   gh = dL/dh + sum_taps W_h^T dA_{t+1}[p - tap]            (MFMA)
 //   gc = gh o (1 - tanh^2 c) + (gc f)_{t+1}
 //   dA_i = gc g i (1 - i), dA_f = gc c_{t-1} f (1 - f), dA_g = gc i (1 - g^2),
 //   dA_o = gh tanh(c) o (1 - o)
-template <int U>
+template <int U, bool SPLIT>
 __global__ void __launch_bounds__(64 * kSW)
 k_step_bwd(BwdStepArgs a)
 {
     constexpr int O = 16 * U, G = 4 * O, MB = 4 * U, KG = 9 * MB;
+    constexpr int KS = SPLIT ? kSW : 1;
+    constexpr int NE = SPLIT ? 1 : kNT;
+    static_assert(kNT == kSW, "wave w finishes tile w");
+    __shared__ f4 red[SPLIT ? kSW : 1][U][kNT][64];
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
-    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int item = SPLIT ? (int)blockIdx.x : (int)blockIdx.x * kSW + wave;
     if (item >= a.base[kDirs]) return;
     const int d = item_dir(a.base, item);
     const DirGeom dg = a.g.dir[d];
@@ -426,42 +442,35 @@ k_step_bwd(BwdStepArgs a)
     }
     const long long sbase = ((long long)d * a.g.N + n) * V;
     const auto rs_dA = slice_rsrc(a.dA + sbase * G, V * G);
-    const auto rs_dh = slice_rsrc(a.dh + (long long)n * V * O, V * O);
     const float *fr = a.frag + (long long)d * U * KG * 256 + lane * 4;
 
     f4 acc[U][kNT];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int nt = 0; nt < kNT; ++nt)
-            acc[u][nt] = bload4(rs_dh, sel_off((nbm[nt] >> 4) & 1,
-                                               (unsigned)(vox[nt] * O + u * 16 + 4 * q4) * 4u));
+        for (int nt = 0; nt < kNT; ++nt) acc[u][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
     if (has_next) {
         struct Ops {
             f4 a[U];
             f4 b[kNT];
         };
-        auto load = [&](int tap, int mb, Ops &o) {
-            const int kg = tap * MB + mb;
+        auto load = [&](int kg, Ops &o) {
+            const int tap = kg / MB, mb = kg - tap * MB;
 #pragma unroll
             for (int u = 0; u < U; ++u) o.a[u] = *(const f4 *)(fr + ((long long)u * KG + kg) * 256);
             const int dv = noff - (tap / 3 - 1) * sp - (tap % 3 - 1) * sq;
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
                 o.b[nt] = bload4(rs_dA, sel_off((nbm[nt] >> tap) & 1,
-                                                (unsigned)((vox[nt] + dv) * G + mb * 16 + 4 * q4) * 4u));
+                                                (unsigned)((vox[nt] + dv) * G + mb * 16 + 4 * q4) *
+                                                    4u));
         };
+        const int k0 = SPLIT ? wave : 0;
         Ops cur, nxt;
-        load(0, 0, cur);
-        int tap = 0, mb = 0;
-        for (int kg = 0; kg < KG; ++kg) {
-            int ntap = tap, nmb = mb + 1;
-            if (nmb == MB) {
-                nmb = 0;
-                ++ntap;
-            }
-            if (kg + 1 < KG) load(ntap, nmb, nxt);
+        load(k0, cur);
+        for (int kg = k0; kg < KG; kg += KS) {
+            if (kg + KS < KG) load(kg + KS, nxt);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -470,15 +479,31 @@ k_step_bwd(BwdStepArgs a)
                     for (int nt = 0; nt < kNT; ++nt)
                         acc[u][nt] = mfma(cur.a[u][i], cur.b[nt][i], acc[u][nt]);
             cur = nxt;
-            tap = ntap;
-            mb = nmb;
         }
+    }
+    if (SPLIT) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) red[SPLIT ? wave : 0][u][nt][lane] = acc[u][nt];
+        __syncthreads();
     }
 
 #pragma unroll
-    for (int nt = 0; nt < kNT; ++nt) {
-        if (!((nbm[nt] >> 4) & 1)) continue;
-        const long long vo = sbase + vox[nt];
+    for (int e = 0; e < NE; ++e) {
+        int evox = vox[e];
+        unsigned ebits = nbm[e];
+        if (SPLIT) {
+#pragma unroll
+            for (int nt = 1; nt < kNT; ++nt)
+                if (wave == nt) {
+                    evox = vox[nt];
+                    ebits = nbm[nt];
+                }
+        }
+        if (!((ebits >> 4) & 1)) continue;
+        const long long vo = sbase + evox;
+        const float *dhp = a.dh + ((long long)n * V + evox) * O;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int uo = u * 16 + 4 * q4;
@@ -489,10 +514,17 @@ k_step_bwd(BwdStepArgs a)
             f4 cp = {0.0f, 0.0f, 0.0f, 0.0f}, gn = {0.0f, 0.0f, 0.0f, 0.0f};
             if (t > 0) cp = *(const f4 *)(a.cell + (vo - noff) * O + uo);
             if (has_next) gn = *(const f4 *)(a.gcf + (vo + noff) * O + uo);
+            f4 ghv = acc[u][e];
+            if (SPLIT) {
+                ghv = red[0][u][wave][lane];
+#pragma unroll
+                for (int w = 1; w < KS; ++w) ghv += red[SPLIT ? w : 0][u][wave][lane];
+            }
+            ghv += *(const f4 *)(dhp + uo);
             f4 di, df, dgv, dov, gco;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float gh = acc[u][nt][i];
+                const float gh = ghv[i];
                 const float tc = ftanh(c[i]);
                 const float gc = gh * go[i] * (1.0f - tc * tc) + gn[i];
                 di[i] = gc * gg[i] * gi[i] * (1.0f - gi[i]);
@@ -870,10 +902,21 @@ inline WgShape wg_shape(const Geom &g)
     return w;
 }
 
+// Waves below which a step splits each tile's K over a workgroup's waves:
+// about two per SIMD (or always / never, when set for testing).
+inline int split_threshold()
+{
+    if (g_step_split == 1) return 1 << 30;
+    if (g_step_split == 2) return 0;
+    const DevInfo di = device_info();
+    return 8 * (di.cus > 0 ? di.cus : 256);
+}
+
 template <int U>
 int launch_fwd_steps(const Geom &g, FwdStepArgs &a, hipStream_t st)
 {
     const int T = max_T(g);
+    const int few = split_threshold();
     for (int t = 0; t < T; ++t) {
         a.t = t;
         int tot = 0;
@@ -882,7 +925,10 @@ int launch_fwd_steps(const Geom &g, FwdStepArgs &a, hipStream_t st)
             if (t < g.dir[d].T) tot += g.N * U * a.npg[d];
         }
         a.base[kDirs] = tot;
-        k_step_fwd<U><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
+        if (tot < few)
+            k_step_fwd<U, true><<<tot, 64 * kSW, 0, st>>>(a);
+        else
+            k_step_fwd<U, false><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
         PLSTM_LAUNCH_CHECK();
     }
     return PLSTM_OK;
@@ -891,6 +937,9 @@ int launch_fwd_steps(const Geom &g, FwdStepArgs &a, hipStream_t st)
 template <int U>
 int launch_bwd_steps(const Geom &g, BwdStepArgs &a, hipStream_t st)
 {
+    // an item of the reverse step holds every unit group: split up to four
+    // waves per SIMD
+    const int few = g_step_split == 0 ? 2 * split_threshold() : split_threshold();
     for (int t = max_T(g) - 1; t >= 0; --t) {
         a.t = t;
         int tot = 0;
@@ -899,7 +948,10 @@ int launch_bwd_steps(const Geom &g, BwdStepArgs &a, hipStream_t st)
             if (t < g.dir[d].T) tot += g.N * a.npg[d];
         }
         a.base[kDirs] = tot;
-        k_step_bwd<U><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
+        if (tot < few)
+            k_step_bwd<U, true><<<tot, 64 * kSW, 0, st>>>(a);
+        else
+            k_step_bwd<U, false><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
         PLSTM_LAUNCH_CHECK();
     }
     return PLSTM_OK;
@@ -926,6 +978,8 @@ int launch_dx_ct(const DxStepArgs &a, hipStream_t st)
 }
 
 }  // namespace
+
+int g_step_split = 0;
 
 bool step_supported(const Geom &g)
 {
@@ -985,6 +1039,7 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     FwdStepArgs a;
     a.g = g;
     a.Cp = Cp; a.KX = KX; a.KG = KG;
+    a.cx_mul = (65536 + Cp / 16 - 1) / (Cp / 16);
     a.xp = xp; a.frag = frag; a.bias = bias;
     a.hd = hd; a.cell = cell; a.gates = gates;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
@@ -1108,3 +1163,10 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
 }
 
 }  // namespace plstm
+
+extern "C" int pyramid_lstm_set_step_split(int mode)
+{
+    if (mode < 0 || mode > 2) return PLSTM_EINVAL;
+    plstm::g_step_split = mode;
+    return PLSTM_OK;
+}

@@ -166,8 +166,17 @@ STEP_SHAPES = [(1, 5, 37, 29, 3, 16), (2, 4, 9, 7, 1, 16), (1, 6, 5, 4, 20, 16),
                (1, 2, 19, 3, 64, 64)]
 
 
+@pytest.fixture(params=[1, 2], ids=["split", "nosplit"])
+def step_split(request):
+    """Both launch shapes of the plane-step kernels (K split over a
+    workgroup's waves, or one tile group per wave)."""
+    P.pyramid_lstm_set_step_split(request.param)
+    yield request.param
+    P.pyramid_lstm_set_step_split(0)
+
+
 @pytest.mark.parametrize("shape", STEP_SHAPES, ids=lambda s: "x".join(map(str, s)))
-def test_step_path_matches_oracle(shape, step_path):
+def test_step_path_matches_oracle(shape, step_path, step_split):
     inst = instance(shape, 4000 + sum(shape))
     L = inst.layers[0]
     dh = synth.upstream_grad(inst.x.shape[:-1] + (shape[-1],), 11 + sum(shape))

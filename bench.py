@@ -13,6 +13,12 @@ layer forward alone (inference, the single-layer forward workload) is timed as
 well and reported under "fwd".  Inputs are resident in HBM before timing.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+Two more workloads can be timed instead (not the headline; no CPU baseline):
+    --workload stacked-bf16   8 x 64^3 x 3, three layers (16, 32, 64) + FC tanh
+                              + softmax, bf16 storage, forward
+    --workload train-2layer   48 x 240 x 240 x 3, two layers (16, 32) + FC tanh
+                              + softmax cross-entropy, fp32, forward + backward
 """
 from __future__ import annotations
 
@@ -105,6 +111,93 @@ def roofline(phases, name, passes, V, C, O, mode="training"):
             "avg_launch_ms": round(ms / launches, 4)}
 
 
+def layer_path(C, O, dtype):
+    """Which kernels the library runs for a layer: the persistent sweeps
+    (fp32, 16 hidden units, at most 4 input channels) or the plane-step MFMA
+    path; phase names end in _mfma or _step accordingly."""
+    return "mfma" if dtype == "f32" and O == 16 and C <= 4 else "step"
+
+
+def network_roofline(phases, passes, V, shapes, dtype):
+    """Roofline of the slowest phase of a multi-layer pass: its algorithmic
+    work summed over the layers that ran it."""
+    cand = {k: v for k, v in phases.items() if phase_work(k, 1, 1, 16)[0] == "mfma"}
+    name = max(cand, key=lambda k: cand[k][0])
+    ms, launches = phases[name]
+    flops = 0
+    for C, O in shapes:
+        if name.endswith("_" + layer_path(C, O, dtype)) or (name.startswith("dx") and
+                                                           layer_path(C, O, dtype) == "step"):
+            flops += phase_work(name, V, C, O)[1]
+    achieved = flops * passes / (ms / 1e3) / 1e12
+    return {"kernel": name, "bound": "mfma", "achieved": round(achieved, 3),
+            "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": None,
+            "launches_per_pass": launches // passes,
+            "avg_launch_ms": round(ms / launches, 4)}
+
+
+def bench_network(args, cfg):
+    """Configs 4 (stacked, bf16 storage, forward) and 5 (two layers, fp32,
+    training step) through the same entry points."""
+    import torch
+    import synth
+    import paper_1506_07452_amd as P
+    from paper_1506_07452_amd.network import (LayerW, network_forward, network_train_step,
+                                              workspace_for)
+    inst = synth.config(cfg)
+    wl = inst.wl
+    tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+
+    def dev(a):
+        return torch.from_numpy(a).to("cuda:0").to(tdt).contiguous()
+
+    torch.cuda.init()
+    x = dev(inst.x)
+    layers = [LayerW(dev(L.wx), dev(L.wh), dev(L.b)) for L in inst.layers]
+    fcs = [(dev(w), dev(b)) for w, b in inst.fcs]
+    head = (dev(inst.head[0]), dev(inst.head[1]))
+    train = wl.labels
+    labels = torch.from_numpy(inst.labels).to("cuda:0") if train else None
+    ws = workspace_for(x.shape, wl.hidden, True, tdt, train, "cuda:0")
+    torch.cuda.synchronize()
+
+    def step():
+        if train:
+            return network_train_step(x, layers, fcs, head, labels, ws=ws)
+        return network_forward(x, layers, fcs, head, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    P.pyramid_lstm_timing_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / args.steps
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    V = wl.voxels
+    shapes, C = [], wl.C
+    for O in wl.hidden:
+        shapes.append((C, O))
+        C = 2 * O
+    vdu = wl.vdu_per_pass()
+    out = {
+        "metric": METRIC, "value": vdu / t, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": t * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name + (", fwd+bwd" if train else ", fwd"), "N": wl.N,
+                   "D": wl.D, "H": wl.H, "W": wl.W, "C": wl.C, "hidden": wl.hidden,
+                   "storage": wl.dtype, "classes": wl.classes},
+        "tflops": wl.flops_per_pass() / t / 1e12 if not train else None,
+        "roofline": network_roofline(phases, args.steps, V, shapes, wl.dtype),
+        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def cpu_baseline(inst_cfg, crop):
     """The fp64 oracle (as is) on a bounded crop of the same workload."""
     import numpy as np
@@ -132,6 +225,9 @@ def main():
     ap.add_argument("--cpu-crop", default="48x120x120")
     ap.add_argument("--separate-head", action="store_true",
                     help="run the FC / softmax head as separate kernels instead of the fused one")
+    ap.add_argument("--workload", default="mr-layer",
+                    choices=["mr-layer", "stacked-bf16", "train-2layer"],
+                    help="mr-layer: the headline single-layer MR workload (default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device three times (a plain copy kernel "
                          "of known size, to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -141,6 +237,9 @@ def main():
               "on a single MI355X and this build has no multi-GPU path (--gpus 1).",
               file=sys.stderr)
         sys.exit(2)
+    if args.workload != "mr-layer":
+        bench_network(args, 4 if args.workload == "stacked-bf16" else 5)
+        return
 
     import torch
     import synth

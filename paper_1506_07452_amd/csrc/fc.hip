@@ -750,9 +750,133 @@ size_t fc_ws(long long M, int Cin, int Cout)
     return cv.off;
 }
 
+// ---- FC + tanh on the MFMA ----------------------------------------------------
+// y = tanh(W x + b) for 16-voxel tiles: M = output units (16 per tile, CO
+// tiles), N = voxels, K = inputs in CI blocks of 16 (v_mfma_f32_16x16x4f32).
+// In each block lane group q takes inputs 4q .. 4q+3 (k-step i: input
+// 4q + i), so W rows and x rows are read as 16-byte (fp32) or 8-byte (bf16)
+// vectors in place, and every lane ends with four consecutive outputs of one
+// voxel.  A wave takes kFcNT voxel tiles.
+constexpr int kFcNT = 2;
+
+template <typename TS> struct Vec4;
+template <> struct Vec4<float> {
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    __device__ static f4v load(const float *p) { return *(const f4v *)p; }
+    __device__ static void store(float *p, f4v v) { *(f4v *)p = v; }
+};
+template <> struct Vec4<uint16_t> {
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    typedef unsigned short u4 __attribute__((ext_vector_type(4)));
+    __device__ static f4v load(const uint16_t *p)
+    {
+        const u4 v = *(const u4 *)p;
+        return f4v{bf16_to_f32(v[0]), bf16_to_f32(v[1]), bf16_to_f32(v[2]), bf16_to_f32(v[3])};
+    }
+    __device__ static void store(uint16_t *p, f4v v)
+    {
+        *(u4 *)p = u4{f32_to_bf16(v[0]), f32_to_bf16(v[1]), f32_to_bf16(v[2]), f32_to_bf16(v[3])};
+    }
+};
+
+template <typename TS, int CI, int CO>
+__global__ void __launch_bounds__(256)
+k_fc_tanh_mfma(long long M, const TS *__restrict__ x, const TS *__restrict__ w,
+               const TS *__restrict__ b, TS *__restrict__ y)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    constexpr int Cin = 16 * CI, Cout = 16 * CO;
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const long long tile0 = ((long long)blockIdx.x * 4 + (threadIdx.x >> 6)) * kFcNT;
+    long long row[kFcNT];
+    bool live[kFcNT];
+#pragma unroll
+    for (int nt = 0; nt < kFcNT; ++nt) {
+        row[nt] = (tile0 + nt) * 16 + col;
+        live[nt] = row[nt] < M;
+    }
+    f4 acc[CO][kFcNT];
+#pragma unroll
+    for (int mt = 0; mt < CO; ++mt) {
+        const f4 bv = Vec4<TS>::load(b + mt * 16 + 4 * q4);
+#pragma unroll
+        for (int nt = 0; nt < kFcNT; ++nt) acc[mt][nt] = bv;
+    }
+#pragma unroll
+    for (int kb = 0; kb < CI; ++kb) {
+        f4 xv[kFcNT];
+#pragma unroll
+        for (int nt = 0; nt < kFcNT; ++nt) {
+            xv[nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+            if (live[nt]) xv[nt] = Vec4<TS>::load(x + row[nt] * Cin + kb * 16 + 4 * q4);
+        }
+#pragma unroll
+        for (int mt = 0; mt < CO; ++mt) {
+            const f4 wv = Vec4<TS>::load(w + (long long)(mt * 16 + col) * Cin + kb * 16 + 4 * q4);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int nt = 0; nt < kFcNT; ++nt)
+                    acc[mt][nt] =
+                        __builtin_amdgcn_mfma_f32_16x16x4f32(wv[i], xv[nt][i], acc[mt][nt], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int nt = 0; nt < kFcNT; ++nt) {
+        if (!live[nt]) continue;
+#pragma unroll
+        for (int mt = 0; mt < CO; ++mt) {
+            f4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = tanh_fast(acc[mt][nt][i]);
+            Vec4<TS>::store(y + row[nt] * Cout + mt * 16 + 4 * q4, v);
+        }
+    }
+}
+
+template <typename TS, int CI>
+int fc_mfma_co(long long M, int Cout, const TS *x, const TS *w, const TS *b, TS *y,
+               hipStream_t st)
+{
+    const long long waves = (M + 16 * kFcNT - 1) / (16 * kFcNT);
+    const unsigned blocks = (unsigned)((waves + 3) / 4);
+    switch (Cout) {
+    case 32: k_fc_tanh_mfma<TS, CI, 2><<<blocks, 256, 0, st>>>(M, x, w, b, y); break;
+    case 64: k_fc_tanh_mfma<TS, CI, 4><<<blocks, 256, 0, st>>>(M, x, w, b, y); break;
+    case 128: k_fc_tanh_mfma<TS, CI, 8><<<blocks, 256, 0, st>>>(M, x, w, b, y); break;
+    default: return PLSTM_EUNSUPPORTED;
+    }
+    PLSTM_LAUNCH_CHECK();
+    return PLSTM_OK;
+}
+
+// Shapes of the MFMA FC: 16, 32 or 64 inputs, 32, 64 or 128 outputs.
+inline bool fc_mfma_ok(int Cin, int Cout)
+{
+    return (Cin == 16 || Cin == 32 || Cin == 64) && (Cout == 32 || Cout == 64 || Cout == 128);
+}
+
+template <typename TS>
+int fc_mfma(long long M, int Cin, int Cout, const TS *x, const TS *w, const TS *b, TS *y,
+            hipStream_t st)
+{
+    switch (Cin) {
+    case 16: return fc_mfma_co<TS, 1>(M, Cout, x, w, b, y, st);
+    case 32: return fc_mfma_co<TS, 2>(M, Cout, x, w, b, y, st);
+    default: return fc_mfma_co<TS, 4>(M, Cout, x, w, b, y, st);
+    }
+}
+
 static int fc_tanh_forward_impl(long long M, int Cin, int Cout, int dtype, const void *x,
                                 const void *w, const void *b, void *y, hipStream_t st)
 {
+    if (fc_mfma_ok(Cin, Cout)) {
+        if (dtype == PLSTM_BF16)
+            return fc_mfma<uint16_t>(M, Cin, Cout, (const uint16_t *)x, (const uint16_t *)w,
+                                     (const uint16_t *)b, (uint16_t *)y, st);
+        return fc_mfma<float>(M, Cin, Cout, (const float *)x, (const float *)w,
+                              (const float *)b, (float *)y, st);
+    }
     if (rows_ok(Cin)) {
         const dim3 grid((unsigned)((M + kRB - 1) / kRB), (Cout + kOC - 1) / kOC);
         const size_t lds = rows_lds(Cin, kOC, kOC * (Cin + 1));

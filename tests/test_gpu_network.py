@@ -101,6 +101,26 @@ def test_fc_and_softmax_match_oracle():
         assert normwise(host(got), want) <= TOL["f32"]
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cin,cout", [(16, 32), (32, 64), (64, 128), (16, 128), (64, 32),
+                                      (24, 40)], ids=lambda v: str(v))
+def test_fc_tanh_forward_widths(cin, cout, dtype):
+    """FC + tanh at every width the MFMA kernel takes (and one it does not),
+    a ragged number of rows, both storage types."""
+    rng = np.random.default_rng(91 + cin + cout)
+    M = 1037
+    xd = dev(rng.standard_normal((M, cin)), dtype)
+    wd = dev(rng.uniform(-0.3, 0.3, (cout, cin)), dtype)
+    bd = dev(rng.uniform(-0.3, 0.3, cout), dtype)
+    import paper_1506_07452_amd as P
+    say("fc tanh forward", cin, cout, dtype)
+    y = torch.empty(M, cout, device=DEV, dtype=xd.dtype)
+    P.pyramid_fc_tanh_forward(xd, wd, bd, y)
+    torch.cuda.synchronize()
+    ref = oracle.fc_tanh_forward(host(xd), host(wd), host(bd))
+    assert normwise(host(y), ref) <= TOL[dtype]
+
+
 def oracle_head(xa, w1, b1, w2, b2, lab):
     """FC tanh -> softmax CE -> backward, chained from the oracle's pieces."""
     ry = oracle.fc_tanh_forward(xa, w1, b1)

@@ -34,6 +34,7 @@ sys.path.insert(0, ROOT)
 METRIC = "voxel-direction LSTM updates/sec (fwd, fwd+bwd) + % peak MFMA, 1 MI355X"
 UNIT = "voxel-direction updates/s"
 PEAK_FP32_TFLOPS = 157.3     # MI355X dense fp32 MFMA
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 
 
@@ -112,10 +113,13 @@ def roofline(phases, name, passes, V, C, O, mode="training"):
 
 
 def layer_path(C, O, dtype):
-    """Which kernels the library runs for a layer: the persistent sweeps
-    (fp32, 16 hidden units, at most 4 input channels) or the plane-step MFMA
-    path; phase names end in _mfma or _step accordingly."""
-    return "mfma" if dtype == "f32" and O == 16 and C <= 4 else "step"
+    """Which forward kernels the library runs for a layer: the persistent
+    sweeps (fp32, 16 hidden units, at most 4 input channels), the plane-step
+    bf16 MFMA (bf16 storage, 32 or 64 hidden units) or the plane-step fp32
+    MFMA; phase names end in _mfma, _step_bf16 or _step accordingly."""
+    if dtype == "f32" and O == 16 and C <= 4:
+        return "mfma"
+    return "step_bf16" if dtype == "bf16" and O in (32, 64) else "step"
 
 
 def network_roofline(phases, passes, V, shapes, dtype):
@@ -126,13 +130,14 @@ def network_roofline(phases, passes, V, shapes, dtype):
     ms, launches = phases[name]
     flops = 0
     for C, O in shapes:
-        if name.endswith("_" + layer_path(C, O, dtype)) or (name.startswith("dx") and
-                                                           layer_path(C, O, dtype) == "step"):
+        path = layer_path(C, O, dtype)
+        if name.endswith("_" + path) or (name.startswith("dx") and path != "mfma"):
             flops += phase_work(name, V, C, O)[1]
     achieved = flops * passes / (ms / 1e3) / 1e12
+    peak = PEAK_BF16_TFLOPS if name.endswith("_bf16") else PEAK_FP32_TFLOPS
     return {"kernel": name, "bound": "mfma", "achieved": round(achieved, 3),
-            "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": None,
+            "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None,
             "launches_per_pass": launches // passes,
             "avg_launch_ms": round(ms / launches, 4)}
 
@@ -187,7 +192,9 @@ def bench_network(args, cfg):
     out = {
         "metric": METRIC, "value": vdu / t, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": t * 1e3, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
         "config": {"workload": wl.name + (", fwd+bwd" if train else ", fwd"), "N": wl.N,
                    "D": wl.D, "H": wl.H, "W": wl.W, "C": wl.C, "hidden": wl.hidden,
                    "storage": wl.dtype, "classes": wl.classes},

@@ -209,6 +209,13 @@ int pyramid_lstm_set_backward_path(int path);
  * values. */
 int pyramid_lstm_set_step_split(int mode);
 
+/* Contraction type of bf16-storage layers with 32 or 64 hidden units, for
+ * testing and tuning (process-wide): 1 = bf16 MFMA with fp32 accumulation
+ * (default; h_{t-1} enters the recurrent contraction rounded to bf16),
+ * 0 = fp32 MFMA on the widened values.  Returns PLSTM_EINVAL for other
+ * values. */
+int pyramid_lstm_set_bf16_mfma(int on);
+
 #ifdef __cplusplus
 }
 #endif

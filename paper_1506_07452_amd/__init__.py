@@ -21,7 +21,7 @@ __all__ = [
     "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
     "pyramid_head_workspace_size", "pyramid_head_train",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
-    "pyramid_lstm_set_backward_path", "pyramid_lstm_set_step_split",
+    "pyramid_lstm_set_backward_path", "pyramid_lstm_set_step_split", "pyramid_lstm_set_bf16_mfma",
     "library_path", "load",
 ]
 
@@ -89,6 +89,8 @@ def load():
                                              ctypes.POINTER(ctypes.c_int),
                                              ctypes.POINTER(ctypes.c_int)]
     lib.pyramid_lstm_timing_read.restype = ctypes.c_int
+    lib.pyramid_lstm_set_bf16_mfma.argtypes = [ctypes.c_int]
+    lib.pyramid_lstm_set_bf16_mfma.restype = ctypes.c_int
     lib.pyramid_lstm_set_step_split.argtypes = [ctypes.c_int]
     lib.pyramid_lstm_set_step_split.restype = ctypes.c_int
     lib.pyramid_lstm_set_forward_path.argtypes = [ctypes.c_int]
@@ -263,3 +265,9 @@ def pyramid_lstm_set_step_split(mode: int) -> None:
     """Plane-step launch shape: 0 = automatic, 1 = always split each tile's K
     over a workgroup's waves, 2 = never."""
     _check("pyramid_lstm_set_step_split", load().pyramid_lstm_set_step_split(int(mode)))
+
+
+def pyramid_lstm_set_bf16_mfma(on: int) -> None:
+    """bf16-storage layers with 32 or 64 hidden units: 1 = bf16 MFMA (fp32
+    accumulation), 0 = fp32 MFMA."""
+    _check("pyramid_lstm_set_bf16_mfma", load().pyramid_lstm_set_bf16_mfma(int(on)))

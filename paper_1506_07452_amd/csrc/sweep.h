@@ -62,5 +62,8 @@ extern int g_backward_path;
 // Plane-step launches: 0 = automatic, 1 = always split each tile's K over a
 // workgroup's waves, 2 = never.
 extern int g_step_split;
+// bf16 storage with 32 or 64 hidden units: 1 = contraction on the bf16 MFMA
+// (default), 0 = on the fp32 MFMA.
+extern int g_step_bf16_mfma;
 
 }  // namespace plstm

@@ -374,6 +374,236 @@ k_step_fwd(FwdStepArgs a)
     }
 }
 
+// ---- forward step on the bf16 MFMA (bf16 storage, O = 32 or 64) --------------
+// For bf16 storage the contraction runs on v_mfma_f32_16x16x32_bf16 with fp32
+// accumulation: x and the weights are bf16 values already, and h_{t-1}
+// enters as bf16 (h^d is also kept in fp32 for the direction sum; c stays
+// fp32).  Lane l supplies A[m = l%16][k = 8(l/16) + j] and B[k][n = l%16],
+// j = 0..7, so lane group q takes channels 8q .. 8q+7 of a 32-channel block:
+// one 16-byte load per operand, one MFMA per block, gate, tile.
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef unsigned short us4 __attribute__((ext_vector_type(4)));
+
+__device__ inline f4 mfma_bf16(bf8 a, bf8 b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ inline bf8 bload8h(__amdgpu_buffer_rsrc_t rs, unsigned off)
+{
+    return __builtin_bit_cast(bf8, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0));
+}
+
+// x [N][V][C] bf16 -> xb [N][V][C32] bf16, channels >= C zero.
+__global__ void __launch_bounds__(256)
+k_pad_x_b16(long long nvox, int C, int C32, const uint16_t *__restrict__ x,
+            uint16_t *__restrict__ xb)
+{
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= nvox * C32) return;
+    const long long v = i / C32;
+    const int c = (int)(i - v * C32);
+    xb[i] = c < C ? x[v * C + c] : (uint16_t)0;
+}
+
+// bf16 A fragments fragb[d][ug][kg][gate][lane][8]: K-group kg < KX is input
+// tap kg / (C32/32), channel block kg % (C32/32); the rest are h taps
+// (kg - KX) / (O/32), block (kg - KX) % (O/32).  Entry j of lane (q, col)
+// is the weight of gate-unit gate*O + 16 ug + col for channel 32 cb + 8q + j.
+__global__ void __launch_bounds__(256)
+k_pack_fwd_b16(int O, int C, int C32, int KX, int KG, const uint16_t *__restrict__ wx,
+               const uint16_t *__restrict__ wh, const uint16_t *__restrict__ b,
+               uint16_t *__restrict__ frag, float *__restrict__ bias)
+{
+    const int U = O / 16, G = 4 * O, CX = C32 / 32, UH = O / 32;
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i < (long long)kDirs * G) bias[i] = bf16_to_f32(b[i]);
+    if (i >= (long long)kDirs * U * KG * 2048) return;
+    const int j8 = (int)(i & 7), lane = (int)((i >> 3) & 63), gate = (int)((i >> 9) & 3);
+    long long r = i >> 11;
+    const int kg = (int)(r % KG);
+    r /= KG;
+    const int ug = (int)(r % U), d = (int)(r / U);
+    const int q = lane >> 4, col = lane & 15;
+    const long long gu = (long long)d * G + gate * O + ug * 16 + col;
+    uint16_t v = 0;
+    if (kg < KX) {
+        const int tap = kg / CX, c = (kg % CX) * 32 + 8 * q + j8;
+        if (c < C) v = wx[(gu * C + c) * 9 + tap];
+    } else {
+        const int kh = kg - KX, tap = kh / UH, jj = (kh % UH) * 32 + 8 * q + j8;
+        v = wh[(gu * O + jj) * 9 + tap];
+    }
+    frag[i] = v;
+}
+
+struct FwdB16Args {
+    Geom g;
+    int t;
+    int C32, KX, KG;          // padded channels, input K-groups (9 C32/32), all K-groups
+    int cx_mul32;             // ceil(2^16 / (C32/32)): division by C32/32
+    const uint16_t *xb;       // [N][V][C32] bf16
+    const uint16_t *frag;     // [6][U][KG][4][64][8] bf16
+    const float *bias;        // [6][4O]
+    float *hd, *cell;         // [6][N][V][O] fp32
+    uint16_t *hb;             // [6][N][V][O] bf16 copy of h^d (the recurrence's operand)
+    int npg[kDirs];
+    int base[kDirs + 1];
+};
+
+// Same items and launch shapes as k_step_fwd.
+template <int U, bool SPLIT>
+__global__ void __launch_bounds__(64 * kSW)
+k_step_fwd_b16(FwdB16Args a)
+{
+    constexpr int O = 16 * U, G = 4 * O, UH = O / 32;
+    constexpr int KS = SPLIT ? kSW : 1;
+    constexpr int NE = SPLIT ? 1 : kNT;
+    static_assert(kNT == kSW && O % 32 == 0, "wave w finishes tile w; 32-channel blocks");
+    __shared__ f4 red[SPLIT ? kSW : 1][4][kNT][64];
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int item = SPLIT ? (int)blockIdx.x : (int)blockIdx.x * kSW + wave;
+    if (item >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, item);
+    const DirGeom dg = a.g.dir[d];
+    const int npg = a.npg[d];
+    int r = item - a.base[d];
+    const int n = r / (U * npg);
+    r -= n * U * npg;
+    const int ug = r / npg, pg = r - ug * npg;
+    const int t = a.t;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const int C32 = a.C32, CX = C32 >> 5, KX = a.KX;
+    const int hoff = -dg.sign * ss;
+    const int uo = ug * 16 + 4 * q4;
+
+    int vox[kNT];
+    unsigned nbm[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const int pix = (pg * kNT + nt) * 16 + col;
+        const bool live = pix < P * Q;
+        const int p = live ? pix / Q : 0, qq = live ? pix - p * Q : 0;
+        vox[nt] = s * ss + p * sp + qq * sq;
+        unsigned m = 0;
+#pragma unroll
+        for (int ka = 0; ka < 3; ++ka)
+#pragma unroll
+            for (int kb = 0; kb < 3; ++kb)
+                m |= (unsigned)(live & ((unsigned)(p + ka - 1) < (unsigned)P) &
+                                ((unsigned)(qq + kb - 1) < (unsigned)Q))
+                     << (ka * 3 + kb);
+        nbm[nt] = m;
+    }
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    // byte sizes: V * C32 * 2 and V * O * 2 (< 2^31, checked on the host)
+    const auto rs_x = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(a.xb + (long long)n * V * C32), (short)0, (int)(V * C32 * 2),
+        kRsrcWord3);
+    const auto rs_h = __builtin_amdgcn_make_buffer_rsrc(a.hb + sbase * O, (short)0,
+                                                        (int)(V * O * 2), kRsrcWord3);
+    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+    const uint16_t *fr = a.frag + (long long)(d * U + ug) * a.KG * 2048 + lane * 8;
+
+    int evox[NE];
+    unsigned ebits[NE];
+    f4 cprev[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+        evox[e] = vox[e];
+        ebits[e] = nbm[e];
+        if (SPLIT) {
+#pragma unroll
+            for (int nt = 1; nt < kNT; ++nt)
+                if (wave == nt) {
+                    evox[e] = vox[nt];
+                    ebits[e] = nbm[nt];
+                }
+        }
+        cprev[e] = bload4(rs_c, sel_off(t > 0 && ((ebits[e] >> 4) & 1),
+                                        (unsigned)((evox[e] + hoff) * O + uo) * 4u));
+    }
+
+    f4 acc[4][kNT];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    struct Ops {
+        bf8 a[4];
+        bf8 b[kNT];
+    };
+    auto load = [&](int kg, Ops &o) {
+        const bool is_x = kg < KX;
+        const int kk = is_x ? kg : kg - KX;
+        const int tap = is_x ? (kk * a.cx_mul32) >> 16 : kk / UH;
+        const int cb = kk - tap * (is_x ? CX : UH);
+        const int stride = is_x ? C32 : O;
+        const int dv = (is_x ? 0 : hoff) + (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
+        const auto rs = is_x ? rs_x : rs_h;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) o.a[g] = *(const bf8 *)(fr + (kg * 4 + g) * 512);
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt)
+            o.b[nt] = bload8h(rs, sel_off((nbm[nt] >> tap) & 1,
+                                          (unsigned)((vox[nt] + dv) * stride + cb * 32 + 8 * q4) *
+                                              2u));
+    };
+    const int KG = t > 0 ? a.KG : KX;
+    const int k0 = SPLIT ? wave : 0;
+    Ops cur, nxt;
+    if (k0 < KG) load(k0, cur);
+    for (int kg = k0; kg < KG; kg += KS) {
+        if (kg + KS < KG) load(kg + KS, nxt);
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = mfma_bf16(cur.a[g], cur.b[nt], acc[g][nt]);
+        cur = nxt;
+    }
+    if (SPLIT) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) red[SPLIT ? wave : 0][g][nt][lane] = acc[g][nt];
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+        if (!((ebits[e] >> 4) & 1)) continue;
+        f4 pre[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            f4 v = acc[g][e];
+            if (SPLIT) {
+                v = red[0][g][wave][lane];
+#pragma unroll
+                for (int w = 1; w < KS; ++w) v += red[SPLIT ? w : 0][g][wave][lane];
+            }
+            pre[g] = v + *(const f4 *)(a.bias + d * G + g * O + uo);
+        }
+        const long long vo = sbase + evox[e];
+        f4 c, h;
+        us4 hbv;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float gi = fsig(pre[0][i]), gf = fsig(pre[1][i]);
+            const float gg = ftanh(pre[2][i]), go = fsig(pre[3][i]);
+            c[i] = gg * gi + cprev[e][i] * gf;
+            h[i] = go * ftanh(c[i]);
+            hbv[i] = f32_to_bf16(h[i]);
+        }
+        *(f4 *)(a.cell + vo * O + uo) = c;
+        *(f4 *)(a.hd + vo * O + uo) = h;
+        *(us4 *)(a.hb + vo * O + uo) = hbv;
+    }
+}
+
 // ---- backward step ----------------------------------------------------------
 
 struct BwdStepArgs {
@@ -980,6 +1210,7 @@ int launch_dx_ct(const DxStepArgs &a, hipStream_t st)
 }  // namespace
 
 int g_step_split = 0;
+int g_step_bf16_mfma = 1;
 
 bool step_supported(const Geom &g)
 {
@@ -995,6 +1226,13 @@ bool step_supported(const Geom &g)
     return items < (1LL << 30);
 }
 
+// bf16 storage with 32 or 64 hidden units takes the bf16 MFMA.
+inline bool use_b16(const Geom &g, int dtype)
+{
+    return dtype == PLSTM_BF16 && (g.O == 32 || g.O == 64) && g_step_bf16_mfma;
+}
+inline int pad32(int c) { return (c + 31) / 32 * 32; }
+
 size_t step_fwd_ws(const Geom &g)
 {
     const int U = g.O / 16, Cp = pad16(g.C), KG = 9 * (Cp + g.O) / 16;
@@ -1002,13 +1240,80 @@ size_t step_fwd_ws(const Geom &g)
     cv.take<float>((size_t)g.N * g.V * Cp);          // padded x
     cv.take<float>((size_t)kDirs * U * KG * 1024);   // A fragments
     cv.take<float>((size_t)kDirs * 4 * g.O);         // bias
-    return cv.off;
+    size_t need = cv.off;
+    if (g.O % 32 == 0) {                             // bf16 variant
+        const int C32 = pad32(g.C), KGb = 9 * (C32 + g.O) / 32;
+        Carve cb(nullptr);
+        cb.take<uint16_t>((size_t)g.N * g.V * C32);
+        cb.take<uint16_t>((size_t)kDirs * U * KGb * 2048);
+        cb.take<float>((size_t)kDirs * 4 * g.O);
+        cb.take<uint16_t>((size_t)kDirs * g.N * g.V * g.O);
+        if (cb.off > need) need = cb.off;
+    }
+    return need;
+}
+
+template <int U>
+int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
+{
+    const int T = max_T(g);
+    const int few = split_threshold();
+    for (int t = 0; t < T; ++t) {
+        a.t = t;
+        int tot = 0;
+        for (int d = 0; d < kDirs; ++d) {
+            a.base[d] = tot;
+            if (t < g.dir[d].T) tot += g.N * U * a.npg[d];
+        }
+        a.base[kDirs] = tot;
+        if (tot < few)
+            k_step_fwd_b16<U, true><<<tot, 64 * kSW, 0, st>>>(a);
+        else
+            k_step_fwd_b16<U, false><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
+        PLSTM_LAUNCH_CHECK();
+    }
+    return PLSTM_OK;
+}
+
+static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
+                        const uint16_t *wh, const uint16_t *b, float *hd, float *cell, void *ws,
+                        hipStream_t st)
+{
+    const int U = g.O / 16, C32 = pad32(g.C);
+    const int KX = 9 * C32 / 32, KG = KX + 9 * g.O / 32;
+    Carve cv(ws);
+    uint16_t *xb = cv.take<uint16_t>((size_t)g.N * g.V * C32);
+    uint16_t *frag = cv.take<uint16_t>((size_t)kDirs * U * KG * 2048);
+    float *bias = cv.take<float>((size_t)kDirs * 4 * g.O);
+    uint16_t *hb = cv.take<uint16_t>((size_t)kDirs * g.N * g.V * g.O);
+    const long long nvox = (long long)g.N * g.V;
+    const long long nfrag = (long long)kDirs * U * KG * 2048;
+    timing_begin("sweep_fwd_step_bf16", st);
+    k_pad_x_b16<<<blocks_for(nvox * C32, 256), 256, 0, st>>>(nvox, g.C, C32, x, xb);
+    PLSTM_LAUNCH_CHECK();
+    k_pack_fwd_b16<<<blocks_for(nfrag, 256), 256, 0, st>>>(g.O, g.C, C32, KX, KG, wx, wh, b,
+                                                           frag, bias);
+    PLSTM_LAUNCH_CHECK();
+    FwdB16Args a;
+    a.g = g;
+    a.C32 = C32; a.KX = KX; a.KG = KG;
+    a.cx_mul32 = (65536 + C32 / 32 - 1) / (C32 / 32);
+    a.xb = xb; a.frag = frag; a.bias = bias;
+    a.hd = hd; a.cell = cell; a.hb = hb;
+    for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
+    const int rc = U == 2 ? launch_fwd_b16_steps<2>(g, a, st) : launch_fwd_b16_steps<4>(g, a, st);
+    if (rc != PLSTM_OK) return rc;
+    timing_end(2 + max_T(g), st);
+    return PLSTM_OK;
 }
 
 int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
              const void *b, float *hd, float *cell, float *gates, void *ws, hipStream_t st)
 {
     if (!step_supported(g)) return PLSTM_EUNSUPPORTED;
+    if (use_b16(g, dtype) && !gates)
+        return step_fwd_b16(g, (const uint16_t *)x, (const uint16_t *)wx, (const uint16_t *)wh,
+                            (const uint16_t *)b, hd, cell, ws, st);
     const int U = g.O / 16, Cp = pad16(g.C);
     const int KX = 9 * Cp / 16, KG = KX + 9 * U;
     Carve cv(ws);
@@ -1168,5 +1473,12 @@ extern "C" int pyramid_lstm_set_step_split(int mode)
 {
     if (mode < 0 || mode > 2) return PLSTM_EINVAL;
     plstm::g_step_split = mode;
+    return PLSTM_OK;
+}
+
+extern "C" int pyramid_lstm_set_bf16_mfma(int on)
+{
+    if (on != 0 && on != 1) return PLSTM_EINVAL;
+    plstm::g_step_bf16_mfma = on;
     return PLSTM_OK;
 }

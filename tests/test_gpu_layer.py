@@ -276,6 +276,32 @@ def test_forward_bf16_matches_oracle(shape):
     assert err <= TOL["bf16"], err
 
 
+@pytest.mark.parametrize("bf16_mfma", [1, 0], ids=["bf16_mfma", "fp32_mfma"])
+@pytest.mark.parametrize("shape", [(1, 4, 6, 70, 3, 64), (2, 9, 17, 40, 32, 32),
+                                   (1, 5, 23, 9, 40, 32), (2, 3, 7, 66, 64, 64)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_forward_bf16_large_hidden_matches_oracle(shape, bf16_mfma, step_split):
+    """bf16 storage with 32 or 64 hidden units: the bf16-MFMA forward step
+    (and the fp32-MFMA one), both launch shapes, channel counts below, at
+    and between 32-channel blocks."""
+    inst = instance(shape, 2500 + sum(shape), "bf16")
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    say("forward bf16 large hidden", shape, bf16_mfma)
+    P.pyramid_lstm_set_bf16_mfma(bf16_mfma)
+    try:
+        P.pyramid_lstm_timing_enable(True)
+        h, _ = layer_forward(dev(inst.x, "bf16"), layer_dev(L, "bf16"))
+        torch.cuda.synchronize()
+        phases = P.pyramid_lstm_timing_read()
+        P.pyramid_lstm_timing_enable(False)
+    finally:
+        P.pyramid_lstm_set_bf16_mfma(1)
+    assert ("sweep_fwd_step_bf16" in phases) == bool(bf16_mfma), phases
+    err = normwise(host(h), ref)
+    assert err <= TOL["bf16"], err
+
+
 @pytest.mark.parametrize("shape", SHAPES + [(3, 6, 20, 18, 2, 16), (1, 7, 130, 90, 1, 16)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_training_forward_and_backward_match_oracle(shape):

@@ -397,6 +397,46 @@ def test_network_backward_finite_differences():
             assert abs(fd - an) <= 1e-8 + 1e-5 * abs(an), (fd, an)
 
 
+def test_paper_topology_backward_finite_differences():
+    """The network shape of Section 3 ("Experimental Setup"), scaled down:
+    PyraMiD (5 x 5 filters) -> FC tanh -> PyraMiD -> output layer directly
+    (no hidden FC after the last PyraMiD layer), softmax, mean CE: every
+    parameter tensor's gradient against central differences."""
+    rng = np.random.default_rng(151)
+    N, D, H, W, C = 1, 2, 4, 3, 2
+    x = rng.standard_normal((N, D, H, W, C))
+    layers = [synth.layer_params(rng, C, 2, K=5), synth.layer_params(rng, 3, 2, K=5)]
+    layers = [(l.wx.astype(np.float64) * 3, l.wh.astype(np.float64) * 3, l.b.astype(np.float64))
+              for l in layers]
+    fcs = [(rng.uniform(-0.5, 0.5, (3, 2)), rng.uniform(-0.5, 0.5, 3))]
+    head = (rng.uniform(-0.5, 0.5, (4, 2)), rng.uniform(-0.5, 0.5, 4))
+    lab = rng.integers(0, 4, N * D * H * W)
+    g = onet.backward(x, layers, fcs, head, lab)
+    assert len(g["fcs"]) == 1 and len(g["layers"]) == 2
+    eps = 1e-6
+
+    def L():
+        return onet.forward(x, layers, fcs, head, lab)["loss"]
+
+    checks = [(head[0], g["head"][0]), (head[1], g["head"][1]),
+              (fcs[0][0], g["fcs"][0][0]), (fcs[0][1], g["fcs"][0][1])]
+    for li in range(2):
+        checks += [(layers[li][0], g["layers"][li][0]), (layers[li][1], g["layers"][li][1]),
+                   (layers[li][2], g["layers"][li][2])]
+    for arr, grad in checks:
+        flat = arr.reshape(-1)
+        for k in rng.choice(flat.size, size=min(flat.size, 6), replace=False):
+            s = flat[k]
+            flat[k] = s + eps
+            lp = L()
+            flat[k] = s - eps
+            lm = L()
+            flat[k] = s
+            fd = (lp - lm) / (2 * eps)
+            an = grad.reshape(-1)[k]
+            assert abs(fd - an) <= 1e-8 + 1e-5 * abs(an), (fd, an)
+
+
 # ------------------------------------------------- P8 parameter structure
 def test_parameter_count_matches_paper():
     """Section 3 ("Experimental Setup") prints 10,751,549 weights for three

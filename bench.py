@@ -19,6 +19,10 @@ Two more workloads can be timed instead (not the headline; no CPU baseline):
                               + softmax, bf16 storage, forward
     --workload train-2layer   48 x 240 x 240 x 3, two layers (16, 32) + FC tanh
                               + softmax cross-entropy, fp32, forward + backward
+    --workload paper-net      the network of the paper's experiments (7x7
+                              filters, 16 / FC 25 / 32 / FC 45 / 64 -> output)
+                              on a 25 x 240 x 240 x 5 MR sub-volume, softmax
+                              cross-entropy, fp32, forward + backward
 """
 from __future__ import annotations
 
@@ -38,19 +42,19 @@ PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 
 
-def phase_work(name, V, C, O):
+def phase_work(name, V, C, O, K=3):
     """(bound, algorithmic amount per pass, unit) of a library phase for one
-    layer over V voxels.  Contraction flops count the dense 3x3 stencils."""
-    G = 4 * O
+    layer over V voxels.  Contraction flops count the dense K x K stencils."""
+    G, KK = 4 * O, K * K
     if name.startswith("sweep_fwd"):
-        return "mfma", 6 * V * 2 * 9 * G * (C + O), "TFLOP/s"
+        return "mfma", 6 * V * 2 * KK * G * (C + O), "TFLOP/s"
     if name.startswith("sweep_bwd"):
         # recurrent transposed convolution (dh) plus the gate gradients
-        return "mfma", 6 * V * 2 * 9 * G * O, "TFLOP/s"
+        return "mfma", 6 * V * 2 * KK * G * O, "TFLOP/s"
     if name.startswith("wgrad"):
-        return "mfma", 6 * V * 2 * G * (9 * (C + O) + 1), "TFLOP/s"
+        return "mfma", 6 * V * 2 * G * (KK * (C + O) + 1), "TFLOP/s"
     if name.startswith("dx"):
-        return "mfma", 6 * V * 2 * 9 * G * C, "TFLOP/s"
+        return "mfma", 6 * V * 2 * KK * G * C, "TFLOP/s"
     if name.startswith("sum_dirs"):
         return "hbm", (6 + 1) * V * O * 4, "GB/s"
     if name.startswith("head_fused"):
@@ -112,27 +116,27 @@ def roofline(phases, name, passes, V, C, O, mode="training"):
             "avg_launch_ms": round(ms / launches, 4)}
 
 
-def layer_path(C, O, dtype):
+def layer_path(C, O, dtype, K=3):
     """Which forward kernels the library runs for a layer: the persistent
-    sweeps (fp32, 16 hidden units, at most 4 input channels), the plane-step
-    bf16 MFMA (bf16 storage, 32 or 64 hidden units) or the plane-step fp32
-    MFMA; phase names end in _mfma, _step_bf16 or _step accordingly."""
-    if dtype == "f32" and O == 16 and C <= 4:
+    sweeps (fp32, 16 hidden units, at most 4 input channels, 3x3), the
+    plane-step bf16 MFMA (bf16 storage, 32 or 64 hidden units) or the
+    plane-step fp32 MFMA; phase names end in _mfma, _step_bf16 or _step."""
+    if dtype == "f32" and O == 16 and C <= 4 and K == 3:
         return "mfma"
     return "step_bf16" if dtype == "bf16" and O in (32, 64) else "step"
 
 
-def network_roofline(phases, passes, V, shapes, dtype):
+def network_roofline(phases, passes, V, shapes, dtype, K=3):
     """Roofline of the slowest phase of a multi-layer pass: its algorithmic
     work summed over the layers that ran it."""
     cand = {k: v for k, v in phases.items() if phase_work(k, 1, 1, 16)[0] == "mfma"}
     name = max(cand, key=lambda k: cand[k][0])
     ms, launches = phases[name]
     flops = 0
-    for C, O in shapes:
-        path = layer_path(C, O, dtype)
-        if name.endswith("_" + path) or (name.startswith("dx") and path != "mfma"):
-            flops += phase_work(name, V, C, O)[1]
+    for li, (C, O) in enumerate(shapes):
+        path = layer_path(C, O, dtype, K)
+        if name.endswith("_" + path) or (name.startswith("dx") and li > 0):
+            flops += phase_work(name, V, C, O, K)[1]
     achieved = flops * passes / (ms / 1e3) / 1e12
     peak = PEAK_BF16_TFLOPS if name.endswith("_bf16") else PEAK_FP32_TFLOPS
     return {"kernel": name, "bound": "mfma", "achieved": round(achieved, 3),
@@ -144,13 +148,14 @@ def network_roofline(phases, passes, V, shapes, dtype):
 
 def bench_network(args, cfg):
     """Configs 4 (stacked, bf16 storage, forward) and 5 (two layers, fp32,
-    training step) through the same entry points."""
+    training step), or the paper's network (cfg None), through the same entry
+    points."""
     import torch
     import synth
     import paper_1506_07452_amd as P
     from paper_1506_07452_amd.network import (LayerW, network_forward, network_train_step,
-                                              workspace_for)
-    inst = synth.config(cfg)
+                                              workspace_for_layers)
+    inst = synth.config(cfg) if cfg is not None else synth.make(synth.PAPER_NET)
     wl = inst.wl
     tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
 
@@ -164,7 +169,8 @@ def bench_network(args, cfg):
     head = (dev(inst.head[0]), dev(inst.head[1]))
     train = wl.labels
     labels = torch.from_numpy(inst.labels).to("cuda:0") if train else None
-    ws = workspace_for(x.shape, wl.hidden, True, tdt, train, "cuda:0")
+    ws = workspace_for_layers(x.shape, [(C, O, wl.K) for C, O in wl.layer_shapes()], tdt,
+                              train, "cuda:0")
     torch.cuda.synchronize()
 
     def step():
@@ -184,10 +190,7 @@ def bench_network(args, cfg):
     phases = P.pyramid_lstm_timing_read()
     P.pyramid_lstm_timing_enable(False)
     V = wl.voxels
-    shapes, C = [], wl.C
-    for O in wl.hidden:
-        shapes.append((C, O))
-        C = 2 * O
+    shapes = wl.layer_shapes()
     vdu = wl.vdu_per_pass()
     out = {
         "metric": METRIC, "value": vdu / t, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
@@ -197,9 +200,10 @@ def bench_network(args, cfg):
         "data": "synthetic",
         "config": {"workload": wl.name + (", fwd+bwd" if train else ", fwd"), "N": wl.N,
                    "D": wl.D, "H": wl.H, "W": wl.W, "C": wl.C, "hidden": wl.hidden,
+                   "fc": [wl.fc_width(i) for i in range(len(wl.hidden))], "K": wl.K,
                    "storage": wl.dtype, "classes": wl.classes},
         "tflops": wl.flops_per_pass() / t / 1e12 if not train else None,
-        "roofline": network_roofline(phases, args.steps, V, shapes, wl.dtype),
+        "roofline": network_roofline(phases, args.steps, V, shapes, wl.dtype, wl.K),
         "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
     }
     print(json.dumps(out), flush=True)
@@ -233,7 +237,7 @@ def main():
     ap.add_argument("--separate-head", action="store_true",
                     help="run the FC / softmax head as separate kernels instead of the fused one")
     ap.add_argument("--workload", default="mr-layer",
-                    choices=["mr-layer", "stacked-bf16", "train-2layer"],
+                    choices=["mr-layer", "stacked-bf16", "train-2layer", "paper-net"],
                     help="mr-layer: the headline single-layer MR workload (default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device three times (a plain copy kernel "
@@ -245,7 +249,8 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     if args.workload != "mr-layer":
-        bench_network(args, 4 if args.workload == "stacked-bf16" else 5)
+        bench_network(args, {"stacked-bf16": 4, "train-2layer": 5, "paper-net": None}[
+            args.workload])
         return
 
     import torch

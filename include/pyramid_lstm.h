@@ -25,19 +25,22 @@
  *   - Layouts are row-major, channels last:
  *       x   [N][D][H][W][C]        volume, C input channels
  *       h   [N][D][H][W][O]        layer output (sum of the six directions)
- *       wx  [6][4*O][C][3][3]      input filters, per direction
- *       wh  [6][4*O][O][3][3]      recurrent filters, per direction
+ *       wx  [6][4*O][C][K][K]      input filters, per direction
+ *       wh  [6][4*O][O][K][K]      recurrent filters, per direction
  *       b   [6][4*O]               biases, per direction
  *     Direction order 0..5 = z+, z-, y+, y-, x+, x- (Section 2.3).  Row g*O+o
  *     of wx/wh/b is unit o of gate g, gates in the order (i, f, g=c~, o) of
- *     Eq. (7), (8), (9), (11).  The 3x3 taps (ka, kb) run over the plane's two
- *     in-plane axes in (D, H, W) order: z+- -> (H, W), y+- -> (D, W),
+ *     Eq. (7), (8), (9), (11).  The K x K taps (ka, kb) run over the plane's
+ *     two in-plane axes in (D, H, W) order: z+- -> (H, W), y+- -> (D, W),
  *     x+- -> (D, H); the same for the + and - direction of an axis.  The
- *     convolution is a cross-correlation with zero "same" padding:
- *       A[p][q][g*O+o] += in[p+ka-1][q+kb-1][c] * w[g*O+o][c][ka][kb].
+ *     convolution is a cross-correlation with zero "same" padding, r = (K-1)/2:
+ *       A[p][q][g*O+o] += in[p+ka-r][q+kb-r][c] * w[g*O+o][c][ka][kb].
+ *     K is odd: 3 is the filter of Section 2.3's examples, 7 the one of the
+ *     experiments (Section 3, "Experimental Setup").
  *     Plane t of a + sweep is index t along its axis, of a - sweep index T-1-t;
  *     the first plane has no predecessor (h_{-1} = c_{-1} = 0, Section 2.3).
- *   - Supported: N, D, H, W >= 1; 1 <= C <= 1024; O in {4, 8, 16, 32, 64}.
+ *   - Supported: N, D, H, W >= 1; 1 <= C <= 1024; O in {4, 8, 16, 32, 64};
+ *     K in {1, 3, 5, 7}.
  */
 #ifndef PYRAMID_LSTM_H
 #define PYRAMID_LSTM_H
@@ -65,6 +68,7 @@ typedef struct plstm_shape {
     int32_t C;            /* input channels */
     int32_t O;            /* hidden units per direction */
     int32_t dtype;        /* enum plstm_dtype */
+    int32_t K;            /* filter size (odd, 1..7) of wx and wh; 0 means 3 */
 } plstm_shape;
 
 /* Human-readable name of a status code (static string, never NULL). */

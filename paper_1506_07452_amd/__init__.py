@@ -42,7 +42,7 @@ class PyramidLSTMError(RuntimeError):
 class plstm_shape(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int32), ("D", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("W", ctypes.c_int32), ("C", ctypes.c_int32), ("O", ctypes.c_int32),
-                ("dtype", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("K", ctypes.c_int32)]
 
 
 def library_path() -> str:
@@ -128,14 +128,14 @@ def _check(fn, rc):
         raise PyramidLSTMError(fn, rc)
 
 
-def shape_for(x: torch.Tensor, O: int) -> plstm_shape:
-    """plstm_shape of a [N][D][H][W][C] volume and hidden size O."""
+def shape_for(x: torch.Tensor, O: int, K: int = 3) -> plstm_shape:
+    """plstm_shape of a [N][D][H][W][C] volume, hidden size O and K x K filters."""
     if x.dim() != 5:
         raise ValueError("x must be [N][D][H][W][C]")
     if x.dtype not in _DT:
         raise ValueError("x must be float32 or bfloat16")
     N, D, H, W, C = x.shape
-    return plstm_shape(N, D, H, W, C, O, _DT[x.dtype])
+    return plstm_shape(N, D, H, W, C, O, _DT[x.dtype], K)
 
 
 def _workspace(nbytes, device):

@@ -18,6 +18,8 @@ int check_shape(const plstm_shape *s)
     if (s->N < 1 || s->D < 1 || s->H < 1 || s->W < 1 || s->C < 1 || s->O < 1)
         return PLSTM_EINVAL;
     if (s->dtype != PLSTM_F32 && s->dtype != PLSTM_BF16) return PLSTM_EINVAL;
+    if (s->K != 0 && (s->K < 1 || s->K % 2 == 0)) return PLSTM_EINVAL;
+    if (s->K > 7) return PLSTM_EUNSUPPORTED;
     if (s->C > 1024) return PLSTM_EUNSUPPORTED;
     if (s->O != 4 && s->O != 8 && s->O != 16 && s->O != 32 && s->O != 64)
         return PLSTM_EUNSUPPORTED;

@@ -22,6 +22,7 @@ struct DirGeom {
 
 struct Geom {
     int N, D, H, W, C, O;
+    int K;                // filter size (odd); taps K * K, radius (K - 1) / 2
     long long V;          // D * H * W
     DirGeom dir[kDirs];
 };
@@ -29,6 +30,7 @@ struct Geom {
 inline Geom make_geom(const plstm_shape &s) {
     Geom g;
     g.N = s.N; g.D = s.D; g.H = s.H; g.W = s.W; g.C = s.C; g.O = s.O;
+    g.K = s.K == 0 ? 3 : s.K;
     const long long HW = (long long)s.H * s.W;
     g.V = (long long)s.D * HW;
     for (int d = 0; d < kDirs; ++d) {

@@ -1,18 +1,19 @@
-// Generic PyraMiD-LSTM path: any supported shape, one launch per plane step.
+// Generic PyraMiD-LSTM path: any supported shape and filter size K, one launch
+// per plane step.
 //
 // Forward (Section 2.3, Eq. (7)-(13)): for step t, every direction d with
 // t < T_d updates all pixels of its plane t at once.  One thread owns one
 // (direction, batch element, pixel, hidden unit) and produces the four gate
-// pre-activations of that unit by direct 3x3 loops over the input plane and
+// pre-activations of that unit by direct K x K loops over the input plane and
 // the previous plane's h^d; the cell state lives in a per-direction volume.
 // The six per-direction outputs are summed in the fixed order d = 0..5.
 //
 // Backward (the chain rule through Eq. (7)-(13), reverse plane order): for
 // step t every thread owns one (d, n, pixel, unit j): it collects dL/dh^d from
 // the upstream gradient and from the next plane's gate gradients (a transposed
-// 3x3 convolution with wh), forms dL/dc and the four gate gradients of unit j.
+// K x K convolution with wh), forms dL/dc and the four gate gradients of unit j.
 // Parameter gradients are then block-tiled reductions over all voxels
-// (deterministic two-stage sums), and dL/dx a transposed 3x3 convolution with
+// (deterministic two-stage sums), and dL/dx a transposed K x K convolution with
 // wx summed over the six directions.
 #include "common.h"
 #include "sweep.h"
@@ -37,7 +38,7 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
     const int p = px / dg.Q, q = px % dg.Q;
     const int s = dg.sign > 0 ? t : dg.T - 1 - t;
     const int sprev = s - dg.sign;
-    const int C = g.C, O = g.O, G = 4 * O;
+    const int C = g.C, O = g.O, G = 4 * O, K = g.K, KK = K * K, rad = K / 2;
     const long long nbase = (long long)n * g.V;
     const long long dbase = (long long)d * g.N * g.V;
 
@@ -45,11 +46,11 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
 #pragma unroll
     for (int k = 0; k < 4; ++k) acc[k] = Store<TS>::load(b, (long long)d * G + k * O + o);
 
-    for (int ka = 0; ka < 3; ++ka) {
-        const int pp = p + ka - 1;
+    for (int ka = 0; ka < K; ++ka) {
+        const int pp = p + ka - rad;
         if (pp < 0 || pp >= dg.P) continue;
-        for (int kb = 0; kb < 3; ++kb) {
-            const int qq = q + kb - 1;
+        for (int kb = 0; kb < K; ++kb) {
+            const int qq = q + kb - rad;
             if (qq < 0 || qq >= dg.Q) continue;
             const long long vin = nbase + s * dg.ss + pp * dg.sp + qq * dg.sq;
             for (int c = 0; c < C; ++c) {
@@ -57,7 +58,7 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
                     acc[k] += xv * Store<TS>::load(
-                        wx, (((long long)d * G + k * O + o) * C + c) * 9 + ka * 3 + kb);
+                        wx, (((long long)d * G + k * O + o) * C + c) * KK + ka * K + kb);
             }
             if (t > 0) {
                 const long long vh = dbase + nbase + sprev * dg.ss + pp * dg.sp + qq * dg.sq;
@@ -66,7 +67,7 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
 #pragma unroll
                     for (int k = 0; k < 4; ++k)
                         acc[k] += hv * Store<TS>::load(
-                            wh, (((long long)d * G + k * O + o) * O + j) * 9 + ka * 3 + kb);
+                            wh, (((long long)d * G + k * O + o) * O + j) * KK + ka * K + kb);
                 }
             }
         }
@@ -114,7 +115,7 @@ k_bwd_step(Geom g, int t, const float *__restrict__ wh, const float *__restrict_
     const int p = px / dg.Q, q = px % dg.Q;
     const int s = dg.sign > 0 ? t : dg.T - 1 - t;
     const int snext = s + dg.sign, sprev = s - dg.sign;
-    const int O = g.O, G = 4 * O;
+    const int O = g.O, G = 4 * O, K = g.K, KK = K * K, rad = K / 2;
     const long long nbase = (long long)n * g.V;
     const long long dbase = (long long)d * g.N * g.V;
     const long long vloc = nbase + s * dg.ss + p * dg.sp + q * dg.sq;
@@ -123,16 +124,17 @@ k_bwd_step(Geom g, int t, const float *__restrict__ wh, const float *__restrict_
 
     float gh = dh[vloc * O + j];
     if (has_next) {
-        // h_t[p][q][j] entered A_{t+1}[p - (ka-1)][q - (kb-1)] through tap (ka, kb).
-        for (int ka = 0; ka < 3; ++ka) {
-            const int pp = p - (ka - 1);
+        // h_t[p][q][j] entered A_{t+1}[p - (ka-r)][q - (kb-r)] through tap (ka, kb).
+        for (int ka = 0; ka < K; ++ka) {
+            const int pp = p - (ka - rad);
             if (pp < 0 || pp >= dg.P) continue;
-            for (int kb = 0; kb < 3; ++kb) {
-                const int qq = q - (kb - 1);
+            for (int kb = 0; kb < K; ++kb) {
+                const int qq = q - (kb - rad);
                 if (qq < 0 || qq >= dg.Q) continue;
                 const long long vn = dbase + nbase + snext * dg.ss + pp * dg.sp + qq * dg.sq;
                 for (int gn = 0; gn < G; ++gn)
-                    gh += dA[vn * G + gn] * wh[(((long long)d * G + gn) * O + j) * 9 + ka * 3 + kb];
+                    gh += dA[vn * G + gn] *
+                          wh[(((long long)d * G + gn) * O + j) * KK + ka * K + kb];
             }
         }
     }
@@ -157,11 +159,12 @@ k_bwd_step(Geom g, int t, const float *__restrict__ wh, const float *__restrict_
 }
 
 // Parameter-gradient partial sums.  For direction d the reduction runs over
-// every voxel (n, t, p, q); column k of the "im2col" row is
-//   k < 9C        : x at tap (ka, kb) = divmod(k / C, 3), channel k % C
-//   9C <= k < 9(C+O): h^d_{t-1} at tap, unit, recomputed as o * tanh(c) of the
-//                   previous plane (0 for t = 0 or outside the plane)
-//   k = 9(C+O)    : 1 (bias)
+// every voxel (n, t, p, q); with KK = K * K taps, column k of the "im2col"
+// row is
+//   k < KK C          : x at tap (ka, kb) = divmod(k / C, K), channel k % C
+//   KK C <= k < KK(C+O): h^d_{t-1} at tap, unit, recomputed as o * tanh(c) of
+//                       the previous plane (0 for t = 0 or outside the plane)
+//   k = KK (C+O)      : 1 (bias)
 // Each block owns a 16 x 16 (gate-unit x column) tile and one chunk of voxels;
 // partial[d][chunk][gn][k].
 constexpr int kTile = 16;
@@ -172,8 +175,8 @@ k_wgrad_partial(Geom g, long long chunk_len, int nchunk, const float *__restrict
                 const float *__restrict__ gates, const float *__restrict__ cell,
                 const float *__restrict__ dA, float *__restrict__ partial)
 {
-    const int C = g.C, O = g.O, G = 4 * O;
-    const int KT = 9 * (C + O) + 1;
+    const int C = g.C, O = g.O, G = 4 * O, K = g.K, KK = K * K, rad = K / 2;
+    const int KT = KK * (C + O) + 1;
     const int d = blockIdx.z / nchunk, chunk = blockIdx.z % nchunk;
     const int k0 = blockIdx.x * kTile, g0 = blockIdx.y * kTile;
     const DirGeom dg = g.dir[d];
@@ -203,15 +206,15 @@ k_wgrad_partial(Geom g, long long chunk_len, int nchunk, const float *__restrict
                 const long long v = nbase + s * dg.ss + p * dg.sp + q * dg.sq;
                 if (g0 + col < G) a = dA[(dbase + v) * G + g0 + col];
                 const int k = k0 + col;
-                if (k < 9 * C) {
+                if (k < KK * C) {
                     const int tap = k / C, c = k % C;
-                    const int pp = p + tap / 3 - 1, qq = q + tap % 3 - 1;
+                    const int pp = p + tap / K - rad, qq = q + tap % K - rad;
                     if (pp >= 0 && pp < dg.P && qq >= 0 && qq < dg.Q)
                         in = x[(nbase + s * dg.ss + pp * dg.sp + qq * dg.sq) * C + c];
-                } else if (k < 9 * (C + O)) {
-                    const int kk = k - 9 * C;
+                } else if (k < KK * (C + O)) {
+                    const int kk = k - KK * C;
                     const int tap = kk / O, j = kk % O;
-                    const int pp = p + tap / 3 - 1, qq = q + tap % 3 - 1;
+                    const int pp = p + tap / K - rad, qq = q + tap % K - rad;
                     if (t > 0 && pp >= 0 && pp < dg.P && qq >= 0 && qq < dg.Q) {
                         const long long vp =
                             dbase + nbase + (s - dg.sign) * dg.ss + pp * dg.sp + qq * dg.sq;
@@ -238,8 +241,8 @@ __global__ void __launch_bounds__(kThreads)
 k_wgrad_reduce(Geom g, int nchunk, const float *__restrict__ partial, float *__restrict__ dwx,
                float *__restrict__ dwh, float *__restrict__ db)
 {
-    const int C = g.C, O = g.O, G = 4 * O;
-    const int KT = 9 * (C + O) + 1;
+    const int C = g.C, O = g.O, G = 4 * O, KK = g.K * g.K;
+    const int KT = KK * (C + O) + 1;
     const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
     if (i >= (long long)kDirs * G * KT) return;
     const int k = (int)(i % KT);
@@ -248,13 +251,13 @@ k_wgrad_reduce(Geom g, int nchunk, const float *__restrict__ partial, float *__r
     float acc = 0.0f;
     for (int ch = 0; ch < nchunk; ++ch)
         acc += partial[(((long long)d * nchunk + ch) * G + gn) * KT + k];
-    if (k < 9 * C) {
+    if (k < KK * C) {
         const int tap = k / C, c = k % C;
-        dwx[(((long long)d * G + gn) * C + c) * 9 + tap] = acc;
-    } else if (k < 9 * (C + O)) {
-        const int kk = k - 9 * C;
+        dwx[(((long long)d * G + gn) * C + c) * KK + tap] = acc;
+    } else if (k < KK * (C + O)) {
+        const int kk = k - KK * C;
         const int tap = kk / O, j = kk % O;
-        dwh[(((long long)d * G + gn) * O + j) * 9 + tap] = acc;
+        dwh[(((long long)d * G + gn) * O + j) * KK + tap] = acc;
     } else {
         db[(long long)d * G + gn] = acc;
     }
@@ -265,7 +268,7 @@ __global__ void __launch_bounds__(kThreads)
 k_dx(Geom g, const float *__restrict__ wx, const float *__restrict__ dA, float *__restrict__ dx)
 {
     const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
-    const int C = g.C, O = g.O, G = 4 * O;
+    const int C = g.C, O = g.O, G = 4 * O, K = g.K, KK = K * K, rad = K / 2;
     if (i >= (long long)g.N * g.V * C) return;
     const int c = (int)(i % C);
     const long long vloc = i / C;
@@ -285,16 +288,16 @@ k_dx(Geom g, const float *__restrict__ wx, const float *__restrict__ dA, float *
         default: s = xw; p = z; q = y; break;
         }
         const long long dbase = (long long)d * g.N * g.V;
-        for (int ka = 0; ka < 3; ++ka) {
-            const int pp = p - (ka - 1);
+        for (int ka = 0; ka < K; ++ka) {
+            const int pp = p - (ka - rad);
             if (pp < 0 || pp >= dg.P) continue;
-            for (int kb = 0; kb < 3; ++kb) {
-                const int qq = q - (kb - 1);
+            for (int kb = 0; kb < K; ++kb) {
+                const int qq = q - (kb - rad);
                 if (qq < 0 || qq >= dg.Q) continue;
                 const long long v = dbase + nbase + s * dg.ss + pp * dg.sp + qq * dg.sq;
                 const float *a = dA + v * G;
-                const float *w = wx + ((long long)d * G * C + c) * 9 + ka * 3 + kb;
-                for (int gn = 0; gn < G; ++gn) acc += a[gn] * w[(long long)gn * C * 9];
+                const float *w = wx + ((long long)d * G * C + c) * KK + ka * K + kb;
+                for (int gn = 0; gn < G; ++gn) acc += a[gn] * w[(long long)gn * C * KK];
             }
         }
     }
@@ -379,7 +382,7 @@ int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st)
 size_t generic_backward_ws(const Geom &g)
 {
     Carve cv(nullptr);
-    const int G = 4 * g.O, KT = 9 * (g.C + g.O) + 1;
+    const int G = 4 * g.O, KT = g.K * g.K * (g.C + g.O) + 1;
     cv.take<float>((size_t)kDirs * g.N * g.V * G);                      // dA
     cv.take<float>((size_t)kDirs * g.N * g.V * g.O);                    // dL/dc
     cv.take<float>((size_t)kDirs * wgrad_chunks(g) * G * KT);           // partials
@@ -391,7 +394,7 @@ int generic_backward(const Geom &g, const float *x, const float *wx, const float
                      float *db, void *ws, hipStream_t st)
 {
     const float *gates = sv.gates, *cell = sv.cell;
-    const int G = 4 * g.O, KT = 9 * (g.C + g.O) + 1;
+    const int G = 4 * g.O, KT = g.K * g.K * (g.C + g.O) + 1;
     Carve cv(ws);
     float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * G);
     float *gc = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);

@@ -94,6 +94,17 @@ __device__ inline int item_dir(const int *base, int item)
     return d;
 }
 
+// In-plane coordinates of a pixel, or kDead past the plane: no tap offset
+// (|offset| <= 3) brings kDead back onto a plane.
+constexpr int kDead = -(1 << 20);
+__device__ inline bool on_plane(int p, int q, int P, int Q)
+{
+    return ((unsigned)p < (unsigned)P) & ((unsigned)q < (unsigned)Q);
+}
+// Tap (ka, kb) of a K x K filter from its index: ka = tap / K with the
+// multiplier k_mul = ceil(2^16 / K) (exact for tap < 2^12).
+__device__ inline int tap_row(int tap, int k_mul) { return (tap * k_mul) >> 16; }
+
 // ---- conversion and repacking (once per call) -------------------------------
 
 // x [N][V][C] (fp32 or bf16) -> xp [N][V][C'] fp32, channels >= C zero.
@@ -114,7 +125,7 @@ k_pad_x(long long nvox, int C, int Cp, const TS *__restrict__ x, float *__restri
 // the weight of gate-unit gate*O + 16 ug + col for channel 16 cb + 4q + i.
 template <typename TS>
 __global__ void __launch_bounds__(256)
-k_pack_fwd(int O, int C, int Cp, int KX, int KG, const TS *__restrict__ wx,
+k_pack_fwd(int O, int C, int Cp, int KX, int KG, int KK, const TS *__restrict__ wx,
            const TS *__restrict__ wh, const TS *__restrict__ b, float *__restrict__ frag,
            float *__restrict__ bias)
 {
@@ -132,10 +143,10 @@ k_pack_fwd(int O, int C, int Cp, int KX, int KG, const TS *__restrict__ wx,
     float v = 0.0f;
     if (kg < KX) {
         const int tap = kg / CX, c = (kg % CX) * 16 + 4 * q + i4;
-        if (c < C) v = Store<TS>::load(wx, (gu * C + c) * 9 + tap);
+        if (c < C) v = Store<TS>::load(wx, (gu * C + c) * KK + tap);
     } else {
         const int kh = kg - KX, tap = kh / U, j = (kh % U) * 16 + 4 * q + i4;
-        v = Store<TS>::load(wh, (gu * O + j) * 9 + tap);
+        v = Store<TS>::load(wh, (gu * O + j) * KK + tap);
     }
     frag[i] = v;
 }
@@ -143,9 +154,9 @@ k_pack_fwd(int O, int C, int Cp, int KX, int KG, const TS *__restrict__ wx,
 // Backward A fragments fragB[d][ug][kg][lane][4], kg = tap * 4U + mb: entry
 // i of lane (q, col) is W_h[d][gate-unit 16 mb + 4q + i][unit 16 ug + col][tap].
 __global__ void __launch_bounds__(256)
-k_pack_bwd(int O, const float *__restrict__ wh, float *__restrict__ frag)
+k_pack_bwd(int O, int KK, const float *__restrict__ wh, float *__restrict__ frag)
 {
-    const int U = O / 16, G = 4 * O, KG = 9 * 4 * U;
+    const int U = O / 16, G = 4 * O, KG = KK * 4 * U;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
     if (i >= (long long)kDirs * U * KG * 256) return;
     const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63);
@@ -156,28 +167,28 @@ k_pack_bwd(int O, const float *__restrict__ wh, float *__restrict__ frag)
     const int tap = kg / (4 * U), mb = kg % (4 * U);
     const int q = lane >> 4, col = lane & 15;
     const long long gu = (long long)d * G + mb * 16 + 4 * q + i4;
-    frag[i] = wh[(gu * O + ug * 16 + col) * 9 + tap];
+    frag[i] = wh[(gu * O + ug * 16 + col) * KK + tap];
 }
 
 // dL/dx A fragments fragX[d][tap][mb][ct][lane][4]: entry i of lane (q, col)
 // is W_x[d][gate-unit 16 mb + 4q + i][channel 16 ct + col][tap] (0 past C).
 __global__ void __launch_bounds__(256)
-k_pack_dx(int O, int C, int CT, const float *__restrict__ wx, float *__restrict__ frag)
+k_pack_dx(int O, int C, int CT, int KK, const float *__restrict__ wx, float *__restrict__ frag)
 {
     const int G = 4 * O, MB = G / 16;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (i >= (long long)kDirs * 9 * MB * CT * 256) return;
+    if (i >= (long long)kDirs * KK * MB * CT * 256) return;
     const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63);
     long long r = i >> 8;
     const int ct = (int)(r % CT);
     r /= CT;
     const int mb = (int)(r % MB);
     r /= MB;
-    const int tap = (int)(r % 9), d = (int)(r / 9);
+    const int tap = (int)(r % KK), d = (int)(r / KK);
     const int q = lane >> 4, col = lane & 15;
     const int c = ct * 16 + col;
     const long long gu = (long long)d * G + mb * 16 + 4 * q + i4;
-    frag[i] = c < C ? wx[(gu * C + c) * 9 + tap] : 0.0f;
+    frag[i] = c < C ? wx[(gu * C + c) * KK + tap] : 0.0f;
 }
 
 // ---- forward step -----------------------------------------------------------
@@ -185,7 +196,8 @@ k_pack_dx(int O, int C, int CT, const float *__restrict__ wx, float *__restrict_
 struct FwdStepArgs {
     Geom g;
     int t;
-    int Cp, KX, KG;           // padded channels, input K-groups (9 C'/16), all K-groups
+    int Cp, KX, KG;           // padded channels, input K-groups (KK C'/16), all K-groups
+    int k_mul;                // ceil(2^16 / K): tap row from tap index
     int cx_mul;               // ceil(2^16 / (C'/16)): division by C'/16
     const float *xp;          // [N][V][C']
     const float *frag;        // [6][U][KG][4][64][4]
@@ -234,26 +246,18 @@ k_step_fwd(FwdStepArgs a)
     const int Cp = a.Cp, CX = Cp >> 4, KX = a.KX;
     const int hoff = -dg.sign * ss;   // voxel of plane t - 1 = voxel of plane t + hoff
     const int uo = ug * 16 + 4 * q4;
+    const int K = a.g.K, rad = K >> 1;
 
-    // this lane's pixel of each tile; bit tap of nbm: the tap's pixel is on
-    // the plane (bit 4: the pixel itself exists)
-    int vox[kNT];
-    unsigned nbm[kNT];
+    // this lane's pixel of each tile: voxel and in-plane coordinates
+    int vox[kNT], tp[kNT], tq[kNT];
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt) {
         const int pix = (pg * kNT + nt) * 16 + col;
         const bool live = pix < P * Q;
         const int p = live ? pix / Q : 0, qq = live ? pix - p * Q : 0;
         vox[nt] = s * ss + p * sp + qq * sq;
-        unsigned m = 0;
-#pragma unroll
-        for (int ka = 0; ka < 3; ++ka)
-#pragma unroll
-            for (int kb = 0; kb < 3; ++kb)
-                m |= (unsigned)(live & ((unsigned)(p + ka - 1) < (unsigned)P) &
-                                ((unsigned)(qq + kb - 1) < (unsigned)Q))
-                     << (ka * 3 + kb);
-        nbm[nt] = m;
+        tp[nt] = live ? p : kDead;
+        tq[nt] = qq;
     }
     const long long sbase = ((long long)d * a.g.N + n) * V;
     const auto rs_x = slice_rsrc(a.xp + (long long)n * V * Cp, V * Cp);
@@ -264,21 +268,21 @@ k_step_fwd(FwdStepArgs a)
     // the tiles this wave finishes and their c_{t-1}, in flight during the
     // contraction
     int evox[NE];
-    unsigned ebits[NE];
+    bool elive[NE];
     f4 cprev[NE];
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
         evox[e] = vox[e];
-        ebits[e] = nbm[e];
+        elive[e] = tp[e] >= 0;
         if (SPLIT) {
 #pragma unroll
             for (int nt = 1; nt < kNT; ++nt)
                 if (wave == nt) {
                     evox[e] = vox[nt];
-                    ebits[e] = nbm[nt];
+                    elive[e] = tp[nt] >= 0;
                 }
         }
-        cprev[e] = bload4(rs_c, sel_off(t > 0 && ((ebits[e] >> 4) & 1),
+        cprev[e] = bload4(rs_c, sel_off(t > 0 && elive[e],
                                         (unsigned)((evox[e] + hoff) * O + uo) * 4u));
     }
 
@@ -301,13 +305,14 @@ k_step_fwd(FwdStepArgs a)
         const int tap = is_x ? (kk * a.cx_mul) >> 16 : kk / U;
         const int cb = kk - tap * (is_x ? CX : U);
         const int stride = is_x ? Cp : O;
-        const int dv = (is_x ? 0 : hoff) + (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
+        const int ka = tap_row(tap, a.k_mul) - rad, kb = tap - (ka + rad) * K - rad;
+        const int dv = (is_x ? 0 : hoff) + ka * sp + kb * sq;
         const auto rs = is_x ? rs_x : rs_h;
 #pragma unroll
         for (int g = 0; g < 4; ++g) o.a[g] = *(const f4 *)(fr + kg * 1024 + g * 256);
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
-            o.b[nt] = bload4(rs, sel_off((nbm[nt] >> tap) & 1,
+            o.b[nt] = bload4(rs, sel_off(on_plane(tp[nt] + ka, tq[nt] + kb, P, Q),
                                          (unsigned)((vox[nt] + dv) * stride + cb * 16 + 4 * q4) *
                                              4u));
     };
@@ -339,7 +344,7 @@ k_step_fwd(FwdStepArgs a)
     // (split partials added in wave order, then the bias)
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-        if (!((ebits[e] >> 4) & 1)) continue;
+        if (!elive[e]) continue;
         f4 pre[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -410,7 +415,7 @@ k_pad_x_b16(long long nvox, int C, int C32, const uint16_t *__restrict__ x,
 // (kg - KX) / (O/32), block (kg - KX) % (O/32).  Entry j of lane (q, col)
 // is the weight of gate-unit gate*O + 16 ug + col for channel 32 cb + 8q + j.
 __global__ void __launch_bounds__(256)
-k_pack_fwd_b16(int O, int C, int C32, int KX, int KG, const uint16_t *__restrict__ wx,
+k_pack_fwd_b16(int O, int C, int C32, int KX, int KG, int KK, const uint16_t *__restrict__ wx,
                const uint16_t *__restrict__ wh, const uint16_t *__restrict__ b,
                uint16_t *__restrict__ frag, float *__restrict__ bias)
 {
@@ -428,10 +433,10 @@ k_pack_fwd_b16(int O, int C, int C32, int KX, int KG, const uint16_t *__restrict
     uint16_t v = 0;
     if (kg < KX) {
         const int tap = kg / CX, c = (kg % CX) * 32 + 8 * q + j8;
-        if (c < C) v = wx[(gu * C + c) * 9 + tap];
+        if (c < C) v = wx[(gu * C + c) * KK + tap];
     } else {
         const int kh = kg - KX, tap = kh / UH, jj = (kh % UH) * 32 + 8 * q + j8;
-        v = wh[(gu * O + jj) * 9 + tap];
+        v = wh[(gu * O + jj) * KK + tap];
     }
     frag[i] = v;
 }
@@ -439,7 +444,8 @@ k_pack_fwd_b16(int O, int C, int C32, int KX, int KG, const uint16_t *__restrict
 struct FwdB16Args {
     Geom g;
     int t;
-    int C32, KX, KG;          // padded channels, input K-groups (9 C32/32), all K-groups
+    int C32, KX, KG;          // padded channels, input K-groups (KK C32/32), all K-groups
+    int k_mul;                // ceil(2^16 / K)
     int cx_mul32;             // ceil(2^16 / (C32/32)): division by C32/32
     const uint16_t *xb;       // [N][V][C32] bf16
     const uint16_t *frag;     // [6][U][KG][4][64][8] bf16
@@ -479,24 +485,17 @@ k_step_fwd_b16(FwdB16Args a)
     const int C32 = a.C32, CX = C32 >> 5, KX = a.KX;
     const int hoff = -dg.sign * ss;
     const int uo = ug * 16 + 4 * q4;
+    const int K = a.g.K, rad = K >> 1;
 
-    int vox[kNT];
-    unsigned nbm[kNT];
+    int vox[kNT], tp[kNT], tq[kNT];
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt) {
         const int pix = (pg * kNT + nt) * 16 + col;
         const bool live = pix < P * Q;
         const int p = live ? pix / Q : 0, qq = live ? pix - p * Q : 0;
         vox[nt] = s * ss + p * sp + qq * sq;
-        unsigned m = 0;
-#pragma unroll
-        for (int ka = 0; ka < 3; ++ka)
-#pragma unroll
-            for (int kb = 0; kb < 3; ++kb)
-                m |= (unsigned)(live & ((unsigned)(p + ka - 1) < (unsigned)P) &
-                                ((unsigned)(qq + kb - 1) < (unsigned)Q))
-                     << (ka * 3 + kb);
-        nbm[nt] = m;
+        tp[nt] = live ? p : kDead;
+        tq[nt] = qq;
     }
     const long long sbase = ((long long)d * a.g.N + n) * V;
     // byte sizes: V * C32 * 2 and V * O * 2 (< 2^31, checked on the host)
@@ -509,21 +508,21 @@ k_step_fwd_b16(FwdB16Args a)
     const uint16_t *fr = a.frag + (long long)(d * U + ug) * a.KG * 2048 + lane * 8;
 
     int evox[NE];
-    unsigned ebits[NE];
+    bool elive[NE];
     f4 cprev[NE];
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
         evox[e] = vox[e];
-        ebits[e] = nbm[e];
+        elive[e] = tp[e] >= 0;
         if (SPLIT) {
 #pragma unroll
             for (int nt = 1; nt < kNT; ++nt)
                 if (wave == nt) {
                     evox[e] = vox[nt];
-                    ebits[e] = nbm[nt];
+                    elive[e] = tp[nt] >= 0;
                 }
         }
-        cprev[e] = bload4(rs_c, sel_off(t > 0 && ((ebits[e] >> 4) & 1),
+        cprev[e] = bload4(rs_c, sel_off(t > 0 && elive[e],
                                         (unsigned)((evox[e] + hoff) * O + uo) * 4u));
     }
 
@@ -543,13 +542,14 @@ k_step_fwd_b16(FwdB16Args a)
         const int tap = is_x ? (kk * a.cx_mul32) >> 16 : kk / UH;
         const int cb = kk - tap * (is_x ? CX : UH);
         const int stride = is_x ? C32 : O;
-        const int dv = (is_x ? 0 : hoff) + (tap / 3 - 1) * sp + (tap % 3 - 1) * sq;
+        const int ka = tap_row(tap, a.k_mul) - rad, kb = tap - (ka + rad) * K - rad;
+        const int dv = (is_x ? 0 : hoff) + ka * sp + kb * sq;
         const auto rs = is_x ? rs_x : rs_h;
 #pragma unroll
         for (int g = 0; g < 4; ++g) o.a[g] = *(const bf8 *)(fr + (kg * 4 + g) * 512);
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
-            o.b[nt] = bload8h(rs, sel_off((nbm[nt] >> tap) & 1,
+            o.b[nt] = bload8h(rs, sel_off(on_plane(tp[nt] + ka, tq[nt] + kb, P, Q),
                                           (unsigned)((vox[nt] + dv) * stride + cb * 32 + 8 * q4) *
                                               2u));
     };
@@ -575,7 +575,7 @@ k_step_fwd_b16(FwdB16Args a)
 
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-        if (!((ebits[e] >> 4) & 1)) continue;
+        if (!elive[e]) continue;
         f4 pre[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -609,7 +609,8 @@ k_step_fwd_b16(FwdB16Args a)
 struct BwdStepArgs {
     Geom g;
     int t;
-    const float *frag;        // [6][U][9 * 4U][64][4]
+    const float *frag;        // [6][U][KK * 4U][64][4]
+    int k_mul;                // ceil(2^16 / K)
     const float *gates, *cell, *dh;
     float *dA;                // [6][N][V][4O]
     float *gcf;               // [6][N][V][O]: dL/dc_t * f_t
@@ -628,7 +629,7 @@ template <int U, bool SPLIT>
 __global__ void __launch_bounds__(64 * kSW)
 k_step_bwd(BwdStepArgs a)
 {
-    constexpr int O = 16 * U, G = 4 * O, MB = 4 * U, KG = 9 * MB;
+    constexpr int O = 16 * U, G = 4 * O, MB = 4 * U;
     constexpr int KS = SPLIT ? kSW : 1;
     constexpr int NE = SPLIT ? 1 : kNT;
     static_assert(kNT == kSW, "wave w finishes tile w");
@@ -649,26 +650,19 @@ k_step_bwd(BwdStepArgs a)
     const long long V = a.g.V;
     const bool has_next = t + 1 < dg.T;
     const int noff = dg.sign * ss;    // voxel of plane t + 1 = voxel of plane t + noff
+    const int K = a.g.K, rad = K >> 1, KG = K * K * MB;
 
-    // bit tap of nbm: the pixel that received this pixel's h through tap
-    // (p - (ka - 1), q - (kb - 1)) is on the plane
-    int vox[kNT];
-    unsigned nbm[kNT];
+    // this lane's pixel of each tile: voxel and in-plane coordinates (the
+    // pixels that received its h through tap (ka, kb) are (p - ka + r, q - kb + r))
+    int vox[kNT], tp[kNT], tq[kNT];
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt) {
         const int pix = (pg * kNT + nt) * 16 + col;
         const bool live = pix < P * Q;
         const int p = live ? pix / Q : 0, qq = live ? pix - p * Q : 0;
         vox[nt] = s * ss + p * sp + qq * sq;
-        unsigned m = 0;
-#pragma unroll
-        for (int ka = 0; ka < 3; ++ka)
-#pragma unroll
-            for (int kb = 0; kb < 3; ++kb)
-                m |= (unsigned)(live & ((unsigned)(p - ka + 1) < (unsigned)P) &
-                                ((unsigned)(qq - kb + 1) < (unsigned)Q))
-                     << (ka * 3 + kb);
-        nbm[nt] = m;
+        tp[nt] = live ? p : kDead;
+        tq[nt] = qq;
     }
     const long long sbase = ((long long)d * a.g.N + n) * V;
     const auto rs_dA = slice_rsrc(a.dA + sbase * G, V * G);
@@ -689,10 +683,11 @@ k_step_bwd(BwdStepArgs a)
             const int tap = kg / MB, mb = kg - tap * MB;
 #pragma unroll
             for (int u = 0; u < U; ++u) o.a[u] = *(const f4 *)(fr + ((long long)u * KG + kg) * 256);
-            const int dv = noff - (tap / 3 - 1) * sp - (tap % 3 - 1) * sq;
+            const int ka = tap_row(tap, a.k_mul) - rad, kb = tap - (ka + rad) * K - rad;
+            const int dv = noff - ka * sp - kb * sq;
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
-                o.b[nt] = bload4(rs_dA, sel_off((nbm[nt] >> tap) & 1,
+                o.b[nt] = bload4(rs_dA, sel_off(on_plane(tp[nt] - ka, tq[nt] - kb, P, Q),
                                                 (unsigned)((vox[nt] + dv) * G + mb * 16 + 4 * q4) *
                                                     4u));
         };
@@ -722,16 +717,16 @@ k_step_bwd(BwdStepArgs a)
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
         int evox = vox[e];
-        unsigned ebits = nbm[e];
+        bool elive = tp[e] >= 0;
         if (SPLIT) {
 #pragma unroll
             for (int nt = 1; nt < kNT; ++nt)
                 if (wave == nt) {
                     evox = vox[nt];
-                    ebits = nbm[nt];
+                    elive = tp[nt] >= 0;
                 }
         }
-        if (!((ebits >> 4) & 1)) continue;
+        if (!elive) continue;
         const long long vo = sbase + evox;
         const float *dhp = a.dh + ((long long)n * V + evox) * O;
 #pragma unroll
@@ -791,10 +786,10 @@ struct WgBlocks {
     int nh, nx;       // blocks of each part
     int th, tx;       // tiles per block of each part (last block may have fewer)
 };
-__host__ __device__ inline WgBlocks wg_blocks(int U, int CX)
+__host__ __device__ inline WgBlocks wg_blocks(int U, int CX, int KK)
 {
     WgBlocks w;
-    const int h = 9 * U, x = 9 * CX + 1;
+    const int h = KK * U, x = KK * CX + 1;
     w.nh = (h + kWgN - 1) / kWgN;
     w.nx = (x + kWgN - 1) / kWgN;
     w.th = (h + w.nh - 1) / w.nh;
@@ -805,7 +800,8 @@ __host__ __device__ inline WgBlocks wg_blocks(int U, int CX)
 struct WgStepArgs {
     Geom g;
     int Cp;
-    int NTt;                  // N-tiles: 9U + 9C'/16 + 1
+    int NTt;                  // N-tiles: KK U + KK C'/16 + 1
+    int k_mul;                // ceil(2^16 / K)
     int kch;                  // voxel chunks per (direction, M-block, N-block)
     const float *xp, *hd, *dA;
     float *partial;           // [6][kch][4O][16 NTt]
@@ -819,7 +815,8 @@ k_wgrad_step(WgStepArgs a)
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
     const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int Cp = a.Cp, CX = Cp >> 4;
-    const WgBlocks wb = wg_blocks(U, CX);
+    const int K = a.g.K, KK = K * K, rad = K >> 1;
+    const WgBlocks wb = wg_blocks(U, CX, KK);
     const int nblk = wb.nh + wb.nx;
     const int per_dir = U * nblk * a.kch;
     if (item >= kDirs * per_dir) return;
@@ -832,9 +829,9 @@ k_wgrad_step(WgStepArgs a)
     // first N-tile and tile count of this block; tiles of the x part are
     // numbered from 0 after the h part
     const int t0 = is_h ? nb * wb.th : (nb - wb.nh) * wb.tx;
-    const int tend = is_h ? 9 * U : 9 * CX + 1;
+    const int tend = is_h ? KK * U : KK * CX + 1;
     const int ntl = (t0 + (is_h ? wb.th : wb.tx) < tend ? (is_h ? wb.th : wb.tx) : tend - t0);
-    const int first_nt = (is_h ? 0 : 9 * U) + t0;
+    const int first_nt = (is_h ? 0 : KK * U) + t0;
     const DirGeom dg = a.g.dir[d];
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
     const int P = dg.P, Q = dg.Q;
@@ -850,19 +847,20 @@ k_wgrad_step(WgStepArgs a)
 #pragma unroll
     for (int j = 0; j < kWgN; ++j) {
         const int tt = t0 + j;
-        const bool bias = !is_h && tt == 9 * CX;
-        const int tap = bias || j >= ntl ? 4 : tt / cbn;
-        dtap[j] = __builtin_amdgcn_readfirstlane((tap / 3 - 1) * sp + (tap % 3 - 1) * sq);
+        const bool bias = !is_h && tt == KK * CX;
+        const int tap = bias || j >= ntl ? KK / 2 : tt / cbn;
+        const int ka = tap / K - rad, kb = tap % K - rad;
+        dtap[j] = __builtin_amdgcn_readfirstlane(ka * sp + kb * sq);
         chn[j] = (bias || j >= ntl) ? -1 : (tt % cbn) * 16 + col;
         one[j] = (bias && col == 0) ? 1.0f : 0.0f;
         (void)tap;
     }
-    unsigned tapok[kWgN];   // per tile: row and column offsets + 1, packed
+    unsigned tapok[kWgN];   // per tile: tap row and column (3 bits each), packed
 #pragma unroll
     for (int j = 0; j < kWgN; ++j) {
         const int tt = t0 + j;
-        const int tap = (!is_h && tt == 9 * CX) || j >= ntl ? 4 : tt / cbn;
-        tapok[j] = __builtin_amdgcn_readfirstlane((tap / 3) | (tap % 3) << 2);
+        const int tap = (!is_h && tt == KK * CX) || j >= ntl ? KK / 2 : tt / cbn;
+        tapok[j] = __builtin_amdgcn_readfirstlane((tap / K) | (tap % K) << 3);
     }
 
     f4 acc[4][kWgN];
@@ -925,7 +923,7 @@ k_wgrad_step(WgStepArgs a)
             const int vb = pl * ss + c.p * sp + qq * sq;
 #pragma unroll
             for (int j = 0; j < kWgN; ++j) {
-                const int pp = c.p + (int)(tapok[j] & 3) - 1, qn = qq + (int)(tapok[j] >> 2) - 1;
+                const int pp = c.p + (int)(tapok[j] & 7) - rad, qn = qq + (int)(tapok[j] >> 3) - rad;
                 const bool ok = src_ok & (chn[j] >= 0) & ((unsigned)pp < (unsigned)P) &
                                 ((unsigned)qn < (unsigned)Q);
                 o.b[ks][j] =
@@ -965,23 +963,24 @@ k_wgrad_step(WgStepArgs a)
 
 // dW = sum of the chunk partials in chunk order, scattered to the ABI layouts.
 __global__ void __launch_bounds__(256)
-k_wgrad_step_reduce(int O, int C, int Cp, int NTt, int kch, const float *__restrict__ partial,
-                    float *__restrict__ dwx, float *__restrict__ dwh, float *__restrict__ db)
+k_wgrad_step_reduce(int O, int C, int Cp, int KK, int NTt, int kch,
+                    const float *__restrict__ partial, float *__restrict__ dwx,
+                    float *__restrict__ dwh, float *__restrict__ db)
 {
-    const int G = 4 * O, KC = 9 * (O + Cp) + 1, KCp = NTt * 16;
+    const int G = 4 * O, KC = KK * (O + Cp) + 1, KCp = NTt * 16;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
     if (i >= (long long)kDirs * G * KC) return;
     const int k = (int)(i % KC);
     const int gu = (int)((i / KC) % G);
     const int d = (int)(i / ((long long)KC * G));
-    if (k >= 9 * O && k < 9 * (O + Cp) && (k - 9 * O) % Cp >= C) return;   // padding channel
+    if (k >= KK * O && k < KK * (O + Cp) && (k - KK * O) % Cp >= C) return;   // padding channel
     float acc = 0.0f;
     for (int c = 0; c < kch; ++c) acc += partial[(((long long)d * kch + c) * G + gu) * KCp + k];
-    if (k < 9 * O) {
-        dwh[(((long long)d * G + gu) * O + k % O) * 9 + k / O] = acc;
-    } else if (k < 9 * (O + Cp)) {
-        const int kx = k - 9 * O;
-        dwx[(((long long)d * G + gu) * C + kx % Cp) * 9 + kx / Cp] = acc;
+    if (k < KK * O) {
+        dwh[(((long long)d * G + gu) * O + k % O) * KK + k / O] = acc;
+    } else if (k < KK * (O + Cp)) {
+        const int kx = k - KK * O;
+        dwx[(((long long)d * G + gu) * C + kx % Cp) * KK + kx / Cp] = acc;
     } else {
         db[(long long)d * G + gu] = acc;
     }
@@ -994,7 +993,8 @@ k_wgrad_step_reduce(int O, int C, int Cp, int NTt, int kch, const float *__restr
 struct DxStepArgs {
     Geom g;
     int CT;
-    const float *frag;        // [6][9][4U][CT][64][4]
+    const float *frag;        // [6][KK][4U][CT][64][4]
+    int k_mul;                // ceil(2^16 / K)
     const float *dA;          // [6][N][V][4O]
     float *dx;                // [N][V][C]
     int nvg;                  // voxel groups (kNT tiles) per batch element
@@ -1004,10 +1004,11 @@ template <int U, int CT>
 __global__ void __launch_bounds__(64 * kSW)
 k_dx_step(DxStepArgs a)
 {
-    constexpr int O = 16 * U, G = 4 * O, MB = 4 * U, KG = 9 * MB;
+    constexpr int O = 16 * U, G = 4 * O, MB = 4 * U;
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
     const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (item >= a.g.N * a.nvg) return;
+    const int K = a.g.K, rad = K >> 1, KG = K * K * MB;
     const int n = item / a.nvg, vg = item - n * a.nvg;
     const long long V = a.g.V;
     const int H = a.g.H, W = a.g.W, C = a.g.C;
@@ -1035,33 +1036,26 @@ k_dx_step(DxStepArgs a)
     for (int d = 0; d < kDirs; ++d) {
         const DirGeom dg = a.g.dir[d];
         const int sp = (int)dg.sp, sq = (int)dg.sq, P = dg.P, Q = dg.Q;
-        // in-plane coordinates of each voxel for this direction; bit tap:
-        // the pixel (p - (ka - 1), q - (kb - 1)) is on the plane
-        unsigned nbm[kNT];
+        // in-plane coordinates of each voxel for this direction (the pixel
+        // (p - ka + r, q - kb + r) received x through tap (ka, kb))
+        int tp[kNT], tq[kNT];
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) {
-            const int p = d < 2 ? yc[nt] : zc[nt];
-            const int q = d < 4 ? xc[nt] : yc[nt];
-            unsigned m = 0;
-#pragma unroll
-            for (int ka = 0; ka < 3; ++ka)
-#pragma unroll
-                for (int kb = 0; kb < 3; ++kb)
-                    m |= (unsigned)((vv[nt] >= 0) & ((unsigned)(p - ka + 1) < (unsigned)P) &
-                                    ((unsigned)(q - kb + 1) < (unsigned)Q))
-                         << (ka * 3 + kb);
-            nbm[nt] = m;
+            tp[nt] = vv[nt] >= 0 ? (d < 2 ? yc[nt] : zc[nt]) : kDead;
+            tq[nt] = d < 4 ? xc[nt] : yc[nt];
         }
         const auto rs = slice_rsrc(a.dA + ((long long)d * a.g.N + n) * V * G, V * G);
         const float *fr = a.frag + (long long)d * KG * CT * 256 + lane * 4;
         auto load = [&](int tap, int mb, Ops &o) {
             const int kg = tap * MB + mb;
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct) o.a[ct] = *(const f4 *)(fr + ((long long)kg * CT + ct) * 256);
-            const int dv = -(tap / 3 - 1) * sp - (tap % 3 - 1) * sq;
+            for (int ct = 0; ct < CT; ++ct)
+                o.a[ct] = *(const f4 *)(fr + ((long long)kg * CT + ct) * 256);
+            const int ka = tap_row(tap, a.k_mul) - rad, kb = tap - (ka + rad) * K - rad;
+            const int dv = -ka * sp - kb * sq;
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
-                o.b[nt] = bload4(rs, sel_off((nbm[nt] >> tap) & 1,
+                o.b[nt] = bload4(rs, sel_off(on_plane(tp[nt] - ka, tq[nt] - kb, P, Q),
                                              (unsigned)((vv[nt] + dv) * G + mb * 16 + 4 * q4) * 4u));
         };
         Ops cur, nxt;
@@ -1110,6 +1104,7 @@ inline int pad16(int c) { return (c + 15) / 16 * 16; }
 inline unsigned blocks_for(long long n, int per) { return (unsigned)((n + per - 1) / per); }
 
 inline int npg_of(const DirGeom &dg) { return (dg.P * dg.Q + 16 * kNT - 1) / (16 * kNT); }
+inline int k_mul_of(const Geom &g) { return (65536 + g.K - 1) / g.K; }
 inline int max_T(const Geom &g)
 {
     int m = 0;
@@ -1122,10 +1117,10 @@ struct WgShape {
 };
 inline WgShape wg_shape(const Geom &g)
 {
-    const int U = g.O / 16, CX = pad16(g.C) / 16;
-    const WgBlocks wb = wg_blocks(U, CX);
+    const int U = g.O / 16, CX = pad16(g.C) / 16, KK = g.K * g.K;
+    const WgBlocks wb = wg_blocks(U, CX, KK);
     WgShape w;
-    w.NTt = 9 * U + 9 * CX + 1;
+    w.NTt = KK * U + KK * CX + 1;
     w.nblk = wb.nh + wb.nx;
     const int per = U * w.nblk;
     w.kch = kWgTarget / per > 1 ? kWgTarget / per : 1;
@@ -1215,6 +1210,7 @@ int g_step_bf16_mfma = 1;
 bool step_supported(const Geom &g)
 {
     if (g.O != 16 && g.O != 32 && g.O != 64) return false;
+    if (g.K < 1 || g.K > 7 || g.K % 2 == 0) return false;
     const long long Cp = pad16(g.C);
     if (Cp > 64) return false;
     // slices addressed through buffer resources: byte sizes fit 31 bits
@@ -1235,14 +1231,14 @@ inline int pad32(int c) { return (c + 31) / 32 * 32; }
 
 size_t step_fwd_ws(const Geom &g)
 {
-    const int U = g.O / 16, Cp = pad16(g.C), KG = 9 * (Cp + g.O) / 16;
+    const int U = g.O / 16, Cp = pad16(g.C), KK = g.K * g.K, KG = KK * (Cp + g.O) / 16;
     Carve cv(nullptr);
     cv.take<float>((size_t)g.N * g.V * Cp);          // padded x
     cv.take<float>((size_t)kDirs * U * KG * 1024);   // A fragments
     cv.take<float>((size_t)kDirs * 4 * g.O);         // bias
     size_t need = cv.off;
     if (g.O % 32 == 0) {                             // bf16 variant
-        const int C32 = pad32(g.C), KGb = 9 * (C32 + g.O) / 32;
+        const int C32 = pad32(g.C), KGb = KK * (C32 + g.O) / 32;
         Carve cb(nullptr);
         cb.take<uint16_t>((size_t)g.N * g.V * C32);
         cb.take<uint16_t>((size_t)kDirs * U * KGb * 2048);
@@ -1280,7 +1276,7 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
                         hipStream_t st)
 {
     const int U = g.O / 16, C32 = pad32(g.C);
-    const int KX = 9 * C32 / 32, KG = KX + 9 * g.O / 32;
+    const int KK = g.K * g.K, KX = KK * C32 / 32, KG = KX + KK * g.O / 32;
     Carve cv(ws);
     uint16_t *xb = cv.take<uint16_t>((size_t)g.N * g.V * C32);
     uint16_t *frag = cv.take<uint16_t>((size_t)kDirs * U * KG * 2048);
@@ -1291,13 +1287,14 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     timing_begin("sweep_fwd_step_bf16", st);
     k_pad_x_b16<<<blocks_for(nvox * C32, 256), 256, 0, st>>>(nvox, g.C, C32, x, xb);
     PLSTM_LAUNCH_CHECK();
-    k_pack_fwd_b16<<<blocks_for(nfrag, 256), 256, 0, st>>>(g.O, g.C, C32, KX, KG, wx, wh, b,
+    k_pack_fwd_b16<<<blocks_for(nfrag, 256), 256, 0, st>>>(g.O, g.C, C32, KX, KG, KK, wx, wh, b,
                                                            frag, bias);
     PLSTM_LAUNCH_CHECK();
     FwdB16Args a;
     a.g = g;
     a.C32 = C32; a.KX = KX; a.KG = KG;
     a.cx_mul32 = (65536 + C32 / 32 - 1) / (C32 / 32);
+    a.k_mul = k_mul_of(g);
     a.xb = xb; a.frag = frag; a.bias = bias;
     a.hd = hd; a.cell = cell; a.hb = hb;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
@@ -1315,7 +1312,7 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
         return step_fwd_b16(g, (const uint16_t *)x, (const uint16_t *)wx, (const uint16_t *)wh,
                             (const uint16_t *)b, hd, cell, ws, st);
     const int U = g.O / 16, Cp = pad16(g.C);
-    const int KX = 9 * Cp / 16, KG = KX + 9 * U;
+    const int KK = g.K * g.K, KX = KK * Cp / 16, KG = KX + KK * U;
     Carve cv(ws);
     float *xp = cv.take<float>((size_t)g.N * g.V * Cp);
     float *frag = cv.take<float>((size_t)kDirs * U * KG * 1024);
@@ -1329,14 +1326,14 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
                                                                       (const uint16_t *)x, xp);
         PLSTM_LAUNCH_CHECK();
         k_pack_fwd<uint16_t><<<blocks_for(nfrag, 256), 256, 0, st>>>(
-            g.O, g.C, Cp, KX, KG, (const uint16_t *)wx, (const uint16_t *)wh,
+            g.O, g.C, Cp, KX, KG, KK, (const uint16_t *)wx, (const uint16_t *)wh,
             (const uint16_t *)b, frag, bias);
     } else {
         k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
                                                                    (const float *)x, xp);
         PLSTM_LAUNCH_CHECK();
         k_pack_fwd<float><<<blocks_for(nfrag, 256), 256, 0, st>>>(
-            g.O, g.C, Cp, KX, KG, (const float *)wx, (const float *)wh, (const float *)b, frag,
+            g.O, g.C, Cp, KX, KG, KK, (const float *)wx, (const float *)wh, (const float *)b, frag,
             bias);
     }
     PLSTM_LAUNCH_CHECK();
@@ -1345,6 +1342,7 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     a.g = g;
     a.Cp = Cp; a.KX = KX; a.KG = KG;
     a.cx_mul = (65536 + Cp / 16 - 1) / (Cp / 16);
+    a.k_mul = k_mul_of(g);
     a.xp = xp; a.frag = frag; a.bias = bias;
     a.hd = hd; a.cell = cell; a.gates = gates;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
@@ -1361,15 +1359,15 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
 
 size_t step_bwd_ws(const Geom &g)
 {
-    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O;
+    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O, KK = g.K * g.K;
     const WgShape w = wg_shape(g);
     Carve cv(nullptr);
     cv.take<float>((size_t)kDirs * g.N * g.V * G);                 // dA
     cv.take<float>((size_t)kDirs * g.N * g.V * g.O);               // dL/dc * f
-    cv.take<float>((size_t)kDirs * U * 9 * 4 * U * 256);           // W_h^T fragments
+    cv.take<float>((size_t)kDirs * U * KK * 4 * U * 256);          // W_h^T fragments
     cv.take<float>((size_t)g.N * g.V * Cp);                        // padded x
     cv.take<float>((size_t)kDirs * w.kch * G * w.NTt * 16);        // weight-gradient partials
-    cv.take<float>((size_t)kDirs * 9 * 4 * U * (Cp / 16) * 256);   // W_x^T fragments
+    cv.take<float>((size_t)kDirs * KK * 4 * U * (Cp / 16) * 256);  // W_x^T fragments
     return cv.off;
 }
 
@@ -1379,14 +1377,16 @@ int step_dx(const Geom &g, const float *wx, const float *dA, float *fragx, float
             hipStream_t st)
 {
     const int U = g.O / 16, CT = pad16(g.C) / 16;
-    const long long nf = (long long)kDirs * 9 * 4 * U * CT * 256;
+    const int KK = g.K * g.K;
+    const long long nf = (long long)kDirs * KK * 4 * U * CT * 256;
     timing_begin("dx_step", st);
-    k_pack_dx<<<blocks_for(nf, 256), 256, 0, st>>>(g.O, g.C, CT, wx, fragx);
+    k_pack_dx<<<blocks_for(nf, 256), 256, 0, st>>>(g.O, g.C, CT, KK, wx, fragx);
     PLSTM_LAUNCH_CHECK();
     DxStepArgs a;
     a.g = g;
     a.CT = CT;
     a.frag = fragx;
+    a.k_mul = k_mul_of(g);
     a.dA = dA;
     a.dx = dx;
     a.nvg = (int)((g.V + 16 * kNT - 1) / (16 * kNT));
@@ -1404,7 +1404,7 @@ int step_dx(const Geom &g, const float *wx, const float *dA, float *fragx, float
 size_t step_dx_ws(const Geom &g)
 {
     Carve cv(nullptr);
-    cv.take<float>((size_t)kDirs * 9 * 4 * (g.O / 16) * (pad16(g.C) / 16) * 256);
+    cv.take<float>((size_t)kDirs * g.K * g.K * 4 * (g.O / 16) * (pad16(g.C) / 16) * 256);
     return cv.off;
 }
 
@@ -1413,23 +1413,25 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
              hipStream_t st)
 {
     if (!step_supported(g)) return PLSTM_EUNSUPPORTED;
-    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O;
+    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O, KK = g.K * g.K;
     const WgShape w = wg_shape(g);
     Carve cv(ws);
     float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * G);
     float *gcf = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
-    float *frag = cv.take<float>((size_t)kDirs * U * 9 * 4 * U * 256);
+    float *frag = cv.take<float>((size_t)kDirs * U * KK * 4 * U * 256);
     float *xp = cv.take<float>((size_t)g.N * g.V * Cp);
     float *partial = cv.take<float>((size_t)kDirs * w.kch * G * w.NTt * 16);
-    float *fragx = cv.take<float>((size_t)kDirs * 9 * 4 * U * (Cp / 16) * 256);
+    float *fragx = cv.take<float>((size_t)kDirs * KK * 4 * U * (Cp / 16) * 256);
     const long long nvox = (long long)g.N * g.V;
 
     timing_begin("sweep_bwd_step", st);
-    k_pack_bwd<<<blocks_for((long long)kDirs * U * 36 * U * 256, 256), 256, 0, st>>>(g.O, wh, frag);
+    k_pack_bwd<<<blocks_for((long long)kDirs * U * KK * 4 * U * 256, 256), 256, 0, st>>>(
+        g.O, KK, wh, frag);
     PLSTM_LAUNCH_CHECK();
     BwdStepArgs a;
     a.g = g;
     a.frag = frag;
+    a.k_mul = k_mul_of(g);
     a.gates = sv.gates; a.cell = sv.cell; a.dh = dh;
     a.dA = dA; a.gcf = gcf;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
@@ -1451,6 +1453,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     wa.NTt = w.NTt; wa.kch = w.kch;
     wa.xp = xp; wa.hd = sv.hd; wa.dA = dA;
     wa.partial = partial;
+    wa.k_mul = k_mul_of(g);
     const long long witems = (long long)kDirs * U * w.nblk * w.kch;
     switch (U) {
     case 1: k_wgrad_step<1><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
@@ -1458,8 +1461,8 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     default: k_wgrad_step<4><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
     }
     PLSTM_LAUNCH_CHECK();
-    const long long nout = (long long)kDirs * G * (9 * (g.O + Cp) + 1);
-    k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.O, g.C, Cp, w.NTt, w.kch,
+    const long long nout = (long long)kDirs * G * (KK * (g.O + Cp) + 1);
+    k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.O, g.C, Cp, KK, w.NTt, w.kch,
                                                                partial, dwx, dwh, db);
     PLSTM_LAUNCH_CHECK();
     timing_end(3, st);

@@ -20,18 +20,22 @@ from . import (plstm_shape, pyramid_fc_tanh_backward, pyramid_fc_tanh_forward,
 
 @dataclass
 class LayerW:
-    wx: torch.Tensor      # [6][4O][C][3][3]
-    wh: torch.Tensor      # [6][4O][O][3][3]
+    wx: torch.Tensor      # [6][4O][C][K][K]
+    wh: torch.Tensor      # [6][4O][O][K][K]
     b: torch.Tensor       # [6][4O]
 
     @property
     def O(self):
         return self.wh.shape[2]
 
+    @property
+    def K(self):
+        return self.wh.shape[-1]
+
 
 def layer_forward(x: torch.Tensor, L: LayerW, training: bool = False, ws=None, stream=None):
     """One layer; returns (h, saved or None)."""
-    s = shape_for(x, L.O)
+    s = shape_for(x, L.O, L.K)
     h = torch.empty(x.shape[:-1] + (L.O,), dtype=x.dtype, device=x.device)
     saved = None
     if training:
@@ -41,7 +45,7 @@ def layer_forward(x: torch.Tensor, L: LayerW, training: bool = False, ws=None, s
 
 
 def layer_backward(x, L: LayerW, saved, dh, want_dx=True, ws=None, stream=None):
-    s = shape_for(x, L.O)
+    s = shape_for(x, L.O, L.K)
     dx = torch.empty_like(x) if want_dx else None
     dwx, dwh, db = (torch.empty_like(t, dtype=torch.float32) for t in (L.wx, L.wh, L.b))
     pyramid_lstm_backward(s, x, L.wx, L.wh, L.b, saved, dh, dx, dwx, dwh, db, ws, stream)
@@ -49,13 +53,22 @@ def layer_backward(x, L: LayerW, saved, dh, want_dx=True, ws=None, stream=None):
 
 
 def workspace_for(x_shape, hidden: List[int], fc: bool, dtype, training: bool, device):
-    """One workspace big enough for every layer of a network."""
-    need = 256
-    C = x_shape[-1]
+    """One workspace big enough for every layer of a network whose FC layers
+    are twice as wide as the layer before (3 x 3 filters)."""
+    shapes, C = [], x_shape[-1]
     for O in hidden:
-        s = plstm_shape(*x_shape[:-1], C, O, 0 if dtype == torch.float32 else 1)
-        need = max(need, pyramid_lstm_workspace_size(s, int(training)))
+        shapes.append((C, O, 3))
         C = 2 * O if fc else O
+    return workspace_for_layers(x_shape, shapes, dtype, training, device)
+
+
+def workspace_for_layers(x_shape, shapes, dtype, training: bool, device):
+    """One workspace big enough for layers of (input channels, hidden units,
+    filter size) `shapes` over the volume of `x_shape`."""
+    need = 256
+    for C, O, K in shapes:
+        s = plstm_shape(*x_shape[:-1], C, O, 0 if dtype == torch.float32 else 1, K)
+        need = max(need, pyramid_lstm_workspace_size(s, int(training)))
     return torch.empty(need, dtype=torch.uint8, device=device)
 
 
@@ -66,14 +79,21 @@ def network_forward(x, layers: List[LayerW], fcs: List[Tuple[torch.Tensor, torch
     'acts' (per-layer inputs/outputs and saved activations for training)."""
     N, D, H, W, _ = x.shape
     M = N * D * H * W
+    if len(fcs) not in (len(layers), len(layers) - 1):
+        raise ValueError("one hidden FC layer per PyraMiD-LSTM layer, or none after the last")
     a = x
     acts = []
-    for L, (wf, bf) in zip(layers, fcs):
+    for li, L in enumerate(layers):
         h, saved = layer_forward(a, L, training, ws, stream)
-        y = torch.empty((N, D, H, W, wf.shape[0]), dtype=a.dtype, device=a.device)
-        pyramid_fc_tanh_forward(h.view(M, -1), wf, bf, y.view(M, -1), stream)
-        acts.append({"in": a, "h": h, "y": y, "saved": saved})
-        a = y
+        act = {"in": a, "h": h, "saved": saved}
+        a = h
+        if li < len(fcs):
+            wf, bf = fcs[li]
+            y = torch.empty((N, D, H, W, wf.shape[0]), dtype=a.dtype, device=a.device)
+            pyramid_fc_tanh_forward(h.view(M, -1), wf, bf, y.view(M, -1), stream)
+            act["y"] = y
+            a = y
+        acts.append(act)
     K = head[0].shape[0]
     p = torch.empty((M, K), dtype=torch.float32, device=x.device)
     out = {"p": p, "acts": acts}
@@ -104,7 +124,8 @@ def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None, fused
     M = N * D * H * W
     nl = len(layers)
     O_last, F_last, K = layers[-1].O, fcs[-1][0].shape[0], head[0].shape[0]
-    if not (fused_head and pyramid_head_workspace_size(M, O_last, F_last, K) > 0):
+    if not (fused_head and len(fcs) == nl and
+            pyramid_head_workspace_size(M, O_last, F_last, K) > 0):
         return _train_step_unfused(x, layers, fcs, head, labels, ws, stream)
     a = x
     acts = []
@@ -158,14 +179,17 @@ def _train_step_unfused(x, layers, fcs, head, labels, ws=None, stream=None):
     fc_grads = [None] * len(fcs)
     layer_grads = [None] * len(layers)
     for li in range(len(layers) - 1, -1, -1):
-        wf, _ = fcs[li]
         act = acts[li]
         O = act["h"].shape[-1]
-        dh = torch.empty((M, O), dtype=torch.float32, device=x.device)
-        dwf, dbf = torch.empty_like(wf), torch.empty(wf.shape[0], device=x.device)
-        pyramid_fc_tanh_backward(act["h"].view(M, O), wf, act["y"].view(M, -1), g.view(M, -1),
-                                 dh, dwf, dbf, stream=stream)
-        fc_grads[li] = (dwf, dbf)
+        if li < len(fcs):
+            wf, _ = fcs[li]
+            dh = torch.empty((M, O), dtype=torch.float32, device=x.device)
+            dwf, dbf = torch.empty_like(wf), torch.empty(wf.shape[0], device=x.device)
+            pyramid_fc_tanh_backward(act["h"].view(M, O), wf, act["y"].view(M, -1),
+                                     g.view(M, -1), dh, dwf, dbf, stream=stream)
+            fc_grads[li] = (dwf, dbf)
+        else:
+            dh = g      # the output layer reads h directly
         dx, dwx, dwh, db = layer_backward(act["in"], layers[li], act["saved"],
                                           dh.view(act["h"].shape), want_dx=li > 0, ws=ws,
                                           stream=stream)

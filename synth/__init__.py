@@ -114,6 +114,16 @@ class Workload:
     kind: str = "normal"
     cfg: int = 0
     seed: Optional[int] = None
+    K: int = 3                      # filter size of every PyraMiD-LSTM layer
+    # explicit hidden FC widths (overrides `fc`); one per layer, or one fewer
+    # when the last layer feeds the output layer directly
+    fc_widths: Optional[List[int]] = None
+
+    def fc_width(self, li: int) -> Optional[int]:
+        """Width of the hidden FC tanh after layer li (None: no FC there)."""
+        if self.fc_widths is not None:
+            return self.fc_widths[li] if li < len(self.fc_widths) else None
+        return 2 * self.hidden[li] if self.fc else None
 
     def seeds(self):
         base = self.seed if self.seed is not None else SEED_BASE + 10 * self.cfg
@@ -127,14 +137,20 @@ class Workload:
         """Voxel-direction updates per forward pass (6 per voxel per layer)."""
         return 6 * self.voxels * len(self.hidden)
 
+    def layer_shapes(self):
+        """(input channels, hidden units) of every PyraMiD-LSTM layer."""
+        out, C = [], self.C
+        for li, O in enumerate(self.hidden):
+            out.append((C, O))
+            w = self.fc_width(li)
+            C = w if w is not None else O
+        return out
+
     def flops_per_pass(self) -> int:
-        """Algorithmic contraction flops of the layers (dense 3 x 3 stencils):
-        2 * 9 * 4O * (C + O) per voxel-direction update."""
-        tot, C = 0, self.C
-        for O in self.hidden:
-            tot += 6 * self.voxels * 2 * 9 * 4 * O * (C + O)
-            C = 2 * O if self.fc else O
-        return tot
+        """Algorithmic contraction flops of the layers (dense K x K stencils):
+        2 * K^2 * 4O * (C + O) per voxel-direction update."""
+        return sum(6 * self.voxels * 2 * self.K * self.K * 4 * O * (C + O)
+                   for C, O in self.layer_shapes())
 
 
 CONFIGS = {
@@ -146,6 +162,15 @@ CONFIGS = {
     5: Workload("MR-like 48x240x240x3 2 layers O=16/32 + FC + softmax CE, fwd+bwd f32", 1, 48,
                 240, 240, 3, [16, 32], fc=True, classes=4, labels=True, kind="mr", cfg=5),
 }
+
+# The network of Section 3 ("Experimental Setup"): 7 x 7 filters, PyraMiD-LSTM
+# 16 -> FC tanh 25 -> PyraMiD-LSTM 32 -> FC tanh 45 -> PyraMiD-LSTM 64 -> output
+# layer, on the last bootstrapping sub-volume of the MR data (25 slices of
+# 240 x 240).  Five input channels and five classes are the reading under which
+# the paper's weight count is matched (to within 2); labels for training.
+PAPER_NET = Workload("paper network 7x7 16/25/32/45/64, MR sub-volume 25x240x240x5, "
+                     "softmax CE, fwd+bwd f32", 1, 25, 240, 240, 5, [16, 32, 64], classes=5,
+                     labels=True, kind="mr", cfg=6, K=7, fc_widths=[25, 45])
 
 
 @dataclass
@@ -164,11 +189,12 @@ def make(wl: Workload) -> Instance:
     x = to_storage(volume(wl.kind, wl.N, wl.D, wl.H, wl.W, wl.C, rin), wl.dtype)
     layers, fcs = [], []
     C = wl.C
-    for O in wl.hidden:
-        layers.append(layer_params(rw, C, O, wl.dtype))
-        if wl.fc:
-            fcs.append(fc_params(rw, O, 2 * O, wl.dtype))
-            C = 2 * O
+    for li, O in enumerate(wl.hidden):
+        layers.append(layer_params(rw, C, O, wl.dtype, K=wl.K))
+        w = wl.fc_width(li)
+        if w is not None:
+            fcs.append(fc_params(rw, O, w, wl.dtype))
+            C = w
         else:
             C = O
     head = fc_params(rw, C, wl.classes, wl.dtype) if wl.classes else None

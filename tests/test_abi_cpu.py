@@ -88,6 +88,21 @@ def test_forward_validation(lib):
     need = P.pyramid_lstm_workspace_size(s, 1)
     assert fwd(lib, s, saved=FAKE, nbytes=need - 1) == -3
     assert fwd(lib, shape(dtype=P.PLSTM_BF16), saved=FAKE, nbytes=1 << 40) == -2
+    assert fwd(lib, shape(K=4)) == -1                                 # even filter
+    assert fwd(lib, shape(K=-3)) == -1
+    assert fwd(lib, shape(K=9)) == -2                                 # larger than 7
+
+
+def test_filter_size_in_sizes(lib):
+    """K = 0 means 3; the workspace grows with the filter's taps."""
+    assert (P.pyramid_lstm_workspace_size(shape(K=0), 1) ==
+            P.pyramid_lstm_workspace_size(shape(K=3), 1))
+    assert (P.pyramid_lstm_workspace_size(shape(O=32, K=7), 1) >
+            P.pyramid_lstm_workspace_size(shape(O=32, K=3), 1))
+    for k in (1, 3, 5, 7):
+        assert P.pyramid_lstm_workspace_size(shape(K=k), 1) > 0
+    for k in (2, 9, -1):
+        assert P.pyramid_lstm_workspace_size(shape(K=k), 1) == 0
 
 
 def test_backward_validation(lib):

@@ -232,6 +232,87 @@ def test_large_hidden_layers_take_the_step_path():
         assert "sweep_fwd_generic" not in phases and "sweep_bwd_generic" not in phases
 
 
+def instance_k(shape, K, seed, dtype="f32"):
+    N, D, H, W, C, O = shape
+    wl = synth.Workload("t", N, D, H, W, C, [O], dtype=dtype, seed=seed, K=K)
+    return synth.make(wl)
+
+
+# K x K filters (Section 3 uses 7 x 7): every unit count, channel counts of
+# the paper's network (5, 25, 45), K = 1, a plane smaller than the filter
+K_CASES = [((1, 5, 17, 13, 3, 16), 5), ((1, 4, 11, 9, 25, 32), 7), ((2, 3, 8, 12, 5, 16), 7),
+           ((1, 6, 9, 10, 2, 16), 1), ((1, 3, 9, 8, 45, 64), 7), ((1, 2, 3, 9, 4, 32), 7)]
+
+
+@pytest.mark.parametrize("case", K_CASES, ids=lambda c: "x".join(map(str, c[0])) + "_k%d" % c[1])
+def test_filter_size_matches_oracle(case, step_split):
+    shape, K = case
+    inst = instance_k(shape, K, 7000 + sum(shape) + K)
+    L = inst.layers[0]
+    dh = synth.upstream_grad(inst.x.shape[:-1] + (shape[-1],), 13 + sum(shape))
+    ref_h = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    ref = oracle.backward(inst.x, L.wx, L.wh, L.b, dh)
+    say("filter size", shape, K)
+    x, Ld = dev(inst.x), layer_dev(L)
+    assert Ld.K == K
+    P.pyramid_lstm_timing_enable(True)
+    h_inf, _ = layer_forward(x, Ld)
+    h, saved = layer_forward(x, Ld, training=True)
+    dx, dwx, dwh, db = layer_backward(x, Ld, saved, dev(dh))
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    torch.cuda.synchronize()
+    if K != 3:
+        assert "sweep_fwd_step" in phases and "sweep_bwd_step" in phases, phases
+    assert normwise(host(h_inf), ref_h) <= TOL["f32"]
+    assert normwise(host(h), ref_h) <= TOL["f32"]
+    for name, got in (("dx", dx), ("dwx", dwx), ("dwh", dwh), ("db", db)):
+        err = normwise(host(got), ref[name])
+        assert err <= TOL["f32"], (name, err)
+
+
+@pytest.mark.parametrize("case", [((1, 5, 9, 7, 3, 16), 5), ((1, 3, 6, 5, 2, 8), 7)],
+                         ids=lambda c: "x".join(map(str, c[0])) + "_k%d" % c[1])
+def test_filter_size_generic_path(case):
+    """The generic per-plane kernels with K x K filters (forced)."""
+    shape, K = case
+    inst = instance_k(shape, K, 7100 + sum(shape) + K)
+    L = inst.layers[0]
+    dh = synth.upstream_grad(inst.x.shape[:-1] + (shape[-1],), 17 + sum(shape))
+    ref_h = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    ref = oracle.backward(inst.x, L.wx, L.wh, L.b, dh)
+    say("filter size generic", shape, K)
+    P.pyramid_lstm_set_forward_path(1)
+    P.pyramid_lstm_set_backward_path(1)
+    try:
+        x, Ld = dev(inst.x), layer_dev(L)
+        h, saved = layer_forward(x, Ld, training=True)
+        grads = layer_backward(x, Ld, saved, dev(dh))
+        torch.cuda.synchronize()
+    finally:
+        P.pyramid_lstm_set_forward_path(0)
+        P.pyramid_lstm_set_backward_path(0)
+    assert normwise(host(h), ref_h) <= TOL["f32"]
+    for name, got in zip(("dx", "dwx", "dwh", "db"), grads):
+        assert normwise(host(got), ref[name]) <= TOL["f32"], name
+
+
+@pytest.mark.parametrize("bf16_mfma", [1, 0], ids=["bf16_mfma", "fp32_mfma"])
+def test_filter_size_bf16(bf16_mfma):
+    shape, K = (1, 4, 11, 9, 25, 32), 7
+    inst = instance_k(shape, K, 7200, "bf16")
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    say("filter size bf16", shape, K, bf16_mfma)
+    P.pyramid_lstm_set_bf16_mfma(bf16_mfma)
+    try:
+        h, _ = layer_forward(dev(inst.x, "bf16"), layer_dev(L, "bf16"))
+        torch.cuda.synchronize()
+    finally:
+        P.pyramid_lstm_set_bf16_mfma(1)
+    assert normwise(host(h), ref) <= TOL["bf16"]
+
+
 def test_mfma_backward_runs_for_o16():
     """The persistent MFMA reverse sweep and MFMA parameter gradients are the
     path taken for 16 hidden units."""

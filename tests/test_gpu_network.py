@@ -67,6 +67,43 @@ def test_small_network_training_step(fused):
         assert normwise(host(got), want) <= TOL["f32"]
 
 
+def paper_small(seed, dtype="f32"):
+    """The network of Section 3 ("Experimental Setup") on a small volume: 7 x 7
+    filters, PyraMiD 16 -> FC tanh 25 -> PyraMiD 32 -> FC tanh 45 ->
+    PyraMiD 64 -> output layer (5 classes), 5 input channels."""
+    wl = synth.Workload("paper small", 1, 3, 9, 8, 5, [16, 32, 64], dtype=dtype, classes=5,
+                        labels=dtype == "f32", K=7, fc_widths=[25, 45], seed=seed)
+    return synth.make(wl)
+
+
+def test_paper_network_training_step():
+    inst = paper_small(95)
+    ref = onet.backward(inst.x, *oracle_args(inst), inst.labels)
+    say("paper network training step")
+    x, layers, fcs, head, labels = to_device(inst, "f32")
+    g = network_train_step(x, layers, fcs, head, labels)
+    torch.cuda.synchronize()
+    assert abs(g["loss"].item() - ref["loss"]) <= TOL["f32"] * abs(ref["loss"])
+    assert normwise(host(g["p"]), ref["p"]) <= TOL["f32"]
+    pairs = [(g["head"][0], ref["head"][0]), (g["head"][1], ref["head"][1])]
+    for li in range(2):
+        pairs += list(zip(g["fcs"][li], ref["fcs"][li]))
+    for li in range(3):
+        pairs += list(zip(g["layers"][li], ref["layers"][li]))
+    for got, want in pairs:
+        assert normwise(host(got), want) <= TOL["f32"]
+
+
+def test_paper_network_forward_bf16():
+    inst = paper_small(96, "bf16")
+    ref = onet.forward(inst.x, *oracle_args(inst))["p"]
+    say("paper network forward bf16")
+    x, layers, fcs, head, _ = to_device(inst, "bf16")
+    out = network_forward(x, layers, fcs, head)
+    torch.cuda.synchronize()
+    assert normwise(host(out["p"]), ref) <= TOL["bf16"]
+
+
 def test_fc_and_softmax_match_oracle():
     rng = np.random.default_rng(90)
     M, Cin, Cout, K = 1000, 16, 32, 4

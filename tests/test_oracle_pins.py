@@ -476,3 +476,53 @@ def test_generators_are_deterministic():
     bf = synth.round_bf16(np.array([1.0, 1.00390625, 1.005859375, -3.14159], np.float32))
     assert bf[0] == 1.0 and bf[1] == 1.0 and bf[2] == 1.0078125   # ties to even
     assert np.all(synth.bf16_bits(bf).astype(np.uint32) << 16 == bf.view(np.uint32))
+
+
+# ------------------------------------------------- training update (Section 3)
+import oracle.optim as optim
+
+
+def test_learning_rate_schedule():
+    """Starts at 1e-2 + 1e-6, halves its decaying part every 100 epochs and
+    tends to 1e-6."""
+    assert optim.learning_rate(0) == pytest.approx(1e-2 + 1e-6, rel=1e-15)
+    for e in (100, 200, 300):
+        assert optim.learning_rate(e) - 1e-6 == pytest.approx(1e-2 * 0.5 ** (e // 100),
+                                                               rel=1e-12)
+    assert optim.learning_rate(5000) == pytest.approx(1e-6, rel=1e-6)
+
+
+def test_rmsprop_first_steps_closed_form():
+    """From zero state with a constant gradient g, by hand:
+    step 1: MSE = 0.1 g^2, G = g / (sqrt(0.1)|g| + eps), M = 0.1 G;
+    step 2: MSE = 0.19 g^2, G2 = g / (sqrt(0.19)|g| + eps), M = 0.09 G + 0.1 G2."""
+    g = np.array([3.0, -0.5, 1e-3, 0.0, 7.0])
+    th0 = np.array([1.0, 2.0, -3.0, 0.5, 0.0])
+    lr = 0.01
+    z = np.zeros_like(g)
+    th1, m1, M1 = optim.rmsprop_step(th0, g, z, z, lr)
+    G1 = g / (np.sqrt(0.1) * np.abs(g) + 1e-5)
+    np.testing.assert_allclose(m1, 0.1 * g * g, rtol=1e-15, atol=0)
+    np.testing.assert_allclose(M1, 0.1 * G1, rtol=1e-14, atol=0)
+    np.testing.assert_allclose(th1, th0 - lr * 0.1 * G1, rtol=1e-14, atol=0)
+    th2, m2, M2 = optim.rmsprop_step(th1, g, m1, M1, lr)
+    G2 = g / (np.sqrt(0.19) * np.abs(g) + 1e-5)
+    np.testing.assert_allclose(m2, 0.19 * g * g, rtol=1e-14, atol=0)
+    np.testing.assert_allclose(M2, 0.09 * G1 + 0.1 * G2, rtol=1e-14, atol=0)
+    np.testing.assert_allclose(th2, th1 - lr * (0.09 * G1 + 0.1 * G2), rtol=1e-14, atol=0)
+
+
+def test_rmsprop_normalises_gradient_scale():
+    """The point of Eq. (16): after the running mean has settled, the update
+    is nearly independent of the gradient's scale (|G| -> 1 for |g| >> eps),
+    and a zero gradient moves nothing."""
+    th = np.zeros(3)
+    z = np.zeros(3)
+    for scale in (1e-2, 1.0, 1e3):
+        g = np.array([scale, -scale, 0.0])
+        t, m, M = th, z, z
+        for _ in range(200):
+            t, m, M = optim.rmsprop_step(t, g, m, M, 1.0)
+        np.testing.assert_allclose(M[:2], [1.0, -1.0], rtol=2e-3)
+        assert M[2] == 0.0 and t[2] == 0.0
+

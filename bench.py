@@ -173,9 +173,20 @@ def bench_network(args, cfg):
                               train, "cuda:0")
     torch.cuda.synchronize()
 
+    # the paper's network trains with its own update (RMS-prop with momentum,
+    # Section 3) inside the timed step
+    opt = None
+    if cfg is None:
+        from paper_1506_07452_amd import RMSprop
+        from paper_1506_07452_amd.network import network_gradients, network_parameters
+        opt = RMSprop(network_parameters(layers, fcs, head))
+
     def step():
         if train:
-            return network_train_step(x, layers, fcs, head, labels, ws=ws)
+            g = network_train_step(x, layers, fcs, head, labels, ws=ws)
+            if opt is not None:
+                opt.step(network_gradients(g), 0)
+            return g
         return network_forward(x, layers, fcs, head, ws=ws)
 
     for _ in range(args.warmup):
@@ -198,7 +209,8 @@ def bench_network(args, cfg):
         "scaling": "weak", "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic",
-        "config": {"workload": wl.name + (", fwd+bwd" if train else ", fwd"), "N": wl.N,
+        "config": {"workload": wl.name + (", fwd+bwd" if train else ", fwd") +
+                               (" + RMS-prop update" if opt is not None else ""), "N": wl.N,
                    "D": wl.D, "H": wl.H, "W": wl.W, "C": wl.C, "hidden": wl.hidden,
                    "fc": [wl.fc_width(i) for i in range(len(wl.hidden))], "K": wl.K,
                    "storage": wl.dtype, "classes": wl.classes},

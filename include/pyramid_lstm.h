@@ -186,6 +186,36 @@ int pyramid_lstm_timing_read(int max_phases, char *names, double *ms, int *launc
                              int *count);
 
 
+/* ---- training update (Section 3, "Training") ---------------------------- */
+
+/* One parameter tensor for pyramid_rmsprop_step: n fp32 elements of the
+ * parameters theta (updated in place), their gradient grad (read), and the
+ * optimiser state ms (running mean of grad^2) and mom (smoothed normalised
+ * gradient), both updated in place and zero before the first step.  All
+ * device pointers, 4-byte aligned, owned by the caller. */
+typedef struct plstm_param_segment {
+    float *theta;
+    const float *grad;
+    float *ms;
+    float *mom;
+    int64_t n;
+} plstm_param_segment;
+
+/* RMS-prop with momentum, Eq. (15)-(18), over `count` (1..64) tensors in one
+ * launch: ms = rho_ms ms + (1 - rho_ms) g^2; G = g / (sqrt(ms) + eps);
+ * mom = rho_m mom + (1 - rho_m) G; theta -= lr mom.  The paper's values are
+ * rho_ms = rho_m = 0.9 and eps = 1e-5, with lr from
+ * pyramid_rmsprop_learning_rate.  `segs` is a host array read before the call
+ * returns; segments must not overlap.  Returns PLSTM_EINVAL for a bad count,
+ * null or misaligned pointers, negative n, lr < 0, rho outside [0, 1) or
+ * eps <= 0. */
+int pyramid_rmsprop_step(int32_t count, const plstm_param_segment *segs, float lr,
+                         float rho_ms, float rho_m, float eps, void *stream);
+
+/* The decaying learning rate of Section 3: 1e-6 + 1e-2 (2^(-1/100))^epoch
+ * (host function). */
+double pyramid_rmsprop_learning_rate(int32_t epoch);
+
 /* Forward implementation selection, for testing and tuning (process-wide):
  * 0 = automatic (default): the persistent MFMA sweep where it supports the
  * shape (fp32, O = 16, C <= 4, grid co-resident), else the plane-step MFMA

@@ -19,7 +19,8 @@ __all__ = [
     "pyramid_lstm_status_string", "pyramid_lstm_workspace_size", "pyramid_lstm_saved_size",
     "pyramid_lstm_forward", "pyramid_lstm_backward", "pyramid_fc_tanh_forward",
     "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
-    "pyramid_head_workspace_size", "pyramid_head_train",
+    "pyramid_head_workspace_size", "pyramid_head_train", "plstm_param_segment",
+    "pyramid_rmsprop_step", "pyramid_rmsprop_learning_rate", "RMSprop",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
     "pyramid_lstm_set_backward_path", "pyramid_lstm_set_step_split", "pyramid_lstm_set_bf16_mfma",
     "library_path", "load",
@@ -43,6 +44,11 @@ class plstm_shape(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int32), ("D", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("W", ctypes.c_int32), ("C", ctypes.c_int32), ("O", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("K", ctypes.c_int32)]
+
+
+class plstm_param_segment(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("ms", ctypes.c_void_p),
+                ("mom", ctypes.c_void_p), ("n", ctypes.c_int64)]
 
 
 def library_path() -> str:
@@ -82,6 +88,12 @@ def load():
     lib.pyramid_head_workspace_size.restype = sz
     lib.pyramid_head_train.argtypes = [i64, i32, i32, i32] + [vp] * 14 + [sz, vp]
     lib.pyramid_head_train.restype = ctypes.c_int
+    f32 = ctypes.c_float
+    lib.pyramid_rmsprop_step.argtypes = [i32, ctypes.POINTER(plstm_param_segment), f32, f32, f32,
+                                         f32, vp]
+    lib.pyramid_rmsprop_step.restype = ctypes.c_int
+    lib.pyramid_rmsprop_learning_rate.argtypes = [i32]
+    lib.pyramid_rmsprop_learning_rate.restype = ctypes.c_double
     lib.pyramid_lstm_timing_enable.argtypes = [ctypes.c_int]
     lib.pyramid_lstm_timing_enable.restype = ctypes.c_int
     lib.pyramid_lstm_timing_read.argtypes = [ctypes.c_int, ctypes.c_char_p,
@@ -226,6 +238,43 @@ def pyramid_head_train(x, w1, b1, w2, b2, labels, p, loss, dx, dw1, db1, dw2, db
         M, Cin, F, K, _ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(labels), _ptr(p),
         _ptr(loss), _ptr(dx), _ptr(dw1), _ptr(db1), _ptr(dw2), _ptr(db2), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_rmsprop_step(params, grads, ms, mom, lr, rho_ms=0.9, rho_m=0.9, eps=1e-5,
+                         stream=None):
+    """RMS-prop with momentum (Section 3, Eq. (15)-(18)) over lists of fp32
+    device tensors, in place, in one launch."""
+    n = len(params)
+    if not (len(grads) == len(ms) == len(mom) == n):
+        raise ValueError("params, grads, ms and mom must have the same length")
+    segs = (plstm_param_segment * max(n, 1))()
+    for k, (t, g, a, m) in enumerate(zip(params, grads, ms, mom)):
+        for u in (t, g, a, m):
+            if u.dtype != torch.float32 or u.numel() != t.numel():
+                raise ValueError("fp32 tensors of one size per parameter expected")
+        segs[k] = plstm_param_segment(_ptr(t), _ptr(g), _ptr(a), _ptr(m), t.numel())
+    _check("pyramid_rmsprop_step", load().pyramid_rmsprop_step(
+        n, segs, float(lr), float(rho_ms), float(rho_m), float(eps), _stream(stream)))
+
+
+def pyramid_rmsprop_learning_rate(epoch: int) -> float:
+    """1e-6 + 1e-2 (2^(-1/100))^epoch (Section 3, "Training")."""
+    return load().pyramid_rmsprop_learning_rate(int(epoch))
+
+
+class RMSprop:
+    """Optimiser state (zero-initialised) for a fixed list of parameter
+    tensors; `step(grads, epoch)` applies one update with the paper's
+    hyper-parameters and learning-rate schedule."""
+
+    def __init__(self, params):
+        self.params = list(params)
+        self.ms = [torch.zeros_like(p) for p in self.params]
+        self.mom = [torch.zeros_like(p) for p in self.params]
+
+    def step(self, grads, epoch: int, stream=None):
+        pyramid_rmsprop_step(self.params, list(grads), self.ms, self.mom,
+                             pyramid_rmsprop_learning_rate(epoch), stream=stream)
 
 
 def pyramid_lstm_timing_enable(on: bool) -> None:

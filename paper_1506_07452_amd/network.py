@@ -198,3 +198,26 @@ def _train_step_unfused(x, layers, fcs, head, labels, ws=None, stream=None):
             g = dx
     return {"loss": out["loss"], "p": out["p"], "head": out["head_grad"], "fcs": fc_grads,
             "layers": layer_grads}
+
+
+def network_parameters(layers, fcs, head):
+    """Every parameter tensor of a network, in the order of
+    `network_gradients`: per layer (wx, wh, b), per hidden FC (w, b), head."""
+    out = []
+    for L in layers:
+        out += [L.wx, L.wh, L.b]
+    for w, b in fcs:
+        out += [w, b]
+    return out + [head[0], head[1]]
+
+
+def network_gradients(g):
+    """The gradients of a `network_train_step` result, in the order of
+    `network_parameters`."""
+    out = []
+    for t in g["layers"]:
+        out += list(t)
+    for t in g["fcs"]:
+        out += list(t)
+    return out + [g["head"][0], g["head"][1]]
+

@@ -183,3 +183,33 @@ def test_path_knobs_and_timing_without_gpu():
     P.pyramid_lstm_timing_enable(True)
     assert P.pyramid_lstm_timing_read() == {}
     P.pyramid_lstm_timing_enable(False)
+
+
+def test_rmsprop_validation(lib):
+    """Argument checks of the optimiser entry point (no GPU work: an update
+    of zero elements returns before any launch)."""
+    Seg = P.plstm_param_segment
+    segs = (Seg * 2)(Seg(FAKE, FAKE, FAKE, FAKE, 0), Seg(FAKE, FAKE, FAKE, FAKE, 0))
+    step = lib.pyramid_rmsprop_step
+    assert step(2, segs, 0.01, 0.9, 0.9, 1e-5, None) == 0
+    assert step(0, segs, 0.01, 0.9, 0.9, 1e-5, None) == -1
+    assert step(65, segs, 0.01, 0.9, 0.9, 1e-5, None) == -1
+    assert step(2, None, 0.01, 0.9, 0.9, 1e-5, None) == -1
+    assert step(2, segs, -1.0, 0.9, 0.9, 1e-5, None) == -1
+    assert step(2, segs, 0.01, 1.0, 0.9, 1e-5, None) == -1
+    assert step(2, segs, 0.01, 0.9, -0.1, 1e-5, None) == -1
+    assert step(2, segs, 0.01, 0.9, 0.9, 0.0, None) == -1
+    bad = (Seg * 1)(Seg(None, FAKE, FAKE, FAKE, 5))
+    assert step(1, bad, 0.01, 0.9, 0.9, 1e-5, None) == -1
+    bad = (Seg * 1)(Seg(FAKE, FAKE, ctypes.c_void_p(0x10002), FAKE, 5))
+    assert step(1, bad, 0.01, 0.9, 0.9, 1e-5, None) == -1
+    bad = (Seg * 1)(Seg(FAKE, FAKE, FAKE, FAKE, -1))
+    assert step(1, bad, 0.01, 0.9, 0.9, 1e-5, None) == -1
+
+
+def test_learning_rate_schedule_matches_oracle():
+    import oracle.optim as optim
+    for e in (0, 1, 50, 100, 1234, 6000):
+        assert P.pyramid_rmsprop_learning_rate(e) == pytest.approx(optim.learning_rate(e),
+                                                                   rel=1e-14)
+

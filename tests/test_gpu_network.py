@@ -104,6 +104,52 @@ def test_paper_network_forward_bf16():
     assert normwise(host(out["p"]), ref) <= TOL["bf16"]
 
 
+def test_rmsprop_matches_oracle():
+    """Three RMS-prop updates (Section 3, Eq. (15)-(18)) of four tensors of
+    ragged sizes in one launch each, against the fp64 oracle fed the same
+    fp32 gradients."""
+    import oracle.optim as optim
+    import paper_1506_07452_amd as P
+    rng = np.random.default_rng(97)
+    sizes = [1, 1000, 4097, 3 * 64 * 64]
+    th = [rng.uniform(-0.1, 0.1, n).astype(np.float32) for n in sizes]
+    ref = [(t.astype(np.float64), np.zeros(n), np.zeros(n)) for t, n in zip(th, sizes)]
+    params = [dev(t) for t in th]
+    ms = [torch.zeros(n, device=DEV) for n in sizes]
+    mom = [torch.zeros(n, device=DEV) for n in sizes]
+    say("rmsprop")
+    for epoch in range(3):
+        grads = [(rng.standard_normal(n) * 10.0 ** rng.integers(-4, 2, n)).astype(np.float32)
+                 for n in sizes]
+        lr = optim.learning_rate(epoch)
+        P.pyramid_rmsprop_step(params, [dev(g) for g in grads], ms, mom, lr)
+        ref = [optim.rmsprop_step(t, g, a, m, lr) for (t, a, m), g in zip(ref, grads)]
+    torch.cuda.synchronize()
+    for k in range(len(sizes)):
+        assert normwise(host(params[k]), ref[k][0]) <= 1e-6
+        assert normwise(host(ms[k]), ref[k][1]) <= 1e-6
+        assert normwise(host(mom[k]), ref[k][2]) <= 1e-5
+
+
+def test_paper_network_training_reduces_loss():
+    """A few full training iterations of the paper's network (train step +
+    RMS-prop update with the decaying rate) on one fixed small batch: the
+    loss goes down."""
+    from paper_1506_07452_amd import RMSprop
+    from paper_1506_07452_amd.network import network_gradients, network_parameters
+    inst = paper_small(98)
+    say("paper network training iterations")
+    x, layers, fcs, head, labels = to_device(inst, "f32")
+    opt = RMSprop(network_parameters(layers, fcs, head))
+    losses = []
+    for epoch in range(6):
+        g = network_train_step(x, layers, fcs, head, labels)
+        losses.append(g["loss"].item())
+        opt.step(network_gradients(g), epoch)
+    torch.cuda.synchronize()
+    assert losses[-1] < 0.9 * losses[0], losses
+
+
 def test_fc_and_softmax_match_oracle():
     rng = np.random.default_rng(90)
     M, Cin, Cout, K = 1000, 16, 32, 4

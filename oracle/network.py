@@ -21,10 +21,13 @@ from . import backward as layer_backward
 from . import fc_tanh_backward, fc_tanh_forward
 from . import forward as layer_forward
 from . import softmax_ce
+from .loss import softmax_sq
 
 
-def forward(x, layers, fcs, head, labels=None):
+def forward(x, layers, fcs, head, labels=None, loss="ce"):
     """x [N][D][H][W][C]; layers = [(wx, wh, b)], fcs = [(w, b)], head = (w, b).
+    loss: "ce" (mean cross-entropy) or "sq" (mean squared error against the
+    one-hot target, Eq. (14)).
 
     Returns dict: 'p' [N*D*H*W][classes], 'loss' (if labels), and the
     per-layer activations needed by ``backward`` under 'acts'."""
@@ -42,18 +45,20 @@ def forward(x, layers, fcs, head, labels=None):
             act["y"] = y
             a = y
         acts.append(act)
-    out = softmax_ce(a.reshape(-1, a.shape[-1]), head[0], head[1], labels,
-                     grad=labels is not None)
+    head_fn = {"ce": softmax_ce, "sq": softmax_sq}[loss]
+    out = head_fn(a.reshape(-1, a.shape[-1]), head[0], head[1], labels,
+                  grad=labels is not None)
     out["acts"] = acts
     return out
 
 
-def backward(x, layers, fcs, head, labels):
-    """Gradients of the mean cross-entropy w.r.t. every parameter.
+def backward(x, layers, fcs, head, labels, loss="ce"):
+    """Gradients of the loss ("ce" or "sq", as in ``forward``) w.r.t. every
+    parameter.
 
     Returns dict: 'loss', 'head' (dw, db), 'fcs' [(dw, db)], 'layers'
     [(dwx, dwh, db)], in the order of the arguments."""
-    fwd = forward(x, layers, fcs, head, labels)
+    fwd = forward(x, layers, fcs, head, labels, loss)
     acts = fwd["acts"]
     N, D, H, W, _ = x.shape
     last = acts[-1]["y"] if "y" in acts[-1] else acts[-1]["h"]

@@ -526,3 +526,91 @@ def test_rmsprop_normalises_gradient_scale():
         np.testing.assert_allclose(M[:2], [1.0, -1.0], rtol=2e-3)
         assert M[2] == 0.0 and t[2] == 0.0
 
+
+# ------------------------------------------------- squared loss (Eq. (14))
+import oracle.loss as oloss
+
+
+def test_squared_loss_closed_forms():
+    """Uniform logits give p = 1/K and E = (1 - 1/K)^2 + (K - 1)/K^2 = (K - 1)/K
+    per voxel; a confident correct prediction gives E -> 0."""
+    rng = np.random.default_rng(160)
+    M, Cin, K = 7, 3, 5
+    x = rng.standard_normal((M, Cin))
+    lab = rng.integers(0, K, M)
+    r = oloss.softmax_sq(x, np.zeros((K, Cin)), np.zeros(K), lab, grad=True)
+    np.testing.assert_allclose(r["p"], 1.0 / K, rtol=1e-15)
+    assert r["loss"] == pytest.approx((K - 1) / K, rel=1e-14)
+    # logits 40 on the label, 0 elsewhere, for one voxel
+    w = np.zeros((K, 1))
+    b = np.zeros(K)
+    b[2] = 40.0
+    r = oloss.softmax_sq(np.ones((1, 1)), w, b, [2], grad=True)
+    assert r["loss"] < 1e-30 and np.abs(r["db"]).max() < 1e-15
+
+
+def test_squared_loss_gradient_against_autograd_and_differences():
+    """The hand-derived chain rule against torch autograd of the definition
+    (fp64) and against central differences."""
+    rng = np.random.default_rng(161)
+    M, Cin, K = 9, 4, 3
+    x = rng.standard_normal((M, Cin))
+    w = rng.uniform(-0.8, 0.8, (K, Cin))
+    b = rng.uniform(-0.5, 0.5, K)
+    lab = rng.integers(0, K, M)
+    r = oloss.softmax_sq(x, w, b, lab, grad=True)
+    tx, tw, tb = (torch.tensor(a, requires_grad=True) for a in (x, w, b))
+    tp = torch.softmax(tx @ tw.T + tb, dim=1)
+    ty = torch.nn.functional.one_hot(torch.tensor(lab), K).double()
+    E = ((tp - ty) ** 2).sum() / M
+    E.backward()
+    assert r["loss"] == pytest.approx(E.item(), rel=1e-13)
+    for got, t in ((r["dx"], tx), (r["dw"], tw), (r["db"], tb)):
+        np.testing.assert_allclose(got, t.grad.numpy(), rtol=1e-11, atol=1e-14)
+    eps = 1e-6
+    for arr, grad in ((w, r["dw"]), (b, r["db"])):
+        flat = arr.reshape(-1)
+        for k in range(flat.size):
+            s0 = flat[k]
+            flat[k] = s0 + eps
+            lp = oloss.softmax_sq(x, w, b, lab)["loss"]
+            flat[k] = s0 - eps
+            lm = oloss.softmax_sq(x, w, b, lab)["loss"]
+            flat[k] = s0
+            assert (lp - lm) / (2 * eps) == pytest.approx(grad.reshape(-1)[k], abs=1e-8)
+
+
+def test_network_squared_loss_finite_differences():
+    """The paper-shaped network trained on the squared loss: chain-rule
+    gradients of a sample of every parameter tensor against differences."""
+    rng = np.random.default_rng(162)
+    N, D, H, W, C = 1, 2, 3, 3, 2
+    x = rng.standard_normal((N, D, H, W, C))
+    layers = [synth.layer_params(rng, C, 2), synth.layer_params(rng, 3, 2)]
+    layers = [(l.wx.astype(np.float64) * 3, l.wh.astype(np.float64) * 3, l.b.astype(np.float64))
+              for l in layers]
+    fcs = [(rng.uniform(-0.5, 0.5, (3, 2)), rng.uniform(-0.5, 0.5, 3))]
+    head = (rng.uniform(-0.9, 0.9, (4, 2)), rng.uniform(-0.5, 0.5, 4))
+    lab = rng.integers(0, 4, N * D * H * W)
+    g = onet.backward(x, layers, fcs, head, lab, loss="sq")
+    eps = 1e-6
+
+    def L():
+        return onet.forward(x, layers, fcs, head, lab, loss="sq")["loss"]
+
+    checks = [(head[0], g["head"][0]), (fcs[0][0], g["fcs"][0][0]),
+              (layers[0][1], g["layers"][0][1]), (layers[1][0], g["layers"][1][0]),
+              (layers[1][2], g["layers"][1][2])]
+    for arr, grad in checks:
+        flat = arr.reshape(-1)
+        for k in rng.choice(flat.size, size=min(flat.size, 5), replace=False):
+            s0 = flat[k]
+            flat[k] = s0 + eps
+            lp = L()
+            flat[k] = s0 - eps
+            lm = L()
+            flat[k] = s0
+            fd = (lp - lm) / (2 * eps)
+            an = grad.reshape(-1)[k]
+            assert abs(fd - an) <= 1e-9 + 1e-5 * abs(an), (fd, an)
+

@@ -123,7 +123,7 @@ int pyramid_fc_tanh_forward(int64_t M, int32_t Cin, int32_t Cout, int32_t dtype,
                             const void *x, const void *w, const void *b, void *y,
                             void *stream);
 
-/* Bytes of workspace for pyramid_fc_tanh_backward / pyramid_softmax_ce. */
+/* Bytes of workspace for pyramid_fc_tanh_backward / pyramid_softmax_ce / _sq. */
 size_t pyramid_fc_workspace_size(int64_t M, int32_t Cin, int32_t Cout);
 
 /* Gradient of pyramid_fc_tanh_forward (fp32): given x, w, the forward's output
@@ -142,6 +142,16 @@ int pyramid_fc_tanh_backward(int64_t M, int32_t Cin, int32_t Cout, const void *x
  * dL/dw [K][Cin], dL/db [K] (overwritten).  ws: pyramid_fc_workspace_size(M,
  * Cin, K) bytes when labels is non-NULL, else may be NULL. */
 int pyramid_softmax_ce(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const void *x,
+                       const void *w, const void *b, const int32_t *labels, void *p,
+                       void *loss, void *dx, void *dw, void *db, void *ws,
+                       size_t ws_bytes, void *stream);
+
+/* As pyramid_softmax_ce, with the squared loss of Section 3 ("Training",
+ * Eq. (14)) instead of the cross-entropy: with y the one-hot label,
+ *   loss = (1/M) sum_m sum_k (p[m][k] - y[m][k])^2,
+ * and its gradient through the softmax.  Same arguments, layouts and
+ * workspace. */
+int pyramid_softmax_sq(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const void *x,
                        const void *w, const void *b, const int32_t *labels, void *p,
                        void *loss, void *dx, void *dw, void *db, void *ws,
                        size_t ws_bytes, void *stream);

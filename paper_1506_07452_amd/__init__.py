@@ -20,7 +20,7 @@ __all__ = [
     "pyramid_lstm_forward", "pyramid_lstm_backward", "pyramid_fc_tanh_forward",
     "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
     "pyramid_head_workspace_size", "pyramid_head_train", "plstm_param_segment",
-    "pyramid_rmsprop_step", "pyramid_rmsprop_learning_rate", "RMSprop",
+    "pyramid_rmsprop_step", "pyramid_rmsprop_learning_rate", "RMSprop", "pyramid_softmax_sq",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
     "pyramid_lstm_set_backward_path", "pyramid_lstm_set_step_split", "pyramid_lstm_set_bf16_mfma",
     "library_path", "load",
@@ -84,6 +84,8 @@ def load():
     lib.pyramid_fc_tanh_backward.restype = ctypes.c_int
     lib.pyramid_softmax_ce.argtypes = [i64, i32, i32, i32] + [vp] * 10 + [sz, vp]
     lib.pyramid_softmax_ce.restype = ctypes.c_int
+    lib.pyramid_softmax_sq.argtypes = [i64, i32, i32, i32] + [vp] * 10 + [sz, vp]
+    lib.pyramid_softmax_sq.restype = ctypes.c_int
     lib.pyramid_head_workspace_size.argtypes = [i64, i32, i32, i32]
     lib.pyramid_head_workspace_size.restype = sz
     lib.pyramid_head_train.argtypes = [i64, i32, i32, i32] + [vp] * 14 + [sz, vp]
@@ -211,16 +213,24 @@ def pyramid_fc_tanh_backward(x, w, y, dy, dx, dw, db, ws=None, stream=None):
 
 
 def pyramid_softmax_ce(x, w, b, p, labels=None, loss=None, dx=None, dw=None, db=None, ws=None,
-                       stream=None):
-    """Final linear + softmax (+ mean cross-entropy and its gradient)."""
+                       stream=None, squared=False):
+    """Final linear + softmax (+ mean cross-entropy, or with `squared` the
+    squared error of Eq. (14), and its gradient)."""
     M, Cin = x.shape
     K = w.shape[0]
     if labels is not None and ws is None:
         ws = _workspace(pyramid_fc_workspace_size(M, Cin, K), x.device)
-    _check("pyramid_softmax_ce", load().pyramid_softmax_ce(
+    name = "pyramid_softmax_sq" if squared else "pyramid_softmax_ce"
+    _check(name, getattr(load(), name)(
         M, Cin, K, _DT[x.dtype], _ptr(x), _ptr(w), _ptr(b), _ptr(labels), _ptr(p), _ptr(loss),
         _ptr(dx), _ptr(dw), _ptr(db), _ptr(ws),
         0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_softmax_sq(x, w, b, p, labels=None, loss=None, dx=None, dw=None, db=None, ws=None,
+                       stream=None):
+    """Final linear + softmax (+ the squared loss of Eq. (14) and its gradient)."""
+    pyramid_softmax_ce(x, w, b, p, labels, loss, dx, dw, db, ws, stream, squared=True)
 
 
 def pyramid_head_workspace_size(M: int, Cin: int, F: int, K: int) -> int:

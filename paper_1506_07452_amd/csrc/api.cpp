@@ -140,9 +140,10 @@ int pyramid_fc_tanh_backward(int64_t M, int32_t Cin, int32_t Cout, const void *x
                             (hipStream_t)stream);
 }
 
-int pyramid_softmax_ce(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const void *x,
-                       const void *w, const void *b, const int32_t *labels, void *p, void *loss,
-                       void *dx, void *dw, void *db, void *ws, size_t ws_bytes, void *stream)
+static int softmax_entry(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const void *x,
+                         const void *w, const void *b, const int32_t *labels, void *p,
+                         void *loss, void *dx, void *dw, void *db, void *ws, size_t ws_bytes,
+                         void *stream, bool squared)
 {
     if (M < 1 || Cin < 1 || K < 1) return PLSTM_EINVAL;
     if (Cin > 1024 || K > 16 || M > (1LL << 40) / 16) return PLSTM_EUNSUPPORTED;
@@ -160,7 +161,23 @@ int pyramid_softmax_ce(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const v
         if ((dx && !aligned(dx)) || !aligned(dw) || !aligned(db)) return PLSTM_EINVAL;
     }
     return softmax_ce(M, Cin, K, dtype, x, w, b, labels, (float *)p, (float *)loss,
-                      (float *)dx, (float *)dw, (float *)db, ws, (hipStream_t)stream);
+                      (float *)dx, (float *)dw, (float *)db, ws, (hipStream_t)stream, squared);
+}
+
+int pyramid_softmax_ce(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const void *x,
+                       const void *w, const void *b, const int32_t *labels, void *p, void *loss,
+                       void *dx, void *dw, void *db, void *ws, size_t ws_bytes, void *stream)
+{
+    return softmax_entry(M, Cin, K, dtype, x, w, b, labels, p, loss, dx, dw, db, ws, ws_bytes,
+                         stream, false);
+}
+
+int pyramid_softmax_sq(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const void *x,
+                       const void *w, const void *b, const int32_t *labels, void *p, void *loss,
+                       void *dx, void *dw, void *db, void *ws, size_t ws_bytes, void *stream)
+{
+    return softmax_entry(M, Cin, K, dtype, x, w, b, labels, p, loss, dx, dw, db, ws, ws_bytes,
+                         stream, true);
 }
 
 size_t pyramid_head_workspace_size(int64_t M, int32_t Cin, int32_t F, int32_t K)

@@ -139,9 +139,10 @@ int fc_tanh_backward(long long M, int Cin, int Cout, const float *x, const float
                      const float *y, const float *dy, float *dx, float *dw, float *db,
                      void *ws, hipStream_t st);
 size_t fc_ws(long long M, int Cin, int Cout);
+// `squared`: the squared error of Eq. (14) instead of the cross-entropy.
 int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void *w,
                const void *b, const int32_t *labels, float *p, float *loss, float *dx,
-               float *dw, float *db, void *ws, hipStream_t st);
+               float *dw, float *db, void *ws, hipStream_t st, bool squared = false);
 // Fused FC + tanh, linear + softmax, cross-entropy and backward (fp32).
 bool head_supported(int Cin, int F, int K);
 size_t head_ws(long long M, int Cin, int F, int K);

@@ -113,7 +113,10 @@ k_fc_wgrad_reduce(int Cin, int Cout, int nchunk, const float *__restrict__ parti
 // dlogits = (p - onehot) / M.
 constexpr int kMaxK = 16;
 
-template <typename TS>
+// SQ: the squared error of Eq. (14) against the one-hot label, summed over
+// the classes, instead of the cross-entropy; its logit gradient is
+// 2/M p_j ((p_j - y_j) - sum_k p_k (p_k - y_k)).
+template <typename TS, bool SQ>
 __global__ void __launch_bounds__(kThreads)
 k_softmax(long long M, int Cin, int K, const TS *__restrict__ x, const TS *__restrict__ w,
           const TS *__restrict__ b, const int32_t *__restrict__ labels, float *__restrict__ p,
@@ -143,9 +146,24 @@ k_softmax(long long M, int Cin, int K, const TS *__restrict__ x, const TS *__res
             // reading outside the row.
             const int lab = labels[m];
             const bool ok = lab >= 0 && lab < K;
-            l = ok ? -logf(z[lab] * inv) : NAN;
-            for (int k = 0; k < K; ++k)
-                dlogits[m * K + k] = ok ? (z[k] * inv - (k == lab ? 1.0f : 0.0f)) / (float)M : NAN;
+            if (SQ) {
+                float e = 0.0f, sd = 0.0f;
+                for (int k = 0; k < K; ++k) {
+                    const float pk = z[k] * inv, dk = pk - (k == lab ? 1.0f : 0.0f);
+                    e += dk * dk;
+                    sd += pk * dk;
+                }
+                l = ok ? e : NAN;
+                for (int k = 0; k < K; ++k) {
+                    const float pk = z[k] * inv, dk = pk - (k == lab ? 1.0f : 0.0f);
+                    dlogits[m * K + k] = ok ? 2.0f * pk * (dk - sd) / (float)M : NAN;
+                }
+            } else {
+                l = ok ? -logf(z[lab] * inv) : NAN;
+                for (int k = 0; k < K; ++k)
+                    dlogits[m * K + k] =
+                        ok ? (z[k] * inv - (k == lab ? 1.0f : 0.0f)) / (float)M : NAN;
+            }
         }
     }
     if (labels) {
@@ -296,7 +314,7 @@ k_fc_dx_rows(long long M, int Cin, int Cout, RowGrad rg, const float *__restrict
 
 // Softmax head, one thread per row: logits in registers (K <= 16), the
 // label's probability picked by comparison (no dynamically indexed arrays).
-template <typename TS>
+template <typename TS, bool SQ>
 __global__ void __launch_bounds__(kRB)
 k_softmax_rows(long long M, int Cin, int K, const TS *__restrict__ x, const TS *__restrict__ w,
                const TS *__restrict__ b, const int32_t *__restrict__ labels,
@@ -344,11 +362,26 @@ k_softmax_rows(long long M, int Cin, int K, const TS *__restrict__ x, const TS *
             // An out-of-range label poisons the loss with NaN.
             const int lab = labels[m0 + r];
             const bool ok = lab >= 0 && lab < K;
-            float pl = 0.0f;
+            if (SQ) {
+                // squared error; sum_k p_k (p_k - y_k) kept in the row's pad slot
+                float e = 0.0f, sd = 0.0f;
 #pragma unroll
-            for (int k = 0; k < 16; ++k)
-                if (k == lab) pl = z[k] * inv;
-            l = ok ? -logf(pl) : NAN;
+                for (int k = 0; k < 16; ++k) {
+                    if (k < K) {
+                        const float pk = z[k] * inv, dk = pk - (k == lab ? 1.0f : 0.0f);
+                        e += dk * dk;
+                        sd += pk * dk;
+                    }
+                }
+                l = ok ? e : NAN;
+                ps[r * (K + 1) + K] = sd;
+            } else {
+                float pl = 0.0f;
+#pragma unroll
+                for (int k = 0; k < 16; ++k)
+                    if (k == lab) pl = z[k] * inv;
+                l = ok ? -logf(pl) : NAN;
+            }
         }
     }
     __syncthreads();
@@ -360,8 +393,9 @@ k_softmax_rows(long long M, int Cin, int K, const TS *__restrict__ x, const TS *
             const int rr = e / K, k = e - (e / K) * K;
             const int lab = labels[m0 + rr];
             const bool ok = lab >= 0 && lab < K;
-            dlogits[(m0 + rr) * K + k] =
-                ok ? (ps[rr * (K + 1) + k] - (k == lab ? 1.0f : 0.0f)) / (float)M : NAN;
+            const float pk = ps[rr * (K + 1) + k], dk = pk - (k == lab ? 1.0f : 0.0f);
+            const float g = SQ ? 2.0f * pk * (dk - ps[rr * (K + 1) + K]) : dk;
+            dlogits[(m0 + rr) * K + k] = ok ? g / (float)M : NAN;
         }
         __shared__ float red[kRB];
         red[threadIdx.x] = l;
@@ -917,10 +951,11 @@ static int fc_tanh_backward_impl(long long M, int Cin, int Cout, const float *x,
     return fc_wgrad(M, Cin, Cout, rg, x, dw, db, partial, st);
 }
 
-static int softmax_ce_impl(long long M, int Cin, int K, int dtype, const void *x,
-                           const void *w, const void *b, const int32_t *labels, float *p,
-                           float *loss, float *dx, float *dw, float *db, void *ws,
-                           hipStream_t st)
+template <bool SQ>
+static int softmax_loss_impl(long long M, int Cin, int K, int dtype, const void *x,
+                             const void *w, const void *b, const int32_t *labels, float *p,
+                             float *loss, float *dx, float *dw, float *db, void *ws,
+                             hipStream_t st)
 {
     Carve cv(ws);
     float *partial = cv.take<float>((size_t)fc_chunks(M) * K * (Cin + 1));
@@ -931,19 +966,19 @@ static int softmax_ce_impl(long long M, int Cin, int K, int dtype, const void *x
         nb = (unsigned)((M + kRB - 1) / kRB);
         const size_t lds = rows_lds(Cin, 16, K * (Cin + 1));
         if (dtype == PLSTM_BF16)
-            k_softmax_rows<uint16_t><<<nb, kRB, lds, st>>>(
+            k_softmax_rows<uint16_t, SQ><<<nb, kRB, lds, st>>>(
                 M, Cin, K, (const uint16_t *)x, (const uint16_t *)w, (const uint16_t *)b, labels,
                 p, dlogits, lossp);
         else
-            k_softmax_rows<float><<<nb, kRB, lds, st>>>(
+            k_softmax_rows<float, SQ><<<nb, kRB, lds, st>>>(
                 M, Cin, K, (const float *)x, (const float *)w, (const float *)b, labels, p,
                 dlogits, lossp);
     } else if (dtype == PLSTM_BF16) {
-        k_softmax<uint16_t><<<nb, kThreads, 0, st>>>(M, Cin, K, (const uint16_t *)x,
+        k_softmax<uint16_t, SQ><<<nb, kThreads, 0, st>>>(M, Cin, K, (const uint16_t *)x,
                                                       (const uint16_t *)w, (const uint16_t *)b,
                                                       labels, p, dlogits, lossp);
     } else {
-        k_softmax<float><<<nb, kThreads, 0, st>>>(M, Cin, K, (const float *)x, (const float *)w,
+        k_softmax<float, SQ><<<nb, kThreads, 0, st>>>(M, Cin, K, (const float *)x, (const float *)w,
                                                    (const float *)b, labels, p, dlogits, lossp);
     }
     PLSTM_LAUNCH_CHECK();
@@ -980,10 +1015,14 @@ int fc_tanh_backward(long long M, int Cin, int Cout, const float *x, const float
 
 int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void *w,
                const void *b, const int32_t *labels, float *p, float *loss, float *dx,
-               float *dw, float *db, void *ws, hipStream_t st)
+               float *dw, float *db, void *ws, hipStream_t st, bool squared)
 {
-    timing_begin("softmax_ce", st);
-    const int rc = softmax_ce_impl(M, Cin, K, dtype, x, w, b, labels, p, loss, dx, dw, db, ws, st);
+    timing_begin(squared ? "softmax_sq" : "softmax_ce", st);
+    const int rc =
+        squared ? softmax_loss_impl<true>(M, Cin, K, dtype, x, w, b, labels, p, loss, dx, dw, db,
+                                          ws, st)
+                : softmax_loss_impl<false>(M, Cin, K, dtype, x, w, b, labels, p, loss, dx, dw, db,
+                                           ws, st);
     timing_end(1 + (labels ? 1 : 0) + (dw ? 2 : 0) + (dx ? 1 : 0), st);
     return rc;
 }

@@ -74,9 +74,10 @@ def workspace_for_layers(x_shape, shapes, dtype, training: bool, device):
 
 def network_forward(x, layers: List[LayerW], fcs: List[Tuple[torch.Tensor, torch.Tensor]],
                     head: Tuple[torch.Tensor, torch.Tensor], labels: Optional[torch.Tensor] = None,
-                    training: bool = False, ws=None, stream=None):
+                    training: bool = False, ws=None, stream=None, loss: str = "ce"):
     """Returns dict: 'p' [M][K] fp32, 'loss' (device scalar, with labels),
-    'acts' (per-layer inputs/outputs and saved activations for training)."""
+    'acts' (per-layer inputs/outputs and saved activations for training).
+    loss: "ce" (mean cross-entropy) or "sq" (squared error, Eq. (14))."""
     N, D, H, W, _ = x.shape
     M = N * D * H * W
     if len(fcs) not in (len(layers), len(layers) - 1):
@@ -100,21 +101,25 @@ def network_forward(x, layers: List[LayerW], fcs: List[Tuple[torch.Tensor, torch
     if labels is None:
         pyramid_softmax_ce(a.view(M, -1), head[0], head[1], p, stream=stream)
         return out
-    loss = torch.empty(1, dtype=torch.float32, device=x.device)
-    out["loss"] = loss
+    if loss not in ("ce", "sq"):
+        raise ValueError("loss must be 'ce' or 'sq'")
+    lval = torch.empty(1, dtype=torch.float32, device=x.device)
+    out["loss"] = lval
     if training:
         dlast = torch.empty((M, a.shape[-1]), dtype=torch.float32, device=x.device)
         dw = torch.empty_like(head[0])
         db = torch.empty_like(head[1])
-        pyramid_softmax_ce(a.view(M, -1), head[0], head[1], p, labels, loss, dlast, dw, db,
-                           stream=stream)
+        pyramid_softmax_ce(a.view(M, -1), head[0], head[1], p, labels, lval, dlast, dw, db,
+                           stream=stream, squared=loss == "sq")
         out.update({"dlast": dlast, "head_grad": (dw, db)})
     else:
-        pyramid_softmax_ce(a.view(M, -1), head[0], head[1], p, labels, loss, stream=stream)
+        pyramid_softmax_ce(a.view(M, -1), head[0], head[1], p, labels, lval, stream=stream,
+                           squared=loss == "sq")
     return out
 
 
-def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None, fused_head=True):
+def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None, fused_head=True,
+                       loss="ce"):
     """Forward + back-propagation through the whole network (fp32).
     Returns dict with 'loss', 'p', 'head' (dw, db), 'fcs' [(dw, db)],
     'layers' [(dwx, dwh, db)].  With `fused_head` (default) the last FC + tanh,
@@ -124,9 +129,9 @@ def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None, fused
     M = N * D * H * W
     nl = len(layers)
     O_last, F_last, K = layers[-1].O, fcs[-1][0].shape[0], head[0].shape[0]
-    if not (fused_head and len(fcs) == nl and
+    if not (fused_head and loss == "ce" and len(fcs) == nl and
             pyramid_head_workspace_size(M, O_last, F_last, K) > 0):
-        return _train_step_unfused(x, layers, fcs, head, labels, ws, stream)
+        return _train_step_unfused(x, layers, fcs, head, labels, ws, stream, loss)
     a = x
     acts = []
     for li in range(nl):
@@ -140,12 +145,12 @@ def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None, fused
             a = y
         acts.append(act)
     p = torch.empty((M, K), dtype=torch.float32, device=x.device)
-    loss = torch.empty(1, dtype=torch.float32, device=x.device)
+    lval = torch.empty(1, dtype=torch.float32, device=x.device)
     dh = torch.empty((M, O_last), dtype=torch.float32, device=x.device)
     wf, bf = fcs[-1]
     dwf, dbf = torch.empty_like(wf), torch.empty_like(bf)
     dw, db = torch.empty_like(head[0]), torch.empty_like(head[1])
-    pyramid_head_train(acts[-1]["h"].view(M, O_last), wf, bf, head[0], head[1], labels, p, loss,
+    pyramid_head_train(acts[-1]["h"].view(M, O_last), wf, bf, head[0], head[1], labels, p, lval,
                        dh, dwf, dbf, dw, db, stream=stream)
     fc_grads = [None] * len(fcs)
     layer_grads = [None] * nl
@@ -166,12 +171,13 @@ def network_train_step(x, layers, fcs, head, labels, ws=None, stream=None, fused
                                             stream=stream)
         layer_grads[li] = (dwx, dwh, db_l)
         g = dx
-    return {"loss": loss, "p": p, "head": (dw, db), "fcs": fc_grads, "layers": layer_grads}
+    return {"loss": lval, "p": p, "head": (dw, db), "fcs": fc_grads, "layers": layer_grads}
 
 
-def _train_step_unfused(x, layers, fcs, head, labels, ws=None, stream=None):
+def _train_step_unfused(x, layers, fcs, head, labels, ws=None, stream=None, loss="ce"):
     """network_train_step composed from the separate FC / softmax entry points."""
-    out = network_forward(x, layers, fcs, head, labels, training=True, ws=ws, stream=stream)
+    out = network_forward(x, layers, fcs, head, labels, training=True, ws=ws, stream=stream,
+                          loss=loss)
     acts = out["acts"]
     g = out["dlast"]
     N, D, H, W, _ = x.shape

@@ -104,6 +104,52 @@ def test_paper_network_forward_bf16():
     assert normwise(host(out["p"]), ref) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("cin", [16, 200], ids=["rows", "wide"])
+def test_softmax_squared_loss_matches_oracle(cin):
+    """The squared loss of Eq. (14) on the softmax output, and its gradient,
+    on both softmax kernels (rows staged in LDS, and the wide-input one)."""
+    import oracle.loss as oloss
+    import paper_1506_07452_amd as P
+    rng = np.random.default_rng(93 + cin)
+    M, K = 1037, 5
+    xa = rng.standard_normal((M, cin)).astype(np.float32)
+    w = rng.uniform(-0.3, 0.3, (K, cin)).astype(np.float32)
+    b = rng.uniform(-0.3, 0.3, K).astype(np.float32)
+    lab = rng.integers(0, K, M).astype(np.int32)
+    say("softmax squared loss", cin)
+    p = torch.empty(M, K, device=DEV)
+    loss = torch.empty(1, device=DEV)
+    dx, dw, db = (torch.empty(M, cin, device=DEV), torch.empty(K, cin, device=DEV),
+                  torch.empty(K, device=DEV))
+    P.pyramid_softmax_sq(dev(xa), dev(w), dev(b), p, torch.from_numpy(lab).to(DEV), loss, dx,
+                         dw, db)
+    torch.cuda.synchronize()
+    ref = oloss.softmax_sq(xa, w, b, lab, grad=True)
+    assert normwise(host(p), ref["p"]) <= TOL["f32"]
+    assert abs(loss.item() - ref["loss"]) <= TOL["f32"] * ref["loss"]
+    for got, want in ((dx, ref["dx"]), (dw, ref["dw"]), (db, ref["db"])):
+        assert normwise(host(got), want) <= TOL["f32"]
+
+
+def test_paper_network_training_step_squared_loss():
+    """The paper's network trained as in Section 3: squared loss, every
+    gradient against the oracle."""
+    inst = paper_small(99)
+    ref = onet.backward(inst.x, *oracle_args(inst), inst.labels, loss="sq")
+    say("paper network squared loss")
+    x, layers, fcs, head, labels = to_device(inst, "f32")
+    g = network_train_step(x, layers, fcs, head, labels, loss="sq")
+    torch.cuda.synchronize()
+    assert abs(g["loss"].item() - ref["loss"]) <= TOL["f32"] * abs(ref["loss"])
+    pairs = [(g["head"][0], ref["head"][0]), (g["head"][1], ref["head"][1])]
+    for li in range(2):
+        pairs += list(zip(g["fcs"][li], ref["fcs"][li]))
+    for li in range(3):
+        pairs += list(zip(g["layers"][li], ref["layers"][li]))
+    for got, want in pairs:
+        assert normwise(host(got), want) <= TOL["f32"]
+
+
 def test_rmsprop_matches_oracle():
     """Three RMS-prop updates (Section 3, Eq. (15)-(18)) of four tensors of
     ragged sizes in one launch each, against the fp64 oracle fed the same

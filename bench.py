@@ -183,7 +183,9 @@ def bench_network(args, cfg):
 
     def step():
         if train:
-            g = network_train_step(x, layers, fcs, head, labels, ws=ws)
+            # the paper trains on the squared loss of Eq. (14)
+            g = network_train_step(x, layers, fcs, head, labels, ws=ws,
+                                   loss="sq" if cfg is None else "ce")
             if opt is not None:
                 opt.step(network_gradients(g), 0)
             return g
@@ -210,7 +212,8 @@ def bench_network(args, cfg):
         "dtype": wl.dtype,
         "data": "synthetic",
         "config": {"workload": wl.name + (", fwd+bwd" if train else ", fwd") +
-                               (" + RMS-prop update" if opt is not None else ""), "N": wl.N,
+                               (" + RMS-prop update, squared loss" if opt is not None else ""),
+                   "N": wl.N,
                    "D": wl.D, "H": wl.H, "W": wl.W, "C": wl.C, "hidden": wl.hidden,
                    "fc": [wl.fc_width(i) for i in range(len(wl.hidden))], "K": wl.K,
                    "storage": wl.dtype, "classes": wl.classes},

@@ -770,26 +770,27 @@ k_step_bwd(BwdStepArgs a)
 
 // ---- parameter gradients ----------------------------------------------------
 // dW[d][m][k] = sum over the voxels of direction d of dA[v][m] col[v][k],
-// col = [im2col(h_{t-1}) (9 O) | im2col(x_t) (9 C') | 1]; K of the MFMA runs
-// over voxels.  A wave owns 4 M-tiles x up to kWgN N-tiles of one direction,
-// all of the h part or all of the x part (+ the bias column), and a chunk
-// of the direction's voxels, visited as units of 16 pixels of a row (lane
-// group q takes pixels 4q .. 4q+3, one per k-step), walking each column
-// group down the rows so that the rows read for one unit are re-read from
-// cache by the next two.  The partial sums of the chunks are added in order.
-constexpr int kWgN = 8;
-constexpr int kWgTarget = 170;   // waves per direction (about one per SIMD in all)
+// col = [im2col(h_{t-1}) (KK O) | im2col(x_t) (KK C')]; K of the MFMA runs over
+// voxels.  A wave owns 4 M-tiles x NTL N-tiles of one direction, all of the
+// h part or all of the x part, and a chunk of the direction's voxels,
+// visited as units of 16 pixels of a row (lane group q takes pixels
+// 4q .. 4q+3, one per k-step), walking each column group down the rows so
+// that the rows read for one unit are re-read from cache by the next ones.
+// The partial sums of the chunks are added in order.  db = sum_v dA[v] is a
+// separate column sum of dA.
+constexpr int kWgN = 8;          // most N-tiles a wave holds
+constexpr int kWgMaxChunks = 64;
 
-// N-tiles per block: the h part (9U tiles) and the x part with the bias
-// tile (9 C'/16 + 1 tiles) are each cut into blocks of at most kWgN.
+// N-tiles per block: each part (KK U tiles of h, KK C'/16 tiles of x) is cut
+// into the fewest blocks of at most kWgN tiles, as even as possible.
 struct WgBlocks {
     int nh, nx;       // blocks of each part
-    int th, tx;       // tiles per block of each part (last block may have fewer)
+    int th, tx;       // tiles per block of each part (the last block may have fewer)
 };
 __host__ __device__ inline WgBlocks wg_blocks(int U, int CX, int KK)
 {
     WgBlocks w;
-    const int h = KK * U, x = KK * CX + 1;
+    const int h = KK * U, x = KK * CX;
     w.nh = (h + kWgN - 1) / kWgN;
     w.nx = (x + kWgN - 1) / kWgN;
     w.th = (h + w.nh - 1) / w.nh;
@@ -800,78 +801,54 @@ __host__ __device__ inline WgBlocks wg_blocks(int U, int CX, int KK)
 struct WgStepArgs {
     Geom g;
     int Cp;
-    int NTt;                  // N-tiles: KK U + KK C'/16 + 1
-    int k_mul;                // ceil(2^16 / K)
+    int NTt;                  // N-tiles: KK U + KK C'/16
     int kch;                  // voxel chunks per (direction, M-block, N-block)
+    int k_mul;                // ceil(2^16 / K)
     const float *xp, *hd, *dA;
     float *partial;           // [6][kch][4O][16 NTt]
 };
 
-template <int U>
-__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(1)))
-k_wgrad_step(WgStepArgs a)
+// The wave's share: NTL tiles (compile time) of which `ntl` are real.
+template <int U, int NTL>
+__device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, bool is_h, int t0,
+                               int ntl, int first_nt)
 {
     constexpr int O = 16 * U, G = 4 * O;
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
-    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int Cp = a.Cp, CX = Cp >> 4;
     const int K = a.g.K, KK = K * K, rad = K >> 1;
-    const WgBlocks wb = wg_blocks(U, CX, KK);
-    const int nblk = wb.nh + wb.nx;
-    const int per_dir = U * nblk * a.kch;
-    if (item >= kDirs * per_dir) return;
-    const int d = item / per_dir;
-    int r = item - d * per_dir;
-    const int kc = r % a.kch;
-    r /= a.kch;
-    const int nb = r % nblk, mblk = r / nblk;
-    const bool is_h = nb < wb.nh;
-    // first N-tile and tile count of this block; tiles of the x part are
-    // numbered from 0 after the h part
-    const int t0 = is_h ? nb * wb.th : (nb - wb.nh) * wb.tx;
-    const int tend = is_h ? KK * U : KK * CX + 1;
-    const int ntl = (t0 + (is_h ? wb.th : wb.tx) < tend ? (is_h ? wb.th : wb.tx) : tend - t0);
-    const int first_nt = (is_h ? 0 : KK * U) + t0;
     const DirGeom dg = a.g.dir[d];
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
     const int P = dg.P, Q = dg.Q;
     const long long V = a.g.V;
+    const int Cp = a.Cp, CX = Cp >> 4;
     const int ngrp = (Q + 15) >> 4;
     const int cbn = is_h ? U : CX;              // channel blocks per tap
     const int stride = is_h ? O : Cp;           // floats per voxel of the source
 
-    // per tile: tap offsets (uniform) and this lane's channel; the bias
-    // tile (last of the x part) is 1 in its first column and loads nothing
-    int dtap[kWgN], chn[kWgN];
-    float one[kWgN];
+    // per tile: tap offset in the slice (uniform), tap row and column
+    // (packed, uniform) and this lane's channel (-1: a tile past the part)
+    int dtap[NTL], chn[NTL];
+    unsigned tapok[NTL];
 #pragma unroll
-    for (int j = 0; j < kWgN; ++j) {
+    for (int j = 0; j < NTL; ++j) {
         const int tt = t0 + j;
-        const bool bias = !is_h && tt == KK * CX;
-        const int tap = bias || j >= ntl ? KK / 2 : tt / cbn;
-        const int ka = tap / K - rad, kb = tap % K - rad;
-        dtap[j] = __builtin_amdgcn_readfirstlane(ka * sp + kb * sq);
-        chn[j] = (bias || j >= ntl) ? -1 : (tt % cbn) * 16 + col;
-        one[j] = (bias && col == 0) ? 1.0f : 0.0f;
-        (void)tap;
-    }
-    unsigned tapok[kWgN];   // per tile: tap row and column (3 bits each), packed
-#pragma unroll
-    for (int j = 0; j < kWgN; ++j) {
-        const int tt = t0 + j;
-        const int tap = (!is_h && tt == KK * CX) || j >= ntl ? KK / 2 : tt / cbn;
-        tapok[j] = __builtin_amdgcn_readfirstlane((tap / K) | (tap % K) << 3);
+        const bool real = j < ntl;
+        const int tap = real ? tt / cbn : KK / 2;
+        const int ka = tap / K, kb = tap % K;
+        dtap[j] = __builtin_amdgcn_readfirstlane((ka - rad) * sp + (kb - rad) * sq);
+        tapok[j] = __builtin_amdgcn_readfirstlane(ka | kb << 3);
+        chn[j] = real ? (tt % cbn) * 16 + col : -1;
     }
 
-    f4 acc[4][kWgN];
+    f4 acc[4][NTL];
 #pragma unroll
     for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int j = 0; j < kWgN; ++j) acc[m][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int j = 0; j < NTL; ++j) acc[m][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
     struct Ops {
         float a[4][4];            // [k-step][M-tile]
-        float b[4][kWgN];         // [k-step][N-tile]
+        float b[4][NTL];          // [k-step][N-tile]
     };
     struct Cursor {
         int n, t, qg, p;
@@ -902,7 +879,7 @@ k_wgrad_step(WgStepArgs a)
         }
     };
     // Branch-free loads: an operand outside the volume, of h_{-1} or of a
-    // zero tile gets an out-of-range offset.
+    // tile past the part gets an out-of-range offset.
     auto load = [&](const Cursor &c, bool live_unit, Ops &o) {
         const long long sb = ((long long)d * a.g.N + c.n) * V;
         const auto rs_a = slice_rsrc(a.dA + sb * G, V * G);
@@ -922,7 +899,7 @@ k_wgrad_step(WgStepArgs a)
                     bload1(rs_a, sel_off(live, (unsigned)(v * G + mblk * 64 + m * 16 + col) * 4u));
             const int vb = pl * ss + c.p * sp + qq * sq;
 #pragma unroll
-            for (int j = 0; j < kWgN; ++j) {
+            for (int j = 0; j < NTL; ++j) {
                 const int pp = c.p + (int)(tapok[j] & 7) - rad, qn = qq + (int)(tapok[j] >> 3) - rad;
                 const bool ok = src_ok & (chn[j] >= 0) & ((unsigned)pp < (unsigned)P) &
                                 ((unsigned)qn < (unsigned)Q);
@@ -942,8 +919,8 @@ k_wgrad_step(WgStepArgs a)
 #pragma unroll
             for (int m = 0; m < 4; ++m)
 #pragma unroll
-                for (int j = 0; j < kWgN; ++j)
-                    acc[m][j] = mfma(cur.a[ks][m], cur.b[ks][j] + one[j], acc[m][j]);
+                for (int j = 0; j < NTL; ++j)
+                    acc[m][j] = mfma(cur.a[ks][m], cur.b[ks][j], acc[m][j]);
         cur = nxt;
     }
     const int KCp = a.NTt * 16;
@@ -951,7 +928,7 @@ k_wgrad_step(WgStepArgs a)
 #pragma unroll
     for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int j = 0; j < kWgN; ++j) {
+        for (int j = 0; j < NTL; ++j) {
             if (j >= ntl) continue;
             const int nt = first_nt + j;
 #pragma unroll
@@ -961,28 +938,85 @@ k_wgrad_step(WgStepArgs a)
         }
 }
 
+template <int U>
+__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(1)))
+k_wgrad_step(WgStepArgs a)
+{
+    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int Cp = a.Cp, CX = Cp >> 4;
+    const int KK = a.g.K * a.g.K;
+    const WgBlocks wb = wg_blocks(U, CX, KK);
+    const int nblk = wb.nh + wb.nx;
+    const int per_dir = U * nblk * a.kch;
+    if (item >= kDirs * per_dir) return;
+    const int d = item / per_dir;
+    int r = item - d * per_dir;
+    const int kc = r % a.kch;
+    r /= a.kch;
+    const int nb = r % nblk, mblk = r / nblk;
+    const bool is_h = nb < wb.nh;
+    // first N-tile and tile count of this block; x tiles numbered after h's
+    const int tb = is_h ? wb.th : wb.tx;
+    const int t0 = is_h ? nb * wb.th : (nb - wb.nh) * wb.tx;
+    const int tend = is_h ? KK * U : KK * CX;
+    const int ntl = t0 + tb < tend ? tb : tend - t0;
+    const int first_nt = (is_h ? 0 : KK * U) + t0;
+    if (ntl <= 4)
+        wg_wave<U, 4>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+    else if (ntl <= 6)
+        wg_wave<U, 6>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+    else
+        wg_wave<U, 8>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+}
+
+// db: column sums of dA over the voxels of each direction, in fixed chunks
+// (partials[d][chunk][4O]), then the chunks in order.
+constexpr int kDbChunks = 512;
+
+__global__ void __launch_bounds__(256)
+k_db_partial(int G, long long nvox, const float *__restrict__ dA, float *__restrict__ part)
+{
+    const int d = blockIdx.y, ch = blockIdx.x;
+    const long long v0 = nvox * ch / kDbChunks, v1 = nvox * (ch + 1) / kDbChunks;
+    const float *src = dA + (long long)d * nvox * G;
+    for (int m = threadIdx.x; m < G; m += 256) {
+        float acc = 0.0f;
+        for (long long v = v0; v < v1; ++v) acc += src[v * G + m];
+        part[((long long)d * kDbChunks + ch) * G + m] = acc;
+    }
+}
+
+__global__ void __launch_bounds__(256)
+k_db_reduce(int G, const float *__restrict__ part, float *__restrict__ db)
+{
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= kDirs * G) return;
+    const int d = i / G, m = i % G;
+    float acc = 0.0f;
+    for (int ch = 0; ch < kDbChunks; ++ch) acc += part[((long long)d * kDbChunks + ch) * G + m];
+    db[i] = acc;
+}
+
 // dW = sum of the chunk partials in chunk order, scattered to the ABI layouts.
 __global__ void __launch_bounds__(256)
 k_wgrad_step_reduce(int O, int C, int Cp, int KK, int NTt, int kch,
                     const float *__restrict__ partial, float *__restrict__ dwx,
-                    float *__restrict__ dwh, float *__restrict__ db)
+                    float *__restrict__ dwh)
 {
-    const int G = 4 * O, KC = KK * (O + Cp) + 1, KCp = NTt * 16;
+    const int G = 4 * O, KC = KK * (O + Cp), KCp = NTt * 16;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
     if (i >= (long long)kDirs * G * KC) return;
     const int k = (int)(i % KC);
     const int gu = (int)((i / KC) % G);
     const int d = (int)(i / ((long long)KC * G));
-    if (k >= KK * O && k < KK * (O + Cp) && (k - KK * O) % Cp >= C) return;   // padding channel
+    if (k >= KK * O && (k - KK * O) % Cp >= C) return;   // padding channel
     float acc = 0.0f;
     for (int c = 0; c < kch; ++c) acc += partial[(((long long)d * kch + c) * G + gu) * KCp + k];
     if (k < KK * O) {
         dwh[(((long long)d * G + gu) * O + k % O) * KK + k / O] = acc;
-    } else if (k < KK * (O + Cp)) {
+    } else {
         const int kx = k - KK * O;
         dwx[(((long long)d * G + gu) * C + kx % Cp) * KK + kx / Cp] = acc;
-    } else {
-        db[(long long)d * G + gu] = acc;
     }
 }
 
@@ -1115,15 +1149,28 @@ inline int max_T(const Geom &g)
 struct WgShape {
     int NTt, nblk, kch;
 };
+// Voxel chunks per (direction, block): one wave per SIMD at a time, so the
+// launch takes ceil(waves / SIMDs) rounds of 1/kch of a block's work; pick
+// the chunk count that minimises that (ties: fewer chunks).
 inline WgShape wg_shape(const Geom &g)
 {
     const int U = g.O / 16, CX = pad16(g.C) / 16, KK = g.K * g.K;
     const WgBlocks wb = wg_blocks(U, CX, KK);
     WgShape w;
-    w.NTt = KK * U + KK * CX + 1;
+    w.NTt = KK * U + KK * CX;
     w.nblk = wb.nh + wb.nx;
-    const int per = U * w.nblk;
-    w.kch = kWgTarget / per > 1 ? kWgTarget / per : 1;
+    const DevInfo di = device_info();
+    const long long simds = 4LL * (di.cus > 0 ? di.cus : 256);
+    const long long per = (long long)kDirs * U * w.nblk;
+    double best = 1e30;
+    w.kch = 1;
+    for (int k = 1; k <= kWgMaxChunks; ++k) {
+        const double cost = (double)((per * k + simds - 1) / simds) / k;
+        if (cost < best * (1.0 - 1e-9)) {
+            best = cost;
+            w.kch = k;
+        }
+    }
     return w;
 }
 
@@ -1368,6 +1415,7 @@ size_t step_bwd_ws(const Geom &g)
     cv.take<float>((size_t)g.N * g.V * Cp);                        // padded x
     cv.take<float>((size_t)kDirs * w.kch * G * w.NTt * 16);        // weight-gradient partials
     cv.take<float>((size_t)kDirs * KK * 4 * U * (Cp / 16) * 256);  // W_x^T fragments
+    cv.take<float>((size_t)kDirs * kDbChunks * G);                 // db partials
     return cv.off;
 }
 
@@ -1422,6 +1470,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     float *xp = cv.take<float>((size_t)g.N * g.V * Cp);
     float *partial = cv.take<float>((size_t)kDirs * w.kch * G * w.NTt * 16);
     float *fragx = cv.take<float>((size_t)kDirs * KK * 4 * U * (Cp / 16) * 256);
+    float *dbpart = cv.take<float>((size_t)kDirs * kDbChunks * G);
     const long long nvox = (long long)g.N * g.V;
 
     timing_begin("sweep_bwd_step", st);
@@ -1461,11 +1510,15 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     default: k_wgrad_step<4><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
     }
     PLSTM_LAUNCH_CHECK();
-    const long long nout = (long long)kDirs * G * (KK * (g.O + Cp) + 1);
+    const long long nout = (long long)kDirs * G * KK * (g.O + Cp);
     k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.O, g.C, Cp, KK, w.NTt, w.kch,
-                                                               partial, dwx, dwh, db);
+                                                               partial, dwx, dwh);
     PLSTM_LAUNCH_CHECK();
-    timing_end(3, st);
+    k_db_partial<<<dim3(kDbChunks, kDirs), 256, 0, st>>>(G, nvox, dA, dbpart);
+    PLSTM_LAUNCH_CHECK();
+    k_db_reduce<<<blocks_for(kDirs * G, 256), 256, 0, st>>>(G, dbpart, db);
+    PLSTM_LAUNCH_CHECK();
+    timing_end(5, st);
     if (dx) return step_dx(g, wx, dA, fragx, dx, st);
     return PLSTM_OK;
 }

@@ -614,3 +614,59 @@ def test_network_squared_loss_finite_differences():
             an = grad.reshape(-1)[k]
             assert abs(fd - an) <= 1e-9 + 1e-5 * abs(an), (fd, an)
 
+
+# ------------------------------------------------- test-time stitching (Section 3)
+import oracle.stitch as ostitch
+
+
+def test_tile_starts_cover_every_voxel():
+    for extent, size, stride in [(48, 25, 12), (240, 128, 96), (7, 9, 4), (10, 5, 5), (11, 4, 3)]:
+        starts, sz = ostitch.tile_starts(extent, size, stride)
+        cover = np.zeros(extent, dtype=int)
+        for s0 in starts:
+            cover[s0:s0 + sz] += 1
+        assert cover.min() >= 1 and starts[0] == 0 and starts[-1] + sz == extent
+        assert sz == min(size, extent)
+
+
+def test_gaussian_weights_closed_form():
+    w = ostitch.gaussian_weights((3, 4, 5), 0.25)
+    # centre of the odd axes, between the two middle voxels of the even one
+    z, y, x = 1, 1, 2
+    expect = math.exp(-0.5 * (((y - 1.5) / 1.0) ** 2))
+    assert w[z, y, x] == pytest.approx(expect, rel=1e-15)
+    corner = math.exp(-0.5 * ((1 / 0.75) ** 2 + (1.5 / 1.0) ** 2 + (2 / 1.25) ** 2))
+    assert w[0, 0, 0] == pytest.approx(corner, rel=1e-14)
+
+
+def test_stitch_of_a_consistent_field_is_the_field():
+    """Tiles that all report the same per-voxel values (a fixed field cut
+    into tiles) stitch back to that field exactly, overlap or not; one tile
+    covering the volume returns its output unchanged."""
+    rng = np.random.default_rng(170)
+    D, H, W, K = 6, 9, 7, 3
+    field = rng.random((D, H, W, K))
+
+    def fn(z0, y0, x0, d, h, w):
+        return field[z0:z0 + d, y0:y0 + h, x0:x0 + w]
+
+    for tile, stride in [((3, 4, 4), (2, 3, 2)), ((6, 9, 7), (6, 9, 7)), ((2, 5, 3), (2, 5, 3))]:
+        np.testing.assert_allclose(ostitch.stitch((D, H, W), tile, stride, fn, K), field,
+                                   rtol=1e-14, atol=0)
+
+
+def test_stitch_two_tiles_by_hand():
+    """Two tiles overlapping on one voxel along x: that voxel is the
+    Gaussian-weighted mean of the two tiles' values, the others keep their
+    tile's value."""
+    D, H, W, K = 1, 1, 5, 1
+    vals = {0: 1.0, 2: 3.0}
+
+    def fn(z0, y0, x0, d, h, w):
+        return np.full((d, h, w, K), vals[x0])
+
+    out = ostitch.stitch((D, H, W), (1, 1, 3), (1, 1, 2), fn, K)
+    g = ostitch.gaussian_weights((1, 1, 3))[0, 0]
+    np.testing.assert_allclose(out[0, 0, [0, 1, 3, 4], 0], [1.0, 1.0, 3.0, 3.0], rtol=1e-15)
+    assert out[0, 0, 2, 0] == pytest.approx((g[2] * 1.0 + g[0] * 3.0) / (g[2] + g[0]), rel=1e-15)
+

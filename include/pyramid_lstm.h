@@ -226,6 +226,38 @@ int pyramid_rmsprop_step(int32_t count, const plstm_param_segment *segs, float l
  * (host function). */
 double pyramid_rmsprop_learning_rate(int32_t epoch);
 
+/* ---- inference over volumes larger than one pass (Section 3, "Sub-volumes
+ * and Augmentation") -------------------------------------------------------- */
+
+/* Copies the sub-volume [z0, z0+d) x [y0, y0+h) x [x0, x0+w) of batch element n
+ * of x [N][D][H][W][C] (storage `dtype`) into tile [d][h][w][C], same type.
+ * The box must lie inside the volume (else PLSTM_EINVAL); 4-byte aligned
+ * device pointers. */
+int pyramid_crop(int32_t N, int32_t D, int32_t H, int32_t W, int32_t C, int32_t dtype,
+                 int32_t n, int32_t z0, int32_t y0, int32_t x0, int32_t d, int32_t h, int32_t w,
+                 const void *x, void *tile, void *stream);
+
+/* Gaussian-weighted stitching of per-voxel class probabilities (fp32) into a
+ * D x H x W volume with K classes.  acc [D][H][W][K] and wsum [D][H][W] are
+ * caller-owned fp32 device buffers:
+ *   pyramid_stitch_clear   zeroes them;
+ *   pyramid_stitch_add     adds tile p [d][h][w][K] placed at (z0, y0, x0):
+ *                          acc += g p, wsum += g, with g the separable Gaussian
+ *                          exp(-1/2 sum_axes ((i - c) / (sigma_scale * n))^2)
+ *                          over the tile (c its centre, n its extent per axis);
+ *   pyramid_stitch_finish  out [D][H][W][K] = acc / wsum (every voxel must have
+ *                          been covered by a tile).
+ * Calls on one stream accumulate in call order (deterministic).  Returns
+ * PLSTM_EINVAL for null pointers, a box outside the volume or
+ * sigma_scale <= 0. */
+int pyramid_stitch_clear(int32_t D, int32_t H, int32_t W, int32_t K, void *acc, void *wsum,
+                         void *stream);
+int pyramid_stitch_add(int32_t D, int32_t H, int32_t W, int32_t K, int32_t z0, int32_t y0,
+                       int32_t x0, int32_t d, int32_t h, int32_t w, float sigma_scale,
+                       const void *p, void *acc, void *wsum, void *stream);
+int pyramid_stitch_finish(int32_t D, int32_t H, int32_t W, int32_t K, const void *acc,
+                          const void *wsum, void *out, void *stream);
+
 /* Forward implementation selection, for testing and tuning (process-wide):
  * 0 = automatic (default): the persistent MFMA sweep where it supports the
  * shape (fp32, O = 16, C <= 4, grid co-resident), else the plane-step MFMA

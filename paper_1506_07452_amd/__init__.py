@@ -21,6 +21,7 @@ __all__ = [
     "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
     "pyramid_head_workspace_size", "pyramid_head_train", "plstm_param_segment",
     "pyramid_rmsprop_step", "pyramid_rmsprop_learning_rate", "RMSprop", "pyramid_softmax_sq",
+    "pyramid_crop", "pyramid_stitch_clear", "pyramid_stitch_add", "pyramid_stitch_finish",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
     "pyramid_lstm_set_backward_path", "pyramid_lstm_set_step_split", "pyramid_lstm_set_bf16_mfma",
     "library_path", "load",
@@ -96,6 +97,14 @@ def load():
     lib.pyramid_rmsprop_step.restype = ctypes.c_int
     lib.pyramid_rmsprop_learning_rate.argtypes = [i32]
     lib.pyramid_rmsprop_learning_rate.restype = ctypes.c_double
+    lib.pyramid_crop.argtypes = [i32] * 13 + [vp, vp, vp]
+    lib.pyramid_crop.restype = ctypes.c_int
+    lib.pyramid_stitch_clear.argtypes = [i32] * 4 + [vp, vp, vp]
+    lib.pyramid_stitch_clear.restype = ctypes.c_int
+    lib.pyramid_stitch_add.argtypes = [i32] * 10 + [f32, vp, vp, vp, vp]
+    lib.pyramid_stitch_add.restype = ctypes.c_int
+    lib.pyramid_stitch_finish.argtypes = [i32] * 4 + [vp, vp, vp, vp]
+    lib.pyramid_stitch_finish.restype = ctypes.c_int
     lib.pyramid_lstm_timing_enable.argtypes = [ctypes.c_int]
     lib.pyramid_lstm_timing_enable.restype = ctypes.c_int
     lib.pyramid_lstm_timing_read.argtypes = [ctypes.c_int, ctypes.c_char_p,
@@ -285,6 +294,36 @@ class RMSprop:
     def step(self, grads, epoch: int, stream=None):
         pyramid_rmsprop_step(self.params, list(grads), self.ms, self.mom,
                              pyramid_rmsprop_learning_rate(epoch), stream=stream)
+
+
+def pyramid_crop(x, n, box, tile, stream=None):
+    """tile [d][h][w][C] = x[n, z0:z0+d, y0:y0+h, x0:x0+w, :]; box = (z0, y0,
+    x0, d, h, w)."""
+    N, D, H, W, C = x.shape
+    if tile.dtype != x.dtype or tuple(tile.shape[-4:]) != (box[3], box[4], box[5], C):
+        raise ValueError("tile must be [d][h][w][C] of x's dtype")
+    _check("pyramid_crop", load().pyramid_crop(N, D, H, W, C, _DT[x.dtype], n, *box, _ptr(x),
+                                               _ptr(tile), _stream(stream)))
+
+
+def pyramid_stitch_clear(acc, wsum, stream=None):
+    D, H, W, K = acc.shape
+    _check("pyramid_stitch_clear", load().pyramid_stitch_clear(D, H, W, K, _ptr(acc),
+                                                               _ptr(wsum), _stream(stream)))
+
+
+def pyramid_stitch_add(p, box, acc, wsum, sigma_scale=0.25, stream=None):
+    """acc += g p, wsum += g for the tile p [d][h][w][K] at box (z0, y0, x0, d,
+    h, w) with Gaussian weights g."""
+    D, H, W, K = acc.shape
+    _check("pyramid_stitch_add", load().pyramid_stitch_add(
+        D, H, W, K, *box, float(sigma_scale), _ptr(p), _ptr(acc), _ptr(wsum), _stream(stream)))
+
+
+def pyramid_stitch_finish(acc, wsum, out, stream=None):
+    D, H, W, K = acc.shape
+    _check("pyramid_stitch_finish", load().pyramid_stitch_finish(
+        D, H, W, K, _ptr(acc), _ptr(wsum), _ptr(out), _stream(stream)))
 
 
 def pyramid_lstm_timing_enable(on: bool) -> None:

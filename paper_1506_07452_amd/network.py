@@ -227,3 +227,42 @@ def network_gradients(g):
         out += list(t)
     return out + [g["head"][0], g["head"][1]]
 
+
+def _tile_starts(extent, size, stride):
+    size = min(size, extent)
+    starts = list(range(0, extent - size + 1, stride))
+    if starts[-1] + size < extent:
+        starts.append(extent - size)
+    return starts, size
+
+
+def network_infer_volume(x, layers, fcs, head, tile, stride, sigma_scale=0.25, ws=None,
+                         stream=None):
+    """Class probabilities [N][D][H][W][K] of a volume processed as sub-volumes
+    (Section 3, "Sub-volumes and Augmentation"): tiles of size `tile` (d, h, w)
+    at multiples of `stride` along each axis (plus one flush with the far end
+    where the grid falls short), each run through the network on its own, and
+    stitched with Gaussian weights (sigma = sigma_scale x tile extent)."""
+    from . import pyramid_crop, pyramid_stitch_add, pyramid_stitch_clear, pyramid_stitch_finish
+    N, D, H, W, C = x.shape
+    K = head[0].shape[0]
+    zs, td = _tile_starts(D, tile[0], stride[0])
+    ys, th = _tile_starts(H, tile[1], stride[1])
+    xs, tw = _tile_starts(W, tile[2], stride[2])
+    out = torch.empty((N, D, H, W, K), dtype=torch.float32, device=x.device)
+    acc = torch.empty((D, H, W, K), dtype=torch.float32, device=x.device)
+    wsum = torch.empty((D, H, W), dtype=torch.float32, device=x.device)
+    sub = torch.empty((1, td, th, tw, C), dtype=x.dtype, device=x.device)
+    for n in range(N):
+        pyramid_stitch_clear(acc, wsum, stream)
+        for z0 in zs:
+            for y0 in ys:
+                for x0 in xs:
+                    box = (z0, y0, x0, td, th, tw)
+                    pyramid_crop(x, n, box, sub, stream)
+                    p = network_forward(sub, layers, fcs, head, ws=ws, stream=stream)["p"]
+                    pyramid_stitch_add(p.view(td, th, tw, K), box, acc, wsum, sigma_scale,
+                                       stream)
+        pyramid_stitch_finish(acc, wsum, out[n], stream)
+    return out
+

@@ -213,3 +213,19 @@ def test_learning_rate_schedule_matches_oracle():
         assert P.pyramid_rmsprop_learning_rate(e) == pytest.approx(optim.learning_rate(e),
                                                                    rel=1e-14)
 
+
+def test_stitch_and_crop_validation(lib):
+    """Boxes outside the volume, null pointers and a non-positive Gaussian
+    width are refused before any launch."""
+    assert lib.pyramid_crop(1, 4, 5, 6, 2, 0, 0, 0, 0, 0, 5, 5, 6, FAKE, FAKE, None) == -1
+    assert lib.pyramid_crop(1, 4, 5, 6, 2, 0, 1, 0, 0, 0, 4, 5, 6, FAKE, FAKE, None) == -1
+    assert lib.pyramid_crop(1, 4, 5, 6, 2, 0, 0, 0, 0, -1, 2, 2, 2, FAKE, FAKE, None) == -1
+    assert lib.pyramid_crop(1, 4, 5, 6, 2, 0, 0, 0, 0, 0, 2, 2, 2, None, FAKE, None) == -1
+    assert lib.pyramid_crop(1, 4, 5, 6, 2, 7, 0, 0, 0, 0, 2, 2, 2, FAKE, FAKE, None) == -1
+    add = lib.pyramid_stitch_add
+    assert add(4, 5, 6, 3, 0, 0, 4, 2, 2, 3, 0.25, FAKE, FAKE, FAKE, None) == -1
+    assert add(4, 5, 6, 3, 0, 0, 0, 2, 2, 3, 0.0, FAKE, FAKE, FAKE, None) == -1
+    assert add(4, 5, 6, 3, 0, 0, 0, 2, 2, 3, 0.25, None, FAKE, FAKE, None) == -1
+    assert lib.pyramid_stitch_clear(0, 5, 6, 3, FAKE, FAKE, None) == -1
+    assert lib.pyramid_stitch_finish(4, 5, 6, 3, FAKE, None, FAKE, None) == -1
+

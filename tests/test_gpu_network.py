@@ -150,6 +150,55 @@ def test_paper_network_training_step_squared_loss():
         assert normwise(host(got), want) <= TOL["f32"]
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_crop_is_the_subvolume(dtype):
+    import paper_1506_07452_amd as P
+    rng = np.random.default_rng(101)
+    xa = rng.standard_normal((2, 5, 9, 7, 3))
+    x = dev(xa, dtype)
+    box = (1, 2, 3, 3, 6, 4)
+    say("crop", dtype)
+    tile = torch.empty((1, 3, 6, 4, 3), dtype=x.dtype, device=DEV)
+    P.pyramid_crop(x, 1, box, tile)
+    torch.cuda.synchronize()
+    want = host(x)[1, 1:4, 2:8, 3:7]
+    assert np.array_equal(host(tile)[0], want)
+
+
+def test_stitched_inference_matches_oracle():
+    """A volume run as overlapping sub-volumes and stitched with Gaussian
+    weights (Section 3) against the oracle doing the same with its own
+    network."""
+    import oracle.stitch as ostitch
+    from paper_1506_07452_amd.network import network_infer_volume
+    inst = small(dict(N=1, D=6, H=20, W=18, C=3, hidden=[16, 32], fc=True, classes=4), 102)
+    tile, stride = (4, 12, 10), (2, 8, 8)
+    lw, fw, hw = oracle_args(inst)
+
+    def tile_fn(z0, y0, x0, d, h, w):
+        xs = inst.x[:, z0:z0 + d, y0:y0 + h, x0:x0 + w]
+        return onet.forward(xs, lw, fw, hw)["p"].reshape(d, h, w, -1)
+
+    ref = ostitch.stitch((6, 20, 18), tile, stride, tile_fn, 4)
+    say("stitched inference")
+    x, layers, fcs, head, _ = to_device(inst, "f32")
+    p = network_infer_volume(x, layers, fcs, head, tile, stride)
+    torch.cuda.synchronize()
+    assert normwise(host(p)[0], ref) <= TOL["f32"]
+    assert np.allclose(host(p).sum(-1), 1.0, atol=1e-5)
+
+
+def test_single_tile_stitch_is_the_network_output():
+    from paper_1506_07452_amd.network import network_infer_volume
+    inst = small(dict(N=2, D=4, H=9, W=8, C=3, hidden=[16], fc=True, classes=3), 103)
+    say("single tile stitch")
+    x, layers, fcs, head, _ = to_device(inst, "f32")
+    p = network_infer_volume(x, layers, fcs, head, (4, 9, 8), (4, 9, 8))
+    q = network_forward(x, layers, fcs, head)["p"].view(p.shape)
+    torch.cuda.synchronize()
+    assert normwise(host(p), host(q)) <= 1e-6
+
+
 def test_rmsprop_matches_oracle():
     """Three RMS-prop updates (Section 3, Eq. (15)-(18)) of four tensors of
     ragged sizes in one launch each, against the fp64 oracle fed the same

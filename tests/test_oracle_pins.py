@@ -670,3 +670,78 @@ def test_stitch_two_tiles_by_hand():
     np.testing.assert_allclose(out[0, 0, [0, 1, 3, 4], 0], [1.0, 1.0, 3.0, 3.0], rtol=1e-15)
     assert out[0, 0, 2, 0] == pytest.approx((g[2] * 1.0 + g[0] * 3.0) / (g[2] + g[0]), rel=1e-15)
 
+
+# ------------------------------------------------- 2D PyraMiD-LSTM (Fig. 1)
+import oracle.layer2d as o2d
+
+
+def _params2d(rng, C, O, K, scale=0.3):
+    wx = rng.uniform(-scale, scale, (4, 4 * O, C, K))
+    wh = rng.uniform(-scale, scale, (4, 4 * O, O, K))
+    b = rng.uniform(-0.2, 0.2, (4, 4 * O))
+    return wx, wh, b
+
+
+@pytest.mark.parametrize("shape", [(1, 5, 6, 2, 3, 3), (2, 4, 7, 1, 2, 5), (1, 3, 3, 2, 2, 1),
+                                   (1, 6, 2, 3, 4, 7)], ids=lambda s: "x".join(map(str, s)))
+def test_2d_line_sweeps_equal_the_embedded_volume(shape):
+    """The numpy line-sweep definition and the volume oracle (C) through the
+    D = 1 embedding agree: two independent codes of the same layer."""
+    N, H, W, C, O, K = shape
+    rng = np.random.default_rng(180 + sum(shape))
+    x = rng.standard_normal((N, H, W, C))
+    wx, wh, b = _params2d(rng, C, O, K)
+    np.testing.assert_allclose(o2d.forward2d(x, wx, wh, b), o2d.forward2d_via_volume(x, wx, wh, b),
+                               rtol=1e-12, atol=1e-13)
+
+
+def test_2d_filter_of_one_is_four_1d_lstms():
+    """K = 1: each direction is a textbook LSTM (Eq. (1)-(6)) along every
+    row or column; torch.nn.LSTM in fp64 gives the same sum."""
+    rng = np.random.default_rng(181)
+    N, H, W, C, O = 1, 4, 5, 2, 3
+    x = rng.standard_normal((N, H, W, C))
+    wx, wh, b = _params2d(rng, C, O, 1)
+    want = np.zeros((N, H, W, O))
+    for d in range(4):
+        lstm = torch.nn.LSTM(C, O, batch_first=True).double()
+        with torch.no_grad():
+            lstm.weight_ih_l0.copy_(torch.tensor(wx[d, :, :, 0]))
+            lstm.weight_hh_l0.copy_(torch.tensor(wh[d, :, :, 0]))
+            lstm.bias_ih_l0.copy_(torch.tensor(b[d]))
+            lstm.bias_hh_l0.zero_()
+        seq = x[0] if d >= 2 else x[0].transpose(1, 0, 2)     # lines along the scan axis
+        if d % 2 == 1:
+            seq = seq[:, ::-1]
+        out, _ = lstm(torch.tensor(np.ascontiguousarray(seq)))
+        out = out.detach().numpy()
+        if d % 2 == 1:
+            out = out[:, ::-1]
+        want[0] += out if d >= 2 else out.transpose(1, 0, 2)
+    np.testing.assert_allclose(o2d.forward2d(x, wx, wh, b), want, rtol=1e-12, atol=1e-13)
+
+
+def test_2d_backward_finite_differences():
+    rng = np.random.default_rng(182)
+    N, H, W, C, O, K = 1, 3, 4, 2, 2, 3
+    x = rng.standard_normal((N, H, W, C))
+    wx, wh, b = _params2d(rng, C, O, K, 0.5)
+    dh = rng.standard_normal((N, H, W, O))
+    g = o2d.backward2d(x, wx, wh, b, dh)
+    eps = 1e-6
+
+    def L():
+        return float((o2d.forward2d(x, wx, wh, b) * dh).sum())
+
+    for arr, grad in ((x, g["dx"]), (wx, g["dwx"]), (wh, g["dwh"]), (b, g["db"])):
+        flat = arr.reshape(-1)
+        for k in rng.choice(flat.size, size=min(flat.size, 8), replace=False):
+            s0 = flat[k]
+            flat[k] = s0 + eps
+            lp = L()
+            flat[k] = s0 - eps
+            lm = L()
+            flat[k] = s0
+            fd = (lp - lm) / (2 * eps)
+            assert abs(fd - grad.reshape(-1)[k]) <= 1e-8 + 1e-6 * abs(fd)
+

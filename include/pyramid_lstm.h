@@ -71,6 +71,15 @@ typedef struct plstm_shape {
     int32_t K;            /* filter size (odd, 1..7) of wx and wh; 0 means 3 */
 } plstm_shape;
 
+/* Shape of a 2D PyraMiD-LSTM layer over images (see pyramid_lstm2d_forward). */
+typedef struct plstm2d_shape {
+    int32_t N, H, W;      /* batch and image extents */
+    int32_t C;            /* input channels */
+    int32_t O;            /* hidden units per direction */
+    int32_t dtype;        /* enum plstm_dtype */
+    int32_t K;            /* filter length (odd, 1..7) along the line; 0 means 3 */
+} plstm2d_shape;
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *pyramid_lstm_status_string(int status);
 
@@ -195,6 +204,32 @@ int pyramid_lstm_timing_enable(int on);
 int pyramid_lstm_timing_read(int max_phases, char *names, double *ms, int *launches,
                              int *count);
 
+
+/* ---- 2D PyraMiD-LSTM (Section 2.1-2.2, Fig. 1) -------------------------- */
+
+/* The layer over images: 2 x 2 = 4 directions instead of 6.  Direction
+ * 0 = y+ sweeps the rows top to bottom (each step a row of W pixels),
+ * 1 = y- bottom to top, 2 = x+ sweeps the columns left to right (each step a
+ * column of H pixels), 3 = x- right to left.  At each step a pixel's gates
+ * take a 1D convolution of length K along the line of the input line and of
+ * the previous line's h (the rotated connections of Fig. 1 (b)-(c)), then the
+ * cell update of Eq. (10)-(12); h = sum of the four directions.
+ *   x   [N][H][W][C]     h [N][H][W][O]
+ *   wx  [4][4*O][C][K]   wh [4][4*O][O][K]   b [4][4*O]
+ *   A[q][g*O+o] += in[q+k-r][c] * w[g*O+o][c][k], r = (K-1)/2, q along the
+ *   line, zero padding.
+ * Entry points mirror the 3D ones (same conventions, workspace and saved
+ * buffers sized by the 2D functions; the saved layout has 4 directions).
+ * Supported: as the 3D layer with D = 1. */
+size_t pyramid_lstm2d_workspace_size(const plstm2d_shape *s, int training);
+size_t pyramid_lstm2d_saved_size(const plstm2d_shape *s);
+int pyramid_lstm2d_forward(const plstm2d_shape *s, const void *x, const void *wx,
+                           const void *wh, const void *b, void *h, void *saved, void *ws,
+                           size_t ws_bytes, void *stream);
+int pyramid_lstm2d_backward(const plstm2d_shape *s, const void *x, const void *wx,
+                            const void *wh, const void *b, const void *saved, const void *dh,
+                            void *dx, void *dwx, void *dwh, void *db, void *ws,
+                            size_t ws_bytes, void *stream);
 
 /* ---- training update (Section 3, "Training") ---------------------------- */
 

@@ -24,7 +24,8 @@ __all__ = [
     "pyramid_crop", "pyramid_stitch_clear", "pyramid_stitch_add", "pyramid_stitch_finish",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
     "pyramid_lstm_set_backward_path", "pyramid_lstm_set_step_split", "pyramid_lstm_set_bf16_mfma",
-    "library_path", "load",
+    "library_path", "load", "plstm2d_shape", "shape2d_for", "pyramid_lstm2d_workspace_size",
+    "pyramid_lstm2d_saved_size", "pyramid_lstm2d_forward", "pyramid_lstm2d_backward",
 ]
 
 PLSTM_F32 = 0
@@ -45,6 +46,12 @@ class plstm_shape(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int32), ("D", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("W", ctypes.c_int32), ("C", ctypes.c_int32), ("O", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("K", ctypes.c_int32)]
+
+
+class plstm2d_shape(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32),
+                ("C", ctypes.c_int32), ("O", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("K", ctypes.c_int32)]
 
 
 class plstm_param_segment(ctypes.Structure):
@@ -77,6 +84,15 @@ def load():
     lib.pyramid_lstm_forward.restype = ctypes.c_int
     lib.pyramid_lstm_backward.argtypes = [sp] + [vp] * 11 + [sz, vp]
     lib.pyramid_lstm_backward.restype = ctypes.c_int
+    sp2 = ctypes.POINTER(plstm2d_shape)
+    lib.pyramid_lstm2d_workspace_size.argtypes = [sp2, ctypes.c_int]
+    lib.pyramid_lstm2d_workspace_size.restype = sz
+    lib.pyramid_lstm2d_saved_size.argtypes = [sp2]
+    lib.pyramid_lstm2d_saved_size.restype = sz
+    lib.pyramid_lstm2d_forward.argtypes = [sp2] + [vp] * 7 + [sz, vp]
+    lib.pyramid_lstm2d_forward.restype = ctypes.c_int
+    lib.pyramid_lstm2d_backward.argtypes = [sp2] + [vp] * 11 + [sz, vp]
+    lib.pyramid_lstm2d_backward.restype = ctypes.c_int
     lib.pyramid_fc_tanh_forward.argtypes = [i64, i32, i32, i32] + [vp] * 4 + [vp]
     lib.pyramid_fc_tanh_forward.restype = ctypes.c_int
     lib.pyramid_fc_workspace_size.argtypes = [i64, i32, i32]
@@ -161,6 +177,16 @@ def shape_for(x: torch.Tensor, O: int, K: int = 3) -> plstm_shape:
     return plstm_shape(N, D, H, W, C, O, _DT[x.dtype], K)
 
 
+def shape2d_for(x: torch.Tensor, O: int, K: int = 3) -> plstm2d_shape:
+    """plstm2d_shape of a [N][H][W][C] image batch, hidden size O, filters of K taps."""
+    if x.dim() != 4:
+        raise ValueError("x must be [N][H][W][C]")
+    if x.dtype not in _DT:
+        raise ValueError("x must be float32 or bfloat16")
+    N, H, W, C = x.shape
+    return plstm2d_shape(N, H, W, C, O, _DT[x.dtype], K)
+
+
 def _workspace(nbytes, device):
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
@@ -194,6 +220,35 @@ def pyramid_lstm_backward(shape, x, wx, wh, b, saved, dh, dx, dwx, dwh, db, ws=N
     if ws is None:
         ws = _workspace(pyramid_lstm_workspace_size(shape, 1), x.device)
     _check("pyramid_lstm_backward", lib.pyramid_lstm_backward(
+        ctypes.byref(shape), _ptr(x), _ptr(wx), _ptr(wh), _ptr(b), _ptr(saved), _ptr(dh),
+        _ptr(dx), _ptr(dwx), _ptr(dwh), _ptr(db), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def pyramid_lstm2d_workspace_size(shape: plstm2d_shape, training: int) -> int:
+    return int(load().pyramid_lstm2d_workspace_size(ctypes.byref(shape), int(training)))
+
+
+def pyramid_lstm2d_saved_size(shape: plstm2d_shape) -> int:
+    return int(load().pyramid_lstm2d_saved_size(ctypes.byref(shape)))
+
+
+def pyramid_lstm2d_forward(shape, x, wx, wh, b, h, saved=None, ws=None, stream=None):
+    """2D layer forward over x [N][H][W][C].  ws=None allocates the workspace with torch."""
+    lib = load()
+    if ws is None:
+        ws = _workspace(pyramid_lstm2d_workspace_size(shape, saved is not None), x.device)
+    _check("pyramid_lstm2d_forward", lib.pyramid_lstm2d_forward(
+        ctypes.byref(shape), _ptr(x), _ptr(wx), _ptr(wh), _ptr(b), _ptr(h), _ptr(saved),
+        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_lstm2d_backward(shape, x, wx, wh, b, saved, dh, dx, dwx, dwh, db, ws=None,
+                            stream=None):
+    lib = load()
+    if ws is None:
+        ws = _workspace(pyramid_lstm2d_workspace_size(shape, 1), x.device)
+    _check("pyramid_lstm2d_backward", lib.pyramid_lstm2d_backward(
         ctypes.byref(shape), _ptr(x), _ptr(wx), _ptr(wh), _ptr(b), _ptr(saved), _ptr(dh),
         _ptr(dx), _ptr(dwx), _ptr(dwh), _ptr(db), _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))

@@ -31,6 +31,57 @@ int check_shape(const plstm_shape *s)
     return PLSTM_OK;
 }
 
+// A 2D layer is validated as the volume of one slice it is computed as.
+int check_shape2d(const plstm2d_shape *s)
+{
+    if (!s) return PLSTM_EINVAL;
+    const plstm_shape t{s->N, 1, s->H, s->W, s->C, s->O, s->dtype, s->K};
+    return check_shape(&t);
+}
+
+size_t layer_ws(const Geom &g, int dtype, int training)
+{
+    size_t need = forward_ws(g, dtype, training != 0);
+    if (training) {
+        const size_t b = backward_ws(g);
+        if (b > need) need = b;
+    }
+    return need < 256 ? 256 : need;
+}
+
+int layer_forward(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
+                  const void *b, void *h, void *saved, void *ws, size_t ws_bytes, void *stream)
+{
+    if (!x || !wx || !wh || !b || !h || !ws) return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(wx) || !aligned(wh) || !aligned(b) || !aligned(h) ||
+        !aligned(ws) || (saved && !aligned(saved)))
+        return PLSTM_EINVAL;
+    if (saved && dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
+    if (ws_bytes < layer_ws(g, dtype, saved != nullptr)) return PLSTM_EWORKSPACE;
+    Saved sv{};
+    if (saved) sv = carve_saved(saved, g);
+    return forward_dispatch(g, dtype, x, wx, wh, b, h, saved ? &sv : nullptr, ws,
+                            (hipStream_t)stream);
+}
+
+int layer_backward(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
+                   const void *b, const void *saved, const void *dh, void *dx, void *dwx,
+                   void *dwh, void *db, void *ws, size_t ws_bytes, void *stream)
+{
+    if (!x || !wx || !wh || !b || !saved || !dh || !dwx || !dwh || !db || !ws)
+        return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(wx) || !aligned(wh) || !aligned(b) || !aligned(saved) ||
+        !aligned(dh) || (dx && !aligned(dx)) || !aligned(dwx) || !aligned(dwh) ||
+        !aligned(db) || !aligned(ws))
+        return PLSTM_EINVAL;
+    if (dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
+    if (ws_bytes < layer_ws(g, dtype, 1)) return PLSTM_EWORKSPACE;
+    const Saved sv = carve_saved(const_cast<void *>(saved), g);
+    return backward_dispatch(g, (const float *)x, (const float *)wx, (const float *)wh, sv,
+                             (const float *)dh, (float *)dx, (float *)dwx, (float *)dwh,
+                             (float *)db, ws, (hipStream_t)stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -57,53 +108,59 @@ size_t pyramid_lstm_saved_size(const plstm_shape *s)
 size_t pyramid_lstm_workspace_size(const plstm_shape *s, int training)
 {
     if (check_shape(s) != PLSTM_OK) return 0;
-    const Geom g = make_geom(*s);
-    size_t need = forward_ws(g, s->dtype, training != 0);
-    if (training) {
-        const size_t b = backward_ws(g);
-        if (b > need) need = b;
-    }
-    return need < 256 ? 256 : need;
+    return layer_ws(make_geom(*s), s->dtype, training);
 }
 
 int pyramid_lstm_forward(const plstm_shape *s, const void *x, const void *wx, const void *wh,
                          const void *b, void *h, void *saved, void *ws, size_t ws_bytes,
                          void *stream)
 {
-    int rc = check_shape(s);
+    const int rc = check_shape(s);
     if (rc != PLSTM_OK) return rc;
-    if (!x || !wx || !wh || !b || !h || !ws) return PLSTM_EINVAL;
-    if (!aligned(x) || !aligned(wx) || !aligned(wh) || !aligned(b) || !aligned(h) ||
-        !aligned(ws) || (saved && !aligned(saved)))
-        return PLSTM_EINVAL;
-    if (saved && s->dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
-    if (ws_bytes < pyramid_lstm_workspace_size(s, saved != nullptr)) return PLSTM_EWORKSPACE;
-    const Geom g = make_geom(*s);
-    Saved sv{};
-    if (saved) sv = carve_saved(saved, g);
-    return forward_dispatch(g, s->dtype, x, wx, wh, b, h, saved ? &sv : nullptr, ws,
-                            (hipStream_t)stream);
+    return layer_forward(make_geom(*s), s->dtype, x, wx, wh, b, h, saved, ws, ws_bytes, stream);
 }
 
 int pyramid_lstm_backward(const plstm_shape *s, const void *x, const void *wx, const void *wh,
                           const void *b, const void *saved, const void *dh, void *dx, void *dwx,
                           void *dwh, void *db, void *ws, size_t ws_bytes, void *stream)
 {
-    int rc = check_shape(s);
+    const int rc = check_shape(s);
     if (rc != PLSTM_OK) return rc;
-    if (!x || !wx || !wh || !b || !saved || !dh || !dwx || !dwh || !db || !ws)
-        return PLSTM_EINVAL;
-    if (!aligned(x) || !aligned(wx) || !aligned(wh) || !aligned(b) || !aligned(saved) ||
-        !aligned(dh) || (dx && !aligned(dx)) || !aligned(dwx) || !aligned(dwh) ||
-        !aligned(db) || !aligned(ws))
-        return PLSTM_EINVAL;
-    if (s->dtype != PLSTM_F32) return PLSTM_EUNSUPPORTED;
-    if (ws_bytes < pyramid_lstm_workspace_size(s, 1)) return PLSTM_EWORKSPACE;
-    const Geom g = make_geom(*s);
-    const Saved sv = carve_saved(const_cast<void *>(saved), g);
-    return backward_dispatch(g, (const float *)x, (const float *)wx, (const float *)wh, sv,
-                             (const float *)dh, (float *)dx, (float *)dwx, (float *)dwh,
-                             (float *)db, ws, (hipStream_t)stream);
+    return layer_backward(make_geom(*s), s->dtype, x, wx, wh, b, saved, dh, dx, dwx, dwh, db, ws,
+                          ws_bytes, stream);
+}
+
+size_t pyramid_lstm2d_saved_size(const plstm2d_shape *s)
+{
+    if (check_shape2d(s) != PLSTM_OK) return 0;
+    return saved_bytes(make_geom2d(*s));
+}
+
+size_t pyramid_lstm2d_workspace_size(const plstm2d_shape *s, int training)
+{
+    if (check_shape2d(s) != PLSTM_OK) return 0;
+    return layer_ws(make_geom2d(*s), s->dtype, training);
+}
+
+int pyramid_lstm2d_forward(const plstm2d_shape *s, const void *x, const void *wx, const void *wh,
+                           const void *b, void *h, void *saved, void *ws, size_t ws_bytes,
+                           void *stream)
+{
+    const int rc = check_shape2d(s);
+    if (rc != PLSTM_OK) return rc;
+    return layer_forward(make_geom2d(*s), s->dtype, x, wx, wh, b, h, saved, ws, ws_bytes,
+                         stream);
+}
+
+int pyramid_lstm2d_backward(const plstm2d_shape *s, const void *x, const void *wx,
+                            const void *wh, const void *b, const void *saved, const void *dh,
+                            void *dx, void *dwx, void *dwh, void *db, void *ws, size_t ws_bytes,
+                            void *stream)
+{
+    const int rc = check_shape2d(s);
+    if (rc != PLSTM_OK) return rc;
+    return layer_backward(make_geom2d(*s), s->dtype, x, wx, wh, b, saved, dh, dx, dwx, dwh, db,
+                          ws, ws_bytes, stream);
 }
 
 size_t pyramid_fc_workspace_size(int64_t M, int32_t Cin, int32_t Cout)

@@ -20,27 +20,61 @@ struct DirGeom {
     long long ss, sp, sq; // voxel strides of s, p, q
 };
 
+// A layer's geometry.  Directions d < nd are active: the six sweeps of a
+// volume (nd = 6, axis[d] = d / 2: z, y, x) or the four line sweeps of an
+// image (nd = 4: y+, y-, x+, x-, the image being a volume with D = 1).  The
+// filters have KP x KQ taps over the plane's (first, second) axis: K x K for
+// a volume, 1 x K along the line for an image.  Per-direction arrays
+// (weights, saved states, gradients) hold nd directions.
 struct Geom {
     int N, D, H, W, C, O;
-    int K;                // filter size (odd); taps K * K, radius (K - 1) / 2
+    int K;                // filter size (odd)
+    int KP, KQ;           // taps along the plane's first and second axis
+    int nd;               // active directions
+    int axis[kDirs];      // sweep axis of direction d: 0 z, 1 y, 2 x
     long long V;          // D * H * W
     DirGeom dir[kDirs];
 };
+
+inline void set_dir(Geom &g, int d, int axis, int sign)
+{
+    const long long HW = (long long)g.H * g.W;
+    DirGeom &r = g.dir[d];
+    r.sign = sign;
+    g.axis[d] = axis;
+    switch (axis) {
+    case 0: r.T = g.D; r.P = g.H; r.Q = g.W; r.ss = HW; r.sp = g.W; r.sq = 1; break;
+    case 1: r.T = g.H; r.P = g.D; r.Q = g.W; r.ss = g.W; r.sp = HW; r.sq = 1; break;
+    default: r.T = g.W; r.P = g.D; r.Q = g.H; r.ss = 1; r.sp = HW; r.sq = g.W; break;
+    }
+}
 
 inline Geom make_geom(const plstm_shape &s) {
     Geom g;
     g.N = s.N; g.D = s.D; g.H = s.H; g.W = s.W; g.C = s.C; g.O = s.O;
     g.K = s.K == 0 ? 3 : s.K;
-    const long long HW = (long long)s.H * s.W;
-    g.V = (long long)s.D * HW;
-    for (int d = 0; d < kDirs; ++d) {
-        DirGeom &r = g.dir[d];
-        r.sign = (d % 2 == 0) ? 1 : -1;
-        switch (d / 2) {
-        case 0: r.T = s.D; r.P = s.H; r.Q = s.W; r.ss = HW; r.sp = s.W; r.sq = 1; break;
-        case 1: r.T = s.H; r.P = s.D; r.Q = s.W; r.ss = s.W; r.sp = HW; r.sq = 1; break;
-        default: r.T = s.W; r.P = s.D; r.Q = s.H; r.ss = 1; r.sp = HW; r.sq = s.W; break;
-        }
+    g.KP = g.KQ = g.K;
+    g.nd = kDirs;
+    g.V = (long long)s.D * s.H * s.W;
+    for (int d = 0; d < kDirs; ++d) set_dir(g, d, d / 2, (d % 2 == 0) ? 1 : -1);
+    return g;
+}
+
+// An image [N][H][W][C] as a volume with D = 1: directions y+, y- (rows top to
+// bottom and back, each step a row of W pixels) and x+, x- (columns), 1 x K
+// filters along the line.  Unused direction slots have no planes.
+inline Geom make_geom2d(const plstm2d_shape &s) {
+    Geom g;
+    g.N = s.N; g.D = 1; g.H = s.H; g.W = s.W; g.C = s.C; g.O = s.O;
+    g.K = s.K == 0 ? 3 : s.K;
+    g.KP = 1;
+    g.KQ = g.K;
+    g.nd = 4;
+    g.V = (long long)s.H * s.W;
+    for (int d = 0; d < 4; ++d) set_dir(g, d, 1 + d / 2, (d % 2 == 0) ? 1 : -1);
+    for (int d = 4; d < kDirs; ++d) {
+        set_dir(g, d, 0, 1);
+        g.dir[d].T = 0;
     }
     return g;
 }
@@ -92,15 +126,15 @@ struct Carve {
     } while (0)
 
 // Saved-activation layout shared by every forward/backward pair (fp32,
-// per-direction volumes in [N][D][H][W] voxel order):
-//   gates [6][N][V][4O]  i, f, g, o after the nonlinearity
-//   cell  [6][N][V][O]   c^d
-//   hd    [6][N][V][O]   h^d
+// per-direction volumes in [N][D][H][W] voxel order, nd directions):
+//   gates [nd][N][V][4O]  i, f, g, o after the nonlinearity
+//   cell  [nd][N][V][O]   c^d
+//   hd    [nd][N][V][O]   h^d
 struct Saved {
     float *gates, *cell, *hd;
 };
-inline size_t saved_gates_count(const Geom &g) { return (size_t)kDirs * g.N * g.V * 4 * g.O; }
-inline size_t saved_state_count(const Geom &g) { return (size_t)kDirs * g.N * g.V * g.O; }
+inline size_t saved_gates_count(const Geom &g) { return (size_t)g.nd * g.N * g.V * 4 * g.O; }
+inline size_t saved_state_count(const Geom &g) { return (size_t)g.nd * g.N * g.V * g.O; }
 inline Saved carve_saved(void *p, const Geom &g) {
     Carve cv(p);
     Saved s;

@@ -1,19 +1,20 @@
-// Generic PyraMiD-LSTM path: any supported shape and filter size K, one launch
-// per plane step.
+// Generic PyraMiD-LSTM path: any supported shape, any KP x KQ filter (K x K
+// over a volume's planes, 1 x K along an image's lines), one launch per plane
+// step.
 //
 // Forward (Section 2.3, Eq. (7)-(13)): for step t, every direction d with
 // t < T_d updates all pixels of its plane t at once.  One thread owns one
 // (direction, batch element, pixel, hidden unit) and produces the four gate
-// pre-activations of that unit by direct K x K loops over the input plane and
+// pre-activations of that unit by direct KP x KQ loops over the input plane and
 // the previous plane's h^d; the cell state lives in a per-direction volume.
 // The six per-direction outputs are summed in the fixed order d = 0..5.
 //
 // Backward (the chain rule through Eq. (7)-(13), reverse plane order): for
 // step t every thread owns one (d, n, pixel, unit j): it collects dL/dh^d from
 // the upstream gradient and from the next plane's gate gradients (a transposed
-// K x K convolution with wh), forms dL/dc and the four gate gradients of unit j.
+// KP x KQ convolution with wh), forms dL/dc and the four gate gradients of unit j.
 // Parameter gradients are then block-tiled reductions over all voxels
-// (deterministic two-stage sums), and dL/dx a transposed K x K convolution with
+// (deterministic two-stage sums), and dL/dx a transposed KP x KQ convolution with
 // wx summed over the six directions.
 #include "common.h"
 #include "sweep.h"
@@ -38,7 +39,8 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
     const int p = px / dg.Q, q = px % dg.Q;
     const int s = dg.sign > 0 ? t : dg.T - 1 - t;
     const int sprev = s - dg.sign;
-    const int C = g.C, O = g.O, G = 4 * O, K = g.K, KK = K * K, rad = K / 2;
+    const int C = g.C, O = g.O, G = 4 * O, KP = g.KP, KQ = g.KQ, KK = KP * KQ;
+    const int radp = KP / 2, radq = KQ / 2;
     const long long nbase = (long long)n * g.V;
     const long long dbase = (long long)d * g.N * g.V;
 
@@ -46,11 +48,11 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
 #pragma unroll
     for (int k = 0; k < 4; ++k) acc[k] = Store<TS>::load(b, (long long)d * G + k * O + o);
 
-    for (int ka = 0; ka < K; ++ka) {
-        const int pp = p + ka - rad;
+    for (int ka = 0; ka < KP; ++ka) {
+        const int pp = p + ka - radp;
         if (pp < 0 || pp >= dg.P) continue;
-        for (int kb = 0; kb < K; ++kb) {
-            const int qq = q + kb - rad;
+        for (int kb = 0; kb < KQ; ++kb) {
+            const int qq = q + kb - radq;
             if (qq < 0 || qq >= dg.Q) continue;
             const long long vin = nbase + s * dg.ss + pp * dg.sp + qq * dg.sq;
             for (int c = 0; c < C; ++c) {
@@ -58,7 +60,7 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
                     acc[k] += xv * Store<TS>::load(
-                        wx, (((long long)d * G + k * O + o) * C + c) * KK + ka * K + kb);
+                        wx, (((long long)d * G + k * O + o) * C + c) * KK + ka * KQ + kb);
             }
             if (t > 0) {
                 const long long vh = dbase + nbase + sprev * dg.ss + pp * dg.sp + qq * dg.sq;
@@ -67,7 +69,7 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
 #pragma unroll
                     for (int k = 0; k < 4; ++k)
                         acc[k] += hv * Store<TS>::load(
-                            wh, (((long long)d * G + k * O + o) * O + j) * KK + ka * K + kb);
+                            wh, (((long long)d * G + k * O + o) * O + j) * KK + ka * KQ + kb);
                 }
             }
         }
@@ -92,13 +94,12 @@ k_fwd_step(Geom g, int t, const TS *__restrict__ x, const TS *__restrict__ wx,
 // h = sum_d h^d in the fixed order d = 0..5 (Eq. (13)).
 template <typename TS>
 __global__ void __launch_bounds__(kThreads)
-k_sum_dirs(long long count, const float *__restrict__ hd, TS *__restrict__ h)
+k_sum_dirs(long long count, int nd, const float *__restrict__ hd, TS *__restrict__ h)
 {
     const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
     if (i >= count) return;
     float acc = hd[i];
-#pragma unroll
-    for (int d = 1; d < kDirs; ++d) acc += hd[(long long)d * count + i];
+    for (int d = 1; d < nd; ++d) acc += hd[(long long)d * count + i];
     Store<TS>::store(h, i, acc);
 }
 
@@ -115,7 +116,8 @@ k_bwd_step(Geom g, int t, const float *__restrict__ wh, const float *__restrict_
     const int p = px / dg.Q, q = px % dg.Q;
     const int s = dg.sign > 0 ? t : dg.T - 1 - t;
     const int snext = s + dg.sign, sprev = s - dg.sign;
-    const int O = g.O, G = 4 * O, K = g.K, KK = K * K, rad = K / 2;
+    const int O = g.O, G = 4 * O, KP = g.KP, KQ = g.KQ, KK = KP * KQ;
+    const int radp = KP / 2, radq = KQ / 2;
     const long long nbase = (long long)n * g.V;
     const long long dbase = (long long)d * g.N * g.V;
     const long long vloc = nbase + s * dg.ss + p * dg.sp + q * dg.sq;
@@ -125,16 +127,16 @@ k_bwd_step(Geom g, int t, const float *__restrict__ wh, const float *__restrict_
     float gh = dh[vloc * O + j];
     if (has_next) {
         // h_t[p][q][j] entered A_{t+1}[p - (ka-r)][q - (kb-r)] through tap (ka, kb).
-        for (int ka = 0; ka < K; ++ka) {
-            const int pp = p - (ka - rad);
+        for (int ka = 0; ka < KP; ++ka) {
+            const int pp = p - (ka - radp);
             if (pp < 0 || pp >= dg.P) continue;
-            for (int kb = 0; kb < K; ++kb) {
-                const int qq = q - (kb - rad);
+            for (int kb = 0; kb < KQ; ++kb) {
+                const int qq = q - (kb - radq);
                 if (qq < 0 || qq >= dg.Q) continue;
                 const long long vn = dbase + nbase + snext * dg.ss + pp * dg.sp + qq * dg.sq;
                 for (int gn = 0; gn < G; ++gn)
                     gh += dA[vn * G + gn] *
-                          wh[(((long long)d * G + gn) * O + j) * KK + ka * K + kb];
+                          wh[(((long long)d * G + gn) * O + j) * KK + ka * KQ + kb];
             }
         }
     }
@@ -159,9 +161,9 @@ k_bwd_step(Geom g, int t, const float *__restrict__ wh, const float *__restrict_
 }
 
 // Parameter-gradient partial sums.  For direction d the reduction runs over
-// every voxel (n, t, p, q); with KK = K * K taps, column k of the "im2col"
+// every voxel (n, t, p, q); with KK = KP * KQ taps, column k of the "im2col"
 // row is
-//   k < KK C          : x at tap (ka, kb) = divmod(k / C, K), channel k % C
+//   k < KK C          : x at tap (ka, kb) = divmod(k / C, KQ), channel k % C
 //   KK C <= k < KK(C+O): h^d_{t-1} at tap, unit, recomputed as o * tanh(c) of
 //                       the previous plane (0 for t = 0 or outside the plane)
 //   k = KK (C+O)      : 1 (bias)
@@ -175,7 +177,8 @@ k_wgrad_partial(Geom g, long long chunk_len, int nchunk, const float *__restrict
                 const float *__restrict__ gates, const float *__restrict__ cell,
                 const float *__restrict__ dA, float *__restrict__ partial)
 {
-    const int C = g.C, O = g.O, G = 4 * O, K = g.K, KK = K * K, rad = K / 2;
+    const int C = g.C, O = g.O, G = 4 * O, KQ = g.KQ, KK = g.KP * KQ;
+    const int radp = g.KP / 2, radq = KQ / 2;
     const int KT = KK * (C + O) + 1;
     const int d = blockIdx.z / nchunk, chunk = blockIdx.z % nchunk;
     const int k0 = blockIdx.x * kTile, g0 = blockIdx.y * kTile;
@@ -208,13 +211,13 @@ k_wgrad_partial(Geom g, long long chunk_len, int nchunk, const float *__restrict
                 const int k = k0 + col;
                 if (k < KK * C) {
                     const int tap = k / C, c = k % C;
-                    const int pp = p + tap / K - rad, qq = q + tap % K - rad;
+                    const int pp = p + tap / KQ - radp, qq = q + tap % KQ - radq;
                     if (pp >= 0 && pp < dg.P && qq >= 0 && qq < dg.Q)
                         in = x[(nbase + s * dg.ss + pp * dg.sp + qq * dg.sq) * C + c];
                 } else if (k < KK * (C + O)) {
                     const int kk = k - KK * C;
                     const int tap = kk / O, j = kk % O;
-                    const int pp = p + tap / K - rad, qq = q + tap % K - rad;
+                    const int pp = p + tap / KQ - radp, qq = q + tap % KQ - radq;
                     if (t > 0 && pp >= 0 && pp < dg.P && qq >= 0 && qq < dg.Q) {
                         const long long vp =
                             dbase + nbase + (s - dg.sign) * dg.ss + pp * dg.sp + qq * dg.sq;
@@ -241,10 +244,10 @@ __global__ void __launch_bounds__(kThreads)
 k_wgrad_reduce(Geom g, int nchunk, const float *__restrict__ partial, float *__restrict__ dwx,
                float *__restrict__ dwh, float *__restrict__ db)
 {
-    const int C = g.C, O = g.O, G = 4 * O, KK = g.K * g.K;
+    const int C = g.C, O = g.O, G = 4 * O, KK = g.KP * g.KQ;
     const int KT = KK * (C + O) + 1;
     const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
-    if (i >= (long long)kDirs * G * KT) return;
+    if (i >= (long long)g.nd * G * KT) return;
     const int k = (int)(i % KT);
     const int gn = (int)((i / KT) % G);
     const int d = (int)(i / ((long long)KT * G));
@@ -268,7 +271,8 @@ __global__ void __launch_bounds__(kThreads)
 k_dx(Geom g, const float *__restrict__ wx, const float *__restrict__ dA, float *__restrict__ dx)
 {
     const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
-    const int C = g.C, O = g.O, G = 4 * O, K = g.K, KK = K * K, rad = K / 2;
+    const int C = g.C, O = g.O, G = 4 * O, KP = g.KP, KQ = g.KQ, KK = KP * KQ;
+    const int radp = KP / 2, radq = KQ / 2;
     if (i >= (long long)g.N * g.V * C) return;
     const int c = (int)(i % C);
     const long long vloc = i / C;
@@ -279,24 +283,24 @@ k_dx(Geom g, const float *__restrict__ wx, const float *__restrict__ dA, float *
     const int xw = (int)(r % g.W);
     const long long nbase = (long long)n * g.V;
     float acc = 0.0f;
-    for (int d = 0; d < kDirs; ++d) {
+    for (int d = 0; d < g.nd; ++d) {
         const DirGeom dg = g.dir[d];
         int s, p, q;
-        switch (d / 2) {
+        switch (g.axis[d]) {
         case 0: s = z; p = y; q = xw; break;
         case 1: s = y; p = z; q = xw; break;
         default: s = xw; p = z; q = y; break;
         }
         const long long dbase = (long long)d * g.N * g.V;
-        for (int ka = 0; ka < K; ++ka) {
-            const int pp = p - (ka - rad);
+        for (int ka = 0; ka < KP; ++ka) {
+            const int pp = p - (ka - radp);
             if (pp < 0 || pp >= dg.P) continue;
-            for (int kb = 0; kb < K; ++kb) {
-                const int qq = q - (kb - rad);
+            for (int kb = 0; kb < KQ; ++kb) {
+                const int qq = q - (kb - radq);
                 if (qq < 0 || qq >= dg.Q) continue;
                 const long long v = dbase + nbase + s * dg.ss + pp * dg.sp + qq * dg.sq;
                 const float *a = dA + v * G;
-                const float *w = wx + ((long long)d * G * C + c) * KK + ka * K + kb;
+                const float *w = wx + ((long long)d * G * C + c) * KK + ka * KQ + kb;
                 for (int gn = 0; gn < G; ++gn) acc += a[gn] * w[(long long)gn * C * KK];
             }
         }
@@ -306,12 +310,12 @@ k_dx(Geom g, const float *__restrict__ wx, const float *__restrict__ dA, float *
 
 inline int max_plane(const Geom &g) {
     int m = 0;
-    for (int d = 0; d < kDirs; ++d) m = g.dir[d].P * g.dir[d].Q > m ? g.dir[d].P * g.dir[d].Q : m;
+    for (int d = 0; d < g.nd; ++d) m = g.dir[d].P * g.dir[d].Q > m ? g.dir[d].P * g.dir[d].Q : m;
     return m;
 }
 inline int max_T(const Geom &g) {
     int m = 0;
-    for (int d = 0; d < kDirs; ++d) m = g.dir[d].T > m ? g.dir[d].T : m;
+    for (int d = 0; d < g.nd; ++d) m = g.dir[d].T > m ? g.dir[d].T : m;
     return m;
 }
 
@@ -347,7 +351,7 @@ int generic_forward(const Geom &g, int dtype, const void *x, const void *wx, con
     float *hd = sv ? sv->hd : cv.take<float>(saved_state_count(g));
     float *cellbuf = sv ? sv->cell : cv.take<float>(saved_state_count(g));
     float *gates = sv ? sv->gates : nullptr;
-    const dim3 grid((max_plane(g) + kThreads - 1) / kThreads, g.O, kDirs * g.N);
+    const dim3 grid((max_plane(g) + kThreads - 1) / kThreads, g.O, g.nd * g.N);
     const int T = max_T(g);
     timing_begin("sweep_fwd_generic", st);
     for (int t = 0; t < T; ++t) {
@@ -371,9 +375,9 @@ int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st)
     const unsigned blocks = (unsigned)((count + kThreads - 1) / kThreads);
     timing_begin("sum_dirs", st);
     if (dtype == PLSTM_BF16)
-        k_sum_dirs<uint16_t><<<blocks, kThreads, 0, st>>>(count, hd, (uint16_t *)h);
+        k_sum_dirs<uint16_t><<<blocks, kThreads, 0, st>>>(count, g.nd, hd, (uint16_t *)h);
     else
-        k_sum_dirs<float><<<blocks, kThreads, 0, st>>>(count, hd, (float *)h);
+        k_sum_dirs<float><<<blocks, kThreads, 0, st>>>(count, g.nd, hd, (float *)h);
     PLSTM_LAUNCH_CHECK();
     timing_end(1, st);
     return PLSTM_OK;
@@ -382,10 +386,10 @@ int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st)
 size_t generic_backward_ws(const Geom &g)
 {
     Carve cv(nullptr);
-    const int G = 4 * g.O, KT = g.K * g.K * (g.C + g.O) + 1;
-    cv.take<float>((size_t)kDirs * g.N * g.V * G);                      // dA
-    cv.take<float>((size_t)kDirs * g.N * g.V * g.O);                    // dL/dc
-    cv.take<float>((size_t)kDirs * wgrad_chunks(g) * G * KT);           // partials
+    const int G = 4 * g.O, KT = g.KP * g.KQ * (g.C + g.O) + 1;
+    cv.take<float>((size_t)g.nd * g.N * g.V * G);                       // dA
+    cv.take<float>((size_t)g.nd * g.N * g.V * g.O);                     // dL/dc
+    cv.take<float>((size_t)g.nd * wgrad_chunks(g) * G * KT);            // partials
     return cv.off;
 }
 
@@ -394,14 +398,14 @@ int generic_backward(const Geom &g, const float *x, const float *wx, const float
                      float *db, void *ws, hipStream_t st)
 {
     const float *gates = sv.gates, *cell = sv.cell;
-    const int G = 4 * g.O, KT = g.K * g.K * (g.C + g.O) + 1;
+    const int G = 4 * g.O, KT = g.KP * g.KQ * (g.C + g.O) + 1;
     Carve cv(ws);
-    float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * G);
-    float *gc = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
+    float *dA = cv.take<float>((size_t)g.nd * g.N * g.V * G);
+    float *gc = cv.take<float>((size_t)g.nd * g.N * g.V * g.O);
     const int nchunk = wgrad_chunks(g);
-    float *partial = cv.take<float>((size_t)kDirs * nchunk * G * KT);
+    float *partial = cv.take<float>((size_t)g.nd * nchunk * G * KT);
 
-    const dim3 grid((max_plane(g) + kThreads - 1) / kThreads, g.O, kDirs * g.N);
+    const dim3 grid((max_plane(g) + kThreads - 1) / kThreads, g.O, g.nd * g.N);
     timing_begin("sweep_bwd_generic", st);
     for (int t = max_T(g) - 1; t >= 0; --t) {
         k_bwd_step<<<grid, kThreads, 0, st>>>(g, t, wh, gates, cell, dh, dA, gc);
@@ -409,10 +413,10 @@ int generic_backward(const Geom &g, const float *x, const float *wx, const float
     }
     timing_end(max_T(g), st);
     timing_begin("wgrad_generic", st);
-    const dim3 wg_grid((KT + kTile - 1) / kTile, (G + kTile - 1) / kTile, kDirs * nchunk);
+    const dim3 wg_grid((KT + kTile - 1) / kTile, (G + kTile - 1) / kTile, g.nd * nchunk);
     k_wgrad_partial<<<wg_grid, kThreads, 0, st>>>(g, wgrad_chunk_len(g), nchunk, x, gates, cell, dA, partial);
     PLSTM_LAUNCH_CHECK();
-    const long long nout = (long long)kDirs * G * KT;
+    const long long nout = (long long)g.nd * G * KT;
     k_wgrad_reduce<<<(unsigned)((nout + kThreads - 1) / kThreads), kThreads, 0, st>>>(
         g, nchunk, partial, dwx, dwh, db);
     PLSTM_LAUNCH_CHECK();

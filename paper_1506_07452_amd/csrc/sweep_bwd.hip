@@ -581,7 +581,7 @@ int launch_wgrad(const Geom &g, const float *x, const float *hd, const float *dA
 bool sweep_bwd_supported(const Geom &g)
 {
     // dA slices are addressed as buffer resources: bytes must fit 32 bits
-    return g.K == 3 && g.O == kO && g.C >= 1 && g.C <= 4 &&
+    return g.nd == kDirs && g.KP == 3 && g.KQ == 3 && g.O == kO && g.C >= 1 && g.C <= 4 &&
            g.V * kG * (long long)sizeof(float) < (1LL << 31);
 }
 

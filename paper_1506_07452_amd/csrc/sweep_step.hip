@@ -101,8 +101,8 @@ __device__ inline bool on_plane(int p, int q, int P, int Q)
 {
     return ((unsigned)p < (unsigned)P) & ((unsigned)q < (unsigned)Q);
 }
-// Tap (ka, kb) of a K x K filter from its index: ka = tap / K with the
-// multiplier k_mul = ceil(2^16 / K) (exact for tap < 2^12).
+// Tap (ka, kb) of a KP x KQ filter from its index: ka = tap / KQ with the
+// multiplier k_mul = ceil(2^16 / KQ) (exact for tap < 2^12).
 __device__ inline int tap_row(int tap, int k_mul) { return (tap * k_mul) >> 16; }
 
 // ---- conversion and repacking (once per call) -------------------------------
@@ -125,14 +125,14 @@ k_pad_x(long long nvox, int C, int Cp, const TS *__restrict__ x, float *__restri
 // the weight of gate-unit gate*O + 16 ug + col for channel 16 cb + 4q + i.
 template <typename TS>
 __global__ void __launch_bounds__(256)
-k_pack_fwd(int O, int C, int Cp, int KX, int KG, int KK, const TS *__restrict__ wx,
+k_pack_fwd(int nd, int O, int C, int Cp, int KX, int KG, int KK, const TS *__restrict__ wx,
            const TS *__restrict__ wh, const TS *__restrict__ b, float *__restrict__ frag,
            float *__restrict__ bias)
 {
     const int U = O / 16, G = 4 * O, CX = Cp / 16;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (i < (long long)kDirs * G) bias[i] = Store<TS>::load(b, i);
-    if (i >= (long long)kDirs * U * KG * 1024) return;
+    if (i < (long long)nd * G) bias[i] = Store<TS>::load(b, i);
+    if (i >= (long long)nd * U * KG * 1024) return;
     const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63), gate = (int)((i >> 8) & 3);
     long long r = i >> 10;
     const int kg = (int)(r % KG);
@@ -154,11 +154,11 @@ k_pack_fwd(int O, int C, int Cp, int KX, int KG, int KK, const TS *__restrict__ 
 // Backward A fragments fragB[d][ug][kg][lane][4], kg = tap * 4U + mb: entry
 // i of lane (q, col) is W_h[d][gate-unit 16 mb + 4q + i][unit 16 ug + col][tap].
 __global__ void __launch_bounds__(256)
-k_pack_bwd(int O, int KK, const float *__restrict__ wh, float *__restrict__ frag)
+k_pack_bwd(int nd, int O, int KK, const float *__restrict__ wh, float *__restrict__ frag)
 {
     const int U = O / 16, G = 4 * O, KG = KK * 4 * U;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (i >= (long long)kDirs * U * KG * 256) return;
+    if (i >= (long long)nd * U * KG * 256) return;
     const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63);
     long long r = i >> 8;
     const int kg = (int)(r % KG);
@@ -173,11 +173,12 @@ k_pack_bwd(int O, int KK, const float *__restrict__ wh, float *__restrict__ frag
 // dL/dx A fragments fragX[d][tap][mb][ct][lane][4]: entry i of lane (q, col)
 // is W_x[d][gate-unit 16 mb + 4q + i][channel 16 ct + col][tap] (0 past C).
 __global__ void __launch_bounds__(256)
-k_pack_dx(int O, int C, int CT, int KK, const float *__restrict__ wx, float *__restrict__ frag)
+k_pack_dx(int nd, int O, int C, int CT, int KK, const float *__restrict__ wx,
+          float *__restrict__ frag)
 {
     const int G = 4 * O, MB = G / 16;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (i >= (long long)kDirs * KK * MB * CT * 256) return;
+    if (i >= (long long)nd * KK * MB * CT * 256) return;
     const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63);
     long long r = i >> 8;
     const int ct = (int)(r % CT);
@@ -246,7 +247,7 @@ k_step_fwd(FwdStepArgs a)
     const int Cp = a.Cp, CX = Cp >> 4, KX = a.KX;
     const int hoff = -dg.sign * ss;   // voxel of plane t - 1 = voxel of plane t + hoff
     const int uo = ug * 16 + 4 * q4;
-    const int K = a.g.K, rad = K >> 1;
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
 
     // this lane's pixel of each tile: voxel and in-plane coordinates
     int vox[kNT], tp[kNT], tq[kNT];
@@ -305,7 +306,7 @@ k_step_fwd(FwdStepArgs a)
         const int tap = is_x ? (kk * a.cx_mul) >> 16 : kk / U;
         const int cb = kk - tap * (is_x ? CX : U);
         const int stride = is_x ? Cp : O;
-        const int ka = tap_row(tap, a.k_mul) - rad, kb = tap - (ka + rad) * K - rad;
+        const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
         const int dv = (is_x ? 0 : hoff) + ka * sp + kb * sq;
         const auto rs = is_x ? rs_x : rs_h;
 #pragma unroll
@@ -415,14 +416,15 @@ k_pad_x_b16(long long nvox, int C, int C32, const uint16_t *__restrict__ x,
 // (kg - KX) / (O/32), block (kg - KX) % (O/32).  Entry j of lane (q, col)
 // is the weight of gate-unit gate*O + 16 ug + col for channel 32 cb + 8q + j.
 __global__ void __launch_bounds__(256)
-k_pack_fwd_b16(int O, int C, int C32, int KX, int KG, int KK, const uint16_t *__restrict__ wx,
+k_pack_fwd_b16(int nd, int O, int C, int C32, int KX, int KG, int KK,
+               const uint16_t *__restrict__ wx,
                const uint16_t *__restrict__ wh, const uint16_t *__restrict__ b,
                uint16_t *__restrict__ frag, float *__restrict__ bias)
 {
     const int U = O / 16, G = 4 * O, CX = C32 / 32, UH = O / 32;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (i < (long long)kDirs * G) bias[i] = bf16_to_f32(b[i]);
-    if (i >= (long long)kDirs * U * KG * 2048) return;
+    if (i < (long long)nd * G) bias[i] = bf16_to_f32(b[i]);
+    if (i >= (long long)nd * U * KG * 2048) return;
     const int j8 = (int)(i & 7), lane = (int)((i >> 3) & 63), gate = (int)((i >> 9) & 3);
     long long r = i >> 11;
     const int kg = (int)(r % KG);
@@ -485,7 +487,7 @@ k_step_fwd_b16(FwdB16Args a)
     const int C32 = a.C32, CX = C32 >> 5, KX = a.KX;
     const int hoff = -dg.sign * ss;
     const int uo = ug * 16 + 4 * q4;
-    const int K = a.g.K, rad = K >> 1;
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
 
     int vox[kNT], tp[kNT], tq[kNT];
 #pragma unroll
@@ -542,7 +544,7 @@ k_step_fwd_b16(FwdB16Args a)
         const int tap = is_x ? (kk * a.cx_mul32) >> 16 : kk / UH;
         const int cb = kk - tap * (is_x ? CX : UH);
         const int stride = is_x ? C32 : O;
-        const int ka = tap_row(tap, a.k_mul) - rad, kb = tap - (ka + rad) * K - rad;
+        const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
         const int dv = (is_x ? 0 : hoff) + ka * sp + kb * sq;
         const auto rs = is_x ? rs_x : rs_h;
 #pragma unroll
@@ -650,7 +652,7 @@ k_step_bwd(BwdStepArgs a)
     const long long V = a.g.V;
     const bool has_next = t + 1 < dg.T;
     const int noff = dg.sign * ss;    // voxel of plane t + 1 = voxel of plane t + noff
-    const int K = a.g.K, rad = K >> 1, KG = K * K * MB;
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1, KG = a.g.KP * KQ * MB;
 
     // this lane's pixel of each tile: voxel and in-plane coordinates (the
     // pixels that received its h through tap (ka, kb) are (p - ka + r, q - kb + r))
@@ -683,7 +685,7 @@ k_step_bwd(BwdStepArgs a)
             const int tap = kg / MB, mb = kg - tap * MB;
 #pragma unroll
             for (int u = 0; u < U; ++u) o.a[u] = *(const f4 *)(fr + ((long long)u * KG + kg) * 256);
-            const int ka = tap_row(tap, a.k_mul) - rad, kb = tap - (ka + rad) * K - rad;
+            const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
             const int dv = noff - ka * sp - kb * sq;
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
@@ -815,7 +817,7 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
 {
     constexpr int O = 16 * U, G = 4 * O;
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
-    const int K = a.g.K, KK = K * K, rad = K >> 1;
+    const int KQ = a.g.KQ, KK = a.g.KP * KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
     const DirGeom dg = a.g.dir[d];
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
     const int P = dg.P, Q = dg.Q;
@@ -833,9 +835,9 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
     for (int j = 0; j < NTL; ++j) {
         const int tt = t0 + j;
         const bool real = j < ntl;
-        const int tap = real ? tt / cbn : KK / 2;
-        const int ka = tap / K, kb = tap % K;
-        dtap[j] = __builtin_amdgcn_readfirstlane((ka - rad) * sp + (kb - rad) * sq);
+        const int tap = real ? tt / cbn : radp * KQ + radq;
+        const int ka = tap / KQ, kb = tap % KQ;
+        dtap[j] = __builtin_amdgcn_readfirstlane((ka - radp) * sp + (kb - radq) * sq);
         tapok[j] = __builtin_amdgcn_readfirstlane(ka | kb << 3);
         chn[j] = real ? (tt % cbn) * 16 + col : -1;
     }
@@ -900,7 +902,8 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
             const int vb = pl * ss + c.p * sp + qq * sq;
 #pragma unroll
             for (int j = 0; j < NTL; ++j) {
-                const int pp = c.p + (int)(tapok[j] & 7) - rad, qn = qq + (int)(tapok[j] >> 3) - rad;
+                const int pp = c.p + (int)(tapok[j] & 7) - radp;
+                const int qn = qq + (int)(tapok[j] >> 3) - radq;
                 const bool ok = src_ok & (chn[j] >= 0) & ((unsigned)pp < (unsigned)P) &
                                 ((unsigned)qn < (unsigned)Q);
                 o.b[ks][j] =
@@ -944,11 +947,11 @@ k_wgrad_step(WgStepArgs a)
 {
     const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int Cp = a.Cp, CX = Cp >> 4;
-    const int KK = a.g.K * a.g.K;
+    const int KK = a.g.KP * a.g.KQ;
     const WgBlocks wb = wg_blocks(U, CX, KK);
     const int nblk = wb.nh + wb.nx;
     const int per_dir = U * nblk * a.kch;
-    if (item >= kDirs * per_dir) return;
+    if (item >= a.g.nd * per_dir) return;
     const int d = item / per_dir;
     int r = item - d * per_dir;
     const int kc = r % a.kch;
@@ -987,10 +990,10 @@ k_db_partial(int G, long long nvox, const float *__restrict__ dA, float *__restr
 }
 
 __global__ void __launch_bounds__(256)
-k_db_reduce(int G, const float *__restrict__ part, float *__restrict__ db)
+k_db_reduce(int nd, int G, const float *__restrict__ part, float *__restrict__ db)
 {
     const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= kDirs * G) return;
+    if (i >= nd * G) return;
     const int d = i / G, m = i % G;
     float acc = 0.0f;
     for (int ch = 0; ch < kDbChunks; ++ch) acc += part[((long long)d * kDbChunks + ch) * G + m];
@@ -999,13 +1002,13 @@ k_db_reduce(int G, const float *__restrict__ part, float *__restrict__ db)
 
 // dW = sum of the chunk partials in chunk order, scattered to the ABI layouts.
 __global__ void __launch_bounds__(256)
-k_wgrad_step_reduce(int O, int C, int Cp, int KK, int NTt, int kch,
+k_wgrad_step_reduce(int nd, int O, int C, int Cp, int KK, int NTt, int kch,
                     const float *__restrict__ partial, float *__restrict__ dwx,
                     float *__restrict__ dwh)
 {
     const int G = 4 * O, KC = KK * (O + Cp), KCp = NTt * 16;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (i >= (long long)kDirs * G * KC) return;
+    if (i >= (long long)nd * G * KC) return;
     const int k = (int)(i % KC);
     const int gu = (int)((i / KC) % G);
     const int d = (int)(i / ((long long)KC * G));
@@ -1042,7 +1045,7 @@ k_dx_step(DxStepArgs a)
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
     const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (item >= a.g.N * a.nvg) return;
-    const int K = a.g.K, rad = K >> 1, KG = K * K * MB;
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1, KG = a.g.KP * KQ * MB;
     const int n = item / a.nvg, vg = item - n * a.nvg;
     const long long V = a.g.V;
     const int H = a.g.H, W = a.g.W, C = a.g.C;
@@ -1067,16 +1070,17 @@ k_dx_step(DxStepArgs a)
         f4 a[CT];
         f4 b[kNT];
     };
-    for (int d = 0; d < kDirs; ++d) {
+    for (int d = 0; d < a.g.nd; ++d) {
         const DirGeom dg = a.g.dir[d];
         const int sp = (int)dg.sp, sq = (int)dg.sq, P = dg.P, Q = dg.Q;
+        const int ax = a.g.axis[d];
         // in-plane coordinates of each voxel for this direction (the pixel
         // (p - ka + r, q - kb + r) received x through tap (ka, kb))
         int tp[kNT], tq[kNT];
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) {
-            tp[nt] = vv[nt] >= 0 ? (d < 2 ? yc[nt] : zc[nt]) : kDead;
-            tq[nt] = d < 4 ? xc[nt] : yc[nt];
+            tp[nt] = vv[nt] >= 0 ? (ax == 0 ? yc[nt] : zc[nt]) : kDead;
+            tq[nt] = ax < 2 ? xc[nt] : yc[nt];
         }
         const auto rs = slice_rsrc(a.dA + ((long long)d * a.g.N + n) * V * G, V * G);
         const float *fr = a.frag + (long long)d * KG * CT * 256 + lane * 4;
@@ -1085,7 +1089,7 @@ k_dx_step(DxStepArgs a)
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
                 o.a[ct] = *(const f4 *)(fr + ((long long)kg * CT + ct) * 256);
-            const int ka = tap_row(tap, a.k_mul) - rad, kb = tap - (ka + rad) * K - rad;
+            const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
             const int dv = -ka * sp - kb * sq;
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
@@ -1138,11 +1142,11 @@ inline int pad16(int c) { return (c + 15) / 16 * 16; }
 inline unsigned blocks_for(long long n, int per) { return (unsigned)((n + per - 1) / per); }
 
 inline int npg_of(const DirGeom &dg) { return (dg.P * dg.Q + 16 * kNT - 1) / (16 * kNT); }
-inline int k_mul_of(const Geom &g) { return (65536 + g.K - 1) / g.K; }
+inline int k_mul_of(const Geom &g) { return (65536 + g.KQ - 1) / g.KQ; }
 inline int max_T(const Geom &g)
 {
     int m = 0;
-    for (int d = 0; d < kDirs; ++d) m = g.dir[d].T > m ? g.dir[d].T : m;
+    for (int d = 0; d < g.nd; ++d) m = g.dir[d].T > m ? g.dir[d].T : m;
     return m;
 }
 
@@ -1154,14 +1158,14 @@ struct WgShape {
 // the chunk count that minimises that (ties: fewer chunks).
 inline WgShape wg_shape(const Geom &g)
 {
-    const int U = g.O / 16, CX = pad16(g.C) / 16, KK = g.K * g.K;
+    const int U = g.O / 16, CX = pad16(g.C) / 16, KK = g.KP * g.KQ;
     const WgBlocks wb = wg_blocks(U, CX, KK);
     WgShape w;
     w.NTt = KK * U + KK * CX;
     w.nblk = wb.nh + wb.nx;
     const DevInfo di = device_info();
     const long long simds = 4LL * (di.cus > 0 ? di.cus : 256);
-    const long long per = (long long)kDirs * U * w.nblk;
+    const long long per = (long long)g.nd * U * w.nblk;
     double best = 1e30;
     w.kch = 1;
     for (int k = 1; k <= kWgMaxChunks; ++k) {
@@ -1257,7 +1261,7 @@ int g_step_bf16_mfma = 1;
 bool step_supported(const Geom &g)
 {
     if (g.O != 16 && g.O != 32 && g.O != 64) return false;
-    if (g.K < 1 || g.K > 7 || g.K % 2 == 0) return false;
+    if (g.KQ < 1 || g.KQ > 7 || g.KQ % 2 == 0 || (g.KP != 1 && g.KP != g.KQ)) return false;
     const long long Cp = pad16(g.C);
     if (Cp > 64) return false;
     // slices addressed through buffer resources: byte sizes fit 31 bits
@@ -1265,7 +1269,7 @@ bool step_supported(const Geom &g)
     if (g.V * 4 * g.O * 4 >= lim || g.V * Cp * 4 >= lim) return false;
     // wave items of a step fit an int
     long long items = 0;
-    for (int d = 0; d < kDirs; ++d) items += (long long)g.N * (g.O / 16) * npg_of(g.dir[d]);
+    for (int d = 0; d < g.nd; ++d) items += (long long)g.N * (g.O / 16) * npg_of(g.dir[d]);
     return items < (1LL << 30);
 }
 
@@ -1278,19 +1282,19 @@ inline int pad32(int c) { return (c + 31) / 32 * 32; }
 
 size_t step_fwd_ws(const Geom &g)
 {
-    const int U = g.O / 16, Cp = pad16(g.C), KK = g.K * g.K, KG = KK * (Cp + g.O) / 16;
+    const int U = g.O / 16, Cp = pad16(g.C), KK = g.KP * g.KQ, KG = KK * (Cp + g.O) / 16;
     Carve cv(nullptr);
     cv.take<float>((size_t)g.N * g.V * Cp);          // padded x
-    cv.take<float>((size_t)kDirs * U * KG * 1024);   // A fragments
-    cv.take<float>((size_t)kDirs * 4 * g.O);         // bias
+    cv.take<float>((size_t)g.nd * U * KG * 1024);    // A fragments
+    cv.take<float>((size_t)g.nd * 4 * g.O);          // bias
     size_t need = cv.off;
     if (g.O % 32 == 0) {                             // bf16 variant
         const int C32 = pad32(g.C), KGb = KK * (C32 + g.O) / 32;
         Carve cb(nullptr);
         cb.take<uint16_t>((size_t)g.N * g.V * C32);
-        cb.take<uint16_t>((size_t)kDirs * U * KGb * 2048);
-        cb.take<float>((size_t)kDirs * 4 * g.O);
-        cb.take<uint16_t>((size_t)kDirs * g.N * g.V * g.O);
+        cb.take<uint16_t>((size_t)g.nd * U * KGb * 2048);
+        cb.take<float>((size_t)g.nd * 4 * g.O);
+        cb.take<uint16_t>((size_t)g.nd * g.N * g.V * g.O);
         if (cb.off > need) need = cb.off;
     }
     return need;
@@ -1323,18 +1327,19 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
                         hipStream_t st)
 {
     const int U = g.O / 16, C32 = pad32(g.C);
-    const int KK = g.K * g.K, KX = KK * C32 / 32, KG = KX + KK * g.O / 32;
+    const int KK = g.KP * g.KQ, KX = KK * C32 / 32, KG = KX + KK * g.O / 32;
     Carve cv(ws);
     uint16_t *xb = cv.take<uint16_t>((size_t)g.N * g.V * C32);
-    uint16_t *frag = cv.take<uint16_t>((size_t)kDirs * U * KG * 2048);
-    float *bias = cv.take<float>((size_t)kDirs * 4 * g.O);
-    uint16_t *hb = cv.take<uint16_t>((size_t)kDirs * g.N * g.V * g.O);
+    uint16_t *frag = cv.take<uint16_t>((size_t)g.nd * U * KG * 2048);
+    float *bias = cv.take<float>((size_t)g.nd * 4 * g.O);
+    uint16_t *hb = cv.take<uint16_t>((size_t)g.nd * g.N * g.V * g.O);
     const long long nvox = (long long)g.N * g.V;
-    const long long nfrag = (long long)kDirs * U * KG * 2048;
+    const long long nfrag = (long long)g.nd * U * KG * 2048;
     timing_begin("sweep_fwd_step_bf16", st);
     k_pad_x_b16<<<blocks_for(nvox * C32, 256), 256, 0, st>>>(nvox, g.C, C32, x, xb);
     PLSTM_LAUNCH_CHECK();
-    k_pack_fwd_b16<<<blocks_for(nfrag, 256), 256, 0, st>>>(g.O, g.C, C32, KX, KG, KK, wx, wh, b,
+    k_pack_fwd_b16<<<blocks_for(nfrag, 256), 256, 0, st>>>(g.nd, g.O, g.C, C32, KX, KG, KK, wx, wh,
+                                                           b,
                                                            frag, bias);
     PLSTM_LAUNCH_CHECK();
     FwdB16Args a;
@@ -1359,13 +1364,13 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
         return step_fwd_b16(g, (const uint16_t *)x, (const uint16_t *)wx, (const uint16_t *)wh,
                             (const uint16_t *)b, hd, cell, ws, st);
     const int U = g.O / 16, Cp = pad16(g.C);
-    const int KK = g.K * g.K, KX = KK * Cp / 16, KG = KX + KK * U;
+    const int KK = g.KP * g.KQ, KX = KK * Cp / 16, KG = KX + KK * U;
     Carve cv(ws);
     float *xp = cv.take<float>((size_t)g.N * g.V * Cp);
-    float *frag = cv.take<float>((size_t)kDirs * U * KG * 1024);
-    float *bias = cv.take<float>((size_t)kDirs * 4 * g.O);
+    float *frag = cv.take<float>((size_t)g.nd * U * KG * 1024);
+    float *bias = cv.take<float>((size_t)g.nd * 4 * g.O);
     const long long nvox = (long long)g.N * g.V;
-    const long long nfrag = (long long)kDirs * U * KG * 1024;
+    const long long nfrag = (long long)g.nd * U * KG * 1024;
 
     timing_begin("sweep_fwd_step", st);
     if (dtype == PLSTM_BF16) {
@@ -1373,14 +1378,15 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
                                                                       (const uint16_t *)x, xp);
         PLSTM_LAUNCH_CHECK();
         k_pack_fwd<uint16_t><<<blocks_for(nfrag, 256), 256, 0, st>>>(
-            g.O, g.C, Cp, KX, KG, KK, (const uint16_t *)wx, (const uint16_t *)wh,
+            g.nd, g.O, g.C, Cp, KX, KG, KK, (const uint16_t *)wx, (const uint16_t *)wh,
             (const uint16_t *)b, frag, bias);
     } else {
         k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
                                                                    (const float *)x, xp);
         PLSTM_LAUNCH_CHECK();
         k_pack_fwd<float><<<blocks_for(nfrag, 256), 256, 0, st>>>(
-            g.O, g.C, Cp, KX, KG, KK, (const float *)wx, (const float *)wh, (const float *)b, frag,
+            g.nd, g.O, g.C, Cp, KX, KG, KK, (const float *)wx, (const float *)wh, (const float *)b,
+            frag,
             bias);
     }
     PLSTM_LAUNCH_CHECK();
@@ -1406,16 +1412,16 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
 
 size_t step_bwd_ws(const Geom &g)
 {
-    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O, KK = g.K * g.K;
+    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O, KK = g.KP * g.KQ;
     const WgShape w = wg_shape(g);
     Carve cv(nullptr);
-    cv.take<float>((size_t)kDirs * g.N * g.V * G);                 // dA
-    cv.take<float>((size_t)kDirs * g.N * g.V * g.O);               // dL/dc * f
-    cv.take<float>((size_t)kDirs * U * KK * 4 * U * 256);          // W_h^T fragments
+    cv.take<float>((size_t)g.nd * g.N * g.V * G);                  // dA
+    cv.take<float>((size_t)g.nd * g.N * g.V * g.O);                // dL/dc * f
+    cv.take<float>((size_t)g.nd * U * KK * 4 * U * 256);           // W_h^T fragments
     cv.take<float>((size_t)g.N * g.V * Cp);                        // padded x
-    cv.take<float>((size_t)kDirs * w.kch * G * w.NTt * 16);        // weight-gradient partials
-    cv.take<float>((size_t)kDirs * KK * 4 * U * (Cp / 16) * 256);  // W_x^T fragments
-    cv.take<float>((size_t)kDirs * kDbChunks * G);                 // db partials
+    cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);         // weight-gradient partials
+    cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);   // W_x^T fragments
+    cv.take<float>((size_t)g.nd * kDbChunks * G);                  // db partials
     return cv.off;
 }
 
@@ -1425,10 +1431,10 @@ int step_dx(const Geom &g, const float *wx, const float *dA, float *fragx, float
             hipStream_t st)
 {
     const int U = g.O / 16, CT = pad16(g.C) / 16;
-    const int KK = g.K * g.K;
-    const long long nf = (long long)kDirs * KK * 4 * U * CT * 256;
+    const int KK = g.KP * g.KQ;
+    const long long nf = (long long)g.nd * KK * 4 * U * CT * 256;
     timing_begin("dx_step", st);
-    k_pack_dx<<<blocks_for(nf, 256), 256, 0, st>>>(g.O, g.C, CT, KK, wx, fragx);
+    k_pack_dx<<<blocks_for(nf, 256), 256, 0, st>>>(g.nd, g.O, g.C, CT, KK, wx, fragx);
     PLSTM_LAUNCH_CHECK();
     DxStepArgs a;
     a.g = g;
@@ -1452,7 +1458,7 @@ int step_dx(const Geom &g, const float *wx, const float *dA, float *fragx, float
 size_t step_dx_ws(const Geom &g)
 {
     Carve cv(nullptr);
-    cv.take<float>((size_t)kDirs * g.K * g.K * 4 * (g.O / 16) * (pad16(g.C) / 16) * 256);
+    cv.take<float>((size_t)g.nd * g.KP * g.KQ * 4 * (g.O / 16) * (pad16(g.C) / 16) * 256);
     return cv.off;
 }
 
@@ -1461,21 +1467,21 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
              hipStream_t st)
 {
     if (!step_supported(g)) return PLSTM_EUNSUPPORTED;
-    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O, KK = g.K * g.K;
+    const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O, KK = g.KP * g.KQ;
     const WgShape w = wg_shape(g);
     Carve cv(ws);
-    float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * G);
-    float *gcf = cv.take<float>((size_t)kDirs * g.N * g.V * g.O);
-    float *frag = cv.take<float>((size_t)kDirs * U * KK * 4 * U * 256);
+    float *dA = cv.take<float>((size_t)g.nd * g.N * g.V * G);
+    float *gcf = cv.take<float>((size_t)g.nd * g.N * g.V * g.O);
+    float *frag = cv.take<float>((size_t)g.nd * U * KK * 4 * U * 256);
     float *xp = cv.take<float>((size_t)g.N * g.V * Cp);
-    float *partial = cv.take<float>((size_t)kDirs * w.kch * G * w.NTt * 16);
-    float *fragx = cv.take<float>((size_t)kDirs * KK * 4 * U * (Cp / 16) * 256);
-    float *dbpart = cv.take<float>((size_t)kDirs * kDbChunks * G);
+    float *partial = cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);
+    float *fragx = cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);
+    float *dbpart = cv.take<float>((size_t)g.nd * kDbChunks * G);
     const long long nvox = (long long)g.N * g.V;
 
     timing_begin("sweep_bwd_step", st);
-    k_pack_bwd<<<blocks_for((long long)kDirs * U * KK * 4 * U * 256, 256), 256, 0, st>>>(
-        g.O, KK, wh, frag);
+    k_pack_bwd<<<blocks_for((long long)g.nd * U * KK * 4 * U * 256, 256), 256, 0, st>>>(
+        g.nd, g.O, KK, wh, frag);
     PLSTM_LAUNCH_CHECK();
     BwdStepArgs a;
     a.g = g;
@@ -1503,20 +1509,20 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     wa.xp = xp; wa.hd = sv.hd; wa.dA = dA;
     wa.partial = partial;
     wa.k_mul = k_mul_of(g);
-    const long long witems = (long long)kDirs * U * w.nblk * w.kch;
+    const long long witems = (long long)g.nd * U * w.nblk * w.kch;
     switch (U) {
     case 1: k_wgrad_step<1><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
     case 2: k_wgrad_step<2><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
     default: k_wgrad_step<4><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
     }
     PLSTM_LAUNCH_CHECK();
-    const long long nout = (long long)kDirs * G * KK * (g.O + Cp);
-    k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.O, g.C, Cp, KK, w.NTt, w.kch,
-                                                               partial, dwx, dwh);
+    const long long nout = (long long)g.nd * G * KK * (g.O + Cp);
+    k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.nd, g.O, g.C, Cp, KK, w.NTt,
+                                                               w.kch, partial, dwx, dwh);
     PLSTM_LAUNCH_CHECK();
-    k_db_partial<<<dim3(kDbChunks, kDirs), 256, 0, st>>>(G, nvox, dA, dbpart);
+    k_db_partial<<<dim3(kDbChunks, g.nd), 256, 0, st>>>(G, nvox, dA, dbpart);
     PLSTM_LAUNCH_CHECK();
-    k_db_reduce<<<blocks_for(kDirs * G, 256), 256, 0, st>>>(G, dbpart, db);
+    k_db_reduce<<<blocks_for(g.nd * G, 256), 256, 0, st>>>(g.nd, G, dbpart, db);
     PLSTM_LAUNCH_CHECK();
     timing_end(5, st);
     if (dx) return step_dx(g, wx, dA, fragx, dx, st);

@@ -15,7 +15,8 @@ import torch
 from . import (plstm_shape, pyramid_fc_tanh_backward, pyramid_fc_tanh_forward,
                pyramid_head_train, pyramid_head_workspace_size, pyramid_lstm_backward,
                pyramid_lstm_forward, pyramid_lstm_saved_size, pyramid_lstm_workspace_size,
-               pyramid_softmax_ce, shape_for)
+               pyramid_lstm2d_backward, pyramid_lstm2d_forward, pyramid_lstm2d_saved_size,
+               pyramid_softmax_ce, shape2d_for, shape_for)
 
 
 @dataclass
@@ -49,6 +50,26 @@ def layer_backward(x, L: LayerW, saved, dh, want_dx=True, ws=None, stream=None):
     dx = torch.empty_like(x) if want_dx else None
     dwx, dwh, db = (torch.empty_like(t, dtype=torch.float32) for t in (L.wx, L.wh, L.b))
     pyramid_lstm_backward(s, x, L.wx, L.wh, L.b, saved, dh, dx, dwx, dwh, db, ws, stream)
+    return dx, dwx, dwh, db
+
+
+def layer2d_forward(x: torch.Tensor, L: LayerW, training: bool = False, ws=None, stream=None):
+    """2D layer over x [N][H][W][C] (weights [4][4O][C|O][K], b [4][4O]);
+    returns (h, saved or None)."""
+    s = shape2d_for(x, L.O, L.K)
+    h = torch.empty(x.shape[:-1] + (L.O,), dtype=x.dtype, device=x.device)
+    saved = None
+    if training:
+        saved = torch.empty(pyramid_lstm2d_saved_size(s), dtype=torch.uint8, device=x.device)
+    pyramid_lstm2d_forward(s, x, L.wx, L.wh, L.b, h, saved, ws, stream)
+    return h, saved
+
+
+def layer2d_backward(x, L: LayerW, saved, dh, want_dx=True, ws=None, stream=None):
+    s = shape2d_for(x, L.O, L.K)
+    dx = torch.empty_like(x) if want_dx else None
+    dwx, dwh, db = (torch.empty_like(t, dtype=torch.float32) for t in (L.wx, L.wh, L.b))
+    pyramid_lstm2d_backward(s, x, L.wx, L.wh, L.b, saved, dh, dx, dwx, dwh, db, ws, stream)
     return dx, dwx, dwh, db
 
 

@@ -208,6 +208,20 @@ def config(cfg: int) -> Instance:
     return make(CONFIGS[cfg])
 
 
+def image2d(N: int, H: int, W: int, C: int, O: int, K: int, seed: int, dtype: str = "f32",
+            scale: float = 0.2):
+    """Seeded image batch x [N][H][W][C] ~ N(0, 1) and 2D layer parameters
+    wx [4][4O][C][K], wh [4][4O][O][K] ~ U(-scale, scale), b [4][4O] (forget
+    gate 1, others 0), rounded to the storage type."""
+    rin, rw = np.random.default_rng(seed), np.random.default_rng(seed + 7919)
+    x = rin.standard_normal((N, H, W, C))
+    wx = rw.uniform(-scale, scale, size=(4, 4 * O, C, K))
+    wh = rw.uniform(-scale, scale, size=(4, 4 * O, O, K))
+    b = np.zeros((4, 4 * O))
+    b[:, O:2 * O] = 1.0
+    return tuple(to_storage(a, dtype) for a in (x, wx, wh, b))
+
+
 def upstream_grad(shape, seed: int, dtype: str = "f32") -> np.ndarray:
     """Seeded dL/dh for single-layer backward tests: N(0, 1)."""
     return to_storage(np.random.default_rng(seed).standard_normal(shape), dtype)

@@ -229,3 +229,51 @@ def test_stitch_and_crop_validation(lib):
     assert lib.pyramid_stitch_clear(0, 5, 6, 3, FAKE, FAKE, None) == -1
     assert lib.pyramid_stitch_finish(4, 5, 6, 3, FAKE, None, FAKE, None) == -1
 
+
+
+def shape2d(**kw):
+    d = dict(N=1, H=8, W=8, C=1, O=4, dtype=P.PLSTM_F32, K=3)
+    d.update(kw)
+    return P.plstm2d_shape(**d)
+
+
+def test_2d_sizes_and_validation(lib):
+    """The 2D entry points: four directions of saved state, the same shape
+    rules as the volume layer, every bad argument rejected before HIP."""
+    s = shape2d()
+    V = 8 * 8
+    assert P.pyramid_lstm2d_saved_size(s) >= 4 * V * 6 * 4 * 4
+    assert P.pyramid_lstm2d_saved_size(s) < 6 * V * 6 * 4 * 4
+    assert P.pyramid_lstm2d_workspace_size(s, 1) >= P.pyramid_lstm2d_workspace_size(s, 0) > 0
+    for bad in (dict(O=5), dict(C=0), dict(H=0), dict(W=-1), dict(dtype=3), dict(K=4),
+                dict(K=9), dict(N=0)):
+        assert P.pyramid_lstm2d_workspace_size(shape2d(**bad), 1) == 0, bad
+        assert P.pyramid_lstm2d_saved_size(shape2d(**bad)) == 0, bad
+    assert lib.pyramid_lstm2d_saved_size(None) == 0
+
+    def f(sh=s, nbytes=0, **over):
+        a = dict(x=FAKE, wx=FAKE, wh=FAKE, b=FAKE, h=FAKE, saved=None, ws=FAKE)
+        a.update(over)
+        return lib.pyramid_lstm2d_forward(ctypes.byref(sh), a["x"], a["wx"], a["wh"], a["b"],
+                                          a["h"], a["saved"], a["ws"], nbytes, None)
+    assert lib.pyramid_lstm2d_forward(None, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 0,
+                                      None) == -1
+    assert f(x=None) == -1
+    assert f(h=None) == -1
+    assert f(b=ctypes.c_void_p(0x10002)) == -1
+    assert f(shape2d(O=5)) == -2
+    assert f(shape2d(K=2)) == -1
+    assert f(shape2d(K=9)) == -2
+    assert f(nbytes=0) == -3
+    assert f(shape2d(dtype=P.PLSTM_BF16), saved=FAKE, nbytes=1 << 40) == -2
+
+    def bw(sh=s, nbytes=0, **over):
+        names = ["x", "wx", "wh", "b", "saved", "dh", "dx", "dwx", "dwh", "db", "ws"]
+        a = [FAKE] * 11
+        for k, v in over.items():
+            a[names.index(k)] = v
+        return lib.pyramid_lstm2d_backward(ctypes.byref(sh), *a, nbytes, None)
+    assert bw(saved=None) == -1
+    assert bw(dwx=None) == -1
+    assert bw(shape2d(dtype=P.PLSTM_BF16), nbytes=1 << 40) == -2
+    assert bw(nbytes=16) == -3

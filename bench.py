@@ -211,8 +211,9 @@ def bench_network(args, cfg):
         "scaling": "weak", "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic",
-        "config": {"workload": wl.name + (", fwd+bwd" if train else ", fwd") +
-                               (" + RMS-prop update, squared loss" if opt is not None else ""),
+        "config": {"workload": wl.name + (" (squared loss)" if opt is not None else "") +
+                               (", fwd+bwd" if train else ", fwd") +
+                               (" + RMS-prop update" if opt is not None else ""),
                    "N": wl.N,
                    "D": wl.D, "H": wl.H, "W": wl.W, "C": wl.C, "hidden": wl.hidden,
                    "fc": [wl.fc_width(i) for i in range(len(wl.hidden))], "K": wl.K,

@@ -169,7 +169,7 @@ CONFIGS = {
 # 240 x 240).  Five input channels and five classes are the reading under which
 # the paper's weight count is matched (to within 2); labels for training.
 PAPER_NET = Workload("paper network 7x7 16/25/32/45/64, MR sub-volume 25x240x240x5, "
-                     "softmax CE, fwd+bwd f32", 1, 25, 240, 240, 5, [16, 32, 64], classes=5,
+                     "softmax, f32", 1, 25, 240, 240, 5, [16, 32, 64], classes=5,
                      labels=True, kind="mr", cfg=6, K=7, fc_widths=[25, 45])
 
 

@@ -745,3 +745,97 @@ def test_2d_backward_finite_differences():
             fd = (lp - lm) / (2 * eps)
             assert abs(fd - grad.reshape(-1)[k]) <= 1e-8 + 1e-6 * abs(fd)
 
+
+
+# ------------------------------ training cubes: rotation about z and flips
+import oracle.augment as oaug
+
+
+def _vol(rng, N=2, D=5, H=23, W=19, C=3):
+    return rng.standard_normal((N, D, H, W, C)), rng.integers(0, 5, (N, D, H, W)).astype(np.int32)
+
+
+def test_augment_identity_is_the_crop():
+    rng = np.random.default_rng(190)
+    v, lab = _vol(rng)
+    cube, cl = oaug.sample(v, lab, 1, (1, 4, 3), (3, 10, 12), 1.0, 0.0, 0)
+    assert np.array_equal(cube, v[1, 1:4, 4:14, 3:15])
+    assert np.array_equal(cl, lab[1, 1:4, 4:14, 3:15])
+
+
+@pytest.mark.parametrize("flips", range(8))
+def test_augment_flips_are_numpy_flips(flips):
+    rng = np.random.default_rng(191)
+    v, lab = _vol(rng)
+    crop, lcrop = v[0, 0:4, 2:11, 5:18], lab[0, 0:4, 2:11, 5:18]
+    axes = [ax for bit, ax in ((1, 0), (2, 1), (4, 2)) if flips & bit]
+    cube, cl = oaug.sample(v, lab, 0, (0, 2, 5), (4, 9, 13), 1.0, 0.0, flips)
+    want = np.flip(crop, axis=axes) if axes else crop
+    lwant = np.flip(lcrop, axis=axes) if axes else lcrop
+    assert np.array_equal(cube, want) and np.array_equal(cl, lwant)
+
+
+@pytest.mark.parametrize("n", [8, 9])
+def test_augment_quarter_turn_is_rot90(n):
+    """(c, s) = (0, 1), exact in fp32: every source coordinate is an integer,
+    and the cube is the crop turned by a quarter (numpy's rot90, clockwise)."""
+    rng = np.random.default_rng(192 + n)
+    v, lab = _vol(rng)
+    crop, lcrop = v[1, 1:3, 3:3 + n, 2:2 + n], lab[1, 1:3, 3:3 + n, 2:2 + n]
+    cube, cl = oaug.sample(v, lab, 1, (1, 3, 2), (2, n, n), 0.0, 1.0, 0)
+    assert np.array_equal(cube, np.rot90(crop, -1, axes=(1, 2)))
+    assert np.array_equal(cl, np.rot90(lcrop, -1, axes=(1, 2)))
+    # the flip acts on the turned cube, not on the source
+    fl, fll = oaug.sample(v, lab, 1, (1, 3, 2), (2, n, n), 0.0, 1.0, oaug.FLIP_X)
+    assert np.array_equal(fl, np.rot90(crop, -1, axes=(1, 2))[:, :, ::-1])
+    assert not np.array_equal(fl, np.rot90(crop[:, :, ::-1], -1, axes=(1, 2)))
+    assert np.array_equal(fll, np.rot90(lcrop, -1, axes=(1, 2))[:, :, ::-1])
+    half, hl = oaug.sample(v, lab, 1, (1, 3, 2), (2, n, n), -1.0, 0.0, 0)   # half turn
+    assert np.array_equal(half, crop[:, ::-1, ::-1])
+    assert np.array_equal(hl, lcrop[:, ::-1, ::-1])
+
+
+@pytest.mark.parametrize("theta", [0.3, 1.0, 2.5, -0.7, 4.0])
+def test_augment_reproduces_affine_fields(theta):
+    """Bilinear interpolation is exact on a field affine in (y, x): the cube
+    is that field at the rotated (and clamped) positions, in closed form."""
+    D, H, W = 3, 40, 37
+    a, by, bx = 0.25, 0.75, -0.5
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    field = a + by * yy + bx * xx
+    v = np.broadcast_to(field[None, None, :, :, None], (1, D, H, W, 2)).copy()
+    v[..., 1] *= 2.0
+    z0, y0, x0, d, h, w = 0, 5, 3, 2, 30, 31
+    c, s = np.cos(theta), np.sin(theta)
+    cube, _ = oaug.sample(v, None, 0, (z0, y0, x0), (d, h, w), c, s, 0)
+    i = np.arange(h)[:, None] - (h - 1) / 2
+    j = np.arange(w)[None, :] - (w - 1) / 2
+    ys = np.clip(y0 + (h - 1) / 2 + c * i - s * j, 0, H - 1)
+    xs = np.clip(x0 + (w - 1) / 2 + s * i + c * j, 0, W - 1)
+    want = a + by * ys + bx * xs
+    for k in range(d):
+        np.testing.assert_allclose(cube[k, ..., 0], want, atol=2e-5)
+        np.testing.assert_allclose(cube[k, ..., 1], 2 * want, atol=4e-5)
+    if theta in (1.0, 2.5):                      # those cubes reach past the slice
+        assert ((ys == 0) | (xs == 0) | (ys == H - 1) | (xs == W - 1)).any()
+
+
+def test_augment_nearest_labels_of_a_half_plane():
+    """Labels of a half plane (y >= 20): the nearest source voxel decides,
+    i.e. floor(y + 1/2) >= 20 at the rotated position, away from ties."""
+    D, H, W = 2, 40, 40
+    lab = np.zeros((1, D, H, W), dtype=np.int32)
+    lab[:, :, 20:, :] = 3
+    v = np.zeros((1, D, H, W, 1))
+    theta = 0.4
+    c, s = np.cos(theta), np.sin(theta)
+    _, cl = oaug.sample(v, lab, 0, (0, 10, 8), (2, 18, 22), c, s, 0)
+    i = np.arange(18)[:, None] - 8.5
+    j = np.arange(22)[None, :] - 10.5
+    ys = np.clip(10 + 8.5 + c * i - s * j, 0, H - 1)
+    want = np.where(np.floor(ys + 0.5) >= 20, 3, 0)
+    frac = np.abs((ys + 0.5) - np.round(ys + 0.5))
+    sure = frac > 1e-3
+    assert sure.mean() > 0.95
+    assert np.array_equal(cl[0][sure], want[sure]) and np.array_equal(cl[1][sure], want[sure])
+    assert set(np.unique(cl)) == {0, 3}

@@ -272,6 +272,39 @@ int pyramid_crop(int32_t N, int32_t D, int32_t H, int32_t W, int32_t C, int32_t 
                  int32_t n, int32_t z0, int32_t y0, int32_t x0, int32_t d, int32_t h, int32_t w,
                  const void *x, void *tile, void *stream);
 
+/* Training cubes (Section 3, "Sub-volumes and Augmentation"): cubes cut at
+ * random positions, possibly turned about z by a random angle and flipped
+ * along any axis.  The caller draws the randomness and passes one plstm_cube
+ * per cube (a host array, copied into the launch; at most PLSTM_MAX_CUBES):
+ *   n                 batch element of x;
+ *   (z0, y0, x0)      corner of the unrotated d x h x w box, which must lie
+ *                     inside the volume;
+ *   cos_t, sin_t      cosine and sine of the rotation about z (in [-1, 1]);
+ *   flips             bit set of PLSTM_FLIP_Z / _Y / _X.
+ * Cube voxel (k, i, j), before the flips, reads the source position
+ *   z = z0 + k, y = yc + c u - s v, x = xc + s u + c v,
+ *   u = i - (h - 1) / 2, v = j - (w - 1) / 2, (yc, xc) the box's centre,
+ * computed in fp32 product by product and clamped to the slice; image values
+ * are bilinear in (y, x), labels take the nearest voxel floor(y + 1/2).  The
+ * flips then act on the cube: out[k][i][j] = cube[k'][i'][j'] with
+ * k' = d - 1 - k when z is flipped (likewise y, x).
+ * x [N][D][H][W][C] (dtype), labels [N][D][H][W] int32 or NULL;
+ * out [count][d][h][w][C] (dtype), out_labels [count][d][h][w] (required when
+ * labels is given).  Device buffers, caller-owned; work on `stream`.
+ * Returns PLSTM_EINVAL for null or misaligned pointers, a cube outside the
+ * volume, count outside 1..PLSTM_MAX_CUBES, flips > 7 or |cos|, |sin| > 1. */
+enum { PLSTM_FLIP_Z = 1, PLSTM_FLIP_Y = 2, PLSTM_FLIP_X = 4 };
+#define PLSTM_MAX_CUBES 64
+typedef struct plstm_cube {
+    int32_t n, z0, y0, x0;
+    float cos_t, sin_t;
+    int32_t flips;
+} plstm_cube;
+int pyramid_sample_cubes(int32_t N, int32_t D, int32_t H, int32_t W, int32_t C, int32_t dtype,
+                         int32_t count, const plstm_cube *cubes, int32_t d, int32_t h, int32_t w,
+                         const void *x, const int32_t *labels, void *out, int32_t *out_labels,
+                         void *stream);
+
 /* Gaussian-weighted stitching of per-voxel class probabilities (fp32) into a
  * D x H x W volume with K classes.  acc [D][H][W][K] and wsum [D][H][W] are
  * caller-owned fp32 device buffers:

@@ -26,10 +26,14 @@ __all__ = [
     "pyramid_lstm_set_backward_path", "pyramid_lstm_set_step_split", "pyramid_lstm_set_bf16_mfma",
     "library_path", "load", "plstm2d_shape", "shape2d_for", "pyramid_lstm2d_workspace_size",
     "pyramid_lstm2d_saved_size", "pyramid_lstm2d_forward", "pyramid_lstm2d_backward",
+    "plstm_cube", "PLSTM_FLIP_Z", "PLSTM_FLIP_Y", "PLSTM_FLIP_X", "PLSTM_MAX_CUBES",
+    "pyramid_sample_cubes", "draw_cubes",
 ]
 
 PLSTM_F32 = 0
 PLSTM_BF16 = 1
+PLSTM_FLIP_Z, PLSTM_FLIP_Y, PLSTM_FLIP_X = 1, 2, 4
+PLSTM_MAX_CUBES = 64
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_PKG, "libpyramid_lstm.so")
@@ -52,6 +56,12 @@ class plstm2d_shape(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32),
                 ("C", ctypes.c_int32), ("O", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("K", ctypes.c_int32)]
+
+
+class plstm_cube(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("z0", ctypes.c_int32), ("y0", ctypes.c_int32),
+                ("x0", ctypes.c_int32), ("cos_t", ctypes.c_float), ("sin_t", ctypes.c_float),
+                ("flips", ctypes.c_int32)]
 
 
 class plstm_param_segment(ctypes.Structure):
@@ -115,6 +125,9 @@ def load():
     lib.pyramid_rmsprop_learning_rate.restype = ctypes.c_double
     lib.pyramid_crop.argtypes = [i32] * 13 + [vp, vp, vp]
     lib.pyramid_crop.restype = ctypes.c_int
+    lib.pyramid_sample_cubes.argtypes = [i32] * 7 + [ctypes.POINTER(plstm_cube)] + [i32] * 3 + \
+        [vp] * 5
+    lib.pyramid_sample_cubes.restype = ctypes.c_int
     lib.pyramid_stitch_clear.argtypes = [i32] * 4 + [vp, vp, vp]
     lib.pyramid_stitch_clear.restype = ctypes.c_int
     lib.pyramid_stitch_add.argtypes = [i32] * 10 + [f32, vp, vp, vp, vp]
@@ -359,6 +372,52 @@ def pyramid_crop(x, n, box, tile, stream=None):
         raise ValueError("tile must be [d][h][w][C] of x's dtype")
     _check("pyramid_crop", load().pyramid_crop(N, D, H, W, C, _DT[x.dtype], n, *box, _ptr(x),
                                                _ptr(tile), _stream(stream)))
+
+
+def pyramid_sample_cubes(x, cubes, size, out, labels=None, out_labels=None, stream=None):
+    """Training cubes out [count][d][h][w][C] (and out_labels [count][d][h][w])
+    from x [N][D][H][W][C] (labels [N][D][H][W] int32); `cubes` is a sequence
+    of plstm_cube (at most PLSTM_MAX_CUBES), `size` = (d, h, w)."""
+    N, D, H, W, C = x.shape
+    d, h, w = size
+    count = len(cubes)
+    if count < 1 or count > PLSTM_MAX_CUBES:
+        raise ValueError("between 1 and %d cubes per call" % PLSTM_MAX_CUBES)
+    if out.dtype != x.dtype or tuple(out.shape) != (count, d, h, w, C):
+        raise ValueError("out must be [count][d][h][w][C] of x's dtype")
+    if labels is not None:
+        if labels.dtype != torch.int32 or out_labels is None or out_labels.dtype != torch.int32:
+            raise ValueError("labels and out_labels must be int32")
+        if tuple(out_labels.shape) != (count, d, h, w) or tuple(labels.shape) != (N, D, H, W):
+            raise ValueError("labels [N][D][H][W], out_labels [count][d][h][w]")
+    arr = (plstm_cube * count)(*cubes)
+    _check("pyramid_sample_cubes", load().pyramid_sample_cubes(
+        N, D, H, W, C, _DT[x.dtype], count, arr, d, h, w, _ptr(x), _ptr(labels), _ptr(out),
+        _ptr(out_labels), _stream(stream)))
+
+
+def draw_cubes(rng, N, volume, size, count, rotate=True, flip_axes="zyx"):
+    """Random training cubes (host side): a uniform batch element and corner
+    among the boxes of `size` = (d, h, w) inside `volume` = (D, H, W); with
+    `rotate` an angle uniform in [0, 2 pi) about z; each axis named in
+    `flip_axes` flipped with probability 1/2.  The EM recipe is the default;
+    the MR recipe is rotate=False, flip_axes="x".  `rng` is a
+    numpy.random.Generator."""
+    import math
+    D, H, W = volume
+    d, h, w = size
+    bits = {"z": PLSTM_FLIP_Z, "y": PLSTM_FLIP_Y, "x": PLSTM_FLIP_X}
+    out = []
+    for _ in range(count):
+        n = int(rng.integers(0, N))
+        z0, y0, x0 = (int(rng.integers(0, E - e + 1)) for E, e in ((D, d), (H, h), (W, w)))
+        theta = float(rng.uniform(0.0, 2.0 * math.pi)) if rotate else 0.0
+        flips = 0
+        for a in flip_axes:
+            if rng.random() < 0.5:
+                flips |= bits[a]
+        out.append(plstm_cube(n, z0, y0, x0, math.cos(theta), math.sin(theta), flips))
+    return out
 
 
 def pyramid_stitch_clear(acc, wsum, stream=None):

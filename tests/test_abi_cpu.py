@@ -277,3 +277,51 @@ def test_2d_sizes_and_validation(lib):
     assert bw(dwx=None) == -1
     assert bw(shape2d(dtype=P.PLSTM_BF16), nbytes=1 << 40) == -2
     assert bw(nbytes=16) == -3
+
+
+def test_sample_cubes_validation(lib):
+    def call(N=1, D=8, H=10, W=12, C=2, dtype=P.PLSTM_F32, cubes=None, size=(4, 5, 6), x=FAKE,
+             labels=None, out=FAKE, out_labels=None):
+        if cubes is None:
+            cubes = [P.plstm_cube(0, 0, 0, 0, 1.0, 0.0, 0)]
+        arr = (P.plstm_cube * len(cubes))(*cubes)
+        return lib.pyramid_sample_cubes(N, D, H, W, C, dtype, len(cubes), arr, *size, x, labels,
+                                        out, out_labels, None)
+    cube = P.plstm_cube
+    assert call(x=None) == -1
+    assert call(out=None) == -1
+    assert call(labels=FAKE) == -1                                    # labels without out_labels
+    assert call(cubes=[cube(1, 0, 0, 0, 1.0, 0.0, 0)]) == -1         # n out of range
+    assert call(cubes=[cube(0, 5, 0, 0, 1.0, 0.0, 0)]) == -1         # z0 + d > D
+    assert call(cubes=[cube(0, 0, 6, 0, 1.0, 0.0, 0)]) == -1
+    assert call(cubes=[cube(0, 0, 0, 7, 1.0, 0.0, 0)]) == -1
+    assert call(cubes=[cube(0, 0, 0, -1, 1.0, 0.0, 0)]) == -1
+    assert call(cubes=[cube(0, 0, 0, 0, 1.0, 0.0, 8)]) == -1         # flips > 7
+    assert call(cubes=[cube(0, 0, 0, 0, 1.5, 0.0, 0)]) == -1         # |cos| > 1
+    assert call(cubes=[cube(0, 0, 0, 0, float("nan"), 0.0, 0)]) == -1
+    assert call(cubes=[cube(0, 0, 0, 0, 1.0, 0.0, 0)] * 65) == -1    # more than the maximum
+    assert call(size=(9, 5, 6)) == -1
+    assert call(dtype=2) == -1
+    assert call(x=ctypes.c_void_p(0x10002)) == -1
+    assert lib.pyramid_sample_cubes(1, 8, 10, 12, 2, 0, 0, None, 4, 5, 6, FAKE, None, FAKE, None,
+                                    None) == -1
+
+
+def test_draw_cubes_recipes():
+    """Host-side draws: boxes inside the volume, EM recipe (any angle, flips
+    on z, y, x each about half the time), MR recipe (no rotation, x only)."""
+    import numpy as np
+    rng = np.random.default_rng(5)
+    em = P.draw_cubes(rng, 2, (30, 512, 512), (15, 128, 128), 2000)
+    for c in em:
+        assert 0 <= c.n < 2 and 0 <= c.z0 <= 15 and 0 <= c.y0 <= 384 and 0 <= c.x0 <= 384
+        assert abs(c.cos_t ** 2 + c.sin_t ** 2 - 1) < 1e-6
+    for bit in (P.PLSTM_FLIP_Z, P.PLSTM_FLIP_Y, P.PLSTM_FLIP_X):
+        frac = np.mean([(c.flips & bit) != 0 for c in em])
+        assert 0.45 < frac < 0.55
+    ang = np.arctan2([c.sin_t for c in em], [c.cos_t for c in em])
+    assert np.histogram(ang, bins=4, range=(-np.pi, np.pi))[0].min() > 400
+    mr = P.draw_cubes(rng, 5, (48, 240, 240), (25, 240, 240), 500, rotate=False, flip_axes="x")
+    assert all(c.cos_t == 1.0 and c.sin_t == 0.0 and c.flips in (0, P.PLSTM_FLIP_X) for c in mr)
+    assert all(c.y0 == 0 and c.x0 == 0 and 0 <= c.z0 <= 23 for c in mr)
+    assert 0.4 < np.mean([c.flips != 0 for c in mr]) < 0.6

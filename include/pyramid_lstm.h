@@ -339,8 +339,9 @@ int pyramid_lstm_set_forward_path(int path);
 /* Backward implementation selection, for testing and tuning (process-wide):
  * 0 = automatic (default): persistent MFMA reverse sweep, else plane-step
  * MFMA path, else generic (same shape rules as the forward); 1 = generic
- * per-plane path only; 2 = same as 0; 3 = the plane-step MFMA path where it
- * supports the shape, else the generic path.  Returns PLSTM_EINVAL for
+ * per-plane path only; 2 = as 0, but the persistent reverse sweep stages
+ * every strip chunk by chunk (no strip kept whole in LDS); 3 = the
+ * plane-step MFMA path where it supports the shape, else the generic path.  Returns PLSTM_EINVAL for
  * other values. */
 int pyramid_lstm_set_backward_path(int path);
 

@@ -75,7 +75,7 @@ int backward_dispatch(const Geom &g, const float *x, const float *wx, const floa
 {
     const int path = g_backward_path;
     if (path != 1 && path != 3 && sweep_bwd_supported(g)) {
-        const int rc = sweep_bwd(g, x, wx, wh, sv, dh, dx, dwx, dwh, db, ws, st);
+        const int rc = sweep_bwd(g, x, wx, wh, sv, dh, dx, dwx, dwh, db, ws, st, path != 2);
         if (rc != PLSTM_ENOTCORESIDENT && rc != PLSTM_EUNSUPPORTED) return rc;
     }
     if (path != 1 && step_supported(g))

@@ -46,6 +46,7 @@ struct StripCostModel {
     bool allow_resident = false;
     size_t res_px_bytes = 0, res_own_bytes = 0, res_fixed_bytes = 0;
     int res_max_staged = 0;   // most staged elements the kernel supports
+    long long res_max_own = 0;   // most strip pixels the kernel supports (0: no limit)
     double c_res_step = 0.0;
 };
 
@@ -73,7 +74,8 @@ inline StripShape strip_shape(const DirGeom &r, int k, const StripCostModel &m, 
         const long long staged = (long long)(r.P + 2) * (sh.w + 2);
         const size_t lds = m.fixed_bytes + m.res_fixed_bytes + (size_t)staged * m.res_px_bytes +
                            (size_t)r.P * sh.w * m.res_own_bytes;
-        if (lds <= lds_limit && staged <= m.res_max_staged) {
+        if (lds <= lds_limit && staged <= m.res_max_staged &&
+            (m.res_max_own == 0 || (long long)r.P * sh.w <= m.res_max_own)) {
             sh.rows = r.P;
             sh.chunks = 1;
             sh.resident = true;

@@ -18,7 +18,7 @@ bool sweep_bwd_supported(const Geom &g);
 size_t sweep_bwd_ws(const Geom &g);
 int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, const Saved &sv,
               const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
-              hipStream_t st);
+              hipStream_t st, bool allow_resident);
 
 // Plane-step MFMA path (sweep_step.hip): O = 16, 32, 64, C <= 64, fp32
 // arithmetic (bf16 storage converted on entry), one launch per plane step.

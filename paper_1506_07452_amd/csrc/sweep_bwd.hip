@@ -59,6 +59,7 @@ struct BwdArgs {
     float *gcf;                  // [6][N][V][16] dL/dc_t * f_t, carried to plane t - 1
     int *flags, *err;
     int nstrip[kDirs], first[kDirs], chunk_rows[kDirs], max_w[kDirs];
+    int resident[kDirs];         // 1: the strip's dA stays in LDS for the sweep
 };
 
 // Epilogue operands of one tile (this lane's pixel, units 4 q4 .. 4 q4 + 3).
@@ -125,6 +126,199 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
         return (pc == q0 - 1) | (pc == q1) | ((pc == q0) & (nb_lo >= 0)) |
                ((pc == q1 - 1) & (nb_hi >= 0));
     };
+
+    if (a.resident[d]) {
+        // ============ resident strip: dA of the whole strip stays in LDS ============
+        // dA_t overwrites dA_{t+1} in place: each wave keeps its tiles' dA in
+        // registers until every wave's contraction has read dA_{t+1} (one
+        // barrier), then writes them.  Only the two halo columns come from
+        // the neighbours each step.  Pixels are numbered column by column
+        // (LDS pixel (column + 1) (P + 2) + row + 1); the tiles touching a
+        // column next to a neighbour strip run first and the step is
+        // published as soon as they are stored.  At most two tiles per wave
+        // (checked on the host).
+        const int P = dg.P, P2 = P + 2;
+        const int npl = P2 * W2;
+        const int npx = P * TQ;
+        const int nmt = (npx + 15) >> 4;
+        int *order = (int *)(as + (size_t)npl * kG);   // tile order, edge tiles first
+        int *cnt = order + nmt;                         // edge tiles stored this step
+        const float inv_p = 1.0f / (float)P;
+        for (int e = threadIdx.x; e < npl * (kG / 4); e += kThreads)
+            *(f4 *)&as[e * 4] = f4{0.0f, 0.0f, 0.0f, 0.0f};   // dA_T = 0, halo rows
+        if (threadIdx.x == 0) {
+            int k = 0, ne = 0;
+            for (int pass = 0; pass < 2; ++pass)
+                for (int mt = 0; mt < nmt; ++mt) {
+                    const int c0 = (mt * 16) / P, c1 = min(mt * 16 + 15, npx - 1) / P;
+                    const bool edge = (c0 == 0 && nb_lo >= 0) || (c1 == TQ - 1 && nb_hi >= 0);
+                    if (edge == (pass == 0)) order[k++] = mt;
+                    ne += (pass == 0 && edge) ? 1 : 0;
+                }
+            cnt[0] = 0;
+            cnt[1] = ne;
+        }
+        __syncthreads();
+        const int n_edge = cnt[1];
+        for (int r = 0; r < dg.T; ++r) {
+            const int t = dg.T - 1 - r;
+            const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+            const bool has_next = t + 1 < dg.T, has_prev = t > 0;
+            const int splane = s * ss;
+            const int nplane = has_next ? (s + dg.sign) * ss : splane;
+            const int pplane = has_prev ? (s - dg.sign) * ss : splane;
+            if (r > 0) {
+                // ---- the neighbours' edge columns of dA_{t+1} -> halo columns
+                const int nb = threadIdx.x == 0 ? nb_lo : (threadIdx.x == 1 ? nb_hi : -1);
+                if (nb >= 0) {
+                    int spins = 0;
+                    while (__hip_atomic_load(&a.flags[nb], __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT) < r) {
+                        __builtin_amdgcn_s_sleep(1);
+                        if (++spins > kMaxSpin) {
+                            __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                            break;
+                        }
+                        if ((spins & 1023) == 0 &&
+                            __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+                            break;
+                    }
+                }
+                __syncthreads();
+                // One instruction moves four consecutive rows of a halo
+                // column (lane l: chunk position l%16 of row 4 j + l/16);
+                // lanes past the last row are inactive, so the halo rows
+                // above and below the plane keep their zeros.
+                const int nslot = (P + 3) >> 2;
+                for (int i = wave; i < 2 * nslot; i += kWaves) {
+                    const int side = i >= nslot ? 1 : 0;
+                    const int j = i - side * nslot;
+                    if ((side ? nb_hi : nb_lo) < 0) continue;
+                    const int row = 4 * j + (lane >> 4);
+                    const int lcol = side ? TQ + 1 : 0;
+                    const int pix = lcol * P2 + 1 + row;
+                    const int pc = side ? q1 : q0 - 1;
+                    const int boff =
+                        ((nplane + row * sp + pc * sq) * kG + (col ^ (pix & 15)) * 4) *
+                        (int)sizeof(float);
+                    lds_void *dst = (lds_void *)&as[(size_t)(lcol * P2 + 1 + 4 * j) * kG];
+                    if (row < P)
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(dA_rs, dst, 16, boff, 0, 0,
+                                                                 kCachePolicySC1);
+                }
+                __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+                __syncthreads();
+            }
+            f4 hold[2][4];
+            int hbase[2];
+#pragma unroll
+            for (int it = 0; it < 2; ++it) {
+                const int k = wave + it * kWaves;
+                hbase[it] = -1;
+                if (k < nmt) {
+                    const int mt = order[k];
+                    const int pa = min(mt * 16 + col, npx - 1);
+                    const int ca = fdiv_floor(pa, inv_p), ra = pa - ca * P;
+                    const int base = (ca + 1) * P2 + ra + 1;
+                    const int vo = splane + ra * sp + (ca + q0) * sq;
+                    const bool shared = is_shared_col(ca + q0);
+                    BwdEpi e;
+                    const int von = vo - splane + nplane, vop = vo - splane + pplane;
+                    e.dh = *(const f4 *)&dh_n[vo * kO + 4 * q4];
+                    e.gi = *(const f4 *)&gates_dn[vo * kG + 0 * kO + 4 * q4];
+                    e.gf = *(const f4 *)&gates_dn[vo * kG + 1 * kO + 4 * q4];
+                    e.gg = *(const f4 *)&gates_dn[vo * kG + 2 * kO + 4 * q4];
+                    e.go = *(const f4 *)&gates_dn[vo * kG + 3 * kO + 4 * q4];
+                    e.c = *(const f4 *)&cell_dn[vo * kO + 4 * q4];
+                    e.gcfn = *(const f4 *)&gcf_dn[von * kO + 4 * q4];
+                    e.cp = *(const f4 *)&cell_dn[vop * kO + 4 * q4];
+                    __builtin_amdgcn_sched_barrier(0);
+                    f4 acc[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) acc[q] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                    for (int tap = 0; tap < 9; ++tap) {
+                        // h_t at pixel p fed A_{t+1} at p - (tap offset); rows
+                        // are consecutive LDS pixels, columns P + 2 apart
+                        const int pp = base - ((tap / 3 - 1) + (tap % 3 - 1) * P2);
+                        f4 bv[4], av[4];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            bv[q] = *(const f4 *)&as[pp * kG + 4 * swz(4 * q4 + q, pp)];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            av[q] = *(const f4 *)&was[((tap * 4 + q) * 64 + lane) * 4];
+#pragma unroll
+                        for (int s2 = 0; s2 < 16; ++s2)
+                            acc[s2 & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                av[s2 >> 2][s2 & 3], bv[s2 >> 2][s2 & 3], acc[s2 & 3], 0, 0, 0);
+                    }
+                    f4 dAi, dAf, dAg, dAo, gcf;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float gh = acc[0][i] + acc[1][i] + acc[2][i] + acc[3][i] + e.dh[i];
+                        const float tc = ftanh(e.c[i]);
+                        const float gcs = gh * e.go[i] * (1.0f - tc * tc) +
+                                          (has_next ? e.gcfn[i] : 0.0f);
+                        const float cprev = has_prev ? e.cp[i] : 0.0f;
+                        gcf[i] = gcs * e.gf[i];
+                        dAi[i] = gcs * e.gg[i] * e.gi[i] * (1.0f - e.gi[i]);
+                        dAf[i] = gcs * cprev * e.gf[i] * (1.0f - e.gf[i]);
+                        dAg[i] = gcs * e.gi[i] * (1.0f - e.gg[i] * e.gg[i]);
+                        dAo[i] = gh * tc * e.go[i] * (1.0f - e.go[i]);
+                    }
+                    const int o4 = vo * kG + 4 * q4;
+                    if (shared) {
+                        store_coherent(dA_rs, o4 + 0 * kO, dAi);
+                        store_coherent(dA_rs, o4 + 1 * kO, dAf);
+                        store_coherent(dA_rs, o4 + 2 * kO, dAg);
+                        store_coherent(dA_rs, o4 + 3 * kO, dAo);
+                    } else {
+                        float *dst = &dA_dn[o4];
+                        *(f4 *)&dst[0 * kO] = dAi;
+                        *(f4 *)&dst[1 * kO] = dAf;
+                        *(f4 *)&dst[2 * kO] = dAg;
+                        *(f4 *)&dst[3 * kO] = dAo;
+                    }
+                    *(f4 *)&gcf_dn[vo * kO + 4 * q4] = gcf;
+                    hold[it][0] = dAi;
+                    hold[it][1] = dAf;
+                    hold[it][2] = dAg;
+                    hold[it][3] = dAo;
+                    hbase[it] = base;
+                    if (k < n_edge) {
+                        // this edge tile's coherent stores have completed:
+                        // count it; the wave that counts the last publishes
+                        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+                        if (lane == 0 && atomicAdd(cnt, 1) == n_edge - 1)
+                            __hip_atomic_store(&a.flags[blockIdx.x], r + 1, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                }
+            }
+            // every contraction has read dA_{t+1}: overwrite it with dA_t
+            __syncthreads();
+#pragma unroll
+            for (int it = 0; it < 2; ++it) {
+                if (hbase[it] >= 0) {
+                    const int pb = hbase[it];
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        *(f4 *)&as[pb * kG + 4 * swz(4 * g + q4, pb)] = hold[it][g];
+                }
+            }
+            if (threadIdx.x == 0) {
+                if (n_edge == 0)
+                    __hip_atomic_store(&a.flags[blockIdx.x], r + 1, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                cnt[0] = 0;
+            }
+            // the next step's first barrier orders these LDS writes before
+            // its contractions
+        }
+        return;
+    }
 
     for (int r = 0; r < dg.T; ++r) {
         const int t = dg.T - 1 - r;                   // plane processed at this step
@@ -544,7 +738,7 @@ __global__ void k_fill_zero(int *p, int n)
     if (i < n) p[i] = 0;
 }
 
-StripCostModel bwd_model()
+StripCostModel bwd_model(bool allow_resident)
 {
     StripCostModel m;
     m.fixed_bytes = kWaFloats * sizeof(float);
@@ -553,6 +747,13 @@ StripCostModel bwd_model()
     m.c_tile = 2.9;
     m.c_stage0 = 1.0;
     m.c_stage_px = 0.008;
+    m.allow_resident = allow_resident;
+    m.res_px_bytes = kG * sizeof(float);          // dA_{t+1} / dA_t, in place
+    m.res_own_bytes = 1;                          // tile order (4 bytes per 16 pixels)
+    m.res_fixed_bytes = 16 * sizeof(int);         // counters
+    m.res_max_staged = 1 << 30;
+    m.res_max_own = 2 * kWaves * 16;              // two tiles per wave
+    m.c_res_step = 2.0;
     return m;
 }
 
@@ -598,16 +799,20 @@ size_t sweep_bwd_ws(const Geom &g)
 
 int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, const Saved &sv,
               const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
-              hipStream_t st)
+              hipStream_t st, bool allow_resident)
 {
     const DevInfo di = device_info();
     if (di.cus <= 0) return PLSTM_EHIP;
     const size_t lds_limit = (size_t)(di.max_lds > 0 ? di.max_lds : 65536) - 1024;
     const int budget = di.cus < 1024 ? di.cus : 1024;
-    const Plan pl = make_plan(g, budget, bwd_model(), lds_limit);
+    const Plan pl = make_plan(g, budget, bwd_model(allow_resident), lds_limit);
     if (pl.blocks > budget) return PLSTM_EUNSUPPORTED;
-    for (int d = 0; d < kDirs; ++d)
+    for (int d = 0; d < kDirs; ++d) {
         if (pl.chunk_rows[d] < 1) return PLSTM_EUNSUPPORTED;
+        // a resident strip: at most two 16-pixel tiles per wave
+        if (pl.resident[d] && (long long)g.dir[d].P * pl.max_w[d] > 2 * kWaves * 16)
+            return PLSTM_EUNSUPPORTED;
+    }
 
     Carve cv(ws);
     float *dA = cv.take<float>((size_t)kDirs * g.N * g.V * kG);
@@ -628,6 +833,7 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
         args.first[d] = pl.first[d];
         args.chunk_rows[d] = pl.chunk_rows[d];
         args.max_w[d] = pl.max_w[d];
+        args.resident[d] = pl.resident[d];
     }
     int per_cu = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_bwd, kThreads, pl.lds) !=

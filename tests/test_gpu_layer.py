@@ -313,6 +313,33 @@ def test_filter_size_bf16(bf16_mfma):
     assert normwise(host(h), ref) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("shape", O16_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("bwd_path", [0, 2], ids=["resident", "chunked"])
+def test_reverse_sweep_strip_kinds_match_oracle(shape, bwd_path):
+    """The persistent reverse sweep with strips kept whole in LDS where they
+    fit (default) and with every strip staged chunk by chunk: same gradients
+    as the oracle."""
+    inst = instance(shape, 1400 + sum(shape))
+    L = inst.layers[0]
+    dh = synth.upstream_grad(inst.x.shape[:-1] + (shape[-1],), 19 + sum(shape))
+    ref = oracle.backward(inst.x, L.wx, L.wh, L.b, dh)
+    say("reverse sweep", shape, bwd_path)
+    x, Ld = dev(inst.x), layer_dev(L)
+    h, saved = layer_forward(x, Ld, training=True)
+    P.pyramid_lstm_set_backward_path(bwd_path)
+    P.pyramid_lstm_timing_enable(True)
+    try:
+        grads = layer_backward(x, Ld, saved, dev(dh))
+        phases = P.pyramid_lstm_timing_read()
+        torch.cuda.synchronize()
+    finally:
+        P.pyramid_lstm_timing_enable(False)
+        P.pyramid_lstm_set_backward_path(0)
+    assert "sweep_bwd_mfma" in phases, phases
+    for name, got in zip(("dx", "dwx", "dwh", "db"), grads):
+        assert normwise(host(got), ref[name]) <= TOL["f32"], name
+
+
 def test_mfma_backward_runs_for_o16():
     """The persistent MFMA reverse sweep and MFMA parameter gradients are the
     path taken for 16 hidden units."""

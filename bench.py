@@ -19,6 +19,8 @@ Two more workloads can be timed instead (not the headline; no CPU baseline):
                               + softmax, bf16 storage, forward
     --workload train-2layer   48 x 240 x 240 x 3, two layers (16, 32) + FC tanh
                               + softmax cross-entropy, fp32, forward + backward
+    --workload em-layer       30 x 512 x 512 x 1 EM-like stack, one layer (16),
+                              fp32, forward (inference)
     --workload paper-net      the network of the paper's experiments (7x7
                               filters, 16 / FC 25 / 32 / FC 45 / 64 -> output)
                               on a 25 x 240 x 240 x 5 MR sub-volume, softmax
@@ -225,6 +227,48 @@ def bench_network(args, cfg):
     print(json.dumps(out), flush=True)
 
 
+def bench_em(args):
+    """The EM-like stack (ISBI 2012 shape) through one layer, inference
+    forward: six sweeps and their sum."""
+    import torch
+    import synth
+    import paper_1506_07452_amd as P
+    from paper_1506_07452_amd.network import LayerW, layer_forward, workspace_for
+    inst = synth.config(3)
+    wl = inst.wl
+    torch.cuda.init()
+    x = torch.from_numpy(inst.x).to("cuda:0").contiguous()
+    L = inst.layers[0]
+    Ld = LayerW(*(torch.from_numpy(a).to("cuda:0").contiguous() for a in (L.wx, L.wh, L.b)))
+    ws = workspace_for(x.shape, wl.hidden, False, torch.float32, False, "cuda:0")
+    for _ in range(args.warmup):
+        layer_forward(x, Ld, False, ws=ws)
+    torch.cuda.synchronize()
+    P.pyramid_lstm_timing_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        layer_forward(x, Ld, False, ws=ws)
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / args.steps
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    N, D, H, W, C = inst.x.shape
+    O = wl.hidden[0]
+    V = N * D * H * W
+    name = next(k for k in phases if k.startswith("sweep_fwd"))
+    out = {
+        "metric": METRIC, "value": 6 * V / t, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": t * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "N": N, "D": D, "H": H, "W": W, "C": C, "O": O},
+        "tflops": 6 * V * 2 * 9 * 4 * O * (C + O) / t / 1e12,
+        "roofline": roofline(phases, name, args.steps, V, C, O, mode="inference"),
+        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
+    }
+    out["roofline"]["traffic"] = None     # the committed counters cover the MR volume only
+    print(json.dumps(out), flush=True)
+
+
 def cpu_baseline(inst_cfg, crop):
     """The fp64 oracle (as is) on a bounded crop of the same workload."""
     import numpy as np
@@ -253,7 +297,8 @@ def main():
     ap.add_argument("--separate-head", action="store_true",
                     help="run the FC / softmax head as separate kernels instead of the fused one")
     ap.add_argument("--workload", default="mr-layer",
-                    choices=["mr-layer", "stacked-bf16", "train-2layer", "paper-net"],
+                    choices=["mr-layer", "em-layer", "stacked-bf16", "train-2layer",
+                             "paper-net"],
                     help="mr-layer: the headline single-layer MR workload (default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device three times (a plain copy kernel "
@@ -264,6 +309,9 @@ def main():
               "on a single MI355X and this build has no multi-GPU path (--gpus 1).",
               file=sys.stderr)
         sys.exit(2)
+    if args.workload == "em-layer":
+        bench_em(args)
+        return
     if args.workload != "mr-layer":
         bench_network(args, {"stacked-bf16": 4, "train-2layer": 5, "paper-net": None}[
             args.workload])

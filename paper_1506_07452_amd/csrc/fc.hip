@@ -951,6 +951,98 @@ static int fc_tanh_backward_impl(long long M, int Cin, int Cout, const float *x,
     return fc_wgrad(M, Cin, Cout, rg, x, dw, db, partial, st);
 }
 
+// Softmax head, one thread per row read straight from global memory in
+// four-element vectors (Cin a multiple of 4), the weights in LDS (every lane
+// reads the same address: broadcast).  Logits stay in registers (K <= 16) and
+// the label's probability is picked by comparison, as in the row-tile kernel.
+template <typename TS, bool SQ>
+__global__ void __launch_bounds__(kThreads)
+k_softmax_vec(long long M, int Cin, int K, const TS *__restrict__ x, const TS *__restrict__ w,
+              const TS *__restrict__ b, const int32_t *__restrict__ labels,
+              float *__restrict__ p, float *__restrict__ dlogits, float *__restrict__ lossp)
+{
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    extern __shared__ float lds[];
+    float *sw = lds;                               // [K][Cin]
+    for (int e = threadIdx.x; e < K * Cin; e += kThreads) sw[e] = Store<TS>::load(w, e);
+    __syncthreads();
+    const long long m = (long long)blockIdx.x * kThreads + threadIdx.x;
+    float l = 0.0f;
+    if (m < M) {
+        float z[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) z[k] = k < K ? Store<TS>::load(b, k) : 0.0f;
+        const TS *xr = x + m * Cin;
+        for (int c = 0; c < Cin; c += 4) {
+            const f4v xv = Vec4<TS>::load(xr + c);
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                if (k < K) {
+                    const f4v wv = *(const f4v *)&sw[k * Cin + c];
+                    z[k] += (xv[0] * wv[0] + xv[1] * wv[1]) + (xv[2] * wv[2] + xv[3] * wv[3]);
+                }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (k < K) mx = fmaxf(mx, z[k]);
+        float sum = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            z[k] = k < K ? __expf(z[k] - mx) : 0.0f;
+            sum += z[k];
+        }
+        const float inv = 1.0f / sum;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (k < K) p[m * K + k] = z[k] * inv;
+        if (labels) {
+            // An out-of-range label poisons the loss and the gradient with NaN.
+            const int lab = labels[m];
+            const bool ok = lab >= 0 && lab < K;
+            if (SQ) {
+                float e = 0.0f, sd = 0.0f;
+#pragma unroll
+                for (int k = 0; k < 16; ++k) {
+                    if (k < K) {
+                        const float pk = z[k] * inv, dk = pk - (k == lab ? 1.0f : 0.0f);
+                        e += dk * dk;
+                        sd += pk * dk;
+                    }
+                }
+                l = ok ? e : NAN;
+#pragma unroll
+                for (int k = 0; k < 16; ++k)
+                    if (k < K) {
+                        const float pk = z[k] * inv, dk = pk - (k == lab ? 1.0f : 0.0f);
+                        dlogits[m * K + k] = ok ? 2.0f * pk * (dk - sd) / (float)M : NAN;
+                    }
+            } else {
+                float pl = 0.0f;
+#pragma unroll
+                for (int k = 0; k < 16; ++k)
+                    if (k == lab) pl = z[k] * inv;
+                l = ok ? -logf(pl) : NAN;
+#pragma unroll
+                for (int k = 0; k < 16; ++k)
+                    if (k < K)
+                        dlogits[m * K + k] =
+                            ok ? (z[k] * inv - (k == lab ? 1.0f : 0.0f)) / (float)M : NAN;
+            }
+        }
+    }
+    if (labels) {
+        __shared__ float red[kThreads];
+        red[threadIdx.x] = l;
+        __syncthreads();
+        for (int off = kThreads / 2; off > 0; off >>= 1) {
+            if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) lossp[blockIdx.x] = red[0];
+    }
+}
+
 template <bool SQ>
 static int softmax_loss_impl(long long M, int Cin, int K, int dtype, const void *x,
                              const void *w, const void *b, const int32_t *labels, float *p,
@@ -962,7 +1054,17 @@ static int softmax_loss_impl(long long M, int Cin, int K, int dtype, const void 
     float *dlogits = cv.take<float>((size_t)M * K);
     float *lossp = cv.take<float>((size_t)(M + kRB - 1) / kRB);
     unsigned nb = blocks_for(M);
-    if (rows_ok(Cin)) {
+    if (Cin % 4 == 0 && (size_t)K * Cin * sizeof(float) <= 65536) {
+        const size_t lds = (size_t)K * Cin * sizeof(float);
+        if (dtype == PLSTM_BF16)
+            k_softmax_vec<uint16_t, SQ><<<nb, kThreads, lds, st>>>(
+                M, Cin, K, (const uint16_t *)x, (const uint16_t *)w, (const uint16_t *)b, labels,
+                p, dlogits, lossp);
+        else
+            k_softmax_vec<float, SQ><<<nb, kThreads, lds, st>>>(
+                M, Cin, K, (const float *)x, (const float *)w, (const float *)b, labels, p,
+                dlogits, lossp);
+    } else if (rows_ok(Cin)) {
         nb = (unsigned)((M + kRB - 1) / kRB);
         const size_t lds = rows_lds(Cin, 16, K * (Cin + 1));
         if (dtype == PLSTM_BF16)

@@ -104,10 +104,15 @@ def test_paper_network_forward_bf16():
     assert normwise(host(out["p"]), ref) <= TOL["bf16"]
 
 
-@pytest.mark.parametrize("cin", [16, 200], ids=["rows", "wide"])
+# input widths of the three softmax kernels: a multiple of 4 (rows read as
+# vectors), other widths up to 128 (rows staged in LDS), wider ones
+SOFTMAX_CIN = [(16, "vec"), (128, "vec128"), (200, "vec200"), (18, "rows"), (203, "wide")]
+
+
+@pytest.mark.parametrize("cin", [c for c, _ in SOFTMAX_CIN], ids=[n for _, n in SOFTMAX_CIN])
 def test_softmax_squared_loss_matches_oracle(cin):
     """The squared loss of Eq. (14) on the softmax output, and its gradient,
-    on both softmax kernels (rows staged in LDS, and the wide-input one)."""
+    on every softmax kernel."""
     import oracle.loss as oloss
     import paper_1506_07452_amd as P
     rng = np.random.default_rng(93 + cin)
@@ -413,3 +418,40 @@ def test_config5_training_step():
     for k, t in named.items():
         err = normwise(host(t), gold[k])
         assert err <= TOL["f32"], (k, err)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cin", [c for c, _ in SOFTMAX_CIN], ids=[n for _, n in SOFTMAX_CIN])
+def test_softmax_ce_kernels_match_oracle(cin, dtype):
+    """Linear + softmax + mean cross-entropy and its gradients on every
+    softmax kernel, fp32 and bf16 inputs; the forward alone (no labels) gives
+    the same probabilities."""
+    import paper_1506_07452_amd as P
+    rng = np.random.default_rng(97 + cin)
+    M, K = 1531, 4
+    xa = synth.to_storage(rng.standard_normal((M, cin)), dtype)
+    w = synth.to_storage(rng.uniform(-0.3, 0.3, (K, cin)), dtype)
+    b = synth.to_storage(rng.uniform(-0.3, 0.3, K), dtype)
+    lab = rng.integers(0, K, M).astype(np.int32)
+    say("softmax ce", cin, dtype)
+    xd, wd, bd = dev(xa, dtype), dev(w, dtype), dev(b, dtype)
+    p = torch.empty(M, K, device=DEV)
+    p_inf = torch.empty(M, K, device=DEV)
+    loss = torch.empty(1, device=DEV)
+    # gradients take fp32 inputs only; bf16 gives probabilities and the loss
+    grads = dtype == "f32"
+    dw = torch.empty(K, cin, device=DEV) if grads else None
+    db = torch.empty(K, device=DEV) if grads else None
+    dx = torch.empty(M, cin, device=DEV) if grads else None
+    P.pyramid_softmax_ce(xd, wd, bd, p, torch.from_numpy(lab).to(DEV), loss, dx, dw, db)
+    P.pyramid_softmax_ce(xd, wd, bd, p_inf)
+    torch.cuda.synchronize()
+    ref = oracle.softmax_ce(xa, w, b, lab, grad=True)
+    tol = TOL[dtype] if dtype == "bf16" else TOL["f32"]
+    assert normwise(host(p), ref["p"]) <= tol
+    assert torch.equal(p, p_inf)
+    assert abs(loss.item() - ref["loss"]) <= TOL["f32"] * ref["loss"]
+    pairs = [(dw, ref["dw"]), (db, ref["db"]), (dx, ref["dx"])] if grads else []
+    for got, want in pairs:
+        assert normwise(host(got), want) <= TOL["f32"]
+

@@ -120,10 +120,11 @@ def roofline(phases, name, passes, V, C, O, mode="training"):
 
 def layer_path(C, O, dtype, K=3):
     """Which forward kernels the library runs for a layer: the persistent
-    sweeps (fp32, 16 hidden units, at most 4 input channels, 3x3), the
-    plane-step bf16 MFMA (bf16 storage, 32 or 64 hidden units) or the
-    plane-step fp32 MFMA; phase names end in _mfma, _step_bf16 or _step."""
-    if dtype == "f32" and O == 16 and C <= 4 and K == 3:
+    sweeps (16 hidden units, at most 4 input channels, 3x3; bf16 storage is
+    widened to fp32 first), the plane-step bf16 MFMA (bf16 storage, 32 or 64
+    hidden units) or the plane-step fp32 MFMA; phase names end in _mfma,
+    _step_bf16 or _step."""
+    if O == 16 and C <= 4 and K == 3:
         return "mfma"
     return "step_bf16" if dtype == "bf16" and O in (32, 64) else "step"
 

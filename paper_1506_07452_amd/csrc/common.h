@@ -166,6 +166,9 @@ size_t generic_backward_ws(const Geom &g);
 // dL/dx from the gate gradients dA [6][N][V][4O] of every direction.
 int generic_dx(const Geom &g, const float *wx, const float *dA, float *dx, hipStream_t st);
 
+// dst[i] = src[i] for n bf16 values widened to fp32.
+int bf16_to_f32(const void *src, float *dst, long long n, hipStream_t st);
+
 // Fully connected glue.
 int fc_tanh_forward(long long M, int Cin, int Cout, int dtype, const void *x, const void *w,
                     const void *b, void *y, hipStream_t st);

@@ -6,12 +6,31 @@ namespace plstm {
 int g_forward_path = 0;
 int g_backward_path = 0;
 
+namespace {
+// fp32 copies of a bf16 layer's input and parameters for the persistent
+// sweep (3 x 3 filters), carved after its own workspace.
+struct Widened {
+    float *x, *wx, *wh, *b;
+};
+Widened widened_params(Carve &cv, const Geom &g)
+{
+    Widened w;
+    w.x = cv.take<float>((size_t)g.N * g.V * g.C);
+    w.wx = cv.take<float>((size_t)g.nd * 4 * g.O * g.C * 9);
+    w.wh = cv.take<float>((size_t)g.nd * 4 * g.O * g.O * 9);
+    w.b = cv.take<float>((size_t)g.nd * 4 * g.O);
+    return w;
+}
+}  // namespace
+
 size_t forward_ws(const Geom &g, int dtype, bool training)
 {
     size_t need = generic_forward_ws(g, training);
     if (sweep_fwd_supported(g, dtype)) {
-        const size_t s = sweep_fwd_ws(g, training);
-        if (s > need) need = s;
+        Carve cv(nullptr);
+        cv.take<char>(sweep_fwd_ws(g, training));
+        if (dtype == PLSTM_BF16) widened_params(cv, g);
+        if (cv.off > need) need = cv.off;
     }
     if (step_supported(g)) {
         Carve cv(nullptr);
@@ -34,9 +53,20 @@ int forward_dispatch(const Geom &g, int dtype, const void *x, const void *wx, co
         float *hd = sv ? sv->hd : cv.take<float>(saved_state_count(g));
         float *cellbuf = sv ? sv->cell : cv.take<float>(saved_state_count(g));
         int *flags = cv.take<int>(1024 + 1);
-        const int rc = sweep_fwd(g, (const float *)x, (const float *)wx, (const float *)wh,
-                                 (const float *)b, hd, cellbuf, sv ? sv->gates : nullptr, flags,
-                                 st, path != 3);
+        const float *xf = (const float *)x, *wxf = (const float *)wx, *whf = (const float *)wh,
+                    *bf = (const float *)b;
+        if (dtype == PLSTM_BF16) {
+            // the persistent sweep computes in fp32: widen the bf16 inputs
+            const Widened wd = widened_params(cv, g);
+            int rc = bf16_to_f32(x, wd.x, (long long)g.N * g.V * g.C, st);
+            if (rc == PLSTM_OK) rc = bf16_to_f32(wx, wd.wx, (long long)g.nd * 4 * g.O * g.C * 9, st);
+            if (rc == PLSTM_OK) rc = bf16_to_f32(wh, wd.wh, (long long)g.nd * 4 * g.O * g.O * 9, st);
+            if (rc == PLSTM_OK) rc = bf16_to_f32(b, wd.b, (long long)g.nd * 4 * g.O, st);
+            if (rc != PLSTM_OK) return rc;
+            xf = wd.x; wxf = wd.wx; whf = wd.wh; bf = wd.b;
+        }
+        const int rc = sweep_fwd(g, xf, wxf, whf, bf, hd, cellbuf, sv ? sv->gates : nullptr,
+                                 flags, st, path != 3);
         if (rc == PLSTM_OK) return sum_dirs(g, dtype, hd, h, st);
         // A grid that cannot be co-resident or a plane too wide for LDS runs
         // on another path instead.

@@ -369,6 +369,24 @@ int generic_forward(const Geom &g, int dtype, const void *x, const void *wx, con
     return sum_dirs(g, dtype, hd, h, st);
 }
 
+namespace {
+__global__ void __launch_bounds__(kThreads)
+k_bf16_to_f32(long long n, const uint16_t *__restrict__ src, float *__restrict__ dst)
+{
+    const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) dst[i] = bf16_to_f32(src[i]);
+}
+}  // namespace
+
+int bf16_to_f32(const void *src, float *dst, long long n, hipStream_t st)
+{
+    if (n <= 0) return PLSTM_OK;
+    k_bf16_to_f32<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, st>>>(
+        n, (const uint16_t *)src, dst);
+    PLSTM_LAUNCH_CHECK();
+    return PLSTM_OK;
+}
+
 int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st)
 {
     const long long count = (long long)g.N * g.V * g.O;

@@ -544,8 +544,9 @@ int launch_sweep(const Plan &pl, SweepArgs &args, hipStream_t st)
 
 bool sweep_fwd_supported(const Geom &g, int dtype)
 {
-    return dtype == PLSTM_F32 && g.nd == kDirs && g.KP == 3 && g.KQ == 3 && g.O == kO &&
-           g.C >= 1 && g.C <= 4;
+    // bf16 storage: the caller widens x and the parameters to fp32 first
+    return (dtype == PLSTM_F32 || dtype == PLSTM_BF16) && g.nd == kDirs && g.KP == 3 &&
+           g.KQ == 3 && g.O == kO && g.C >= 1 && g.C <= 4;
 }
 
 size_t sweep_fwd_ws(const Geom &g, bool training)

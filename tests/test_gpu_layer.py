@@ -340,6 +340,26 @@ def test_reverse_sweep_strip_kinds_match_oracle(shape, bwd_path):
         assert normwise(host(got), ref[name]) <= TOL["f32"], name
 
 
+@pytest.mark.parametrize("shape", [(1, 5, 37, 29, 3, 16), (2, 9, 20, 18, 1, 16)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_bf16_o16_forward_takes_the_persistent_sweep(shape):
+    """bf16 storage with 16 units and C <= 4: the inputs are widened to fp32
+    and the persistent sweep runs; the output is the bf16-rounded sum."""
+    inst = instance(shape, 1500 + sum(shape), "bf16")
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    say("bf16 persistent", shape)
+    P.pyramid_lstm_timing_enable(True)
+    h, _ = layer_forward(dev(inst.x, "bf16"), layer_dev(L, "bf16"))
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    torch.cuda.synchronize()
+    assert "sweep_fwd_mfma" in phases and "sweep_fwd_step" not in phases, phases
+    assert h.dtype == torch.bfloat16
+    # fp32 arithmetic: only the final rounding to bf16 separates it from the oracle
+    assert normwise(host(h), ref) <= 4e-3
+
+
 def test_mfma_backward_runs_for_o16():
     """The persistent MFMA reverse sweep and MFMA parameter gradients are the
     path taken for 16 hidden units."""

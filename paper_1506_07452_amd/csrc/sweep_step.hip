@@ -220,7 +220,7 @@ struct FwdStepArgs {
 //           every A fragment through the L1.
 // Items of a (direction, batch element) are ordered unit group major.
 template <int U, bool SPLIT>
-__global__ void __launch_bounds__(64 * kSW)
+__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(3)))
 k_step_fwd(FwdStepArgs a)
 {
     constexpr int O = 16 * U, G = 4 * O;
@@ -460,7 +460,7 @@ struct FwdB16Args {
 
 // Same items and launch shapes as k_step_fwd.
 template <int U, bool SPLIT>
-__global__ void __launch_bounds__(64 * kSW)
+__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(3)))
 k_step_fwd_b16(FwdB16Args a)
 {
     constexpr int O = 16 * U, G = 4 * O, UH = O / 32;
@@ -628,7 +628,7 @@ struct BwdStepArgs {
 //   dA_i = gc g i (1 - i), dA_f = gc c_{t-1} f (1 - f), dA_g = gc i (1 - g^2),
 //   dA_o = gh tanh(c) o (1 - o)
 template <int U, bool SPLIT>
-__global__ void __launch_bounds__(64 * kSW)
+__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(3)))
 k_step_bwd(BwdStepArgs a)
 {
     constexpr int O = 16 * U, G = 4 * O, MB = 4 * U;

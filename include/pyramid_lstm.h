@@ -356,9 +356,11 @@ int pyramid_lstm_set_step_split(int mode);
 
 /* Contraction type of bf16-storage layers with 32 or 64 hidden units, for
  * testing and tuning (process-wide): 1 = bf16 MFMA with fp32 accumulation
- * (default; h_{t-1} enters the recurrent contraction rounded to bf16),
- * 0 = fp32 MFMA on the widened values.  Returns PLSTM_EINVAL for other
- * values. */
+ * (default; h_{t-1} enters the recurrent contraction rounded to bf16), the
+ * pixel blocks of a step staged in LDS once for all filter taps; 2 = the
+ * same contraction with its operands read from L1 per tap; 0 = fp32 MFMA on
+ * the widened values.  Results of 1 and 2 differ only in summation order.
+ * Returns PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_bf16_mfma(int on);
 
 #ifdef __cplusplus

@@ -481,5 +481,6 @@ def pyramid_lstm_set_step_split(mode: int) -> None:
 
 def pyramid_lstm_set_bf16_mfma(on: int) -> None:
     """bf16-storage layers with 32 or 64 hidden units: 1 = bf16 MFMA (fp32
-    accumulation), 0 = fp32 MFMA."""
+    accumulation) on pixel blocks staged in LDS, 2 = bf16 MFMA reading its
+    operands from L1, 0 = fp32 MFMA."""
     _check("pyramid_lstm_set_bf16_mfma", load().pyramid_lstm_set_bf16_mfma(int(on)))

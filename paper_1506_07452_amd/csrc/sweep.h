@@ -63,7 +63,8 @@ extern int g_backward_path;
 // workgroup's waves, 2 = never.
 extern int g_step_split;
 // bf16 storage with 32 or 64 hidden units: 1 = contraction on the bf16 MFMA
-// (default), 0 = on the fp32 MFMA.
+// with pixel blocks staged in LDS (default), 2 = bf16 MFMA with operands read
+// from L1, 0 = on the fp32 MFMA.
 extern int g_step_bf16_mfma;
 
 }  // namespace plstm

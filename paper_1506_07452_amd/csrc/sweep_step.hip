@@ -456,6 +456,9 @@ struct FwdB16Args {
     uint16_t *hb;             // [6][N][V][O] bf16 copy of h^d (the recurrence's operand)
     int npg[kDirs];
     int base[kDirs + 1];
+    // pixel blocks of the LDS-staged kernel: BP x BQ pixels (BP BQ = 64), nbq
+    // blocks across a plane row, nblk per plane
+    int bp[kDirs], bq[kDirs], nbq[kDirs], nblk[kDirs];
 };
 
 // Same items and launch shapes as k_step_fwd.
@@ -597,6 +600,146 @@ k_step_fwd_b16(FwdB16Args a)
             const float gi = fsig(pre[0][i]), gf = fsig(pre[1][i]);
             const float gg = ftanh(pre[2][i]), go = fsig(pre[3][i]);
             c[i] = gg * gi + cprev[e][i] * gf;
+            h[i] = go * ftanh(c[i]);
+            hbv[i] = f32_to_bf16(h[i]);
+        }
+        *(f4 *)(a.cell + vo * O + uo) = c;
+        *(f4 *)(a.hd + vo * O + uo) = h;
+        *(us4 *)(a.hb + vo * O + uo) = hbv;
+    }
+}
+
+// LDS-staged variant (steps with enough blocks): a workgroup takes a BP x BQ
+// block of 64 pixels of one plane and all U unit groups (wave w: units
+// 16 w .. 16 w + 15).  x_t and h_{t-1} of the block and its filter halo are
+// staged once into LDS (16-byte chunks of 8 channels, [x | h] per pixel, the
+// chunk index XOR-swizzled by the pixel), and every tap reads its B operand
+// from there instead of from L1: the taps of a pixel share one staged copy.
+// The A fragments stream from global memory as in k_step_fwd_b16.  Tile nt
+// of the block is its pixels 16 nt .. 16 nt + 15 in row-major order.
+template <int U>
+__global__ void __launch_bounds__(64 * U) __attribute__((amdgpu_waves_per_eu(3)))
+k_step_fwd_b16_blk(FwdB16Args a)
+{
+    constexpr int O = 16 * U, G = 4 * O, UH = O / 32;
+    extern __shared__ bf8 stg[];
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int ug = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int blk = blockIdx.x;
+    if (blk >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, blk);
+    const DirGeom dg = a.g.dir[d];
+    int r = blk - a.base[d];
+    const int n = r / a.nblk[d];
+    r -= n * a.nblk[d];
+    const int BP = a.bp[d], BQ = a.bq[d];
+    const int bi = r / a.nbq[d], bj = r - bi * a.nbq[d];
+    const int p0 = bi * BP, q0 = bj * BQ;
+    const int t = a.t;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const int C32 = a.C32, CX = C32 >> 5, KX = a.KX;
+    const int hoff = -dg.sign * ss;
+    const int uo = ug * 16 + 4 * q4;
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
+    const int SW = BQ + 2 * radq, SH = BP + 2 * radp;     // staged block with halo
+    const int NXC = C32 >> 3, NCH = NXC + (O >> 3);      // 16-byte chunks per staged pixel
+    const int swm = (NCH & 7) == 0 ? 7 : 3;              // swizzle within the pixel's chunks
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    // byte sizes: V * C32 * 2 and V * O * 2 (< 2^31, checked on the host)
+    const auto rs_x = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(a.xb + (long long)n * V * C32), (short)0, (int)(V * C32 * 2),
+        kRsrcWord3);
+    const auto rs_h = __builtin_amdgcn_make_buffer_rsrc(a.hb + sbase * O, (short)0,
+                                                        (int)(V * O * 2), kRsrcWord3);
+    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+
+    // ---- stage [x_t | h_{t-1}] of the block and its halo (zero off the plane)
+    const int nst = SH * SW * NCH;
+    for (int e = threadIdx.x; e < nst; e += 64 * U) {
+        const int spx = e / NCH, c = e - spx * NCH;
+        const int sy = spx / SW, sx = spx - sy * SW;
+        const int pp = p0 - radp + sy, qq = q0 - radq + sx;
+        const bool on = on_plane(pp, qq, P, Q);
+        const int v = s * ss + pp * sp + qq * sq;
+        bf8 val;
+        if (c < NXC)
+            val = bload8h(rs_x, sel_off(on, (unsigned)(v * C32 + 8 * c) * 2u));
+        else
+            val = bload8h(rs_h, sel_off(on && t > 0, (unsigned)((v + hoff) * O + 8 * (c - NXC)) * 2u));
+        stg[spx * NCH + (c ^ (spx & swm))] = val;
+    }
+
+    // this lane's pixel of each tile (block row-major; BQ is a power of two)
+    const int lbq = 31 - __builtin_clz(BQ);
+    int spix[kNT], evox[kNT];
+    bool elive[kNT];
+    f4 cprev[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const int e = nt * 16 + col;
+        const int ey = e >> lbq, ex = e & (BQ - 1);
+        spix[nt] = (ey + radp) * SW + ex + radq;
+        const int pp = p0 + ey, qq = q0 + ex;
+        elive[nt] = on_plane(pp, qq, P, Q);
+        evox[nt] = s * ss + (elive[nt] ? pp * sp + qq * sq : 0);
+        cprev[nt] = bload4(rs_c, sel_off(t > 0 && elive[nt],
+                                         (unsigned)((evox[nt] + hoff) * O + uo) * 4u));
+    }
+    __syncthreads();
+
+    f4 acc[4][kNT];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    const uint16_t *fr = a.frag + (long long)(d * U + ug) * a.KG * 2048 + lane * 8;
+    auto load_a = [&](int kg, bf8 (&av)[4]) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) av[g] = *(const bf8 *)(fr + (kg * 4 + g) * 512);
+    };
+    const int KG = t > 0 ? a.KG : KX;
+    bf8 acur[4], anxt[4];
+    load_a(0, acur);
+    for (int kg = 0; kg < KG; ++kg) {
+        if (kg + 1 < KG) load_a(kg + 1, anxt);
+        const bool is_x = kg < KX;
+        const int kk = is_x ? kg : kg - KX;
+        const int tap = is_x ? (kk * a.cx_mul32) >> 16 : kk / UH;
+        const int cb = kk - tap * (is_x ? CX : UH);
+        const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
+        const int chunk = (is_x ? 0 : NXC) + cb * 4 + q4;
+        const int doff = ka * SW + kb;
+        bf8 bv[kNT];
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) {
+            const int spx = spix[nt] + doff;
+            bv[nt] = stg[spx * NCH + (chunk ^ (spx & swm))];
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = mfma_bf16(acur[g], bv[nt], acc[g][nt]);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acur[g] = anxt[g];
+    }
+
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        if (!elive[nt]) continue;
+        f4 pre[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) pre[g] = acc[g][nt] + *(const f4 *)(a.bias + d * G + g * O + uo);
+        const long long vo = sbase + evox[nt];
+        f4 c, h;
+        us4 hbv;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float gi = fsig(pre[0][i]), gf = fsig(pre[1][i]);
+            const float gg = ftanh(pre[2][i]), go = fsig(pre[3][i]);
+            c[i] = gg * gi + cprev[nt][i] * gf;
             h[i] = go * ftanh(c[i]);
             hbv[i] = f32_to_bf16(h[i]);
         }
@@ -1300,11 +1443,25 @@ size_t step_fwd_ws(const Geom &g)
     return need;
 }
 
+// LDS bytes of the staged pixel blocks (the largest over the directions).
+size_t b16_block_lds(const Geom &g, const FwdB16Args &a)
+{
+    size_t m = 0;
+    const int nch = (a.C32 + g.O) / 8;
+    for (int d = 0; d < g.nd; ++d) {
+        const size_t b = (size_t)(a.bp[d] + 2 * (g.KP / 2)) * (a.bq[d] + 2 * (g.KQ / 2)) * nch * 16;
+        if (b > m) m = b;
+    }
+    return m;
+}
+
 template <int U>
 int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
 {
     const int T = max_T(g);
     const int few = split_threshold();
+    const size_t lds = b16_block_lds(g, a);
+    const bool staged = g_step_bf16_mfma == 1 && lds <= 64 * 1024;
     for (int t = 0; t < T; ++t) {
         a.t = t;
         int tot = 0;
@@ -1313,10 +1470,19 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
             if (t < g.dir[d].T) tot += g.N * U * a.npg[d];
         }
         a.base[kDirs] = tot;
-        if (tot < few)
+        if (tot < few) {
             k_step_fwd_b16<U, true><<<tot, 64 * kSW, 0, st>>>(a);
-        else
+        } else if (staged) {
+            int nb = 0;
+            for (int d = 0; d < kDirs; ++d) {
+                a.base[d] = nb;
+                if (t < g.dir[d].T) nb += g.N * a.nblk[d];
+            }
+            a.base[kDirs] = nb;
+            k_step_fwd_b16_blk<U><<<nb, 64 * U, lds, st>>>(a);
+        } else {
             k_step_fwd_b16<U, false><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
+        }
         PLSTM_LAUNCH_CHECK();
     }
     return PLSTM_OK;
@@ -1349,7 +1515,18 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     a.k_mul = k_mul_of(g);
     a.xb = xb; a.frag = frag; a.bias = bias;
     a.hd = hd; a.cell = cell; a.hb = hb;
-    for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
+    for (int d = 0; d < kDirs; ++d) {
+        a.npg[d] = npg_of(g.dir[d]);
+        // 64-pixel blocks as square as the plane allows: BP the largest power
+        // of two up to min(P, 8), BQ = 64 / BP
+        const DirGeom &dg = g.dir[d];
+        int bp = 1;
+        while (bp < 8 && 2 * bp <= dg.P) bp *= 2;
+        a.bp[d] = bp;
+        a.bq[d] = 64 / bp;
+        a.nbq[d] = dg.Q > 0 ? (dg.Q + a.bq[d] - 1) / a.bq[d] : 0;
+        a.nblk[d] = dg.P > 0 ? (dg.P + bp - 1) / bp * a.nbq[d] : 0;
+    }
     const int rc = U == 2 ? launch_fwd_b16_steps<2>(g, a, st) : launch_fwd_b16_steps<4>(g, a, st);
     if (rc != PLSTM_OK) return rc;
     timing_end(2 + max_T(g), st);
@@ -1540,7 +1717,7 @@ extern "C" int pyramid_lstm_set_step_split(int mode)
 
 extern "C" int pyramid_lstm_set_bf16_mfma(int on)
 {
-    if (on != 0 && on != 1) return PLSTM_EINVAL;
+    if (on < 0 || on > 2) return PLSTM_EINVAL;
     plstm::g_step_bf16_mfma = on;
     return PLSTM_OK;
 }

@@ -297,7 +297,7 @@ def test_filter_size_generic_path(case):
         assert normwise(host(got), ref[name]) <= TOL["f32"], name
 
 
-@pytest.mark.parametrize("bf16_mfma", [1, 0], ids=["bf16_mfma", "fp32_mfma"])
+@pytest.mark.parametrize("bf16_mfma", [1, 2, 0], ids=["bf16_lds", "bf16_l1", "fp32_mfma"])
 def test_filter_size_bf16(bf16_mfma):
     shape, K = (1, 4, 11, 9, 25, 32), 7
     inst = instance_k(shape, K, 7200, "bf16")
@@ -404,7 +404,7 @@ def test_forward_bf16_matches_oracle(shape):
     assert err <= TOL["bf16"], err
 
 
-@pytest.mark.parametrize("bf16_mfma", [1, 0], ids=["bf16_mfma", "fp32_mfma"])
+@pytest.mark.parametrize("bf16_mfma", [1, 2, 0], ids=["bf16_lds", "bf16_l1", "fp32_mfma"])
 @pytest.mark.parametrize("shape", [(1, 4, 6, 70, 3, 64), (2, 9, 17, 40, 32, 32),
                                    (1, 5, 23, 9, 40, 32), (2, 3, 7, 66, 64, 64)],
                          ids=lambda s: "x".join(map(str, s)))

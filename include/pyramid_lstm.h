@@ -349,8 +349,10 @@ int pyramid_lstm_set_backward_path(int path);
  * (process-wide): 0 = automatic (default): a step whose tiles would give
  * fewer than about two waves per SIMD splits each tile's K dimension over
  * the four waves of a workgroup, other steps give each wave its own tiles;
- * 1 = always split; 2 = never split.  Results are identical up to the
- * summation order of the split partials.  Returns PLSTM_EINVAL for other
+ * 1 = always split; 2 = never split; 3 = never split, and the forward's
+ * operands read from L1 per filter tap instead of from 64-pixel blocks
+ * staged in LDS (the default for fp32 steps that are not split).  Results
+ * are identical up to summation order.  Returns PLSTM_EINVAL for other
  * values. */
 int pyramid_lstm_set_step_split(int mode);
 

@@ -475,7 +475,8 @@ def pyramid_lstm_set_backward_path(path: int) -> None:
 
 def pyramid_lstm_set_step_split(mode: int) -> None:
     """Plane-step launch shape: 0 = automatic, 1 = always split each tile's K
-    over a workgroup's waves, 2 = never."""
+    over a workgroup's waves, 2 = never, 3 = never and the fp32 forward
+    reading its operands from L1 instead of LDS-staged pixel blocks."""
     _check("pyramid_lstm_set_step_split", load().pyramid_lstm_set_step_split(int(mode)))
 
 

@@ -60,7 +60,8 @@ int backward_dispatch(const Geom &g, const float *x, const float *wx, const floa
 extern int g_forward_path;
 extern int g_backward_path;
 // Plane-step launches: 0 = automatic, 1 = always split each tile's K over a
-// workgroup's waves, 2 = never.
+// workgroup's waves, 2 = never, 3 = never and the fp32 forward without LDS
+// staging.
 extern int g_step_split;
 // bf16 storage with 32 or 64 hidden units: 1 = contraction on the bf16 MFMA
 // with pixel blocks staged in LDS (default), 2 = bf16 MFMA with operands read

@@ -207,6 +207,8 @@ struct FwdStepArgs {
     float *gates;             // [6][N][V][4O] or null
     int npg[kDirs];           // pixel groups (kNT tiles) of a plane
     int base[kDirs + 1];      // first workgroup of each direction in this launch
+    // pixel blocks of the LDS-staged kernel (as in FwdB16Args)
+    int bp[kDirs], bq[kDirs], nbq[kDirs], nblk[kDirs];
 };
 
 // The four gates of unit group ug for kNT 16-pixel tiles of one plane (an
@@ -366,6 +368,161 @@ k_step_fwd(FwdStepArgs a)
             gg[i] = ftanh(pre[2][i]);
             go[i] = fsig(pre[3][i]);
             c[i] = gg[i] * gi[i] + cprev[e][i] * gf[i];
+            h[i] = go[i] * ftanh(c[i]);
+        }
+        *(f4 *)(a.cell + vo * O + uo) = c;
+        *(f4 *)(a.hd + vo * O + uo) = h;
+        if (a.gates) {
+            float *gp = a.gates + vo * G + uo;
+            *(f4 *)gp = gi;
+            *(f4 *)(gp + O) = gf;
+            *(f4 *)(gp + 2 * O) = gg;
+            *(f4 *)(gp + 3 * O) = go;
+        }
+    }
+}
+
+// LDS-staged variant of k_step_fwd (steps with enough blocks): a workgroup
+// takes a BP x BQ block of 64 pixels of one plane and all U unit groups (wave
+// w: units 16 w .. 16 w + 15).  The block's x_t with its filter halo is
+// staged in LDS (16-byte chunks of 4 channels, XOR-swizzled by the pixel)
+// and the input taps read their B operands from there; then h_{t-1} is
+// staged over it for the recurrent taps.  The A fragments stream from global
+// memory.  Tile nt of the block is its pixels 16 nt .. 16 nt + 15 in
+// row-major order.
+template <int U>
+__global__ void __launch_bounds__(64 * U) __attribute__((amdgpu_waves_per_eu(3)))
+k_step_fwd_blk(FwdStepArgs a)
+{
+    constexpr int O = 16 * U, G = 4 * O;
+    extern __shared__ f4 stf[];
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int ug = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int blk = blockIdx.x;
+    if (blk >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, blk);
+    const DirGeom dg = a.g.dir[d];
+    int r = blk - a.base[d];
+    const int n = r / a.nblk[d];
+    r -= n * a.nblk[d];
+    const int BP = a.bp[d], BQ = a.bq[d];
+    const int bi = r / a.nbq[d], bj = r - bi * a.nbq[d];
+    const int p0 = bi * BP, q0 = bj * BQ;
+    const int t = a.t;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const int Cp = a.Cp, CX = Cp >> 4, KX = a.KX;
+    const int hoff = -dg.sign * ss;
+    const int uo = ug * 16 + 4 * q4;
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
+    const int SW = BQ + 2 * radq, SH = BP + 2 * radp;
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    const auto rs_x = slice_rsrc(a.xp + (long long)n * V * Cp, V * Cp);
+    const auto rs_h = slice_rsrc(a.hd + sbase * O, V * O);
+    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+
+    // Stage one operand of the block and its halo: nch chunks per pixel of
+    // `stride` floats per voxel from `rs` at voxel offset `dvox` (zero off
+    // the plane or when !ok).
+    auto stage = [&](__amdgpu_buffer_rsrc_t rs, int nch, int stride, int dvox, bool ok) {
+        const int swm = (nch & 7) == 0 ? 7 : 3;
+        const int nst = SH * SW * nch;
+        for (int e = threadIdx.x; e < nst; e += 64 * U) {
+            const int spx = e / nch, c = e - spx * nch;
+            const int sy = spx / SW, sx = spx - sy * SW;
+            const int pp = p0 - radp + sy, qq = q0 - radq + sx;
+            const bool on = ok && on_plane(pp, qq, P, Q);
+            const int v = s * ss + pp * sp + qq * sq + dvox;
+            stf[spx * nch + (c ^ (spx & swm))] =
+                bload4(rs, sel_off(on, (unsigned)(v * stride + 4 * c) * 4u));
+        }
+    };
+
+    const int lbq = 31 - __builtin_clz(BQ);
+    int spix[kNT], evox[kNT];
+    bool elive[kNT];
+    f4 cprev[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const int e = nt * 16 + col;
+        const int ey = e >> lbq, ex = e & (BQ - 1);
+        spix[nt] = (ey + radp) * SW + ex + radq;
+        const int pp = p0 + ey, qq = q0 + ex;
+        elive[nt] = on_plane(pp, qq, P, Q);
+        evox[nt] = s * ss + (elive[nt] ? pp * sp + qq * sq : 0);
+        cprev[nt] = bload4(rs_c, sel_off(t > 0 && elive[nt],
+                                         (unsigned)((evox[nt] + hoff) * O + uo) * 4u));
+    }
+
+    f4 acc[4][kNT];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    const float *fr = a.frag + (long long)(d * U + ug) * a.KG * 1024 + lane * 4;
+    // K-groups kg0 .. kg1 - 1 of one operand (x: kg < KX, else h) from the
+    // staged block; A fragments one K-group ahead
+    auto contract = [&](int kg0, int kg1, bool is_x) {
+        const int nch = is_x ? CX * 4 : U * 4;
+        const int swm = (nch & 7) == 0 ? 7 : 3;
+        f4 acur[4], anxt[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acur[g] = *(const f4 *)(fr + kg0 * 1024 + g * 256);
+        for (int kg = kg0; kg < kg1; ++kg) {
+            if (kg + 1 < kg1) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) anxt[g] = *(const f4 *)(fr + (kg + 1) * 1024 + g * 256);
+            }
+            const int kk = is_x ? kg : kg - KX;
+            const int tap = is_x ? (kk * a.cx_mul) >> 16 : kk / U;
+            const int cb = kk - tap * (is_x ? CX : U);
+            const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
+            const int chunk = cb * 4 + q4;
+            const int doff = ka * SW + kb;
+            f4 bv[kNT];
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) {
+                const int spx = spix[nt] + doff;
+                bv[nt] = stf[spx * nch + (chunk ^ (spx & swm))];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+#pragma unroll
+                    for (int nt = 0; nt < kNT; ++nt)
+                        acc[g][nt] = mfma(acur[g][i], bv[nt][i], acc[g][nt]);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) acur[g] = anxt[g];
+        }
+    };
+    stage(rs_x, CX * 4, Cp, 0, true);
+    __syncthreads();
+    contract(0, KX, true);
+    if (t > 0) {
+        __syncthreads();                 // every wave is done with the staged x
+        stage(rs_h, U * 4, O, hoff, true);
+        __syncthreads();
+        contract(KX, a.KG, false);
+    }
+
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        if (!elive[nt]) continue;
+        f4 pre[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) pre[g] = acc[g][nt] + *(const f4 *)(a.bias + d * G + g * O + uo);
+        const long long vo = sbase + evox[nt];
+        f4 gi, gf, gg, go, c, h;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            gi[i] = fsig(pre[0][i]);
+            gf[i] = fsig(pre[1][i]);
+            gg[i] = ftanh(pre[2][i]);
+            go[i] = fsig(pre[3][i]);
+            c[i] = gg[i] * gi[i] + cprev[nt][i] * gf[i];
             h[i] = go[i] * ftanh(c[i]);
         }
         *(f4 *)(a.cell + vo * O + uo) = c;
@@ -1326,7 +1483,7 @@ inline WgShape wg_shape(const Geom &g)
 inline int split_threshold()
 {
     if (g_step_split == 1) return 1 << 30;
-    if (g_step_split == 2) return 0;
+    if (g_step_split == 2 || g_step_split == 3) return 0;
     const DevInfo di = device_info();
     return 8 * (di.cus > 0 ? di.cus : 256);
 }
@@ -1336,6 +1493,14 @@ int launch_fwd_steps(const Geom &g, FwdStepArgs &a, hipStream_t st)
 {
     const int T = max_T(g);
     const int few = split_threshold();
+    // staged x or h of a block (the larger of the two phases)
+    size_t lds = 0;
+    const int nch = (a.Cp / 4 > 4 * U ? a.Cp / 4 : 4 * U);
+    for (int d = 0; d < g.nd; ++d) {
+        const size_t b = (size_t)(a.bp[d] + 2 * (g.KP / 2)) * (a.bq[d] + 2 * (g.KQ / 2)) * nch * 16;
+        if (b > lds) lds = b;
+    }
+    const bool staged = g_step_split != 3 && lds <= 64 * 1024;
     for (int t = 0; t < T; ++t) {
         a.t = t;
         int tot = 0;
@@ -1344,10 +1509,19 @@ int launch_fwd_steps(const Geom &g, FwdStepArgs &a, hipStream_t st)
             if (t < g.dir[d].T) tot += g.N * U * a.npg[d];
         }
         a.base[kDirs] = tot;
-        if (tot < few)
+        if (tot < few) {
             k_step_fwd<U, true><<<tot, 64 * kSW, 0, st>>>(a);
-        else
+        } else if (staged) {
+            int nb = 0;
+            for (int d = 0; d < kDirs; ++d) {
+                a.base[d] = nb;
+                if (t < g.dir[d].T) nb += g.N * a.nblk[d];
+            }
+            a.base[kDirs] = nb;
+            k_step_fwd_blk<U><<<nb, 64 * U, lds, st>>>(a);
+        } else {
             k_step_fwd<U, false><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
+        }
         PLSTM_LAUNCH_CHECK();
     }
     return PLSTM_OK;
@@ -1443,6 +1617,21 @@ size_t step_fwd_ws(const Geom &g)
     return need;
 }
 
+// 64-pixel blocks of the LDS-staged forward kernels, as square as a plane
+// allows: BP the largest power of two up to min(P, 8), BQ = 64 / BP.
+void set_blocks(const Geom &g, int *bp, int *bq, int *nbq, int *nblk)
+{
+    for (int d = 0; d < kDirs; ++d) {
+        const DirGeom &dg = g.dir[d];
+        int b = 1;
+        while (b < 8 && 2 * b <= dg.P) b *= 2;
+        bp[d] = b;
+        bq[d] = 64 / b;
+        nbq[d] = dg.Q > 0 ? (dg.Q + bq[d] - 1) / bq[d] : 0;
+        nblk[d] = dg.P > 0 ? (dg.P + b - 1) / b * nbq[d] : 0;
+    }
+}
+
 // LDS bytes of the staged pixel blocks (the largest over the directions).
 size_t b16_block_lds(const Geom &g, const FwdB16Args &a)
 {
@@ -1515,18 +1704,8 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     a.k_mul = k_mul_of(g);
     a.xb = xb; a.frag = frag; a.bias = bias;
     a.hd = hd; a.cell = cell; a.hb = hb;
-    for (int d = 0; d < kDirs; ++d) {
-        a.npg[d] = npg_of(g.dir[d]);
-        // 64-pixel blocks as square as the plane allows: BP the largest power
-        // of two up to min(P, 8), BQ = 64 / BP
-        const DirGeom &dg = g.dir[d];
-        int bp = 1;
-        while (bp < 8 && 2 * bp <= dg.P) bp *= 2;
-        a.bp[d] = bp;
-        a.bq[d] = 64 / bp;
-        a.nbq[d] = dg.Q > 0 ? (dg.Q + a.bq[d] - 1) / a.bq[d] : 0;
-        a.nblk[d] = dg.P > 0 ? (dg.P + bp - 1) / bp * a.nbq[d] : 0;
-    }
+    for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
+    set_blocks(g, a.bp, a.bq, a.nbq, a.nblk);
     const int rc = U == 2 ? launch_fwd_b16_steps<2>(g, a, st) : launch_fwd_b16_steps<4>(g, a, st);
     if (rc != PLSTM_OK) return rc;
     timing_end(2 + max_T(g), st);
@@ -1576,6 +1755,7 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     a.xp = xp; a.frag = frag; a.bias = bias;
     a.hd = hd; a.cell = cell; a.gates = gates;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
+    set_blocks(g, a.bp, a.bq, a.nbq, a.nblk);
     int rc;
     switch (U) {
     case 1: rc = launch_fwd_steps<1>(g, a, st); break;
@@ -1710,7 +1890,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
 
 extern "C" int pyramid_lstm_set_step_split(int mode)
 {
-    if (mode < 0 || mode > 2) return PLSTM_EINVAL;
+    if (mode < 0 || mode > 3) return PLSTM_EINVAL;
     plstm::g_step_split = mode;
     return PLSTM_OK;
 }

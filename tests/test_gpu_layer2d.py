@@ -66,7 +66,7 @@ def test_2d_layer_matches_oracle(shape):
         assert "sweep_fwd_generic" in phases and "sweep_bwd_generic" in phases, phases
 
 
-@pytest.fixture(params=[1, 2], ids=["split", "nosplit"])
+@pytest.fixture(params=[1, 2, 3], ids=["split", "nosplit", "nosplit_l1"])
 def step_split(request):
     P.pyramid_lstm_set_step_split(request.param)
     yield

@@ -21,6 +21,9 @@ Two more workloads can be timed instead (not the headline; no CPU baseline):
                               + softmax cross-entropy, fp32, forward + backward
     --workload em-layer       30 x 512 x 512 x 1 EM-like stack, one layer (16),
                               fp32, forward (inference)
+    --workload image-2d       the same 30 slices as a batch of 512 x 512 images
+                              through one 2D layer (16 units, 3 taps), fp32,
+                              forward + backward
     --workload paper-net      the network of the paper's experiments (7x7
                               filters, 16 / FC 25 / 32 / FC 45 / 64 -> output)
                               on a 25 x 240 x 240 x 5 MR sub-volume, softmax
@@ -270,6 +273,64 @@ def bench_em(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_2d(args):
+    """The 2D layer (four line sweeps, Section 2.1-2.2) over the EM-like
+    slices as a batch of images: training forward + backward."""
+    import torch
+    import synth
+    import paper_1506_07452_amd as P
+    from paper_1506_07452_amd.network import LayerW, layer2d_backward, layer2d_forward
+    N, H, W, C, O, K = 30, 512, 512, 1, 16, 3
+    x, wx, wh, b = synth.image2d(N, H, W, C, O, K, seed=2048, scale=0.1)
+    torch.cuda.init()
+    dev = lambda a: torch.from_numpy(a).to("cuda:0").contiguous()
+    xd, L = dev(x), LayerW(dev(wx), dev(wh), dev(b))
+    s = P.shape2d_for(xd, O, K)
+    ws = torch.empty(P.pyramid_lstm2d_workspace_size(s, 1), dtype=torch.uint8, device="cuda:0")
+    dh = torch.ones((N, H, W, O), device="cuda:0")
+
+    def step():
+        h, saved = layer2d_forward(xd, L, training=True, ws=ws)
+        return layer2d_backward(xd, L, saved, dh, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    P.pyramid_lstm_timing_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / args.steps
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    V = N * H * W
+    # algorithmic flops per pixel-direction: forward 2 K 4O (C + O); reverse
+    # 2 K 4O O; weight gradients 2 4O (K (C + O) + 1); dL/dx 2 K 4O C
+    G = 4 * O
+    work = {"sweep_fwd_step": 2 * K * G * (C + O), "sweep_bwd_step": 2 * K * G * O,
+            "wgrad_step": 2 * G * (K * (C + O) + 1), "dx_step": 2 * K * G * C}
+    name = max((k for k in phases if k in work), key=lambda k: phases[k][0])
+    ms, launches = phases[name]
+    per_launch = 4 * V * work[name] * args.steps / launches
+    achieved = per_launch / (ms / 1e3 / launches) / 1e12
+    out = {
+        "metric": METRIC, "value": 4 * V / t, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": t * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "2D PyraMiD-LSTM, 30 EM-like 512x512 slices as images, O=16, "
+                               "1x3 filters, fwd+bwd", "N": N, "H": H, "W": W, "C": C, "O": O,
+                   "K": K},
+        "roofline": {"kernel": name, "bound": "mfma", "achieved": round(achieved, 3),
+                     "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": None,
+                     "launches_per_pass": launches // args.steps,
+                     "avg_launch_ms": round(ms / launches, 4)},
+        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def cpu_baseline(inst_cfg, crop):
     """The fp64 oracle (as is) on a bounded crop of the same workload."""
     import numpy as np
@@ -298,8 +359,8 @@ def main():
     ap.add_argument("--separate-head", action="store_true",
                     help="run the FC / softmax head as separate kernels instead of the fused one")
     ap.add_argument("--workload", default="mr-layer",
-                    choices=["mr-layer", "em-layer", "stacked-bf16", "train-2layer",
-                             "paper-net"],
+                    choices=["mr-layer", "em-layer", "image-2d", "stacked-bf16",
+                             "train-2layer", "paper-net"],
                     help="mr-layer: the headline single-layer MR workload (default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 1 GiB device-to-device three times (a plain copy kernel "
@@ -312,6 +373,9 @@ def main():
         sys.exit(2)
     if args.workload == "em-layer":
         bench_em(args)
+        return
+    if args.workload == "image-2d":
+        bench_2d(args)
         return
     if args.workload != "mr-layer":
         bench_network(args, {"stacked-bf16": 4, "train-2layer": 5, "paper-net": None}[

@@ -1081,7 +1081,7 @@ k_step_bwd(BwdStepArgs a)
 // The partial sums of the chunks are added in order.  db = sum_v dA[v] is a
 // separate column sum of dA.
 constexpr int kWgN = 8;          // most N-tiles a wave holds
-constexpr int kWgMaxChunks = 64;
+constexpr int kWgMaxChunks = 512;
 
 // N-tiles per block: each part (KK U tiles of h, KK C'/16 tiles of x) is cut
 // into the fewest blocks of at most kWgN tiles, as even as possible.

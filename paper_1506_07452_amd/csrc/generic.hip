@@ -103,6 +103,33 @@ k_sum_dirs(long long count, int nd, const float *__restrict__ hd, TS *__restrict
     Store<TS>::store(h, i, acc);
 }
 
+// The same sum, four consecutive elements per thread (count a multiple of 4):
+// every direction's 16-byte load is in flight before the first add, and the
+// additions keep the order d = 0..nd-1, so the result is the scalar kernel's.
+typedef float sf4 __attribute__((ext_vector_type(4)));
+typedef unsigned short su4 __attribute__((ext_vector_type(4)));
+template <typename TS>
+__global__ void __launch_bounds__(kThreads)
+k_sum_dirs4(long long count4, int nd, const float *__restrict__ hd, TS *__restrict__ h)
+{
+    const long long i = (long long)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= count4) return;
+    const sf4 *src = (const sf4 *)hd;
+    sf4 v[kDirs];
+#pragma unroll
+    for (int d = 0; d < kDirs; ++d) v[d] = d < nd ? src[(long long)d * count4 + i] : sf4{0, 0, 0, 0};
+    sf4 acc = v[0];
+#pragma unroll
+    for (int d = 1; d < kDirs; ++d)
+        if (d < nd) acc += v[d];
+    if constexpr (sizeof(TS) == 4) {
+        ((sf4 *)h)[i] = acc;
+    } else {
+        ((su4 *)h)[i] = su4{f32_to_bf16(acc[0]), f32_to_bf16(acc[1]), f32_to_bf16(acc[2]),
+                            f32_to_bf16(acc[3])};
+    }
+}
+
 __global__ void __launch_bounds__(kThreads)
 k_bwd_step(Geom g, int t, const float *__restrict__ wh, const float *__restrict__ gates,
            const float *__restrict__ cell, const float *__restrict__ dh,
@@ -392,10 +419,18 @@ int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st)
     const long long count = (long long)g.N * g.V * g.O;
     const unsigned blocks = (unsigned)((count + kThreads - 1) / kThreads);
     timing_begin("sum_dirs", st);
-    if (dtype == PLSTM_BF16)
+    if (count % 4 == 0) {
+        const long long c4 = count / 4;
+        const unsigned b4 = (unsigned)((c4 + kThreads - 1) / kThreads);
+        if (dtype == PLSTM_BF16)
+            k_sum_dirs4<uint16_t><<<b4, kThreads, 0, st>>>(c4, g.nd, hd, (uint16_t *)h);
+        else
+            k_sum_dirs4<float><<<b4, kThreads, 0, st>>>(c4, g.nd, hd, (float *)h);
+    } else if (dtype == PLSTM_BF16) {
         k_sum_dirs<uint16_t><<<blocks, kThreads, 0, st>>>(count, g.nd, hd, (uint16_t *)h);
-    else
+    } else {
         k_sum_dirs<float><<<blocks, kThreads, 0, st>>>(count, g.nd, hd, (float *)h);
+    }
     PLSTM_LAUNCH_CHECK();
     timing_end(1, st);
     return PLSTM_OK;

@@ -1080,7 +1080,7 @@ k_step_bwd(BwdStepArgs a)
 // that the rows read for one unit are re-read from cache by the next ones.
 // The partial sums of the chunks are added in order.  db = sum_v dA[v] is a
 // separate column sum of dA.
-constexpr int kWgN = 8;          // most N-tiles a wave holds
+constexpr int kWgN = 4;          // most N-tiles a wave holds
 constexpr int kWgMaxChunks = 512;
 
 // N-tiles per block: each part (KK U tiles of h, KK C'/16 tiles of x) is cut
@@ -1242,7 +1242,7 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
 }
 
 template <int U>
-__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(1)))
+__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(2)))
 k_wgrad_step(WgStepArgs a)
 {
     const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1264,12 +1264,16 @@ k_wgrad_step(WgStepArgs a)
     const int tend = is_h ? KK * U : KK * CX;
     const int ntl = t0 + tb < tend ? tb : tend - t0;
     const int first_nt = (is_h ? 0 : KK * U) + t0;
-    if (ntl <= 4)
+    if constexpr (kWgN <= 4) {
         wg_wave<U, 4>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
-    else if (ntl <= 6)
-        wg_wave<U, 6>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
-    else
-        wg_wave<U, 8>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+    } else {
+        if (ntl <= 4)
+            wg_wave<U, 4>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        else if (ntl <= 6)
+            wg_wave<U, 6>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        else
+            wg_wave<U, 8>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+    }
 }
 
 // db: column sums of dA over the voxels of each direction, in fixed chunks

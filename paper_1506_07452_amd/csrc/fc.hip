@@ -1043,6 +1043,104 @@ k_softmax_vec(long long M, int Cin, int K, const TS *__restrict__ x, const TS *_
     }
 }
 
+// Softmax head, 16 lanes per row (Cin a multiple of 4): lane j of a row's
+// group reads elements 4 j .. 4 j + 3 of every 64-element stretch, so a
+// group's loads are contiguous; the partial logits meet in a 16-lane
+// butterfly, after which every lane of the group holds the row's logits and
+// lane k writes class k.  A block of 256 threads takes 128 rows (eight per
+// group), and its loss partial lands in lossp[block].
+template <typename TS, bool SQ>
+__global__ void __launch_bounds__(kThreads)
+k_softmax_coop(long long M, int Cin, int K, const TS *__restrict__ x, const TS *__restrict__ w,
+               const TS *__restrict__ b, const int32_t *__restrict__ labels,
+               float *__restrict__ p, float *__restrict__ dlogits, float *__restrict__ lossp)
+{
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    extern __shared__ float lds[];
+    float *sw = lds;                               // [K][Cin]
+    for (int e = threadIdx.x; e < K * Cin; e += kThreads) sw[e] = Store<TS>::load(w, e);
+    __syncthreads();
+    const int j = threadIdx.x & 15, grp = threadIdx.x >> 4;
+    float l = 0.0f;
+    for (int it = 0; it < 8; ++it) {
+        const long long m = (long long)blockIdx.x * 128 + it * 16 + grp;
+        if (m >= M) break;                          // the group's 16 lanes agree
+        float z[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) z[k] = 0.0f;
+        const TS *xr = x + m * Cin;
+        for (int c = 4 * j; c < Cin; c += 64) {
+            const f4v xv = Vec4<TS>::load(xr + c);
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                if (k < K) {
+                    const f4v wv = *(const f4v *)&sw[k * Cin + c];
+                    z[k] += (xv[0] * wv[0] + xv[1] * wv[1]) + (xv[2] * wv[2] + xv[3] * wv[3]);
+                }
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            if (k < K) {
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1) z[k] += __shfl_xor(z[k], off, 16);
+                z[k] += Store<TS>::load(b, k);
+            }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (k < K) mx = fmaxf(mx, z[k]);
+        float sum = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            z[k] = k < K ? __expf(z[k] - mx) : 0.0f;
+            sum += z[k];
+        }
+        const float inv = 1.0f / sum;
+        float pj = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (k == j) pj = z[k] * inv;
+        if (j < K) p[m * K + j] = pj;
+        if (labels) {
+            // An out-of-range label poisons the loss and the gradient with NaN.
+            const int lab = labels[m];
+            const bool ok = lab >= 0 && lab < K;
+            const float dj = pj - (j == lab ? 1.0f : 0.0f);
+            if (SQ) {
+                float e = 0.0f, sd = 0.0f;
+#pragma unroll
+                for (int k = 0; k < 16; ++k) {
+                    if (k < K) {
+                        const float pk = z[k] * inv, dk = pk - (k == lab ? 1.0f : 0.0f);
+                        e += dk * dk;
+                        sd += pk * dk;
+                    }
+                }
+                if (j == 0) l += ok ? e : NAN;
+                if (j < K) dlogits[m * K + j] = ok ? 2.0f * pj * (dj - sd) / (float)M : NAN;
+            } else {
+                float pl = 0.0f;
+#pragma unroll
+                for (int k = 0; k < 16; ++k)
+                    if (k == lab) pl = z[k] * inv;
+                if (j == 0) l += ok ? -logf(pl) : NAN;
+                if (j < K) dlogits[m * K + j] = ok ? dj / (float)M : NAN;
+            }
+        }
+    }
+    if (labels) {
+        __shared__ float red[kThreads];
+        red[threadIdx.x] = l;
+        __syncthreads();
+        for (int off = kThreads / 2; off > 0; off >>= 1) {
+            if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) lossp[blockIdx.x] = red[0];
+    }
+}
+
 template <bool SQ>
 static int softmax_loss_impl(long long M, int Cin, int K, int dtype, const void *x,
                              const void *w, const void *b, const int32_t *labels, float *p,
@@ -1054,7 +1152,19 @@ static int softmax_loss_impl(long long M, int Cin, int K, int dtype, const void 
     float *dlogits = cv.take<float>((size_t)M * K);
     float *lossp = cv.take<float>((size_t)(M + kRB - 1) / kRB);
     unsigned nb = blocks_for(M);
-    if (Cin % 4 == 0 && (size_t)K * Cin * sizeof(float) <= 65536) {
+    if (Cin % 4 == 0 && Cin >= 64 && (size_t)K * Cin * sizeof(float) <= 65536) {
+        // wide rows: 16 lanes per row, 128 rows per block
+        nb = (unsigned)((M + 127) / 128);
+        const size_t lds = (size_t)K * Cin * sizeof(float);
+        if (dtype == PLSTM_BF16)
+            k_softmax_coop<uint16_t, SQ><<<nb, kThreads, lds, st>>>(
+                M, Cin, K, (const uint16_t *)x, (const uint16_t *)w, (const uint16_t *)b, labels,
+                p, dlogits, lossp);
+        else
+            k_softmax_coop<float, SQ><<<nb, kThreads, lds, st>>>(
+                M, Cin, K, (const float *)x, (const float *)w, (const float *)b, labels, p,
+                dlogits, lossp);
+    } else if (Cin % 4 == 0 && (size_t)K * Cin * sizeof(float) <= 65536) {
         const size_t lds = (size_t)K * Cin * sizeof(float);
         if (dtype == PLSTM_BF16)
             k_softmax_vec<uint16_t, SQ><<<nb, kThreads, lds, st>>>(

@@ -104,9 +104,11 @@ def test_paper_network_forward_bf16():
     assert normwise(host(out["p"]), ref) <= TOL["bf16"]
 
 
-# input widths of the three softmax kernels: a multiple of 4 (rows read as
-# vectors), other widths up to 128 (rows staged in LDS), wider ones
-SOFTMAX_CIN = [(16, "vec"), (128, "vec128"), (200, "vec200"), (18, "rows"), (203, "wide")]
+# input widths of the four softmax kernels: multiples of 4 from 64 (16 lanes
+# per row), smaller multiples of 4 (a row per thread, read as vectors), other
+# widths up to 128 (rows staged in LDS), wider ones
+SOFTMAX_CIN = [(16, "vec"), (64, "coop64"), (128, "coop128"), (200, "coop200"), (18, "rows"),
+               (203, "wide")]
 
 
 @pytest.mark.parametrize("cin", [c for c, _ in SOFTMAX_CIN], ids=[n for _, n in SOFTMAX_CIN])

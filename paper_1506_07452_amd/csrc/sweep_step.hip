@@ -94,6 +94,9 @@ __device__ inline int item_dir(const int *base, int item)
     return d;
 }
 
+constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unconstrained
+typedef __attribute__((address_space(3))) void lds_void;
+
 // In-plane coordinates of a pixel, or kDead past the plane: no tap offset
 // (|offset| <= 3) brings kDead back onto a plane.
 constexpr int kDead = -(1 << 20);
@@ -534,6 +537,168 @@ k_step_fwd_blk(FwdStepArgs a)
             *(f4 *)(gp + 2 * O) = gg;
             *(f4 *)(gp + 3 * O) = go;
         }
+    }
+}
+
+// ---- line blocks of the 2D layer's forward (16 hidden units) ----------------
+// A 2D direction scans whole lines; each step is one line of Q pixels, too
+// little work for a launch of its own.  Here a workgroup owns a 64-pixel
+// segment of a line and advances S lines in one launch with overlapped
+// tiles: at line j of the launch it computes the segment widened by
+// (S - 1 - j) r pixels on each side (r = KQ / 2), which is exactly what line
+// j + 1 reads, so h_{t-1} and c stay in LDS across the S lines; only the
+// segment itself is stored.  The widened pixels are the neighbours' own
+// pixels, recomputed.  Pixels past the line keep h = 0 (zero padding).
+constexpr int kLineSeg = 64;       // stored pixels of a segment
+constexpr int kLineSlots = 128;    // LDS pixel slots: segment + 2 S r (S r <= 16) + a tile
+struct LineFwdArgs {
+    Geom g;
+    int t0, S;                  // first line of this launch, lines per launch
+    int Cp, KX, KG, cx_mul;
+    const float *xp, *frag, *bias;
+    float *hd, *cell, *gates;
+    int nseg[kDirs];            // segments per line
+    int base[kDirs + 1];        // first workgroup of each direction
+};
+
+// LDS bytes of k_line_fwd beyond its static arrays: the launch's A fragments
+// and two lines of x.
+inline size_t line_fwd_dyn_lds(int KG, int Cp)
+{
+    return (size_t)KG * 4 * 64 * 16 + 2 * (size_t)kLineSlots * Cp * 4;
+}
+
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+k_line_fwd(LineFwdArgs a)
+{
+    constexpr int O = 16, G = 64;
+    __shared__ f4 hbuf[2][kLineSlots][4];   // h of the previous and current line
+    __shared__ f4 cbuf[kLineSlots][4];      // c (read and rewritten in place)
+    extern __shared__ f4 dyn[];
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int blk = blockIdx.x;
+    if (blk >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, blk);
+    const DirGeom dg = a.g.dir[d];
+    int r = blk - a.base[d];
+    const int n = r / a.nseg[d], seg = r - n * a.nseg[d];
+    const int Q = dg.Q, rq = a.g.KQ >> 1, S = a.S;
+    const int q0 = seg * kLineSeg;
+    const int pbase = q0 - S * rq;            // pixel of LDS slot 0
+    const int ss = (int)dg.ss, sq = (int)dg.sq;
+    const long long V = a.g.V;
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    const int Cp = a.Cp, CX = Cp >> 4, NXC = Cp >> 2, KX = a.KX, KG = a.KG;
+    const auto rs_x = slice_rsrc(a.xp + (long long)n * V * Cp, V * Cp);
+    const auto rs_h = slice_rsrc(a.hd + sbase * O, V * O);
+    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+    const int t0 = a.t0;
+    const int nlines = min(S, dg.T - t0);
+    f4 *afr = dyn;                                 // [KG][4 gates][64 lanes]
+    f4 *xbuf = dyn + KG * 256;                     // [2][kLineSlots][NXC], chunk ^ (slot & 3)
+
+    // x of line t (pixels pbase + slot) into buffer b: direct-to-LDS loads,
+    // 64 16-byte chunks per instruction; pixels past the line read zero
+    auto stage_x = [&](int t, int b) {
+        const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+        const int nch = kLineSlots * NXC;
+        for (int e0 = wave * 64; e0 < nch; e0 += 256) {
+            const int e = e0 + lane;
+            const int slot = e / NXC, pos = e - slot * NXC;
+            const int c = pos ^ (slot & 3);
+            const int qq = pbase + slot;
+            const bool ok = e < nch && (unsigned)qq < (unsigned)Q;
+            const unsigned off = sel_off(ok, (unsigned)(((s * ss + qq * sq) * Cp + 4 * c) * 4));
+            lds_void *dst = (lds_void *)&xbuf[(size_t)b * kLineSlots * NXC + e0];
+            if (e < nch) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_x, dst, 16, (int)off, 0, 0, 0);
+        }
+    };
+
+    // the launch's A fragments, h and c of line t0 - 1 over the widest range
+    // (zero before the first line and past the line's ends), x of line t0
+    {
+        const f4 *src = (const f4 *)(a.frag + (long long)d * KG * 1024);
+        for (int e = threadIdx.x; e < KG * 256; e += 256) afr[e] = src[e];
+        const int sprev = dg.sign > 0 ? t0 - 1 : dg.T - t0;
+        const int nsl = kLineSeg + 2 * S * rq;
+        for (int e = threadIdx.x; e < kLineSlots * 4; e += 256) {
+            const int slot = e >> 2, part = e & 3;
+            const int qq = pbase + slot;
+            const bool ok = t0 > 0 && slot < nsl && (unsigned)qq < (unsigned)Q;
+            const unsigned off = (unsigned)(((sprev * ss + qq * sq) * O + 4 * part) * 4);
+            hbuf[0][slot][part] = bload4(rs_h, sel_off(ok, off));
+            cbuf[slot][part] = bload4(rs_c, sel_off(ok, off));
+        }
+        stage_x(t0, 0);
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    }
+    __syncthreads();
+
+    for (int j = 0; j < nlines; ++j) {
+        const int t = t0 + j;
+        const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+        if (j + 1 < nlines) stage_x(t + 1, (j + 1) & 1);   // lands while this line computes
+        const int lo = (j + 1) * rq;                        // slot of the first computed pixel
+        const int W = kLineSeg + 2 * (S - 1 - j) * rq;      // computed pixels
+        const int ntl = (W + 15) >> 4;
+        const f4 (*hp)[4] = hbuf[j & 1];
+        f4 (*hc)[4] = hbuf[(j + 1) & 1];
+        const f4 *xb = xbuf + (size_t)(j & 1) * kLineSlots * NXC;
+        const int kgn = t > 0 ? KG : KX;
+        for (int i = wave; i < ntl; i += 4) {               // wave-uniform
+            const int slot = lo + 16 * i + col;
+            const int qq = pbase + slot;
+            const bool on = 16 * i + col < W && (unsigned)qq < (unsigned)Q;
+            f4 acc[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) acc[g] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int kg = 0; kg < kgn; ++kg) {
+                f4 bv;
+                if (kg < KX) {
+                    const int tap = (kg * a.cx_mul) >> 16, cb = kg - tap * CX;
+                    const int sx = slot + tap - rq;
+                    bv = xb[sx * NXC + ((cb * 4 + q4) ^ (sx & 3))];
+                } else {
+                    bv = hp[slot + (kg - KX) - rq][q4];
+                }
+                const f4 *ak = afr + kg * 256 + lane;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f4 av = ak[g * 64];
+#pragma unroll
+                    for (int i4 = 0; i4 < 4; ++i4) acc[g] = mfma(av[i4], bv[i4], acc[g]);
+                }
+            }
+            f4 gi, gf, gg, go, c, h;
+            const f4 cp = cbuf[slot][q4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                gi[u] = fsig(acc[0][u] + a.bias[d * G + 0 * O + 4 * q4 + u]);
+                gf[u] = fsig(acc[1][u] + a.bias[d * G + 1 * O + 4 * q4 + u]);
+                gg[u] = ftanh(acc[2][u] + a.bias[d * G + 2 * O + 4 * q4 + u]);
+                go[u] = fsig(acc[3][u] + a.bias[d * G + 3 * O + 4 * q4 + u]);
+                c[u] = gg[u] * gi[u] + (t > 0 ? cp[u] : 0.0f) * gf[u];
+                h[u] = go[u] * ftanh(c[u]);
+            }
+            const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+            cbuf[slot][q4] = on ? c : zero;
+            hc[slot][q4] = on ? h : zero;
+            if (on && qq >= q0 && qq < q0 + kLineSeg) {
+                const long long vo = sbase + s * ss + qq * sq;
+                *(f4 *)(a.cell + vo * O + 4 * q4) = c;
+                *(f4 *)(a.hd + vo * O + 4 * q4) = h;
+                if (a.gates) {
+                    float *gp = a.gates + vo * G + 4 * q4;
+                    *(f4 *)gp = gi;
+                    *(f4 *)(gp + O) = gf;
+                    *(f4 *)(gp + 2 * O) = gg;
+                    *(f4 *)(gp + 3 * O) = go;
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);            // next line's x has landed
+        __syncthreads();
     }
 }
 
@@ -1751,6 +1916,39 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     }
     PLSTM_LAUNCH_CHECK();
 
+    // 2D layers with 16 units: line blocks, S lines per launch (S r <= 16)
+    if (g.nd == 4 && g.KP == 1 && g.O == 16 && (g_step_split == 0 || g_step_split == 2) &&
+        line_fwd_dyn_lds(KG, Cp) <= 64 * 1024) {
+        LineFwdArgs la;
+        la.g = g;
+        const int rq = g.KQ / 2;
+        la.S = rq == 0 ? 16 : (16 / rq < 16 ? 16 / rq : 16);
+        la.Cp = Cp; la.KX = KX; la.KG = KG;
+        la.cx_mul = (65536 + Cp / 16 - 1) / (Cp / 16);
+        la.xp = xp; la.frag = frag; la.bias = bias;
+        la.hd = hd; la.cell = cell; la.gates = gates;
+        for (int d = 0; d < kDirs; ++d) la.nseg[d] = (g.dir[d].Q + kLineSeg - 1) / kLineSeg;
+        const int T = max_T(g);
+        const size_t dyn = line_fwd_dyn_lds(KG, Cp);
+        if (hipFuncSetAttribute((const void *)k_line_fwd, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)dyn) != hipSuccess)
+            return PLSTM_EHIP;
+        int launches = 0;
+        for (int t0 = 0; t0 < T; t0 += la.S) {
+            la.t0 = t0;
+            int nb = 0;
+            for (int d = 0; d < kDirs; ++d) {
+                la.base[d] = nb;
+                if (t0 < g.dir[d].T) nb += g.N * la.nseg[d];
+            }
+            la.base[kDirs] = nb;
+            k_line_fwd<<<nb, 256, dyn, st>>>(la);
+            PLSTM_LAUNCH_CHECK();
+            ++launches;
+        }
+        timing_end(2 + launches, st);
+        return PLSTM_OK;
+    }
     FwdStepArgs a;
     a.g = g;
     a.Cp = Cp; a.KX = KX; a.KG = KG;

@@ -550,22 +550,52 @@ k_step_fwd_blk(FwdStepArgs a)
 // segment itself is stored.  The widened pixels are the neighbours' own
 // pixels, recomputed.  Pixels past the line keep h = 0 (zero padding).
 constexpr int kLineSeg = 64;       // stored pixels of a segment
-constexpr int kLineSlots = 128;    // LDS pixel slots: segment + 2 S r (S r <= 16) + a tile
+constexpr int kLineSlots = 112;    // LDS pixel slots: segment + 2 S r (S r <= 16) + a tile
 struct LineFwdArgs {
     Geom g;
     int t0, S;                  // first line of this launch, lines per launch
-    int Cp, KX, KG, cx_mul;
+    int Cp, KX, KG;             // padded channels; K-groups of the taps of x (dense), all
+    int c_mul;                  // ceil(2^16 / C): (tap, channel) of a dense K index
     const float *xp, *frag, *bias;
     float *hd, *cell, *gates;
     int nseg[kDirs];            // segments per line
     int base[kDirs + 1];        // first workgroup of each direction
 };
 
-// LDS bytes of k_line_fwd beyond its static arrays: the launch's A fragments
-// and two lines of x.
-inline size_t line_fwd_dyn_lds(int KG, int Cp)
+// A fragments of k_line_fwd, frag[d][kg][gate][lane][4] (16 units): the input
+// taps packed densely, K index kk = 16 kg + 4 q + i of the first KX groups
+// being (tap, channel) = (kk / C, kk % C) (zero past K C); then one group per
+// recurrent tap.  Entry i of lane (q, col) weighs gate-unit gate*16 + col.
+template <typename TS>
+__global__ void __launch_bounds__(256)
+k_pack_line(int nd, int C, int KQ, int KX, int KG, const TS *__restrict__ wx,
+            const TS *__restrict__ wh, const TS *__restrict__ b, float *__restrict__ frag,
+            float *__restrict__ bias)
 {
-    return (size_t)KG * 4 * 64 * 16 + 2 * (size_t)kLineSlots * Cp * 4;
+    constexpr int O = 16, G = 64;
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i < (long long)nd * G) bias[i] = Store<TS>::load(b, i);
+    if (i >= (long long)nd * KG * 1024) return;
+    const int i4 = (int)(i & 3), lane = (int)((i >> 2) & 63), gate = (int)((i >> 8) & 3);
+    const long long r = i >> 10;
+    const int kg = (int)(r % KG), d = (int)(r / KG);
+    const int q = lane >> 4, col = lane & 15;
+    const long long gu = (long long)d * G + gate * O + col;
+    float v = 0.0f;
+    if (kg < KX) {
+        const int kk = 16 * kg + 4 * q + i4;
+        if (kk < KQ * C) v = Store<TS>::load(wx, (gu * C + kk % C) * KQ + kk / C);
+    } else {
+        v = Store<TS>::load(wh, (gu * O + 4 * q + i4) * KQ + (kg - KX));
+    }
+    frag[i] = v;
+}
+
+// LDS bytes of k_line_fwd beyond its static arrays: the launch's A fragments
+// and two lines of x (C floats per pixel).
+inline size_t line_fwd_dyn_lds(int KG, int C)
+{
+    return (size_t)KG * 4 * 64 * 16 + 2 * (size_t)kLineSlots * C * 4;
 }
 
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
@@ -589,29 +619,29 @@ k_line_fwd(LineFwdArgs a)
     const int ss = (int)dg.ss, sq = (int)dg.sq;
     const long long V = a.g.V;
     const long long sbase = ((long long)d * a.g.N + n) * V;
-    const int Cp = a.Cp, CX = Cp >> 4, NXC = Cp >> 2, KX = a.KX, KG = a.KG;
+    const int C = a.g.C, Cp = a.Cp, KX = a.KX, KG = a.KG, KC = a.g.KQ * C;
     const auto rs_x = slice_rsrc(a.xp + (long long)n * V * Cp, V * Cp);
     const auto rs_h = slice_rsrc(a.hd + sbase * O, V * O);
     const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
     const int t0 = a.t0;
     const int nlines = min(S, dg.T - t0);
     f4 *afr = dyn;                                 // [KG][4 gates][64 lanes]
-    f4 *xbuf = dyn + KG * 256;                     // [2][kLineSlots][NXC], chunk ^ (slot & 3)
+    float *xbuf = (float *)(dyn + KG * 256);       // [2][kLineSlots][C]
 
-    // x of line t (pixels pbase + slot) into buffer b: direct-to-LDS loads,
-    // 64 16-byte chunks per instruction; pixels past the line read zero
+    // x of line t (pixels pbase + slot, C channels) into buffer b: 4-byte
+    // direct-to-LDS loads, 64 floats per instruction; pixels past the line
+    // read zero
     auto stage_x = [&](int t, int b) {
         const int s = dg.sign > 0 ? t : dg.T - 1 - t;
-        const int nch = kLineSlots * NXC;
-        for (int e0 = wave * 64; e0 < nch; e0 += 256) {
+        const int nel = kLineSlots * C;
+        for (int e0 = wave * 64; e0 < nel; e0 += 256) {
             const int e = e0 + lane;
-            const int slot = e / NXC, pos = e - slot * NXC;
-            const int c = pos ^ (slot & 3);
+            const int slot = e / C, c = e - slot * C;
             const int qq = pbase + slot;
-            const bool ok = e < nch && (unsigned)qq < (unsigned)Q;
-            const unsigned off = sel_off(ok, (unsigned)(((s * ss + qq * sq) * Cp + 4 * c) * 4));
-            lds_void *dst = (lds_void *)&xbuf[(size_t)b * kLineSlots * NXC + e0];
-            if (e < nch) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_x, dst, 16, (int)off, 0, 0, 0);
+            const bool ok = e < nel && (unsigned)qq < (unsigned)Q;
+            const unsigned off = sel_off(ok, (unsigned)(((s * ss + qq * sq) * Cp + c) * 4));
+            lds_void *dst = (lds_void *)&xbuf[(size_t)b * kLineSlots * C + e0];
+            if (e < nel) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_x, dst, 4, (int)off, 0, 0, 0);
         }
     };
 
@@ -644,7 +674,7 @@ k_line_fwd(LineFwdArgs a)
         const int ntl = (W + 15) >> 4;
         const f4 (*hp)[4] = hbuf[j & 1];
         f4 (*hc)[4] = hbuf[(j + 1) & 1];
-        const f4 *xb = xbuf + (size_t)(j & 1) * kLineSlots * NXC;
+        const float *xb = xbuf + (size_t)(j & 1) * kLineSlots * C;
         const int kgn = t > 0 ? KG : KX;
         for (int i = wave; i < ntl; i += 4) {               // wave-uniform
             const int slot = lo + 16 * i + col;
@@ -656,9 +686,16 @@ k_line_fwd(LineFwdArgs a)
             for (int kg = 0; kg < kgn; ++kg) {
                 f4 bv;
                 if (kg < KX) {
-                    const int tap = (kg * a.cx_mul) >> 16, cb = kg - tap * CX;
-                    const int sx = slot + tap - rq;
-                    bv = xb[sx * NXC + ((cb * 4 + q4) ^ (sx & 3))];
+                    // dense (tap, channel) K indices of this lane's four k-steps
+#pragma unroll
+                    for (int i4 = 0; i4 < 4; ++i4) {
+                        const int kk = 16 * kg + 4 * q4 + i4;
+                        const bool real = kk < KC;          // padding reads tap 0, channel 0
+                        const int tap = real ? (kk * a.c_mul) >> 16 : 0;
+                        const int c = real ? kk - tap * C : 0;
+                        const float xv = xb[(slot + tap - rq) * C + c];
+                        bv[i4] = real ? xv : 0.0f;
+                    }
                 } else {
                     bv = hp[slot + (kg - KX) - rq][q4];
                 }
@@ -1898,38 +1935,40 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     const long long nfrag = (long long)g.nd * U * KG * 1024;
 
     timing_begin("sweep_fwd_step", st);
-    if (dtype == PLSTM_BF16) {
+    if (dtype == PLSTM_BF16)
         k_pad_x<uint16_t><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
                                                                       (const uint16_t *)x, xp);
-        PLSTM_LAUNCH_CHECK();
-        k_pack_fwd<uint16_t><<<blocks_for(nfrag, 256), 256, 0, st>>>(
-            g.nd, g.O, g.C, Cp, KX, KG, KK, (const uint16_t *)wx, (const uint16_t *)wh,
-            (const uint16_t *)b, frag, bias);
-    } else {
+    else
         k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
                                                                    (const float *)x, xp);
-        PLSTM_LAUNCH_CHECK();
-        k_pack_fwd<float><<<blocks_for(nfrag, 256), 256, 0, st>>>(
-            g.nd, g.O, g.C, Cp, KX, KG, KK, (const float *)wx, (const float *)wh, (const float *)b,
-            frag,
-            bias);
-    }
     PLSTM_LAUNCH_CHECK();
 
-    // 2D layers with 16 units: line blocks, S lines per launch (S r <= 16)
+    // 2D layers with 16 units: line blocks, S lines per launch (S r <= 16),
+    // the input taps packed densely as (tap, channel) pairs
+    const int KXL = (g.KQ * g.C + 15) / 16, KGL = KXL + g.KQ;
     if (g.nd == 4 && g.KP == 1 && g.O == 16 && (g_step_split == 0 || g_step_split == 2) &&
-        line_fwd_dyn_lds(KG, Cp) <= 64 * 1024) {
+        line_fwd_dyn_lds(KGL, g.C) <= 64 * 1024) {
+        const long long nfl = (long long)g.nd * KGL * 1024;
+        if (dtype == PLSTM_BF16)
+            k_pack_line<uint16_t><<<blocks_for(nfl, 256), 256, 0, st>>>(
+                g.nd, g.C, g.KQ, KXL, KGL, (const uint16_t *)wx, (const uint16_t *)wh,
+                (const uint16_t *)b, frag, bias);
+        else
+            k_pack_line<float><<<blocks_for(nfl, 256), 256, 0, st>>>(
+                g.nd, g.C, g.KQ, KXL, KGL, (const float *)wx, (const float *)wh,
+                (const float *)b, frag, bias);
+        PLSTM_LAUNCH_CHECK();
         LineFwdArgs la;
         la.g = g;
         const int rq = g.KQ / 2;
         la.S = rq == 0 ? 16 : (16 / rq < 16 ? 16 / rq : 16);
-        la.Cp = Cp; la.KX = KX; la.KG = KG;
-        la.cx_mul = (65536 + Cp / 16 - 1) / (Cp / 16);
+        la.Cp = Cp; la.KX = KXL; la.KG = KGL;
+        la.c_mul = (65536 + g.C - 1) / g.C;
         la.xp = xp; la.frag = frag; la.bias = bias;
         la.hd = hd; la.cell = cell; la.gates = gates;
         for (int d = 0; d < kDirs; ++d) la.nseg[d] = (g.dir[d].Q + kLineSeg - 1) / kLineSeg;
         const int T = max_T(g);
-        const size_t dyn = line_fwd_dyn_lds(KG, Cp);
+        const size_t dyn = line_fwd_dyn_lds(KGL, g.C);
         if (hipFuncSetAttribute((const void *)k_line_fwd, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)dyn) != hipSuccess)
             return PLSTM_EHIP;
@@ -1949,6 +1988,16 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
         timing_end(2 + launches, st);
         return PLSTM_OK;
     }
+
+    if (dtype == PLSTM_BF16)
+        k_pack_fwd<uint16_t><<<blocks_for(nfrag, 256), 256, 0, st>>>(
+            g.nd, g.O, g.C, Cp, KX, KG, KK, (const uint16_t *)wx, (const uint16_t *)wh,
+            (const uint16_t *)b, frag, bias);
+    else
+        k_pack_fwd<float><<<blocks_for(nfrag, 256), 256, 0, st>>>(
+            g.nd, g.O, g.C, Cp, KX, KG, KK, (const float *)wx, (const float *)wh, (const float *)b,
+            frag, bias);
+    PLSTM_LAUNCH_CHECK();
     FwdStepArgs a;
     a.g = g;
     a.Cp = Cp; a.KX = KX; a.KG = KG;

@@ -21,7 +21,11 @@ pytestmark = pytest.mark.gpu
 # filters of 1, 3, 5 and 7 taps, channel counts below and above a 16-block.
 SHAPES = [(1, 5, 6, 2, 16, 3), (2, 17, 33, 3, 16, 3), (1, 9, 70, 5, 32, 7),
           (1, 40, 3, 20, 64, 5), (1, 1, 1, 1, 16, 3), (1, 13, 1, 2, 16, 1),
-          (2, 8, 11, 3, 8, 3), (1, 64, 65, 3, 16, 3), (1, 21, 130, 45, 64, 7)]
+          (2, 8, 11, 3, 8, 3), (1, 64, 65, 3, 16, 3), (1, 21, 130, 45, 64, 7),
+          # 16 units (line blocks): several dense (tap, channel) K-groups, lines
+          # longer than a segment and ragged, the widest filter
+          (1, 9, 70, 5, 16, 7), (2, 12, 40, 20, 16, 5), (1, 30, 150, 17, 16, 3),
+          (1, 40, 129, 1, 16, 1)]
 
 
 def ident(s):

@@ -1285,16 +1285,18 @@ k_step_bwd(BwdStepArgs a)
 constexpr int kWgN = 4;          // most N-tiles a wave holds
 constexpr int kWgMaxChunks = 512;
 
-// N-tiles per block: each part (KK U tiles of h, KK C'/16 tiles of x) is cut
-// into the fewest blocks of at most kWgN tiles, as even as possible.
+// N-tiles per block: each part (KK U tiles of h; ceil(KK C / 16) tiles of x,
+// whose columns are the (tap, channel) pairs packed densely) is cut into the
+// fewest blocks of at most kWgN tiles, as even as possible.
 struct WgBlocks {
     int nh, nx;       // blocks of each part
     int th, tx;       // tiles per block of each part (the last block may have fewer)
 };
-__host__ __device__ inline WgBlocks wg_blocks(int U, int CX, int KK)
+__host__ __device__ inline int wg_xtiles(int KK, int C) { return (KK * C + 15) / 16; }
+__host__ __device__ inline WgBlocks wg_blocks(int U, int XT, int KK)
 {
     WgBlocks w;
-    const int h = KK * U, x = KK * CX;
+    const int h = KK * U, x = XT;
     w.nh = (h + kWgN - 1) / kWgN;
     w.nx = (x + kWgN - 1) / kWgN;
     w.th = (h + w.nh - 1) / w.nh;
@@ -1324,24 +1326,26 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
     const int P = dg.P, Q = dg.Q;
     const long long V = a.g.V;
-    const int Cp = a.Cp, CX = Cp >> 4;
+    const int Cp = a.Cp, C = a.g.C;
     const int ngrp = (Q + 15) >> 4;
-    const int cbn = is_h ? U : CX;              // channel blocks per tap
     const int stride = is_h ? O : Cp;           // floats per voxel of the source
 
-    // per tile: tap offset in the slice (uniform), tap row and column
-    // (packed, uniform) and this lane's channel (-1: a tile past the part)
+    // per tile and lane: tap offset in the slice, tap row and column (packed)
+    // and channel (-1: a column past the part).  An h tile is one tap and 16
+    // channels (uniform tap); an x tile is 16 (tap, channel) pairs, column
+    // kk = 16 tt + col being tap kk / C, channel kk % C.
     int dtap[NTL], chn[NTL];
     unsigned tapok[NTL];
 #pragma unroll
     for (int j = 0; j < NTL; ++j) {
         const int tt = t0 + j;
-        const bool real = j < ntl;
-        const int tap = real ? tt / cbn : radp * KQ + radq;
+        const int kk = tt * 16 + col;
+        const bool real = j < ntl && (is_h || kk < KK * C);
+        const int tap = !real ? radp * KQ + radq : (is_h ? tt / U : kk / C);
         const int ka = tap / KQ, kb = tap % KQ;
-        dtap[j] = __builtin_amdgcn_readfirstlane((ka - radp) * sp + (kb - radq) * sq);
-        tapok[j] = __builtin_amdgcn_readfirstlane(ka | kb << 3);
-        chn[j] = real ? (tt % cbn) * 16 + col : -1;
+        dtap[j] = (ka - radp) * sp + (kb - radq) * sq;
+        tapok[j] = ka | kb << 3;
+        chn[j] = !real ? -1 : (is_h ? (tt % U) * 16 + col : kk % C);
     }
 
     f4 acc[4][NTL];
@@ -1448,9 +1452,8 @@ __global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(2
 k_wgrad_step(WgStepArgs a)
 {
     const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int Cp = a.Cp, CX = Cp >> 4;
-    const int KK = a.g.KP * a.g.KQ;
-    const WgBlocks wb = wg_blocks(U, CX, KK);
+    const int KK = a.g.KP * a.g.KQ, XT = wg_xtiles(KK, a.g.C);
+    const WgBlocks wb = wg_blocks(U, XT, KK);
     const int nblk = wb.nh + wb.nx;
     const int per_dir = U * nblk * a.kch;
     if (item >= a.g.nd * per_dir) return;
@@ -1463,7 +1466,7 @@ k_wgrad_step(WgStepArgs a)
     // first N-tile and tile count of this block; x tiles numbered after h's
     const int tb = is_h ? wb.th : wb.tx;
     const int t0 = is_h ? nb * wb.th : (nb - wb.nh) * wb.tx;
-    const int tend = is_h ? KK * U : KK * CX;
+    const int tend = is_h ? KK * U : XT;
     const int ntl = t0 + tb < tend ? tb : tend - t0;
     const int first_nt = (is_h ? 0 : KK * U) + t0;
     if constexpr (kWgN <= 4) {
@@ -1512,20 +1515,20 @@ k_wgrad_step_reduce(int nd, int O, int C, int Cp, int KK, int NTt, int kch,
                     const float *__restrict__ partial, float *__restrict__ dwx,
                     float *__restrict__ dwh)
 {
-    const int G = 4 * O, KC = KK * (O + Cp), KCp = NTt * 16;
+    // columns: KK O of h (tap-major), then KK C of x ((tap, channel) dense)
+    const int G = 4 * O, KC = KK * (O + C), KCp = NTt * 16;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
     if (i >= (long long)nd * G * KC) return;
     const int k = (int)(i % KC);
     const int gu = (int)((i / KC) % G);
     const int d = (int)(i / ((long long)KC * G));
-    if (k >= KK * O && (k - KK * O) % Cp >= C) return;   // padding channel
     float acc = 0.0f;
     for (int c = 0; c < kch; ++c) acc += partial[(((long long)d * kch + c) * G + gu) * KCp + k];
     if (k < KK * O) {
         dwh[(((long long)d * G + gu) * O + k % O) * KK + k / O] = acc;
     } else {
         const int kx = k - KK * O;
-        dwx[(((long long)d * G + gu) * C + kx % Cp) * KK + kx / Cp] = acc;
+        dwx[(((long long)d * G + gu) * C + kx % C) * KK + kx / C] = acc;
     }
 }
 
@@ -1664,10 +1667,10 @@ struct WgShape {
 // the chunk count that minimises that (ties: fewer chunks).
 inline WgShape wg_shape(const Geom &g)
 {
-    const int U = g.O / 16, CX = pad16(g.C) / 16, KK = g.KP * g.KQ;
-    const WgBlocks wb = wg_blocks(U, CX, KK);
+    const int U = g.O / 16, KK = g.KP * g.KQ, XT = wg_xtiles(KK, g.C);
+    const WgBlocks wb = wg_blocks(U, XT, KK);
     WgShape w;
-    w.NTt = KK * U + KK * CX;
+    w.NTt = KK * U + XT;
     w.nblk = wb.nh + wb.nx;
     const DevInfo di = device_info();
     const long long simds = 4LL * (di.cus > 0 ? di.cus : 256);
@@ -2124,7 +2127,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     default: k_wgrad_step<4><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
     }
     PLSTM_LAUNCH_CHECK();
-    const long long nout = (long long)g.nd * G * KK * (g.O + Cp);
+    const long long nout = (long long)g.nd * G * KK * (g.O + g.C);
     k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.nd, g.O, g.C, Cp, KK, w.NTt,
                                                                w.kch, partial, dwx, dwh);
     PLSTM_LAUNCH_CHECK();

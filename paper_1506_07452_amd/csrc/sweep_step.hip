@@ -1662,9 +1662,10 @@ inline int max_T(const Geom &g)
 struct WgShape {
     int NTt, nblk, kch;
 };
-// Voxel chunks per (direction, block): one wave per SIMD at a time, so the
-// launch takes ceil(waves / SIMDs) rounds of 1/kch of a block's work; pick
-// the chunk count that minimises that (ties: fewer chunks).
+// Voxel chunks per (direction, block): the launch takes ceil(waves / slots)
+// rounds of 1/kch of a block's work; pick the chunk count that minimises that
+// (ties: fewer chunks).  Blocks of four N-tiles count one wave per SIMD;
+// blocks of fewer tiles do less MFMA work per load and are given four.
 inline WgShape wg_shape(const Geom &g)
 {
     const int U = g.O / 16, KK = g.KP * g.KQ, XT = wg_xtiles(KK, g.C);
@@ -1673,7 +1674,8 @@ inline WgShape wg_shape(const Geom &g)
     w.NTt = KK * U + XT;
     w.nblk = wb.nh + wb.nx;
     const DevInfo di = device_info();
-    const long long simds = 4LL * (di.cus > 0 ? di.cus : 256);
+    const int per_simd = (wb.th < kWgN && wb.tx < kWgN) ? 4 : 1;
+    const long long simds = 4LL * per_simd * (di.cus > 0 ? di.cus : 256);   // wave slots
     const long long per = (long long)g.nd * U * w.nblk;
     double best = 1e30;
     w.kch = 1;

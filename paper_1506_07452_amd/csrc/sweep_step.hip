@@ -1122,6 +1122,148 @@ struct BwdStepArgs {
     int base[kDirs + 1];
 };
 
+// ---- line blocks of the 2D layer's reverse sweep (16 hidden units) ----------
+// The reverse of k_line_fwd: a workgroup owns a 64-pixel segment and goes
+// back S lines per launch with overlapped tiles.  At reverse line j it
+// computes the segment widened by (S - 1 - j) r pixels on each side, which is
+// what line j + 1 reads: dA_{t+1} (double-buffered, 64 gate-units per pixel,
+// 16-byte chunks XOR-swizzled by the pixel) and gc_{t+1} f_{t+1} (in place)
+// stay in LDS; the saved gates, cell states and dL/dh are read per tile; only
+// the segment's own dA_t and gc_t f_t are stored.  Pixels past the line keep
+// dA = 0.
+//   gh = dL/dh + sum_taps W_h^T dA_{t+1}[p - tap]                 (MFMA)
+//   gc = gh o (1 - tanh^2 c) + (gc f)_{t+1}
+//   dA_i = gc g i (1 - i), dA_f = gc c_{t-1} f (1 - f), dA_g = gc i (1 - g^2),
+//   dA_o = gh tanh(c) o (1 - o)
+struct LineBwdArgs {
+    Geom g;
+    int r0, S;                  // first reverse step of this launch, steps per launch
+    const float *frag;          // [6][KK * 4][64][4] W_h^T fragments
+    const float *gates, *cell, *dh;
+    float *dA, *gcf;
+    int nseg[kDirs];
+    int base[kDirs + 1];
+};
+
+// LDS bytes of k_line_bwd beyond its static array: W_h^T fragments and two
+// lines of dA.
+inline size_t line_bwd_dyn_lds(int KG) { return (size_t)KG * 64 * 16 + 2 * (size_t)kLineSlots * 256; }
+
+__global__ void __launch_bounds__(256)
+k_line_bwd(LineBwdArgs a)
+{
+    constexpr int O = 16, G = 64;
+    __shared__ f4 gcb[kLineSlots][4];           // gc f, chunk ^ (slot & 3)
+    extern __shared__ f4 dyn[];
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int blk = blockIdx.x;
+    if (blk >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, blk);
+    const DirGeom dg = a.g.dir[d];
+    int r = blk - a.base[d];
+    const int n = r / a.nseg[d], seg = r - n * a.nseg[d];
+    const int Q = dg.Q, rq = a.g.KQ >> 1, S = a.S, KG = a.g.KQ * 4;
+    const int q0 = seg * kLineSeg;
+    const int pbase = q0 - S * rq;
+    const int ss = (int)dg.ss, sq = (int)dg.sq, T = dg.T;
+    const long long V = a.g.V;
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    const auto rs_dA = slice_rsrc(a.dA + sbase * G, V * G);
+    const auto rs_gcf = slice_rsrc(a.gcf + sbase * O, V * O);
+    const auto rs_g = slice_rsrc(a.gates + sbase * G, V * G);
+    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+    const auto rs_dh = slice_rsrc(a.dh + (long long)n * V * O, V * O);
+    const int r0 = a.r0;
+    const int nlines = min(S, T - r0);
+    const int noff = dg.sign * ss;             // plane t + 1 = plane t + noff
+    f4 *afr = dyn;                              // [KG][64 lanes]
+    f4 *dab = dyn + KG * 64;                    // [2][kLineSlots][16], chunk ^ (slot & 15)
+
+    // W_h^T fragments; dA and gc f of line t + 1 over the widest range (zero
+    // after the last line and past the line's ends)
+    {
+        const f4 *src = (const f4 *)(a.frag + (long long)d * KG * 256);
+        for (int e = threadIdx.x; e < KG * 64; e += 256) afr[e] = src[e];
+        const int tn = T - r0;                  // line t + 1 for t = T - 1 - r0
+        const int sn = dg.sign > 0 ? tn : T - 1 - tn;
+        const int nsl = kLineSeg + 2 * S * rq;
+        for (int e = threadIdx.x; e < kLineSlots * 16; e += 256) {
+            const int slot = e >> 4, ch = e & 15;
+            const int qq = pbase + slot;
+            const bool ok = r0 > 0 && slot < nsl && (unsigned)qq < (unsigned)Q;
+            const int v = sn * ss + qq * sq;
+            dab[slot * 16 + (ch ^ (slot & 15))] =
+                bload4(rs_dA, sel_off(ok, (unsigned)((v * G + 4 * ch) * 4)));
+            if (ch < 4)
+                gcb[slot][ch ^ (slot & 3)] = bload4(rs_gcf, sel_off(ok, (unsigned)((v * O + 4 * ch) * 4)));
+        }
+    }
+    __syncthreads();
+
+    for (int j = 0; j < nlines; ++j) {
+        const int t = T - 1 - (r0 + j);
+        const int s = dg.sign > 0 ? t : T - 1 - t;
+        const bool has_next = t + 1 < T;
+        const int lo = (j + 1) * rq;
+        const int W = kLineSeg + 2 * (S - 1 - j) * rq;
+        const int ntl = (W + 15) >> 4;
+        const f4 *dp = dab + (size_t)(j & 1) * kLineSlots * 16;         // dA_{t+1}
+        f4 *dc = dab + (size_t)((j + 1) & 1) * kLineSlots * 16;         // dA_t
+        for (int i = wave; i < ntl; i += 4) {
+            const int slot = lo + 16 * i + col;
+            const int qq = pbase + slot;
+            const bool on = 16 * i + col < W && (unsigned)qq < (unsigned)Q;
+            const int vox = s * ss + (on ? qq : 0) * sq;
+            // epilogue operands in flight during the contraction
+            f4 gv[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                gv[g] = bload4(rs_g, sel_off(on, (unsigned)((vox * G + g * O + 4 * q4) * 4)));
+            const f4 c = bload4(rs_c, sel_off(on, (unsigned)((vox * O + 4 * q4) * 4)));
+            const f4 cp = bload4(rs_c, sel_off(on && t > 0, (unsigned)(((vox - noff) * O + 4 * q4) * 4)));
+            const f4 dhv = bload4(rs_dh, sel_off(on, (unsigned)((vox * O + 4 * q4) * 4)));
+            f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (has_next) {
+                for (int kg = 0; kg < KG; ++kg) {
+                    const int tap = kg >> 2, mb = kg & 3;
+                    const int sx = slot - (tap - rq);
+                    const f4 bv = dp[sx * 16 + ((mb * 4 + q4) ^ (sx & 15))];
+                    const f4 av = afr[kg * 64 + lane];
+#pragma unroll
+                    for (int i4 = 0; i4 < 4; ++i4) acc = mfma(av[i4], bv[i4], acc);
+                }
+            }
+            const int gsw = q4 ^ (slot & 3);
+            const f4 gn = has_next ? gcb[slot][gsw] : f4{0.0f, 0.0f, 0.0f, 0.0f};
+            f4 dv[4], gco;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const float gi = gv[0][u], gf = gv[1][u], gg = gv[2][u], go = gv[3][u];
+                const float gh = acc[u] + dhv[u];
+                const float tc = ftanh(c[u]);
+                const float gc = gh * go * (1.0f - tc * tc) + gn[u];
+                dv[0][u] = gc * gg * gi * (1.0f - gi);
+                dv[1][u] = gc * (t > 0 ? cp[u] : 0.0f) * gf * (1.0f - gf);
+                dv[2][u] = gc * gi * (1.0f - gg * gg);
+                dv[3][u] = gh * tc * go * (1.0f - go);
+                gco[u] = gc * gf;
+            }
+            const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int g = 0; g < 4; ++g) dc[slot * 16 + ((g * 4 + q4) ^ (slot & 15))] = on ? dv[g] : zero;
+            gcb[slot][gsw] = on ? gco : zero;
+            if (on && qq >= q0 && qq < q0 + kLineSeg) {
+                const long long vo = sbase + vox;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) *(f4 *)(a.dA + vo * G + g * O + 4 * q4) = dv[g];
+                *(f4 *)(a.gcf + vo * O + 4 * q4) = gco;
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // Every unit group of kNT 16-pixel tiles of one plane (an item); the two
 // launch shapes of the forward step (SPLIT: one item per workgroup, K split
 // over its waves, wave w finishes tile w; !SPLIT: one item per wave).
@@ -2096,21 +2238,53 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     k_pack_bwd<<<blocks_for((long long)g.nd * U * KK * 4 * U * 256, 256), 256, 0, st>>>(
         g.nd, g.O, KK, wh, frag);
     PLSTM_LAUNCH_CHECK();
-    BwdStepArgs a;
-    a.g = g;
-    a.frag = frag;
-    a.k_mul = k_mul_of(g);
-    a.gates = sv.gates; a.cell = sv.cell; a.dh = dh;
-    a.dA = dA; a.gcf = gcf;
-    for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
-    int rc;
-    switch (U) {
-    case 1: rc = launch_bwd_steps<1>(g, a, st); break;
-    case 2: rc = launch_bwd_steps<2>(g, a, st); break;
-    default: rc = launch_bwd_steps<4>(g, a, st); break;
+    if (g.nd == 4 && g.KP == 1 && g.O == 16 && (g_step_split == 0 || g_step_split == 2) &&
+        line_bwd_dyn_lds(g.KQ * 4) + kLineSlots * 64 <= (size_t)device_info().max_lds) {
+        // 2D layers with 16 units: line blocks, S lines per launch (S r <= 16)
+        LineBwdArgs la;
+        la.g = g;
+        const int rq = g.KQ / 2;
+        la.S = rq == 0 ? 16 : (16 / rq < 16 ? 16 / rq : 16);
+        la.frag = frag;
+        la.gates = sv.gates; la.cell = sv.cell; la.dh = dh;
+        la.dA = dA; la.gcf = gcf;
+        for (int d = 0; d < kDirs; ++d) la.nseg[d] = (g.dir[d].Q + kLineSeg - 1) / kLineSeg;
+        const size_t dyn = line_bwd_dyn_lds(g.KQ * 4);
+        if (hipFuncSetAttribute((const void *)k_line_bwd, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)dyn) != hipSuccess)
+            return PLSTM_EHIP;
+        const int T = max_T(g);
+        int launches = 0;
+        for (int r0 = 0; r0 < T; r0 += la.S) {
+            la.r0 = r0;
+            int nb = 0;
+            for (int d = 0; d < kDirs; ++d) {
+                la.base[d] = nb;
+                if (r0 < g.dir[d].T) nb += g.N * la.nseg[d];
+            }
+            la.base[kDirs] = nb;
+            k_line_bwd<<<nb, 256, dyn, st>>>(la);
+            PLSTM_LAUNCH_CHECK();
+            ++launches;
+        }
+        timing_end(1 + launches, st);
+    } else {
+        BwdStepArgs a;
+        a.g = g;
+        a.frag = frag;
+        a.k_mul = k_mul_of(g);
+        a.gates = sv.gates; a.cell = sv.cell; a.dh = dh;
+        a.dA = dA; a.gcf = gcf;
+        for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
+        int rc;
+        switch (U) {
+        case 1: rc = launch_bwd_steps<1>(g, a, st); break;
+        case 2: rc = launch_bwd_steps<2>(g, a, st); break;
+        default: rc = launch_bwd_steps<4>(g, a, st); break;
+        }
+        if (rc != PLSTM_OK) return rc;
+        timing_end(1 + max_T(g), st);
     }
-    if (rc != PLSTM_OK) return rc;
-    timing_end(1 + max_T(g), st);
 
     timing_begin("wgrad_step", st);
     k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp, x, xp);

@@ -1126,9 +1126,9 @@ struct BwdStepArgs {
 // The reverse of k_line_fwd: a workgroup owns a 64-pixel segment and goes
 // back S lines per launch with overlapped tiles.  At reverse line j it
 // computes the segment widened by (S - 1 - j) r pixels on each side, which is
-// what line j + 1 reads: dA_{t+1} (double-buffered, 64 gate-units per pixel,
-// 16-byte chunks XOR-swizzled by the pixel) and gc_{t+1} f_{t+1} (in place)
-// stay in LDS; the saved gates, cell states and dL/dh are read per tile; only
+// what line j + 1 reads: dA_{t+1} (64 gate-units per pixel, 16-byte chunks
+// XOR-swizzled by the pixel; overwritten after a barrier) and gc_{t+1} f_{t+1}
+// (in place) stay in LDS; the saved gates, cell states and dL/dh are read per tile; only
 // the segment's own dA_t and gc_t f_t are stored.  Pixels past the line keep
 // dA = 0.
 //   gh = dL/dh + sum_taps W_h^T dA_{t+1}[p - tap]                 (MFMA)
@@ -1145,9 +1145,9 @@ struct LineBwdArgs {
     int base[kDirs + 1];
 };
 
-// LDS bytes of k_line_bwd beyond its static array: W_h^T fragments and two
-// lines of dA.
-inline size_t line_bwd_dyn_lds(int KG) { return (size_t)KG * 64 * 16 + 2 * (size_t)kLineSlots * 256; }
+// LDS bytes of k_line_bwd beyond its static array: W_h^T fragments and one
+// line of dA.
+inline size_t line_bwd_dyn_lds(int KG) { return (size_t)KG * 64 * 16 + (size_t)kLineSlots * 256; }
 
 __global__ void __launch_bounds__(256)
 k_line_bwd(LineBwdArgs a)
@@ -1178,7 +1178,7 @@ k_line_bwd(LineBwdArgs a)
     const int nlines = min(S, T - r0);
     const int noff = dg.sign * ss;             // plane t + 1 = plane t + noff
     f4 *afr = dyn;                              // [KG][64 lanes]
-    f4 *dab = dyn + KG * 64;                    // [2][kLineSlots][16], chunk ^ (slot & 15)
+    f4 *dab = dyn + KG * 64;                    // [kLineSlots][16], chunk ^ (slot & 15)
 
     // W_h^T fragments; dA and gc f of line t + 1 over the widest range (zero
     // after the last line and past the line's ends)
@@ -1201,19 +1201,27 @@ k_line_bwd(LineBwdArgs a)
     }
     __syncthreads();
 
+    const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int j = 0; j < nlines; ++j) {
         const int t = T - 1 - (r0 + j);
         const int s = dg.sign > 0 ? t : T - 1 - t;
         const bool has_next = t + 1 < T;
         const int lo = (j + 1) * rq;
         const int W = kLineSeg + 2 * (S - 1 - j) * rq;
-        const int ntl = (W + 15) >> 4;
-        const f4 *dp = dab + (size_t)(j & 1) * kLineSlots * 16;         // dA_{t+1}
-        f4 *dc = dab + (size_t)((j + 1) & 1) * kLineSlots * 16;         // dA_t
-        for (int i = wave; i < ntl; i += 4) {
+        const int ntl = (W + 15) >> 4;          // at most 6: two tiles per wave
+        // dA_t is held in registers until every wave has read dA_{t+1} from
+        // the one LDS buffer
+        f4 dv[2][4];
+        bool onv[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int i = wave + 4 * k;
+            onv[k] = false;
+            if (i >= ntl) continue;             // wave-uniform
             const int slot = lo + 16 * i + col;
             const int qq = pbase + slot;
             const bool on = 16 * i + col < W && (unsigned)qq < (unsigned)Q;
+            onv[k] = on;
             const int vox = s * ss + (on ? qq : 0) * sq;
             // epilogue operands in flight during the contraction
             f4 gv[4];
@@ -1223,42 +1231,49 @@ k_line_bwd(LineBwdArgs a)
             const f4 c = bload4(rs_c, sel_off(on, (unsigned)((vox * O + 4 * q4) * 4)));
             const f4 cp = bload4(rs_c, sel_off(on && t > 0, (unsigned)(((vox - noff) * O + 4 * q4) * 4)));
             const f4 dhv = bload4(rs_dh, sel_off(on, (unsigned)((vox * O + 4 * q4) * 4)));
-            f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            f4 acc = zero;
             if (has_next) {
                 for (int kg = 0; kg < KG; ++kg) {
                     const int tap = kg >> 2, mb = kg & 3;
                     const int sx = slot - (tap - rq);
-                    const f4 bv = dp[sx * 16 + ((mb * 4 + q4) ^ (sx & 15))];
+                    const f4 bv = dab[sx * 16 + ((mb * 4 + q4) ^ (sx & 15))];
                     const f4 av = afr[kg * 64 + lane];
 #pragma unroll
                     for (int i4 = 0; i4 < 4; ++i4) acc = mfma(av[i4], bv[i4], acc);
                 }
             }
+            // gc f is read and rewritten by its own lane only
             const int gsw = q4 ^ (slot & 3);
-            const f4 gn = has_next ? gcb[slot][gsw] : f4{0.0f, 0.0f, 0.0f, 0.0f};
-            f4 dv[4], gco;
+            const f4 gn = has_next ? gcb[slot][gsw] : zero;
+            f4 gco;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const float gi = gv[0][u], gf = gv[1][u], gg = gv[2][u], go = gv[3][u];
                 const float gh = acc[u] + dhv[u];
                 const float tc = ftanh(c[u]);
                 const float gc = gh * go * (1.0f - tc * tc) + gn[u];
-                dv[0][u] = gc * gg * gi * (1.0f - gi);
-                dv[1][u] = gc * (t > 0 ? cp[u] : 0.0f) * gf * (1.0f - gf);
-                dv[2][u] = gc * gi * (1.0f - gg * gg);
-                dv[3][u] = gh * tc * go * (1.0f - go);
+                dv[k][0][u] = gc * gg * gi * (1.0f - gi);
+                dv[k][1][u] = gc * (t > 0 ? cp[u] : 0.0f) * gf * (1.0f - gf);
+                dv[k][2][u] = gc * gi * (1.0f - gg * gg);
+                dv[k][3][u] = gh * tc * go * (1.0f - go);
                 gco[u] = gc * gf;
             }
-            const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int g = 0; g < 4; ++g) dc[slot * 16 + ((g * 4 + q4) ^ (slot & 15))] = on ? dv[g] : zero;
             gcb[slot][gsw] = on ? gco : zero;
             if (on && qq >= q0 && qq < q0 + kLineSeg) {
                 const long long vo = sbase + vox;
 #pragma unroll
-                for (int g = 0; g < 4; ++g) *(f4 *)(a.dA + vo * G + g * O + 4 * q4) = dv[g];
+                for (int g = 0; g < 4; ++g) *(f4 *)(a.dA + vo * G + g * O + 4 * q4) = dv[k][g];
                 *(f4 *)(a.gcf + vo * O + 4 * q4) = gco;
             }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int i = wave + 4 * k;
+            if (i >= ntl) continue;
+            const int slot = lo + 16 * i + col;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) dab[slot * 16 + ((g * 4 + q4) ^ (slot & 15))] = onv[k] ? dv[k][g] : zero;
         }
         __syncthreads();
     }
@@ -1560,19 +1575,33 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
         }
     };
     const long long total = u1 - u0;
-    Ops cur, nxt;
-    load(cu, total > 0, cur);
-    for (long long it = 0; it < total; ++it) {
-        advance();
-        load(cu, it + 1 < total, nxt);
+    auto step = [&](const Ops &o) {
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
             for (int m = 0; m < 4; ++m)
 #pragma unroll
                 for (int j = 0; j < NTL; ++j)
-                    acc[m][j] = mfma(cur.a[ks][m], cur.b[ks][j], acc[m][j]);
-        cur = nxt;
+                    acc[m][j] = mfma(o.a[ks][m], o.b[ks][j], acc[m][j]);
+    };
+    // two operand sets in ping-pong: each is reloaded only after its
+    // products, so no loaded register is copied (a copy would wait for the
+    // load just issued), and the loads of one set are all issued before the
+    // products of the other (a whole unit of MFMAs in flight behind them)
+    Ops o0, o1;
+    load(cu, total > 0, o0);
+    for (long long it = 0; it < total; it += 2) {
+        advance();
+        load(cu, it + 1 < total, o1);
+        __builtin_amdgcn_sched_barrier(0);
+        step(o0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (it + 1 >= total) break;
+        advance();
+        load(cu, it + 2 < total, o0);
+        __builtin_amdgcn_sched_barrier(0);
+        step(o1);
+        __builtin_amdgcn_sched_barrier(0);
     }
     const int KCp = a.NTt * 16;
     float *out = a.partial + ((long long)d * a.kch + kc) * G * KCp;
@@ -1612,7 +1641,15 @@ k_wgrad_step(WgStepArgs a)
     const int ntl = t0 + tb < tend ? tb : tend - t0;
     const int first_nt = (is_h ? 0 : KK * U) + t0;
     if constexpr (kWgN <= 4) {
-        wg_wave<U, 4>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        // as many products per unit as the block has tiles
+        if (ntl <= 1)
+            wg_wave<U, 1>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        else if (ntl <= 2)
+            wg_wave<U, 2>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        else if (ntl <= 3)
+            wg_wave<U, 3>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        else
+            wg_wave<U, 4>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
     } else {
         if (ntl <= 4)
             wg_wave<U, 4>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
@@ -1624,19 +1661,39 @@ k_wgrad_step(WgStepArgs a)
 }
 
 // db: column sums of dA over the voxels of each direction, in fixed chunks
-// (partials[d][chunk][4O]), then the chunks in order.
+// (partials[d][chunk][4O]), then the chunks in order.  A workgroup streams
+// its chunk with 16-byte loads: G / 4 lanes cover a row, 1024 / G rows at a
+// time, four rows in flight per lane; the row partials are summed in LDS in a
+// fixed order.
 constexpr int kDbChunks = 512;
 
 __global__ void __launch_bounds__(256)
 k_db_partial(int G, long long nvox, const float *__restrict__ dA, float *__restrict__ part)
 {
+    __shared__ f4 red[256];
     const int d = blockIdx.y, ch = blockIdx.x;
+    const int cols = G >> 2, R = 256 / cols;
+    const int cg = threadIdx.x % cols, r = threadIdx.x / cols;
     const long long v0 = nvox * ch / kDbChunks, v1 = nvox * (ch + 1) / kDbChunks;
-    const float *src = dA + (long long)d * nvox * G;
-    for (int m = threadIdx.x; m < G; m += 256) {
-        float acc = 0.0f;
-        for (long long v = v0; v < v1; ++v) acc += src[v * G + m];
-        part[((long long)d * kDbChunks + ch) * G + m] = acc;
+    const f4 *src = (const f4 *)(dA + (long long)d * nvox * G) + cg;
+    const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+    f4 a0 = zero, a1 = zero, a2 = zero, a3 = zero;
+    if (r < R) {
+        long long v = v0 + r;
+        for (; v + 3 * R < v1; v += 4 * R) {
+            a0 += src[v * cols];
+            a1 += src[(v + R) * cols];
+            a2 += src[(v + 2 * R) * cols];
+            a3 += src[(v + 3 * R) * cols];
+        }
+        for (; v < v1; v += R) a0 += src[v * cols];
+    }
+    red[threadIdx.x] = (a0 + a1) + (a2 + a3);
+    __syncthreads();
+    if (threadIdx.x < cols) {
+        f4 sum = red[threadIdx.x];
+        for (int k = 1; k < R; ++k) sum += red[k * cols + threadIdx.x];
+        *(f4 *)(part + ((long long)d * kDbChunks + ch) * G + 4 * threadIdx.x) = sum;
     }
 }
 
@@ -2245,6 +2302,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
         la.g = g;
         const int rq = g.KQ / 2;
         la.S = rq == 0 ? 16 : (16 / rq < 16 ? 16 / rq : 16);
+        if (kLineSeg + 2 * (la.S - 1) * rq > 96) return PLSTM_EUNSUPPORTED;   // two tiles per wave
         la.frag = frag;
         la.gates = sv.gates; la.cell = sv.cell; la.dh = dh;
         la.dA = dA; la.gcf = gcf;

@@ -1804,26 +1804,41 @@ k_dx_step(DxStepArgs a)
                 o.b[nt] = bload4(rs, sel_off(on_plane(tp[nt] - ka, tq[nt] - kb, P, Q),
                                              (unsigned)((vv[nt] + dv) * G + mb * 16 + 4 * q4) * 4u));
         };
-        Ops cur, nxt;
-        load(0, 0, cur);
-        int tap = 0, mb = 0;
-        for (int kg = 0; kg < KG; ++kg) {
-            int ntap = tap, nmb = mb + 1;
-            if (nmb == MB) {
-                nmb = 0;
-                ++ntap;
-            }
-            if (kg + 1 < KG) load(ntap, nmb, nxt);
+        auto step = [&](const Ops &o) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
                     for (int nt = 0; nt < kNT; ++nt)
-                        acc[ct][nt] = mfma(cur.a[ct][i], cur.b[nt][i], acc[ct][nt]);
-            cur = nxt;
-            tap = ntap;
-            mb = nmb;
+                        acc[ct][nt] = mfma(o.a[ct][i], o.b[nt][i], acc[ct][nt]);
+        };
+        auto next = [&](int &tap, int &mb) {
+            if (++mb == MB) {
+                mb = 0;
+                ++tap;
+            }
+        };
+        // two operand sets in ping-pong (KG is a multiple of 4): the loads of
+        // one are all issued before the products of the other, and no loaded
+        // register is copied
+        Ops o0, o1;
+        load(0, 0, o0);
+        int tap = 0, mb = 0;
+        for (int kg = 0; kg < KG; kg += 2) {
+            next(tap, mb);
+            load(tap, mb, o1);
+            __builtin_amdgcn_sched_barrier(0);
+            step(o0);
+            __builtin_amdgcn_sched_barrier(0);
+            next(tap, mb);
+            // unconditional (the last pass reloads k-group 0, unused) so that
+            // the products below wait for their own loads only
+            const bool more = kg + 2 < KG;
+            load(more ? tap : 0, more ? mb : 0, o0);
+            __builtin_amdgcn_sched_barrier(0);
+            step(o1);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 #pragma unroll

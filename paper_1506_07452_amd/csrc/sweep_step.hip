@@ -1135,25 +1135,67 @@ struct BwdStepArgs {
 //   gc = gh o (1 - tanh^2 c) + (gc f)_{t+1}
 //   dA_i = gc g i (1 - i), dA_f = gc c_{t-1} f (1 - f), dA_g = gc i (1 - g^2),
 //   dA_o = gh tanh(c) o (1 - o)
+// With dxd (C <= 4) the line also gives this direction's share of dL/dx,
+//   dxd[p] = sum_taps W_x^T dA_t[p - tap],
+// from dA_t in LDS: the computed range is one radius wider than the next
+// line needs, so the segment's taps are all there.  Wave w sums gate w's 16
+// units for the segment's 64 pixels; the four partials meet in LDS and are
+// added, in order, after the next barrier.
 struct LineBwdArgs {
     Geom g;
     int r0, S;                  // first reverse step of this launch, steps per launch
     const float *frag;          // [6][KK * 4][64][4] W_h^T fragments
     const float *gates, *cell, *dh;
     float *dA, *gcf;
+    const float *wx;            // [4][4O][C][K] input filters (dxd only)
+    float *dxd;                 // [4][N][V][C] per-direction dL/dx, or null
     int nseg[kDirs];
     int base[kDirs + 1];
 };
 
-// LDS bytes of k_line_bwd beyond its static array: W_h^T fragments and one
-// line of dA.
-inline size_t line_bwd_dyn_lds(int KG) { return (size_t)KG * 64 * 16 + (size_t)kLineSlots * 256; }
+// LDS bytes of k_line_bwd beyond its static arrays: W_h^T fragments, one line
+// of dA and, for dL/dx, the input filters.
+inline size_t line_bwd_dyn_lds(int KG, int wx_floats)
+{
+    return (size_t)KG * 64 * 16 + (size_t)kLineSlots * 256 + (size_t)(wx_floats + 3) / 4 * 16;
+}
+
+// One wave's share of a segment pixel's dL/dx in the reverse line blocks:
+// gate w's 16 units over the taps, CC channels.  dab: one line of dA (16
+// chunks of 4 gate-units per pixel, chunk ^ (slot & 15)); wxl: [K][4O][CC]
+// input filters (wave-uniform reads); cs: the pixel's slot.
+template <int CC>
+__device__ inline f4 line_dx_px(const f4 *dab, const float *wxl, int cs, int rq, int KQ, int wave)
+{
+    constexpr int G = 64;
+    f4 px = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int tap = 0; tap < KQ; ++tap) {
+        const int sx = cs - (tap - rq);
+        const f4 *wp = (const f4 *)(wxl + (tap * G + wave * 16) * CC);
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            const f4 v = dab[sx * 16 + ((wave * 4 + h) ^ (sx & 15))];
+            f4 w[CC];                       // units 4h .. 4h + 3, CC channels each
+#pragma unroll
+            for (int k = 0; k < CC; ++k) w[k] = wp[h * CC + k];
+#pragma unroll
+            for (int i4 = 0; i4 < 4; ++i4)
+#pragma unroll
+                for (int c = 0; c < CC; ++c) {
+                    const int e = i4 * CC + c;
+                    px[c] += v[i4] * w[e >> 2][e & 3];
+                }
+        }
+    }
+    return px;
+}
 
 __global__ void __launch_bounds__(256)
 k_line_bwd(LineBwdArgs a)
 {
     constexpr int O = 16, G = 64;
     __shared__ f4 gcb[kLineSlots][4];           // gc f, chunk ^ (slot & 3)
+    __shared__ f4 dxr[4][64];                   // dL/dx partials of the four waves
     extern __shared__ f4 dyn[];
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1165,10 +1207,12 @@ k_line_bwd(LineBwdArgs a)
     const int n = r / a.nseg[d], seg = r - n * a.nseg[d];
     const int Q = dg.Q, rq = a.g.KQ >> 1, S = a.S, KG = a.g.KQ * 4;
     const int q0 = seg * kLineSeg;
-    const int pbase = q0 - S * rq;
+    const int pbase = q0 - (S + 1) * rq;       // pixel of LDS slot 0
     const int ss = (int)dg.ss, sq = (int)dg.sq, T = dg.T;
     const long long V = a.g.V;
     const long long sbase = ((long long)d * a.g.N + n) * V;
+    const int C = a.g.C, KQ = a.g.KQ;
+    const bool want_dx = a.dxd != nullptr;
     const auto rs_dA = slice_rsrc(a.dA + sbase * G, V * G);
     const auto rs_gcf = slice_rsrc(a.gcf + sbase * O, V * O);
     const auto rs_g = slice_rsrc(a.gates + sbase * G, V * G);
@@ -1179,15 +1223,23 @@ k_line_bwd(LineBwdArgs a)
     const int noff = dg.sign * ss;             // plane t + 1 = plane t + noff
     f4 *afr = dyn;                              // [KG][64 lanes]
     f4 *dab = dyn + KG * 64;                    // [kLineSlots][16], chunk ^ (slot & 15)
+    float *wxl = (float *)(dab + kLineSlots * 16);  // [K][4O][C] input filters
 
-    // W_h^T fragments; dA and gc f of line t + 1 over the widest range (zero
-    // after the last line and past the line's ends)
+    // W_h^T fragments, the input filters; dA and gc f of line t + 1 over the
+    // widest range (zero after the last line and past the line's ends)
     {
         const f4 *src = (const f4 *)(a.frag + (long long)d * KG * 256);
         for (int e = threadIdx.x; e < KG * 64; e += 256) afr[e] = src[e];
+        if (want_dx) {
+            const int nw = KQ * G * C;
+            for (int e = threadIdx.x; e < nw; e += 256) {
+                const int tap = e / (G * C), mc = e - tap * (G * C);
+                wxl[e] = a.wx[((long long)d * G * C + mc) * KQ + tap];
+            }
+        }
         const int tn = T - r0;                  // line t + 1 for t = T - 1 - r0
         const int sn = dg.sign > 0 ? tn : T - 1 - tn;
-        const int nsl = kLineSeg + 2 * S * rq;
+        const int nsl = kLineSeg + 2 * (S + 1) * rq;
         for (int e = threadIdx.x; e < kLineSlots * 16; e += 256) {
             const int slot = e >> 4, ch = e & 15;
             const int qq = pbase + slot;
@@ -1202,12 +1254,24 @@ k_line_bwd(LineBwdArgs a)
     __syncthreads();
 
     const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+    // the segment's dL/dx of line s: the four waves' partials, added in order
+    auto store_dx = [&](int s) {
+        if (threadIdx.x < kLineSeg) {
+            const int p = threadIdx.x, qq = q0 + p;
+            if (qq < Q) {
+                const f4 v = ((dxr[0][p] + dxr[1][p]) + dxr[2][p]) + dxr[3][p];
+                float *out = a.dxd + (sbase + s * ss + qq * sq) * C;
+                for (int c = 0; c < C; ++c) out[c] = v[c];
+            }
+        }
+    };
+    int s_dx = -1;                              // line whose partials wait in dxr
     for (int j = 0; j < nlines; ++j) {
         const int t = T - 1 - (r0 + j);
         const int s = dg.sign > 0 ? t : T - 1 - t;
         const bool has_next = t + 1 < T;
         const int lo = (j + 1) * rq;
-        const int W = kLineSeg + 2 * (S - 1 - j) * rq;
+        const int W = kLineSeg + 2 * (S - j) * rq;
         const int ntl = (W + 15) >> 4;          // at most 6: two tiles per wave
         // dA_t is held in registers until every wave has read dA_{t+1} from
         // the one LDS buffer
@@ -1267,6 +1331,7 @@ k_line_bwd(LineBwdArgs a)
             }
         }
         __syncthreads();
+        if (want_dx && s_dx >= 0) store_dx(s_dx);
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
             const int i = wave + 4 * k;
@@ -1276,7 +1341,33 @@ k_line_bwd(LineBwdArgs a)
             for (int g = 0; g < 4; ++g) dab[slot * 16 + ((g * 4 + q4) ^ (slot & 15))] = onv[k] ? dv[k][g] : zero;
         }
         __syncthreads();
+        if (want_dx) {
+            // lane = pixel of the segment; wave = gate; taps from dA_t in LDS
+            const int cs = (S + 1) * rq + lane;
+            f4 px;
+            switch (C) {
+            case 1: px = line_dx_px<1>(dab, wxl, cs, rq, KQ, wave); break;
+            case 2: px = line_dx_px<2>(dab, wxl, cs, rq, KQ, wave); break;
+            case 3: px = line_dx_px<3>(dab, wxl, cs, rq, KQ, wave); break;
+            default: px = line_dx_px<4>(dab, wxl, cs, rq, KQ, wave); break;
+            }
+            dxr[wave][lane] = px;
+            s_dx = s;
+        }
     }
+    if (want_dx && s_dx >= 0) {
+        __syncthreads();
+        store_dx(s_dx);
+    }
+}
+
+// dx = the four directions' dL/dx added in order.
+__global__ void __launch_bounds__(256)
+k_sum_dx4(long long n, const float *__restrict__ dxd, float *__restrict__ dx)
+{
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    dx[i] = ((dxd[i] + dxd[n + i]) + dxd[2 * n + i]) + dxd[3 * n + i];
 }
 
 // Every unit group of kNT 16-pixel tiles of one plane (an item); the two
@@ -2237,6 +2328,10 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     return PLSTM_OK;
 }
 
+// The 2D layer with 16 units and at most 4 input channels takes dL/dx from
+// the reverse line blocks.
+inline bool line_bwd_dx(const Geom &g) { return g.nd == 4 && g.KP == 1 && g.O == 16 && g.C <= 4; }
+
 size_t step_bwd_ws(const Geom &g)
 {
     const int U = g.O / 16, Cp = pad16(g.C), G = 4 * g.O, KK = g.KP * g.KQ;
@@ -2249,6 +2344,7 @@ size_t step_bwd_ws(const Geom &g)
     cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);         // weight-gradient partials
     cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);   // W_x^T fragments
     cv.take<float>((size_t)g.nd * kDbChunks * G);                  // db partials
+    if (line_bwd_dx(g)) cv.take<float>((size_t)g.nd * g.N * g.V * g.C);  // dL/dx per direction
     return cv.off;
 }
 
@@ -2304,25 +2400,31 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     float *partial = cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);
     float *fragx = cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);
     float *dbpart = cv.take<float>((size_t)g.nd * kDbChunks * G);
+    float *dxd = line_bwd_dx(g) ? cv.take<float>((size_t)g.nd * g.N * g.V * g.C) : nullptr;
     const long long nvox = (long long)g.N * g.V;
+    bool dx_done = false;
 
     timing_begin("sweep_bwd_step", st);
     k_pack_bwd<<<blocks_for((long long)g.nd * U * KK * 4 * U * 256, 256), 256, 0, st>>>(
         g.nd, g.O, KK, wh, frag);
     PLSTM_LAUNCH_CHECK();
+    const bool fuse_dx = dx && dxd;
+    const size_t line_dyn = line_bwd_dyn_lds(g.KQ * 4, fuse_dx ? g.KQ * G * g.C : 0);
     if (g.nd == 4 && g.KP == 1 && g.O == 16 && (g_step_split == 0 || g_step_split == 2) &&
-        line_bwd_dyn_lds(g.KQ * 4) + kLineSlots * 64 <= (size_t)device_info().max_lds) {
+        line_dyn + kLineSlots * 64 + 4 * 64 * 16 <= (size_t)device_info().max_lds) {
         // 2D layers with 16 units: line blocks, S lines per launch (S r <= 16)
         LineBwdArgs la;
         la.g = g;
         const int rq = g.KQ / 2;
         la.S = rq == 0 ? 16 : (16 / rq < 16 ? 16 / rq : 16);
-        if (kLineSeg + 2 * (la.S - 1) * rq > 96) return PLSTM_EUNSUPPORTED;   // two tiles per wave
+        if (kLineSeg + 2 * la.S * rq > 96) return PLSTM_EUNSUPPORTED;   // two tiles per wave
         la.frag = frag;
         la.gates = sv.gates; la.cell = sv.cell; la.dh = dh;
         la.dA = dA; la.gcf = gcf;
+        la.wx = wx;
+        la.dxd = fuse_dx ? dxd : nullptr;
         for (int d = 0; d < kDirs; ++d) la.nseg[d] = (g.dir[d].Q + kLineSeg - 1) / kLineSeg;
-        const size_t dyn = line_bwd_dyn_lds(g.KQ * 4);
+        const size_t dyn = line_dyn;
         if (hipFuncSetAttribute((const void *)k_line_bwd, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)dyn) != hipSuccess)
             return PLSTM_EHIP;
@@ -2341,6 +2443,14 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
             ++launches;
         }
         timing_end(1 + launches, st);
+        if (fuse_dx) {
+            timing_begin("dx_step", st);
+            const long long ndx = nvox * g.C;
+            k_sum_dx4<<<blocks_for(ndx, 256), 256, 0, st>>>(ndx, dxd, dx);
+            PLSTM_LAUNCH_CHECK();
+            timing_end(1, st);
+            dx_done = true;
+        }
     } else {
         BwdStepArgs a;
         a.g = g;
@@ -2385,7 +2495,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     k_db_reduce<<<blocks_for(g.nd * G, 256), 256, 0, st>>>(g.nd, G, dbpart, db);
     PLSTM_LAUNCH_CHECK();
     timing_end(5, st);
-    if (dx) return step_dx(g, wx, dA, fragx, dx, st);
+    if (dx && !dx_done) return step_dx(g, wx, dA, fragx, dx, st);
     return PLSTM_OK;
 }
 

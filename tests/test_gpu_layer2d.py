@@ -25,7 +25,10 @@ SHAPES = [(1, 5, 6, 2, 16, 3), (2, 17, 33, 3, 16, 3), (1, 9, 70, 5, 32, 7),
           # 16 units (line blocks): several dense (tap, channel) K-groups, lines
           # longer than a segment and ragged, the widest filter
           (1, 9, 70, 5, 16, 7), (2, 12, 40, 20, 16, 5), (1, 30, 150, 17, 16, 3),
-          (1, 40, 129, 1, 16, 1)]
+          (1, 40, 129, 1, 16, 1),
+          # 16 units and at most 4 channels: dL/dx from the reverse line
+          # blocks, at the widest filters and ragged segments
+          (1, 11, 100, 4, 16, 7), (2, 20, 70, 4, 16, 5), (1, 7, 200, 3, 16, 3)]
 
 
 def ident(s):
@@ -66,6 +69,9 @@ def test_2d_layer_matches_oracle(shape):
     phases = run(shape, 9000 + sum(shape), 31 + sum(shape))
     if shape[4] in (16, 32, 64):
         assert "sweep_fwd_step" in phases and "sweep_bwd_step" in phases, phases
+        # one launch (the sum over directions) when the line blocks give dL/dx
+        fused = shape[4] == 16 and shape[3] <= 4
+        assert (phases["dx_step"][1] == 1) == fused, phases
     else:
         assert "sweep_fwd_generic" in phases and "sweep_bwd_generic" in phases, phases
 

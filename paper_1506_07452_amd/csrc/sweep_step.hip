@@ -1125,12 +1125,13 @@ struct BwdStepArgs {
 // ---- line blocks of the 2D layer's reverse sweep (16 hidden units) ----------
 // The reverse of k_line_fwd: a workgroup owns a 64-pixel segment and goes
 // back S lines per launch with overlapped tiles.  At reverse line j it
-// computes the segment widened by (S - 1 - j) r pixels on each side, which is
-// what line j + 1 reads: dA_{t+1} (64 gate-units per pixel, 16-byte chunks
-// XOR-swizzled by the pixel; overwritten after a barrier) and gc_{t+1} f_{t+1}
-// (in place) stay in LDS; the saved gates, cell states and dL/dh are read per tile; only
-// the segment's own dA_t and gc_t f_t are stored.  Pixels past the line keep
-// dA = 0.
+// computes the segment widened by (S - j) r pixels on each side: line j + 1
+// reads all but the outer r of them (the outer r serve dL/dx).  dA_{t+1} (64
+// gate-units per pixel, 16-byte chunks XOR-swizzled by the pixel; overwritten
+// after a barrier) and gc_{t+1} f_{t+1} (in place) stay in LDS, and so does
+// the c_{t-1} read at line t, which is the next line's c.  The saved gates and
+// dL/dh are read per tile; only the segment's own dA_t is stored, and gc_t f_t
+// on the launch's last line.  Pixels past the line keep dA = 0.
 //   gh = dL/dh + sum_taps W_h^T dA_{t+1}[p - tap]                 (MFMA)
 //   gc = gh o (1 - tanh^2 c) + (gc f)_{t+1}
 //   dA_i = gc g i (1 - i), dA_f = gc c_{t-1} f (1 - f), dA_g = gc i (1 - g^2),
@@ -1196,6 +1197,7 @@ k_line_bwd(LineBwdArgs a)
     constexpr int O = 16, G = 64;
     __shared__ f4 gcb[kLineSlots][4];           // gc f, chunk ^ (slot & 3)
     __shared__ f4 dxr[4][64];                   // dL/dx partials of the four waves
+    __shared__ f4 cl[kLineSlots][4];            // c_{t-1} read at line t: line t - 1's c
     extern __shared__ f4 dyn[];
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1292,7 +1294,10 @@ k_line_bwd(LineBwdArgs a)
 #pragma unroll
             for (int g = 0; g < 4; ++g)
                 gv[g] = bload4(rs_g, sel_off(on, (unsigned)((vox * G + g * O + 4 * q4) * 4)));
-            const f4 c = bload4(rs_c, sel_off(on, (unsigned)((vox * O + 4 * q4) * 4)));
+            const int gsw = q4 ^ (slot & 3);
+            // c_t: the previous line's c_{t-1}, kept in LDS (same lane and slot)
+            const f4 c = j == 0 ? bload4(rs_c, sel_off(on, (unsigned)((vox * O + 4 * q4) * 4)))
+                                : cl[slot][gsw];
             const f4 cp = bload4(rs_c, sel_off(on && t > 0, (unsigned)(((vox - noff) * O + 4 * q4) * 4)));
             const f4 dhv = bload4(rs_dh, sel_off(on, (unsigned)((vox * O + 4 * q4) * 4)));
             f4 acc = zero;
@@ -1306,9 +1311,9 @@ k_line_bwd(LineBwdArgs a)
                     for (int i4 = 0; i4 < 4; ++i4) acc = mfma(av[i4], bv[i4], acc);
                 }
             }
-            // gc f is read and rewritten by its own lane only
-            const int gsw = q4 ^ (slot & 3);
+            // gc f and c are read and rewritten by their own lane only
             const f4 gn = has_next ? gcb[slot][gsw] : zero;
+            cl[slot][gsw] = cp;
             f4 gco;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
@@ -1327,7 +1332,8 @@ k_line_bwd(LineBwdArgs a)
                 const long long vo = sbase + vox;
 #pragma unroll
                 for (int g = 0; g < 4; ++g) *(f4 *)(a.dA + vo * G + g * O + 4 * q4) = dv[k][g];
-                *(f4 *)(a.gcf + vo * O + 4 * q4) = gco;
+                // gc f leaves LDS only where the next launch starts
+                if (j == nlines - 1) *(f4 *)(a.gcf + vo * O + 4 * q4) = gco;
             }
         }
         __syncthreads();
@@ -2411,7 +2417,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     const bool fuse_dx = dx && dxd;
     const size_t line_dyn = line_bwd_dyn_lds(g.KQ * 4, fuse_dx ? g.KQ * G * g.C : 0);
     if (g.nd == 4 && g.KP == 1 && g.O == 16 && (g_step_split == 0 || g_step_split == 2) &&
-        line_dyn + kLineSlots * 64 + 4 * 64 * 16 <= (size_t)device_info().max_lds) {
+        line_dyn + 2 * kLineSlots * 64 + 4 * 64 * 16 <= (size_t)device_info().max_lds) {
         // 2D layers with 16 units: line blocks, S lines per launch (S r <= 16)
         LineBwdArgs la;
         la.g = g;

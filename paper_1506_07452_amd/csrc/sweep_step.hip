@@ -1976,7 +1976,8 @@ struct WgShape {
 // Voxel chunks per (direction, block): the launch takes ceil(waves / slots)
 // rounds of 1/kch of a block's work; pick the chunk count that minimises that
 // (ties: fewer chunks).  Blocks of four N-tiles count one wave per SIMD;
-// blocks of fewer tiles do less MFMA work per load and are given four.
+// blocks of fewer tiles do less MFMA work per load and are given three, the
+// kernel's occupancy at its register count.
 inline WgShape wg_shape(const Geom &g)
 {
     const int U = g.O / 16, KK = g.KP * g.KQ, XT = wg_xtiles(KK, g.C);
@@ -1985,7 +1986,7 @@ inline WgShape wg_shape(const Geom &g)
     w.NTt = KK * U + XT;
     w.nblk = wb.nh + wb.nx;
     const DevInfo di = device_info();
-    const int per_simd = (wb.th < kWgN && wb.tx < kWgN) ? 4 : 1;
+    const int per_simd = (wb.th < kWgN && wb.tx < kWgN) ? 3 : 1;
     const long long simds = 4LL * per_simd * (di.cus > 0 ? di.cus : 256);   // wave slots
     const long long per = (long long)g.nd * U * w.nblk;
     double best = 1e30;

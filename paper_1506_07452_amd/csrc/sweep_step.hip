@@ -1142,6 +1142,9 @@ struct BwdStepArgs {
 // line needs, so the segment's taps are all there.  Wave w sums gate w's 16
 // units for the segment's 64 pixels; the four partials meet in LDS and are
 // added, in order, after the next barrier.
+// With dbp the segment's dA_t columns are summed too (db): per lane over its
+// central pixels, then over the lanes and waves in a fixed order, and added
+// to the (image, segment) partial of the earlier launches.
 struct LineBwdArgs {
     Geom g;
     int r0, S;                  // first reverse step of this launch, steps per launch
@@ -1150,6 +1153,8 @@ struct LineBwdArgs {
     float *dA, *gcf;
     const float *wx;            // [4][4O][C][K] input filters (dxd only)
     float *dxd;                 // [4][N][V][C] per-direction dL/dx, or null
+    float *dbp;                 // [4][N][nsegmax][4O] bias-gradient partials, or null
+    int nsegmax;                // segments of the longest line
     int nseg[kDirs];
     int base[kDirs + 1];
 };
@@ -1198,6 +1203,7 @@ k_line_bwd(LineBwdArgs a)
     __shared__ f4 gcb[kLineSlots][4];           // gc f, chunk ^ (slot & 3)
     __shared__ f4 dxr[4][64];                   // dL/dx partials of the four waves
     __shared__ f4 cl[kLineSlots][4];            // c_{t-1} read at line t: line t - 1's c
+    __shared__ f4 dbr[4][4][4];                 // bias-gradient sums [wave][gate][q4]
     extern __shared__ f4 dyn[];
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1215,6 +1221,8 @@ k_line_bwd(LineBwdArgs a)
     const long long sbase = ((long long)d * a.g.N + n) * V;
     const int C = a.g.C, KQ = a.g.KQ;
     const bool want_dx = a.dxd != nullptr;
+    f4 dbacc[4] = {{0.0f, 0.0f, 0.0f, 0.0f}, {0.0f, 0.0f, 0.0f, 0.0f},
+                   {0.0f, 0.0f, 0.0f, 0.0f}, {0.0f, 0.0f, 0.0f, 0.0f}};
     const auto rs_dA = slice_rsrc(a.dA + sbase * G, V * G);
     const auto rs_gcf = slice_rsrc(a.gcf + sbase * O, V * O);
     const auto rs_g = slice_rsrc(a.gates + sbase * G, V * G);
@@ -1329,6 +1337,8 @@ k_line_bwd(LineBwdArgs a)
             }
             gcb[slot][gsw] = on ? gco : zero;
             if (on && qq >= q0 && qq < q0 + kLineSeg) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) dbacc[g] += dv[k][g];
                 const long long vo = sbase + vox;
 #pragma unroll
                 for (int g = 0; g < 4; ++g) *(f4 *)(a.dA + vo * G + g * O + 4 * q4) = dv[k][g];
@@ -1365,6 +1375,54 @@ k_line_bwd(LineBwdArgs a)
         __syncthreads();
         store_dx(s_dx);
     }
+    if (a.dbp) {
+        // over the 16 lanes of a unit group (pixels), then the four waves
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                float v = dbacc[g][u];
+                v += __shfl_xor(v, 1);
+                v += __shfl_xor(v, 2);
+                v += __shfl_xor(v, 4);
+                v += __shfl_xor(v, 8);
+                dbacc[g][u] = v;
+            }
+        if (col == 0) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) dbr[wave][g][q4] = dbacc[g];
+        }
+        __syncthreads();
+        if (threadIdx.x < G) {
+            const int m = threadIdx.x, g = m >> 4, q = (m >> 2) & 3, u = m & 3;
+            const float v = ((dbr[0][g][q][u] + dbr[1][g][q][u]) + dbr[2][g][q][u]) + dbr[3][g][q][u];
+            float *e = a.dbp + (((long long)d * a.g.N + n) * a.nsegmax + seg) * G + m;
+            *e = (r0 == 0 ? 0.0f : *e) + v;
+        }
+    }
+}
+
+// db from the reverse line blocks' partials: each direction's (image,
+// segment) partials added in order.
+struct LineDbReduceArgs {
+    int nd, N, nsegmax;
+    int nseg[kDirs];
+    const float *dbp;
+    float *db;
+};
+
+__global__ void __launch_bounds__(256)
+k_line_db_reduce(LineDbReduceArgs a)
+{
+    constexpr int G = 64;
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= a.nd * G) return;
+    const int d = i / G, m = i - d * G;
+    float acc = 0.0f;
+    for (int n = 0; n < a.N; ++n)
+        for (int seg = 0; seg < a.nseg[d]; ++seg)
+            acc += a.dbp[(((long long)d * a.N + n) * a.nsegmax + seg) * G + m];
+    a.db[i] = acc;
 }
 
 // dx = the four directions' dL/dx added in order.
@@ -2338,6 +2396,18 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
 // The 2D layer with 16 units and at most 4 input channels takes dL/dx from
 // the reverse line blocks.
 inline bool line_bwd_dx(const Geom &g) { return g.nd == 4 && g.KP == 1 && g.O == 16 && g.C <= 4; }
+// Segments of the longest line of the 2D layer (bias-gradient partials of
+// the reverse line blocks).
+inline int line_nsegmax(const Geom &g)
+{
+    int m = 0;
+    for (int d = 0; d < g.nd; ++d) {
+        const int ns = (g.dir[d].Q + kLineSeg - 1) / kLineSeg;
+        m = ns > m ? ns : m;
+    }
+    return m;
+}
+inline bool line_bwd_geom(const Geom &g) { return g.nd == 4 && g.KP == 1 && g.O == 16; }
 
 size_t step_bwd_ws(const Geom &g)
 {
@@ -2352,6 +2422,7 @@ size_t step_bwd_ws(const Geom &g)
     cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);   // W_x^T fragments
     cv.take<float>((size_t)g.nd * kDbChunks * G);                  // db partials
     if (line_bwd_dx(g)) cv.take<float>((size_t)g.nd * g.N * g.V * g.C);  // dL/dx per direction
+    if (line_bwd_geom(g)) cv.take<float>((size_t)g.nd * g.N * line_nsegmax(g) * 64);  // db partials
     return cv.off;
 }
 
@@ -2408,6 +2479,9 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     float *fragx = cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);
     float *dbpart = cv.take<float>((size_t)g.nd * kDbChunks * G);
     float *dxd = line_bwd_dx(g) ? cv.take<float>((size_t)g.nd * g.N * g.V * g.C) : nullptr;
+    float *dbl = line_bwd_geom(g) ? cv.take<float>((size_t)g.nd * g.N * line_nsegmax(g) * 64)
+                                  : nullptr;
+    bool db_done = false;
     const long long nvox = (long long)g.N * g.V;
     bool dx_done = false;
 
@@ -2418,7 +2492,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     const bool fuse_dx = dx && dxd;
     const size_t line_dyn = line_bwd_dyn_lds(g.KQ * 4, fuse_dx ? g.KQ * G * g.C : 0);
     if (g.nd == 4 && g.KP == 1 && g.O == 16 && (g_step_split == 0 || g_step_split == 2) &&
-        line_dyn + 2 * kLineSlots * 64 + 4 * 64 * 16 <= (size_t)device_info().max_lds) {
+        line_dyn + 2 * kLineSlots * 64 + 4 * 64 * 16 + 4 * 4 * 4 * 16 <= (size_t)device_info().max_lds) {
         // 2D layers with 16 units: line blocks, S lines per launch (S r <= 16)
         LineBwdArgs la;
         la.g = g;
@@ -2430,6 +2504,8 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
         la.dA = dA; la.gcf = gcf;
         la.wx = wx;
         la.dxd = fuse_dx ? dxd : nullptr;
+        la.dbp = dbl;
+        la.nsegmax = line_nsegmax(g);
         for (int d = 0; d < kDirs; ++d) la.nseg[d] = (g.dir[d].Q + kLineSeg - 1) / kLineSeg;
         const size_t dyn = line_dyn;
         if (hipFuncSetAttribute((const void *)k_line_bwd, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -2458,6 +2534,16 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
             timing_end(1, st);
             dx_done = true;
         }
+        LineDbReduceArgs ra;
+        ra.nd = g.nd; ra.N = g.N; ra.nsegmax = la.nsegmax;
+        for (int d = 0; d < kDirs; ++d) ra.nseg[d] = la.nseg[d];
+        ra.dbp = dbl;
+        ra.db = db;
+        timing_begin("wgrad_step", st);
+        k_line_db_reduce<<<blocks_for(g.nd * G, 256), 256, 0, st>>>(ra);
+        PLSTM_LAUNCH_CHECK();
+        timing_end(1, st);
+        db_done = true;
     } else {
         BwdStepArgs a;
         a.g = g;
@@ -2497,11 +2583,13 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.nd, g.O, g.C, Cp, KK, w.NTt,
                                                                w.kch, partial, dwx, dwh);
     PLSTM_LAUNCH_CHECK();
-    k_db_partial<<<dim3(kDbChunks, g.nd), 256, 0, st>>>(G, nvox, dA, dbpart);
-    PLSTM_LAUNCH_CHECK();
-    k_db_reduce<<<blocks_for(g.nd * G, 256), 256, 0, st>>>(g.nd, G, dbpart, db);
-    PLSTM_LAUNCH_CHECK();
-    timing_end(5, st);
+    if (!db_done) {
+        k_db_partial<<<dim3(kDbChunks, g.nd), 256, 0, st>>>(G, nvox, dA, dbpart);
+        PLSTM_LAUNCH_CHECK();
+        k_db_reduce<<<blocks_for(g.nd * G, 256), 256, 0, st>>>(g.nd, G, dbpart, db);
+        PLSTM_LAUNCH_CHECK();
+    }
+    timing_end(db_done ? 3 : 5, st);
     if (dx && !dx_done) return step_dx(g, wx, dA, fragx, dx, st);
     return PLSTM_OK;
 }

@@ -1618,11 +1618,11 @@ __host__ __device__ inline WgBlocks wg_blocks(int U, int XT, int KK)
 
 struct WgStepArgs {
     Geom g;
-    int Cp;
+    int Cp;                   // floats per voxel of xp
     int NTt;                  // N-tiles: KK U + KK C'/16
     int kch;                  // voxel chunks per (direction, M-block, N-block)
     int k_mul;                // ceil(2^16 / K)
-    const float *xp, *hd, *dA;
+    const float *xp, *hd, *dA;  // xp: the input x [N][V][Cp] (read one channel per lane)
     float *partial;           // [6][kch][4O][16 NTt]
 };
 
@@ -2417,7 +2417,6 @@ size_t step_bwd_ws(const Geom &g)
     cv.take<float>((size_t)g.nd * g.N * g.V * G);                  // dA
     cv.take<float>((size_t)g.nd * g.N * g.V * g.O);                // dL/dc * f
     cv.take<float>((size_t)g.nd * U * KK * 4 * U * 256);           // W_h^T fragments
-    cv.take<float>((size_t)g.N * g.V * Cp);                        // padded x
     cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);         // weight-gradient partials
     cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);   // W_x^T fragments
     cv.take<float>((size_t)g.nd * kDbChunks * G);                  // db partials
@@ -2474,7 +2473,6 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     float *dA = cv.take<float>((size_t)g.nd * g.N * g.V * G);
     float *gcf = cv.take<float>((size_t)g.nd * g.N * g.V * g.O);
     float *frag = cv.take<float>((size_t)g.nd * U * KK * 4 * U * 256);
-    float *xp = cv.take<float>((size_t)g.N * g.V * Cp);
     float *partial = cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);
     float *fragx = cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);
     float *dbpart = cv.take<float>((size_t)g.nd * kDbChunks * G);
@@ -2563,13 +2561,12 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     }
 
     timing_begin("wgrad_step", st);
-    k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp, x, xp);
-    PLSTM_LAUNCH_CHECK();
+    // the x tiles read one channel per lane: x itself, C floats per voxel
     WgStepArgs wa;
     wa.g = g;
-    wa.Cp = Cp;
+    wa.Cp = g.C;
     wa.NTt = w.NTt; wa.kch = w.kch;
-    wa.xp = xp; wa.hd = sv.hd; wa.dA = dA;
+    wa.xp = x; wa.hd = sv.hd; wa.dA = dA;
     wa.partial = partial;
     wa.k_mul = k_mul_of(g);
     const long long witems = (long long)g.nd * U * w.nblk * w.kch;
@@ -2589,7 +2586,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
         k_db_reduce<<<blocks_for(g.nd * G, 256), 256, 0, st>>>(g.nd, G, dbpart, db);
         PLSTM_LAUNCH_CHECK();
     }
-    timing_end(db_done ? 3 : 5, st);
+    timing_end(db_done ? 2 : 4, st);
     if (dx && !dx_done) return step_dx(g, wx, dA, fragx, dx, st);
     return PLSTM_OK;
 }

@@ -2310,19 +2310,26 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     const long long nfrag = (long long)g.nd * U * KG * 1024;
 
     timing_begin("sweep_fwd_step", st);
-    if (dtype == PLSTM_BF16)
-        k_pad_x<uint16_t><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
-                                                                      (const uint16_t *)x, xp);
-    else
-        k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
-                                                                   (const float *)x, xp);
-    PLSTM_LAUNCH_CHECK();
+    auto pad_x = [&]() {
+        if (dtype == PLSTM_BF16)
+            k_pad_x<uint16_t><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
+                                                                          (const uint16_t *)x, xp);
+        else
+            k_pad_x<float><<<blocks_for(nvox * Cp, 256), 256, 0, st>>>(nvox, g.C, Cp,
+                                                                       (const float *)x, xp);
+    };
 
     // 2D layers with 16 units: line blocks, S lines per launch (S r <= 16),
-    // the input taps packed densely as (tap, channel) pairs
+    // the input taps packed densely as (tap, channel) pairs; fp32 x is staged
+    // from the input itself (C floats per pixel), bf16 from its fp32 copy
     const int KXL = (g.KQ * g.C + 15) / 16, KGL = KXL + g.KQ;
     if (g.nd == 4 && g.KP == 1 && g.O == 16 && (g_step_split == 0 || g_step_split == 2) &&
         line_fwd_dyn_lds(KGL, g.C) <= 64 * 1024) {
+        const bool x_direct = dtype != PLSTM_BF16;
+        if (!x_direct) {
+            pad_x();
+            PLSTM_LAUNCH_CHECK();
+        }
         const long long nfl = (long long)g.nd * KGL * 1024;
         if (dtype == PLSTM_BF16)
             k_pack_line<uint16_t><<<blocks_for(nfl, 256), 256, 0, st>>>(
@@ -2337,9 +2344,9 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
         la.g = g;
         const int rq = g.KQ / 2;
         la.S = rq == 0 ? 16 : (16 / rq < 16 ? 16 / rq : 16);
-        la.Cp = Cp; la.KX = KXL; la.KG = KGL;
+        la.Cp = x_direct ? g.C : Cp; la.KX = KXL; la.KG = KGL;
         la.c_mul = (65536 + g.C - 1) / g.C;
-        la.xp = xp; la.frag = frag; la.bias = bias;
+        la.xp = x_direct ? (const float *)x : xp; la.frag = frag; la.bias = bias;
         la.hd = hd; la.cell = cell; la.gates = gates;
         for (int d = 0; d < kDirs; ++d) la.nseg[d] = (g.dir[d].Q + kLineSeg - 1) / kLineSeg;
         const int T = max_T(g);
@@ -2360,9 +2367,11 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
             PLSTM_LAUNCH_CHECK();
             ++launches;
         }
-        timing_end(2 + launches, st);
+        timing_end((x_direct ? 1 : 2) + launches, st);
         return PLSTM_OK;
     }
+    pad_x();
+    PLSTM_LAUNCH_CHECK();
 
     if (dtype == PLSTM_BF16)
         k_pack_fwd<uint16_t><<<blocks_for(nfrag, 256), 256, 0, st>>>(

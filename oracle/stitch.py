@@ -44,14 +44,19 @@ def gaussian_weights(shape, sigma_scale: float = 0.25):
     return w
 
 
-def stitch(volume_shape, tile, stride, tile_fn, classes: int, sigma_scale: float = 0.25):
+def stitch(volume_shape, tile, stride, tile_fn, classes: int, sigma_scale: float = 0.25,
+           origins=None):
     """Weighted mean over tiles.  volume_shape (D, H, W); tile and stride are
     (d, h, w) triples; tile_fn(z0, y0, x0, d, h, w) returns the tile's output
-    [d][h][w][classes].  Returns [D][H][W][classes]."""
+    [d][h][w][classes].  `origins` = (z list, y list, x list) gives the tile
+    starts per axis instead of the stride grid.  Returns [D][H][W][classes]."""
     D, H, W = volume_shape
-    zs, td = tile_starts(D, tile[0], stride[0])
-    ys, th = tile_starts(H, tile[1], stride[1])
-    xs, tw = tile_starts(W, tile[2], stride[2])
+    if origins is None:
+        zs, td = tile_starts(D, tile[0], stride[0])
+        ys, th = tile_starts(H, tile[1], stride[1])
+        xs, tw = tile_starts(W, tile[2], stride[2])
+    else:
+        (zs, ys, xs), (td, th, tw) = origins, tile
     wt = gaussian_weights((td, th, tw), sigma_scale)
     acc = np.zeros((D, H, W, classes))
     wsum = np.zeros((D, H, W))

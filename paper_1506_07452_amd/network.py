@@ -249,27 +249,41 @@ def network_gradients(g):
     return out + [g["head"][0], g["head"][1]]
 
 
-def _tile_starts(extent, size, stride):
+def grid_axis(extent, size, stride):
+    """Tile origins along one axis of `extent` voxels for tiles of `size`
+    (cut to the extent) advancing by `stride`: n = ceil((extent - size) /
+    stride) + 1 tiles, the i-th at min(i * stride, extent - size), so the
+    last one ends flush with the axis.  Returns (origins, size)."""
+    if extent < 1 or size < 1 or stride < 1:
+        raise ValueError("extent, tile size and stride must be positive")
     size = min(size, extent)
-    starts = list(range(0, extent - size + 1, stride))
-    if starts[-1] + size < extent:
-        starts.append(extent - size)
-    return starts, size
+    span = extent - size
+    n = -(-span // stride) + 1
+    return [min(i * stride, span) for i in range(n)], size
 
 
-def network_infer_volume(x, layers, fcs, head, tile, stride, sigma_scale=0.25, ws=None,
-                         stream=None):
+def network_infer_volume(x, layers, fcs, head, tile, stride=None, sigma_scale=0.25, ws=None,
+                         stream=None, origins=None):
     """Class probabilities [N][D][H][W][K] of a volume processed as sub-volumes
-    (Section 3, "Sub-volumes and Augmentation"): tiles of size `tile` (d, h, w)
-    at multiples of `stride` along each axis (plus one flush with the far end
-    where the grid falls short), each run through the network on its own, and
-    stitched with Gaussian weights (sigma = sigma_scale x tile extent)."""
+    (Section 3, "Sub-volumes and Augmentation"): tiles of size `tile` (d, h, w),
+    each run through the network on its own and stitched with Gaussian weights
+    (sigma = sigma_scale x tile extent).  The tile origins per axis are either
+    given (`origins` = (z list, y list, x list), every tile inside the volume)
+    or laid on a grid of `stride` (d, h, w) by `grid_axis`."""
     from . import pyramid_crop, pyramid_stitch_add, pyramid_stitch_clear, pyramid_stitch_finish
     N, D, H, W, C = x.shape
     K = head[0].shape[0]
-    zs, td = _tile_starts(D, tile[0], stride[0])
-    ys, th = _tile_starts(H, tile[1], stride[1])
-    xs, tw = _tile_starts(W, tile[2], stride[2])
+    if origins is None:
+        if stride is None:
+            raise ValueError("give a stride or explicit tile origins")
+        (zs, td), (ys, th), (xs, tw) = (grid_axis(e, t, s) for e, t, s in
+                                        zip((D, H, W), tile, stride))
+    else:
+        td, th, tw = tile
+        zs, ys, xs = (list(o) for o in origins)
+        for ext, size, starts in ((D, td, zs), (H, th, ys), (W, tw, xs)):
+            if not starts or min(starts) < 0 or max(starts) + size > ext:
+                raise ValueError("tile origins must keep every tile inside the volume")
     out = torch.empty((N, D, H, W, K), dtype=torch.float32, device=x.device)
     acc = torch.empty((D, H, W, K), dtype=torch.float32, device=x.device)
     wsum = torch.empty((D, H, W), dtype=torch.float32, device=x.device)

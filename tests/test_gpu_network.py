@@ -175,24 +175,32 @@ def test_crop_is_the_subvolume(dtype):
 def test_stitched_inference_matches_oracle():
     """A volume run as overlapping sub-volumes and stitched with Gaussian
     weights (Section 3) against the oracle doing the same with its own
-    network."""
+    network.  Both sides get the same hand-written tile origins (ragged
+    overlaps, the last tile flush with each far end); the stride grids of
+    the two sides are pinned separately on the CPU."""
     import oracle.stitch as ostitch
     from paper_1506_07452_amd.network import network_infer_volume
     inst = small(dict(N=1, D=6, H=20, W=18, C=3, hidden=[16, 32], fc=True, classes=4), 102)
-    tile, stride = (4, 12, 10), (2, 8, 8)
+    tile = (4, 12, 10)
+    origins = ([0, 2], [0, 5, 8], [0, 8])
     lw, fw, hw = oracle_args(inst)
 
     def tile_fn(z0, y0, x0, d, h, w):
         xs = inst.x[:, z0:z0 + d, y0:y0 + h, x0:x0 + w]
         return onet.forward(xs, lw, fw, hw)["p"].reshape(d, h, w, -1)
 
-    ref = ostitch.stitch((6, 20, 18), tile, stride, tile_fn, 4)
+    ref = ostitch.stitch((6, 20, 18), tile, None, tile_fn, 4, origins=origins)
     say("stitched inference")
     x, layers, fcs, head, _ = to_device(inst, "f32")
-    p = network_infer_volume(x, layers, fcs, head, tile, stride)
+    p = network_infer_volume(x, layers, fcs, head, tile, origins=origins)
+    p_grid = network_infer_volume(x, layers, fcs, head, tile, (2, 8, 8))
     torch.cuda.synchronize()
     assert normwise(host(p)[0], ref) <= TOL["f32"]
     assert np.allclose(host(p).sum(-1), 1.0, atol=1e-5)
+    # the stride grid (2, 8, 8) lays tiles at z (0, 2), y (0, 8), x (0, 8)
+    ref_grid = ostitch.stitch((6, 20, 18), tile, None, tile_fn, 4,
+                              origins=([0, 2], [0, 8], [0, 8]))
+    assert normwise(host(p_grid)[0], ref_grid) <= TOL["f32"]
 
 
 def test_single_tile_stitch_is_the_network_output():

@@ -629,6 +629,31 @@ def test_tile_starts_cover_every_voxel():
         assert sz == min(size, extent)
 
 
+# (extent, tile size, stride) -> origins, worked out by hand: tiles at
+# multiples of the stride while they fit, then one flush with the far end
+GRID_CASES = [
+    ((48, 25, 12), [0, 12, 23]),
+    ((240, 128, 96), [0, 96, 112]),
+    ((7, 9, 4), [0]),                  # tile larger than the volume: cut to it
+    ((10, 5, 5), [0, 5]),              # the grid ends exactly at the far end
+    ((11, 4, 3), [0, 3, 6, 7]),
+    ((20, 12, 8), [0, 8]),
+    ((1, 1, 1), [0]),
+    ((9, 2, 7), [0, 7]),
+]
+
+
+@pytest.mark.parametrize("case", GRID_CASES, ids=lambda c: "x".join(map(str, c[0])))
+def test_tile_grids_match_hand_lists(case):
+    """The oracle's stitching grid and the library binding's own grid rule
+    (written independently: a tile count and a clamped last origin) both
+    give the hand-computed origins."""
+    from paper_1506_07452_amd.network import grid_axis
+    (extent, size, stride), want = case
+    assert ostitch.tile_starts(extent, size, stride) == (want, min(size, extent))
+    assert grid_axis(extent, size, stride) == (want, min(size, extent))
+
+
 def test_gaussian_weights_closed_form():
     w = ostitch.gaussian_weights((3, 4, 5), 0.25)
     # centre of the odd axes, between the two middle voxels of the even one

@@ -284,8 +284,9 @@ int pyramid_crop(int32_t N, int32_t D, int32_t H, int32_t W, int32_t C, int32_t 
  * Cube voxel (k, i, j), before the flips, reads the source position
  *   z = z0 + k, y = yc + c u - s v, x = xc + s u + c v,
  *   u = i - (h - 1) / 2, v = j - (w - 1) / 2, (yc, xc) the box's centre,
- * computed in fp32 product by product and clamped to the slice; image values
- * are bilinear in (y, x), labels take the nearest voxel floor(y + 1/2).  The
+ * computed in fp64 and clamped to the slice; image values are bilinear in
+ * (y, x) (fp64 weights and blend, rounded to the storage type), labels take
+ * the nearest voxel floor(y + 1/2).  The
  * flips then act on the cube: out[k][i][j] = cube[k'][i'][j'] with
  * k' = d - 1 - k when z is flipped (likewise y, x).
  * x [N][D][H][W][C] (dtype), labels [N][D][H][W] int32 or NULL;

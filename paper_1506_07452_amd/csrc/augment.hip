@@ -7,10 +7,11 @@
 //   z = z0 + k,  y = yc + c u - s v,  x = xc + s u + c v,
 //   u = i - (h - 1) / 2, v = j - (w - 1) / 2, (yc, xc) the cube's centre,
 // clamped to the slice.  Image values are bilinear in (y, x); labels take the
-// nearest voxel, floor(y + 1/2).  The positions are computed in fp32 without
-// contraction (each product and sum rounded), so the cell and the nearest
-// label are decided the same way on every run and by any fp32 reference that
-// follows the same order.  One thread per cube voxel; HBM gather.
+// nearest voxel, floor(y + 1/2).  Positions, weights and the blend are fp64:
+// the kernel is an HBM gather, so the double arithmetic is free, and the
+// interpolation cell and the nearest label are then decided as exactly as the
+// rotation allows (only positions within ~1e-13 of a cell or label boundary
+// could fall either way).  One thread per cube voxel.
 #include "common.h"
 #include "timing.h"
 
@@ -28,19 +29,17 @@ struct CubeArgs {
 };
 
 // Rotated source position of cube voxel (i, j), clamped to the slice.
-__device__ inline void source_yx(const CubeArgs &a, int cube, int i, int j, float &y, float &x)
+__device__ inline void source_yx(const CubeArgs &a, int cube, int i, int j, double &y, double &x)
 {
-#pragma clang fp contract(off)
-    const float u = (float)i - 0.5f * (float)(a.h - 1);
-    const float v = (float)j - 0.5f * (float)(a.w - 1);
-    const float yc = (float)a.y0[cube] + 0.5f * (float)(a.h - 1);
-    const float xc = (float)a.x0[cube] + 0.5f * (float)(a.w - 1);
-    const float c = a.c[cube], s = a.s[cube];
-    const float cu = c * u, sv = s * v, su = s * u, cv = c * v;
-    y = yc + (cu - sv);
-    x = xc + (su + cv);
-    y = fminf(fmaxf(y, 0.0f), (float)(a.H - 1));
-    x = fminf(fmaxf(x, 0.0f), (float)(a.W - 1));
+    const double u = (double)i - 0.5 * (double)(a.h - 1);
+    const double v = (double)j - 0.5 * (double)(a.w - 1);
+    const double yc = (double)a.y0[cube] + 0.5 * (double)(a.h - 1);
+    const double xc = (double)a.x0[cube] + 0.5 * (double)(a.w - 1);
+    const double c = a.c[cube], s = a.s[cube];
+    y = yc + (c * u - s * v);
+    x = xc + (s * u + c * v);
+    y = fmin(fmax(y, 0.0), (double)(a.H - 1));
+    x = fmin(fmax(x, 0.0), (double)(a.W - 1));
 }
 
 template <typename TS>
@@ -57,30 +56,26 @@ k_sample_cubes(const CubeArgs a, const TS *__restrict__ vol, const int32_t *__re
     const int kk = (fl & PLSTM_FLIP_Z) ? a.d - 1 - k : k;
     const int ii = (fl & PLSTM_FLIP_Y) ? a.h - 1 - i : i;
     const int jj = (fl & PLSTM_FLIP_X) ? a.w - 1 - j : j;
-    float y, x;
+    double y, x;
     source_yx(a, cube, ii, jj, y, x);
-    const int ya = (int)floorf(y), xa = (int)floorf(x);
+    const int ya = (int)floor(y), xa = (int)floor(x);
     const int yb = min(ya + 1, a.H - 1), xb = min(xa + 1, a.W - 1);
-    const float wy = y - (float)ya, wx = x - (float)xa;
+    const double wy = y - (double)ya, wx = x - (double)xa;
     const long long slice = ((long long)a.n[cube] * a.D + a.z0[cube] + kk) * a.H;
     const long long paa = ((slice + ya) * a.W + xa) * a.C, pab = ((slice + ya) * a.W + xb) * a.C;
     const long long pba = ((slice + yb) * a.W + xa) * a.C, pbb = ((slice + yb) * a.W + xb) * a.C;
-    const float waa = (1.0f - wy) * (1.0f - wx), wab = (1.0f - wy) * wx;
-    const float wba = wy * (1.0f - wx), wbb = wy * wx;
+    const double waa = (1.0 - wy) * (1.0 - wx), wab = (1.0 - wy) * wx;
+    const double wba = wy * (1.0 - wx), wbb = wy * wx;
     const long long o = ((long long)cube * per + vox) * a.C;
     for (int ch = 0; ch < a.C; ++ch) {
-        const float r = waa * Store<TS>::load(vol, paa + ch) + wab * Store<TS>::load(vol, pab + ch) +
-                        wba * Store<TS>::load(vol, pba + ch) + wbb * Store<TS>::load(vol, pbb + ch);
-        Store<TS>::store(out, o + ch, r);
+        const double r = waa * (double)Store<TS>::load(vol, paa + ch) +
+                         wab * (double)Store<TS>::load(vol, pab + ch) +
+                         wba * (double)Store<TS>::load(vol, pba + ch) +
+                         wbb * (double)Store<TS>::load(vol, pbb + ch);
+        Store<TS>::store(out, o + ch, (float)r);
     }
     if (labels) {
-        float yh, xh;
-        {
-#pragma clang fp contract(off)
-            yh = y + 0.5f;
-            xh = x + 0.5f;
-        }
-        const int yn = (int)floorf(yh), xn = (int)floorf(xh);
+        const int yn = (int)floor(y + 0.5), xn = (int)floor(x + 0.5);
         out_labels[(long long)cube * per + vox] = labels[(slice + yn) * a.W + xn];
     }
 }

@@ -1,7 +1,9 @@
 """GPU parity of the training-cube sampler (rotation about z, flips; Section 3,
 "Sub-volumes and Augmentation") against the oracle, through the C ABI.
-Image values within fp32 rounding of the interpolation, labels bit-exact (the
-source positions are decided in fp32 on both sides)."""
+Image values within fp32 rounding of the interpolation.  Labels are the
+nearest voxel of a rotated position: they must agree bit for bit, except at
+voxels whose position lies within 1e-4 of a nearest-label boundary (where any
+rounding may pick either side), and those must stay rare."""
 from __future__ import annotations
 
 import numpy as np
@@ -36,13 +38,20 @@ def run(x, lab, cubes, size, dtype="f32"):
     return host(out), None if lab is None else out_lab.cpu().numpy()
 
 
+MARGIN = 1e-4          # positions this close to a label boundary may go either way
+MAX_NEAR_TIES = 1e-3   # ... and may make up at most this fraction of a cube
+
+
 def check(x, lab, cubes, size, got, got_lab, tol):
     for q, cb in enumerate(cubes):
-        ref, ref_lab = oaug.sample(x, lab, cb.n, (cb.z0, cb.y0, cb.x0), size, cb.cos_t, cb.sin_t,
-                                   cb.flips)
+        corner = (cb.z0, cb.y0, cb.x0)
+        ref, ref_lab = oaug.sample(x, lab, cb.n, corner, size, cb.cos_t, cb.sin_t, cb.flips)
         assert normwise(got[q], ref) <= tol, (q, normwise(got[q], ref))
         if lab is not None:
-            assert np.array_equal(got_lab[q], ref_lab), q
+            near = oaug.label_margin(x.shape, size, corner, cb.cos_t, cb.sin_t,
+                                     cb.flips) < MARGIN
+            assert near.mean() <= MAX_NEAR_TIES, (q, near.mean())
+            assert np.array_equal(got_lab[q][~near], ref_lab[~near]), q
 
 
 CASES = [  # (N, D, H, W, C), cube size, count, recipe
@@ -93,6 +102,10 @@ def test_quarter_turns_and_flips_exact():
     say("cubes quarter turns")
     got, got_lab = run(x, lab, cubes, (3, 16, 16))
     check(x, lab, cubes, (3, 16, 16), got, got_lab, 0.0)
+    for q, cb in enumerate(cubes):       # on voxel centres: no label is near a boundary
+        ref, ref_lab = oaug.sample(x, lab, cb.n, (cb.z0, cb.y0, cb.x0), (3, 16, 16), cb.cos_t,
+                                   cb.sin_t, cb.flips)
+        assert np.array_equal(got_lab[q], ref_lab)
 
 
 def test_bf16_storage():

@@ -839,10 +839,32 @@ def test_augment_reproduces_affine_fields(theta):
     xs = np.clip(x0 + (w - 1) / 2 + s * i + c * j, 0, W - 1)
     want = a + by * ys + bx * xs
     for k in range(d):
-        np.testing.assert_allclose(cube[k, ..., 0], want, atol=2e-5)
-        np.testing.assert_allclose(cube[k, ..., 1], 2 * want, atol=4e-5)
+        np.testing.assert_allclose(cube[k, ..., 0], want, atol=1e-10)
+        np.testing.assert_allclose(cube[k, ..., 1], 2 * want, atol=2e-10)
     if theta in (1.0, 2.5):                      # those cubes reach past the slice
         assert ((ys == 0) | (xs == 0) | (ys == H - 1) | (xs == W - 1)).any()
+
+
+def test_augment_label_margin():
+    """Unturned and quarter-turned cubes sit on voxel centres: every position
+    is half a voxel from a label boundary.  A turned cube's margin is the
+    distance of p + 1/2 to the nearest integer, worked out here from the
+    positions in closed form, and follows the flips."""
+    shape = (1, 3, 30, 28)
+    m = oaug.label_margin(shape, (2, 10, 12), (0, 4, 5), 1.0, 0.0, 0)
+    assert m.shape == (2, 10, 12) and np.all(m == 0.5)
+    m = oaug.label_margin(shape, (2, 9, 9), (1, 3, 2), 0.0, 1.0, oaug.FLIP_Y)
+    assert np.all(m == 0.5)
+    theta = 0.9
+    c, s = np.cos(theta), np.sin(theta)
+    m = oaug.label_margin(shape, (1, 10, 12), (0, 8, 9), c, s, oaug.FLIP_X)
+    i = np.arange(10)[:, None] - 4.5
+    j = np.arange(12)[None, :] - 5.5
+    ys = 8 + 4.5 + c * i - s * j
+    xs = 9 + 5.5 + s * i + c * j
+    dist = lambda p: np.abs((p + 0.5) - np.round(p + 0.5))
+    want = np.minimum(dist(ys), dist(xs))[:, ::-1]
+    np.testing.assert_allclose(m[0], want, atol=1e-12)
 
 
 def test_augment_nearest_labels_of_a_half_plane():

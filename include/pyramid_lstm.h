@@ -191,6 +191,32 @@ int pyramid_head_train(int64_t M, int32_t Cin, int32_t F, int32_t K, const void 
                        void *stream);
 
 
+/* Failures found on the device after a call returned PLSTM_OK.
+ * The persistent sweeps (forward and reverse, 16 hidden units) hand the
+ * 1-pixel halo between strips of a plane through step flags (Section 2.3:
+ * each plane's convolution reads its neighbours' previous plane).  Every wait
+ * on a flag is bounded, so a neighbour that never arrives cannot hang the
+ * GPU: the wait gives up, the grid drains, and the call's outputs are
+ * overwritten with NaN (h and the saved h^d of the forward; dx, dwx, dwh, db
+ * of the backward).  The failure also raises a bit in this device's sticky
+ * status word:
+ *   PLSTM_DEVICE_WAIT_GAVE_UP   a persistent sweep's wait gave up.
+ * pyramid_lstm_device_status synchronises `stream`, writes the current
+ * device's status bits to *status (host memory; 0 = no failure since the last
+ * clear) and, when `clear` is non-zero, resets them.  Returns PLSTM_EINVAL
+ * for a null `status`, PLSTM_EHIP when the copy or the synchronisation fails.
+ * The word is shared by every caller on the device. */
+enum { PLSTM_DEVICE_WAIT_GAVE_UP = 1 };
+int pyramid_lstm_device_status(int32_t *status, int32_t clear, void *stream);
+
+/* Failure-path test mode (process-wide, for tests): with on = 1 every wait of
+ * the persistent sweeps expects a step no strip ever publishes and gives up
+ * after 16 polls, so each such launch takes the path above and still
+ * finishes normally; on = 0 (default) restores the normal waits.  Returns
+ * PLSTM_EINVAL for other values. */
+int pyramid_lstm_set_wait_test(int on);
+
+
 /* Optional kernel timing for measurement tools (off by default).
  * pyramid_lstm_timing_enable(1) clears earlier records and makes every later
  * call of this library in the process record a pair of HIP events on its

@@ -27,13 +27,15 @@ __all__ = [
     "library_path", "load", "plstm2d_shape", "shape2d_for", "pyramid_lstm2d_workspace_size",
     "pyramid_lstm2d_saved_size", "pyramid_lstm2d_forward", "pyramid_lstm2d_backward",
     "plstm_cube", "PLSTM_FLIP_Z", "PLSTM_FLIP_Y", "PLSTM_FLIP_X", "PLSTM_MAX_CUBES",
-    "pyramid_sample_cubes", "draw_cubes",
+    "pyramid_sample_cubes", "draw_cubes", "pyramid_lstm_device_status",
+    "pyramid_lstm_set_wait_test", "PLSTM_DEVICE_WAIT_GAVE_UP",
 ]
 
 PLSTM_F32 = 0
 PLSTM_BF16 = 1
 PLSTM_FLIP_Z, PLSTM_FLIP_Y, PLSTM_FLIP_X = 1, 2, 4
 PLSTM_MAX_CUBES = 64
+PLSTM_DEVICE_WAIT_GAVE_UP = 1
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_PKG, "libpyramid_lstm.so")
@@ -141,6 +143,10 @@ def load():
                                              ctypes.POINTER(ctypes.c_int),
                                              ctypes.POINTER(ctypes.c_int)]
     lib.pyramid_lstm_timing_read.restype = ctypes.c_int
+    lib.pyramid_lstm_device_status.argtypes = [ctypes.POINTER(ctypes.c_int32), i32, vp]
+    lib.pyramid_lstm_device_status.restype = ctypes.c_int
+    lib.pyramid_lstm_set_wait_test.argtypes = [ctypes.c_int]
+    lib.pyramid_lstm_set_wait_test.restype = ctypes.c_int
     lib.pyramid_lstm_set_bf16_mfma.argtypes = [ctypes.c_int]
     lib.pyramid_lstm_set_bf16_mfma.restype = ctypes.c_int
     lib.pyramid_lstm_set_step_split.argtypes = [ctypes.c_int]
@@ -485,3 +491,19 @@ def pyramid_lstm_set_bf16_mfma(on: int) -> None:
     accumulation) on pixel blocks staged in LDS, 2 = bf16 MFMA reading its
     operands from L1, 0 = fp32 MFMA."""
     _check("pyramid_lstm_set_bf16_mfma", load().pyramid_lstm_set_bf16_mfma(int(on)))
+
+
+def pyramid_lstm_device_status(clear: bool = False, stream=None) -> int:
+    """This device's sticky status bits (synchronises `stream`):
+    PLSTM_DEVICE_WAIT_GAVE_UP when a persistent sweep's bounded wait gave up
+    since the last clear (that call's outputs were overwritten with NaN)."""
+    out = ctypes.c_int32(0)
+    _check("pyramid_lstm_device_status",
+           load().pyramid_lstm_device_status(ctypes.byref(out), int(bool(clear)), _stream(stream)))
+    return int(out.value)
+
+
+def pyramid_lstm_set_wait_test(on: bool) -> None:
+    """Failure-path test mode: every persistent-sweep wait expects a step that
+    is never published and gives up after 16 polls (launches still finish)."""
+    _check("pyramid_lstm_set_wait_test", load().pyramid_lstm_set_wait_test(int(bool(on))))

@@ -36,6 +36,23 @@ size_t step_dx_ws(const Geom &g);
 int step_dx(const Geom &g, const float *wx, const float *dA, float *fragx, float *dx,
             hipStream_t st);
 
+// Outputs overwritten with NaN when a persistent launch's bounded wait gave
+// up (status.hip): up to kMax fp32 arrays, null entries skipped.
+struct PoisonList {
+    static constexpr int kMax = 4;
+    float *ptr[kMax] = {nullptr, nullptr, nullptr, nullptr};
+    long long count[kMax] = {0, 0, 0, 0};
+};
+// Enqueues the check after a persistent launch whose error word is `err`.
+int wait_check(const int *err, const PoisonList &pl, hipStream_t st);
+// This device's sticky status word (null on a HIP error).
+int *device_status_word();
+// Bounded waits of the persistent sweeps: polls before giving up, and the
+// bias added to the step a wait expects (non-zero only in the failure-path
+// test mode, pyramid_lstm_set_wait_test).
+extern int g_wait_spin_limit;
+extern int g_wait_bias;
+
 // h = sum of the six per-direction outputs (generic.hip).
 int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st);
 

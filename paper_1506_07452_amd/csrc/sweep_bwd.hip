@@ -41,7 +41,6 @@ constexpr int kThreads = 64 * kWaves;
 __device__ inline int swz(int c, int pix) { return c ^ (pix & 15); }
 constexpr int kOutOfRange = 0x7ffffff0;    // buffer offset past any resource: reads zero
 typedef __attribute__((address_space(3))) void lds_void;
-constexpr int kMaxSpin = 1 << 21;
 constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unconstrained
 
 __device__ inline float frcp(float v) { return __builtin_amdgcn_rcpf(v); }
@@ -58,6 +57,8 @@ struct BwdArgs {
     float *dA;                   // [6][N][V][64] gate pre-activation gradients
     float *gcf;                  // [6][N][V][16] dL/dc_t * f_t, carried to plane t - 1
     int *flags, *err;
+    int max_spin;                // polls before a wait gives up
+    int wait_bias;               // added to the awaited step (0; failure-path test mode only)
     int nstrip[kDirs], first[kDirs], chunk_rows[kDirs], max_w[kDirs];
     int resident[kDirs];         // 1: the strip's dA stays in LDS for the sweep
 };
@@ -173,9 +174,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                 if (nb >= 0) {
                     int spins = 0;
                     while (__hip_atomic_load(&a.flags[nb], __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT) < r) {
+                                             __HIP_MEMORY_SCOPE_AGENT) < r + a.wait_bias) {
                         __builtin_amdgcn_s_sleep(1);
-                        if (++spins > kMaxSpin) {
+                        if (++spins > a.max_spin) {
                             __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED,
                                                __HIP_MEMORY_SCOPE_AGENT);
                             break;
@@ -330,9 +331,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
             if (nb >= 0) {
                 int spins = 0;
                 while (__hip_atomic_load(&a.flags[nb], __ATOMIC_RELAXED,
-                                         __HIP_MEMORY_SCOPE_AGENT) < r) {
+                                         __HIP_MEMORY_SCOPE_AGENT) < r + a.wait_bias) {
                     __builtin_amdgcn_s_sleep(1);
-                    if (++spins > kMaxSpin) {
+                    if (++spins > a.max_spin) {
                         __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                         break;
                     }
@@ -828,6 +829,8 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     args.dh = dh;
     args.dA = dA; args.gcf = gcf;
     args.flags = flags; args.err = flags + 1024;
+    args.max_spin = g_wait_spin_limit;
+    args.wait_bias = g_wait_bias;
     for (int d = 0; d < kDirs; ++d) {
         args.nstrip[d] = pl.nstrip[d];
         args.first[d] = pl.first[d];
@@ -866,8 +869,16 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
                                                        partial, dwx, dwh, db);
     PLSTM_LAUNCH_CHECK();
     timing_end(2, st);
-    if (dx) return fragx ? step_dx(g, wx, dA, fragx, dx, st) : generic_dx(g, wx, dA, dx, st);
-    return PLSTM_OK;
+    if (dx) {
+        rc = fragx ? step_dx(g, wx, dA, fragx, dx, st) : generic_dx(g, wx, dA, dx, st);
+        if (rc != PLSTM_OK) return rc;
+    }
+    PoisonList poison;
+    poison.ptr[0] = dwx; poison.count[0] = (long long)kDirs * kG * g.C * 9;
+    poison.ptr[1] = dwh; poison.count[1] = (long long)kDirs * kG * kO * 9;
+    poison.ptr[2] = db;  poison.count[2] = (long long)kDirs * kG;
+    poison.ptr[3] = dx;  poison.count[3] = dx ? (long long)g.N * g.V * g.C : 0;
+    return wait_check(args.err, poison, st);
 }
 
 }  // namespace plstm

@@ -48,7 +48,6 @@ constexpr int kWaves = 16;         // four waves per SIMD: gate math of some ove
 constexpr int kWhFloats = 9 * 4 * 64 * 4;   // recurrent A fragments in LDS
 constexpr int kThreads = 64 * kWaves;
 constexpr int kHS = 20;          // LDS floats per staged h pixel (16 + 4 pad)
-constexpr int kMaxSpin = 1 << 21;
 constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt vmcnt(0), other counters unconstrained
 constexpr int kBatch = 4;        // staging loads in flight per thread
 constexpr int kCS = 20;          // LDS floats per cell state of a resident strip (16 + 4 pad)
@@ -62,6 +61,8 @@ struct SweepArgs {
     float *gates;       // [6][N][V][64] or null
     int *flags;         // [blocks] completed steps per strip
     int *err;           // set when a wait gives up
+    int max_spin;       // polls before a wait gives up
+    int wait_bias;      // added to the awaited step (0; failure-path test mode only)
     int nstrip[kDirs];  // strips per (direction, batch element)
     int first[kDirs];   // first block of direction d
     int chunk_rows[kDirs];  // rows staged per LDS chunk, per direction
@@ -94,9 +95,9 @@ __device__ inline void wait_neighbours(const SweepArgs &a, int nb_lo, int nb_hi,
     if (nb >= 0) {
         int spins = 0;
         while (__hip_atomic_load(&a.flags[nb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
-               step) {
+               step + a.wait_bias) {
             __builtin_amdgcn_s_sleep(1);
-            if (++spins > kMaxSpin) {
+            if (++spins > a.max_spin) {
                 __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 break;
             }
@@ -586,6 +587,8 @@ int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     args.hd = hd; args.cell = cell; args.gates = gates;
     args.flags = flags;
     args.err = flags + 1024;
+    args.max_spin = g_wait_spin_limit;
+    args.wait_bias = g_wait_bias;
     for (int d = 0; d < kDirs; ++d) {
         args.nstrip[d] = pl.nstrip[d];
         args.first[d] = pl.first[d];
@@ -607,7 +610,11 @@ int sweep_fwd(const Geom &g, const float *x, const float *wx, const float *wh, c
     default: rc = launch_sweep<4>(pl, args, st); break;
     }
     timing_end(1, st);
-    return rc;
+    if (rc != PLSTM_OK) return rc;
+    PoisonList poison;
+    poison.ptr[0] = hd;
+    poison.count[0] = (long long)saved_state_count(g);
+    return wait_check(args.err, poison, st);
 }
 
 }  // namespace plstm

@@ -189,6 +189,16 @@ def test_path_knobs_and_timing_without_gpu():
     P.pyramid_lstm_timing_enable(False)
 
 
+def test_wait_test_knob_and_status_validation(lib):
+    """The failure-path knob takes 0 or 1 only; the status query rejects a
+    null output before touching HIP."""
+    P.pyramid_lstm_set_wait_test(True)
+    P.pyramid_lstm_set_wait_test(False)
+    assert lib.pyramid_lstm_set_wait_test(2) == -1
+    assert lib.pyramid_lstm_set_wait_test(-1) == -1
+    assert lib.pyramid_lstm_device_status(None, 0, None) == -1
+
+
 def test_rmsprop_validation(lib):
     """Argument checks of the optimiser entry point (no GPU work: an update
     of zero elements returns before any launch)."""

@@ -558,3 +558,46 @@ def test_repeat_runs_bitwise_identical():
     torch.cuda.synchronize()
     assert all(torch.equal(outs[0], o) for o in outs[1:])
     assert all(torch.equal(a, b) for a, b in zip(grads[0], grads[1]))
+
+
+def test_wait_that_gives_up_is_reported():
+    """A persistent sweep whose bounded wait gives up cannot return an error
+    code (the call has returned): its outputs become NaN and the device's
+    sticky status reports it.  The test mode makes every wait expect a step
+    that is never published, so each launch takes that path and still ends
+    normally; afterwards the status clears and results are right again."""
+    shape = (1, 12, 64, 50, 1, 16)          # 7-50 strips per direction in both sweeps
+    inst = instance(shape, 77)
+    L = inst.layers[0]
+    x, Ld = dev(inst.x), layer_dev(L)
+    dh = dev(synth.upstream_grad(shape[:4] + (16,), 78))
+    say("wait failure path: clean run")
+    P.pyramid_lstm_device_status(clear=True)
+    h_ok, _ = layer_forward(x, Ld)
+    assert P.pyramid_lstm_device_status() == 0
+    say("wait failure path: test mode")
+    P.pyramid_lstm_set_wait_test(True)
+    try:
+        h_bad, saved = layer_forward(x, Ld, training=True)
+        torch.cuda.synchronize()
+        st_fwd = P.pyramid_lstm_device_status(clear=True)
+        grads = layer_backward(x, Ld, saved, dh)
+        torch.cuda.synchronize()
+        st_bwd = P.pyramid_lstm_device_status(clear=True)
+    finally:
+        P.pyramid_lstm_set_wait_test(False)
+    assert st_fwd == P.PLSTM_DEVICE_WAIT_GAVE_UP
+    assert st_bwd == P.PLSTM_DEVICE_WAIT_GAVE_UP
+    assert torch.isnan(h_bad).all()
+    for g in grads:
+        assert torch.isnan(g).all()
+    say("wait failure path: clean again")
+    assert P.pyramid_lstm_device_status() == 0
+    h2, saved2 = layer_forward(x, Ld, training=True)
+    grads2 = layer_backward(x, Ld, saved2, dh)
+    torch.cuda.synchronize()
+    assert P.pyramid_lstm_device_status() == 0
+    assert torch.equal(h2, h_ok)
+    ref = oracle.backward(inst.x, L.wx, L.wh, L.b, host(dh))
+    for name, got in zip(("dx", "dwx", "dwh", "db"), grads2):
+        assert normwise(host(got), ref[name]) <= TOL["f32"], name

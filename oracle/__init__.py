@@ -21,20 +21,28 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# PLSTM_ORACLE_LIB selects another build of oracle.c (the sanitizer test
+# loads the ASan/UBSan one through it)
+_LIB = os.environ.get("PLSTM_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
+SAN_LIB = os.path.join(_HERE, "liboracle_san.so")
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+             "-fno-omit-frame-pointer", "-g"]
 
 _lib = None
 
 
-def build(force: bool = True) -> str:
-    """Compile oracle.c with gcc (-O2, OpenMP) into liboracle.so, in-tree."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp%d" % os.getpid()
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile oracle.c with gcc (-O2, OpenMP) into liboracle.so, in-tree;
+    with `sanitize`, an AddressSanitizer + UndefinedBehaviorSanitizer build
+    into liboracle_san.so instead (host code only)."""
+    out = SAN_LIB if sanitize else _LIB
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp%d" % os.getpid()
         subprocess.check_call(
-            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
-             "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
-        os.replace(tmp, _LIB)
-    return _LIB
+            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall", "-Wextra"] +
+            (SAN_FLAGS if sanitize else []) + ["-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, out)
+    return out
 
 
 def _load():

@@ -1,33 +1,35 @@
 #!/usr/bin/env python3
 """Benchmark of the PyraMiD-LSTM hot path on one MI355X; prints one JSON line.
 
-Workload: the MR-like volume 48 x 240 x 240 x 3 (seeded, synthetic; stands in
-for the MRBrainS13 stacks), one PyraMiD-LSTM layer with 16 hidden units and
-3x3 filters (six directions summed), fp32.
-
-A timed step is one pass of the whole hot path: layer forward (six sweeps,
-saving activations), per-voxel FC tanh (16 -> 32), linear + softmax +
-cross-entropy head against seeded labels, and back-propagation through all of
-it (head, FC, the six reverse sweeps, parameter and input gradients).  The
-layer forward alone (inference, the single-layer forward workload) is timed as
-well and reported under "fwd".  Inputs are resident in HBM before timing.
+Default run (the five workloads of the layer, seeded and synthetic; the MR
+and EM shapes stand in for the MRBrainS13 and ISBI 2012 stacks of Section 3):
+  value / ms_per_step  config 5: MR-like 48 x 240 x 240 x 3 volume, two
+                       PyraMiD-LSTM layers (16, 32 hidden units, 3x3) each
+                       followed by FC tanh (32, 64), linear + softmax over 4
+                       classes, mean cross-entropy; forward + backward, fp32
+                       (one timed step = one pass of the whole hot path)
+  fwd                  config 2: the single-layer inference forward (six
+                       sweeps + their sum) on the MR-like volume, fp32
+  configs["3"]         config 3: EM-like 30 x 512 x 512 x 1 stack, one layer,
+                       inference forward, fp32
+  configs["4"]         config 4: 8 x 64^3 x 3, three layers (16, 32, 64) + FC
+                       tanh + softmax, bf16 storage / fp32 accumulation, forward
+  cpu_baseline         the fp64 oracle on the host cores (bounded samples)
+Inputs are resident in HBM before timing.  Each figure carries the roofline
+of its dominant kernel (algorithmic flops per launch / HIP-event launch time).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 
-Two more workloads can be timed instead (not the headline; no CPU baseline):
-    --workload stacked-bf16   8 x 64^3 x 3, three layers (16, 32, 64) + FC tanh
-                              + softmax, bf16 storage, forward
-    --workload train-2layer   48 x 240 x 240 x 3, two layers (16, 32) + FC tanh
-                              + softmax cross-entropy, fp32, forward + backward
-    --workload em-layer       30 x 512 x 512 x 1 EM-like stack, one layer (16),
-                              fp32, forward (inference)
-    --workload image-2d       the same 30 slices as a batch of 512 x 512 images
-                              through one 2D layer (16 units, 3 taps), fp32,
-                              forward + backward
-    --workload paper-net      the network of the paper's experiments (7x7
-                              filters, 16 / FC 25 / 32 / FC 45 / 64 -> output)
-                              on a 25 x 240 x 240 x 5 MR sub-volume, softmax
-                              cross-entropy, fp32, forward + backward
+Single workloads can be timed instead (--workload; not the headline):
+    mr-layer      48 x 240 x 240 x 3, one layer (16) + FC tanh + softmax-CE,
+                  fp32, forward + backward, with the config-2 forward
+    stacked-bf16  config 4 alone          train-2layer  config 5 alone
+    em-layer      config 3 alone
+    image-2d      the 30 EM-like slices as a batch of 512 x 512 images through
+                  one 2D layer (16 units, 3 taps), fp32, forward + backward
+    paper-net     the network of the paper's experiments (7x7 filters,
+                  16 / FC 25 / 32 / FC 45 / 64 -> output) on a 25 x 240 x 240 x 5
+                  MR sub-volume, squared loss, fp32, forward + backward + update
 """
 from __future__ import annotations
 
@@ -152,13 +154,42 @@ def network_roofline(phases, passes, V, shapes, dtype, K=3):
             "avg_launch_ms": round(ms / launches, 4)}
 
 
-def bench_network(args, cfg):
-    """Configs 4 (stacked, bf16 storage, forward) and 5 (two layers, fp32,
-    training step), or the paper's network (cfg None), through the same entry
-    points."""
+def timed(step, args):
+    """W untimed warm-up steps, then K steps bracketed by device
+    synchronisation; per-phase HIP-event times of the K steps.  Raises if a
+    persistent sweep reported a failed wait on the way."""
+    import torch
+    import paper_1506_07452_amd as P
+    P.pyramid_lstm_device_status(clear=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    P.pyramid_lstm_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / args.steps
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    status = P.pyramid_lstm_device_status(clear=True)
+    if status:
+        raise RuntimeError("a persistent sweep's wait gave up during the run (status %d)"
+                           % status)
+    return t, phases
+
+
+def phases_per_step(phases, steps):
+    return {k: round(v[0] / steps, 4) for k, v in phases.items()}
+
+
+def measure_network(args, cfg):
+    """Config 4 (stacked, bf16 storage, forward), config 5 (two layers, fp32,
+    training step) or the paper's network (cfg None), through the same entry
+    points.  Returns (seconds per pass, phases, workload, config dict)."""
     import torch
     import synth
-    import paper_1506_07452_amd as P
     from paper_1506_07452_amd.network import (LayerW, network_forward, network_train_step,
                                               workspace_for_layers)
     inst = synth.config(cfg) if cfg is not None else synth.make(synth.PAPER_NET)
@@ -168,7 +199,6 @@ def bench_network(args, cfg):
     def dev(a):
         return torch.from_numpy(a).to("cuda:0").to(tdt).contiguous()
 
-    torch.cuda.init()
     x = dev(inst.x)
     layers = [LayerW(dev(L.wx), dev(L.wh), dev(L.b)) for L in inst.layers]
     fcs = [(dev(w), dev(b)) for w, b in inst.fcs]
@@ -197,79 +227,171 @@ def bench_network(args, cfg):
             return g
         return network_forward(x, layers, fcs, head, ws=ws)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    P.pyramid_lstm_timing_enable(True)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t = (time.perf_counter() - t0) / args.steps
-    phases = P.pyramid_lstm_timing_read()
-    P.pyramid_lstm_timing_enable(False)
-    V = wl.voxels
-    shapes = wl.layer_shapes()
-    vdu = wl.vdu_per_pass()
-    out = {
-        "metric": METRIC, "value": vdu / t, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": t * 1e3, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None,
-        "dtype": wl.dtype,
-        "data": "synthetic",
-        "config": {"workload": wl.name + (" (squared loss)" if opt is not None else "") +
-                               (", fwd+bwd" if train else ", fwd") +
-                               (" + RMS-prop update" if opt is not None else ""),
-                   "N": wl.N,
-                   "D": wl.D, "H": wl.H, "W": wl.W, "C": wl.C, "hidden": wl.hidden,
-                   "fc": [wl.fc_width(i) for i in range(len(wl.hidden))], "K": wl.K,
-                   "storage": wl.dtype, "classes": wl.classes},
-        "tflops": wl.flops_per_pass() / t / 1e12 if not train else None,
-        "roofline": network_roofline(phases, args.steps, V, shapes, wl.dtype, wl.K),
-        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
+    t, phases = timed(step, args)
+    conf = {"workload": wl.name + (" (squared loss)" if opt is not None else "") +
+                        (", fwd+bwd" if train else ", fwd") +
+                        (" + RMS-prop update" if opt is not None else ""),
+            "N": wl.N, "D": wl.D, "H": wl.H, "W": wl.W, "C": wl.C, "hidden": wl.hidden,
+            "fc": [wl.fc_width(i) for i in range(len(wl.hidden))], "K": wl.K,
+            "storage": wl.dtype, "classes": wl.classes}
+    del x, layers, fcs, head, labels, ws, step, opt
+    torch.cuda.empty_cache()
+    return t, phases, wl, conf
+
+
+def network_summary(args, cfg):
+    """A network workload as a JSON object: time, updates/s, contraction
+    TFLOP/s and the roofline of its slowest phase."""
+    t, phases, wl, conf = measure_network(args, cfg)
+    train = wl.labels
+    return {
+        "config": conf, "ms_per_pass": round(t * 1e3, 4), "value": wl.vdu_per_pass() / t,
+        "unit": UNIT, "dtype": wl.dtype,
+        "tflops": None if train else round(wl.flops_per_pass() / t / 1e12, 3),
+        "roofline": network_roofline(phases, args.steps, wl.voxels, wl.layer_shapes(),
+                                     wl.dtype, wl.K),
+        "phases_ms_per_step": phases_per_step(phases, args.steps),
     }
+
+
+def layer_forward_summary(args, cfg):
+    """Configs 2 and 3: one layer's inference forward (six sweeps and their
+    sum), fp32.  Returns a JSON object with the forward sweep's roofline."""
+    import torch
+    import synth
+    from paper_1506_07452_amd.network import LayerW, layer_forward, workspace_for
+    inst = synth.config(cfg)
+    wl = inst.wl
+    x = torch.from_numpy(inst.x).to("cuda:0").contiguous()
+    L = inst.layers[0]
+    Ld = LayerW(*(torch.from_numpy(a).to("cuda:0").contiguous() for a in (L.wx, L.wh, L.b)))
+    ws = workspace_for(x.shape, wl.hidden, False, torch.float32, False, "cuda:0")
+    torch.cuda.synchronize()
+    t, phases = timed(lambda: layer_forward(x, Ld, False, ws=ws), args)
+    N, D, H, W, C = inst.x.shape
+    O = wl.hidden[0]
+    V = N * D * H * W
+    flops = 6 * V * 2 * 9 * 4 * O * (C + O)
+    name = next(k for k in phases if k.startswith("sweep_fwd"))
+    roof = roofline(phases, name, args.steps, V, C, O, mode="inference")
+    if cfg != 2:
+        roof["traffic"] = None     # the committed counters cover the MR volume only
+    del x, Ld, ws
+    torch.cuda.empty_cache()
+    return {"config": {"workload": wl.name, "N": N, "D": D, "H": H, "W": W, "C": C, "O": O},
+            "ms_per_pass": round(t * 1e3, 4), "value": 6 * V / t, "unit": UNIT, "dtype": "f32",
+            "tflops": round(flops / t / 1e12, 3),
+            "frac_fp32_mfma_peak": round(flops / t / 1e12 / PEAK_FP32_TFLOPS, 4),
+            "roofline": roof, "phases_ms_per_step": phases_per_step(phases, args.steps)}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_legs(threads_all):
+    """The fp64 oracle, as it stands, on the host cores: bounded samples of
+    the headline training step and of the config-2 forward (all threads), and
+    single-thread forwards of configs 1-3 on bounded crops.  Each leg reports
+    voxel-direction updates per second of what it ran."""
+    import numpy as np
+    import oracle
+    import oracle.network as onet
+    import synth
+
+    legs = []
+
+    def leg(cfg, crop, threads, what, fn, x):
+        oracle.set_threads(threads)
+        t0 = time.perf_counter()
+        fn()
+        dt = time.perf_counter() - t0
+        nvox = int(np.prod(x.shape[:4]))
+        layers = len(synth.CONFIGS[cfg].hidden)
+        legs.append({"config": cfg, "what": what, "sample": "x".join(map(str, x.shape[1:4])) +
+                     ("" if crop is None else " crop"), "threads": threads,
+                     "seconds": round(dt, 2), "value": 6 * nvox * layers / dt})
+
+    inst5 = synth.config(5)
+    x5 = np.ascontiguousarray(inst5.x[:, :, :60, :60])
+    lab5 = inst5.labels.reshape(inst5.x.shape[:4])[:, :, :60, :60].reshape(-1)
+    lw5 = [(L.wx, L.wh, L.b) for L in inst5.layers]
+    leg(5, (48, 60, 60), threads_all, "training step fwd+bwd (2 layers, FC, softmax-CE)",
+        lambda: onet.backward(x5, lw5, inst5.fcs, inst5.head, lab5), x5)
+    inst2 = synth.config(2)
+    L2 = inst2.layers[0]
+    leg(2, None, threads_all, "layer forward",
+        lambda: oracle.forward(inst2.x, L2.wx, L2.wh, L2.b), inst2.x)
+    inst1 = synth.config(1)
+    L1 = inst1.layers[0]
+    leg(1, None, 1, "layer forward", lambda: oracle.forward(inst1.x, L1.wx, L1.wh, L1.b),
+        inst1.x)
+    x2c = np.ascontiguousarray(inst2.x[:, :, :40, :40])
+    leg(2, (48, 40, 40), 1, "layer forward", lambda: oracle.forward(x2c, L2.wx, L2.wh, L2.b),
+        x2c)
+    inst3 = synth.config(3)
+    L3 = inst3.layers[0]
+    x3c = np.ascontiguousarray(inst3.x[:, :, :56, :56])
+    leg(3, (30, 56, 56), 1, "layer forward", lambda: oracle.forward(x3c, L3.wx, L3.wh, L3.b),
+        x3c)
+    oracle.set_threads(threads_all)
+    head = legs[0]
+    return {"value": head["value"], "unit": UNIT, "cores": head["threads"], "kind": "oracle",
+            "sample": "oracle fp64 config-5 training step (2 layers fwd+bwd, FC tanh, "
+                      "softmax-CE) on the 48x60x60 corner crop of the same volume, %.1f s on "
+                      "%d threads" % (head["seconds"], head["threads"]),
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(), "legs": legs}
+
+
+def bench_all(args):
+    """The default run: config 5 as the headline, configs 2, 3, 4 beside it."""
+    import torch
+    torch.cuda.init()
+    t5, phases5, wl5, conf5 = measure_network(args, 5)
+    out = {
+        "metric": METRIC, "value": wl5.vdu_per_pass() / t5, "unit": UNIT, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": t5 * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic", "config": conf5,
+        "roofline": network_roofline(phases5, args.steps, wl5.voxels, wl5.layer_shapes(),
+                                     wl5.dtype, wl5.K),
+        "phases_ms_per_step": phases_per_step(phases5, args.steps),
+    }
+    out["fwd"] = layer_forward_summary(args, 2)
+    out["configs"] = {"3": layer_forward_summary(args, 3), "4": network_summary(args, 4)}
+    if not args.no_cpu_baseline:
+        import oracle
+        out["cpu_baseline"] = cpu_legs(oracle.threads())
+    print(json.dumps(out), flush=True)
+
+
+def bench_network(args, cfg):
+    """One network workload as the whole JSON line."""
+    s = network_summary(args, cfg)
+    out = {"metric": METRIC, "value": s["value"], "unit": UNIT, "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": s["ms_per_pass"],
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": s["dtype"], "data": "synthetic", "config": s["config"],
+           "tflops": s["tflops"], "roofline": s["roofline"],
+           "phases_ms_per_step": s["phases_ms_per_step"]}
     print(json.dumps(out), flush=True)
 
 
 def bench_em(args):
     """The EM-like stack (ISBI 2012 shape) through one layer, inference
     forward: six sweeps and their sum."""
-    import torch
-    import synth
-    import paper_1506_07452_amd as P
-    from paper_1506_07452_amd.network import LayerW, layer_forward, workspace_for
-    inst = synth.config(3)
-    wl = inst.wl
-    torch.cuda.init()
-    x = torch.from_numpy(inst.x).to("cuda:0").contiguous()
-    L = inst.layers[0]
-    Ld = LayerW(*(torch.from_numpy(a).to("cuda:0").contiguous() for a in (L.wx, L.wh, L.b)))
-    ws = workspace_for(x.shape, wl.hidden, False, torch.float32, False, "cuda:0")
-    for _ in range(args.warmup):
-        layer_forward(x, Ld, False, ws=ws)
-    torch.cuda.synchronize()
-    P.pyramid_lstm_timing_enable(True)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        layer_forward(x, Ld, False, ws=ws)
-    torch.cuda.synchronize()
-    t = (time.perf_counter() - t0) / args.steps
-    phases = P.pyramid_lstm_timing_read()
-    P.pyramid_lstm_timing_enable(False)
-    N, D, H, W, C = inst.x.shape
-    O = wl.hidden[0]
-    V = N * D * H * W
-    name = next(k for k in phases if k.startswith("sweep_fwd"))
-    out = {
-        "metric": METRIC, "value": 6 * V / t, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": t * 1e3, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": wl.name, "N": N, "D": D, "H": H, "W": W, "C": C, "O": O},
-        "tflops": 6 * V * 2 * 9 * 4 * O * (C + O) / t / 1e12,
-        "roofline": roofline(phases, name, args.steps, V, C, O, mode="inference"),
-        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
-    }
-    out["roofline"]["traffic"] = None     # the committed counters cover the MR volume only
+    s = layer_forward_summary(args, 3)
+    out = {"metric": METRIC, "value": s["value"], "unit": UNIT, "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": s["ms_per_pass"],
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic", "config": s["config"], "tflops": s["tflops"],
+           "roofline": s["roofline"], "phases_ms_per_step": s["phases_ms_per_step"]}
     print(json.dumps(out), flush=True)
 
 
@@ -293,17 +415,7 @@ def bench_2d(args):
         h, saved = layer2d_forward(xd, L, training=True, ws=ws)
         return layer2d_backward(xd, L, saved, dh, ws=ws)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    P.pyramid_lstm_timing_enable(True)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t = (time.perf_counter() - t0) / args.steps
-    phases = P.pyramid_lstm_timing_read()
-    P.pyramid_lstm_timing_enable(False)
+    t, phases = timed(step, args)
     V = N * H * W
     # algorithmic flops per pixel-direction: forward 2 K 4O (C + O); reverse
     # 2 K 4O O; weight gradients 2 4O (K (C + O) + 1); dL/dx 2 K 4O C
@@ -331,8 +443,8 @@ def bench_2d(args):
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(inst_cfg, crop):
-    """The fp64 oracle (as is) on a bounded crop of the same workload."""
+def cpu_baseline_step(inst_cfg, crop):
+    """The fp64 oracle (as is) on a bounded crop of the single-layer step."""
     import numpy as np
     import oracle
     import oracle.network as onet
@@ -345,55 +457,20 @@ def cpu_baseline(inst_cfg, crop):
     dt = time.perf_counter() - t0
     vdu = 6 * int(np.prod(x.shape[:4]))
     return {"value": vdu / dt, "unit": UNIT, "cores": oracle.threads(), "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": "oracle fp64 training step (layer fwd+bwd, FC tanh, softmax-CE) on a "
                       "%dx%dx%dx%d crop of the same volume, %.1f s" % (D, H, W, x.shape[-1], dt)}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-crop", default="48x120x120")
-    ap.add_argument("--separate-head", action="store_true",
-                    help="run the FC / softmax head as separate kernels instead of the fused one")
-    ap.add_argument("--workload", default="mr-layer",
-                    choices=["mr-layer", "em-layer", "image-2d", "stacked-bf16",
-                             "train-2layer", "paper-net"],
-                    help="mr-layer: the headline single-layer MR workload (default)")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="first copy 1 GiB device-to-device three times (a plain copy kernel "
-                         "of known size, to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the six sweeps of a layer run concurrently "
-              "on a single MI355X and this build has no multi-GPU path (--gpus 1).",
-              file=sys.stderr)
-        sys.exit(2)
-    if args.workload == "em-layer":
-        bench_em(args)
-        return
-    if args.workload == "image-2d":
-        bench_2d(args)
-        return
-    if args.workload != "mr-layer":
-        bench_network(args, {"stacked-bf16": 4, "train-2layer": 5, "paper-net": None}[
-            args.workload])
-        return
-
+def bench_mr_layer(args):
+    """48 x 240 x 240 x 3, one layer (16) + FC tanh 32 + softmax-CE, fp32,
+    forward + backward, with the config-2 inference forward beside it."""
     import torch
     import synth
-    import paper_1506_07452_amd as P
-    from paper_1506_07452_amd.network import (layer_forward, network_train_step,
-                                              workspace_for)
-    from paper_1506_07452_amd.network import LayerW
+    from paper_1506_07452_amd.network import LayerW, network_train_step, workspace_for
 
     def dev(a):
         return torch.from_numpy(a).to("cuda:0").contiguous()
-
-    def layer_dev(L):
-        return LayerW(dev(L.wx), dev(L.wh), dev(L.b))
 
     wl = synth.Workload("MR-like 48x240x240x3 O=16 step", 1, 48, 240, 240, 3, [16], fc=True,
                         classes=4, labels=True, kind="mr", cfg=2)
@@ -410,7 +487,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     x = dev(inst.x)
-    layers = [layer_dev(L) for L in inst.layers]
+    layers = [LayerW(dev(L.wx), dev(L.wh), dev(L.b)) for L in inst.layers]
     fcs = [(dev(w), dev(b)) for w, b in inst.fcs]
     head = (dev(inst.head[0]), dev(inst.head[1]))
     labels = torch.from_numpy(inst.labels).to("cuda:0")
@@ -421,69 +498,63 @@ def main():
         return network_train_step(x, layers, fcs, head, labels, ws=ws,
                                   fused_head=not args.separate_head)
 
-    def fwd():
-        return layer_forward(x, layers[0], False, ws=ws)
-
-    # --- fwd+bwd (headline) ---
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    P.pyramid_lstm_timing_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t_step = (time.perf_counter() - t0) / args.steps
-    phases = P.pyramid_lstm_timing_read()
-    P.pyramid_lstm_timing_enable(False)
-
-    # --- forward only ---
-    for _ in range(args.warmup):
-        fwd()
-    torch.cuda.synchronize()
-    P.pyramid_lstm_timing_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        fwd()
-    torch.cuda.synchronize()
-    t_fwd = (time.perf_counter() - t0) / args.steps
-    phases_fwd = P.pyramid_lstm_timing_read()
-    P.pyramid_lstm_timing_enable(False)
-
-    vdu = 6 * V
-    fwd_flops = 6 * V * 2 * 9 * 4 * O * (C + O)
+    t_step, phases = timed(step, args)
+    del x, layers, fcs, head, labels, ws
+    torch.cuda.empty_cache()
     dom = max(phases, key=lambda k: phases[k][0])
-    sweep_fwd_name = [k for k in phases_fwd if k.startswith("sweep_fwd")][0]
     out = {
-        "metric": METRIC,
-        "value": vdu / t_step,
-        "unit": UNIT,
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": t_step * 1e3,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
+        "metric": METRIC, "value": 6 * V / t_step, "unit": UNIT, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": t_step * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": "MR-like 48x240x240x3 volume, one PyraMiD-LSTM layer (O=16, "
                                "3x3, 6 directions) + FC tanh 32 + softmax-CE head, fwd+bwd",
                    "N": N, "D": D, "H": H, "W": W, "C": C, "O": O, "classes": 4},
-        "fwd": {"value": vdu / t_fwd, "ms_per_pass": t_fwd * 1e3,
-                "tflops": fwd_flops / t_fwd / 1e12,
-                "frac_fp32_mfma_peak": fwd_flops / t_fwd / 1e12 / PEAK_FP32_TFLOPS,
-                "roofline": roofline(phases_fwd, sweep_fwd_name, args.steps, V, C, O,
-                                     mode="inference")},
+        "fwd": layer_forward_summary(args, 2),
         "roofline": roofline(phases, dom, args.steps, V, C, O),
-        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
+        "phases_ms_per_step": phases_per_step(phases, args.steps),
     }
     if not args.no_cpu_baseline:
         crop = tuple(int(v) for v in args.cpu_crop.split("x"))
-        out["cpu_baseline"] = cpu_baseline(inst, crop)
+        out["cpu_baseline"] = cpu_baseline_step(inst, crop)
     print(json.dumps(out), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-crop", default="48x120x120",
+                    help="crop of the mr-layer workload's CPU baseline")
+    ap.add_argument("--separate-head", action="store_true",
+                    help="mr-layer: run the FC / softmax head as separate kernels")
+    ap.add_argument("--workload", default="all",
+                    choices=["all", "mr-layer", "em-layer", "image-2d", "stacked-bf16",
+                             "train-2layer", "paper-net"],
+                    help="all: config 5 as the headline with configs 2-4 beside it (default)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="mr-layer: first copy 1 GiB device-to-device three times (a plain "
+                         "copy kernel of known size, to scale rocprofv3 FETCH_SIZE / "
+                         "WRITE_SIZE)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the six sweeps of a layer run concurrently "
+              "on a single MI355X and this build has no multi-GPU path (--gpus 1).",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.workload == "all":
+        bench_all(args)
+    elif args.workload == "mr-layer":
+        bench_mr_layer(args)
+    elif args.workload == "em-layer":
+        bench_em(args)
+    elif args.workload == "image-2d":
+        bench_2d(args)
+    else:
+        bench_network(args, {"stacked-bf16": 4, "train-2layer": 5, "paper-net": None}[
+            args.workload])
 
 
 if __name__ == "__main__":

@@ -66,6 +66,8 @@ def _load():
         lib.oracle_softmax_ce.restype = ctypes.c_double
         lib.oracle_threads.argtypes = []
         lib.oracle_threads.restype = i
+        lib.oracle_set_threads.argtypes = [i]
+        lib.oracle_set_threads.restype = None
         _lib = lib
     return _lib
 
@@ -73,6 +75,11 @@ def _load():
 def threads() -> int:
     """OpenMP threads used by the oracle's parallel loops."""
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads for later oracle calls from this thread."""
+    _load().oracle_set_threads(int(n))
 
 
 def _f64(a):

@@ -90,6 +90,9 @@ static size_t vidx(int D, int H, int W, int n, int z, int y, int x)
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int oracle_threads(void) { return omp_get_max_threads(); }
 
+/* Sets that number for later calls from the calling thread (n >= 1). */
+void oracle_set_threads(int n) { if (n >= 1) omp_set_num_threads(n); }
+
 static double sigmoid(double a) { return 1.0 / (1.0 + exp(-a)); }
 
 /* One direction, one batch element: forward sweep of Eq. (7)-(12).

@@ -2,17 +2,21 @@
 
 Calls only the fp64 oracle (``oracle``, ``oracle.network``) on the seeded
 synthetic workloads of ``synth``; nothing here touches the GPU path.  The
-oracle takes seconds to minutes per workload, too long to rerun inside every
-GPU test, so its results are stored once:
+oracle takes minutes on these workloads, too long to rerun inside every
+GPU test, so its results are stored once (the single-layer workloads 2 and 3
+are compared in full against the oracle run inside their test instead; jobs
+2 and 3 still write their samples for inspection):
 
   cfg2.npz, cfg3.npz  single layer forward: 4096 sampled entries of h, max|h|,
-                      per-slice sums of h and h^2
+                      per-slice sums of h and h^2 (not committed)
   cfg4.npz            3-layer network forward: 4096 sampled voxels of the
                       softmax output, per-class sums
+  cfg4_elem0.npz      the same network's full softmax output for batch
+                      element 0 (64^3 x 4, fp32; 95 s of oracle on 8 cores)
   cfg5.npz            2-layer training step: loss, sampled probabilities and
                       every parameter gradient in full (fp32)
 
-Usage:  python tests/golden/make_golden.py [cfg ...]
+Usage:  python tests/golden/make_golden.py [job ...]   (jobs: 2 3 4 4_elem0 5)
 """
 from __future__ import annotations
 
@@ -60,6 +64,12 @@ def network_forward(cfg):
             "absmax": np.abs(p).max()}
 
 
+def network_forward_element0(cfg):
+    inst = synth.config(cfg)
+    out = onet.forward(inst.x[:1], [_layer_tuple(L) for L in inst.layers], inst.fcs, inst.head)
+    return {"p": out["p"].astype(np.float32)}
+
+
 def training_step(cfg):
     inst = synth.config(cfg)
     g = onet.backward(inst.x, [_layer_tuple(L) for L in inst.layers], inst.fcs, inst.head,
@@ -78,18 +88,20 @@ def training_step(cfg):
                 else v) for k, v in res.items()}
 
 
-JOBS = {2: single_layer, 3: single_layer, 4: network_forward, 5: training_step}
+JOBS = {"2": single_layer, "3": single_layer, "4": network_forward,
+        "4_elem0": network_forward_element0, "5": training_step}
 
 
-def main(cfgs):
-    for cfg in cfgs:
+def main(jobs):
+    for job in jobs:
+        cfg = int(job.split("_")[0])
         t0 = time.time()
-        res = JOBS[cfg](cfg)
-        path = os.path.join(HERE, "cfg%d.npz" % cfg)
+        res = JOBS[job](cfg)
+        path = os.path.join(HERE, "cfg%s.npz" % job)
         np.savez_compressed(path + ".tmp.npz", **res)
         os.replace(path + ".tmp.npz", path)
-        print("cfg%d: %.1f s -> %s" % (cfg, time.time() - t0, path), flush=True)
+        print("cfg%s: %.1f s -> %s" % (job, time.time() - t0, path), flush=True)
 
 
 if __name__ == "__main__":
-    main([int(a) for a in sys.argv[1:]] or [2, 3, 4, 5])
+    main(sys.argv[1:] or ["4", "4_elem0", "5"])

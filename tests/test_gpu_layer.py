@@ -3,6 +3,7 @@ fp64 oracle, plus invariants that hold at any size, through the C ABI."""
 from __future__ import annotations
 
 import os
+import time
 
 import numpy as np
 import pytest
@@ -15,7 +16,6 @@ from paper_1506_07452_amd.network import LayerW, layer_backward, layer_forward
 from tests.gpu_util import DEV, TOL, dev, host, layer_dev, normwise, saved_view, say
 
 pytestmark = pytest.mark.gpu
-GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 # (N, D, H, W, C, O): tiny, ragged (planes not multiples of any tile), several
 # tiles per plane, degenerate extents, every supported O.
@@ -449,32 +449,29 @@ def test_training_forward_and_backward_match_oracle(shape):
         assert err <= TOL["f32"], (name, err)
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("cfg", [1, 2, 3])
 def test_config_forward(cfg):
-    """Configs 1-3 at full size.  Config 1 against the oracle directly; 2 and 3
-    against the oracle's stored results (sampled entries, per-slice sums)."""
+    """Configs 1-3 at full size, every element of h against the oracle run
+    in the test on the host's cores (config 3 takes about a minute there).
+    Prints the largest elementwise error and where it is."""
     inst = synth.config(cfg)
     L = inst.layers[0]
     say("config", cfg)
     h, _ = layer_forward(dev(inst.x), layer_dev(L))
     torch.cuda.synchronize()
-    if cfg == 1:
-        ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
-        assert normwise(host(h), ref) <= TOL["f32"]
-        return
-    gold = np.load(os.path.join(GOLDEN, "cfg%d.npz" % cfg))
-    hv = h.reshape(-1)[torch.from_numpy(gold["idx"]).to(DEV)]
-    err = float(np.abs(host(hv) - gold["val"]).max() / gold["absmax"])
-    assert err <= TOL["f32"], err
-    hh = host(h)
-    N, D = hh.shape[:2]
-    sums = hh.reshape(N * D, -1).sum(1)
-    # a slice sum of V/D entries: allow the per-entry tolerance times sqrt(count)
-    n_per = hh[0, 0].size
-    bound = TOL["f32"] * gold["absmax"] * np.sqrt(n_per) + 1e-6 * np.abs(gold["slice_sum"])
-    assert np.all(np.abs(sums - gold["slice_sum"]) <= bound)
-    sq = (hh.reshape(N * D, -1) ** 2).sum(1)
-    assert np.allclose(sq, gold["slice_sumsq"], rtol=2 * TOL["f32"])
+    got = host(h)
+    del h
+    say("config oracle", cfg, "threads", oracle.threads())
+    t0 = time.time()
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    err = np.abs(got - ref)
+    worst = np.unravel_index(int(np.argmax(err)), err.shape)
+    scale = float(np.abs(ref).max())
+    print("[config %d] oracle %.1f s; max|h| %.4f, max err %.3e at %s (normwise %.3e), "
+          "mean err %.3e" % (cfg, time.time() - t0, scale, err[worst], worst, err[worst] / scale,
+                             err.mean()), flush=True)
+    assert err[worst] / scale <= TOL["f32"]
 
 
 def test_zero_parameters_exact_zero():

@@ -164,3 +164,68 @@ def test_2d_large_image_sampled():
     hd = saved[off:off + cnt_s * 4].view(torch.float32).view(4, N, H, W, O)
     assert normwise(host(hd[0, :, :rows]), ref) <= TOL["f32"]
     assert torch.isfinite(h).all()
+
+
+# The 2D workload that bench.py times: 30 EM-like 512 x 512 slices as images,
+# 16 units, one channel, 3 taps (line blocks of 16 lines per launch).
+BENCH_2D = (30, 512, 512, 1, 16, 3)
+LINES = 40                      # > two 16-line launches
+IMAGES = (0, 13, 29)            # images the oracle checks
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("d", range(4), ids=["y+", "y-", "x+", "x-"])
+def test_2d_line_blocks_at_bench_scale(d):
+    """Direction d alone (the other three given zero parameters, whose output
+    is then exactly zero) over the full bench batch.  The sweep's first 40
+    lines depend only on those lines, and with dL/dh zero everywhere else
+    (other images and later lines) the backward touches nothing else: the
+    oracle on that 40-line crop of three images gives h there, dL/dx there
+    (exactly zero elsewhere) and every parameter gradient.  Full 512-pixel
+    lines cross eight 64-pixel segments and three line-block launches."""
+    N, H, W, C, O, K = BENCH_2D
+    x, wx, wh, b = synth.image2d(N, H, W, C, O, K, seed=2048, scale=0.1)
+    for p in (wx, wh, b):
+        keep = p[d].copy()
+        p[...] = 0.0
+        p[d] = keep
+    rows = d < 2
+    first = d % 2 == 0
+    span = slice(0, LINES) if first else slice((H if rows else W) - LINES, None)
+    crop = (slice(None), span) if rows else (slice(None), slice(None), span)
+    img = list(IMAGES)
+    dh = np.zeros((N, H, W, O), dtype=np.float32)
+    dh_crop = synth.upstream_grad(x[img][crop].shape[:-1] + (O,), 4000 + d)
+    sub = dh[img]
+    sub[crop] = dh_crop
+    dh[img] = sub
+    say("2d bench scale, direction", d)
+    xd, L = dev(x), LayerW(dev(wx), dev(wh), dev(b))
+    P.pyramid_lstm_timing_enable(True)
+    h, saved = layer2d_forward(xd, L, training=True)
+    gdx, gdwx, gdwh, gdb = layer2d_backward(xd, L, saved, dev(dh))
+    phases = P.pyramid_lstm_timing_read()
+    P.pyramid_lstm_timing_enable(False)
+    torch.cuda.synchronize()
+    # the reverse line blocks gave dL/dx: only the sum over directions remains
+    assert "sweep_fwd_step" in phases and phases["dx_step"][1] == 1, phases
+    xc = np.ascontiguousarray(x[img][crop])
+    say("2d bench scale oracle", d)
+    ref_h = o2d.forward2d(xc, wx, wh, b)
+    ref = o2d.backward2d(xc, wx, wh, b, dh_crop)
+    hh = host(h)[img][crop]
+    err_h = normwise(hh, ref_h)
+    dx = host(gdx)
+    dx_crop = dx[img][crop]
+    mask = np.ones(dx.shape, dtype=bool)
+    msub = mask[img]
+    msub[crop] = False
+    mask[img] = msub
+    errs = {"h": err_h, "dx": normwise(dx_crop, ref["dx"]),
+            "dwx": normwise(host(gdwx), ref["dwx"]), "dwh": normwise(host(gdwh), ref["dwh"]),
+            "db": normwise(host(gdb), ref["db"])}
+    print("[2d bench scale] direction %d: %s" % (d, {k: "%.2e" % v for k, v in errs.items()}),
+          flush=True)
+    assert not np.any(dx[mask]), "dL/dx outside the crop must be exactly zero"
+    for k, v in errs.items():
+        assert v <= TOL["f32"], (k, v)

@@ -176,19 +176,25 @@ IMAGES = (0, 13, 29)            # images the oracle checks
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("d", range(4), ids=["y+", "y-", "x+", "x-"])
 def test_2d_line_blocks_at_bench_scale(d):
-    """Direction d alone (the other three given zero parameters, whose output
-    is then exactly zero) over the full bench batch.  The sweep's first 40
-    lines depend only on those lines, and with dL/dh zero everywhere else
-    (other images and later lines) the backward touches nothing else: the
-    oracle on that 40-line crop of three images gives h there, dL/dx there
-    (exactly zero elsewhere) and every parameter gradient.  Full 512-pixel
-    lines cross eight 64-pixel segments and three line-block launches."""
+    """Direction d alone over the full bench batch.  The other three get zero
+    filters and an input-gate bias of -200, so i = 0 exactly in fp32: their
+    h is exactly zero and so is every gate gradient of theirs (with i = 1/2
+    instead, dA_g = dc i (1 - g^2) would carry dL/dc down the opposite sweep
+    of the same axis, past the crop).  The sweep's first 40 lines depend only
+    on those lines, and with dL/dh zero everywhere else (other images and
+    later lines) the backward touches nothing else: the oracle on that
+    40-line crop of three images gives h there, dL/dx there (exactly zero
+    elsewhere) and every parameter gradient.  Full 512-pixel lines cross
+    eight 64-pixel segments and three line-block launches."""
     N, H, W, C, O, K = BENCH_2D
     x, wx, wh, b = synth.image2d(N, H, W, C, O, K, seed=2048, scale=0.1)
     for p in (wx, wh, b):
         keep = p[d].copy()
         p[...] = 0.0
         p[d] = keep
+    for e in range(4):
+        if e != d:
+            b[e, :O] = -200.0
     rows = d < 2
     first = d % 2 == 0
     span = slice(0, LINES) if first else slice((H if rows else W) - LINES, None)

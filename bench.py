@@ -555,6 +555,21 @@ def main():
     else:
         bench_network(args, {"stacked-bf16": 4, "train-2layer": 5, "paper-net": None}[
             args.workload])
+    release_device()
+
+
+def release_device():
+    """Leave nothing of ours on the device at interpreter exit: timing off
+    (its events destroyed), the stream drained, torch's cached blocks
+    returned to the runtime."""
+    import gc
+    import torch
+    import paper_1506_07452_amd as P
+    P.pyramid_lstm_timing_enable(False)
+    torch.cuda.synchronize()
+    gc.collect()
+    torch.cuda.empty_cache()
+    torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

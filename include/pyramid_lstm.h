@@ -58,7 +58,8 @@ enum plstm_status {
     PLSTM_EUNSUPPORTED = -2,    /* valid but not supported (O, dtype, size) */
     PLSTM_EWORKSPACE = -3,      /* ws_bytes smaller than the required size */
     PLSTM_EHIP = -4,            /* a HIP runtime call or launch failed */
-    PLSTM_ENOTCORESIDENT = -5   /* the GPU cannot hold the persistent grid */
+    PLSTM_ENOTCORESIDENT = -5,  /* the GPU cannot hold the persistent grid */
+    PLSTM_ESCRATCH = -6         /* more scratch than pyramid_lstm_forward_noalloc holds */
 };
 
 enum plstm_dtype { PLSTM_F32 = 0, PLSTM_BF16 = 1 };
@@ -108,6 +109,24 @@ size_t pyramid_lstm_saved_size(const plstm_shape *s);
 int pyramid_lstm_forward(const plstm_shape *s, const void *x, const void *wx,
                          const void *wh, const void *b, void *h, void *saved,
                          void *ws, size_t ws_bytes, void *stream);
+
+/* Inference forward for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): pyramid_lstm_forward with saved = NULL, whose workspace is
+ * instead a scratch array that the library holds on every GPU it runs on
+ * (PLSTM_NOALLOC_SCRATCH_BYTES per GPU, until the process ends).  The call
+ * allocates nothing.  Arguments, layouts and results are those of
+ * pyramid_lstm_forward.  Returns PLSTM_ESCRATCH when the shape needs more
+ * than the scratch (pyramid_lstm_workspace_size(s, 0) tells); e.g. a layer
+ * of 16 units with C <= 4 needs about 840 bytes per voxel, so a 64^3 volume
+ * (262 k voxels) fits.  Every call on a GPU uses
+ * that GPU's one array, so calls that overlap on one GPU (other streams, or
+ * other host threads) race and must be serialised by the caller; a call on
+ * one stream after another needs nothing more, since each call writes the
+ * scratch before reading it. */
+#define PLSTM_NOALLOC_SCRATCH_BYTES (256u << 20)
+int pyramid_lstm_forward_noalloc(const plstm_shape *s, const void *x, const void *wx,
+                                 const void *wh, const void *b, void *h, void *stream);
 
 /* Backward pass of one layer: back-propagation through the six sweeps (the
  * chain rule through Eq. (7)-(13); the paper trains the layer by gradient

@@ -28,7 +28,8 @@ __all__ = [
     "pyramid_lstm2d_saved_size", "pyramid_lstm2d_forward", "pyramid_lstm2d_backward",
     "plstm_cube", "PLSTM_FLIP_Z", "PLSTM_FLIP_Y", "PLSTM_FLIP_X", "PLSTM_MAX_CUBES",
     "pyramid_sample_cubes", "draw_cubes", "pyramid_lstm_device_status",
-    "pyramid_lstm_set_wait_test", "PLSTM_DEVICE_WAIT_GAVE_UP",
+    "pyramid_lstm_set_wait_test", "PLSTM_DEVICE_WAIT_GAVE_UP", "pyramid_lstm_forward_noalloc",
+    "PLSTM_NOALLOC_SCRATCH_BYTES", "PLSTM_ESCRATCH",
 ]
 
 PLSTM_F32 = 0
@@ -36,6 +37,8 @@ PLSTM_BF16 = 1
 PLSTM_FLIP_Z, PLSTM_FLIP_Y, PLSTM_FLIP_X = 1, 2, 4
 PLSTM_MAX_CUBES = 64
 PLSTM_DEVICE_WAIT_GAVE_UP = 1
+PLSTM_NOALLOC_SCRATCH_BYTES = 256 << 20
+PLSTM_ESCRATCH = -6
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_PKG, "libpyramid_lstm.so")
@@ -94,6 +97,8 @@ def load():
     lib.pyramid_lstm_saved_size.restype = sz
     lib.pyramid_lstm_forward.argtypes = [sp] + [vp] * 7 + [sz, vp]
     lib.pyramid_lstm_forward.restype = ctypes.c_int
+    lib.pyramid_lstm_forward_noalloc.argtypes = [sp] + [vp] * 6
+    lib.pyramid_lstm_forward_noalloc.restype = ctypes.c_int
     lib.pyramid_lstm_backward.argtypes = [sp] + [vp] * 11 + [sz, vp]
     lib.pyramid_lstm_backward.restype = ctypes.c_int
     sp2 = ctypes.POINTER(plstm2d_shape)
@@ -231,6 +236,14 @@ def pyramid_lstm_forward(shape, x, wx, wh, b, h, saved=None, ws=None, stream=Non
     _check("pyramid_lstm_forward", lib.pyramid_lstm_forward(
         ctypes.byref(shape), _ptr(x), _ptr(wx), _ptr(wh), _ptr(b), _ptr(h), _ptr(saved),
         _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_lstm_forward_noalloc(shape, x, wx, wh, b, h, stream=None):
+    """Inference forward on the library's own per-GPU scratch (no workspace,
+    nothing allocated); raises PyramidLSTMError (PLSTM_ESCRATCH) for shapes
+    whose workspace exceeds PLSTM_NOALLOC_SCRATCH_BYTES."""
+    _check("pyramid_lstm_forward_noalloc", load().pyramid_lstm_forward_noalloc(
+        ctypes.byref(shape), _ptr(x), _ptr(wx), _ptr(wh), _ptr(b), _ptr(h), _stream(stream)))
 
 
 def pyramid_lstm_backward(shape, x, wx, wh, b, saved, dh, dx, dwx, dwh, db, ws=None,

@@ -3,12 +3,37 @@
 // first HIP call; errors are status codes (no abort, no exception).
 #include <limits.h>
 
+#include <atomic>
+
 #include "common.h"
 #include "sweep.h"
 
 using namespace plstm;
 
 namespace {
+
+// Workspace of pyramid_lstm_forward_noalloc.  Every GPU the library runs on
+// holds its own copy until the process ends.  In host code `scratch` only
+// names the symbol: the device address of the current GPU's copy comes from
+// the runtime (scratch_ptr), and only that address reaches a kernel.
+static __device__ __align__(256) unsigned char scratch[PLSTM_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch_ptr[kMaxDevices];
+
+// The current device's copy of `scratch`, looked up on the first call made
+// with that device current; null on a HIP error.
+void *scratch_ptr()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+    return p;
+}
 
 bool aligned(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -95,6 +120,7 @@ const char *pyramid_lstm_status_string(int status)
     case PLSTM_EWORKSPACE: return "workspace too small";
     case PLSTM_EHIP: return "HIP runtime error";
     case PLSTM_ENOTCORESIDENT: return "persistent grid does not fit on the device";
+    case PLSTM_ESCRATCH: return "shape needs more than the no-allocation entry point's scratch";
     default: return "unknown status";
     }
 }
@@ -118,6 +144,20 @@ int pyramid_lstm_forward(const plstm_shape *s, const void *x, const void *wx, co
     const int rc = check_shape(s);
     if (rc != PLSTM_OK) return rc;
     return layer_forward(make_geom(*s), s->dtype, x, wx, wh, b, h, saved, ws, ws_bytes, stream);
+}
+
+int pyramid_lstm_forward_noalloc(const plstm_shape *s, const void *x, const void *wx,
+                                 const void *wh, const void *b, void *h, void *stream)
+{
+    const int rc = check_shape(s);
+    if (rc != PLSTM_OK) return rc;
+    if (!x || !wx || !wh || !b || !h) return PLSTM_EINVAL;
+    const Geom g = make_geom(*s);
+    if (layer_ws(g, s->dtype, 0) > (size_t)PLSTM_NOALLOC_SCRATCH_BYTES) return PLSTM_ESCRATCH;
+    void *ws = scratch_ptr();
+    if (!ws) return PLSTM_EHIP;
+    return layer_forward(g, s->dtype, x, wx, wh, b, h, nullptr, ws,
+                         (size_t)PLSTM_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int pyramid_lstm_backward(const plstm_shape *s, const void *x, const void *wx, const void *wh,

@@ -50,7 +50,7 @@ def shape(**kw):
 
 
 def test_status_strings(lib):
-    for code in (0, -1, -2, -3, -4, -5):
+    for code in (0, -1, -2, -3, -4, -5, -6):
         assert P.pyramid_lstm_status_string(code) not in ("", "unknown status")
     assert P.pyramid_lstm_status_string(-99) == "unknown status"
 
@@ -339,3 +339,16 @@ def test_draw_cubes_recipes():
     assert all(c.cos_t == 1.0 and c.sin_t == 0.0 and c.flips in (0, P.PLSTM_FLIP_X) for c in mr)
     assert all(c.y0 == 0 and c.x0 == 0 and 0 <= c.z0 <= 23 for c in mr)
     assert 0.4 < np.mean([c.flips != 0 for c in mr]) < 0.6
+
+
+def test_noalloc_validation_without_gpu(lib):
+    """The no-allocation forward rejects null pointers and shapes beyond its
+    scratch before any HIP call."""
+    big = shape(D=80, H=64, W=64, C=3, O=16)
+    assert P.pyramid_lstm_workspace_size(big, 0) > P.PLSTM_NOALLOC_SCRATCH_BYTES
+    f = lib.pyramid_lstm_forward_noalloc
+    assert f(ctypes.byref(big), FAKE, FAKE, FAKE, FAKE, FAKE, None) == P.PLSTM_ESCRATCH
+    small = shape(C=3, O=16)
+    assert f(ctypes.byref(small), None, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert f(ctypes.byref(small), FAKE, FAKE, FAKE, FAKE, None, None) == -1
+    assert f(None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1

@@ -479,13 +479,6 @@ def bench_mr_layer(args):
     O = wl.hidden[0]
     V = N * D * H * W
     torch.cuda.init()
-    if args.copy_calibration:
-        src = torch.zeros(1 << 28, dtype=torch.float32, device="cuda:0")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
     x = dev(inst.x)
     layers = [LayerW(dev(L.wx), dev(L.wh), dev(L.b)) for L in inst.layers]
     fcs = [(dev(w), dev(b)) for w, b in inst.fcs]
@@ -535,15 +528,16 @@ def main():
                              "train-2layer", "paper-net"],
                     help="all: config 5 as the headline with configs 2-4 beside it (default)")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="mr-layer: first copy 1 GiB device-to-device three times (a plain "
-                         "copy kernel of known size, to scale rocprofv3 FETCH_SIZE / "
-                         "WRITE_SIZE)")
+                    help="first copy 1 GiB device-to-device three times (a plain copy kernel "
+                         "of known size, to scale rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the six sweeps of a layer run concurrently "
               "on a single MI355X and this build has no multi-GPU path (--gpus 1).",
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
     if args.workload == "all":
         bench_all(args)
     elif args.workload == "mr-layer":
@@ -556,6 +550,19 @@ def main():
         bench_network(args, {"stacked-bf16": 4, "train-2layer": 5, "paper-net": None}[
             args.workload])
     release_device()
+
+
+def copy_calibration():
+    """Three device-to-device copies of 1 GiB: a plain copy kernel of known
+    size that scales rocprofv3's FETCH_SIZE / WRITE_SIZE to bytes."""
+    import torch
+    src = torch.zeros(1 << 28, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 def release_device():

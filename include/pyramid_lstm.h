@@ -392,14 +392,16 @@ int pyramid_lstm_set_forward_path(int path);
 int pyramid_lstm_set_backward_path(int path);
 
 /* Launch shape of the plane-step MFMA path, for testing and tuning
- * (process-wide): 0 = automatic (default): a step whose tiles would give
- * fewer than about two waves per SIMD splits each tile's K dimension over
- * the four waves of a workgroup, other steps give each wave its own tiles;
- * 1 = always split; 2 = never split; 3 = never split, and the forward's
- * operands read from L1 per filter tap instead of from 64-pixel blocks
- * staged in LDS (the default for fp32 steps that are not split).  Results
- * are identical up to summation order.  Returns PLSTM_EINVAL for other
- * values. */
+ * (process-wide): 0 = automatic (default): the reverse step (16 or 32 units)
+ * runs on 64-pixel blocks with dA_{t+1} staged in LDS, its K split over a
+ * workgroup's four waves; a forward step whose tiles would give fewer than
+ * about two waves per SIMD splits each tile's K dimension over the four
+ * waves of a workgroup, other steps give each wave its own tiles;
+ * 1 = always split (the reverse step's operands read from L1); 2 = never
+ * split; 3 = never split, and the forward's operands read from L1 per
+ * filter tap instead of from 64-pixel blocks staged in LDS (the default for
+ * fp32 steps that are not split).  Results are identical up to summation
+ * order.  Returns PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_step_split(int mode);
 
 /* Contraction type of bf16-storage layers with 32 or 64 hidden units, for

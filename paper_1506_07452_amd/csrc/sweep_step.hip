@@ -1120,6 +1120,15 @@ struct BwdStepArgs {
     float *gcf;               // [6][N][V][O]: dL/dc_t * f_t
     int npg[kDirs];
     int base[kDirs + 1];
+    // pixel blocks of the LDS-staged kernel (as in FwdStepArgs) and one
+    // wave's LDS region in 16-byte units (its staged block + filter halo, or
+    // its partial sums, whichever is larger)
+    int bp[kDirs], bq[kDirs], nbq[kDirs], nblk[kDirs];
+    int reg_f4;
+    // dL/dx inside the staged reverse step: W_x^T fragments
+    // [6][KK * 4U][CT][64][4] and each direction's share [6][N][V][C]
+    const float *fragx;
+    float *dxd;
 };
 
 // ---- line blocks of the 2D layer's reverse sweep (16 hidden units) ----------
@@ -1584,6 +1593,243 @@ k_step_bwd(BwdStepArgs a)
     }
 }
 
+// Reverse step on LDS-staged pixel blocks (U = 1 or 2 unit tiles), with
+// this direction's share of dL/dx for the plane before it in sweep order when
+// CT > 0.  A workgroup takes a BP x BQ block of 64 pixels of one plane (the
+// blocks of the staged forward).  The K dimension of the contraction is (tap,
+// gate-unit block of 16): wave w takes the blocks mb = w + 4 j (j < U) of
+// every tap.  It stages those channels of dA_{t+1} for the block and its
+// filter halo in its own LDS region (16-byte chunks XOR-swizzled by the
+// pixel), so every tap's B operand comes from LDS, and contracts them with
+//   W_h^T (U unit tiles):     gh_t[p]     = sum_taps W_h^T dA_{t+1}[p - tap]
+//   W_x^T (CT channel tiles): dx_{t+1}[p] = sum_taps W_x^T dA_{t+1}[p - tap]
+// for the block's four pixel tiles: the input x_{t+1} entered plane t + 1's
+// gates through the same taps (Eq. (7)-(9), (11)), so its gradient is the
+// same transposed convolution of the same staged dA_{t+1}.  The partial sums
+// of the three tiles a wave does not finish then go to its region; after a
+// barrier wave w adds tile w's four partials in wave order, runs the
+// gate-gradient epilogue and stores dx_{t+1}.  t = -1 gives dL/dx of plane 0
+// only.
+template <int U, int CT>
+__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(3)))
+k_step_bwd_blk(BwdStepArgs a)
+{
+    constexpr int O = 16 * U, G = 4 * O, MB = 4 * U;
+    constexpr int NCH = 4 * U;                       // staged 16-byte chunks per pixel
+    constexpr int SWM = NCH >= 8 ? 7 : 3;
+    static_assert(kNT == kSW, "wave w finishes tile w");
+    extern __shared__ f4 lds[];
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int blk = blockIdx.x;
+    if (blk >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, blk);
+    const DirGeom dg = a.g.dir[d];
+    int r = blk - a.base[d];
+    const int n = r / a.nblk[d];
+    r -= n * a.nblk[d];
+    const int BP = a.bp[d], BQ = a.bq[d];
+    const int bi = r / a.nbq[d], bj = r - bi * a.nbq[d];
+    const int p0 = bi * BP, q0 = bj * BQ;
+    const int t = a.t;
+    const bool do_h = t >= 0;                        // plane t exists (t = -1: dL/dx only)
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const bool has_next = t + 1 < dg.T;
+    const int noff = dg.sign * ss;    // voxel of plane t + 1 = voxel of plane t + noff
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1, KK = a.g.KP * KQ;
+    const int KG = KK * MB;
+    const int SW = BQ + 2 * radq, SH = BP + 2 * radp;
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    f4 *mine = lds + (long long)wave * a.reg_f4;
+
+    // ---- the epilogue's pixel (tile `wave`)
+    const int lbq = 31 - __builtin_clz(BQ);
+    const int ee = wave * 16 + col;
+    const int ey = ee >> lbq, ex = ee & (BQ - 1);
+    const bool elive = on_plane(p0 + ey, q0 + ex, P, Q);
+    const int pix = elive ? (p0 + ey) * sp + (q0 + ex) * sq : 0;
+    const int evox = s * ss + pix;
+    const long long vo = sbase + evox;
+    const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+
+    // ---- contraction over this wave's gate-unit blocks of dA_{t+1}
+    f4 acc[U][kNT], accx[CT > 0 ? CT : 1][kNT];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[u][nt] = zero;
+#pragma unroll
+    for (int c = 0; c < (CT > 0 ? CT : 1); ++c)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) accx[c][nt] = zero;
+    if (has_next) {
+        const auto rs_dA = slice_rsrc(a.dA + sbase * G, V * G);
+        const int nst = SH * SW * NCH;
+        for (int e = lane; e < nst; e += 64) {
+            const int spx = e / NCH, c = e - spx * NCH;
+            const int sy = spx / SW, sx = spx - sy * SW;
+            const int pp = p0 - radp + sy, qq = q0 - radq + sx;
+            const int mb = wave + kSW * (c >> 2);
+            const int v = (s + dg.sign) * ss + pp * sp + qq * sq;
+            mine[spx * NCH + (c ^ (spx & SWM))] =
+                bload4(rs_dA, sel_off(on_plane(pp, qq, P, Q),
+                                      (unsigned)(v * G + mb * 16 + 4 * (c & 3)) * 4u));
+        }
+    }
+    __syncthreads();
+    if (has_next) {
+        int spix[kNT];
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) {
+            const int e = nt * 16 + col;
+            spix[nt] = ((e >> lbq) + radp) * SW + (e & (BQ - 1)) + radq;
+        }
+        const float *fr = a.frag + (long long)d * U * KG * 256 + lane * 4;
+        const float *frx = a.fragx + (long long)d * KG * CT * 256 + lane * 4;
+        // K-steps in (tap, j) order; A fragments one K-group ahead
+        auto afrag = [&](int tap, int j, f4 *o, f4 *ox) {
+            const int kg = tap * MB + wave + kSW * j;
+#pragma unroll
+            for (int u = 0; u < U; ++u) o[u] = *(const f4 *)(fr + ((long long)u * KG + kg) * 256);
+#pragma unroll
+            for (int c = 0; c < CT; ++c) ox[c] = *(const f4 *)(frx + ((long long)kg * CT + c) * 256);
+        };
+        f4 acur[U], anxt[U], axc[CT > 0 ? CT : 1], axn[CT > 0 ? CT : 1];
+        afrag(0, 0, acur, axc);
+        const int nk = KK * U;
+        for (int k = 0; k < nk; ++k) {
+            const int tap = k / U, j = k - tap * U;
+            if (k + 1 < nk) afrag((k + 1) / U, (k + 1) - ((k + 1) / U) * U, anxt, axn);
+            const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
+            // the pixels that received this pixel's h (and x) through tap (ka, kb)
+            const int doff = -ka * SW - kb;
+            const int chunk = j * 4 + q4;
+            f4 bv[kNT];
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) {
+                const int spx = spix[nt] + doff;
+                bv[nt] = mine[spx * NCH + (chunk ^ (spx & SWM))];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int nt = 0; nt < kNT; ++nt)
+                        acc[u][nt] = mfma(acur[u][i], bv[nt][i], acc[u][nt]);
+#pragma unroll
+                for (int c = 0; c < CT; ++c)
+#pragma unroll
+                    for (int nt = 0; nt < kNT; ++nt)
+                        accx[c][nt] = mfma(axc[c][i], bv[nt][i], accx[c][nt]);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) acur[u] = anxt[u];
+#pragma unroll
+            for (int c = 0; c < CT; ++c) axc[c] = axn[c];
+        }
+    }
+    // partial sums of the tiles other waves finish, into this wave's own
+    // region (only this wave read it): slot nt - (nt > wave) of each M-tile
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        if (nt == wave) continue;
+        const int sl = nt - (nt > wave ? 1 : 0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) mine[(u * (kNT - 1) + sl) * 64 + lane] = acc[u][nt];
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+            mine[((U + c) * (kNT - 1) + sl) * 64 + lane] = accx[c][nt];
+    }
+    __syncthreads();
+    if (!elive) return;
+    // tile `wave` of M-tile m: the four waves' partials in wave order
+    auto partial = [&](int m, f4 own) {
+        f4 v = zero;
+#pragma unroll
+        for (int w = 0; w < kSW; ++w) {
+            if (w == wave) {
+                v += own;
+            } else {
+                const int sl = wave - (wave > w ? 1 : 0);
+                v += lds[(long long)w * a.reg_f4 + (m * (kNT - 1) + sl) * 64 + lane];
+            }
+        }
+        return v;
+    };
+    f4 own_h[U], own_x[CT > 0 ? CT : 1];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt)
+        if (nt == wave) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) own_h[u] = acc[u][nt];
+#pragma unroll
+            for (int c = 0; c < CT; ++c) own_x[c] = accx[c][nt];
+        }
+
+    if (CT > 0 && has_next) {
+        const int C = a.g.C;
+        float *out = a.dxd + (sbase + evox + noff) * C;
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            const f4 v = partial(U + c, own_x[c]);
+            const int c0 = c * 16 + 4 * q4;
+            if ((C & 3) == 0 && c0 + 3 < C) {
+                *(f4 *)(out + c0) = v;
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (c0 + i < C) out[c0 + i] = v[i];
+            }
+        }
+    }
+    if (!do_h) return;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int uo = u * 16 + 4 * q4;
+        const float *gp = a.gates + vo * G + uo;
+        const f4 gi = *(const f4 *)gp, gf = *(const f4 *)(gp + O);
+        const f4 gg = *(const f4 *)(gp + 2 * O), go = *(const f4 *)(gp + 3 * O);
+        const f4 c = *(const f4 *)(a.cell + vo * O + uo);
+        f4 cp = zero, gn = zero;
+        if (t > 0) cp = *(const f4 *)(a.cell + (vo - noff) * O + uo);
+        if (has_next) gn = *(const f4 *)(a.gcf + (vo + noff) * O + uo);
+        f4 ghv = partial(u, own_h[u]) + *(const f4 *)(a.dh + ((long long)n * V + evox) * O + uo);
+        f4 di, df, dgv, dov, gco;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float gh = ghv[i];
+            const float tc = ftanh(c[i]);
+            const float gcv = gh * go[i] * (1.0f - tc * tc) + gn[i];
+            di[i] = gcv * gg[i] * gi[i] * (1.0f - gi[i]);
+            df[i] = gcv * cp[i] * gf[i] * (1.0f - gf[i]);
+            dgv[i] = gcv * gi[i] * (1.0f - gg[i] * gg[i]);
+            dov[i] = gh * tc * go[i] * (1.0f - go[i]);
+            gco[i] = gcv * gf[i];
+        }
+        float *dp = a.dA + vo * G + uo;
+        *(f4 *)dp = di;
+        *(f4 *)(dp + O) = df;
+        *(f4 *)(dp + 2 * O) = dgv;
+        *(f4 *)(dp + 3 * O) = dov;
+        *(f4 *)(a.gcf + vo * O + uo) = gco;
+    }
+}
+
+// dx = sum of the nd directions' shares in direction order.
+__global__ void __launch_bounds__(256)
+k_sum_dxn(long long n, int nd, const float *__restrict__ dxd, float *__restrict__ dx)
+{
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    float v = dxd[i];
+    for (int d = 1; d < nd; ++d) v += dxd[d * n + i];
+    dx[i] = v;
+}
+
 // ---- parameter gradients ----------------------------------------------------
 // dW[d][m][k] = sum over the voxels of direction d of dA[v][m] col[v][k],
 // col = [im2col(h_{t-1}) (KK O) | im2col(x_t) (KK C')]; K of the MFMA runs over
@@ -1592,19 +1838,20 @@ k_step_bwd(BwdStepArgs a)
 // visited as units of 16 pixels of a row (lane group q takes pixels
 // 4q .. 4q+3, one per k-step), walking each column group down the rows so
 // that the rows read for one unit are re-read from cache by the next ones.
-// The partial sums of the chunks are added in order.  db = sum_v dA[v] is a
-// separate column sum of dA.
+// The partial sums of the chunks are added in order.  db = sum_v dA[v] is the
+// product with a column of ones appended to the x part.
 constexpr int kWgN = 4;          // most N-tiles a wave holds
 constexpr int kWgMaxChunks = 512;
 
-// N-tiles per block: each part (KK U tiles of h; ceil(KK C / 16) tiles of x,
-// whose columns are the (tap, channel) pairs packed densely) is cut into the
-// fewest blocks of at most kWgN tiles, as even as possible.
+// N-tiles per block: each part (KK U tiles of h; ceil((KK C + 1) / 16) tiles
+// of x, whose columns are the (tap, channel) pairs packed densely and then a
+// column of ones, which gives db) is cut into the fewest blocks of at most
+// kWgN tiles, as even as possible.
 struct WgBlocks {
     int nh, nx;       // blocks of each part
     int th, tx;       // tiles per block of each part (the last block may have fewer)
 };
-__host__ __device__ inline int wg_xtiles(int KK, int C) { return (KK * C + 15) / 16; }
+__host__ __device__ inline int wg_xtiles(int KK, int C) { return (KK * C + 16) / 16; }
 __host__ __device__ inline WgBlocks wg_blocks(int U, int XT, int KK)
 {
     WgBlocks w;
@@ -1626,8 +1873,9 @@ struct WgStepArgs {
     float *partial;           // [6][kch][4O][16 NTt]
 };
 
-// The wave's share: NTL tiles (compile time) of which `ntl` are real.
-template <int U, int NTL>
+// The wave's share: NTL tiles (compile time) of which `ntl` are real; ONES:
+// the block holds the column of ones.
+template <int U, int NTL, bool ONES>
 __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, bool is_h, int t0,
                                int ntl, int first_nt)
 {
@@ -1645,13 +1893,18 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
     // per tile and lane: tap offset in the slice, tap row and column (packed)
     // and channel (-1: a column past the part).  An h tile is one tap and 16
     // channels (uniform tap); an x tile is 16 (tap, channel) pairs, column
-    // kk = 16 tt + col being tap kk / C, channel kk % C.
+    // kk = 16 tt + col being tap kk / C, channel kk % C; column KK C is the
+    // column of ones (db): its lanes load nothing (an out-of-range offset) and
+    // their operand becomes 1 where the products use it, so the loads stay
+    // unconditional and nothing waits for them early.
     int dtap[NTL], chn[NTL];
     unsigned tapok[NTL];
+    bool ones[NTL];
 #pragma unroll
     for (int j = 0; j < NTL; ++j) {
         const int tt = t0 + j;
         const int kk = tt * 16 + col;
+        ones[j] = ONES && !is_h && j < ntl && kk == KK * C;
         const bool real = j < ntl && (is_h || kk < KK * C);
         const int tap = !real ? radp * KQ + radq : (is_h ? tt / U : kk / C);
         const int ka = tap / KQ, kb = tap % KQ;
@@ -1737,7 +1990,7 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
             for (int m = 0; m < 4; ++m)
 #pragma unroll
                 for (int j = 0; j < NTL; ++j)
-                    acc[m][j] = mfma(o.a[ks][m], o.b[ks][j], acc[m][j]);
+                    acc[m][j] = mfma(o.a[ks][m], ONES && ones[j] ? 1.0f : o.b[ks][j], acc[m][j]);
     };
     // two operand sets in ping-pong: each is reloaded only after its
     // products, so no loaded register is copied (a copy would wait for the
@@ -1795,82 +2048,42 @@ k_wgrad_step(WgStepArgs a)
     const int tend = is_h ? KK * U : XT;
     const int ntl = t0 + tb < tend ? tb : tend - t0;
     const int first_nt = (is_h ? 0 : KK * U) + t0;
-    if constexpr (kWgN <= 4) {
-        // as many products per unit as the block has tiles
+    // the x block holding the column of ones (tile KK C / 16 of the x part)
+    const int ones_tile = KK * a.g.C / 16;
+    const bool ones = !is_h && t0 <= ones_tile && ones_tile < t0 + ntl;
+    static_assert(kWgN <= 4, "at most four N-tiles per wave");
+    // as many products per unit as the block has tiles
+    if (ones) {
         if (ntl <= 1)
-            wg_wave<U, 1>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+            wg_wave<U, 1, true>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
         else if (ntl <= 2)
-            wg_wave<U, 2>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+            wg_wave<U, 2, true>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
         else if (ntl <= 3)
-            wg_wave<U, 3>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+            wg_wave<U, 3, true>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
         else
-            wg_wave<U, 4>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+            wg_wave<U, 4, true>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
     } else {
-        if (ntl <= 4)
-            wg_wave<U, 4>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
-        else if (ntl <= 6)
-            wg_wave<U, 6>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        if (ntl <= 1)
+            wg_wave<U, 1, false>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        else if (ntl <= 2)
+            wg_wave<U, 2, false>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+        else if (ntl <= 3)
+            wg_wave<U, 3, false>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
         else
-            wg_wave<U, 8>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
+            wg_wave<U, 4, false>(a, d, kc, mblk, is_h, t0, ntl, first_nt);
     }
 }
 
-// db: column sums of dA over the voxels of each direction, in fixed chunks
-// (partials[d][chunk][4O]), then the chunks in order.  A workgroup streams
-// its chunk with 16-byte loads: G / 4 lanes cover a row, 1024 / G rows at a
-// time, four rows in flight per lane; the row partials are summed in LDS in a
-// fixed order.
-constexpr int kDbChunks = 512;
-
-__global__ void __launch_bounds__(256)
-k_db_partial(int G, long long nvox, const float *__restrict__ dA, float *__restrict__ part)
-{
-    __shared__ f4 red[256];
-    const int d = blockIdx.y, ch = blockIdx.x;
-    const int cols = G >> 2, R = 256 / cols;
-    const int cg = threadIdx.x % cols, r = threadIdx.x / cols;
-    const long long v0 = nvox * ch / kDbChunks, v1 = nvox * (ch + 1) / kDbChunks;
-    const f4 *src = (const f4 *)(dA + (long long)d * nvox * G) + cg;
-    const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-    f4 a0 = zero, a1 = zero, a2 = zero, a3 = zero;
-    if (r < R) {
-        long long v = v0 + r;
-        for (; v + 3 * R < v1; v += 4 * R) {
-            a0 += src[v * cols];
-            a1 += src[(v + R) * cols];
-            a2 += src[(v + 2 * R) * cols];
-            a3 += src[(v + 3 * R) * cols];
-        }
-        for (; v < v1; v += R) a0 += src[v * cols];
-    }
-    red[threadIdx.x] = (a0 + a1) + (a2 + a3);
-    __syncthreads();
-    if (threadIdx.x < cols) {
-        f4 sum = red[threadIdx.x];
-        for (int k = 1; k < R; ++k) sum += red[k * cols + threadIdx.x];
-        *(f4 *)(part + ((long long)d * kDbChunks + ch) * G + 4 * threadIdx.x) = sum;
-    }
-}
-
-__global__ void __launch_bounds__(256)
-k_db_reduce(int nd, int G, const float *__restrict__ part, float *__restrict__ db)
-{
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= nd * G) return;
-    const int d = i / G, m = i % G;
-    float acc = 0.0f;
-    for (int ch = 0; ch < kDbChunks; ++ch) acc += part[((long long)d * kDbChunks + ch) * G + m];
-    db[i] = acc;
-}
-
-// dW = sum of the chunk partials in chunk order, scattered to the ABI layouts.
+// dW = sum of the chunk partials in chunk order, scattered to the ABI layouts;
+// the column of ones gives db (skipped when db is null).
 __global__ void __launch_bounds__(256)
 k_wgrad_step_reduce(int nd, int O, int C, int Cp, int KK, int NTt, int kch,
                     const float *__restrict__ partial, float *__restrict__ dwx,
-                    float *__restrict__ dwh)
+                    float *__restrict__ dwh, float *__restrict__ db)
 {
-    // columns: KK O of h (tap-major), then KK C of x ((tap, channel) dense)
-    const int G = 4 * O, KC = KK * (O + C), KCp = NTt * 16;
+    // columns: KK O of h (tap-major), then KK C of x ((tap, channel) dense),
+    // then the column of ones
+    const int G = 4 * O, KC = KK * (O + C) + 1, KCp = NTt * 16;
     const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
     if (i >= (long long)nd * G * KC) return;
     const int k = (int)(i % KC);
@@ -1880,9 +2093,11 @@ k_wgrad_step_reduce(int nd, int O, int C, int Cp, int KK, int NTt, int kch,
     for (int c = 0; c < kch; ++c) acc += partial[(((long long)d * kch + c) * G + gu) * KCp + k];
     if (k < KK * O) {
         dwh[(((long long)d * G + gu) * O + k % O) * KK + k / O] = acc;
-    } else {
+    } else if (k < KC - 1) {
         const int kx = k - KK * O;
         dwx[(((long long)d * G + gu) * C + kx % C) * KK + kx / C] = acc;
+    } else if (db) {
+        db[(long long)d * G + gu] = acc;
     }
 }
 
@@ -2108,9 +2323,60 @@ int launch_fwd_steps(const Geom &g, FwdStepArgs &a, hipStream_t st)
     return PLSTM_OK;
 }
 
+// One wave's LDS region of the staged reverse step, in 16-byte units: its
+// staged block (reg_px pixels of 4U chunks) or its partial sums (three
+// tiles of U + CT M-tiles, 64 lanes), whichever is larger.
+inline int bwd_blk_reg_f4(int U, int CT, int reg_px)
+{
+    const int st = reg_px * 4 * U, part = (U + CT) * (kNT - 1) * 64;
+    return st > part ? st : part;
+}
+
+// The staged reverse step for this shape: U <= 2 unit tiles and, with dL/dx
+// inside it, at most two channel tiles; `reg_px` the largest staged block.
+inline bool bwd_blk_ok(const Geom &g, bool with_dx, int reg_px)
+{
+    const int U = g.O / 16, CT = with_dx ? pad16(g.C) / 16 : 0;
+    if (g_step_split != 0 || U > 2 || CT > 2) return false;
+    return (size_t)kSW * bwd_blk_reg_f4(U, CT, reg_px) * 16 <= (size_t)device_info().max_lds;
+}
+
+template <int U, int CT>
+int launch_bwd_blk(const Geom &g, BwdStepArgs &a, hipStream_t st)
+{
+    const size_t lds = (size_t)kSW * a.reg_f4 * 16;
+    if (hipFuncSetAttribute((const void *)k_step_bwd_blk<U, CT>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return PLSTM_EHIP;
+    // with dL/dx, a last launch (t = -1) gives plane 0's share
+    for (int t = max_T(g) - 1; t >= (CT > 0 ? -1 : 0); --t) {
+        a.t = t;
+        int nb = 0;
+        for (int d = 0; d < kDirs; ++d) {
+            a.base[d] = nb;
+            if (t < g.dir[d].T && g.dir[d].T > 0) nb += g.N * a.nblk[d];
+        }
+        a.base[kDirs] = nb;
+        k_step_bwd_blk<U, CT><<<nb, 64 * kSW, lds, st>>>(a);
+        PLSTM_LAUNCH_CHECK();
+    }
+    return PLSTM_OK;
+}
+
 template <int U>
 int launch_bwd_steps(const Geom &g, BwdStepArgs &a, hipStream_t st)
 {
+    if constexpr (U <= 2) {
+        if (a.reg_f4 > 0) {
+            const int CT = a.dxd ? pad16(g.C) / 16 : 0;
+            switch (CT) {
+            case 0: return launch_bwd_blk<U, 0>(g, a, st);
+            case 1: return launch_bwd_blk<U, 1>(g, a, st);
+            case 2: return launch_bwd_blk<U, 2>(g, a, st);
+            default: return PLSTM_EUNSUPPORTED;
+            }
+        }
+    }
     // an item of the reverse step holds every unit group: split up to four
     // waves per SIMD
     const int few = g_step_split == 0 ? 2 * split_threshold() : split_threshold();
@@ -2370,8 +2636,12 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
         timing_end((x_direct ? 1 : 2) + launches, st);
         return PLSTM_OK;
     }
-    pad_x();
-    PLSTM_LAUNCH_CHECK();
+    // fp32 x whose channel count is already a multiple of 16 is read in place
+    const bool x_in_place = dtype == PLSTM_F32 && Cp == g.C;
+    if (!x_in_place) {
+        pad_x();
+        PLSTM_LAUNCH_CHECK();
+    }
 
     if (dtype == PLSTM_BF16)
         k_pack_fwd<uint16_t><<<blocks_for(nfrag, 256), 256, 0, st>>>(
@@ -2387,7 +2657,7 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     a.Cp = Cp; a.KX = KX; a.KG = KG;
     a.cx_mul = (65536 + Cp / 16 - 1) / (Cp / 16);
     a.k_mul = k_mul_of(g);
-    a.xp = xp; a.frag = frag; a.bias = bias;
+    a.xp = x_in_place ? (const float *)x : xp; a.frag = frag; a.bias = bias;
     a.hd = hd; a.cell = cell; a.gates = gates;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
     set_blocks(g, a.bp, a.bq, a.nbq, a.nblk);
@@ -2398,7 +2668,7 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     default: rc = launch_fwd_steps<4>(g, a, st); break;
     }
     if (rc != PLSTM_OK) return rc;
-    timing_end(2 + max_T(g), st);
+    timing_end((x_in_place ? 1 : 2) + max_T(g), st);
     return PLSTM_OK;
 }
 
@@ -2417,6 +2687,9 @@ inline int line_nsegmax(const Geom &g)
     return m;
 }
 inline bool line_bwd_geom(const Geom &g) { return g.nd == 4 && g.KP == 1 && g.O == 16; }
+// Shapes whose reverse sweep may give dL/dx per direction (the 2D line blocks,
+// or the staged reverse step with at most 32 units and 32 input channels).
+inline bool bwd_dxd(const Geom &g) { return line_bwd_dx(g) || (g.O <= 32 && pad16(g.C) <= 32); }
 
 size_t step_bwd_ws(const Geom &g)
 {
@@ -2428,8 +2701,7 @@ size_t step_bwd_ws(const Geom &g)
     cv.take<float>((size_t)g.nd * U * KK * 4 * U * 256);           // W_h^T fragments
     cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);         // weight-gradient partials
     cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);   // W_x^T fragments
-    cv.take<float>((size_t)g.nd * kDbChunks * G);                  // db partials
-    if (line_bwd_dx(g)) cv.take<float>((size_t)g.nd * g.N * g.V * g.C);  // dL/dx per direction
+    if (bwd_dxd(g)) cv.take<float>((size_t)g.nd * g.N * g.V * g.C);   // dL/dx per direction
     if (line_bwd_geom(g)) cv.take<float>((size_t)g.nd * g.N * line_nsegmax(g) * 64);  // db partials
     return cv.off;
 }
@@ -2484,8 +2756,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     float *frag = cv.take<float>((size_t)g.nd * U * KK * 4 * U * 256);
     float *partial = cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);
     float *fragx = cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);
-    float *dbpart = cv.take<float>((size_t)g.nd * kDbChunks * G);
-    float *dxd = line_bwd_dx(g) ? cv.take<float>((size_t)g.nd * g.N * g.V * g.C) : nullptr;
+    float *dxd = bwd_dxd(g) ? cv.take<float>((size_t)g.nd * g.N * g.V * g.C) : nullptr;
     float *dbl = line_bwd_geom(g) ? cv.take<float>((size_t)g.nd * g.N * line_nsegmax(g) * 64)
                                   : nullptr;
     bool db_done = false;
@@ -2496,7 +2767,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     k_pack_bwd<<<blocks_for((long long)g.nd * U * KK * 4 * U * 256, 256), 256, 0, st>>>(
         g.nd, g.O, KK, wh, frag);
     PLSTM_LAUNCH_CHECK();
-    const bool fuse_dx = dx && dxd;
+    const bool fuse_dx = dx && dxd && line_bwd_dx(g);
     const size_t line_dyn = line_bwd_dyn_lds(g.KQ * 4, fuse_dx ? g.KQ * G * g.C : 0);
     if (g.nd == 4 && g.KP == 1 && g.O == 16 && (g_step_split == 0 || g_step_split == 2) &&
         line_dyn + 2 * kLineSlots * 64 + 4 * 64 * 16 + 4 * 4 * 4 * 16 <= (size_t)device_info().max_lds) {
@@ -2559,6 +2830,24 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
         a.gates = sv.gates; a.cell = sv.cell; a.dh = dh;
         a.dA = dA; a.gcf = gcf;
         for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
+        set_blocks(g, a.bp, a.bq, a.nbq, a.nblk);
+        int reg_px = 64;
+        for (int d = 0; d < g.nd; ++d) {
+            const int px = (a.bp[d] + 2 * (g.KP / 2)) * (a.bq[d] + 2 * (g.KQ / 2));
+            if (px > reg_px) reg_px = px;
+        }
+        // the staged reverse step, with dL/dx inside it where it takes it
+        const bool with_dx = dx && dxd && bwd_blk_ok(g, true, reg_px);
+        a.reg_f4 = bwd_blk_ok(g, with_dx, reg_px)
+                       ? bwd_blk_reg_f4(U, with_dx ? Cp / 16 : 0, reg_px) : 0;
+        a.fragx = fragx;
+        a.dxd = with_dx ? dxd : nullptr;
+        if (with_dx) {
+            const long long nf = (long long)g.nd * KK * 4 * U * (Cp / 16) * 256;
+            k_pack_dx<<<blocks_for(nf, 256), 256, 0, st>>>(g.nd, g.O, g.C, Cp / 16, KK, wx,
+                                                            fragx);
+            PLSTM_LAUNCH_CHECK();
+        }
         int rc;
         switch (U) {
         case 1: rc = launch_bwd_steps<1>(g, a, st); break;
@@ -2566,7 +2855,15 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
         default: rc = launch_bwd_steps<4>(g, a, st); break;
         }
         if (rc != PLSTM_OK) return rc;
-        timing_end(1 + max_T(g), st);
+        timing_end((with_dx ? 3 : 1) + max_T(g), st);
+        if (with_dx) {
+            timing_begin("dx_step", st);
+            const long long ndx = nvox * g.C;
+            k_sum_dxn<<<blocks_for(ndx, 256), 256, 0, st>>>(ndx, g.nd, dxd, dx);
+            PLSTM_LAUNCH_CHECK();
+            timing_end(1, st);
+            dx_done = true;
+        }
     }
 
     timing_begin("wgrad_step", st);
@@ -2585,17 +2882,12 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     default: k_wgrad_step<4><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
     }
     PLSTM_LAUNCH_CHECK();
-    const long long nout = (long long)g.nd * G * KK * (g.O + g.C);
-    k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(g.nd, g.O, g.C, Cp, KK, w.NTt,
-                                                               w.kch, partial, dwx, dwh);
+    // db: the column of ones, unless the line blocks summed it already
+    const long long nout = (long long)g.nd * G * (KK * (g.O + g.C) + 1);
+    k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(
+        g.nd, g.O, g.C, Cp, KK, w.NTt, w.kch, partial, dwx, dwh, db_done ? nullptr : db);
     PLSTM_LAUNCH_CHECK();
-    if (!db_done) {
-        k_db_partial<<<dim3(kDbChunks, g.nd), 256, 0, st>>>(G, nvox, dA, dbpart);
-        PLSTM_LAUNCH_CHECK();
-        k_db_reduce<<<blocks_for(g.nd * G, 256), 256, 0, st>>>(g.nd, G, dbpart, db);
-        PLSTM_LAUNCH_CHECK();
-    }
-    timing_end(db_done ? 2 : 4, st);
+    timing_end(2, st);
     if (dx && !dx_done) return step_dx(g, wx, dA, fragx, dx, st);
     return PLSTM_OK;
 }

@@ -166,10 +166,11 @@ STEP_SHAPES = [(1, 5, 37, 29, 3, 16), (2, 4, 9, 7, 1, 16), (1, 6, 5, 4, 20, 16),
                (1, 2, 19, 3, 64, 64)]
 
 
-@pytest.fixture(params=[1, 2, 3], ids=["split", "nosplit", "nosplit_l1"])
+@pytest.fixture(params=[0, 1, 2, 3], ids=["auto", "split", "nosplit", "nosplit_l1"])
 def step_split(request):
-    """Both launch shapes of the plane-step kernels (K split over a
-    workgroup's waves, or one tile group per wave)."""
+    """Every launch shape of the plane-step kernels: the default (staged pixel
+    blocks; the reverse step's K split over a workgroup's waves by gate-unit
+    block), K split over a workgroup's waves, or one tile group per wave."""
     P.pyramid_lstm_set_step_split(request.param)
     yield request.param
     P.pyramid_lstm_set_step_split(0)

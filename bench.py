@@ -134,17 +134,29 @@ def layer_path(C, O, dtype, K=3):
     return "step_bf16" if dtype == "bf16" and O in (32, 64) else "step"
 
 
+def dx_in_reverse(li, C, O, path):
+    """Whether the library's staged reverse step computes dL/dx of this layer
+    (layers after the first on the fp32 plane-step path with at most 32 units
+    and 32 input channels, padded to 16); dx_step then only adds the
+    directions."""
+    return li > 0 and path == "step" and O <= 32 and (C + 15) // 16 * 16 <= 32
+
+
 def network_roofline(phases, passes, V, shapes, dtype, K=3):
     """Roofline of the slowest phase of a multi-layer pass: its algorithmic
-    work summed over the layers that ran it."""
+    work summed over the layers that ran it (the reverse step's includes
+    dL/dx where it computes it)."""
     cand = {k: v for k, v in phases.items() if phase_work(k, 1, 1, 16)[0] == "mfma"}
     name = max(cand, key=lambda k: cand[k][0])
     ms, launches = phases[name]
     flops = 0
     for li, (C, O) in enumerate(shapes):
         path = layer_path(C, O, dtype, K)
-        if name.endswith("_" + path) or (name.startswith("dx") and li > 0):
+        fused = dx_in_reverse(li, C, O, path)
+        if name.endswith("_" + path) or (name.startswith("dx") and li > 0 and not fused):
             flops += phase_work(name, V, C, O, K)[1]
+        if name == "sweep_bwd_step" and fused:
+            flops += phase_work("dx", V, C, O, K)[1]
     achieved = flops * passes / (ms / 1e3) / 1e12
     peak = PEAK_BF16_TFLOPS if name.endswith("_bf16") else PEAK_FP32_TFLOPS
     return {"kernel": name, "bound": "mfma", "achieved": round(achieved, 3),

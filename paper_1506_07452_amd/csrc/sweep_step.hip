@@ -540,6 +540,207 @@ k_step_fwd_blk(FwdStepArgs a)
     }
 }
 
+// Forward step on LDS-staged pixel blocks with K split over the waves (U =
+// 1, 2 or 4 unit groups).  A workgroup takes a BP x BQ block of 64 pixels of
+// one plane; x_t and h_{t-1} of the block and its filter halo are staged in
+// LDS once ([x | h] per pixel in 16-byte chunks of 4 channels, XOR-swizzled
+// by the pixel), so every tap's B operand comes from LDS.  Wave w owns unit
+// group w % U and K-part w / U of the KP = 4 / U parts (K-groups kp,
+// kp + KP, ...; input and recurrent K-groups as in k_step_fwd) for all four
+// pixel tiles.  It then leaves the partial sums of the tiles it does not
+// finish in LDS and finishes tiles kp, kp + KP, ... itself: the KP partials
+// added in K-part order, the bias, the gates and the cell update.  Four
+// waves per block whatever U is, for steps with few blocks.
+template <int U>
+__global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(3)))
+k_step_fwd_bls(FwdStepArgs a)
+{
+    constexpr int O = 16 * U, G = 4 * O;
+    constexpr int KP = kSW / U;                  // K-parts
+    constexpr int NF = kNT / KP;                 // tiles a wave finishes
+    constexpr int NU = kNT - NF;                 // tiles it leaves to others
+    static_assert(kSW % U == 0 && kNT % KP == 0, "waves cover unit groups x K-parts");
+    extern __shared__ f4 stf[];
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int ug = wave % U, kp = wave / U;
+    const int blk = blockIdx.x;
+    if (blk >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, blk);
+    const DirGeom dg = a.g.dir[d];
+    int r = blk - a.base[d];
+    const int n = r / a.nblk[d];
+    r -= n * a.nblk[d];
+    const int BP = a.bp[d], BQ = a.bq[d];
+    const int bi = r / a.nbq[d], bj = r - bi * a.nbq[d];
+    const int p0 = bi * BP, q0 = bj * BQ;
+    const int t = a.t;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const int Cp = a.Cp, CX = Cp >> 4, KX = a.KX;
+    const int hoff = -dg.sign * ss;   // voxel of plane t - 1 = voxel of plane t + hoff
+    const int uo = ug * 16 + 4 * q4;
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
+    const int SW = BQ + 2 * radq, SH = BP + 2 * radp;
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    const auto rs_x = slice_rsrc(a.xp + (long long)n * V * Cp, V * Cp);
+    const auto rs_h = slice_rsrc(a.hd + sbase * O, V * O);
+    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+    const int nxc = CX * 4, nch = nxc + U * 4;   // staged chunks per pixel: x, then h
+    const int swm = (nch & 7) == 0 ? 7 : 3;
+    const int lbq = 31 - __builtin_clz(BQ);
+
+    // the tiles this wave finishes and their c_{t-1}, in flight meanwhile
+    int evox[NF];
+    bool elive[NF];
+    f4 cprev[NF];
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+        const int e = (kp + KP * j) * 16 + col;
+        const int ey = e >> lbq, ex = e & (BQ - 1);
+        elive[j] = on_plane(p0 + ey, q0 + ex, P, Q);
+        evox[j] = s * ss + (elive[j] ? (p0 + ey) * sp + (q0 + ex) * sq : 0);
+        cprev[j] = bload4(rs_c, sel_off(t > 0 && elive[j],
+                                        (unsigned)((evox[j] + hoff) * O + uo) * 4u));
+    }
+
+    // stage x_t and h_{t-1} of the block and its halo (zero off the plane,
+    // and h at t = 0)
+    {
+        const int nst_x = SH * SW * nxc;
+        for (int e = threadIdx.x; e < nst_x; e += 64 * kSW) {
+            const int spx = e / nxc, c = e - spx * nxc;
+            const int sy = spx / SW, sx = spx - sy * SW;
+            const int pp = p0 - radp + sy, qq = q0 - radq + sx;
+            const int v = s * ss + pp * sp + qq * sq;
+            stf[spx * nch + (c ^ (spx & swm))] =
+                bload4(rs_x, sel_off(on_plane(pp, qq, P, Q), (unsigned)(v * Cp + 4 * c) * 4u));
+        }
+        const int nhc = U * 4, nst_h = SH * SW * nhc;
+        for (int e = threadIdx.x; e < nst_h; e += 64 * kSW) {
+            const int spx = e / nhc, c = e - spx * nhc;
+            const int sy = spx / SW, sx = spx - sy * SW;
+            const int pp = p0 - radp + sy, qq = q0 - radq + sx;
+            const int v = s * ss + pp * sp + qq * sq + hoff;
+            stf[spx * nch + ((nxc + c) ^ (spx & swm))] =
+                bload4(rs_h, sel_off(t > 0 && on_plane(pp, qq, P, Q), (unsigned)(v * O + 4 * c) * 4u));
+        }
+    }
+    __syncthreads();
+
+    int spix[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const int e = nt * 16 + col;
+        spix[nt] = ((e >> lbq) + radp) * SW + (e & (BQ - 1)) + radq;
+    }
+    f4 acc[4][kNT];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[g][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    const float *fr = a.frag + (long long)(d * U + ug) * a.KG * 1024 + lane * 4;
+    const int KGe = t > 0 ? a.KG : KX;
+    f4 acur[4], anxt[4];
+    if (kp < KGe) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acur[g] = *(const f4 *)(fr + kp * 1024 + g * 256);
+    }
+    for (int kg = kp; kg < KGe; kg += KP) {
+        if (kg + KP < KGe) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) anxt[g] = *(const f4 *)(fr + (kg + KP) * 1024 + g * 256);
+        }
+        const bool is_x = kg < KX;
+        const int kk = is_x ? kg : kg - KX;
+        const int tap = is_x ? (kk * a.cx_mul) >> 16 : kk / U;
+        const int cb = kk - tap * (is_x ? CX : U);
+        const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
+        const int doff = ka * SW + kb;
+        const int chunk = (is_x ? 0 : nxc) + cb * 4 + q4;
+        f4 bv[kNT];
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) {
+            const int spx = spix[nt] + doff;
+            bv[nt] = stf[spx * nch + (chunk ^ (spx & swm))];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int nt = 0; nt < kNT; ++nt)
+                    acc[g][nt] = mfma(acur[g][i], bv[nt][i], acc[g][nt]);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acur[g] = anxt[g];
+    }
+
+    // slot of tile nt among the tiles K-part k leaves to others
+    auto slot = [](int nt, int k) {
+        int sl = 0;
+#pragma unroll
+        for (int m = 0; m < kNT; ++m) sl += (m < nt && m % KP != k) ? 1 : 0;
+        return sl;
+    };
+    if constexpr (KP > 1) {
+        __syncthreads();                 // every wave is done with the staged block
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) {
+            if (nt % KP == kp) continue;
+            const int sl = slot(nt, kp);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) stf[((wave * 4 + g) * NU + sl) * 64 + lane] = acc[g][nt];
+        }
+        __syncthreads();
+    }
+
+    // Eq. (7)-(12) for the tiles this wave finishes: the K-parts' partials in
+    // order, the bias, gates, cell and hidden state of units uo .. uo+3
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+        if (!elive[j]) continue;
+        const int nt = kp + KP * j;
+        f4 pre[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            f4 v = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int k = 0; k < KP; ++k) {
+                if (k == kp) {
+#pragma unroll
+                    for (int m = 0; m < kNT; ++m)
+                        if (m == nt) v += acc[g][m];
+                } else {
+                    v += stf[(((ug + U * k) * 4 + g) * NU + slot(nt, k)) * 64 + lane];
+                }
+            }
+            pre[g] = v + *(const f4 *)(a.bias + d * G + g * O + uo);
+        }
+        const long long vo = sbase + evox[j];
+        f4 gi, gf, gg, go, c, h;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            gi[i] = fsig(pre[0][i]);
+            gf[i] = fsig(pre[1][i]);
+            gg[i] = ftanh(pre[2][i]);
+            go[i] = fsig(pre[3][i]);
+            c[i] = gg[i] * gi[i] + cprev[j][i] * gf[i];
+            h[i] = go[i] * ftanh(c[i]);
+        }
+        *(f4 *)(a.cell + vo * O + uo) = c;
+        *(f4 *)(a.hd + vo * O + uo) = h;
+        if (a.gates) {
+            float *gp = a.gates + vo * G + uo;
+            *(f4 *)gp = gi;
+            *(f4 *)(gp + O) = gf;
+            *(f4 *)(gp + 2 * O) = gg;
+            *(f4 *)(gp + 3 * O) = go;
+        }
+    }
+}
+
 // ---- line blocks of the 2D layer's forward (16 hidden units) ----------------
 // A 2D direction scans whole lines; each step is one line of Q pixels, too
 // little work for a launch of its own.  Here a workgroup owns a 64-pixel
@@ -2284,10 +2485,45 @@ inline int split_threshold()
     return 8 * (di.cus > 0 ? di.cus : 256);
 }
 
+// LDS bytes of k_step_fwd_bls: the staged [x | h] block or the partial sums,
+// whichever is larger.
+inline size_t fwd_bls_lds(const Geom &g, const FwdStepArgs &a, int U)
+{
+    const int KP = kSW / U, NU = kNT - kNT / KP;
+    size_t m = (size_t)kSW * 4 * NU * 64 * 16;
+    const int nch = a.Cp / 4 + 4 * U;
+    for (int d = 0; d < g.nd; ++d) {
+        const size_t b = (size_t)(a.bp[d] + 2 * (g.KP / 2)) * (a.bq[d] + 2 * (g.KQ / 2)) * nch * 16;
+        if (b > m) m = b;
+    }
+    return m;
+}
+
 template <int U>
 int launch_fwd_steps(const Geom &g, FwdStepArgs &a, hipStream_t st)
 {
     const int T = max_T(g);
+    if (g_step_split == 0) {
+        const size_t lds = fwd_bls_lds(g, a, U);
+        if (lds <= (size_t)device_info().max_lds) {
+            if (hipFuncSetAttribute((const void *)k_step_fwd_bls<U>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)lds) != hipSuccess)
+                return PLSTM_EHIP;
+            for (int t = 0; t < T; ++t) {
+                a.t = t;
+                int nb = 0;
+                for (int d = 0; d < kDirs; ++d) {
+                    a.base[d] = nb;
+                    if (t < g.dir[d].T) nb += g.N * a.nblk[d];
+                }
+                a.base[kDirs] = nb;
+                k_step_fwd_bls<U><<<nb, 64 * kSW, lds, st>>>(a);
+                PLSTM_LAUNCH_CHECK();
+            }
+            return PLSTM_OK;
+        }
+    }
     const int few = split_threshold();
     // staged x or h of a block (the larger of the two phases)
     size_t lds = 0;

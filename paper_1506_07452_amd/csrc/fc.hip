@@ -701,7 +701,7 @@ k_head_reduce(long long M, int Cin, int F, int K, int nblk, const float *__restr
         const int k = (i - P1) / (F + 1), f = (i - P1) % (F + 1);
         if (f < F) dw2[k * F + f] = acc;
         else db2[k] = acc;
-    } else {
+    } else if (loss) {
         *loss = acc / (float)M;
     }
 }
@@ -733,6 +733,178 @@ int head_launch(long long M, int K, const float *x, const float *w1, const float
     PLSTM_LAUNCH_CHECK();
     timing_end(2, st);
     return PLSTM_OK;
+}
+
+// ---- FC + tanh backward on the MFMA ---------------------------------------------
+// For 16 rows at a time (rows on N, as in the fused head): dz = dy (1 - y^2),
+// dX^T = W^T dz^T, and dW = dz^T x, db = sum dz accumulated over the wave's
+// rows through a per-wave LDS transpose of dz and x; workgroup partials in
+// [F][CIN + 1] (then one unused slot) are summed by k_head_reduce in a fixed
+// order.  The next rows' dy, y and x are loaded while these compute.
+template <int CIN, int F>
+struct FcBwdCfg {
+    static constexpr int CT = CIN / 16, FT = F / 16;
+    static constexpr int XP = CIN + 4, ZP = F + 4;        // LDS row pitches (floats)
+    static constexpr int per_wave = 16 * (XP + ZP);
+    static constexpr int red = F * (CIN + 1) + 1;
+    static constexpr size_t bytes = (size_t)(kHW * per_wave + red) * sizeof(float);
+};
+
+template <int CIN, int F>
+__global__ void __launch_bounds__(kHT)
+k_fc_tanh_bwd_mfma(long long M, const float *__restrict__ x, const float *__restrict__ w,
+                   const float *__restrict__ y, const float *__restrict__ dy,
+                   float *__restrict__ dx, float *__restrict__ partial)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    using FC = FcBwdCfg<CIN, F>;
+    static_assert(CIN % 16 == 0 && F % 16 == 0, "tile multiples");
+    constexpr int CT = FC::CT, FT = FC::FT;
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int q = lane >> 4, col = lane & 15;
+    float *xs = lds + wave * FC::per_wave;   // [16][XP]  x
+    float *zs = xs + 16 * FC::XP;            // [16][ZP]  dz
+    float *R = lds + kHW * FC::per_wave;     // workgroup reduction
+
+    float a4[CT][FT][4];   // W[f = 16mt + 4q + i][c = 16ct + col]
+#pragma unroll
+    for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) a4[ct][mt][i] = w[(16 * mt + 4 * q + i) * CIN + 16 * ct + col];
+
+    f4 g1[FT][CT], gb1[FT];
+#pragma unroll
+    for (int mt = 0; mt < FT; ++mt) {
+        gb1[mt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) g1[mt][ct] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    const long long nsub = (M + 15) / 16;
+    const long long gw = (long long)blockIdx.x * kHW + wave, nw = (long long)gridDim.x * kHW;
+    f4 xn[CT], yn[FT], dn[FT];
+    auto load = [&](long long st) {
+        const long long row = st * 16 + col;
+        const long long rr = (st < nsub && row < M) ? row : 0;
+#pragma unroll
+        for (int kt = 0; kt < CT; ++kt) xn[kt] = *(const f4 *)&x[rr * CIN + 16 * kt + 4 * q];
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt) {
+            yn[mt] = *(const f4 *)&y[rr * F + 16 * mt + 4 * q];
+            dn[mt] = *(const f4 *)&dy[rr * F + 16 * mt + 4 * q];
+        }
+    };
+    load(gw);
+    for (long long st = gw; st < nsub; st += nw) {
+        const long long row = st * 16 + col;
+        const bool valid = row < M;
+        f4 xv[CT], dz[FT];
+        const f4 zero = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int kt = 0; kt < CT; ++kt) xv[kt] = valid ? xn[kt] : zero;
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt) {
+            f4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = dn[mt][i] * (1.0f - yn[mt][i] * yn[mt][i]);
+            dz[mt] = valid ? v : zero;
+            gb1[mt] += dz[mt];
+        }
+        load(st + nw);
+        if (dx) {
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                f4 acc = zero;
+#pragma unroll
+                for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[ct][mt][i], dz[mt][i], acc,
+                                                                   0, 0, 0);
+                if (valid) *(f4 *)&dx[row * CIN + 16 * ct + 4 * q] = acc;
+            }
+        }
+#pragma unroll
+        for (int kt = 0; kt < CT; ++kt) *(f4 *)&xs[col * FC::XP + 16 * kt + 4 * q] = xv[kt];
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt) *(f4 *)&zs[col * FC::ZP + 16 * mt + 4 * q] = dz[mt];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int r = 4 * ks + q;
+#pragma unroll
+            for (int mt = 0; mt < FT; ++mt) {
+                const float az = zs[r * FC::ZP + 16 * mt + col];
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+                    g1[mt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        az, xs[r * FC::XP + 16 * ct + col], g1[mt][ct], 0, 0, 0);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    // bias sums over the 16 row lanes of each lane group
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1)
+#pragma unroll
+        for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) gb1[mt][i] += __shfl_xor(gb1[mt][i], off);
+    // workgroup sum in wave order: [F][CIN + 1], then an unused slot
+    constexpr int P1 = F * (CIN + 1), PT = P1 + 1;
+    for (int wv = 0; wv < kHW; ++wv) {
+        if (wave == wv) {
+            auto put = [&](int idx, float v) { R[idx] = wv == 0 ? v : R[idx] + v; };
+#pragma unroll
+            for (int mt = 0; mt < FT; ++mt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int f = 16 * mt + 4 * q + i;
+#pragma unroll
+                    for (int ct = 0; ct < CT; ++ct) put(f * (CIN + 1) + 16 * ct + col, g1[mt][ct][i]);
+                    if (col == 0) put(f * (CIN + 1) + CIN, gb1[mt][i]);
+                }
+            if (lane == 0) put(P1, 0.0f);
+        }
+        __syncthreads();
+    }
+    float *part = partial + (long long)blockIdx.x * PT;
+    for (int e = threadIdx.x; e < PT; e += kHT) part[e] = R[e];
+}
+
+template <int CIN, int F>
+int fc_bwd_mfma_launch(long long M, const float *x, const float *w, const float *y,
+                       const float *dy, float *dx, float *dw, float *db, float *partial,
+                       hipStream_t st)
+{
+    const int nb = head_blocks(M);
+    const size_t lds = FcBwdCfg<CIN, F>::bytes;
+    (void)hipFuncSetAttribute((const void *)k_fc_tanh_bwd_mfma<CIN, F>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    k_fc_tanh_bwd_mfma<CIN, F><<<nb, kHT, lds, st>>>(M, x, w, y, dy, dx, partial);
+    PLSTM_LAUNCH_CHECK();
+    const int PT = F * (CIN + 1) + 1;
+    k_head_reduce<<<(PT + kRedOut - 1) / kRedOut, kThreads, 0, st>>>(
+        M, CIN, F, 0, nb, partial, dw, db, nullptr, nullptr, nullptr);
+    PLSTM_LAUNCH_CHECK();
+    return PLSTM_OK;
+}
+
+// Row counts of the MFMA FC backward's partials (one row of F (CIN + 1) + 1
+// floats per workgroup).
+inline size_t fc_bwd_mfma_floats(long long M, int Cin, int Cout)
+{
+    return (size_t)head_blocks(M) * (Cout * (Cin + 1) + 1);
+}
+inline bool fc_bwd_mfma_ok(int Cin, int Cout)
+{
+    return (Cin == 16 && Cout == 32) || (Cin == 32 && Cout == 64);
 }
 
 inline long long fc_chunk_len(long long M) {
@@ -781,7 +953,10 @@ size_t fc_ws(long long M, int Cin, int Cout)
     cv.take<float>((size_t)fc_chunks(M) * Cout * (Cin + 1));   // weight-gradient partials
     cv.take<float>((size_t)M * (Cout < kMaxK ? Cout : kMaxK)); // dlogits (softmax head)
     cv.take<float>((size_t)(M + kRB - 1) / kRB);               // per-block losses
-    return cv.off;
+    // the MFMA FC backward's workgroup partials use the same workspace
+    const size_t mfma = fc_bwd_mfma_ok(Cin, Cout) ? fc_bwd_mfma_floats(M, Cin, Cout) * sizeof(float)
+                                                  : 0;
+    return cv.off > mfma ? cv.off : mfma;
 }
 
 // ---- FC + tanh on the MFMA ----------------------------------------------------
@@ -941,6 +1116,10 @@ static int fc_tanh_backward_impl(long long M, int Cin, int Cout, const float *x,
                                  const float *w, const float *y, const float *dy, float *dx,
                                  float *dw, float *db, void *ws, hipStream_t st)
 {
+    if (Cin == 16 && Cout == 32)
+        return fc_bwd_mfma_launch<16, 32>(M, x, w, y, dy, dx, dw, db, (float *)ws, st);
+    if (Cin == 32 && Cout == 64)
+        return fc_bwd_mfma_launch<32, 64>(M, x, w, y, dy, dx, dw, db, (float *)ws, st);
     Carve cv(ws);
     float *partial = cv.take<float>((size_t)fc_chunks(M) * Cout * (Cin + 1));
     const RowGrad rg{y, dy};
@@ -1221,7 +1400,7 @@ int fc_tanh_backward(long long M, int Cin, int Cout, const float *x, const float
 {
     timing_begin("fc_tanh_bwd", st);
     const int rc = fc_tanh_backward_impl(M, Cin, Cout, x, w, y, dy, dx, dw, db, ws, st);
-    timing_end(dx ? 3 : 2, st);
+    timing_end(fc_bwd_mfma_ok(Cin, Cout) ? 2 : (dx ? 3 : 2), st);
     return rc;
 }
 

@@ -2020,7 +2020,9 @@ k_step_bwd_blk(BwdStepArgs a)
     }
 }
 
-// dx = sum of the nd directions' shares in direction order.
+// dx = sum of the nd directions' shares in direction order; four elements
+// per thread (n4 = n / 4 vectors, n a multiple of 4), every direction's load
+// in flight before the first add.
 __global__ void __launch_bounds__(256)
 k_sum_dxn(long long n, int nd, const float *__restrict__ dxd, float *__restrict__ dx)
 {
@@ -2028,6 +2030,21 @@ k_sum_dxn(long long n, int nd, const float *__restrict__ dxd, float *__restrict_
     if (i >= n) return;
     float v = dxd[i];
     for (int d = 1; d < nd; ++d) v += dxd[d * n + i];
+    dx[i] = v;
+}
+__global__ void __launch_bounds__(256)
+k_sum_dxn4(long long n4, int nd, const f4 *__restrict__ dxd, f4 *__restrict__ dx)
+{
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n4) return;
+    f4 t[kDirs];
+#pragma unroll
+    for (int d = 0; d < kDirs; ++d)
+        if (d < nd) t[d] = dxd[d * n4 + i];
+    f4 v = t[0];
+#pragma unroll
+    for (int d = 1; d < kDirs; ++d)
+        if (d < nd) v += t[d];
     dx[i] = v;
 }
 
@@ -3095,7 +3112,11 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
         if (with_dx) {
             timing_begin("dx_step", st);
             const long long ndx = nvox * g.C;
-            k_sum_dxn<<<blocks_for(ndx, 256), 256, 0, st>>>(ndx, g.nd, dxd, dx);
+            if ((ndx & 3) == 0 && ((uintptr_t)dx & 15) == 0)
+                k_sum_dxn4<<<blocks_for(ndx / 4, 256), 256, 0, st>>>(ndx / 4, g.nd,
+                                                                      (const f4 *)dxd, (f4 *)dx);
+            else
+                k_sum_dxn<<<blocks_for(ndx, 256), 256, 0, st>>>(ndx, g.nd, dxd, dx);
             PLSTM_LAUNCH_CHECK();
             timing_end(1, st);
             dx_done = true;

@@ -314,6 +314,32 @@ def test_fc_tanh_forward_widths(cin, cout, dtype):
     assert normwise(host(y), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("case", [(1, 16, 32), (129, 16, 32), (1037, 32, 64), (140001, 16, 32),
+                                  (2049, 32, 64), (1037, 64, 128), (515, 24, 40)],
+                         ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("want_dx", [True, False], ids=["dx", "nodx"])
+def test_fc_tanh_backward_widths(case, want_dx):
+    """FC + tanh backward on the MFMA kernel (16 -> 32, 32 -> 64) and the row
+    kernels (other widths): one row, ragged tiles, more row tiles than
+    workgroups, with and without dL/dx."""
+    import paper_1506_07452_amd as P
+    M, cin, cout = case
+    rng = np.random.default_rng(93 + M + cin)
+    xa = rng.standard_normal((M, cin)).astype(np.float32)
+    w1 = rng.uniform(-0.3, 0.3, (cout, cin)).astype(np.float32)
+    ya = np.tanh(rng.standard_normal((M, cout))).astype(np.float32)
+    dy = rng.standard_normal((M, cout)).astype(np.float32)
+    say("fc tanh backward", case, want_dx)
+    dx = torch.empty(M, cin, device=DEV) if want_dx else None
+    dw, db = torch.empty(cout, cin, device=DEV), torch.empty(cout, device=DEV)
+    P.pyramid_fc_tanh_backward(dev(xa), dev(w1), dev(ya), dev(dy), dx, dw, db)
+    torch.cuda.synchronize()
+    rb = oracle.fc_tanh_backward(xa, w1, ya, dy)
+    pairs = [(dw, rb["dw"]), (db, rb["db"])] + ([(dx, rb["dx"])] if want_dx else [])
+    for got, want in pairs:
+        assert normwise(host(got), want) <= TOL["f32"]
+
+
 def oracle_head(xa, w1, b1, w2, b2, lab):
     """FC tanh -> softmax CE -> backward, chained from the oracle's pieces."""
     ry = oracle.fc_tanh_forward(xa, w1, b1)

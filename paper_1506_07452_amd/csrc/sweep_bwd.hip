@@ -161,6 +161,13 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
         }
         __syncthreads();
         const int n_edge = cnt[1];
+        // A lane handles the same pixel of its tiles at every step, so it
+        // keeps (gc f)_t for the next step and the c_{t-1} it loaded, which is
+        // the next step's c_t, in registers: neither is loaded again and gc f
+        // is never stored.
+        f4 carry_gcf[2], carry_c[2];
+#pragma unroll
+        for (int it = 0; it < 2; ++it) carry_gcf[it] = carry_c[it] = f4{0.0f, 0.0f, 0.0f, 0.0f};
         for (int r = 0; r < dg.T; ++r) {
             const int t = dg.T - 1 - r;
             const int s = dg.sign > 0 ? t : dg.T - 1 - t;
@@ -225,14 +232,14 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                     const int vo = splane + ra * sp + (ca + q0) * sq;
                     const bool shared = is_shared_col(ca + q0);
                     BwdEpi e;
-                    const int von = vo - splane + nplane, vop = vo - splane + pplane;
+                    const int vop = vo - splane + pplane;
                     e.dh = *(const f4 *)&dh_n[vo * kO + 4 * q4];
                     e.gi = *(const f4 *)&gates_dn[vo * kG + 0 * kO + 4 * q4];
                     e.gf = *(const f4 *)&gates_dn[vo * kG + 1 * kO + 4 * q4];
                     e.gg = *(const f4 *)&gates_dn[vo * kG + 2 * kO + 4 * q4];
                     e.go = *(const f4 *)&gates_dn[vo * kG + 3 * kO + 4 * q4];
-                    e.c = *(const f4 *)&cell_dn[vo * kO + 4 * q4];
-                    e.gcfn = *(const f4 *)&gcf_dn[von * kO + 4 * q4];
+                    e.c = r == 0 ? *(const f4 *)&cell_dn[vo * kO + 4 * q4] : carry_c[it];
+                    e.gcfn = carry_gcf[it];
                     e.cp = *(const f4 *)&cell_dn[vop * kO + 4 * q4];
                     __builtin_amdgcn_sched_barrier(0);
                     f4 acc[4];
@@ -282,7 +289,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                         *(f4 *)&dst[2 * kO] = dAg;
                         *(f4 *)&dst[3 * kO] = dAo;
                     }
-                    *(f4 *)&gcf_dn[vo * kO + 4 * q4] = gcf;
+                    carry_gcf[it] = gcf;
+                    carry_c[it] = e.cp;
                     hold[it][0] = dAi;
                     hold[it][1] = dAf;
                     hold[it][2] = dAg;

@@ -68,6 +68,43 @@ struct BwdEpi {
     f4 dh, gi, gf, gg, go, c, gcfn, cp;
 };
 
+// sum over taps of dA_{t+1}[p - tap] W_h^T for one 16-pixel tile, on the
+// MFMA: `base` is the lane's LDS pixel, whose row and column neighbours are
+// `rs` and `cs` LDS pixels apart.  The K loop runs in quarters of a tap
+// (quarter j = 4 tap + s: gate-units 16 q4 + 4 s .. + 3 of the lane's pixel
+// as B, the matching W_h^T fragment as A, four MFMAs); each quarter's two LDS
+// reads are issued three quarters (twelve MFMAs) before their use, in a
+// ring of four register slots, so a wave alone keeps the matrix unit busy.
+__device__ __forceinline__ void contract_bwd(const float *as, const float *was, int base, int rs,
+                                             int cs, int q4, int lane, f4 (&acc)[4])
+{
+    constexpr int kQuarters = 36;
+    constexpr int kAhead = 2;
+    f4 bq[kAhead + 1], aq[kAhead + 1];
+    auto load = [&](int j) {
+        const int tap = j >> 2, sq = j & 3;
+        // h_t at pixel p fed A_{t+1} at p - (tap offset)
+        const int pp = base - ((tap / 3 - 1) * rs + (tap % 3 - 1) * cs);
+        bq[j % (kAhead + 1)] = *(const f4 *)&as[pp * kG + 4 * swz(4 * q4 + sq, pp)];
+        aq[j % (kAhead + 1)] = *(const f4 *)&was[((tap * 4 + sq) * 64 + lane) * 4];
+    };
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc[k] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int j = 0; j < kAhead; ++j) load(j);
+#pragma unroll
+    for (int j = 0; j < kQuarters; ++j) {
+        if (j + kAhead < kQuarters) load(j + kAhead);
+        // keep the reads ahead of this quarter's MFMAs
+        __builtin_amdgcn_sched_barrier(0);
+        const int sl = j % (kAhead + 1);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[sl][i], bq[sl][i], acc[i], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
 {
     extern __shared__ float smem[];
@@ -243,25 +280,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                     e.cp = *(const f4 *)&cell_dn[vop * kO + 4 * q4];
                     __builtin_amdgcn_sched_barrier(0);
                     f4 acc[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) acc[q] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-                    for (int tap = 0; tap < 9; ++tap) {
-                        // h_t at pixel p fed A_{t+1} at p - (tap offset); rows
-                        // are consecutive LDS pixels, columns P + 2 apart
-                        const int pp = base - ((tap / 3 - 1) + (tap % 3 - 1) * P2);
-                        f4 bv[4], av[4];
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            bv[q] = *(const f4 *)&as[pp * kG + 4 * swz(4 * q4 + q, pp)];
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            av[q] = *(const f4 *)&was[((tap * 4 + q) * 64 + lane) * 4];
-#pragma unroll
-                        for (int s2 = 0; s2 < 16; ++s2)
-                            acc[s2 & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                av[s2 >> 2][s2 & 3], bv[s2 >> 2][s2 & 3], acc[s2 & 3], 0, 0, 0);
-                    }
+                    contract_bwd(as, was, base, 1, P2, q4, lane, acc);
                     f4 dAi, dAf, dAg, dAo, gcf;
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
@@ -411,27 +430,6 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                 e.gcfn = *(const f4 *)&gcf_dn[von * kO + 4 * q4];
                 e.cp = *(const f4 *)&cell_dn[vop * kO + 4 * q4];
             };
-            auto contract = [&](int base, f4 (&acc)[4]) {
-#pragma unroll
-                for (int k = 0; k < 4; ++k) acc[k] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-                for (int tap = 0; tap < 9; ++tap) {
-                    // h_t at pixel p fed A_{t+1} at p - (tap offset)
-                    const int o = (tap / 3 - 1) * W2 + (tap % 3 - 1);
-                    const int pp = base - o;
-                    f4 bv[4], av[4];
-#pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        bv[k] = *(const f4 *)&as[pp * kG + 4 * swz(4 * q4 + k, pp)];
-#pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        av[k] = *(const f4 *)&was[((tap * 4 + k) * 64 + lane) * 4];
-#pragma unroll
-                    for (int s2 = 0; s2 < 16; ++s2)
-                        acc[s2 & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            av[s2 >> 2][s2 & 3], bv[s2 >> 2][s2 & 3], acc[s2 & 3], 0, 0, 0);
-                }
-            };
             auto epilogue = [&](int vo, bool shared, const f4 (&acc)[4], const BwdEpi &e) {
                 f4 dAi, dAf, dAg, dAo, gcf;
 #pragma unroll
@@ -472,7 +470,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_sweep_bwd(BwdArgs a)
                 // otherwise sink them to their use and expose their latency)
                 __builtin_amdgcn_sched_barrier(0);
                 f4 acc[4];
-                contract(base, acc);
+                contract_bwd(as, was, base, W2, 1, q4, lane, acc);
                 epilogue(vo, shared, acc, e);
             }
             __syncthreads();

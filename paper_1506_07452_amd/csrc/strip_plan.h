@@ -87,8 +87,24 @@ inline StripShape strip_shape(const DirGeom &r, int k, const StripCostModel &m, 
     const long long max_rows =
         lds_limit > m.fixed_bytes ? (long long)((lds_limit - m.fixed_bytes) / per_row) - 2 : 0;
     if (max_rows < 1) return sh;   // rows = 0: does not fit
-    sh.chunks = (int)((r.P + max_rows - 1) / max_rows);
-    sh.rows = (r.P + sh.chunks - 1) / sh.chunks;
+    // Rows per chunk: the four SIMDs take a chunk's 16-pixel tiles in rounds
+    // of four, so among the row counts that fit, take the one with the
+    // fewest modelled rounds plus stagings over the plane (the last chunk
+    // holds the remaining rows); ties go to the larger chunk.
+    const long long lo = max_rows / 2 > 1 ? max_rows / 2 : 1;
+    double best = 1e300;
+    for (long long rows = max_rows; rows >= lo; --rows) {
+        const long long chunks = (r.P + rows - 1) / rows;
+        const long long last = r.P - (chunks - 1) * rows;
+        const long long rounds = (chunks - 1) * ((rows * sh.w + 63) / 64) + (last * sh.w + 63) / 64;
+        const double c = (double)chunks * (m.c_stage0 + m.c_stage_px * (rows + 2) * (sh.w + 2)) +
+                         (double)rounds * m.c_tile;
+        if (c < best * (1.0 - 1e-9)) {
+            best = c;
+            sh.rows = (int)rows;
+            sh.chunks = (int)chunks;
+        }
+    }
     sh.lds = m.fixed_bytes + (size_t)(sh.rows + 2) * per_row;
     return sh;
 }
@@ -100,7 +116,9 @@ inline double strip_cost(const DirGeom &r, int k, const StripCostModel &m, size_
     const int tiles = (sh.rows * sh.w + 15) / 16;
     if (sh.resident) return (double)r.T * (m.c_res_step + ((tiles + 3) / 4) * m.c_tile);
     const double stage = m.c_stage0 + m.c_stage_px * (sh.rows + 2) * (sh.w + 2);
-    return (double)r.T * (m.c_sync + sh.chunks * (stage + ((tiles + 3) / 4) * m.c_tile));
+    const int last = r.P - (sh.chunks - 1) * sh.rows;
+    const int rounds = (sh.chunks - 1) * ((sh.rows * sh.w + 63) / 64) + (last * sh.w + 63) / 64;
+    return (double)r.T * (m.c_sync + sh.chunks * stage + rounds * m.c_tile);
 }
 
 // For each axis only the counts k = ceil(Q / w) (the fewest strips of

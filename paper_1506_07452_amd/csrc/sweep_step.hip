@@ -46,6 +46,7 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kSW = 4;                   // waves per workgroup
+constexpr int kXcds = 8;                 // XCDs: workgroup b runs on XCD b % 8
 constexpr int kNT = 4;                   // 16-pixel tiles per wave
 constexpr int kOOB = 0x7ffffff0;         // byte offset past any buffer: loads return 0
 constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data
@@ -2244,11 +2245,17 @@ __device__ inline void wg_wave(const WgStepArgs &a, int d, int kc, int mblk, boo
         }
 }
 
+// Work items run N-block fastest, so the waves that read the same voxel chunk
+// of dA (one per N-block) are neighbours; the grid (a multiple of eight
+// workgroups) is remapped so that each XCD, which takes every eighth
+// workgroup, runs a contiguous range of items and those waves share its L2.
 template <int U>
 __global__ void __launch_bounds__(64 * kSW) __attribute__((amdgpu_waves_per_eu(2)))
 k_wgrad_step(WgStepArgs a)
 {
-    const int item = blockIdx.x * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int per_xcd = gridDim.x / kXcds;
+    const int lblk = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    const int item = lblk * kSW + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int KK = a.g.KP * a.g.KQ, XT = wg_xtiles(KK, a.g.C);
     const WgBlocks wb = wg_blocks(U, XT, KK);
     const int nblk = wb.nh + wb.nx;
@@ -2256,9 +2263,9 @@ k_wgrad_step(WgStepArgs a)
     if (item >= a.g.nd * per_dir) return;
     const int d = item / per_dir;
     int r = item - d * per_dir;
-    const int kc = r % a.kch;
-    r /= a.kch;
-    const int nb = r % nblk, mblk = r / nblk;
+    const int nb = r % nblk;
+    r /= nblk;
+    const int kc = r % a.kch, mblk = r / a.kch;
     const bool is_h = nb < wb.nh;
     // first N-tile and tile count of this block; x tiles numbered after h's
     const int tb = is_h ? wb.th : wb.tx;
@@ -3133,10 +3140,11 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     wa.partial = partial;
     wa.k_mul = k_mul_of(g);
     const long long witems = (long long)g.nd * U * w.nblk * w.kch;
+    const long long wblocks = (blocks_for(witems, kSW) + kXcds - 1) / kXcds * kXcds;
     switch (U) {
-    case 1: k_wgrad_step<1><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
-    case 2: k_wgrad_step<2><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
-    default: k_wgrad_step<4><<<blocks_for(witems, kSW), 64 * kSW, 0, st>>>(wa); break;
+    case 1: k_wgrad_step<1><<<wblocks, 64 * kSW, 0, st>>>(wa); break;
+    case 2: k_wgrad_step<2><<<wblocks, 64 * kSW, 0, st>>>(wa); break;
+    default: k_wgrad_step<4><<<wblocks, 64 * kSW, 0, st>>>(wa); break;
     }
     PLSTM_LAUNCH_CHECK();
     // db: the column of ones, unless the line blocks summed it already

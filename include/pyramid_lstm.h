@@ -413,6 +413,15 @@ int pyramid_lstm_set_step_split(int mode);
  * Returns PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_bf16_mfma(int on);
 
+/* Weight gradients of the plane-step backward, for testing and tuning
+ * (process-wide): 1 = a staged GEMM (default where it applies: at most 32
+ * hidden units and C a multiple of 4): each workgroup stages a 16-voxel unit
+ * of dA and of the im2col columns in LDS once for eight waves; 0 = the
+ * register-streamed kernel, each wave reading its own operands from memory.
+ * Results differ only in summation order.  Returns PLSTM_EINVAL for other
+ * values. */
+int pyramid_lstm_set_wgrad_staged(int on);
+
 #ifdef __cplusplus
 }
 #endif

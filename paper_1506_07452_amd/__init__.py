@@ -24,6 +24,7 @@ __all__ = [
     "pyramid_crop", "pyramid_stitch_clear", "pyramid_stitch_add", "pyramid_stitch_finish",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
     "pyramid_lstm_set_backward_path", "pyramid_lstm_set_step_split", "pyramid_lstm_set_bf16_mfma",
+    "pyramid_lstm_set_wgrad_staged",
     "library_path", "load", "plstm2d_shape", "shape2d_for", "pyramid_lstm2d_workspace_size",
     "pyramid_lstm2d_saved_size", "pyramid_lstm2d_forward", "pyramid_lstm2d_backward",
     "plstm_cube", "PLSTM_FLIP_Z", "PLSTM_FLIP_Y", "PLSTM_FLIP_X", "PLSTM_MAX_CUBES",
@@ -156,6 +157,8 @@ def load():
     lib.pyramid_lstm_set_bf16_mfma.restype = ctypes.c_int
     lib.pyramid_lstm_set_step_split.argtypes = [ctypes.c_int]
     lib.pyramid_lstm_set_step_split.restype = ctypes.c_int
+    lib.pyramid_lstm_set_wgrad_staged.argtypes = [ctypes.c_int]
+    lib.pyramid_lstm_set_wgrad_staged.restype = ctypes.c_int
     lib.pyramid_lstm_set_forward_path.argtypes = [ctypes.c_int]
     lib.pyramid_lstm_set_forward_path.restype = ctypes.c_int
     lib.pyramid_lstm_set_backward_path.argtypes = [ctypes.c_int]
@@ -504,6 +507,13 @@ def pyramid_lstm_set_bf16_mfma(on: int) -> None:
     accumulation) on pixel blocks staged in LDS, 2 = bf16 MFMA reading its
     operands from L1, 0 = fp32 MFMA."""
     _check("pyramid_lstm_set_bf16_mfma", load().pyramid_lstm_set_bf16_mfma(int(on)))
+
+
+def pyramid_lstm_set_wgrad_staged(on: int) -> None:
+    """Plane-step weight gradients: 1 = the LDS-staged GEMM where it applies
+    (at most 32 hidden units, C a multiple of 4), 0 = the register-streamed
+    kernel."""
+    _check("pyramid_lstm_set_wgrad_staged", load().pyramid_lstm_set_wgrad_staged(int(on)))
 
 
 def pyramid_lstm_device_status(clear: bool = False, stream=None) -> int:

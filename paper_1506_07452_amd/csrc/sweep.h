@@ -84,5 +84,9 @@ extern int g_step_split;
 // with pixel blocks staged in LDS (default), 2 = bf16 MFMA with operands read
 // from L1, 0 = on the fp32 MFMA.
 extern int g_step_bf16_mfma;
+// Weight gradients of the plane-step path: 1 = the LDS-staged GEMM where it
+// applies (at most 32 hidden units, C % 4 == 0; default), 0 = the
+// register-streamed kernel.
+extern int g_wgrad_staged;
 
 }  // namespace plstm

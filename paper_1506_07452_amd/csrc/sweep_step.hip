@@ -2299,6 +2299,251 @@ k_wgrad_step(WgStepArgs a)
     }
 }
 
+// ---- parameter gradients through LDS (up to 32 hidden units, C % 4 == 0) ----
+// The same products as k_wgrad_step, organised as a staged GEMM: one
+// workgroup of eight waves per (direction, N-part, voxel chunk) holds the
+// whole [4O x 16 NT] partial sum of its N-part (at most kWlPartNT N-tiles;
+// wave w takes N-tiles w, w + 8, w + 16 and all 4U M-tiles).  Pairs of
+// 16-voxel units (as in k_wgrad_step: consecutive rows of a column group)
+// are staged once for all eight waves:
+//   dA transposed to [gate][voxel] and the im2col columns of the part to
+//   [column][voxel] (h_{t-1} taps, x_t taps, the column of ones; zero off
+//   the plane and before the first plane),
+// each row holding the pair's 32 voxels padded to kWlRow floats, so that
+// the 16 rows a lane group reads fall in 16 different bank groups; one
+// ds_read_b128 gives a lane its four k-steps of a unit (voxels 4 q .. 4 q + 3).
+// Two stage buffers: the next pair's global loads are in flight while this
+// pair's MFMAs run, then go to the other buffer, one barrier per pair.  dA
+// is read from memory once per N-part instead of once per N-block wave.
+constexpr int kWlWaves = 8;
+constexpr int kWlThreads = 64 * kWlWaves;
+template <int N> struct IntC {
+    static constexpr int value = N;
+};
+constexpr int kWlPartNT = 20;             // most N-tiles of a part
+constexpr int kWlNT = 3;                  // N-tiles per wave: ceil(20 / 8)
+constexpr int kWlRow = 36;                // floats per staged row: 2 x 16 voxels + pad
+constexpr int kWlBSlots = 3;              // column quads x voxels per thread: 20 * 64 / 512
+
+struct WlArgs {
+    Geom g;
+    int NTt, nparts, kch;
+    const float *x, *hd, *dA;
+    float *partial;           // [6][kch][4O][16 NTt] (chunk partials of every part)
+};
+
+template <int U>
+__global__ void __launch_bounds__(kWlThreads, 1) __attribute__((amdgpu_waves_per_eu(1, 2)))
+k_wgrad_lds(WlArgs a)
+{
+    constexpr int O = 16 * U, G = 4 * O, MT = 4 * U;
+    extern __shared__ float wl_smem[];
+    const int per_dir = a.nparts * a.kch;
+    const int d = blockIdx.x / per_dir;
+    const int part = (blockIdx.x % per_dir) / a.kch, kc = blockIdx.x % a.kch;
+    const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, col = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int KQ = a.g.KQ, KK = a.g.KP * KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
+    const int C = a.g.C, NTt = a.NTt, KCp = NTt * 16;
+    const int KO = KK * O, KX = KK * C;          // h columns, x columns
+    // this part's N-tiles [nt0, nt1)
+    const int nt0 = (int)((long long)NTt * part / a.nparts);
+    const int nt1 = (int)((long long)NTt * (part + 1) / a.nparts);
+    const int ncol = (nt1 - nt0) * 16;
+    const DirGeom dg = a.g.dir[d];
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const int ngrp = (Q + 15) >> 4;
+    const int rows = G + ncol;
+    float *const buf0 = wl_smem, *const buf1 = wl_smem + (size_t)rows * kWlRow;
+
+    // columns that never change: the column of ones and the padding past it
+    for (int e = tid; e < 2 * ncol * 32; e += kWlThreads) {
+        const int b = e / (ncol * 32), r = e - b * ncol * 32;
+        const int c = nt0 * 16 + r / 32;
+        if (c >= KO + KX)
+            (b ? buf1 : buf0)[(G + r / 32) * kWlRow + (r & 31)] = c == KO + KX ? 1.0f : 0.0f;
+    }
+
+    // unit cursor over this chunk: (n, t, column group, row), row fastest
+    const long long units = (long long)a.g.N * dg.T * ngrp * P;
+    const long long u0 = units * kc / a.kch, u1 = units * (kc + 1) / a.kch;
+    int cn, ct, cg, cp;
+    {
+        long long rest = u0;
+        cp = (int)(rest % P); rest /= P;
+        cg = (int)(rest % ngrp); rest /= ngrp;
+        ct = (int)(rest % dg.T);
+        cn = (int)(rest / dg.T);
+        if (cn >= a.g.N) cn = a.g.N - 1;
+    }
+    auto advance = [&]() __attribute__((always_inline)) {
+        if (++cp == P) {
+            cp = 0;
+            if (++cg == ngrp) {
+                cg = 0;
+                if (++ct == dg.T) {
+                    ct = 0;
+                    if (cn + 1 < a.g.N) ++cn;
+                }
+            }
+        }
+    };
+
+    // staged registers of a pair of units: dA (one quad of gates of one
+    // voxel per thread and unit) and the part's im2col quads (column quad,
+    // voxel); a unit past the chunk stages zeros
+    struct Stage {
+        f4 a[2];
+        f4 b[2][kWlBSlots];
+    };
+    const int nbq = ncol / 4 * 16;                 // column quads x voxels of a unit
+    // Branch-free loads: a masked operand (past the plane, off the volume,
+    // h_{-1}, a column past the layer's or a unit past the chunk) gets an
+    // out-of-range offset and reads zero.  A wave's 64 lanes of one slot
+    // cover one 16-column N-tile, all of h or all of x, so the source
+    // (resource, stride, plane) is uniform per slot; the slot's tap offset
+    // and channel do not change from unit to unit.
+    int s_dp[kWlBSlots], s_dq[kWlBSlots], s_ch[kWlBSlots];
+    bool s_h[kWlBSlots], s_ok[kWlBSlots];
+#pragma unroll
+    for (int k = 0; k < kWlBSlots; ++k) {
+        const int e = k * kWlThreads + tid;
+        const int c = nt0 * 16 + 4 * (e >> 4);   // first column of the lane's quad
+        s_h[k] = __builtin_amdgcn_readfirstlane(c < KO ? 1 : 0) != 0;
+        const int kk = s_h[k] ? c : c - KO;
+        const int tap = s_h[k] ? kk / O : kk / C;
+        s_ch[k] = s_h[k] ? kk % O : kk % C;
+        s_dp[k] = tap / KQ - radp;
+        s_dq[k] = tap % KQ - radq;
+        s_ok[k] = (e < nbq) & (c < KO + KX);
+    }
+    auto fetch_unit = [&](f4 &sa, f4 (&sb4)[kWlBSlots], bool live) __attribute__((always_inline)) {
+        const long long sb = ((long long)d * a.g.N + cn) * V;
+        const int s = dg.sign > 0 ? ct : dg.T - 1 - ct;
+        const auto rs_a = slice_rsrc(a.dA + sb * G, V * G);
+        const auto rs_h = slice_rsrc(a.hd + sb * O, V * O);
+        const auto rs_x = slice_rsrc(a.x + (long long)cn * V * C, V * C);
+        const int q = cg * 16 + (tid & 15);
+        {
+            // dA: thread -> (voxel, gate quad), voxel fastest
+            const int gq = tid >> 4;
+            const bool ok = live & (tid < 16 * (G / 4)) & (q < Q);
+            sa = bload4(rs_a, sel_off(ok, (unsigned)((s * ss + cp * sp + q * sq) * G + 4 * gq) * 4u));
+        }
+#pragma unroll
+        for (int k = 0; k < kWlBSlots; ++k) {
+            const int pp = cp + s_dp[k], qn = q + s_dq[k];
+            const bool ok = live & s_ok[k] & ((unsigned)pp < (unsigned)P) &
+                            ((unsigned)qn < (unsigned)Q) & (!s_h[k] | (ct > 0));
+            const int pl = s_h[k] ? s - dg.sign : s;
+            const int stride = s_h[k] ? O : C;
+            const auto rs = s_h[k] ? rs_h : rs_x;
+            sb4[k] = bload4(rs, sel_off(ok, (unsigned)((pl * ss + pp * sp + qn * sq) * stride +
+                                                       s_ch[k]) * 4u));
+        }
+    };
+    // stage units u and u + 1 (of `total`); the cursor is at unit u
+    auto fetch = [&](Stage &st, long long u, long long total) __attribute__((always_inline)) {
+        fetch_unit(st.a[0], st.b[0], u < total);
+        if (u + 1 < total) advance();
+        fetch_unit(st.a[1], st.b[1], u + 1 < total);
+    };
+    auto put = [&](const Stage &st, float *bf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            {
+                const int i = tid & 15, gq = tid >> 4;
+                if (tid < 16 * (G / 4)) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        bf[(4 * gq + j) * kWlRow + 16 * h + i] = st.a[h][j];
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kWlBSlots; ++k) {
+                const int e = k * kWlThreads + tid;
+                const int i = e & 15, cq = e >> 4;
+                if (e < nbq && nt0 * 16 + 4 * cq < KO + KX) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        bf[(G + 4 * cq + j) * kWlRow + 16 * h + i] = st.b[h][k][j];
+                }
+            }
+        }
+    };
+
+    f4 acc[MT][kWlNT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int j = 0; j < kWlNT; ++j) acc[m][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int nmy = max(0, (nt1 - nt0 - wave + kWlWaves - 1) / kWlWaves);   // this wave's N-tiles
+
+    // products of one staged unit (h: which half of the rows) for the wave's
+    // NTW N-tiles
+    auto compute = [&](const float *bf, int h, auto ntw) __attribute__((always_inline)) {
+        constexpr int NTW = decltype(ntw)::value;
+        f4 bv[NTW];
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+            bv[j] = *(const f4 *)&bf[(G + (wave + kWlWaves * j) * 16 + col) * kWlRow + 16 * h +
+                                     4 * q4];
+        f4 av[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+            av[m] = *(const f4 *)&bf[(m * 16 + col) * kWlRow + 16 * h + 4 * q4];
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int j = 0; j < NTW; ++j) acc[m][j] = mfma(av[m][ks], bv[j][ks], acc[m][j]);
+    };
+    auto compute_pair = [&](const float *bf, bool second) __attribute__((always_inline)) {
+        if (nmy >= 3) {
+            compute(bf, 0, IntC<3>{});
+            if (second) compute(bf, 1, IntC<3>{});
+        } else if (nmy == 2) {
+            compute(bf, 0, IntC<2>{});
+            if (second) compute(bf, 1, IntC<2>{});
+        } else if (nmy == 1) {
+            compute(bf, 0, IntC<1>{});
+            if (second) compute(bf, 1, IntC<1>{});
+        }
+    };
+
+    const long long total = u1 - u0;
+    if (total > 0) {
+        Stage st;
+        fetch(st, 0, total);
+        put(st, buf0);
+        __syncthreads();
+        for (long long u = 0; u < total; u += 2) {
+            const bool more = u + 2 < total;
+            if (more) {
+                advance();
+                fetch(st, u + 2, total);
+            }
+            compute_pair((u >> 1) & 1 ? buf1 : buf0, u + 1 < total);
+            if (more) put(st, (u >> 1) & 1 ? buf0 : buf1);
+            __syncthreads();
+        }
+    }
+    float *out = a.partial + ((long long)d * a.kch + kc) * G * KCp;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int j = 0; j < kWlNT; ++j) {
+            if (j >= nmy) continue;
+            const int nt = nt0 + wave + kWlWaves * j;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                out[(long long)(m * 16 + 4 * q4 + i) * KCp + nt * 16 + col] = acc[m][j][i];
+        }
+}
+
 // dW = sum of the chunk partials in chunk order, scattered to the ABI layouts;
 // the column of ones gives db (skipped when db is null).
 __global__ void __launch_bounds__(256)
@@ -2470,13 +2715,14 @@ inline int max_T(const Geom &g)
 
 struct WgShape {
     int NTt, nblk, kch;
+    int lds_parts;    // > 0: k_wgrad_lds with this many N-parts (kch chunks each)
 };
 // Voxel chunks per (direction, block): the launch takes ceil(waves / slots)
 // rounds of 1/kch of a block's work; pick the chunk count that minimises that
 // (ties: fewer chunks).  Blocks of four N-tiles count one wave per SIMD;
 // blocks of fewer tiles do less MFMA work per load and are given three, the
 // kernel's occupancy at its register count.
-inline WgShape wg_shape(const Geom &g)
+inline WgShape wg_shape(const Geom &g, bool staged = g_wgrad_staged != 0)
 {
     const int U = g.O / 16, KK = g.KP * g.KQ, XT = wg_xtiles(KK, g.C);
     const WgBlocks wb = wg_blocks(U, XT, KK);
@@ -2484,6 +2730,18 @@ inline WgShape wg_shape(const Geom &g)
     w.NTt = KK * U + XT;
     w.nblk = wb.nh + wb.nx;
     const DevInfo di = device_info();
+    w.lds_parts = 0;
+    // (the staged kernel addresses dA, h and x of a (direction, batch
+    // element) slice as buffer resources: byte sizes within 31 bits)
+    if (staged && U <= 2 && g.C % 4 == 0 &&
+        g.V * 4 * g.O * (long long)sizeof(float) < (1LL << 31)) {
+        // N-parts of at most kWlPartNT tiles, about one workgroup per CU
+        w.lds_parts = (w.NTt + kWlPartNT - 1) / kWlPartNT;
+        const int per = g.nd * w.lds_parts;
+        const int cus = di.cus > 0 ? di.cus : 256;
+        w.kch = cus / per > 1 ? cus / per : 1;
+        return w;
+    }
     const int per_simd = (wb.th < kWgN && wb.tx < kWgN) ? 3 : 1;
     const long long simds = 4LL * per_simd * (di.cus > 0 ? di.cus : 256);   // wave slots
     const long long per = (long long)g.nd * U * w.nblk;
@@ -2497,6 +2755,15 @@ inline WgShape wg_shape(const Geom &g)
         }
     }
     return w;
+}
+
+// Weight-gradient partial sums for either kernel (the choice may change
+// between a workspace query and the call).
+inline size_t wg_partial_floats(const Geom &g)
+{
+    const WgShape w0 = wg_shape(g, false), w1 = wg_shape(g, true);
+    const int kch = w0.kch > w1.kch ? w0.kch : w1.kch;
+    return (size_t)g.nd * kch * 4 * g.O * w0.NTt * 16;
 }
 
 // Waves below which a step splits each tile's K over a workgroup's waves:
@@ -2681,6 +2948,7 @@ int launch_dx_ct(const DxStepArgs &a, hipStream_t st)
 
 int g_step_split = 0;
 int g_step_bf16_mfma = 1;
+int g_wgrad_staged = 1;
 
 bool step_supported(const Geom &g)
 {
@@ -2959,7 +3227,7 @@ size_t step_bwd_ws(const Geom &g)
     cv.take<float>((size_t)g.nd * g.N * g.V * G);                  // dA
     cv.take<float>((size_t)g.nd * g.N * g.V * g.O);                // dL/dc * f
     cv.take<float>((size_t)g.nd * U * KK * 4 * U * 256);           // W_h^T fragments
-    cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);         // weight-gradient partials
+    cv.take<float>(wg_partial_floats(g));                           // weight-gradient partials
     cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);   // W_x^T fragments
     if (bwd_dxd(g)) cv.take<float>((size_t)g.nd * g.N * g.V * g.C);   // dL/dx per direction
     if (line_bwd_geom(g)) cv.take<float>((size_t)g.nd * g.N * line_nsegmax(g) * 64);  // db partials
@@ -3014,7 +3282,7 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     float *dA = cv.take<float>((size_t)g.nd * g.N * g.V * G);
     float *gcf = cv.take<float>((size_t)g.nd * g.N * g.V * g.O);
     float *frag = cv.take<float>((size_t)g.nd * U * KK * 4 * U * 256);
-    float *partial = cv.take<float>((size_t)g.nd * w.kch * G * w.NTt * 16);
+    float *partial = cv.take<float>(wg_partial_floats(g));
     float *fragx = cv.take<float>((size_t)g.nd * KK * 4 * U * (Cp / 16) * 256);
     float *dxd = bwd_dxd(g) ? cv.take<float>((size_t)g.nd * g.N * g.V * g.C) : nullptr;
     float *dbl = line_bwd_geom(g) ? cv.take<float>((size_t)g.nd * g.N * line_nsegmax(g) * 64)
@@ -3131,6 +3399,33 @@ int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, co
     }
 
     timing_begin("wgrad_step", st);
+    if (w.lds_parts > 0) {
+        WlArgs la;
+        la.g = g;
+        la.NTt = w.NTt; la.nparts = w.lds_parts; la.kch = w.kch;
+        la.x = x; la.hd = sv.hd; la.dA = dA;
+        la.partial = partial;
+        const int nb = g.nd * w.lds_parts * w.kch;
+        const int nmax = (w.NTt + w.lds_parts - 1) / w.lds_parts * 16;   // widest part's columns
+        const size_t lds = 2 * (size_t)(G + nmax) * kWlRow * sizeof(float);
+        if (U == 1) {
+            (void)hipFuncSetAttribute((const void *)k_wgrad_lds<1>,
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            k_wgrad_lds<1><<<nb, kWlThreads, lds, st>>>(la);
+        } else {
+            (void)hipFuncSetAttribute((const void *)k_wgrad_lds<2>,
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            k_wgrad_lds<2><<<nb, kWlThreads, lds, st>>>(la);
+        }
+        PLSTM_LAUNCH_CHECK();
+        const long long nout = (long long)g.nd * G * (KK * (g.O + g.C) + 1);
+        k_wgrad_step_reduce<<<blocks_for(nout, 256), 256, 0, st>>>(
+            g.nd, g.O, g.C, Cp, KK, w.NTt, w.kch, partial, dwx, dwh, db_done ? nullptr : db);
+        PLSTM_LAUNCH_CHECK();
+        timing_end(2, st);
+        if (dx && !dx_done) return step_dx(g, wx, dA, fragx, dx, st);
+        return PLSTM_OK;
+    }
     // the x tiles read one channel per lane: x itself, C floats per voxel
     WgStepArgs wa;
     wa.g = g;
@@ -3170,5 +3465,12 @@ extern "C" int pyramid_lstm_set_bf16_mfma(int on)
 {
     if (on < 0 || on > 2) return PLSTM_EINVAL;
     plstm::g_step_bf16_mfma = on;
+    return PLSTM_OK;
+}
+
+extern "C" int pyramid_lstm_set_wgrad_staged(int on)
+{
+    if (on != 0 && on != 1) return PLSTM_EINVAL;
+    plstm::g_wgrad_staged = on;
     return PLSTM_OK;
 }

@@ -175,7 +175,8 @@ def test_binding_refuses_host_tensors():
 
 def test_path_knobs_and_timing_without_gpu():
     for fn, top in ((P.pyramid_lstm_set_forward_path, 4), (P.pyramid_lstm_set_backward_path, 3),
-                    (P.pyramid_lstm_set_step_split, 3), (P.pyramid_lstm_set_bf16_mfma, 2)):
+                    (P.pyramid_lstm_set_step_split, 3), (P.pyramid_lstm_set_bf16_mfma, 2),
+                    (P.pyramid_lstm_set_wgrad_staged, 1)):
         for v in list(range(1, top + 1)) + [0]:
             fn(v)
         with pytest.raises(P.PyramidLSTMError):
@@ -183,6 +184,7 @@ def test_path_knobs_and_timing_without_gpu():
         with pytest.raises(P.PyramidLSTMError):
             fn(-1)
     P.pyramid_lstm_set_bf16_mfma(1)       # back to the defaults
+    P.pyramid_lstm_set_wgrad_staged(1)
     P.pyramid_lstm_set_forward_path(0)
     P.pyramid_lstm_timing_enable(True)
     assert P.pyramid_lstm_timing_read() == {}

@@ -201,6 +201,32 @@ def test_step_path_matches_oracle(shape, step_path, step_split):
         assert err <= TOL["f32"], (name, err)
 
 
+@pytest.mark.parametrize("staged", [1, 0], ids=["lds", "streamed"])
+@pytest.mark.parametrize("shape", [(2, 9, 17, 40, 32, 32), (1, 6, 5, 4, 20, 16),
+                                   (1, 5, 12, 70, 8, 32), (1, 3, 21, 5, 4, 16)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_step_weight_gradients_both_kernels(shape, staged, step_path):
+    """The plane-step weight gradients from the LDS-staged GEMM (several
+    N-parts and voxel chunks, ragged 16-voxel units, batch > 1) and from the
+    register-streamed kernel, against the oracle."""
+    inst = instance(shape, 4500 + sum(shape))
+    L = inst.layers[0]
+    dh = synth.upstream_grad(inst.x.shape[:-1] + (shape[-1],), 17 + sum(shape))
+    ref = oracle.backward(inst.x, L.wx, L.wh, L.b, dh)
+    say("wgrad kernels", shape, staged)
+    P.pyramid_lstm_set_wgrad_staged(staged)
+    try:
+        x, Ld = dev(inst.x), layer_dev(L)
+        h, saved = layer_forward(x, Ld, training=True)
+        dx, dwx, dwh, db = layer_backward(x, Ld, saved, dev(dh))
+        torch.cuda.synchronize()
+    finally:
+        P.pyramid_lstm_set_wgrad_staged(1)
+    for name, got in (("dx", dx), ("dwx", dwx), ("dwh", dwh), ("db", db)):
+        err = normwise(host(got), ref[name])
+        assert err <= TOL["f32"], (name, err)
+
+
 @pytest.mark.parametrize("shape", [(1, 5, 37, 29, 3, 16), (1, 4, 6, 70, 3, 64)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_step_path_saved_state_matches_oracle(shape, step_path):

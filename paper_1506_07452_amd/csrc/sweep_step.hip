@@ -2309,9 +2309,12 @@ k_wgrad_step(WgStepArgs a)
 //   dA transposed to [gate][voxel] and the im2col columns of the part to
 //   [column][voxel] (h_{t-1} taps, x_t taps, the column of ones; zero off
 //   the plane and before the first plane),
-// each row holding the pair's 32 voxels padded to kWlRow floats, so that
-// the 16 rows a lane group reads fall in 16 different bank groups; one
+// each row holding the pair's 32 voxels padded to kWlRow floats; one
 // ds_read_b128 gives a lane its four k-steps of a unit (voxels 4 q .. 4 q + 3).
+// (On gfx950, 64 lanes reading 16 bytes each at row r = lane % 16, offset
+// 4 (lane / 16) run without bank conflicts when the row stride is 8 mod 16
+// floats (24, 40, 56, ...); strides of 36 or 20 floats take half as long
+// again, measured.)
 // Two stage buffers: the next pair's global loads are in flight while this
 // pair's MFMAs run, then go to the other buffer, one barrier per pair.  dA
 // is read from memory once per N-part instead of once per N-block wave.
@@ -2322,7 +2325,7 @@ template <int N> struct IntC {
 };
 constexpr int kWlPartNT = 20;             // most N-tiles of a part
 constexpr int kWlNT = 3;                  // N-tiles per wave: ceil(20 / 8)
-constexpr int kWlRow = 36;                // floats per staged row: 2 x 16 voxels + pad
+constexpr int kWlRow = 40;                // floats per staged row: 2 x 16 voxels + pad
 constexpr int kWlBSlots = 3;              // column quads x voxels per thread: 20 * 64 / 512
 
 struct WlArgs {

@@ -70,15 +70,28 @@ def phase_work(name, V, C, O, K=3):
     return None, None, None
 
 
-# HBM bytes per launch measured with rocprofv3 counters (FETCH_SIZE, WRITE_SIZE,
-# calibrated against a copy of known size); valid while the kernel sources are
-# the ones measured.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_mr48x240x240.md")
+# Counter figures measured with rocprofv3 and committed under profiles/ as
+# machine-readable lines (one per workload and bench phase):
+#   traffic workload=W kernel=K mode=M bytes_per_pass=B src=S
+#       HBM bytes (FETCH_SIZE + WRITE_SIZE, each calibrated against a copy of
+#       known size) of the phase's kernels over one pass of the workload
+#   mfma workload=W kernel=K flops_per_pass=F busy=U src=S
+#       executed MFMA flops (SQ_INSTS_VALU_MFMA_MOPS_F32/BF16 x 512) and the
+#       matrix units' busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over
+#       GRBM_GUI_ACTIVE x 128)
+# S is the first 16 hex digits of the SHA-256 of the kernel's sources when
+# measured; a figure whose sources changed since is reported as null.
+PROFILES = os.path.join(ROOT, "profiles")
+_STEP = ["sweep_step.hip", "common.h"]
 KERNEL_SOURCES = {
     "sweep_fwd_mfma": ["sweep_fwd.hip", "strip_plan.h", "common.h", "coherent.h"],
     "sweep_bwd_mfma": ["sweep_bwd.hip", "strip_plan.h", "common.h", "coherent.h"],
     "wgrad_mfma": ["sweep_bwd.hip", "strip_plan.h", "common.h", "coherent.h"],
-    "head_fused": ["fc.hip", "common.h"],
+    "sweep_fwd_step": _STEP, "sweep_bwd_step": _STEP, "wgrad_step": _STEP, "dx_step": _STEP,
+    "sweep_fwd_step_bf16": _STEP,
+    "sum_dirs": ["generic.hip", "common.h"],
+    "head_fused": ["fc.hip", "common.h"], "fc_tanh_fwd": ["fc.hip", "common.h"],
+    "fc_tanh_bwd": ["fc.hip", "common.h"], "softmax_ce": ["fc.hip", "common.h"],
 }
 
 
@@ -91,21 +104,53 @@ def source_hash(kernel):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel, mode):
-    """Bytes per launch from the committed counter profile, or None when the
-    kernel is not in it or its sources changed since."""
-    if kernel not in KERNEL_SOURCES or not os.path.exists(TRAFFIC_FILE):
+_PROFILE_LINES = None
+
+
+def profile_lines():
+    global _PROFILE_LINES
+    if _PROFILE_LINES is None:
+        _PROFILE_LINES = []
+        if os.path.isdir(PROFILES):
+            for fn in sorted(os.listdir(PROFILES)):
+                if not fn.endswith(".md"):
+                    continue
+                for line in open(os.path.join(PROFILES, fn)):
+                    if line.startswith(("traffic ", "mfma ")):
+                        kind, rest = line.split(None, 1)
+                        _PROFILE_LINES.append(
+                            (kind, dict(kv.split("=", 1) for kv in rest.split())))
+    return _PROFILE_LINES
+
+
+def measured(kind, kernel, workload, mode=None):
+    """The committed counter line for (kind, kernel, workload[, mode]), or
+    None when there is none or the kernel's sources changed since."""
+    if kernel not in KERNEL_SOURCES or workload is None:
         return None
-    for line in open(TRAFFIC_FILE):
-        if not line.startswith("traffic "):
-            continue
-        f = dict(kv.split("=", 1) for kv in line.split()[1:])
-        if f["kernel"] == kernel and f["mode"] == mode:
-            return int(f["bytes"]) if f["src"] == source_hash(kernel) else None
+    for k, f in profile_lines():
+        if (k == kind and f.get("kernel") == kernel and f.get("workload") == workload and
+                (mode is None or f.get("mode") == mode)):
+            return f if f.get("src") == source_hash(kernel) else None
     return None
 
 
-def roofline(phases, name, passes, V, C, O, mode="training"):
+def counter_fields(name, workload, mode, passes, launches, algorithmic_per_pass):
+    """traffic (HBM bytes per launch) and the MFMA figures of a phase from the
+    committed profiles."""
+    out = {"traffic": None, "mfma_executed_over_algorithmic": None, "mfma_busy": None}
+    t = measured("traffic", name, workload, mode)
+    if t is not None:
+        out["traffic"] = int(float(t["bytes_per_pass"]) * passes / launches)
+    m = measured("mfma", name, workload)
+    if m is not None and algorithmic_per_pass:
+        out["mfma_executed_over_algorithmic"] = round(
+            float(m["flops_per_pass"]) / algorithmic_per_pass, 4)
+        out["mfma_busy"] = round(float(m["busy"]), 4)
+    return out
+
+
+def roofline(phases, name, passes, V, C, O, mode="training", workload=None):
     ms, launches = phases[name]
     bound, amount, unit = phase_work(name, V, C, O)
     if bound is None:
@@ -116,11 +161,13 @@ def roofline(phases, name, passes, V, C, O, mode="training"):
         achieved, peak = per_launch / avg_s / 1e9, PEAK_HBM_GBS
     else:
         achieved, peak = per_launch / avg_s / 1e12, PEAK_FP32_TFLOPS
-    return {"kernel": name, "bound": bound, "achieved": round(achieved, 3), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4),
-            "traffic": measured_traffic(name, mode),
-            "launches_per_pass": launches // passes,
-            "avg_launch_ms": round(ms / launches, 4)}
+    out = {"kernel": name, "bound": bound, "achieved": round(achieved, 3), "peak": peak,
+           "unit": unit, "frac": round(achieved / peak, 4)}
+    out.update(counter_fields(name, workload, mode, passes, launches,
+                              amount if bound == "mfma" else None))
+    out.update({"launches_per_pass": launches // passes,
+                "avg_launch_ms": round(ms / launches, 4)})
+    return out
 
 
 def layer_path(C, O, dtype, K=3):
@@ -142,7 +189,7 @@ def dx_in_reverse(li, C, O, path):
     return li > 0 and path == "step" and O <= 32 and (C + 15) // 16 * 16 <= 32
 
 
-def network_roofline(phases, passes, V, shapes, dtype, K=3):
+def network_roofline(phases, passes, V, shapes, dtype, K=3, workload=None, mode=None):
     """Roofline of the slowest phase of a multi-layer pass: its algorithmic
     work summed over the layers that ran it (the reverse step's includes
     dL/dx where it computes it)."""
@@ -153,17 +200,21 @@ def network_roofline(phases, passes, V, shapes, dtype, K=3):
     for li, (C, O) in enumerate(shapes):
         path = layer_path(C, O, dtype, K)
         fused = dx_in_reverse(li, C, O, path)
-        if name.endswith("_" + path) or (name.startswith("dx") and li > 0 and not fused):
+        if name.startswith("dx"):
+            if li > 0 and not fused:
+                flops += phase_work(name, V, C, O, K)[1]
+        elif name.endswith("_" + path):
             flops += phase_work(name, V, C, O, K)[1]
         if name == "sweep_bwd_step" and fused:
             flops += phase_work("dx", V, C, O, K)[1]
     achieved = flops * passes / (ms / 1e3) / 1e12
     peak = PEAK_BF16_TFLOPS if name.endswith("_bf16") else PEAK_FP32_TFLOPS
-    return {"kernel": name, "bound": "mfma", "achieved": round(achieved, 3),
-            "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None,
-            "launches_per_pass": launches // passes,
-            "avg_launch_ms": round(ms / launches, 4)}
+    out = {"kernel": name, "bound": "mfma", "achieved": round(achieved, 3),
+           "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
+    out.update(counter_fields(name, workload, mode, passes, launches, flops))
+    out.update({"launches_per_pass": launches // passes,
+                "avg_launch_ms": round(ms / launches, 4)})
+    return out
 
 
 def timed(step, args):
@@ -261,7 +312,9 @@ def network_summary(args, cfg):
         "unit": UNIT, "dtype": wl.dtype,
         "tflops": None if train else round(wl.flops_per_pass() / t / 1e12, 3),
         "roofline": network_roofline(phases, args.steps, wl.voxels, wl.layer_shapes(),
-                                     wl.dtype, wl.K),
+                                     wl.dtype, wl.K, workload=None if cfg is None else
+                                     "cfg%d" % cfg,
+                                     mode="training" if train else "inference"),
         "phases_ms_per_step": phases_per_step(phases, args.steps),
     }
 
@@ -285,9 +338,8 @@ def layer_forward_summary(args, cfg):
     V = N * D * H * W
     flops = 6 * V * 2 * 9 * 4 * O * (C + O)
     name = next(k for k in phases if k.startswith("sweep_fwd"))
-    roof = roofline(phases, name, args.steps, V, C, O, mode="inference")
-    if cfg != 2:
-        roof["traffic"] = None     # the committed counters cover the MR volume only
+    roof = roofline(phases, name, args.steps, V, C, O, mode="inference",
+                    workload="cfg%d" % cfg)
     del x, Ld, ws
     torch.cuda.empty_cache()
     return {"config": {"workload": wl.name, "N": N, "D": D, "H": H, "W": W, "C": C, "O": O},
@@ -372,7 +424,7 @@ def bench_all(args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic", "config": conf5,
         "roofline": network_roofline(phases5, args.steps, wl5.voxels, wl5.layer_shapes(),
-                                     wl5.dtype, wl5.K),
+                                     wl5.dtype, wl5.K, workload="cfg5", mode="training"),
         "phases_ms_per_step": phases_per_step(phases5, args.steps),
     }
     out["fwd"] = layer_forward_summary(args, 2)
@@ -516,7 +568,11 @@ def bench_mr_layer(args):
                                "3x3, 6 directions) + FC tanh 32 + softmax-CE head, fwd+bwd",
                    "N": N, "D": D, "H": H, "W": W, "C": C, "O": O, "classes": 4},
         "fwd": layer_forward_summary(args, 2),
-        "roofline": roofline(phases, dom, args.steps, V, C, O),
+        # the first layer of the 2-layer step is this layer (same kernels and
+        # shapes): its counter figures apply
+        "roofline": roofline(phases, dom, args.steps, V, C, O,
+                             workload="cfg5" if dom in ("sweep_fwd_mfma", "sweep_bwd_mfma",
+                                                        "wgrad_mfma") else None),
         "phases_ms_per_step": phases_per_step(phases, args.steps),
     }
     if not args.no_cpu_baseline:

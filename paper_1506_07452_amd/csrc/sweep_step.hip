@@ -1934,6 +1934,28 @@ k_step_bwd_blk(BwdStepArgs a)
             for (int c = 0; c < CT; ++c) axc[c] = axn[c];
         }
     }
+    // the epilogue's operands of tile `wave`, in flight during the exchange
+    // of partial sums below
+    f4 e_g[U][4], e_c[U], e_cp[U], e_gn[U], e_dh[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) e_g[u][k] = zero;
+        e_c[u] = e_cp[u] = e_gn[u] = e_dh[u] = zero;
+    }
+    if (do_h && elive) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int uo = u * 16 + 4 * q4;
+            const float *gp = a.gates + vo * G + uo;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) e_g[u][k] = *(const f4 *)(gp + k * O);
+            e_c[u] = *(const f4 *)(a.cell + vo * O + uo);
+            if (t > 0) e_cp[u] = *(const f4 *)(a.cell + (vo - noff) * O + uo);
+            if (has_next) e_gn[u] = *(const f4 *)(a.gcf + (vo + noff) * O + uo);
+            e_dh[u] = *(const f4 *)(a.dh + ((long long)n * V + evox) * O + uo);
+        }
+    }
     // partial sums of the tiles other waves finish, into this wave's own
     // region (only this wave read it): slot nt - (nt > wave) of each M-tile
 #pragma unroll
@@ -1992,14 +2014,9 @@ k_step_bwd_blk(BwdStepArgs a)
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int uo = u * 16 + 4 * q4;
-        const float *gp = a.gates + vo * G + uo;
-        const f4 gi = *(const f4 *)gp, gf = *(const f4 *)(gp + O);
-        const f4 gg = *(const f4 *)(gp + 2 * O), go = *(const f4 *)(gp + 3 * O);
-        const f4 c = *(const f4 *)(a.cell + vo * O + uo);
-        f4 cp = zero, gn = zero;
-        if (t > 0) cp = *(const f4 *)(a.cell + (vo - noff) * O + uo);
-        if (has_next) gn = *(const f4 *)(a.gcf + (vo + noff) * O + uo);
-        f4 ghv = partial(u, own_h[u]) + *(const f4 *)(a.dh + ((long long)n * V + evox) * O + uo);
+        const f4 gi = e_g[u][0], gf = e_g[u][1], gg = e_g[u][2], go = e_g[u][3];
+        const f4 c = e_c[u], cp = e_cp[u], gn = e_gn[u];
+        f4 ghv = partial(u, own_h[u]) + e_dh[u];
         f4 di, df, dgv, dov, gco;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {

@@ -593,7 +593,11 @@ k_step_fwd_bls(FwdStepArgs a)
     const int swm = (nch & 7) == 0 ? 7 : 3;
     const int lbq = 31 - __builtin_clz(BQ);
 
-    // the tiles this wave finishes and their c_{t-1}, in flight meanwhile
+    // the bias of this lane's units, and the tiles this wave finishes and
+    // their c_{t-1}, in flight meanwhile
+    f4 biasv[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) biasv[g] = *(const f4 *)(a.bias + d * G + g * O + uo);
     int evox[NF];
     bool elive[NF];
     f4 cprev[NF];
@@ -717,7 +721,7 @@ k_step_fwd_bls(FwdStepArgs a)
                     v += stf[(((ug + U * k) * 4 + g) * NU + slot(nt, k)) * 64 + lane];
                 }
             }
-            pre[g] = v + *(const f4 *)(a.bias + d * G + g * O + uo);
+            pre[g] = v + biasv[g];
         }
         const long long vo = sbase + evox[j];
         f4 gi, gf, gg, go, c, h;

@@ -612,26 +612,33 @@ k_step_fwd_bls(FwdStepArgs a)
     }
 
     // stage x_t and h_{t-1} of the block and its halo (zero off the plane,
-    // and h at t = 0)
+    // and h at t = 0) with direct-to-LDS loads, all in flight at once: one
+    // instruction fills 64 consecutive 16-byte slots, slot p of pixel spx
+    // holding chunk p ^ (spx & swm), each lane loading the chunk its slot
+    // holds; x and h chunks go out as two instructions masked by source.
     {
-        const int nst_x = SH * SW * nxc;
-        for (int e = threadIdx.x; e < nst_x; e += 64 * kSW) {
-            const int spx = e / nxc, c = e - spx * nxc;
+        const int nslot = SH * SW * nch;
+        for (int e0 = wave * 64; e0 < nslot; e0 += 64 * kSW) {
+            const int e = e0 + lane;
+            const int spx = e / nch, pos = e - spx * nch;
+            const int c = pos ^ (spx & swm);
             const int sy = spx / SW, sx = spx - sy * SW;
             const int pp = p0 - radp + sy, qq = q0 - radq + sx;
+            const bool on = e < nslot && on_plane(pp, qq, P, Q);
             const int v = s * ss + pp * sp + qq * sq;
-            stf[spx * nch + (c ^ (spx & swm))] =
-                bload4(rs_x, sel_off(on_plane(pp, qq, P, Q), (unsigned)(v * Cp + 4 * c) * 4u));
+            lds_void *dst = (lds_void *)&stf[e0];
+            if (e < nslot) {
+                if (c < nxc)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        rs_x, dst, 16, (int)sel_off(on, (unsigned)(v * Cp + 4 * c) * 4u), 0, 0, 0);
+                else
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        rs_h, dst, 16,
+                        (int)sel_off(on && t > 0, (unsigned)((v + hoff) * O + 4 * (c - nxc)) * 4u),
+                        0, 0, 0);
+            }
         }
-        const int nhc = U * 4, nst_h = SH * SW * nhc;
-        for (int e = threadIdx.x; e < nst_h; e += 64 * kSW) {
-            const int spx = e / nhc, c = e - spx * nhc;
-            const int sy = spx / SW, sx = spx - sy * SW;
-            const int pp = p0 - radp + sy, qq = q0 - radq + sx;
-            const int v = s * ss + pp * sp + qq * sq + hoff;
-            stf[spx * nch + ((nxc + c) ^ (spx & swm))] =
-                bload4(rs_h, sel_off(t > 0 && on_plane(pp, qq, P, Q), (unsigned)(v * O + 4 * c) * 4u));
-        }
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     }
     __syncthreads();
 

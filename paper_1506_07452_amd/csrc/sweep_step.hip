@@ -1879,18 +1879,28 @@ k_step_bwd_blk(BwdStepArgs a)
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) accx[c][nt] = zero;
     if (has_next) {
+        // direct-to-LDS loads, all in flight at once: one instruction fills
+        // 64 consecutive 16-byte slots, slot p of pixel spx holding chunk
+        // p ^ (spx & SWM), each lane loading the chunk its slot holds
         const auto rs_dA = slice_rsrc(a.dA + sbase * G, V * G);
         const int nst = SH * SW * NCH;
-        for (int e = lane; e < nst; e += 64) {
-            const int spx = e / NCH, c = e - spx * NCH;
+        for (int e0 = 0; e0 < nst; e0 += 64) {
+            const int e = e0 + lane;
+            const int spx = e / NCH, pos = e - spx * NCH;
+            const int c = pos ^ (spx & SWM);
             const int sy = spx / SW, sx = spx - sy * SW;
             const int pp = p0 - radp + sy, qq = q0 - radq + sx;
             const int mb = wave + kSW * (c >> 2);
             const int v = (s + dg.sign) * ss + pp * sp + qq * sq;
-            mine[spx * NCH + (c ^ (spx & SWM))] =
-                bload4(rs_dA, sel_off(on_plane(pp, qq, P, Q),
-                                      (unsigned)(v * G + mb * 16 + 4 * (c & 3)) * 4u));
+            lds_void *dst = (lds_void *)&mine[e0];
+            if (e < nst)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs_dA, dst, 16,
+                    (int)sel_off(on_plane(pp, qq, P, Q),
+                                 (unsigned)(v * G + mb * 16 + 4 * (c & 3)) * 4u),
+                    0, 0, 0);
         }
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     }
     __syncthreads();
     if (has_next) {

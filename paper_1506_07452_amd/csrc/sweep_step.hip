@@ -1229,19 +1229,31 @@ k_step_fwd_b16_blk(FwdB16Args a)
     const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
 
     // ---- stage [x_t | h_{t-1}] of the block and its halo (zero off the plane)
+    // with direct-to-LDS loads, all in flight at once: one instruction fills
+    // 64 consecutive 16-byte slots, slot p of pixel spx holding chunk
+    // p ^ (spx & swm), each lane loading the chunk its slot holds; x and h
+    // chunks go out as two instructions masked by source
     const int nst = SH * SW * NCH;
-    for (int e = threadIdx.x; e < nst; e += 64 * U) {
-        const int spx = e / NCH, c = e - spx * NCH;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    for (int e0 = wv * 64; e0 < nst; e0 += 64 * U) {
+        const int e = e0 + (threadIdx.x & 63);
+        const int spx = e / NCH, pos = e - spx * NCH;
+        const int c = pos ^ (spx & swm);
         const int sy = spx / SW, sx = spx - sy * SW;
         const int pp = p0 - radp + sy, qq = q0 - radq + sx;
         const bool on = on_plane(pp, qq, P, Q);
         const int v = s * ss + pp * sp + qq * sq;
-        bf8 val;
-        if (c < NXC)
-            val = bload8h(rs_x, sel_off(on, (unsigned)(v * C32 + 8 * c) * 2u));
-        else
-            val = bload8h(rs_h, sel_off(on && t > 0, (unsigned)((v + hoff) * O + 8 * (c - NXC)) * 2u));
-        stg[spx * NCH + (c ^ (spx & swm))] = val;
+        lds_void *dst = (lds_void *)&stg[e0];
+        if (e < nst) {
+            if (c < NXC)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs_x, dst, 16, (int)sel_off(on, (unsigned)(v * C32 + 8 * c) * 2u), 0, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs_h, dst, 16,
+                    (int)sel_off(on && t > 0, (unsigned)((v + hoff) * O + 8 * (c - NXC)) * 2u),
+                    0, 0, 0);
+        }
     }
 
     // this lane's pixel of each tile (block row-major; BQ is a power of two)
@@ -1260,6 +1272,7 @@ k_step_fwd_b16_blk(FwdB16Args a)
         cprev[nt] = bload4(rs_c, sel_off(t > 0 && elive[nt],
                                          (unsigned)((evox[nt] + hoff) * O + uo) * 4u));
     }
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
 
     f4 acc[4][kNT];

@@ -406,11 +406,14 @@ int pyramid_lstm_set_step_split(int mode);
 
 /* Contraction type of bf16-storage layers with 32 or 64 hidden units, for
  * testing and tuning (process-wide): 1 = bf16 MFMA with fp32 accumulation
- * (default; h_{t-1} enters the recurrent contraction rounded to bf16), the
- * pixel blocks of a step staged in LDS once for all filter taps; 2 = the
- * same contraction with its operands read from L1 per tap; 0 = fp32 MFMA on
- * the widened values.  Results of 1 and 2 differ only in summation order.
- * Returns PLSTM_EINVAL for other values. */
+ * (default; h_{t-1} enters the recurrent contraction rounded to bf16) on
+ * 256-pixel blocks, the block staged in LDS once for all filter taps and the
+ * weights streamed through LDS for all of a workgroup's waves (3 where its
+ * LDS does not fit, e.g. 64 units with 5 x 5 filters); 3 = the same
+ * contraction on 64-pixel blocks, the weights read by each wave from L1;
+ * 2 = operands read from L1 per tap; 0 = fp32 MFMA on the widened values.
+ * Results of 1, 2 and 3 differ only in summation order.  Returns
+ * PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_bf16_mfma(int on);
 
 /* Weight gradients of the plane-step backward, for testing and tuning

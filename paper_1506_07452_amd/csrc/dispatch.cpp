@@ -77,10 +77,8 @@ int forward_dispatch(const Geom &g, int dtype, const void *x, const void *wx, co
         float *hd = sv ? sv->hd : cv.take<float>(saved_state_count(g));
         float *cellbuf = sv ? sv->cell : cv.take<float>(saved_state_count(g));
         char *rest = (char *)ws + align_up(cv.off, 256);
-        const int rc = step_fwd(g, dtype, x, wx, wh, b, hd, cellbuf, sv ? sv->gates : nullptr,
-                                rest, st);
-        if (rc != PLSTM_OK) return rc;
-        return sum_dirs(g, dtype, hd, h, st);
+        return step_fwd(g, dtype, x, wx, wh, b, hd, cellbuf, sv ? sv->gates : nullptr, h, rest,
+                        st);
     }
     return generic_forward(g, dtype, x, wx, wh, b, h, sv, ws, st);
 }

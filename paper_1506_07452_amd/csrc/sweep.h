@@ -24,8 +24,11 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
 // arithmetic (bf16 storage converted on entry), one launch per plane step.
 bool step_supported(const Geom &g);
 size_t step_fwd_ws(const Geom &g);
+// Writes c^d, the gates when `gates` is set, h^d (fp32; bf16 storage on the
+// bf16 MFMA keeps h^d in bf16 in the workspace instead) and the direction sum h.
 int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
-             const void *b, float *hd, float *cell, float *gates, void *ws, hipStream_t st);
+             const void *b, float *hd, float *cell, float *gates, void *h, void *ws,
+             hipStream_t st);
 size_t step_bwd_ws(const Geom &g);
 int step_bwd(const Geom &g, const float *x, const float *wh, const float *wx, const Saved &sv,
              const float *dh, float *dx, float *dwx, float *dwh, float *db, void *ws,
@@ -53,8 +56,10 @@ int *device_status_word();
 extern int g_wait_spin_limit;
 extern int g_wait_bias;
 
-// h = sum of the six per-direction outputs (generic.hip).
+// h = sum of the six per-direction outputs (generic.hip): from fp32 h^d, or
+// (sum_dirs_bf16, bf16 h) from bf16 h^d, added in fp32 and rounded once.
 int sum_dirs(const Geom &g, int dtype, const float *hd, void *h, hipStream_t st);
+int sum_dirs_bf16(const Geom &g, const uint16_t *hb, void *h, hipStream_t st);
 
 // Workspace bytes of the forward for this shape (covers every path it may take).
 size_t forward_ws(const Geom &g, int dtype, bool training);

@@ -954,9 +954,9 @@ k_line_fwd(LineFwdArgs a)
 
 // ---- forward step on the bf16 MFMA (bf16 storage, O = 32 or 64) --------------
 // For bf16 storage the contraction runs on v_mfma_f32_16x16x32_bf16 with fp32
-// accumulation: x and the weights are bf16 values already, and h_{t-1}
-// enters as bf16 (h^d is also kept in fp32 for the direction sum; c stays
-// fp32).  Lane l supplies A[m = l%16][k = 8(l/16) + j] and B[k][n = l%16],
+// accumulation: x and the weights are bf16 values already, and h^d is kept
+// in bf16 only (h_{t-1} enters the recurrence as bf16, and the direction sum
+// adds the bf16 values in fp32); c stays fp32.  Lane l supplies A[m = l%16][k = 8(l/16) + j] and B[k][n = l%16],
 // j = 0..7, so lane group q takes channels 8q .. 8q+7 of a 32-channel block:
 // one 16-byte load per operand, one MFMA per block, gate, tile.
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
@@ -1024,8 +1024,9 @@ struct FwdB16Args {
     const uint16_t *xb;       // [N][V][C32] bf16
     const uint16_t *frag;     // [6][U][KG][4][64][8] bf16
     const float *bias;        // [6][4O]
-    float *hd, *cell;         // [6][N][V][O] fp32
-    uint16_t *hb;             // [6][N][V][O] bf16 copy of h^d (the recurrence's operand)
+    float *cell;              // [6][N][V][O] fp32 c^d
+    uint16_t *hb;             // [6][N][V][O] bf16 h^d (the recurrence's operand and the
+                              // direction sum's input)
     int npg[kDirs];
     int base[kDirs + 1];
     // pixel blocks of the LDS-staged kernel: BP x BQ pixels (BP BQ = 64), nbq
@@ -1176,7 +1177,6 @@ k_step_fwd_b16(FwdB16Args a)
             hbv[i] = f32_to_bf16(h[i]);
         }
         *(f4 *)(a.cell + vo * O + uo) = c;
-        *(f4 *)(a.hd + vo * O + uo) = h;
         *(us4 *)(a.hb + vo * O + uo) = hbv;
     }
 }
@@ -1329,8 +1329,246 @@ k_step_fwd_b16_blk(FwdB16Args a)
             hbv[i] = f32_to_bf16(h[i]);
         }
         *(f4 *)(a.cell + vo * O + uo) = c;
-        *(f4 *)(a.hd + vo * O + uo) = h;
         *(us4 *)(a.hb + vo * O + uo) = hbv;
+    }
+}
+
+// Macro-tiled variant (the default where its LDS fits): a workgroup of
+// NW = (U / 2) WN waves takes a (4 WN) x 16 block of pixels of one plane and
+// all 4O gate rows.  Wave (wm, wn) computes unit groups 2 wm and 2 wm + 1
+// (eight 16-row gate tiles) for block rows 4 wn .. 4 wn + 3 (four 16-pixel
+// tiles, one block row each), so every A fragment read from LDS feeds four
+// MFMAs and every B fragment eight.
+// - [x_t | h_{t-1}] of the block and its filter halo is staged once, with
+//   direct-to-LDS loads as in k_step_fwd_b16_blk; the staged pixel is padded
+//   to NCH + 2 chunks (a stride of 8 mod 16 floats), so the 16 lanes that
+//   read one chunk of 16 consecutive pixels hit distinct banks.
+// - The A fragments of a K-group (4O gate rows x 32 channels, 1 KB per
+//   16-row tile) stream through a ring of three LDS arrays, also with
+//   direct-to-LDS loads issued two K-groups ahead.  Step kg reads K-group
+//   kg + 1 into registers and refills the array that held kg with kg + 3;
+//   its barrier publishes kg + 2 (each wave has waited for its own share)
+//   and frees the array of kg + 1 for step kg + 2 (each wave has waited for
+//   its reads).  The arrays are distinct objects and each step names its
+//   two statically (the loop is unrolled by six), so the compiler knows that
+//   the reads do not touch the array a load is still filling.
+// - The reads of K-group kg + 1 are interleaved with kg's MFMAs (one A and
+//   at most one B fragment per four MFMAs), so neither waits on the other.
+// Workgroups are remapped so that each XCD runs a contiguous range of blocks
+// (at most two directions' weights per L2).
+template <int U, int WN>
+__global__ void __launch_bounds__(64 * (U / 2) * WN) __attribute__((amdgpu_waves_per_eu(2)))
+k_step_fwd_b16_mt(FwdB16Args a)
+{
+    constexpr int O = 16 * U, G = 4 * O, WM = U / 2, NW = WM * WN, T = 4 * U;
+    constexpr int BP = 4 * WN, BQ = 16;
+    constexpr int NDMA = T / NW;             // ring loads per wave per K-group
+    static_assert(U == 2 || U == 4, "two unit groups per wave");
+    static_assert(T % NW == 0 && NDMA < 16, "ring tiles split evenly over the waves");
+    constexpr int kWaitRingLds = 0x0070 | NDMA;  // s_waitcnt vmcnt(NDMA) lgkmcnt(0)
+    constexpr int kWaitAllLds = 0x0070;          // s_waitcnt vmcnt(0) lgkmcnt(0)
+    __shared__ bf8 ring0[T * 64], ring1[T * 64], ring2[T * 64];
+    extern __shared__ bf8 stg[];             // [SH][SW][NCH + 2]: staged pixels
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wv % WM, wn = wv / WM;
+    const int per_xcd = gridDim.x / kXcds;
+    const int blk = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    if (blk >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, blk);
+    const DirGeom dg = a.g.dir[d];
+    int r = blk - a.base[d];
+    const int n = r / a.nblk[d];
+    r -= n * a.nblk[d];
+    const int bi = r / a.nbq[d], bj = r - bi * a.nbq[d];
+    const int p0 = bi * BP, q0 = bj * BQ;
+    const int t = a.t;
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const long long V = a.g.V;
+    const int C32 = a.C32, CX = C32 >> 5, KX = a.KX, KGA = a.KG;
+    const int hoff = -dg.sign * ss;
+    const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
+    const int SW = BQ + 2 * radq, SH = BP + 2 * radp;
+    const int NXC = C32 >> 3, NCH = NXC + (O >> 3), NCHP = NCH + 2;
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    // byte sizes: V * C32 * 2, V * O * 2 and U * KG * 4096 (< 2^31, checked on the host)
+    const auto rs_x = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(a.xb + (long long)n * V * C32), (short)0, (int)(V * C32 * 2),
+        kRsrcWord3);
+    const auto rs_h = __builtin_amdgcn_make_buffer_rsrc(a.hb + sbase * O, (short)0,
+                                                        (int)(V * O * 2), kRsrcWord3);
+    const auto rs_a = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(a.frag + (long long)d * U * KGA * 2048), (short)0,
+        U * KGA * 4096, kRsrcWord3);
+    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+
+    // A fragments of K-group kg into a ring array: tile j = 4 ug + gate
+    auto issue_a = [&](int kg, bf8 *slot) {
+#pragma unroll
+        for (int j0 = 0; j0 < T; j0 += NW) {
+            const int j = j0 + wv, ug = j >> 2, gt = j & 3;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs_a, (lds_void *)&slot[j * 64], 16,
+                (int)((unsigned)(((ug * KGA + kg) * 4 + gt) * 512 + lane * 8) * 2u), 0, 0, 0);
+        }
+    };
+
+    // ---- stage [x_t | h_{t-1}] of the block and its halo (zero off the
+    // plane, before the first plane and in the two pad chunks): one
+    // instruction fills 64 consecutive 16-byte slots, x and h chunks as two
+    // instructions masked by source
+    const int nst = SH * SW * NCHP;
+    for (int e0 = wv * 64; e0 < nst; e0 += 64 * NW) {
+        const int e = e0 + lane;
+        const int spx = e / NCHP, c = e - spx * NCHP;
+        const int sy = spx / SW, sx = spx - sy * SW;
+        const int pp = p0 - radp + sy, qq = q0 - radq + sx;
+        const bool on = on_plane(pp, qq, P, Q);
+        const int v = s * ss + pp * sp + qq * sq;
+        lds_void *dst = (lds_void *)&stg[e0];
+        if (e < nst) {
+            if (c < NXC)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs_x, dst, 16, (int)sel_off(on, (unsigned)(v * C32 + 8 * c) * 2u), 0, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs_h, dst, 16,
+                    (int)sel_off(on && t > 0 && c < NCH,
+                                 (unsigned)((v + hoff) * O + 8 * (c - NXC)) * 2u),
+                    0, 0, 0);
+        }
+    }
+    const int KG = t > 0 ? KGA : KX;
+    issue_a(0, ring0);
+    if (KG > 1) issue_a(1, ring1);
+    if (KG > 2) issue_a(2, ring2);
+
+    // staged chunk of this lane in tile nt (block row 4 wn + nt) at tap
+    // (0, 0), channel chunk q4
+    int spb[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) spb[nt] = ((4 * wn + nt + radp) * SW + col + radq) * NCHP + q4;
+    // uniform part of the B offset of K-group kg: tap shift and chunk block
+    auto b_off = [&](int kg) {
+        const bool is_x = kg < KX;
+        const int kk = is_x ? kg : kg - KX;
+        const int tap = is_x ? (kk * a.cx_mul32) >> 16 : kk / (O / 32);
+        const int cb = kk - tap * (is_x ? CX : O / 32);
+        const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
+        return (ka * SW + kb) * NCHP + (is_x ? 0 : NXC) + cb * 4;
+    };
+
+    struct Ops {
+        bf8 a[8];
+        bf8 b[kNT];
+    };
+    f4 acc[8][kNT];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[i][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    auto mfmas = [&](const Ops &o) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) acc[i][nt] = mfma_bf16(o.a[i], o.b[nt], acc[i][nt]);
+    };
+    auto step = [&](int kg, const Ops &cur, Ops &nxt, const bf8 *rd, bf8 *dm) {
+        const int bb = b_off(kg + 1);
+        const bool more = kg + 3 < KG;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) acc[i][nt] = mfma_bf16(cur.a[i], cur.b[nt], acc[i][nt]);
+            if (i == 0 && more) issue_a(kg + 3, dm);
+            nxt.a[i] = rd[(8 * wm + i) * 64 + lane];
+            if (i < kNT) nxt.b[i] = stg[spb[i] + bb];
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // the reads done, this wave's share of kg + 2 landed (kg + 3 may stay
+        // in flight), then the barrier; no fence: one would also wait for
+        // kg + 3.  The empty asm keeps the compiler from moving LDS accesses
+        // across the barrier.
+        if (more)
+            __builtin_amdgcn_s_waitcnt(kWaitRingLds);
+        else
+            __builtin_amdgcn_s_waitcnt(kWaitAllLds);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+    Ops X, Y;
+    {
+        const int bb = b_off(0);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) X.a[i] = ring0[(8 * wm + i) * 64 + lane];
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) X.b[nt] = stg[spb[nt] + bb];
+    }
+    // step 0 refills ring0: every wave has read K-group 0 from it first
+    __syncthreads();
+    // after step kg the operands of kg + 1 are in Y for even kg, X for odd
+    for (int kg = 0; kg + 1 < KG; kg += 6) {
+        step(kg, X, Y, ring1, ring0);
+        if (kg + 2 < KG) step(kg + 1, Y, X, ring2, ring1);
+        if (kg + 3 < KG) step(kg + 2, X, Y, ring0, ring2);
+        if (kg + 4 < KG) step(kg + 3, Y, X, ring1, ring0);
+        if (kg + 5 < KG) step(kg + 4, X, Y, ring2, ring1);
+        if (kg + 6 < KG) step(kg + 5, Y, X, ring0, ring2);
+    }
+    if ((KG - 1) & 1) X = Y;
+
+    // epilogue operands, in flight during the last K-group's MFMAs
+    const int ug0 = 2 * wm;
+    f4 bias[2][4], cprev[2][kNT];
+    int evox[kNT];
+    bool elive[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const int pp = p0 + 4 * wn + nt, qq = q0 + col;
+        elive[nt] = on_plane(pp, qq, P, Q);
+        evox[nt] = s * ss + (elive[nt] ? pp * sp + qq * sq : 0);
+    }
+#pragma unroll
+    for (int ui = 0; ui < 2; ++ui) {
+        const int uo = (ug0 + ui) * 16 + 4 * q4;
+#pragma unroll
+        for (int gt = 0; gt < 4; ++gt) bias[ui][gt] = *(const f4 *)(a.bias + d * G + gt * O + uo);
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt)
+            cprev[ui][nt] = bload4(rs_c, sel_off(t > 0 && elive[nt],
+                                                 (unsigned)((evox[nt] + hoff) * O + uo) * 4u));
+    }
+    mfmas(X);
+
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        if (!elive[nt]) continue;
+        const long long vo = sbase + evox[nt];
+#pragma unroll
+        for (int ui = 0; ui < 2; ++ui) {
+            const int uo = (ug0 + ui) * 16 + 4 * q4;
+            f4 pre[4];
+#pragma unroll
+            for (int gt = 0; gt < 4; ++gt) pre[gt] = acc[ui * 4 + gt][nt] + bias[ui][gt];
+            f4 c, h;
+            us4 hbv;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float gi = fsig(pre[0][i]), gf = fsig(pre[1][i]);
+                const float gg = ftanh(pre[2][i]), go = fsig(pre[3][i]);
+                c[i] = gg * gi + cprev[ui][nt][i] * gf;
+                h[i] = go * ftanh(c[i]);
+                hbv[i] = f32_to_bf16(h[i]);
+            }
+            *(f4 *)(a.cell + vo * O + uo) = c;
+            *(us4 *)(a.hb + vo * O + uo) = hbv;
+        }
     }
 }
 
@@ -3073,15 +3311,65 @@ size_t b16_block_lds(const Geom &g, const FwdB16Args &a)
     return m;
 }
 
+// Pixel blocks of the macro-tiled bf16 forward: (4 kMtWN) x 16 pixels, one
+// workgroup column of waves per four block rows.
+constexpr int kMtWN = 4;
+void set_mt_blocks(const Geom &g, int *bp, int *bq, int *nbq, int *nblk)
+{
+    for (int d = 0; d < kDirs; ++d) {
+        const DirGeom &dg = g.dir[d];
+        bp[d] = 4 * kMtWN;
+        bq[d] = 16;
+        nbq[d] = dg.Q > 0 ? (dg.Q + 15) / 16 : 0;
+        nblk[d] = dg.P > 0 ? (dg.P + bp[d] - 1) / bp[d] * nbq[d] : 0;
+    }
+}
+
+// Dynamic LDS bytes of the macro-tiled kernel: the staged block with its
+// halo, NCH + 2 chunks per pixel.  Its A ring (three arrays of 4U tiles of
+// 1 KB) is static.
+size_t b16_mt_stage_lds(const Geom &g, const FwdB16Args &a)
+{
+    const int nchp = (a.C32 + g.O) / 8 + 2;
+    return (size_t)(4 * kMtWN + 2 * (g.KP / 2)) * (16 + 2 * (g.KQ / 2)) * nchp * 16;
+}
+
 template <int U>
 int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
 {
     const int T = max_T(g);
     const int few = split_threshold();
-    const size_t lds = b16_block_lds(g, a);
-    const bool staged = g_step_bf16_mfma == 1 && lds <= 64 * 1024;
+    const size_t lds_mt = b16_mt_stage_lds(g, a);
+    const bool mt = g_step_bf16_mfma == 1 &&
+                    (size_t)3 * 4 * U * 1024 + lds_mt <= (size_t)device_info().max_lds;
+    size_t lds = 0;
+    bool staged = false;
+    if (mt) {
+        set_mt_blocks(g, a.bp, a.bq, a.nbq, a.nblk);
+        if (hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, kMtWN>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds_mt) != hipSuccess)
+            return PLSTM_EHIP;
+    } else {
+        set_blocks(g, a.bp, a.bq, a.nbq, a.nblk);
+        lds = b16_block_lds(g, a);
+        staged = (g_step_bf16_mfma == 1 || g_step_bf16_mfma == 3) && lds <= 64 * 1024;
+    }
     for (int t = 0; t < T; ++t) {
         a.t = t;
+        if (mt) {
+            int nb = 0;
+            for (int d = 0; d < kDirs; ++d) {
+                a.base[d] = nb;
+                if (t < g.dir[d].T) nb += g.N * a.nblk[d];
+            }
+            a.base[kDirs] = nb;
+            if (nb == 0) continue;
+            const int grid = (nb + kXcds - 1) / kXcds * kXcds;
+            k_step_fwd_b16_mt<U, kMtWN><<<grid, 64 * (U / 2) * kMtWN, lds_mt, st>>>(a);
+            PLSTM_LAUNCH_CHECK();
+            continue;
+        }
         int tot = 0;
         for (int d = 0; d < kDirs; ++d) {
             a.base[d] = tot;
@@ -3107,7 +3395,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
 }
 
 static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
-                        const uint16_t *wh, const uint16_t *b, float *hd, float *cell, void *ws,
+                        const uint16_t *wh, const uint16_t *b, void *h, float *cell, void *ws,
                         hipStream_t st)
 {
     const int U = g.O / 16, C32 = pad32(g.C);
@@ -3132,22 +3420,22 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     a.cx_mul32 = (65536 + C32 / 32 - 1) / (C32 / 32);
     a.k_mul = k_mul_of(g);
     a.xb = xb; a.frag = frag; a.bias = bias;
-    a.hd = hd; a.cell = cell; a.hb = hb;
+    a.cell = cell; a.hb = hb;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
-    set_blocks(g, a.bp, a.bq, a.nbq, a.nblk);
     const int rc = U == 2 ? launch_fwd_b16_steps<2>(g, a, st) : launch_fwd_b16_steps<4>(g, a, st);
     if (rc != PLSTM_OK) return rc;
     timing_end(2 + max_T(g), st);
-    return PLSTM_OK;
+    return sum_dirs_bf16(g, hb, h, st);
 }
 
 int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void *wh,
-             const void *b, float *hd, float *cell, float *gates, void *ws, hipStream_t st)
+             const void *b, float *hd, float *cell, float *gates, void *h, void *ws,
+             hipStream_t st)
 {
     if (!step_supported(g)) return PLSTM_EUNSUPPORTED;
     if (use_b16(g, dtype) && !gates)
         return step_fwd_b16(g, (const uint16_t *)x, (const uint16_t *)wx, (const uint16_t *)wh,
-                            (const uint16_t *)b, hd, cell, ws, st);
+                            (const uint16_t *)b, h, cell, ws, st);
     const int U = g.O / 16, Cp = pad16(g.C);
     const int KK = g.KP * g.KQ, KX = KK * Cp / 16, KG = KX + KK * U;
     Carve cv(ws);
@@ -3216,7 +3504,7 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
             ++launches;
         }
         timing_end((x_direct ? 1 : 2) + launches, st);
-        return PLSTM_OK;
+        return sum_dirs(g, dtype, hd, h, st);
     }
     // fp32 x whose channel count is already a multiple of 16 is read in place
     const bool x_in_place = dtype == PLSTM_F32 && Cp == g.C;
@@ -3251,7 +3539,7 @@ int step_fwd(const Geom &g, int dtype, const void *x, const void *wx, const void
     }
     if (rc != PLSTM_OK) return rc;
     timing_end((x_in_place ? 1 : 2) + max_T(g), st);
-    return PLSTM_OK;
+    return sum_dirs(g, dtype, hd, h, st);
 }
 
 // The 2D layer with 16 units and at most 4 input channels takes dL/dx from
@@ -3517,7 +3805,7 @@ extern "C" int pyramid_lstm_set_step_split(int mode)
 
 extern "C" int pyramid_lstm_set_bf16_mfma(int on)
 {
-    if (on < 0 || on > 2) return PLSTM_EINVAL;
+    if (on < 0 || on > 3) return PLSTM_EINVAL;
     plstm::g_step_bf16_mfma = on;
     return PLSTM_OK;
 }

@@ -324,10 +324,20 @@ def test_filter_size_generic_path(case):
         assert normwise(host(got), ref[name]) <= TOL["f32"], name
 
 
-@pytest.mark.parametrize("bf16_mfma", [1, 2, 0], ids=["bf16_lds", "bf16_l1", "fp32_mfma"])
-def test_filter_size_bf16(bf16_mfma):
-    shape, K = (1, 4, 11, 9, 25, 32), 7
-    inst = instance_k(shape, K, 7200, "bf16")
+# bf16 K x K cases: 32 units with 7 x 7; 64 units with 5 x 5 at 20 input
+# channels (the 256-pixel kernel) and at 40 (its LDS does not fit: the
+# default falls back to 64-pixel blocks)
+BF16_K_CASES = [((1, 4, 11, 9, 25, 32), 7), ((2, 3, 19, 35, 20, 64), 5),
+                ((1, 3, 21, 18, 40, 64), 5)]
+
+
+@pytest.mark.parametrize("case", BF16_K_CASES,
+                         ids=lambda c: "x".join(map(str, c[0])) + "_k%d" % c[1])
+@pytest.mark.parametrize("bf16_mfma", [1, 3, 2, 0],
+                         ids=["bf16_mt", "bf16_lds", "bf16_l1", "fp32_mfma"])
+def test_filter_size_bf16(bf16_mfma, case):
+    shape, K = case
+    inst = instance_k(shape, K, 7200 + sum(shape), "bf16")
     L = inst.layers[0]
     ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
     say("filter size bf16", shape, K, bf16_mfma)
@@ -431,7 +441,8 @@ def test_forward_bf16_matches_oracle(shape):
     assert err <= TOL["bf16"], err
 
 
-@pytest.mark.parametrize("bf16_mfma", [1, 2, 0], ids=["bf16_lds", "bf16_l1", "fp32_mfma"])
+@pytest.mark.parametrize("bf16_mfma", [1, 3, 2, 0],
+                         ids=["bf16_mt", "bf16_lds", "bf16_l1", "fp32_mfma"])
 @pytest.mark.parametrize("shape", [(1, 4, 6, 70, 3, 64), (2, 9, 17, 40, 32, 32),
                                    (1, 5, 23, 9, 40, 32), (2, 3, 7, 66, 64, 64)],
                          ids=lambda s: "x".join(map(str, s)))

@@ -1334,11 +1334,11 @@ k_step_fwd_b16_blk(FwdB16Args a)
 }
 
 // Macro-tiled variant (the default where its LDS fits): a workgroup of
-// NW = (U / 2) WN waves takes a (4 WN) x 16 block of pixels of one plane and
-// all 4O gate rows.  Wave (wm, wn) computes unit groups 2 wm and 2 wm + 1
-// (eight 16-row gate tiles) for block rows 4 wn .. 4 wn + 3 (four 16-pixel
-// tiles, one block row each), so every A fragment read from LDS feeds four
-// MFMAs and every B fragment eight.
+// NW = WM WN waves takes a (4 WN) x 16 block of pixels of one plane and all
+// 4O gate rows.  Wave (wm, wn) computes the UGW = U / WM unit groups from
+// UGW wm (4 UGW 16-row gate tiles) for block rows 4 wn .. 4 wn + 3 (four
+// 16-pixel tiles, one block row each), so every A fragment read from LDS
+// feeds four MFMAs and every B fragment 4 UGW.
 // - [x_t | h_{t-1}] of the block and its filter halo is staged once, with
 //   direct-to-LDS loads as in k_step_fwd_b16_blk; the staged pixel is padded
 //   to NCH + 2 chunks (a stride of 8 mod 16 floats), so the 16 lanes that
@@ -1353,17 +1353,20 @@ k_step_fwd_b16_blk(FwdB16Args a)
 //   two statically (the loop is unrolled by six), so the compiler knows that
 //   the reads do not touch the array a load is still filling.
 // - The reads of K-group kg + 1 are interleaved with kg's MFMAs (one A and
-//   at most one B fragment per four MFMAs), so neither waits on the other.
+//   at most one B fragment per four MFMAs, the ring load mid-step), so
+//   neither waits on the other.
 // Workgroups are remapped so that each XCD runs a contiguous range of blocks
 // (at most two directions' weights per L2).
-template <int U, int WN>
-__global__ void __launch_bounds__(64 * (U / 2) * WN) __attribute__((amdgpu_waves_per_eu(2)))
+template <int U, int WM, int WN>
+__global__ void __launch_bounds__(64 * WM * WN)
+__attribute__((amdgpu_waves_per_eu(U / WM == 1 ? 3 : 2)))
 k_step_fwd_b16_mt(FwdB16Args a)
 {
-    constexpr int O = 16 * U, G = 4 * O, WM = U / 2, NW = WM * WN, T = 4 * U;
+    constexpr int O = 16 * U, G = 4 * O, NW = WM * WN, T = 4 * U;
+    constexpr int UGW = U / WM, AT = 4 * UGW;   // unit groups and A tiles per wave
     constexpr int BP = 4 * WN, BQ = 16;
     constexpr int NDMA = T / NW;             // ring loads per wave per K-group
-    static_assert(U == 2 || U == 4, "two unit groups per wave");
+    static_assert(U % WM == 0 && (UGW == 1 || UGW == 2), "one or two unit groups per wave");
     static_assert(T % NW == 0 && NDMA < 16, "ring tiles split evenly over the waves");
     constexpr int kWaitRingLds = 0x0070 | NDMA;  // s_waitcnt vmcnt(NDMA) lgkmcnt(0)
     constexpr int kWaitAllLds = 0x0070;          // s_waitcnt vmcnt(0) lgkmcnt(0)
@@ -1461,17 +1464,17 @@ k_step_fwd_b16_mt(FwdB16Args a)
     };
 
     struct Ops {
-        bf8 a[8];
+        bf8 a[AT];
         bf8 b[kNT];
     };
-    f4 acc[8][kNT];
+    f4 acc[AT][kNT];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < AT; ++i)
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) acc[i][nt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
     auto mfmas = [&](const Ops &o) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < AT; ++i)
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt) acc[i][nt] = mfma_bf16(o.a[i], o.b[nt], acc[i][nt]);
     };
@@ -1479,12 +1482,16 @@ k_step_fwd_b16_mt(FwdB16Args a)
         const int bb = b_off(kg + 1);
         const bool more = kg + 3 < KG;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < AT; ++i) {
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt) acc[i][nt] = mfma_bf16(cur.a[i], cur.b[nt], acc[i][nt]);
-            if (i == 0 && more) issue_a(kg + 3, dm);
-            nxt.a[i] = rd[(8 * wm + i) * 64 + lane];
-            if (i < kNT) nxt.b[i] = stg[spb[i] + bb];
+            if (i == AT / 2 && more) issue_a(kg + 3, dm);
+            nxt.a[i] = rd[(AT * wm + i) * 64 + lane];
+            if (AT == 2 * kNT) {
+                if (i & 1) nxt.b[i >> 1] = stg[spb[i >> 1] + bb];
+            } else if (i < kNT) {
+                nxt.b[i] = stg[spb[i] + bb];
+            }
             __builtin_amdgcn_sched_barrier(0);
         }
         // the reads done, this wave's share of kg + 2 landed (kg + 3 may stay
@@ -1506,7 +1513,7 @@ k_step_fwd_b16_mt(FwdB16Args a)
     {
         const int bb = b_off(0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) X.a[i] = ring0[(8 * wm + i) * 64 + lane];
+        for (int i = 0; i < AT; ++i) X.a[i] = ring0[(AT * wm + i) * 64 + lane];
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) X.b[nt] = stg[spb[nt] + bb];
     }
@@ -1524,8 +1531,8 @@ k_step_fwd_b16_mt(FwdB16Args a)
     if ((KG - 1) & 1) X = Y;
 
     // epilogue operands, in flight during the last K-group's MFMAs
-    const int ug0 = 2 * wm;
-    f4 bias[2][4], cprev[2][kNT];
+    const int ug0 = UGW * wm;
+    f4 bias[UGW][4], cprev[UGW][kNT];
     int evox[kNT];
     bool elive[kNT];
 #pragma unroll
@@ -1535,7 +1542,7 @@ k_step_fwd_b16_mt(FwdB16Args a)
         evox[nt] = s * ss + (elive[nt] ? pp * sp + qq * sq : 0);
     }
 #pragma unroll
-    for (int ui = 0; ui < 2; ++ui) {
+    for (int ui = 0; ui < UGW; ++ui) {
         const int uo = (ug0 + ui) * 16 + 4 * q4;
 #pragma unroll
         for (int gt = 0; gt < 4; ++gt) bias[ui][gt] = *(const f4 *)(a.bias + d * G + gt * O + uo);
@@ -1551,7 +1558,7 @@ k_step_fwd_b16_mt(FwdB16Args a)
         if (!elive[nt]) continue;
         const long long vo = sbase + evox[nt];
 #pragma unroll
-        for (int ui = 0; ui < 2; ++ui) {
+        for (int ui = 0; ui < UGW; ++ui) {
             const int uo = (ug0 + ui) * 16 + 4 * q4;
             f4 pre[4];
 #pragma unroll
@@ -3311,14 +3318,18 @@ size_t b16_block_lds(const Geom &g, const FwdB16Args &a)
     return m;
 }
 
-// Pixel blocks of the macro-tiled bf16 forward: (4 kMtWN) x 16 pixels, one
-// workgroup column of waves per four block rows.
-constexpr int kMtWN = 4;
-void set_mt_blocks(const Geom &g, int *bp, int *bq, int *nbq, int *nblk)
+// Wave layout of the macro-tiled bf16 forward: WM x WN waves, pixel blocks
+// of (4 WN) x 16.  64 units: 2 x 4 waves, one workgroup of 256 pixels per
+// CU; 32 units: 2 x 2 waves of one unit group each, three workgroups of 128
+// pixels per CU.
+template <int U> struct MtShape;
+template <> struct MtShape<4> { static constexpr int WM = 2, WN = 4; };
+template <> struct MtShape<2> { static constexpr int WM = 2, WN = 2; };
+void set_mt_blocks(const Geom &g, int wn, int *bp, int *bq, int *nbq, int *nblk)
 {
     for (int d = 0; d < kDirs; ++d) {
         const DirGeom &dg = g.dir[d];
-        bp[d] = 4 * kMtWN;
+        bp[d] = 4 * wn;
         bq[d] = 16;
         nbq[d] = dg.Q > 0 ? (dg.Q + 15) / 16 : 0;
         nblk[d] = dg.P > 0 ? (dg.P + bp[d] - 1) / bp[d] * nbq[d] : 0;
@@ -3328,10 +3339,10 @@ void set_mt_blocks(const Geom &g, int *bp, int *bq, int *nbq, int *nblk)
 // Dynamic LDS bytes of the macro-tiled kernel: the staged block with its
 // halo, NCH + 2 chunks per pixel.  Its A ring (three arrays of 4U tiles of
 // 1 KB) is static.
-size_t b16_mt_stage_lds(const Geom &g, const FwdB16Args &a)
+size_t b16_mt_stage_lds(const Geom &g, const FwdB16Args &a, int wn)
 {
     const int nchp = (a.C32 + g.O) / 8 + 2;
-    return (size_t)(4 * kMtWN + 2 * (g.KP / 2)) * (16 + 2 * (g.KQ / 2)) * nchp * 16;
+    return (size_t)(4 * wn + 2 * (g.KP / 2)) * (16 + 2 * (g.KQ / 2)) * nchp * 16;
 }
 
 template <int U>
@@ -3339,14 +3350,15 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
 {
     const int T = max_T(g);
     const int few = split_threshold();
-    const size_t lds_mt = b16_mt_stage_lds(g, a);
+    constexpr int WM = MtShape<U>::WM, WN = MtShape<U>::WN;
+    const size_t lds_mt = b16_mt_stage_lds(g, a, WN);
     const bool mt = g_step_bf16_mfma == 1 &&
                     (size_t)3 * 4 * U * 1024 + lds_mt <= (size_t)device_info().max_lds;
     size_t lds = 0;
     bool staged = false;
     if (mt) {
-        set_mt_blocks(g, a.bp, a.bq, a.nbq, a.nblk);
-        if (hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, kMtWN>,
+        set_mt_blocks(g, WN, a.bp, a.bq, a.nbq, a.nblk);
+        if (hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, WM, WN>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds_mt) != hipSuccess)
             return PLSTM_EHIP;
@@ -3366,7 +3378,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
             a.base[kDirs] = nb;
             if (nb == 0) continue;
             const int grid = (nb + kXcds - 1) / kXcds * kXcds;
-            k_step_fwd_b16_mt<U, kMtWN><<<grid, 64 * (U / 2) * kMtWN, lds_mt, st>>>(a);
+            k_step_fwd_b16_mt<U, WM, WN><<<grid, 64 * WM * WN, lds_mt, st>>>(a);
             PLSTM_LAUNCH_CHECK();
             continue;
         }

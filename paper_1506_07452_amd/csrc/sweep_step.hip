@@ -2819,13 +2819,21 @@ k_wgrad_lds(WlArgs a)
         fetch(st, 0, total);
         put(st, buf0);
         __syncthreads();
+        // the first wave of each SIMD (waves 0-3) issues the next pair's
+        // loads before its products, the second one (waves 4-7) after them,
+        // so that one wave's address arithmetic runs beside the other's MFMAs
+        const bool early = wave < kWlWaves / 2;
         for (long long u = 0; u < total; u += 2) {
             const bool more = u + 2 < total;
-            if (more) {
+            if (more && early) {
                 advance();
                 fetch(st, u + 2, total);
             }
             compute_pair((u >> 1) & 1 ? buf1 : buf0, u + 1 < total);
+            if (more && !early) {
+                advance();
+                fetch(st, u + 2, total);
+            }
             if (more) put(st, (u >> 1) & 1 ? buf0 : buf1);
             __syncthreads();
         }

@@ -326,9 +326,11 @@ def test_filter_size_generic_path(case):
 
 # bf16 K x K cases: 32 units with 7 x 7; 64 units with 5 x 5 at 20 input
 # channels (the 256-pixel kernel) and at 40 (its LDS does not fit: the
-# default falls back to 64-pixel blocks)
+# default falls back to 64-pixel blocks); 1 x 1 filters, whose steps have
+# two or three K-groups (one on the first plane)
 BF16_K_CASES = [((1, 4, 11, 9, 25, 32), 7), ((2, 3, 19, 35, 20, 64), 5),
-                ((1, 3, 21, 18, 40, 64), 5)]
+                ((1, 3, 21, 18, 40, 64), 5), ((1, 5, 17, 20, 7, 32), 1),
+                ((2, 3, 9, 33, 30, 64), 1)]
 
 
 @pytest.mark.parametrize("case", BF16_K_CASES,

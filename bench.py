@@ -80,7 +80,8 @@ def phase_work(name, V, C, O, K=3):
 #       matrix units' busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over
 #       GRBM_GUI_ACTIVE x 128)
 # S is the first 16 hex digits of the SHA-256 of the kernel's sources when
-# measured; a figure whose sources changed since is reported as null.
+# measured (comments and whitespace aside); a figure whose sources changed
+# since is reported as null.
 PROFILES = os.path.join(ROOT, "profiles")
 _STEP = ["sweep_step.hip", "common.h"]
 KERNEL_SOURCES = {
@@ -96,11 +97,17 @@ KERNEL_SOURCES = {
 
 
 def source_hash(kernel):
+    """Hash of the code of the kernel's sources: comments and whitespace are
+    dropped first, so that editing a comment keeps the measured figures."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, "paper_1506_07452_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_1506_07452_amd", "csrc", f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -1348,8 +1348,8 @@ k_step_fwd_b16_blk(FwdB16Args a)
 //   direct-to-LDS loads issued two K-groups ahead.  Step kg reads K-group
 //   kg + 1 into registers and refills the array that held kg with kg + 3;
 //   its barrier publishes kg + 2 (each wave has waited for its own share)
-//   and frees the array of kg + 1 for step kg + 2 (each wave has waited for
-//   its reads).  The arrays are distinct objects and each step names its
+//   and frees the array of kg + 1, which step kg + 1 refills (each wave has
+//   waited for its reads).  The arrays are distinct objects and each step names its
 //   two statically (the loop is unrolled by six), so the compiler knows that
 //   the reads do not touch the array a load is still filling.
 // - The reads of K-group kg + 1 are interleaved with kg's MFMAs (one A and

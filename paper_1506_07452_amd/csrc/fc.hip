@@ -1059,6 +1059,93 @@ int fc_mfma_co(long long M, int Cout, const TS *x, const TS *w, const TS *b, TS 
     return PLSTM_OK;
 }
 
+// bf16 storage with 32 or 64 inputs on the bf16 MFMA: the same tiles as
+// k_fc_tanh_mfma, each K-group of 32 inputs one v_mfma_f32_16x16x32_bf16 in
+// which lane group q supplies inputs 8q .. 8q+7 of its W row and of its x
+// row, each a 16-byte load.  Products of bf16 values are exact in fp32, so
+// only the order of the fp32 sums differs from the widened kernel.  A wave
+// takes NT voxel tiles (four, two for 128 outputs to keep two waves per
+// SIMD), so each W fragment feeds NT MFMAs.
+template <int CO> struct FcB16NT {
+    static constexpr int value = CO >= 8 ? 2 : 4;
+};
+
+template <int CI32, int CO>
+__global__ void __launch_bounds__(256)
+k_fc_tanh_b16(long long M, const uint16_t *__restrict__ x, const uint16_t *__restrict__ w,
+              const uint16_t *__restrict__ b, uint16_t *__restrict__ y)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+    typedef unsigned u4v __attribute__((ext_vector_type(4)));
+    constexpr int Cin = 32 * CI32, Cout = 16 * CO, kFcNTb = FcB16NT<CO>::value;
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const long long tile0 = ((long long)blockIdx.x * 4 + (threadIdx.x >> 6)) * kFcNTb;
+    long long row[kFcNTb];
+    bool live[kFcNTb];
+#pragma unroll
+    for (int nt = 0; nt < kFcNTb; ++nt) {
+        row[nt] = (tile0 + nt) * 16 + col;
+        live[nt] = row[nt] < M;
+    }
+    f4 acc[CO][kFcNTb];
+#pragma unroll
+    for (int mt = 0; mt < CO; ++mt) {
+        const f4 bv = Vec4<uint16_t>::load(b + mt * 16 + 4 * q4);
+#pragma unroll
+        for (int nt = 0; nt < kFcNTb; ++nt) acc[mt][nt] = bv;
+    }
+    const bf8v zero = __builtin_bit_cast(bf8v, u4v{0u, 0u, 0u, 0u});
+#pragma unroll
+    for (int kb = 0; kb < CI32; ++kb) {
+        bf8v xv[kFcNTb];
+#pragma unroll
+        for (int nt = 0; nt < kFcNTb; ++nt)
+            xv[nt] = live[nt] ? *(const bf8v *)(x + row[nt] * Cin + kb * 32 + 8 * q4) : zero;
+#pragma unroll
+        for (int mt = 0; mt < CO; ++mt) {
+            const bf8v wv = *(const bf8v *)(w + (long long)(mt * 16 + col) * Cin + kb * 32 + 8 * q4);
+#pragma unroll
+            for (int nt = 0; nt < kFcNTb; ++nt)
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wv, xv[nt], acc[mt][nt], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int nt = 0; nt < kFcNTb; ++nt) {
+        if (!live[nt]) continue;
+#pragma unroll
+        for (int mt = 0; mt < CO; ++mt) {
+            f4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = tanh_fast(acc[mt][nt][i]);
+            Vec4<uint16_t>::store(y + row[nt] * Cout + mt * 16 + 4 * q4, v);
+        }
+    }
+}
+
+template <int CI32, int CO>
+void launch_fc_b16(long long M, const uint16_t *x, const uint16_t *w, const uint16_t *b,
+                   uint16_t *y, hipStream_t st)
+{
+    constexpr int NT = FcB16NT<CO>::value;
+    const long long waves = (M + 16 * NT - 1) / (16 * NT);
+    k_fc_tanh_b16<CI32, CO><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(M, x, w, b, y);
+}
+
+template <int CI32>
+int fc_b16_co(long long M, int Cout, const uint16_t *x, const uint16_t *w, const uint16_t *b,
+              uint16_t *y, hipStream_t st)
+{
+    switch (Cout) {
+    case 32: launch_fc_b16<CI32, 2>(M, x, w, b, y, st); break;
+    case 64: launch_fc_b16<CI32, 4>(M, x, w, b, y, st); break;
+    case 128: launch_fc_b16<CI32, 8>(M, x, w, b, y, st); break;
+    default: return PLSTM_EUNSUPPORTED;
+    }
+    PLSTM_LAUNCH_CHECK();
+    return PLSTM_OK;
+}
+
 // Shapes of the MFMA FC: 16, 32 or 64 inputs, 32, 64 or 128 outputs.
 inline bool fc_mfma_ok(int Cin, int Cout)
 {
@@ -1080,6 +1167,11 @@ static int fc_tanh_forward_impl(long long M, int Cin, int Cout, int dtype, const
                                 const void *w, const void *b, void *y, hipStream_t st)
 {
     if (fc_mfma_ok(Cin, Cout)) {
+        if (dtype == PLSTM_BF16 && Cin >= 32)
+            return Cin == 32 ? fc_b16_co<1>(M, Cout, (const uint16_t *)x, (const uint16_t *)w,
+                                            (const uint16_t *)b, (uint16_t *)y, st)
+                             : fc_b16_co<2>(M, Cout, (const uint16_t *)x, (const uint16_t *)w,
+                                            (const uint16_t *)b, (uint16_t *)y, st);
         if (dtype == PLSTM_BF16)
             return fc_mfma<uint16_t>(M, Cin, Cout, (const uint16_t *)x, (const uint16_t *)w,
                                      (const uint16_t *)b, (uint16_t *)y, st);

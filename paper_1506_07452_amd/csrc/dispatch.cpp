@@ -48,7 +48,8 @@ int forward_dispatch(const Geom &g, int dtype, const void *x, const void *wx, co
                      const void *b, void *h, const Saved *sv, void *ws, hipStream_t st)
 {
     const int path = g_forward_path;
-    if (path != 1 && path != 4 && sweep_fwd_supported(g, dtype)) {
+    const bool b16_step = !sv && step_supported(g) && step_b16_packed(g, dtype);
+    if (path != 1 && path != 4 && !b16_step && sweep_fwd_supported(g, dtype)) {
         Carve cv(ws);
         float *hd = sv ? sv->hd : cv.take<float>(saved_state_count(g));
         float *cellbuf = sv ? sv->cell : cv.take<float>(saved_state_count(g));

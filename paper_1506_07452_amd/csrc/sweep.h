@@ -23,6 +23,9 @@ int sweep_bwd(const Geom &g, const float *x, const float *wx, const float *wh, c
 // Plane-step MFMA path (sweep_step.hip): O = 16, 32, 64, C <= 64, fp32
 // arithmetic (bf16 storage converted on entry), one launch per plane step.
 bool step_supported(const Geom &g);
+// bf16 inference of a 16-unit layer on the macro-tiled bf16 step (packed taps),
+// taken before the persistent fp32 sweep
+bool step_b16_packed(const Geom &g, int dtype);
 size_t step_fwd_ws(const Geom &g);
 // Writes c^d, the gates when `gates` is set, h^d (fp32; bf16 storage on the
 // bf16 MFMA keeps h^d in bf16 in the workspace instead) and the direction sum h.

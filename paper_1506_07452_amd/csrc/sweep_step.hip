@@ -987,8 +987,12 @@ k_pad_x_b16(long long nvox, int C, int C32, const uint16_t *__restrict__ x,
 // tap kg / (C32/32), channel block kg % (C32/32); the rest are h taps
 // (kg - KX) / (O/32), block (kg - KX) % (O/32).  Entry j of lane (q, col)
 // is the weight of gate-unit gate*O + 16 ug + col for channel 32 cb + 8q + j.
+// Packed taps (pk, 16 units, C <= 8): the four lane groups of a K-group take
+// four 8-channel slots, input slot 4 kg + q being tap 4 kg + q, h slot
+// 4 (kg - KX) + q being channels 8 (slot & 1) .. + 7 of tap slot / 2; slots
+// past the last tap hold zeros.
 __global__ void __launch_bounds__(256)
-k_pack_fwd_b16(int nd, int O, int C, int C32, int KX, int KG, int KK,
+k_pack_fwd_b16(int nd, int O, int C, int C32, int KX, int KG, int KK, int pk,
                const uint16_t *__restrict__ wx,
                const uint16_t *__restrict__ wh, const uint16_t *__restrict__ b,
                uint16_t *__restrict__ frag, float *__restrict__ bias)
@@ -1005,7 +1009,15 @@ k_pack_fwd_b16(int nd, int O, int C, int C32, int KX, int KG, int KK,
     const int q = lane >> 4, col = lane & 15;
     const long long gu = (long long)d * G + gate * O + ug * 16 + col;
     uint16_t v = 0;
-    if (kg < KX) {
+    if (pk) {
+        if (kg < KX) {
+            const int tap = 4 * kg + q;
+            if (tap < KK && j8 < C) v = wx[(gu * C + j8) * KK + tap];
+        } else {
+            const int slot = 4 * (kg - KX) + q, tap = slot >> 1;
+            if (tap < KK) v = wh[(gu * O + 8 * (slot & 1) + j8) * KK + tap];
+        }
+    } else if (kg < KX) {
         const int tap = kg / CX, c = (kg % CX) * 32 + 8 * q + j8;
         if (c < C) v = wx[(gu * C + c) * KK + tap];
     } else {
@@ -1018,7 +1030,8 @@ k_pack_fwd_b16(int nd, int O, int C, int C32, int KX, int KG, int KK,
 struct FwdB16Args {
     Geom g;
     int t;
-    int C32, KX, KG;          // padded channels, input K-groups (KK C32/32), all K-groups
+    int C32, KX, KG;          // padded channels (a multiple of 32; 8 for packed taps),
+                              // input K-groups, all K-groups
     int k_mul;                // ceil(2^16 / K)
     int cx_mul32;             // ceil(2^16 / (C32/32)): division by C32/32
     const uint16_t *xb;       // [N][V][C32] bf16
@@ -1355,6 +1368,11 @@ k_step_fwd_b16_blk(FwdB16Args a)
 // - The reads of K-group kg + 1 are interleaved with kg's MFMAs (one A and
 //   at most one B fragment per four MFMAs, the ring load mid-step), so
 //   neither waits on the other.
+// - 16-unit layers with at most 8 input channels pack their taps (PK): each
+//   lane group q of a K-group reads its own 8-channel slot, one input tap or
+//   half of an h tap, so a K-group holds four input taps or two h taps instead
+//   of one padded to 32 channels.  The staged pixel then has one x chunk, two
+//   h chunks and three pad chunks.
 // Workgroups are remapped so that each XCD runs a contiguous range of blocks
 // (at most two directions' weights per L2).
 template <int U, int WM, int WN>
@@ -1363,6 +1381,7 @@ __attribute__((amdgpu_waves_per_eu(U / WM == 1 ? 3 : 2)))
 k_step_fwd_b16_mt(FwdB16Args a)
 {
     constexpr int O = 16 * U, G = 4 * O, NW = WM * WN, T = 4 * U;
+    constexpr bool PK = U == 1;                 // packed taps
     constexpr int UGW = U / WM, AT = 4 * UGW;   // unit groups and A tiles per wave
     constexpr int BP = 4 * WN, BQ = 16;
     constexpr int NDMA = T / NW;             // ring loads per wave per K-group
@@ -1394,7 +1413,8 @@ k_step_fwd_b16_mt(FwdB16Args a)
     const int hoff = -dg.sign * ss;
     const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
     const int SW = BQ + 2 * radq, SH = BP + 2 * radp;
-    const int NXC = C32 >> 3, NCH = NXC + (O >> 3), NCHP = NCH + 2;
+    const int NXC = C32 >> 3, NCH = NXC + (O >> 3), NCHP = PK ? 6 : NCH + 2;
+    const int KK = a.g.KP * KQ;
     const long long sbase = ((long long)d * a.g.N + n) * V;
     // byte sizes: V * C32 * 2, V * O * 2 and U * KG * 4096 (< 2^31, checked on the host)
     const auto rs_x = __builtin_amdgcn_make_buffer_rsrc(
@@ -1449,12 +1469,22 @@ k_step_fwd_b16_mt(FwdB16Args a)
     if (KG > 2) issue_a(2, ring2);
 
     // staged chunk of this lane in tile nt (block row 4 wn + nt) at tap
-    // (0, 0), channel chunk q4
+    // (0, 0), channel chunk q4 (chunk 0 with packed taps)
     int spb[kNT];
 #pragma unroll
-    for (int nt = 0; nt < kNT; ++nt) spb[nt] = ((4 * wn + nt + radp) * SW + col + radq) * NCHP + q4;
-    // uniform part of the B offset of K-group kg: tap shift and chunk block
+    for (int nt = 0; nt < kNT; ++nt)
+        spb[nt] = ((4 * wn + nt + radp) * SW + col + radq) * NCHP + (PK ? 0 : q4);
+    // B offset of K-group kg past spb: tap shift and chunk block (uniform),
+    // with packed taps the lane's own slot (a slot past the last tap, whose
+    // weights are zero, reads the last tap)
     auto b_off = [&](int kg) {
+        if constexpr (PK) {
+            const bool is_x = kg < KX;
+            const int slot = 4 * (is_x ? kg : kg - KX) + q4;
+            const int tap = min(is_x ? slot : slot >> 1, KK - 1);
+            const int row = tap_row(tap, a.k_mul), ka = row - radp, kb = tap - row * KQ - radq;
+            return (ka * SW + kb) * NCHP + (is_x ? 0 : NXC + (slot & 1));
+        }
         const bool is_x = kg < KX;
         const int kk = is_x ? kg : kg - KX;
         const int tap = is_x ? (kk * a.cx_mul32) >> 16 : kk / (O / 32);
@@ -3273,11 +3303,29 @@ bool step_supported(const Geom &g)
 }
 
 // bf16 storage with 32 or 64 hidden units takes the bf16 MFMA.
+// 16-unit layers take the bf16 MFMA only as the macro-tiled kernel with packed
+// taps (3D, at most 8 input channels).
+inline bool b16_packed(const Geom &g) { return g.O == 16 && g.C <= 8 && g.nd == kDirs; }
 inline bool use_b16(const Geom &g, int dtype)
 {
-    return dtype == PLSTM_BF16 && (g.O == 32 || g.O == 64) && g_step_bf16_mfma;
+    return dtype == PLSTM_BF16 && g_step_bf16_mfma &&
+           (g.O == 32 || g.O == 64 || (b16_packed(g) && g_step_bf16_mfma == 1));
 }
 inline int pad32(int c) { return (c + 31) / 32 * 32; }
+// bf16 channel padding and K-groups: taps padded to 32 channels each, or
+// packed (four input slots or two h taps per K-group)
+struct B16K {
+    int C32, KX, KG;
+};
+inline B16K b16_k(const Geom &g)
+{
+    const int KK = g.KP * g.KQ;
+    if (g.O == 16) return {8, (KK + 3) / 4, (KK + 3) / 4 + (KK + 1) / 2};
+    const int C32 = pad32(g.C);
+    return {C32, KK * C32 / 32, KK * (C32 + g.O) / 32};
+}
+
+bool step_b16_packed(const Geom &g, int dtype) { return use_b16(g, dtype) && g.O == 16; }
 
 size_t step_fwd_ws(const Geom &g)
 {
@@ -3287,11 +3335,11 @@ size_t step_fwd_ws(const Geom &g)
     cv.take<float>((size_t)g.nd * U * KG * 1024);    // A fragments
     cv.take<float>((size_t)g.nd * 4 * g.O);          // bias
     size_t need = cv.off;
-    if (g.O % 32 == 0) {                             // bf16 variant
-        const int C32 = pad32(g.C), KGb = KK * (C32 + g.O) / 32;
+    if (g.O % 32 == 0 || b16_packed(g)) {           // bf16 variant
+        const B16K k = b16_k(g);
         Carve cb(nullptr);
-        cb.take<uint16_t>((size_t)g.N * g.V * C32);
-        cb.take<uint16_t>((size_t)g.nd * U * KGb * 2048);
+        cb.take<uint16_t>((size_t)g.N * g.V * k.C32);
+        cb.take<uint16_t>((size_t)g.nd * U * k.KG * 2048);
         cb.take<float>((size_t)g.nd * 4 * g.O);
         cb.take<uint16_t>((size_t)g.nd * g.N * g.V * g.O);
         if (cb.off > need) need = cb.off;
@@ -3333,6 +3381,7 @@ size_t b16_block_lds(const Geom &g, const FwdB16Args &a)
 template <int U> struct MtShape;
 template <> struct MtShape<4> { static constexpr int WM = 2, WN = 4; };
 template <> struct MtShape<2> { static constexpr int WM = 2, WN = 2; };
+template <> struct MtShape<1> { static constexpr int WM = 1, WN = 4; };
 void set_mt_blocks(const Geom &g, int wn, int *bp, int *bq, int *nbq, int *nblk)
 {
     for (int d = 0; d < kDirs; ++d) {
@@ -3345,11 +3394,11 @@ void set_mt_blocks(const Geom &g, int wn, int *bp, int *bq, int *nbq, int *nblk)
 }
 
 // Dynamic LDS bytes of the macro-tiled kernel: the staged block with its
-// halo, NCH + 2 chunks per pixel.  Its A ring (three arrays of 4U tiles of
-// 1 KB) is static.
+// halo, NCH + 2 chunks per pixel (6 with packed taps).  Its A ring (three
+// arrays of 4U tiles of 1 KB) is static.
 size_t b16_mt_stage_lds(const Geom &g, const FwdB16Args &a, int wn)
 {
-    const int nchp = (a.C32 + g.O) / 8 + 2;
+    const int nchp = g.O == 16 ? 6 : (a.C32 + g.O) / 8 + 2;
     return (size_t)(4 * wn + 2 * (g.KP / 2)) * (16 + 2 * (g.KQ / 2)) * nchp * 16;
 }
 
@@ -3364,6 +3413,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
                     (size_t)3 * 4 * U * 1024 + lds_mt <= (size_t)device_info().max_lds;
     size_t lds = 0;
     bool staged = false;
+    if (U == 1 && !mt) return PLSTM_EUNSUPPORTED;   // packed taps: macro-tiled only
     if (mt) {
         set_mt_blocks(g, WN, a.bp, a.bq, a.nbq, a.nblk);
         if (hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, WM, WN>,
@@ -3390,6 +3440,8 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
             PLSTM_LAUNCH_CHECK();
             continue;
         }
+        if constexpr (U == 1) return PLSTM_EUNSUPPORTED;
+        else {
         int tot = 0;
         for (int d = 0; d < kDirs; ++d) {
             a.base[d] = tot;
@@ -3410,6 +3462,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
             k_step_fwd_b16<U, false><<<blocks_for(tot, kSW), 64 * kSW, 0, st>>>(a);
         }
         PLSTM_LAUNCH_CHECK();
+        }
     }
     return PLSTM_OK;
 }
@@ -3418,8 +3471,8 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
                         const uint16_t *wh, const uint16_t *b, void *h, float *cell, void *ws,
                         hipStream_t st)
 {
-    const int U = g.O / 16, C32 = pad32(g.C);
-    const int KK = g.KP * g.KQ, KX = KK * C32 / 32, KG = KX + KK * g.O / 32;
+    const B16K k = b16_k(g);
+    const int U = g.O / 16, C32 = k.C32, KK = g.KP * g.KQ, KX = k.KX, KG = k.KG;
     Carve cv(ws);
     uint16_t *xb = cv.take<uint16_t>((size_t)g.N * g.V * C32);
     uint16_t *frag = cv.take<uint16_t>((size_t)g.nd * U * KG * 2048);
@@ -3428,21 +3481,26 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     const long long nvox = (long long)g.N * g.V;
     const long long nfrag = (long long)g.nd * U * KG * 2048;
     timing_begin("sweep_fwd_step_bf16", st);
-    k_pad_x_b16<<<blocks_for(nvox * C32, 256), 256, 0, st>>>(nvox, g.C, C32, x, xb);
-    PLSTM_LAUNCH_CHECK();
-    k_pack_fwd_b16<<<blocks_for(nfrag, 256), 256, 0, st>>>(g.nd, g.O, g.C, C32, KX, KG, KK, wx, wh,
-                                                           b,
-                                                           frag, bias);
+    // channels already a multiple of 32: the input is its own padded copy
+    if (C32 != g.C) {
+        k_pad_x_b16<<<blocks_for(nvox * C32, 256), 256, 0, st>>>(nvox, g.C, C32, x, xb);
+        PLSTM_LAUNCH_CHECK();
+    }
+    k_pack_fwd_b16<<<blocks_for(nfrag, 256), 256, 0, st>>>(g.nd, g.O, g.C, C32, KX, KG, KK,
+                                                           g.O == 16, wx, wh, b, frag, bias);
     PLSTM_LAUNCH_CHECK();
     FwdB16Args a;
     a.g = g;
     a.C32 = C32; a.KX = KX; a.KG = KG;
-    a.cx_mul32 = (65536 + C32 / 32 - 1) / (C32 / 32);
+    a.cx_mul32 = C32 >= 32 ? (65536 + C32 / 32 - 1) / (C32 / 32) : 0;
     a.k_mul = k_mul_of(g);
-    a.xb = xb; a.frag = frag; a.bias = bias;
+    a.xb = C32 != g.C ? xb : x;
+    a.frag = frag; a.bias = bias;
     a.cell = cell; a.hb = hb;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
-    const int rc = U == 2 ? launch_fwd_b16_steps<2>(g, a, st) : launch_fwd_b16_steps<4>(g, a, st);
+    const int rc = U == 1   ? launch_fwd_b16_steps<1>(g, a, st)
+                   : U == 2 ? launch_fwd_b16_steps<2>(g, a, st)
+                            : launch_fwd_b16_steps<4>(g, a, st);
     if (rc != PLSTM_OK) return rc;
     timing_end(2 + max_T(g), st);
     return sum_dirs_bf16(g, hb, h, st);

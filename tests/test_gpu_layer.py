@@ -330,7 +330,12 @@ def test_filter_size_generic_path(case):
 # two or three K-groups (one on the first plane)
 BF16_K_CASES = [((1, 4, 11, 9, 25, 32), 7), ((2, 3, 19, 35, 20, 64), 5),
                 ((1, 3, 21, 18, 40, 64), 5), ((1, 5, 17, 20, 7, 32), 1),
-                ((2, 3, 9, 33, 30, 64), 1)]
+                ((2, 3, 9, 33, 30, 64), 1),
+                # 16 units, packed taps: 16 x 16 pixel blocks with ragged
+                # edges, every filter size, one to eight input channels
+                ((2, 5, 19, 35, 3, 16), 3), ((1, 4, 11, 9, 8, 16), 7),
+                ((1, 3, 21, 18, 5, 16), 5), ((1, 5, 17, 20, 1, 16), 1),
+                ((1, 2, 3, 9, 4, 16), 7)]
 
 
 @pytest.mark.parametrize("case", BF16_K_CASES,
@@ -381,22 +386,33 @@ def test_reverse_sweep_strip_kinds_match_oracle(shape, bwd_path):
 
 @pytest.mark.parametrize("shape", [(1, 5, 37, 29, 3, 16), (2, 9, 20, 18, 1, 16)],
                          ids=lambda s: "x".join(map(str, s)))
-def test_bf16_o16_forward_takes_the_persistent_sweep(shape):
-    """bf16 storage with 16 units and C <= 4: the inputs are widened to fp32
-    and the persistent sweep runs; the output is the bf16-rounded sum."""
+@pytest.mark.parametrize("bf16_mfma", [1, 3], ids=["packed_step", "persistent"])
+def test_bf16_o16_forward_paths(shape, bf16_mfma):
+    """bf16 storage with 16 units and C <= 8: by default the bf16 plane steps
+    with packed taps run (h^d rounded to bf16 for the recurrence and the
+    sum); with the 256-pixel blocks off the inputs are widened to fp32 and
+    the persistent sweep runs, the output being the bf16-rounded sum."""
     inst = instance(shape, 1500 + sum(shape), "bf16")
     L = inst.layers[0]
     ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
-    say("bf16 persistent", shape)
+    say("bf16 o16", shape, bf16_mfma)
+    P.pyramid_lstm_set_bf16_mfma(bf16_mfma)
     P.pyramid_lstm_timing_enable(True)
-    h, _ = layer_forward(dev(inst.x, "bf16"), layer_dev(L, "bf16"))
-    phases = P.pyramid_lstm_timing_read()
-    P.pyramid_lstm_timing_enable(False)
+    try:
+        h, _ = layer_forward(dev(inst.x, "bf16"), layer_dev(L, "bf16"))
+        phases = P.pyramid_lstm_timing_read()
+    finally:
+        P.pyramid_lstm_timing_enable(False)
+        P.pyramid_lstm_set_bf16_mfma(1)
     torch.cuda.synchronize()
-    assert "sweep_fwd_mfma" in phases and "sweep_fwd_step" not in phases, phases
     assert h.dtype == torch.bfloat16
-    # fp32 arithmetic: only the final rounding to bf16 separates it from the oracle
-    assert normwise(host(h), ref) <= 4e-3
+    if bf16_mfma == 1:
+        assert "sweep_fwd_step_bf16" in phases and "sweep_fwd_mfma" not in phases, phases
+        assert normwise(host(h), ref) <= TOL["bf16"]
+    else:
+        assert "sweep_fwd_mfma" in phases and "sweep_fwd_step" not in phases, phases
+        # fp32 arithmetic: only the final rounding to bf16 separates it from the oracle
+        assert normwise(host(h), ref) <= 4e-3
 
 
 def test_mfma_backward_runs_for_o16():

@@ -184,6 +184,23 @@ int pyramid_softmax_sq(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const v
                        void *loss, void *dx, void *dw, void *db, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* The output end of inference in one pass over the rows (Section 2.3,
+ * "Fully-Connected Layer"; Fig. 3): the last per-voxel fully connected layer
+ * with tanh, then the per-voxel linear layer and softmax,
+ *   y = tanh(w1 x + b1) (rounded to the storage type),  p = softmax(w2 y + b2),
+ * without writing y.  x [M][Cin], w1 [F][Cin], b1 [F], w2 [K][F], b2 [K] in
+ * `dtype`; p [M][K] fp32, overwritten.  All pointers device memory, 16-byte
+ * aligned, owned by the caller; runs on `stream`.  y equals
+ * pyramid_fc_tanh_forward's output bit for bit and p equals
+ * pyramid_softmax_ce's (no labels) up to the order of fp32 sums.  Covers bf16
+ * storage with Cin 32 or 64, F 32, 64 or 128 and K <= 16
+ * (pyramid_head_forward_supported returns 1 for those, 0 otherwise); other
+ * shapes return PLSTM_EUNSUPPORTED, bad sizes or pointers PLSTM_EINVAL. */
+int pyramid_head_forward_supported(int32_t dtype, int32_t Cin, int32_t F, int32_t K);
+int pyramid_head_forward(int64_t M, int32_t Cin, int32_t F, int32_t K, int32_t dtype,
+                         const void *x, const void *w1, const void *b1, const void *w2,
+                         const void *b2, void *p, void *stream);
+
 /* Bytes of workspace for pyramid_head_train, or 0 when the fused kernel does
  * not cover (Cin, F, K). */
 size_t pyramid_head_workspace_size(int64_t M, int32_t Cin, int32_t F, int32_t K);

@@ -20,6 +20,7 @@ __all__ = [
     "pyramid_lstm_forward", "pyramid_lstm_backward", "pyramid_fc_tanh_forward",
     "pyramid_fc_workspace_size", "pyramid_fc_tanh_backward", "pyramid_softmax_ce",
     "pyramid_head_workspace_size", "pyramid_head_train", "plstm_param_segment",
+    "pyramid_head_forward", "pyramid_head_forward_supported",
     "pyramid_rmsprop_step", "pyramid_rmsprop_learning_rate", "RMSprop", "pyramid_softmax_sq",
     "pyramid_crop", "pyramid_stitch_clear", "pyramid_stitch_add", "pyramid_stitch_finish",
     "pyramid_lstm_timing_enable", "pyramid_lstm_timing_read", "pyramid_lstm_set_forward_path",
@@ -125,6 +126,10 @@ def load():
     lib.pyramid_head_workspace_size.restype = sz
     lib.pyramid_head_train.argtypes = [i64, i32, i32, i32] + [vp] * 14 + [sz, vp]
     lib.pyramid_head_train.restype = ctypes.c_int
+    lib.pyramid_head_forward_supported.argtypes = [i32, i32, i32, i32]
+    lib.pyramid_head_forward_supported.restype = ctypes.c_int
+    lib.pyramid_head_forward.argtypes = [i64, i32, i32, i32, i32] + [vp] * 7
+    lib.pyramid_head_forward.restype = ctypes.c_int
     f32 = ctypes.c_float
     lib.pyramid_rmsprop_step.argtypes = [i32, ctypes.POINTER(plstm_param_segment), f32, f32, f32,
                                          f32, vp]
@@ -347,6 +352,20 @@ def pyramid_head_train(x, w1, b1, w2, b2, labels, p, loss, dx, dw1, db1, dw2, db
         M, Cin, F, K, _ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(labels), _ptr(p),
         _ptr(loss), _ptr(dx), _ptr(dw1), _ptr(db1), _ptr(dw2), _ptr(db2), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def pyramid_head_forward_supported(dtype, Cin: int, F: int, K: int) -> bool:
+    return bool(load().pyramid_head_forward_supported(_DT[dtype], Cin, F, K))
+
+
+def pyramid_head_forward(x, w1, b1, w2, b2, p, stream=None):
+    """Fused FC tanh + linear + softmax for inference: x [M][Cin], w1 [F][Cin],
+    b1 [F], w2 [K][F], b2 [K] (same dtype), p [M][K] fp32."""
+    M, Cin = x.shape
+    F, K = w1.shape[0], w2.shape[0]
+    _check("pyramid_head_forward", load().pyramid_head_forward(
+        M, Cin, F, K, _DT[x.dtype], _ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(p),
+        _stream(stream)))
 
 
 def pyramid_rmsprop_step(params, grads, ms, mom, lr, rho_ms=0.9, rho_m=0.9, eps=1e-5,

@@ -277,6 +277,27 @@ int pyramid_softmax_sq(int64_t M, int32_t Cin, int32_t K, int32_t dtype, const v
                          stream, true);
 }
 
+int pyramid_head_forward_supported(int32_t dtype, int32_t Cin, int32_t F, int32_t K)
+{
+    return head_fwd_supported(dtype, Cin, F, K) ? 1 : 0;
+}
+
+int pyramid_head_forward(int64_t M, int32_t Cin, int32_t F, int32_t K, int32_t dtype,
+                         const void *x, const void *w1, const void *b1, const void *w2,
+                         const void *b2, void *p, void *stream)
+{
+    if (M < 1 || M > (1LL << 40) / 256 || Cin < 1 || F < 1 || K < 1) return PLSTM_EINVAL;
+    if (dtype != PLSTM_F32 && dtype != PLSTM_BF16) return PLSTM_EINVAL;
+    if (!x || !w1 || !b1 || !w2 || !b2 || !p) return PLSTM_EINVAL;
+    if (!aligned(x) || !aligned(w1) || !aligned(b1) || !aligned(w2) || !aligned(b2) ||
+        !aligned(p))
+        return PLSTM_EINVAL;
+    if (!head_fwd_supported(dtype, Cin, F, K)) return PLSTM_EUNSUPPORTED;
+    return head_forward(M, Cin, F, K, (const uint16_t *)x, (const uint16_t *)w1,
+                        (const uint16_t *)b1, (const uint16_t *)w2, (const uint16_t *)b2,
+                        (float *)p, (hipStream_t)stream);
+}
+
 size_t pyramid_head_workspace_size(int64_t M, int32_t Cin, int32_t F, int32_t K)
 {
     if (M < 1 || M > (1LL << 40) / 64 || !head_supported(Cin, F, K)) return 0;

@@ -180,6 +180,11 @@ size_t fc_ws(long long M, int Cin, int Cout);
 int softmax_ce(long long M, int Cin, int K, int dtype, const void *x, const void *w,
                const void *b, const int32_t *labels, float *p, float *loss, float *dx,
                float *dw, float *db, void *ws, hipStream_t st, bool squared = false);
+// Fused FC + tanh, linear + softmax for inference (bf16 storage).
+bool head_fwd_supported(int dtype, int Cin, int F, int K);
+int head_forward(long long M, int Cin, int F, int K, const uint16_t *x, const uint16_t *w1,
+                 const uint16_t *b1, const uint16_t *w2, const uint16_t *b2, float *p,
+                 hipStream_t st);
 // Fused FC + tanh, linear + softmax, cross-entropy and backward (fp32).
 bool head_supported(int Cin, int F, int K);
 size_t head_ws(long long M, int Cin, int F, int K);

@@ -3,6 +3,7 @@
 // followed by a per-voxel softmax, with the mean cross-entropy and its
 // gradient for training.  Weight-gradient sums over voxels are deterministic
 // two-stage reductions (fixed chunking, fixed order).
+#include <type_traits>
 #include "common.h"
 #include "timing.h"
 
@@ -1146,6 +1147,143 @@ int fc_b16_co(long long M, int Cout, const uint16_t *x, const uint16_t *w, const
     return PLSTM_OK;
 }
 
+// Inference output end for bf16 storage (Section 2.3, "Fully-Connected
+// Layer"; Fig. 3): the FC + tanh tiles of k_fc_tanh_b16, whose outputs stay
+// in registers, then the per-voxel linear layer as a second MFMA with the
+// classes as its 16 rows and the voxels as its columns.  After the first
+// contraction lane group q of a voxel column holds FC outputs 16 mt + 4q + i
+// (i < 4) of tile mt; K-group kk of the second takes outputs 32 kk + 4q + i
+// from tile 2 kk and 32 kk + 16 + 4q + i from tile 2 kk + 1 as lane group q's
+// eight values, and the W2 fragments are permuted the same way, so nothing
+// crosses lanes.  The FC tiles are made two at a time and consumed at once,
+// so only two tiles per voxel tile are live and a wave takes four voxel
+// tiles.  The logits of a voxel land in the four lane groups of its column
+// (class 4q + i); their maximum and sum meet over the groups with two
+// exchanges each.  y is rounded to bf16 before the second contraction, as the
+// separate kernels store it, and its tiles are summed in the same order, so
+// y is the separate kernels' y bit for bit.
+constexpr int kHeadNT = 4;
+
+template <int CI32, int FO>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+k_head_fwd_b16(long long M, int K, const uint16_t *__restrict__ x,
+               const uint16_t *__restrict__ w1, const uint16_t *__restrict__ b1,
+               const uint16_t *__restrict__ w2, const uint16_t *__restrict__ b2,
+               float *__restrict__ p)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+    typedef unsigned u4v __attribute__((ext_vector_type(4)));
+    typedef unsigned short us4v __attribute__((ext_vector_type(4)));
+    typedef unsigned short us8v __attribute__((ext_vector_type(8)));
+    constexpr int Cin = 32 * CI32, F = 16 * FO, NT = kHeadNT, KK2 = FO / 2;
+    static_assert(FO % 2 == 0, "F a multiple of 32");
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const long long tile0 = ((long long)blockIdx.x * 4 + (threadIdx.x >> 6)) * NT;
+    long long row[NT];
+    bool live[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        row[nt] = (tile0 + nt) * 16 + col;
+        live[nt] = row[nt] < M;
+    }
+    const bf8v zero = __builtin_bit_cast(bf8v, u4v{0u, 0u, 0u, 0u});
+    bf8v xv[CI32][NT];
+#pragma unroll
+    for (int kb = 0; kb < CI32; ++kb)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+            xv[kb][nt] = live[nt] ? *(const bf8v *)(x + row[nt] * Cin + kb * 32 + 8 * q4) : zero;
+    f4 z[NT];
+    {
+        f4 bias2;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            bias2[i] = 4 * q4 + i < K ? bf16_to_f32(b2[4 * q4 + i]) : 0.0f;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) z[nt] = bias2;
+    }
+#pragma unroll
+    for (int kk = 0; kk < KK2; ++kk) {
+        // W2 fragment kk: lane (class col, group q4), permuted as above; zero
+        // rows past the last class
+        us4v lo = us4v{0, 0, 0, 0}, hi = lo;
+        if (col < K) {
+            lo = *(const us4v *)(w2 + col * F + 32 * kk + 4 * q4);
+            hi = *(const us4v *)(w2 + col * F + 32 * kk + 16 + 4 * q4);
+        }
+        const bf8v a2 = __builtin_bit_cast(bf8v, us8v{lo[0], lo[1], lo[2], lo[3],
+                                                      hi[0], hi[1], hi[2], hi[3]});
+        f4 acc[2][NT];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int mt = 2 * kk + h;
+            const f4 bv = Vec4<uint16_t>::load(b1 + mt * 16 + 4 * q4);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) acc[h][nt] = bv;
+#pragma unroll
+            for (int kb = 0; kb < CI32; ++kb) {
+                const bf8v wv =
+                    *(const bf8v *)(w1 + (long long)(mt * 16 + col) * Cin + kb * 32 + 8 * q4);
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+                    acc[h][nt] =
+                        __builtin_amdgcn_mfma_f32_16x16x32_bf16(wv, xv[kb][nt], acc[h][nt], 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            us8v yv;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                yv[i] = f32_to_bf16(tanh_fast(acc[0][nt][i]));
+                yv[4 + i] = f32_to_bf16(tanh_fast(acc[1][nt][i]));
+            }
+            z[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, __builtin_bit_cast(bf8v, yv),
+                                                            z[nt], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        // every lane takes part in the exchanges, live or not
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (4 * q4 + i < K) mx = fmaxf(mx, z[nt][i]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        f4 e;
+        float sum = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            e[i] = 4 * q4 + i < K ? __expf(z[nt][i] - mx) : 0.0f;
+            sum += e[i];
+        }
+        sum += __shfl_xor(sum, 16);
+        sum += __shfl_xor(sum, 32);
+        const float inv = 1.0f / sum;
+        if (!live[nt]) continue;
+        if (K == 4) {
+            if (q4 == 0) *(f4 *)(p + row[nt] * 4) = e * inv;
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (4 * q4 + i < K) p[row[nt] * K + 4 * q4 + i] = e[i] * inv;
+        }
+    }
+}
+
+template <int CI32, int FO>
+void launch_head_fwd_b16(long long M, int K, const uint16_t *x, const uint16_t *w1,
+                         const uint16_t *b1, const uint16_t *w2, const uint16_t *b2, float *p,
+                         hipStream_t st)
+{
+    constexpr int NT = kHeadNT;
+    const long long waves = (M + 16 * NT - 1) / (16 * NT);
+    k_head_fwd_b16<CI32, FO><<<(unsigned)((waves + 3) / 4), 256, 0, st>>>(M, K, x, w1, b1, w2,
+                                                                         b2, p);
+}
+
 // Shapes of the MFMA FC: 16, 32 or 64 inputs, 32, 64 or 128 outputs.
 inline bool fc_mfma_ok(int Cin, int Cout)
 {
@@ -1518,6 +1656,39 @@ bool head_supported(int Cin, int F, int K)
 size_t head_ws(long long M, int Cin, int F, int K)
 {
     return (size_t)head_blocks(M) * (F * (Cin + 1) + K * (F + 1) + 1) * sizeof(float);
+}
+
+bool head_fwd_supported(int dtype, int Cin, int F, int K)
+{
+    return dtype == PLSTM_BF16 && (Cin == 32 || Cin == 64) && (F == 32 || F == 64 || F == 128) &&
+           K >= 1 && K <= 16;
+}
+
+int head_forward(long long M, int Cin, int F, int K, const uint16_t *x, const uint16_t *w1,
+                 const uint16_t *b1, const uint16_t *w2, const uint16_t *b2, float *p,
+                 hipStream_t st)
+{
+    timing_begin("head_fwd", st);
+    auto go = [&](auto ci, auto fo) {
+        launch_head_fwd_b16<decltype(ci)::value, decltype(fo)::value>(M, K, x, w1, b1, w2, b2, p,
+                                                                      st);
+    };
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I4 = std::integral_constant<int, 4>;
+    using I8 = std::integral_constant<int, 8>;
+    if (Cin == 32) {
+        if (F == 32) go(I1(), I2());
+        else if (F == 64) go(I1(), I4());
+        else go(I1(), I8());
+    } else {
+        if (F == 32) go(I2(), I2());
+        else if (F == 64) go(I2(), I4());
+        else go(I2(), I8());
+    }
+    PLSTM_LAUNCH_CHECK();
+    timing_end(1, st);
+    return PLSTM_OK;
 }
 
 int head_train(long long M, int Cin, int F, int K, const float *x, const float *w1,

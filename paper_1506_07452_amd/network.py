@@ -13,6 +13,7 @@ from typing import List, Optional, Tuple
 import torch
 
 from . import (plstm_shape, pyramid_fc_tanh_backward, pyramid_fc_tanh_forward,
+               pyramid_head_forward, pyramid_head_forward_supported,
                pyramid_head_train, pyramid_head_workspace_size, pyramid_lstm_backward,
                pyramid_lstm_forward, pyramid_lstm_saved_size, pyramid_lstm_workspace_size,
                pyramid_lstm2d_backward, pyramid_lstm2d_forward, pyramid_lstm2d_saved_size,
@@ -103,12 +104,24 @@ def network_forward(x, layers: List[LayerW], fcs: List[Tuple[torch.Tensor, torch
     M = N * D * H * W
     if len(fcs) not in (len(layers), len(layers) - 1):
         raise ValueError("one hidden FC layer per PyraMiD-LSTM layer, or none after the last")
+    K = head[0].shape[0]
+    # inference with bf16 storage: the last FC and the softmax as one pass
+    # (the last layer's act then has no "y")
+    fused = (labels is None and not training and len(fcs) == len(layers) and
+             x.dtype == torch.bfloat16 and
+             pyramid_head_forward_supported(x.dtype, layers[-1].O, fcs[-1][0].shape[0], K))
     a = x
     acts = []
     for li, L in enumerate(layers):
         h, saved = layer_forward(a, L, training, ws, stream)
         act = {"in": a, "h": h, "saved": saved}
         a = h
+        if fused and li == len(layers) - 1:
+            acts.append(act)
+            p = torch.empty((M, K), dtype=torch.float32, device=x.device)
+            pyramid_head_forward(h.view(M, -1), fcs[li][0], fcs[li][1], head[0], head[1], p,
+                                 stream)
+            return {"p": p, "acts": acts}
         if li < len(fcs):
             wf, bf = fcs[li]
             y = torch.empty((N, D, H, W, wf.shape[0]), dtype=a.dtype, device=a.device)
@@ -116,7 +129,6 @@ def network_forward(x, layers: List[LayerW], fcs: List[Tuple[torch.Tensor, torch
             act["y"] = y
             a = y
         acts.append(act)
-    K = head[0].shape[0]
     p = torch.empty((M, K), dtype=torch.float32, device=x.device)
     out = {"p": p, "acts": acts}
     if labels is None:

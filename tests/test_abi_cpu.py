@@ -165,6 +165,32 @@ def test_head_validation(lib):
     assert call(nbytes=16) == -3
 
 
+def test_head_forward_validation(lib):
+    bf16, f32 = P.PLSTM_BF16, P.PLSTM_F32
+    for cin in (32, 64):
+        for f in (32, 64, 128):
+            for k in (1, 4, 16):
+                assert lib.pyramid_head_forward_supported(bf16, cin, f, k) == 1
+    for bad in ((f32, 64, 128, 4), (bf16, 16, 32, 4), (bf16, 64, 48, 4), (bf16, 64, 128, 17),
+                (bf16, 64, 128, 0), (bf16, 128, 128, 4)):
+        assert lib.pyramid_head_forward_supported(*bad) == 0, bad
+    def call(M=1000, Cin=64, F=128, K=4, dtype=bf16, **over):
+        names = ["x", "w1", "b1", "w2", "b2", "p"]
+        a = [FAKE] * 6
+        for k, v in over.items():
+            a[names.index(k)] = v
+        return lib.pyramid_head_forward(M, Cin, F, K, dtype, *a, None)
+    assert call(M=0) == -1
+    assert call(K=0) == -1
+    assert call(dtype=7) == -1
+    assert call(p=None) == -1
+    assert call(w2=None) == -1
+    assert call(x=ctypes.c_void_p(0x10008)) == -1
+    assert call(dtype=f32) == -2
+    assert call(F=48) == -2
+    assert call(K=17) == -2
+
+
 def test_binding_refuses_host_tensors():
     import torch
     x = torch.zeros(1, 2, 2, 2, 1)

@@ -314,6 +314,39 @@ def test_fc_tanh_forward_widths(cin, cout, dtype):
     assert normwise(host(y), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("case", [(1, 32, 32, 4), (1037, 64, 128, 4), (515, 32, 64, 5),
+                                  (2049, 64, 32, 16), (777, 64, 64, 1), (140001, 64, 128, 4),
+                                  (33, 32, 128, 3)],
+                         ids=lambda c: "x".join(map(str, c)))
+def test_head_forward_bf16(case):
+    """The fused inference head (FC tanh + linear + softmax, bf16 storage)
+    against the separate entry points (same y, fp32 sums in another order)
+    and the oracle: one row, ragged tiles, one to sixteen classes."""
+    import paper_1506_07452_amd as P
+    M, cin, F, K = case
+    rng = np.random.default_rng(131 + M + cin + F + K)
+    xd = dev(rng.standard_normal((M, cin)), "bf16")
+    w1 = dev(rng.uniform(-0.3, 0.3, (F, cin)), "bf16")
+    b1 = dev(rng.uniform(-0.3, 0.3, F), "bf16")
+    w2 = dev(rng.uniform(-0.5, 0.5, (K, F)), "bf16")
+    b2 = dev(rng.uniform(-0.5, 0.5, K), "bf16")
+    say("head forward bf16", case)
+    assert P.pyramid_head_forward_supported(torch.bfloat16, cin, F, K)
+    p = torch.full((M, K), float("nan"), device=DEV)
+    P.pyramid_head_forward(xd, w1, b1, w2, b2, p)
+    y = torch.empty(M, F, device=DEV, dtype=torch.bfloat16)
+    P.pyramid_fc_tanh_forward(xd, w1, b1, y)
+    p_sep = torch.empty(M, K, device=DEV)
+    P.pyramid_softmax_ce(y, w2, b2, p_sep)
+    torch.cuda.synchronize()
+    assert torch.isfinite(p).all()
+    err = (p - p_sep).abs().max().item()
+    assert err <= 2e-6, err
+    ref_y = oracle.fc_tanh_forward(host(xd), host(w1), host(b1))
+    ref = oracle.softmax_ce(ref_y, host(w2), host(b2))["p"]
+    assert normwise(host(p), ref) <= TOL["bf16"]
+
+
 @pytest.mark.parametrize("case", [(1, 16, 32), (129, 16, 32), (1037, 32, 64), (140001, 16, 32),
                                   (2049, 32, 64), (1037, 64, 128), (515, 24, 40)],
                          ids=lambda c: "x".join(map(str, c)))

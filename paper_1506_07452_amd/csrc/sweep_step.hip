@@ -1040,6 +1040,9 @@ struct FwdB16Args {
     float *cell;              // [6][N][V][O] fp32 c^d
     uint16_t *hb;             // [6][N][V][O] bf16 h^d (the recurrence's operand and the
                               // direction sum's input)
+    float *cpp;               // macro-tiled kernel: c^d of the last two planes,
+                              // [6][N][2][pqmax][O] fp32, plane t at parity t & 1
+    int pqmax;                // largest plane (P Q) over the directions
     int npg[kDirs];
     int base[kDirs + 1];
     // pixel blocks of the LDS-staged kernel: BP x BQ pixels (BP BQ = 64), nbq
@@ -1373,6 +1376,9 @@ k_step_fwd_b16_blk(FwdB16Args a)
 //   half of an h tap, so a K-group holds four input taps or two h taps instead
 //   of one padded to 32 channels.  The staged pixel then has one x chunk, two
 //   h chunks and three pad chunks.
+// - c^d is needed one plane later only, so it lives in a two-plane buffer
+//   (100 MB for the stacked network's 64-unit layer) that stays in the
+//   memory-side cache instead of a volume written out to HBM.
 // Workgroups are remapped so that each XCD runs a contiguous range of blocks
 // (at most two directions' weights per L2).
 template <int U, int WM, int WN>
@@ -1425,7 +1431,11 @@ k_step_fwd_b16_mt(FwdB16Args a)
     const auto rs_a = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t *>(a.frag + (long long)d * U * KGA * 2048), (short)0,
         U * KGA * 4096, kRsrcWord3);
-    const auto rs_c = slice_rsrc(a.cell + sbase * O, V * O);
+    // c of this block's pixels: plane parity t & 1 of the two-plane buffer,
+    // c_{t-1} from the other parity
+    const long long cpq = (long long)a.pqmax * O;
+    float *cpl = a.cpp + ((long long)d * a.g.N + n) * 2 * cpq;
+    const auto rs_c = slice_rsrc(cpl + ((t + 1) & 1) * cpq, cpq);
 
     // A fragments of K-group kg into a ring array: tile j = 4 ug + gate
     auto issue_a = [&](int kg, bf8 *slot) {
@@ -1563,13 +1573,14 @@ k_step_fwd_b16_mt(FwdB16Args a)
     // epilogue operands, in flight during the last K-group's MFMAs
     const int ug0 = UGW * wm;
     f4 bias[UGW][4], cprev[UGW][kNT];
-    int evox[kNT];
+    int evox[kNT], epix[kNT];
     bool elive[kNT];
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt) {
         const int pp = p0 + 4 * wn + nt, qq = q0 + col;
         elive[nt] = on_plane(pp, qq, P, Q);
         evox[nt] = s * ss + (elive[nt] ? pp * sp + qq * sq : 0);
+        epix[nt] = elive[nt] ? pp * Q + qq : 0;
     }
 #pragma unroll
     for (int ui = 0; ui < UGW; ++ui) {
@@ -1579,7 +1590,7 @@ k_step_fwd_b16_mt(FwdB16Args a)
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
             cprev[ui][nt] = bload4(rs_c, sel_off(t > 0 && elive[nt],
-                                                 (unsigned)((evox[nt] + hoff) * O + uo) * 4u));
+                                                 (unsigned)(epix[nt] * O + uo) * 4u));
     }
     mfmas(X);
 
@@ -1603,7 +1614,7 @@ k_step_fwd_b16_mt(FwdB16Args a)
                 h[i] = go * ftanh(c[i]);
                 hbv[i] = f32_to_bf16(h[i]);
             }
-            *(f4 *)(a.cell + vo * O + uo) = c;
+            *(f4 *)(cpl + (t & 1) * cpq + epix[nt] * O + uo) = c;
             *(us4 *)(a.hb + vo * O + uo) = hbv;
         }
     }
@@ -3312,6 +3323,13 @@ inline bool use_b16(const Geom &g, int dtype)
            (g.O == 32 || g.O == 64 || (b16_packed(g) && g_step_bf16_mfma == 1));
 }
 inline int pad32(int c) { return (c + 31) / 32 * 32; }
+inline int max_pq(const Geom &g)
+{
+    int m = 0;
+    for (int d = 0; d < g.nd; ++d)
+        if (g.dir[d].P * g.dir[d].Q > m) m = g.dir[d].P * g.dir[d].Q;
+    return m;
+}
 // bf16 channel padding and K-groups: taps padded to 32 channels each, or
 // packed (four input slots or two h taps per K-group)
 struct B16K {
@@ -3342,6 +3360,7 @@ size_t step_fwd_ws(const Geom &g)
         cb.take<uint16_t>((size_t)g.nd * U * k.KG * 2048);
         cb.take<float>((size_t)g.nd * 4 * g.O);
         cb.take<uint16_t>((size_t)g.nd * g.N * g.V * g.O);
+        cb.take<float>((size_t)g.nd * g.N * 2 * max_pq(g) * g.O);   // c^d, two planes
         if (cb.off > need) need = cb.off;
     }
     return need;
@@ -3478,6 +3497,7 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     uint16_t *frag = cv.take<uint16_t>((size_t)g.nd * U * KG * 2048);
     float *bias = cv.take<float>((size_t)g.nd * 4 * g.O);
     uint16_t *hb = cv.take<uint16_t>((size_t)g.nd * g.N * g.V * g.O);
+    float *cpp = cv.take<float>((size_t)g.nd * g.N * 2 * max_pq(g) * g.O);
     const long long nvox = (long long)g.N * g.V;
     const long long nfrag = (long long)g.nd * U * KG * 2048;
     timing_begin("sweep_fwd_step_bf16", st);
@@ -3497,6 +3517,7 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     a.xb = C32 != g.C ? xb : x;
     a.frag = frag; a.bias = bias;
     a.cell = cell; a.hb = hb;
+    a.cpp = cpp; a.pqmax = max_pq(g);
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
     const int rc = U == 1   ? launch_fwd_b16_steps<1>(g, a, st)
                    : U == 2 ? launch_fwd_b16_steps<2>(g, a, st)

@@ -67,6 +67,9 @@ def phase_work(name, V, C, O, K=3):
     if name.startswith("head_fused"):
         # reads h and the label, writes p (4 classes) and dL/dh per voxel
         return "hbm", V * (O * 4 + 4 + 4 * 4 + O * 4), "GB/s"
+    if name.startswith("head_fwd"):
+        # bf16 inference head: reads h, writes p (4 classes, fp32) per voxel
+        return "hbm", V * (O * 2 + 4 * 4), "GB/s"
     return None, None, None
 
 
@@ -92,6 +95,7 @@ KERNEL_SOURCES = {
     "sweep_fwd_step_bf16": _STEP,
     "sum_dirs": ["generic.hip", "common.h"],
     "head_fused": ["fc.hip", "common.h"], "fc_tanh_fwd": ["fc.hip", "common.h"],
+    "head_fwd": ["fc.hip", "common.h"],
     "fc_tanh_bwd": ["fc.hip", "common.h"], "softmax_ce": ["fc.hip", "common.h"],
 }
 
@@ -178,14 +182,16 @@ def roofline(phases, name, passes, V, C, O, mode="training", workload=None):
 
 
 def layer_path(C, O, dtype, K=3):
-    """Which forward kernels the library runs for a layer: the persistent
-    sweeps (16 hidden units, at most 4 input channels, 3x3; bf16 storage is
-    widened to fp32 first), the plane-step bf16 MFMA (bf16 storage, 32 or 64
-    hidden units) or the plane-step fp32 MFMA; phase names end in _mfma,
-    _step_bf16 or _step."""
+    """Which forward kernels the library runs for a layer (inference with
+    bf16 storage, training in fp32): the plane-step bf16 MFMA (bf16 storage,
+    32 or 64 hidden units, or 16 with at most 8 input channels), the persistent
+    sweeps (16 hidden units, at most 4 input channels, 3x3) or the plane-step
+    fp32 MFMA; phase names end in _step_bf16, _mfma or _step."""
+    if dtype == "bf16" and (O in (32, 64) or (O == 16 and C <= 8)):
+        return "step_bf16"
     if O == 16 and C <= 4 and K == 3:
         return "mfma"
-    return "step_bf16" if dtype == "bf16" and O in (32, 64) else "step"
+    return "step"
 
 
 def dx_in_reverse(li, C, O, path):

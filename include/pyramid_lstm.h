@@ -428,9 +428,11 @@ int pyramid_lstm_set_step_split(int mode);
  * weights streamed through LDS for all of a workgroup's waves (3 where its
  * LDS does not fit, e.g. 64 units with 5 x 5 filters); 3 = the same
  * contraction on 64-pixel blocks, the weights read by each wave from L1;
- * 2 = operands read from L1 per tap; 0 = fp32 MFMA on the widened values.
- * Results of 1, 2 and 3 differ only in summation order.  Returns
- * PLSTM_EINVAL for other values. */
+ * 2 = operands read from L1 per tap; 0 = fp32 MFMA on the widened values;
+ * 4 = as 1, but 16-unit layers (3D, at most 8 input channels, which take
+ * the bf16 MFMA on packed taps under 1 and 4 only) run one plane per launch
+ * instead of two.  Results of 1, 2 and 3 differ only in summation order, 1
+ * and 4 not at all.  Returns PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_bf16_mfma(int on);
 
 /* Weight gradients of the plane-step backward, for testing and tuning

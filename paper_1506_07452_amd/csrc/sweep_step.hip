@@ -966,6 +966,20 @@ __device__ inline f4 mfma_bf16(bf8 a, bf8 b, f4 c)
 {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
+// Gates and cell update of four units (Eq. (7)-(12)) for the bf16 steps,
+// h rounded to bf16.  The fused multiply-adds are written out, so every
+// kernel that uses it rounds alike whatever the compiler would contract.
+__device__ inline void lstm_cell4_b16(const f4 (&pre)[4], const f4 &cprev, f4 &c, us4 &hbv)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float gi = fsig(pre[0][i]), gf = fsig(pre[1][i]), go = fsig(pre[3][i]);
+        const float gg = __builtin_fmaf(-2.0f, frcp(__expf(2.0f * pre[2][i]) + 1.0f), 1.0f);
+        c[i] = __builtin_fmaf(gg, gi, cprev[i] * gf);
+        const float tc = __builtin_fmaf(-2.0f, frcp(__expf(2.0f * c[i]) + 1.0f), 1.0f);
+        hbv[i] = f32_to_bf16(go * tc);
+    }
+}
 __device__ inline bf8 bload8h(__amdgpu_buffer_rsrc_t rs, unsigned off)
 {
     return __builtin_bit_cast(bf8, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0));
@@ -1604,18 +1618,225 @@ k_step_fwd_b16_mt(FwdB16Args a)
             f4 pre[4];
 #pragma unroll
             for (int gt = 0; gt < 4; ++gt) pre[gt] = acc[ui * 4 + gt][nt] + bias[ui][gt];
-            f4 c, h;
+            f4 c;
             us4 hbv;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float gi = fsig(pre[0][i]), gf = fsig(pre[1][i]);
-                const float gg = ftanh(pre[2][i]), go = fsig(pre[3][i]);
-                c[i] = gg * gi + cprev[ui][nt][i] * gf;
-                h[i] = go * ftanh(c[i]);
-                hbv[i] = f32_to_bf16(h[i]);
-            }
+            lstm_cell4_b16(pre, cprev[ui][nt], c, hbv);
             *(f4 *)(cpl + (t & 1) * cpq + epix[nt] * O + uo) = c;
             *(us4 *)(a.hb + vo * O + uo) = hbv;
+        }
+    }
+}
+
+// Two plane steps per launch for 16-unit layers on packed taps with 3 x 3
+// filters: Eq. (7)-(12) for planes t and t + 1 of every direction.  These
+// steps are bound by each launch's fixed latency (staging, a contraction of
+// eight K-groups, the epilogue), not by their work, so a workgroup takes a
+// 16 x 16 block through both planes:
+// - it stages x_t, x_{t+1} and h_{t-1} on the block and a two-pixel halo
+//   (a 20 x 20 grid of six 16-byte chunks per pixel: x_t, h_{t-1} twice,
+//   x_{t+1}, and h_t twice, written by step t);
+// - step t covers the block and the one-pixel ring around it, whose h_t the
+//   block's step t + 1 reads (the ring is also computed, identically, by the
+//   neighbouring blocks: 27% more work for step t in exchange for half the
+//   launches); h_t goes to LDS (zero off the plane) and, for the block, to h^d;
+// - step t + 1 covers the block.  Wave w takes block rows 4w .. 4w + 3 in
+//   both steps, so c_t of its pixels stays in its registers; the 68 ring
+//   pixels fill five more tiles (two for wave 0, one for the others).
+// All eight K-groups of A fragments stay in LDS.  The contraction, its order
+// and the cell update are those of k_step_fwd_b16_mt, so h^d and c^d are the
+// same bit for bit.  c^d alternates between the halves of the two-plane
+// buffer by launch: launch L = t / 2 reads c_{t-1} from half (L + 1) & 1 and
+// writes c_{t+1} to half L & 1 (a neighbour may still read c_{t-1} of this
+// block's pixels).  Every direction's plane count must be even.
+constexpr int kS2Grid = 20, kS2Chunks = 6, kS2KG = 8;
+
+template <int NT>
+__device__ inline void s2_contract(const bf8 *afr, const bf8 *stg, const int (&pb)[NT], int xch,
+                                   int hch, int q4, int lane, f4 (&acc)[NT][4])
+{
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acc[i][g] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int kg = 0; kg < kS2KG; ++kg) {
+        // packed taps: input slot 4 kg + q4 is tap 4 kg + q4; h slot
+        // 4 (kg - 3) + q4 is half slot & 1 of tap slot / 2; slots past the
+        // ninth tap carry zero weights and read the last tap
+        const bool is_x = kg < 3;
+        const int slot = 4 * (is_x ? kg : kg - 3) + q4;
+        const int tap = min(is_x ? slot : slot >> 1, 8);
+        const int ka = tap / 3 - 1, kb = tap - (tap / 3) * 3 - 1;
+        const int off = (ka * kS2Grid + kb) * kS2Chunks + (is_x ? xch : hch + (slot & 1));
+        bf8 av[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) av[g] = afr[(kg * 4 + g) * 64 + lane];
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const bf8 bv = stg[pb[i] + off];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) acc[i][g] = mfma_bf16(av[g], bv, acc[i][g]);
+        }
+    }
+}
+
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+k_step2_fwd_b16_pk(FwdB16Args a)
+{
+    constexpr int O = 16, G = 4 * O, SG = kS2Grid, NC = kS2Chunks, KG = kS2KG;
+    __shared__ bf8 afr[KG * 4 * 64];          // A fragments [kg][gate][lane]
+    extern __shared__ bf8 stg[];              // [SG][SG][NC]
+    const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int per_xcd = gridDim.x / kXcds;
+    const int blk = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    if (blk >= a.base[kDirs]) return;
+    const int d = item_dir(a.base, blk);
+    const DirGeom dg = a.g.dir[d];
+    int r = blk - a.base[d];
+    const int n = r / a.nblk[d];
+    r -= n * a.nblk[d];
+    const int bi = r / a.nbq[d], bj = r - bi * a.nbq[d];
+    const int p0 = bi * 16, q0 = bj * 16;
+    const int t = a.t;                         // even: this launch makes planes t and t + 1
+    const int s = dg.sign > 0 ? t : dg.T - 1 - t;
+    const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
+    const int P = dg.P, Q = dg.Q;
+    const int nxt = dg.sign * ss;              // voxel offset of the next plane
+    const long long V = a.g.V;
+    const long long sbase = ((long long)d * a.g.N + n) * V;
+    // byte sizes: V * 16, V * O * 2 and KG * 4096 (< 2^31, checked on the host)
+    const auto rs_x = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(a.xb + (long long)n * V * 8), (short)0, (int)(V * 16), kRsrcWord3);
+    const auto rs_h = __builtin_amdgcn_make_buffer_rsrc(a.hb + sbase * O, (short)0,
+                                                        (int)(V * O * 2), kRsrcWord3);
+    const auto rs_a = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(a.frag + (long long)d * KG * 2048), (short)0, KG * 4096,
+        kRsrcWord3);
+    const long long cpq = (long long)a.pqmax * O;
+    float *cpl = a.cpp + ((long long)d * a.g.N + n) * 2 * cpq;
+    const int half = (t >> 1) & 1;
+    const auto rs_c = slice_rsrc(cpl + (half ^ 1) * cpq, cpq);
+    float *cw = cpl + half * cpq;
+
+    // A fragments, tile j = 4 kg + gate, eight tiles per wave
+#pragma unroll
+    for (int j0 = 0; j0 < KG * 4; j0 += 4) {
+        const int j = j0 + wv;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_a, (lds_void *)&afr[j * 64], 16,
+                                                 (int)((unsigned)(j * 512 + lane * 8) * 2u), 0, 0,
+                                                 0);
+    }
+    // staged grid: pixel (gy, gx) is plane pixel (p0 - 2 + gy, q0 - 2 + gx);
+    // zero off the plane, h_{t-1} zero before the first plane, chunks 4-5
+    // zero until step t writes them
+    constexpr int nst = SG * SG * NC;
+    for (int e0 = wv * 64; e0 < nst; e0 += 256) {
+        const int e = e0 + lane;
+        const int spx = e / NC, c = e - spx * NC;
+        const int gy = spx / SG, gx = spx - gy * SG;
+        const int pp = p0 - 2 + gy, qq = q0 - 2 + gx;
+        const bool on = on_plane(pp, qq, P, Q);
+        const int v = s * ss + pp * sp + qq * sq;
+        lds_void *dst = (lds_void *)&stg[e0];
+        if (e < nst) {
+            if (c == 0 || c == 3)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs_x, dst, 16, (int)sel_off(on, (unsigned)((c == 0 ? v : v + nxt) * 8) * 2u),
+                    0, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs_h, dst, 16,
+                    (int)sel_off(on && t > 0 && c < 3, (unsigned)((v - nxt) * O + 8 * (c - 1)) * 2u),
+                    0, 0, 0);
+        }
+    }
+    const int uo = 4 * q4;
+    f4 bias[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) bias[g] = *(const f4 *)(a.bias + d * G + g * O + uo);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+
+    // gates and cell update of one tile (as in k_step_fwd_b16_mt)
+    auto cell = [&](const f4 (&acc)[4], const f4 &cprev, f4 &c, us4 &hbv) {
+        f4 pre[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) pre[g] = acc[g] + bias[g];
+        lstm_cell4_b16(pre, cprev, c, hbv);
+    };
+    // h_t of staged pixel sp into chunks 4-5 (units uo .. uo + 3)
+    auto put_h = [&](int spx, us4 v) {
+        *(us4 *)((char *)stg + (size_t)(spx * NC + 4) * 16 + q4 * 8) = v;
+    };
+
+    // ---- step t, block rows 4 wv .. 4 wv + 3
+    int pb[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) pb[nt] = ((4 * wv + nt + 2) * SG + col + 2) * NC;
+    bool live[kNT];
+    int pix[kNT];
+    f4 cprev[kNT], ct[kNT];
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt) {
+        const int pp = p0 + 4 * wv + nt, qq = q0 + col;
+        live[nt] = on_plane(pp, qq, P, Q);
+        pix[nt] = live[nt] ? pp * Q + qq : 0;
+        cprev[nt] = bload4(rs_c, sel_off(t > 0 && live[nt], (unsigned)(pix[nt] * O + uo) * 4u));
+    }
+    {
+        f4 acc[kNT][4];
+        s2_contract<kNT>(afr, stg, pb, 0, 1, q4, lane, acc);
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) {
+            us4 hbv;
+            cell(acc[nt], cprev[nt], ct[nt], hbv);
+            if (!live[nt]) hbv = us4{0, 0, 0, 0};
+            put_h(pb[nt] / NC, hbv);
+            if (live[nt]) {
+                const int pp = p0 + 4 * wv + nt, qq = q0 + col;
+                *(us4 *)(a.hb + (sbase + s * ss + pp * sp + qq * sq) * O + uo) = hbv;
+            }
+        }
+    }
+    // ---- step t, the ring: index k < 68 walks the top row, the bottom row,
+    // then the left and right columns of the 18 x 18 region around the block
+    for (int j = wv; j < 5; j += 4) {
+        const int k = 16 * j + col;
+        const bool slot = k < 68;
+        int rr, cc;
+        if (k < 18) { rr = 0; cc = k; }
+        else if (k < 36) { rr = 17; cc = k - 18; }
+        else if (k < 52) { rr = k - 36 + 1; cc = 0; }
+        else if (k < 68) { rr = k - 52 + 1; cc = 17; }
+        else { rr = 0; cc = 0; }
+        const int pp = p0 - 1 + rr, qq = q0 - 1 + cc;
+        const bool on = slot && on_plane(pp, qq, P, Q);
+        const f4 cp = bload4(rs_c, sel_off(t > 0 && on, (unsigned)((on ? pp * Q + qq : 0) * O + uo) * 4u));
+        int rb[1] = {((rr + 1) * SG + cc + 1) * NC};
+        f4 acc[1][4];
+        s2_contract<1>(afr, stg, rb, 0, 1, q4, lane, acc);
+        f4 c;
+        us4 hbv;
+        cell(acc[0], cp, c, hbv);
+        if (!on) hbv = us4{0, 0, 0, 0};
+        if (slot) put_h(rb[0] / NC, hbv);
+    }
+    __syncthreads();
+
+    // ---- step t + 1 of the block: x_{t+1} in chunk 3, h_t in chunks 4-5
+    {
+        f4 acc[kNT][4];
+        s2_contract<kNT>(afr, stg, pb, 3, 4, q4, lane, acc);
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) {
+            if (!live[nt]) continue;
+            f4 c;
+            us4 hbv;
+            cell(acc[nt], ct[nt], c, hbv);
+            const int pp = p0 + 4 * wv + nt, qq = q0 + col;
+            *(f4 *)(cw + pix[nt] * O + uo) = c;
+            *(us4 *)(a.hb + (sbase + s * ss + nxt + pp * sp + qq * sq) * O + uo) = hbv;
         }
     }
 }
@@ -3298,6 +3519,12 @@ int g_step_split = 0;
 int g_step_bf16_mfma = 1;
 int g_wgrad_staged = 1;
 
+namespace {
+// knob values 1 and 4 select the macro-tiled bf16 kernels; 4 keeps the
+// 16-unit layers at one plane per launch
+inline bool b16_mt_mode() { return g_step_bf16_mfma == 1 || g_step_bf16_mfma == 4; }
+}  // namespace
+
 bool step_supported(const Geom &g)
 {
     if (g.O != 16 && g.O != 32 && g.O != 64) return false;
@@ -3320,7 +3547,7 @@ inline bool b16_packed(const Geom &g) { return g.O == 16 && g.C <= 8 && g.nd == 
 inline bool use_b16(const Geom &g, int dtype)
 {
     return dtype == PLSTM_BF16 && g_step_bf16_mfma &&
-           (g.O == 32 || g.O == 64 || (b16_packed(g) && g_step_bf16_mfma == 1));
+           (g.O == 32 || g.O == 64 || (b16_packed(g) && b16_mt_mode()));
 }
 inline int pad32(int c) { return (c + 31) / 32 * 32; }
 inline int max_pq(const Geom &g)
@@ -3428,11 +3655,39 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
     const int few = split_threshold();
     constexpr int WM = MtShape<U>::WM, WN = MtShape<U>::WN;
     const size_t lds_mt = b16_mt_stage_lds(g, a, WN);
-    const bool mt = g_step_bf16_mfma == 1 &&
+    const bool mt = b16_mt_mode() &&
                     (size_t)3 * 4 * U * 1024 + lds_mt <= (size_t)device_info().max_lds;
     size_t lds = 0;
     bool staged = false;
     if (U == 1 && !mt) return PLSTM_EUNSUPPORTED;   // packed taps: macro-tiled only
+    if constexpr (U == 1) {
+        // two planes per launch: 3 x 3 filters, an even number of planes in
+        // every direction
+        bool two = g_step_bf16_mfma == 1 && g.KP == 3 && g.KQ == 3;
+        for (int d = 0; d < g.nd; ++d) two = two && g.dir[d].T % 2 == 0;
+        if (two) {
+            set_mt_blocks(g, 4, a.bp, a.bq, a.nbq, a.nblk);
+            const int lds2 = kS2Grid * kS2Grid * kS2Chunks * 16;
+            if (hipFuncSetAttribute((const void *)k_step2_fwd_b16_pk,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    lds2) != hipSuccess)
+                return PLSTM_EHIP;
+            for (int t = 0; t < T; t += 2) {
+                a.t = t;
+                int nb = 0;
+                for (int d = 0; d < kDirs; ++d) {
+                    a.base[d] = nb;
+                    if (t < g.dir[d].T) nb += g.N * a.nblk[d];
+                }
+                a.base[kDirs] = nb;
+                if (nb == 0) continue;
+                const int grid = (nb + kXcds - 1) / kXcds * kXcds;
+                k_step2_fwd_b16_pk<<<grid, 256, lds2, st>>>(a);
+                PLSTM_LAUNCH_CHECK();
+            }
+            return PLSTM_OK;
+        }
+    }
     if (mt) {
         set_mt_blocks(g, WN, a.bp, a.bq, a.nbq, a.nblk);
         if (hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, WM, WN>,
@@ -3904,7 +4159,7 @@ extern "C" int pyramid_lstm_set_step_split(int mode)
 
 extern "C" int pyramid_lstm_set_bf16_mfma(int on)
 {
-    if (on < 0 || on > 3) return PLSTM_EINVAL;
+    if (on < 0 || on > 4) return PLSTM_EINVAL;
     plstm::g_step_bf16_mfma = on;
     return PLSTM_OK;
 }

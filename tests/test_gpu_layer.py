@@ -415,6 +415,32 @@ def test_bf16_o16_forward_paths(shape, bf16_mfma):
         assert normwise(host(h), ref) <= 4e-3
 
 
+@pytest.mark.parametrize("shape", [(2, 6, 20, 34, 3, 16), (1, 4, 18, 16, 8, 16),
+                                   (1, 2, 33, 18, 1, 16), (3, 8, 8, 8, 3, 16)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_bf16_o16_two_planes_per_launch(shape):
+    """16-unit bf16 layers with 3 x 3 filters and an even number of planes in
+    every direction run two planes per launch (each block also computes the
+    one-pixel ring of its first plane): the same h bit for bit as one plane
+    per launch, and the oracle's within the bf16 bound; ragged 16 x 16
+    blocks, a single launch pair (D = 2), planes smaller than a block."""
+    inst = instance(shape, 1600 + sum(shape), "bf16")
+    L = inst.layers[0]
+    ref = oracle.forward(inst.x, L.wx, L.wh, L.b)["h"]
+    say("bf16 o16 two planes", shape)
+    x, Ld = dev(inst.x, "bf16"), layer_dev(L, "bf16")
+    out = {}
+    for knob in (1, 4):
+        P.pyramid_lstm_set_bf16_mfma(knob)
+        try:
+            out[knob], _ = layer_forward(x, Ld)
+            torch.cuda.synchronize()
+        finally:
+            P.pyramid_lstm_set_bf16_mfma(1)
+    assert torch.equal(out[1], out[4])
+    assert normwise(host(out[1]), ref) <= TOL["bf16"]
+
+
 def test_mfma_backward_runs_for_o16():
     """The persistent MFMA reverse sweep and MFMA parameter gradients are the
     path taken for 16 hidden units."""

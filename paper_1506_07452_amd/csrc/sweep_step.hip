@@ -1639,9 +1639,9 @@ k_step_fwd_b16_mt(FwdB16Args a)
 //   block's step t + 1 reads (the ring is also computed, identically, by the
 //   neighbouring blocks: 27% more work for step t in exchange for half the
 //   launches); h_t goes to LDS (zero off the plane) and, for the block, to h^d;
-// - step t + 1 covers the block.  Wave w takes block rows 4w .. 4w + 3 in
+// - step t + 1 covers the block.  Wave w takes block rows 2w and 2w + 1 in
 //   both steps, so c_t of its pixels stays in its registers; the 68 ring
-//   pixels fill five more tiles (two for wave 0, one for the others).
+//   pixels fill five more tiles, one each for waves 0-4.
 // All eight K-groups of A fragments stay in LDS.  The contraction, its order
 // and the cell update are those of k_step_fwd_b16_mt, so h^d and c^d are the
 // same bit for bit.  c^d alternates between the halves of the two-plane
@@ -1680,10 +1680,16 @@ __device__ inline void s2_contract(const bf8 *afr, const bf8 *stg, const int (&p
     }
 }
 
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+// eight waves of two block rows each: 118 VGPRs, two workgroups (16 waves)
+// per CU; four waves of four rows (198 VGPRs, 8 waves per CU) took 9% longer
+constexpr int kS2Waves = 8;
+
+template <int NWV>
+__global__ void __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV == 8 ? 4 : 2)))
 k_step2_fwd_b16_pk(FwdB16Args a)
 {
     constexpr int O = 16, G = 4 * O, SG = kS2Grid, NC = kS2Chunks, KG = kS2KG;
+    constexpr int RPW = 16 / NWV;             // block rows per wave
     __shared__ bf8 afr[KG * 4 * 64];          // A fragments [kg][gate][lane]
     extern __shared__ bf8 stg[];              // [SG][SG][NC]
     const int lane = threadIdx.x & 63, q4 = lane >> 4, col = lane & 15;
@@ -1719,9 +1725,9 @@ k_step2_fwd_b16_pk(FwdB16Args a)
     const auto rs_c = slice_rsrc(cpl + (half ^ 1) * cpq, cpq);
     float *cw = cpl + half * cpq;
 
-    // A fragments, tile j = 4 kg + gate, eight tiles per wave
+    // A fragments, tile j = 4 kg + gate
 #pragma unroll
-    for (int j0 = 0; j0 < KG * 4; j0 += 4) {
+    for (int j0 = 0; j0 < KG * 4; j0 += NWV) {
         const int j = j0 + wv;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_a, (lds_void *)&afr[j * 64], 16,
                                                  (int)((unsigned)(j * 512 + lane * 8) * 2u), 0, 0,
@@ -1731,7 +1737,7 @@ k_step2_fwd_b16_pk(FwdB16Args a)
     // zero off the plane, h_{t-1} zero before the first plane, chunks 4-5
     // zero until step t writes them
     constexpr int nst = SG * SG * NC;
-    for (int e0 = wv * 64; e0 < nst; e0 += 256) {
+    for (int e0 = wv * 64; e0 < nst; e0 += 64 * NWV) {
         const int e = e0 + lane;
         const int spx = e / NC, c = e - spx * NC;
         const int gy = spx / SG, gx = spx - gy * SG;
@@ -1770,38 +1776,38 @@ k_step2_fwd_b16_pk(FwdB16Args a)
         *(us4 *)((char *)stg + (size_t)(spx * NC + 4) * 16 + q4 * 8) = v;
     };
 
-    // ---- step t, block rows 4 wv .. 4 wv + 3
-    int pb[kNT];
+    // ---- step t, block rows RPW wv .. RPW wv + RPW - 1
+    int pb[RPW];
 #pragma unroll
-    for (int nt = 0; nt < kNT; ++nt) pb[nt] = ((4 * wv + nt + 2) * SG + col + 2) * NC;
-    bool live[kNT];
-    int pix[kNT];
-    f4 cprev[kNT], ct[kNT];
+    for (int nt = 0; nt < RPW; ++nt) pb[nt] = ((RPW * wv + nt + 2) * SG + col + 2) * NC;
+    bool live[RPW];
+    int pix[RPW];
+    f4 cprev[RPW], ct[RPW];
 #pragma unroll
-    for (int nt = 0; nt < kNT; ++nt) {
-        const int pp = p0 + 4 * wv + nt, qq = q0 + col;
+    for (int nt = 0; nt < RPW; ++nt) {
+        const int pp = p0 + RPW * wv + nt, qq = q0 + col;
         live[nt] = on_plane(pp, qq, P, Q);
         pix[nt] = live[nt] ? pp * Q + qq : 0;
         cprev[nt] = bload4(rs_c, sel_off(t > 0 && live[nt], (unsigned)(pix[nt] * O + uo) * 4u));
     }
     {
-        f4 acc[kNT][4];
-        s2_contract<kNT>(afr, stg, pb, 0, 1, q4, lane, acc);
+        f4 acc[RPW][4];
+        s2_contract<RPW>(afr, stg, pb, 0, 1, q4, lane, acc);
 #pragma unroll
-        for (int nt = 0; nt < kNT; ++nt) {
+        for (int nt = 0; nt < RPW; ++nt) {
             us4 hbv;
             cell(acc[nt], cprev[nt], ct[nt], hbv);
             if (!live[nt]) hbv = us4{0, 0, 0, 0};
             put_h(pb[nt] / NC, hbv);
             if (live[nt]) {
-                const int pp = p0 + 4 * wv + nt, qq = q0 + col;
+                const int pp = p0 + RPW * wv + nt, qq = q0 + col;
                 *(us4 *)(a.hb + (sbase + s * ss + pp * sp + qq * sq) * O + uo) = hbv;
             }
         }
     }
     // ---- step t, the ring: index k < 68 walks the top row, the bottom row,
     // then the left and right columns of the 18 x 18 region around the block
-    for (int j = wv; j < 5; j += 4) {
+    for (int j = wv; j < 5; j += NWV) {
         const int k = 16 * j + col;
         const bool slot = k < 68;
         int rr, cc;
@@ -1826,15 +1832,15 @@ k_step2_fwd_b16_pk(FwdB16Args a)
 
     // ---- step t + 1 of the block: x_{t+1} in chunk 3, h_t in chunks 4-5
     {
-        f4 acc[kNT][4];
-        s2_contract<kNT>(afr, stg, pb, 3, 4, q4, lane, acc);
+        f4 acc[RPW][4];
+        s2_contract<RPW>(afr, stg, pb, 3, 4, q4, lane, acc);
 #pragma unroll
-        for (int nt = 0; nt < kNT; ++nt) {
+        for (int nt = 0; nt < RPW; ++nt) {
             if (!live[nt]) continue;
             f4 c;
             us4 hbv;
             cell(acc[nt], ct[nt], c, hbv);
-            const int pp = p0 + 4 * wv + nt, qq = q0 + col;
+            const int pp = p0 + RPW * wv + nt, qq = q0 + col;
             *(f4 *)(cw + pix[nt] * O + uo) = c;
             *(us4 *)(a.hb + (sbase + s * ss + nxt + pp * sp + qq * sq) * O + uo) = hbv;
         }
@@ -3668,7 +3674,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
         if (two) {
             set_mt_blocks(g, 4, a.bp, a.bq, a.nbq, a.nblk);
             const int lds2 = kS2Grid * kS2Grid * kS2Chunks * 16;
-            if (hipFuncSetAttribute((const void *)k_step2_fwd_b16_pk,
+            if (hipFuncSetAttribute((const void *)k_step2_fwd_b16_pk<kS2Waves>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize,
                                     lds2) != hipSuccess)
                 return PLSTM_EHIP;
@@ -3682,7 +3688,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
                 a.base[kDirs] = nb;
                 if (nb == 0) continue;
                 const int grid = (nb + kXcds - 1) / kXcds * kXcds;
-                k_step2_fwd_b16_pk<<<grid, 256, lds2, st>>>(a);
+                k_step2_fwd_b16_pk<kS2Waves><<<grid, 64 * kS2Waves, lds2, st>>>(a);
                 PLSTM_LAUNCH_CHECK();
             }
             return PLSTM_OK;

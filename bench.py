@@ -614,7 +614,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the six sweeps of a layer run concurrently "
-              "on a single MI355X and this build has no multi-GPU path (--gpus 1).",
+              "on a single MI355X and the library has no multi-GPU path (--gpus 1).",
               file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:

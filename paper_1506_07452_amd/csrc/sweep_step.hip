@@ -3655,8 +3655,9 @@ size_t b16_mt_stage_lds(const Geom &g, const FwdB16Args &a, int wn)
 }
 
 template <int U>
-int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
+int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st, int *launches)
 {
+    *launches = max_T(g);
     const int T = max_T(g);
     const int few = split_threshold();
     constexpr int WM = MtShape<U>::WM, WN = MtShape<U>::WN;
@@ -3691,6 +3692,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st)
                 k_step2_fwd_b16_pk<kS2Waves><<<grid, 64 * kS2Waves, lds2, st>>>(a);
                 PLSTM_LAUNCH_CHECK();
             }
+            *launches = (T + 1) / 2;
             return PLSTM_OK;
         }
     }
@@ -3780,11 +3782,12 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     a.cell = cell; a.hb = hb;
     a.cpp = cpp; a.pqmax = max_pq(g);
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
-    const int rc = U == 1   ? launch_fwd_b16_steps<1>(g, a, st)
-                   : U == 2 ? launch_fwd_b16_steps<2>(g, a, st)
-                            : launch_fwd_b16_steps<4>(g, a, st);
+    int steps = 0;
+    const int rc = U == 1   ? launch_fwd_b16_steps<1>(g, a, st, &steps)
+                   : U == 2 ? launch_fwd_b16_steps<2>(g, a, st, &steps)
+                            : launch_fwd_b16_steps<4>(g, a, st, &steps);
     if (rc != PLSTM_OK) return rc;
-    timing_end(2 + max_T(g), st);
+    timing_end((C32 != g.C ? 2 : 1) + steps, st);
     return sum_dirs_bf16(g, hb, h, st);
 }
 

@@ -431,8 +431,13 @@ int pyramid_lstm_set_step_split(int mode);
  * 2 = operands read from L1 per tap; 0 = fp32 MFMA on the widened values;
  * 4 = as 1, but 16-unit layers (3D, at most 8 input channels, which take
  * the bf16 MFMA on packed taps under 1 and 4 only) run one plane per launch
- * instead of two.  Results of 1, 2 and 3 differ only in summation order, 1
- * and 4 not at all.  Returns PLSTM_EINVAL for other values. */
+ * instead of two; 5 = for 32 and 64 units, x's contraction for every plane
+ * first (one launch writing bf16 pre-activations, 2 bytes per gate-unit and
+ * voxel-direction of workspace), then the recurrent contraction plane by
+ * plane (an all-plane input projection; slower than 1, kept for measurement).
+ * Results of 1, 2 and 3 differ only in summation order, 1 and 4 not at all;
+ * 5 also rounds x's part of the pre-activations to bf16.  Returns
+ * PLSTM_EINVAL for other values. */
 int pyramid_lstm_set_bf16_mfma(int on);
 
 /* Weight gradients of the plane-step backward, for testing and tuning

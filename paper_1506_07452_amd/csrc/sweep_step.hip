@@ -1054,6 +1054,8 @@ struct FwdB16Args {
     float *cell;              // [6][N][V][O] fp32 c^d
     uint16_t *hb;             // [6][N][V][O] bf16 h^d (the recurrence's operand and the
                               // direction sum's input)
+    uint16_t *preact;         // projection variant: x's part of the pre-activations and
+                              // the bias, [6][N][V][4O] bf16
     float *cpp;               // macro-tiled kernel: c^d of the last two planes,
                               // [6][N][2][pqmax][O] fp32, plane t at parity t & 1
     int pqmax;                // largest plane (P Q) over the directions
@@ -1395,7 +1397,7 @@ k_step_fwd_b16_blk(FwdB16Args a)
 //   memory-side cache instead of a volume written out to HBM.
 // Workgroups are remapped so that each XCD runs a contiguous range of blocks
 // (at most two directions' weights per L2).
-template <int U, int WM, int WN>
+template <int U, int WM, int WN, int MODE>
 __global__ void __launch_bounds__(64 * WM * WN)
 __attribute__((amdgpu_waves_per_eu(U / WM == 1 ? 3 : 2)))
 k_step_fwd_b16_mt(FwdB16Args a)
@@ -1420,11 +1422,21 @@ k_step_fwd_b16_mt(FwdB16Args a)
     const int d = item_dir(a.base, blk);
     const DirGeom dg = a.g.dir[d];
     int r = blk - a.base[d];
-    const int n = r / a.nblk[d];
-    r -= n * a.nblk[d];
+    int n, t_ = a.t;
+    if constexpr (MODE == 1) {
+        // projection: every plane of the direction in one launch
+        const int per_n = dg.T * a.nblk[d];
+        n = r / per_n;
+        r -= n * per_n;
+        t_ = r / a.nblk[d];
+        r -= t_ * a.nblk[d];
+    } else {
+        n = r / a.nblk[d];
+        r -= n * a.nblk[d];
+    }
+    const int t = t_;
     const int bi = r / a.nbq[d], bj = r - bi * a.nbq[d];
     const int p0 = bi * BP, q0 = bj * BQ;
-    const int t = a.t;
     const int s = dg.sign > 0 ? t : dg.T - 1 - t;
     const int ss = (int)dg.ss, sp = (int)dg.sp, sq = (int)dg.sq;
     const int P = dg.P, Q = dg.Q;
@@ -1433,7 +1445,7 @@ k_step_fwd_b16_mt(FwdB16Args a)
     const int hoff = -dg.sign * ss;
     const int KQ = a.g.KQ, radp = a.g.KP >> 1, radq = KQ >> 1;
     const int SW = BQ + 2 * radq, SH = BP + 2 * radp;
-    const int NXC = C32 >> 3, NCH = NXC + (O >> 3), NCHP = PK ? 6 : NCH + 2;
+    const int NXC = C32 >> 3, NCH = NXC + (MODE == 1 ? 0 : O >> 3), NCHP = PK ? 6 : NCH + 2;
     const int KK = a.g.KP * KQ;
     const long long sbase = ((long long)d * a.g.N + n) * V;
     // byte sizes: V * C32 * 2, V * O * 2 and U * KG * 4096 (< 2^31, checked on the host)
@@ -1487,8 +1499,10 @@ k_step_fwd_b16_mt(FwdB16Args a)
                     0, 0, 0);
         }
     }
-    const int KG = t > 0 ? KGA : KX;
-    issue_a(0, ring0);
+    const int KG = MODE == 1 ? KX : (t > 0 ? KGA : KX);   // KX = 0 for MODE 2
+    // only the recurrent-only mode has no K-group (its first plane)
+    const bool any_kg = MODE != 2 || KG > 0;
+    if (any_kg) issue_a(0, ring0);
     if (KG > 1) issue_a(1, ring1);
     if (KG > 2) issue_a(2, ring2);
 
@@ -1564,7 +1578,7 @@ k_step_fwd_b16_mt(FwdB16Args a)
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
     Ops X, Y;
-    {
+    if (any_kg) {
         const int bb = b_off(0);
 #pragma unroll
         for (int i = 0; i < AT; ++i) X.a[i] = ring0[(AT * wm + i) * 64 + lane];
@@ -1572,7 +1586,7 @@ k_step_fwd_b16_mt(FwdB16Args a)
         for (int nt = 0; nt < kNT; ++nt) X.b[nt] = stg[spb[nt] + bb];
     }
     // step 0 refills ring0: every wave has read K-group 0 from it first
-    __syncthreads();
+    if (any_kg) __syncthreads();
     // after step kg the operands of kg + 1 are in Y for even kg, X for odd
     for (int kg = 0; kg + 1 < KG; kg += 6) {
         step(kg, X, Y, ring1, ring0);
@@ -1600,13 +1614,15 @@ k_step_fwd_b16_mt(FwdB16Args a)
     for (int ui = 0; ui < UGW; ++ui) {
         const int uo = (ug0 + ui) * 16 + 4 * q4;
 #pragma unroll
-        for (int gt = 0; gt < 4; ++gt) bias[ui][gt] = *(const f4 *)(a.bias + d * G + gt * O + uo);
+        for (int gt = 0; gt < 4; ++gt)
+            bias[ui][gt] = MODE == 2 ? f4{0.0f, 0.0f, 0.0f, 0.0f}
+                                     : *(const f4 *)(a.bias + d * G + gt * O + uo);
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
-            cprev[ui][nt] = bload4(rs_c, sel_off(t > 0 && elive[nt],
+            cprev[ui][nt] = bload4(rs_c, sel_off(MODE != 1 && t > 0 && elive[nt],
                                                  (unsigned)(epix[nt] * O + uo) * 4u));
     }
-    mfmas(X);
+    if (any_kg) mfmas(X);
 
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt) {
@@ -1618,6 +1634,25 @@ k_step_fwd_b16_mt(FwdB16Args a)
             f4 pre[4];
 #pragma unroll
             for (int gt = 0; gt < 4; ++gt) pre[gt] = acc[ui * 4 + gt][nt] + bias[ui][gt];
+            if constexpr (MODE == 1) {
+                // x's part of the pre-activations (and the bias), rounded to bf16
+#pragma unroll
+                for (int gt = 0; gt < 4; ++gt) {
+                    us4 pv;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) pv[i] = f32_to_bf16(pre[gt][i]);
+                    *(us4 *)(a.preact + vo * G + gt * O + uo) = pv;
+                }
+                continue;
+            }
+            if constexpr (MODE == 2) {
+#pragma unroll
+                for (int gt = 0; gt < 4; ++gt) {
+                    const us4 pv = *(const us4 *)(a.preact + vo * G + gt * O + uo);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) pre[gt][i] += bf16_to_f32(pv[i]);
+                }
+            }
             f4 c;
             us4 hbv;
             lstm_cell4_b16(pre, cprev[ui][nt], c, hbv);
@@ -3594,6 +3629,11 @@ size_t step_fwd_ws(const Geom &g)
         cb.take<float>((size_t)g.nd * 4 * g.O);
         cb.take<uint16_t>((size_t)g.nd * g.N * g.V * g.O);
         cb.take<float>((size_t)g.nd * g.N * 2 * max_pq(g) * g.O);   // c^d, two planes
+        if (g.O >= 32) {                             // projection variant
+            cb.take<uint16_t>((size_t)g.nd * (g.O / 16) * k.KX * 2048);
+            cb.take<uint16_t>((size_t)g.nd * (g.O / 16) * (k.KG - k.KX) * 2048);
+            cb.take<uint16_t>((size_t)g.nd * g.N * g.V * 4 * g.O);
+        }
         if (cb.off > need) need = cb.off;
     }
     return need;
@@ -3698,7 +3738,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st, int *laun
     }
     if (mt) {
         set_mt_blocks(g, WN, a.bp, a.bq, a.nbq, a.nblk);
-        if (hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, WM, WN>,
+        if (hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, WM, WN, 0>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds_mt) != hipSuccess)
             return PLSTM_EHIP;
@@ -3718,7 +3758,7 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st, int *laun
             a.base[kDirs] = nb;
             if (nb == 0) continue;
             const int grid = (nb + kXcds - 1) / kXcds * kXcds;
-            k_step_fwd_b16_mt<U, WM, WN><<<grid, 64 * WM * WN, lds_mt, st>>>(a);
+            k_step_fwd_b16_mt<U, WM, WN, 0><<<grid, 64 * WM * WN, lds_mt, st>>>(a);
             PLSTM_LAUNCH_CHECK();
             continue;
         }
@@ -3746,6 +3786,65 @@ int launch_fwd_b16_steps(const Geom &g, FwdB16Args &a, hipStream_t st, int *laun
         PLSTM_LAUNCH_CHECK();
         }
     }
+    return PLSTM_OK;
+}
+
+// Projection variant (knob value 5, 32 or 64 units): x's contraction for every
+// plane of every direction in one launch of the macro-tiled kernel (MODE 1),
+// which writes bf16 pre-activations, then one launch per plane of the
+// recurrent part alone (MODE 2), which adds them in its epilogue.
+template <int U>
+int launch_fwd_b16_proj(const Geom &g, FwdB16Args &a, const uint16_t *fragx,
+                        const uint16_t *fragh, int KX, int KH, hipStream_t st, int *launches)
+{
+    constexpr int WM = MtShape<U>::WM, WN = MtShape<U>::WN, O = 16 * U;
+    const int T = max_T(g);
+    const size_t ring = (size_t)3 * 4 * U * 1024;
+    const size_t halo = (size_t)(4 * WN + 2 * (g.KP / 2)) * (16 + 2 * (g.KQ / 2)) * 16;
+    const size_t lds1 = halo * (a.C32 / 8 + 2), lds2 = halo * (O / 8 + 2);
+    if (ring + lds1 > (size_t)device_info().max_lds || ring + lds2 > (size_t)device_info().max_lds)
+        return PLSTM_EUNSUPPORTED;
+    if (hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, WM, WN, 1>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds1) != hipSuccess ||
+        hipFuncSetAttribute((const void *)k_step_fwd_b16_mt<U, WM, WN, 2>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds2) != hipSuccess)
+        return PLSTM_EHIP;
+    set_mt_blocks(g, WN, a.bp, a.bq, a.nbq, a.nblk);
+    // MODE 1: all planes
+    FwdB16Args p = a;
+    p.KX = KX; p.KG = KX; p.frag = fragx; p.t = 0;
+    long long nb = 0;
+    for (int d = 0; d < kDirs; ++d) {
+        p.base[d] = (int)nb;
+        nb += (long long)g.N * g.dir[d].T * a.nblk[d];
+    }
+    if (nb >= (1LL << 30)) return PLSTM_EUNSUPPORTED;
+    p.base[kDirs] = (int)nb;
+    int n_launch = 0;
+    if (nb > 0) {
+        const int grid = (int)((nb + kXcds - 1) / kXcds * kXcds);
+        k_step_fwd_b16_mt<U, WM, WN, 1><<<grid, 64 * WM * WN, lds1, st>>>(p);
+        PLSTM_LAUNCH_CHECK();
+        ++n_launch;
+    }
+    // MODE 2: the recurrence, plane by plane
+    FwdB16Args q = a;
+    q.C32 = 0; q.KX = 0; q.KG = KH; q.frag = fragh; q.cx_mul32 = 0;
+    for (int t = 0; t < T; ++t) {
+        q.t = t;
+        int nbt = 0;
+        for (int d = 0; d < kDirs; ++d) {
+            q.base[d] = nbt;
+            if (t < g.dir[d].T) nbt += g.N * a.nblk[d];
+        }
+        q.base[kDirs] = nbt;
+        if (nbt == 0) continue;
+        const int grid = (nbt + kXcds - 1) / kXcds * kXcds;
+        k_step_fwd_b16_mt<U, WM, WN, 2><<<grid, 64 * WM * WN, lds2, st>>>(q);
+        PLSTM_LAUNCH_CHECK();
+        ++n_launch;
+    }
+    *launches = n_launch;
     return PLSTM_OK;
 }
 
@@ -3781,11 +3880,31 @@ static int step_fwd_b16(const Geom &g, const uint16_t *x, const uint16_t *wx,
     a.frag = frag; a.bias = bias;
     a.cell = cell; a.hb = hb;
     a.cpp = cpp; a.pqmax = max_pq(g);
+    a.preact = nullptr;
     for (int d = 0; d < kDirs; ++d) a.npg[d] = npg_of(g.dir[d]);
     int steps = 0;
-    const int rc = U == 1   ? launch_fwd_b16_steps<1>(g, a, st, &steps)
-                   : U == 2 ? launch_fwd_b16_steps<2>(g, a, st, &steps)
-                            : launch_fwd_b16_steps<4>(g, a, st, &steps);
+    int rc;
+    if (g_step_bf16_mfma == 5 && U >= 2) {
+        // projection variant: x-only and h-only fragments, pre-activations
+        const int KH = KG - KX;
+        uint16_t *fragx = cv.take<uint16_t>((size_t)g.nd * U * KX * 2048);
+        uint16_t *fragh = cv.take<uint16_t>((size_t)g.nd * U * KH * 2048);
+        a.preact = cv.take<uint16_t>((size_t)g.nd * g.N * g.V * 4 * g.O);
+        const long long nfx = (long long)g.nd * U * KX * 2048, nfh = (long long)g.nd * U * KH * 2048;
+        k_pack_fwd_b16<<<blocks_for(nfx, 256), 256, 0, st>>>(g.nd, g.O, g.C, C32, KX, KX, KK, 0,
+                                                              wx, wh, b, fragx, bias);
+        PLSTM_LAUNCH_CHECK();
+        k_pack_fwd_b16<<<blocks_for(nfh, 256), 256, 0, st>>>(g.nd, g.O, g.C, C32, 0, KH, KK, 0,
+                                                              wx, wh, b, fragh, bias);
+        PLSTM_LAUNCH_CHECK();
+        rc = U == 2 ? launch_fwd_b16_proj<2>(g, a, fragx, fragh, KX, KH, st, &steps)
+                    : launch_fwd_b16_proj<4>(g, a, fragx, fragh, KX, KH, st, &steps);
+        steps += 2;
+    } else {
+        rc = U == 1   ? launch_fwd_b16_steps<1>(g, a, st, &steps)
+             : U == 2 ? launch_fwd_b16_steps<2>(g, a, st, &steps)
+                      : launch_fwd_b16_steps<4>(g, a, st, &steps);
+    }
     if (rc != PLSTM_OK) return rc;
     timing_end((C32 != g.C ? 2 : 1) + steps, st);
     return sum_dirs_bf16(g, hb, h, st);
@@ -4168,7 +4287,7 @@ extern "C" int pyramid_lstm_set_step_split(int mode)
 
 extern "C" int pyramid_lstm_set_bf16_mfma(int on)
 {
-    if (on < 0 || on > 4) return PLSTM_EINVAL;
+    if (on < 0 || on > 5) return PLSTM_EINVAL;
     plstm::g_step_bf16_mfma = on;
     return PLSTM_OK;
 }

@@ -201,7 +201,7 @@ def test_binding_refuses_host_tensors():
 
 def test_path_knobs_and_timing_without_gpu():
     for fn, top in ((P.pyramid_lstm_set_forward_path, 4), (P.pyramid_lstm_set_backward_path, 3),
-                    (P.pyramid_lstm_set_step_split, 3), (P.pyramid_lstm_set_bf16_mfma, 4),
+                    (P.pyramid_lstm_set_step_split, 3), (P.pyramid_lstm_set_bf16_mfma, 5),
                     (P.pyramid_lstm_set_wgrad_staged, 1)):
         for v in list(range(1, top + 1)) + [0]:
             fn(v)

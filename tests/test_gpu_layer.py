@@ -340,8 +340,8 @@ BF16_K_CASES = [((1, 4, 11, 9, 25, 32), 7), ((2, 3, 19, 35, 20, 64), 5),
 
 @pytest.mark.parametrize("case", BF16_K_CASES,
                          ids=lambda c: "x".join(map(str, c[0])) + "_k%d" % c[1])
-@pytest.mark.parametrize("bf16_mfma", [1, 3, 2, 0],
-                         ids=["bf16_mt", "bf16_lds", "bf16_l1", "fp32_mfma"])
+@pytest.mark.parametrize("bf16_mfma", [1, 3, 2, 0, 5],
+                         ids=["bf16_mt", "bf16_lds", "bf16_l1", "fp32_mfma", "bf16_proj"])
 def test_filter_size_bf16(bf16_mfma, case):
     shape, K = case
     inst = instance_k(shape, K, 7200 + sum(shape), "bf16")

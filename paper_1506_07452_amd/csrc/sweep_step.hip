@@ -1806,7 +1806,7 @@ k_step2_fwd_b16_pk(FwdB16Args a)
         for (int g = 0; g < 4; ++g) pre[g] = acc[g] + bias[g];
         lstm_cell4_b16(pre, cprev, c, hbv);
     };
-    // h_t of staged pixel sp into chunks 4-5 (units uo .. uo + 3)
+    // h_t of staged pixel spx into chunks 4-5 (units uo .. uo + 3)
     auto put_h = [&](int spx, us4 v) {
         *(us4 *)((char *)stg + (size_t)(spx * NC + 4) * 16 + q4 * 8) = v;
     };

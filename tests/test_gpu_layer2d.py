@@ -125,8 +125,8 @@ def test_2d_saved_state_matches_oracle(shape):
         assert normwise(got.reshape(want.shape), want) <= TOL["f32"], name
 
 
-@pytest.mark.parametrize("bf16_mfma", [1, 3, 2, 0],
-                         ids=["bf16_mt", "bf16_lds", "bf16_l1", "fp32_mfma"])
+@pytest.mark.parametrize("bf16_mfma", [1, 3, 2, 0, 5],
+                         ids=["bf16_mt", "bf16_lds", "bf16_l1", "fp32_mfma", "bf16_proj"])
 @pytest.mark.parametrize("shape", [(1, 9, 70, 5, 32, 7), (1, 40, 3, 20, 64, 5),
                                    (2, 17, 33, 3, 16, 3)], ids=ident)
 def test_2d_bf16_forward(shape, bf16_mfma):
